@@ -1,0 +1,31 @@
+import functools
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+    config.addinivalue_line("markers", "slow: long-running CPU test")
+
+
+@functools.lru_cache(maxsize=None)
+def model_blob(name: str, **overrides) -> bytes:
+    import dataclasses
+
+    from synth import generate as G
+
+    cfg = getattr(G, name)
+    if overrides:
+        cfg = dataclasses.replace(cfg, **overrides)
+    return G.build_model(cfg)
+
+
+@pytest.fixture(scope="session")
+def blobs():
+    return model_blob
