@@ -1,0 +1,195 @@
+"""Benchmark of the INT8 encoder-decoder hot path on one MI355X.
+
+One step = one whole translation of the batch-1 latency workload: a seeded
+synthetic 12-encoder / 2-decoder model (d_model 256, 4 heads, FFN 1024,
+shared vocabulary 32000, int8 weights with per-channel scales), one source of
+30 tokens, encoder + exactly 30 greedy decode steps (embedding, int8 linear
+layers, int8 self/cross attention with the int8 key/value cache, fused
+logits + arg-max), replayed from a captured hipGraph, inputs already in HBM.
+
+Prints one JSON line: decoded tokens per second (value), ms per sentence,
+the roofline of the dominant kernel (the fused logits + arg-max pass over
+the 8.19 MB int8 embedding, HBM bound), the int8 GEMM throughput of the
+largest quantized-linear sweep shape against the i8 matrix-core peak, and the
+CPU oracle timed on the host as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+I8_PEAK_TOPS = 5000.0  # MI355X dense int8 matrix-core peak
+
+
+def _events_ms(torch, fn, reps, stream):
+    """Average ms per call of fn() over reps back-to-back calls on `stream`."""
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def _source_hash():
+    h = hashlib.sha256()
+    for f in ("qlinear.hip", "canon.hpp"):
+        with open(os.path.join(ROOT, "paper_2306_04235_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _traffic(kernel_tag):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    rec = data.get(kernel_tag)
+    if not rec or rec.get("source_hash") != _source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(workload, min_seconds=10.0):
+    import oracle
+    from synth import generate as G
+
+    m = oracle.Model(G.build_model(workload.model))
+    src, lens = G.workload_inputs(workload)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        m.greedy(src, lens, workload.steps)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds and n >= 2:
+            break
+    return {"value": n * workload.steps * workload.batch / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} sentences of the same workload (batch 1, 30 source tokens, 30 greedy steps), "
+                      f"{el:.1f} s, single-threaded scalar C"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the batch-1 path does not "
+              "shard; larger batches shard by sentence, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2306_04235_amd import mnmt, workload as WL
+    from synth import generate as G
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    w = G.WORKLOADS["mobile"]
+    blob = G.build_model(w.model)
+    model = mnmt.Model(blob)
+    info = model.info
+    src, lens = G.workload_inputs(w)
+    tsrc = torch.from_numpy(src).to(dev)
+    tlen = torch.from_numpy(lens).to(dev)
+    sess = mnmt.Session(model, w.batch, w.s_max, w.steps, 1)
+    stream = torch.cuda.current_stream()
+    outs = (torch.empty((w.batch, w.steps), dtype=torch.int32, device=dev),
+            torch.empty(w.batch, dtype=torch.int32, device=dev), torch.empty(w.batch, dtype=torch.float32, device=dev))
+
+    def step():
+        sess.translate(tsrc, tlen, beam=1, max_steps=w.steps, use_graph=True, out=outs)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    tokens = int(outs[1].sum().item()) * args.steps
+    ms_per_sentence = elapsed * 1e3 / (args.steps * w.batch)
+
+    # Dominant kernel: fused logits + arg-max over the int8 embedding (batch 1).
+    dims = WL.Dims(info.d_model, info.n_heads, info.d_ffn, info.n_enc, info.n_dec, info.vocab)
+    alg_bytes = WL.logits_gemv_bytes(dims) + info.d_model + 8
+    from synth.modelfile import read_model
+
+    _, tens = read_model(blob)
+    x = torch.randint(-127, 128, (1, info.d_model), dtype=torch.int8, device=dev)
+    E = torch.from_numpy(np.ascontiguousarray(tens["emb.w"])).to(dev)
+    # per-row output scales (their values do not affect the timing)
+    c_out = torch.from_numpy(np.ascontiguousarray(tens["emb.s"])).to(dev)
+    slot = torch.zeros(1, dtype=torch.int64, device=dev)
+    fn = lambda: mnmt.mnmt_qlinear(x, E, c_out, None, mnmt.EPI_ARGMAX, out=slot, stream=stream)  # noqa: E731
+    for _ in range(10):
+        fn()
+    kern_ms = _events_ms(torch, fn, 400, stream)
+    achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": _traffic("logits_argmax_b1"),
+                "kernel": "k_qgemv<1,16,4> (fused logits + arg-max, M=1 K=256 N=32000)",
+                "alg_bytes_per_launch": alg_bytes, "avg_us": round(kern_ms * 1e3, 3)}
+
+    # Largest quantized-linear sweep shape on the matrix cores.
+    M, K, N = 4096, 256, 32000
+    Xg = torch.randint(-127, 128, (M, K), dtype=torch.int8, device=dev)
+    Wg = torch.randint(-127, 128, (N, K), dtype=torch.int8, device=dev)
+    sc = torch.full((N,), 1e-4, dtype=torch.float32, device=dev)
+    bi = torch.zeros(N, dtype=torch.float32, device=dev)
+    Yg = torch.empty((M, N), dtype=torch.int8, device=dev)
+    g = lambda: mnmt.mnmt_qlinear(Xg, Wg, sc, bi, mnmt.EPI_I8, out=Yg, stream=stream)  # noqa: E731
+    for _ in range(3):
+        g()
+    gemm_ms = _events_ms(torch, g, 20, stream)
+    tops = 2.0 * M * K * N / (gemm_ms * 1e-3) / 1e12
+    qgemm = {"shape": [M, K, N], "epilogue": "i8 requant", "tops": round(tops, 1), "peak": I8_PEAK_TOPS,
+             "frac": round(tops / I8_PEAK_TOPS, 4), "avg_us": round(gemm_ms * 1e3, 2)}
+
+    line = {
+        "metric": "decoded tokens/sec at batch 1 (greedy, 30-token sentences)",
+        "value": round(tokens / elapsed, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "ms_per_sentence": round(ms_per_sentence, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "src_len": int(lens[0]), "greedy_steps": w.steps,
+                   "d_model": info.d_model, "heads": info.n_heads, "ffn": info.d_ffn, "enc_layers": info.n_enc,
+                   "dec_layers": info.n_dec, "vocab": info.vocab, "graph": True},
+        "roofline": roofline,
+        "qgemm": qgemm,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(line), flush=True)
+    sess.close()
+    model.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,210 @@
+/*
+ * mnmt.h -- C ABI of libmnmt, an INT8 encoder-decoder Transformer inference
+ * engine for AMD Instinct MI355X (gfx950), after MobileNMT (arXiv 2306.04235).
+ *
+ * What the engine computes (paper passages):
+ *   - Transformer encoder-decoder with self-attention, cross-attention and a
+ *     ReLU FFN, residual connections (Appendix A, self-weight / self-sum / FFN
+ *     equations), LayerNorm at each sublayer input (Appendix D) or, for
+ *     post-LN model files, after each residual add.
+ *   - One shared vocabulary embedding for encoder input, decoder input and the
+ *     output projection (Appendix D; "Embed x1" in the settings tables).
+ *   - Quantizers of Section 3.2 (quantizer figure): every linear layer takes
+ *     int8 inputs and int8 weights and accumulates in int32; Q, K and V are
+ *     int8 (the key/value caches hold these codes); biases, the residual
+ *     stream, attention scores, softmax output and logits stay fp32; a
+ *     learnable weight gamma scales each sublayer's residual.
+ *   - 8-bit integer GEMM (Section 4.1) and fused element-wise work between
+ *     GEMMs plus shared scratch buffers (Section 4.2).
+ *   - Greedy search (Appendix D) and beam search.
+ * Every fp32 step is fixed to a canonical IEEE binary32 evaluation order so
+ * that results are reproducible bit for bit (documented in the design notes).
+ *
+ * Conventions for every entry point:
+ *   - Return MNMT_OK (0) or a negative MNMT_E_* status; no C++ exception
+ *     crosses this boundary.  mnmt_last_error() gives a thread-local message.
+ *   - The library never allocates device memory.  The caller allocates the
+ *     model arena and the session workspace (sizes from mnmt_model_bytes /
+ *     mnmt_session_bytes) and owns them; they must stay valid while the model
+ *     or session exists.  The library owns only small host structures.
+ *   - "d_" pointers are device pointers (HIP global memory); "h_" pointers are
+ *     host pointers.  `stream` is a hipStream_t passed as void* (NULL is the
+ *     null stream); device work is enqueued on it asynchronously unless stated.
+ *   - Device pointers passed to the engine must be 16-byte aligned.
+ *   - A session is not thread-safe.  Several sessions may share one model.
+ *   - Token ids are int32: PAD, BOS, EOS, UNK come from the model file
+ *     (0, 1, 2, 3 in the files this project writes).
+ *
+ * Model file (little endian), version 1:
+ *   header, 64 bytes: char magic[4] = "MNMT"; u32 version = 1; u32 d_model,
+ *   n_heads, d_ffn, n_enc, n_dec, vocab, max_pos, ln_post (0 pre-LN,
+ *   1 post-LN); i32 pad_id, bos_id, eos_id, unk_id; f32 ln_eps; u32 n_tensors.
+ *   n_tensors entries of 64 bytes: char name[40] (NUL padded); u32 dtype
+ *   (1 int8, 2 fp32); u32 rank (1 or 2); u32 dim0; u32 dim1 (1 for rank 1);
+ *   u64 offset (from file start, multiple of 256).  Tensors, d = d_model,
+ *   F = d_ffn, V = vocab, P = max_pos; <e> = "enc.<l>", <t> = "dec.<l>":
+ *     emb.w i8 [V,d], emb.s f32 [V] (per-row scale), pe f32 [P,d],
+ *     enc.sout, dec.sout f32 [1] (encoder-output / final activation scales),
+ *     enc.ln.{g,b}, dec.ln.{g,b} f32 [d] (final LayerNorms, pre-LN files),
+ *     <e|t>.sa.ln.{g,b}, .sa.qkv.{w [3d,d], sw [3d], b [3d], sin [1], sout [3]},
+ *     .sa.o.{w [d,d], sw, b, sin (= context scale)}, .sa.gamma [1],
+ *     <t>.ca.ln.{g,b}, .ca.q.{w,sw,b,sin,sout [1]}, .ca.kv.{w [2d,d],sw,b,
+ *     sout [2]} (input scale = enc.sout), .ca.o.{w,sw,b,sin}, .ca.gamma,
+ *     <e|t>.ff.ln.{g,b}, .ff.w1.{w [F,d],sw,b,sin,sout [1]},
+ *     .ff.w2.{w [d,F],sw,b} (input scale = ff.w1.sout), .ff.gamma.
+ *   Weights are symmetric per-output-channel int8: w_real = sw[n] * w[n,k].
+ */
+#ifndef MNMT_H
+#define MNMT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MNMT_OK 0
+#define MNMT_E_INVALID_ARG (-1)  /* bad pointer, size, alignment or value */
+#define MNMT_E_BAD_MODEL (-2)    /* model file malformed or inconsistent */
+#define MNMT_E_CAPACITY (-3)     /* request exceeds the session's capacity */
+#define MNMT_E_HIP (-4)          /* a HIP runtime call failed (text in last_error) */
+#define MNMT_E_UNSUPPORTED (-5)  /* valid but not supported by this build */
+
+/* Linear-layer epilogues (quantizer figure, Section 3.2), y = acc*scale+bias:
+ *   MNMT_EPI_I32:       Y int32 = acc
+ *   MNMT_EPI_I8:        Y int8  = clamp(rint(fma(acc, scale[n], bias[n])), -127, 127)
+ *   MNMT_EPI_I8_RELU:   Y int8  = clamp(rint(max(fma(acc, scale[n], bias[n]), 0)), ..)
+ *   MNMT_EPI_F32:       Y fp32  = fma(acc, scale[n], bias[n])
+ *   MNMT_EPI_F32_RESID: Y fp32  = fma(gamma, Y, fma(acc, scale[n], bias[n]))  (in place)
+ *   MNMT_EPI_LOGITS:    Y fp32  = acc * scale[n]                      (bias unused)
+ *   MNMT_EPI_ARGMAX:    Y uint64 [M] (caller zero-fills) receives, per row, the
+ *                       maximum over n of key(z) << 32 | (0xFFFFFFFF - n) with
+ *                       z = acc * scale[n] and key() order-preserving on
+ *                       floats: the arg max with the smallest index among
+ *                       equal maxima, fused into the logits pass (M <= 8).
+ * acc = sum_k X[m,k] W[n,k] in int32, converted to fp32 with round-to-nearest-even. */
+#define MNMT_EPI_I32 0
+#define MNMT_EPI_I8 1
+#define MNMT_EPI_I8_RELU 2
+#define MNMT_EPI_F32 3
+#define MNMT_EPI_F32_RESID 4
+#define MNMT_EPI_LOGITS 5
+#define MNMT_EPI_ARGMAX 6
+
+typedef struct mnmt_model mnmt_model;
+typedef struct mnmt_session mnmt_session;
+
+typedef struct {
+  int32_t d_model, n_heads, d_ffn, n_enc, n_dec, vocab, max_pos, ln_post;
+  int32_t pad_id, bos_id, eos_id, unk_id;
+  float ln_eps;
+} mnmt_model_info;
+
+/* Capacity of a session: batch, source and target lengths, beam width. */
+typedef struct {
+  int32_t max_batch;
+  int32_t max_src_len;
+  int32_t max_tgt_len;
+  int32_t beam; /* 1 = greedy only */
+} mnmt_session_cfg;
+
+typedef struct {
+  int32_t beam;              /* 1 = greedy search; else beam width (<= session beam) */
+  int32_t max_steps;         /* decode steps (<= max_tgt_len) */
+  float len_penalty_alpha;   /* beam: final score = score / ((5 + L) / 6)^alpha */
+  int32_t stop_at_eos;       /* greedy: rows stop (PAD-fill) after EOS; beam always stops */
+  int32_t use_graph;         /* replay a captured hipGraph of the whole search */
+} mnmt_search_cfg;
+
+/* ---- model --------------------------------------------------------------- */
+
+/* Validate a model file held in host memory and report the device arena size
+ * it needs.  Host only.  blob: the whole file; device_bytes: out. */
+int mnmt_model_bytes(const void* h_blob, size_t blob_bytes, size_t* device_bytes);
+
+/* Load a model into a caller-allocated device arena (>= mnmt_model_bytes,
+ * 256-byte aligned): validates, derives the folded fp32 constants in double
+ * precision (each rounded once), lays the tensors out for the kernels and
+ * copies them with one transfer on `stream`, then synchronizes `stream`.
+ * *out receives a host handle; free it with mnmt_model_free (the arena stays
+ * the caller's).  The model is bound to the current HIP device. */
+int mnmt_model_load(const void* h_blob, size_t blob_bytes, void* d_arena, size_t arena_bytes,
+                    void* stream, mnmt_model** out);
+
+int mnmt_model_get_info(const mnmt_model* model, mnmt_model_info* out);
+void mnmt_model_free(mnmt_model* model);
+
+/* ---- session ------------------------------------------------------------- */
+
+/* Workspace bytes for a session of capacity `cfg` (host only).  The plan
+ * shares one region between encoder scratch and decoder logits (Section 4.2). */
+int mnmt_session_bytes(const mnmt_model* model, const mnmt_session_cfg* cfg, size_t* bytes);
+
+/* Create a session over a caller-allocated device workspace (>= the size
+ * above, 256-byte aligned). */
+int mnmt_session_create(const mnmt_model* model, const mnmt_session_cfg* cfg, void* d_ws,
+                        size_t ws_bytes, mnmt_session** out);
+void mnmt_session_free(mnmt_session* session);
+
+/* Encode a batch: d_src [B, S_max] int32 row-major, right-padded; d_len [B]
+ * int32 with 1 <= len <= S_max.  Computes the encoder output and every decoder
+ * layer's cross-attention keys and values, and resets the decode state (step
+ * 0, every row's next input BOS).  Asynchronous on `stream`.
+ * Errors: MNMT_E_CAPACITY if B or S_max exceed the session. */
+int mnmt_encode(mnmt_session* session, const int32_t* d_src, const int32_t* d_len, int B, int S_max,
+                void* stream);
+
+/* One greedy decoder step for the B rows of the last encode: input tokens
+ * d_prev [B] (NULL: the session's device-resident tokens, BOS at step 0 or
+ * the previous step's outputs), output d_next [B] = arg max of the logits
+ * (smallest id among equal maxima), optional d_logits [B, V] fp32.  The step
+ * index lives in device memory.  Errors: MNMT_E_CAPACITY past max_tgt_len. */
+int mnmt_decode_step(mnmt_session* session, const int32_t* d_prev, int32_t* d_next, float* d_logits,
+                     void* stream);
+
+/* Encode and search.  d_out [B, max_steps] int32 (PAD after the end),
+ * d_out_len [B] int32, d_score [B] fp32 (beam: normalized score of the
+ * returned hypothesis; greedy: unused, may be NULL).  Asynchronous; results
+ * are valid after `stream` synchronizes.  Greedy with stop_at_eos = 0 runs
+ * exactly max_steps steps. */
+int mnmt_translate(mnmt_session* session, const int32_t* d_src, const int32_t* d_len, int B,
+                   int S_max, const mnmt_search_cfg* search, int32_t* d_out, int32_t* d_out_len,
+                   float* d_score, void* stream);
+
+/* Device pointer and size of a session buffer, for inspection by tests:
+ * "enc_out" int8 [B*S_max, d] (encoder output codes, padded rows undefined),
+ * "cross_kv.<l>" int8 [B*S_max, 2d], "dec_x" fp32 [R, d], "logits" fp32 [R, V],
+ * "step" int32 [1]. */
+int mnmt_session_tensor(const mnmt_session* session, const char* name, void** d_ptr, size_t* bytes);
+
+/* ---- single quantized linear layer --------------------------------------- */
+
+/* Y = epilogue(X W^T): d_X int8 [M, K] row-major (row stride K), d_W int8
+ * [N, K] row-major, d_scale/d_bias fp32 [N] (bias may be NULL for I32 and
+ * LOGITS), d_Y [M, N] of the epilogue's type.  K must be a positive multiple
+ * of 64 and at most 8192; M >= 0, N >= 1.  M <= 8 runs the wavefront
+ * reduction kernel, larger M the i8 matrix-core kernel. */
+int mnmt_qlinear(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias,
+                 int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream);
+
+/* Folded requantization constants (host): scale[n] = s_in*s_w[n]/s_out,
+ * bias[n] = b[n]/s_out, each computed in double and rounded once to fp32. */
+int mnmt_fold_requant(float s_in, const float* h_s_w, const float* h_b, float s_out, int N,
+                      float* h_scale, float* h_bias);
+
+/* ---- canonical arithmetic self-check -------------------------------------- */
+
+/* Run the engine's device fp32 primitives on d_x[n] -> d_y[n]: fn 0 exp
+ * (x <= 0), 1 natural log (x > 0), 2 canonical-order sum of all n values
+ * into d_y[0].  For tests of the canonical arithmetic. */
+int mnmt_debug_canon(int fn, const float* d_x, int n, float* d_y, void* stream);
+
+/* ---- errors ---------------------------------------------------------------- */
+const char* mnmt_status_str(int status);
+const char* mnmt_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,99 @@
+// api.cpp -- C ABI entry points for models, single linear layers, the
+// canonical-arithmetic self check and error reporting.
+#include <cmath>
+#include <string>
+
+#include "internal.h"
+
+namespace mnmt {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+int set_error(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+
+int hip_error(hipError_t e, const char* what) {
+  return set_error(MNMT_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+}  // namespace mnmt
+
+using namespace mnmt;
+
+extern "C" const char* mnmt_status_str(int status) {
+  switch (status) {
+    case MNMT_OK: return "ok";
+    case MNMT_E_INVALID_ARG: return "invalid argument";
+    case MNMT_E_BAD_MODEL: return "bad model file";
+    case MNMT_E_CAPACITY: return "capacity exceeded";
+    case MNMT_E_HIP: return "HIP runtime error";
+    case MNMT_E_UNSUPPORTED: return "unsupported";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* mnmt_last_error(void) { return g_last_error.c_str(); }
+
+extern "C" int mnmt_model_bytes(const void* blob, size_t blob_bytes, size_t* device_bytes) {
+  if (!device_bytes) return set_error(MNMT_E_INVALID_ARG, "device_bytes is null");
+  std::string err;
+  const int rc = model_size(blob, blob_bytes, device_bytes, err);
+  return rc ? set_error(rc, err) : MNMT_OK;
+}
+
+extern "C" int mnmt_model_load(const void* blob, size_t blob_bytes, void* d_arena, size_t arena_bytes, void* stream,
+                               mnmt_model** out) {
+  if (!out || !d_arena) return set_error(MNMT_E_INVALID_ARG, "out or arena is null");
+  std::string err;
+  const int rc = model_create(blob, blob_bytes, d_arena, arena_bytes, static_cast<hipStream_t>(stream), out, err);
+  return rc ? set_error(rc, err) : MNMT_OK;
+}
+
+extern "C" int mnmt_model_get_info(const mnmt_model* model, mnmt_model_info* out) {
+  if (!model || !out) return set_error(MNMT_E_INVALID_ARG, "null argument");
+  *out = model->info;
+  return MNMT_OK;
+}
+
+extern "C" void mnmt_model_free(mnmt_model* model) { delete model; }
+
+extern "C" int mnmt_qlinear(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias, int M,
+                            int K, int N, int epilogue, float gamma, void* d_Y, void* stream) {
+  if (M < 0 || N < 1 || K < 64 || K % 64 || K > 8192)
+    return set_error(MNMT_E_INVALID_ARG, "need M >= 0, N >= 1 and K a multiple of 64 in [64, 8192]");
+  if (epilogue < MNMT_EPI_I32 || epilogue > MNMT_EPI_ARGMAX) return set_error(MNMT_E_INVALID_ARG, "unknown epilogue");
+  if (epilogue == MNMT_EPI_ARGMAX && M > 8)
+    return set_error(MNMT_E_UNSUPPORTED, "the fused arg-max epilogue takes at most 8 rows");
+  if (M == 0) return MNMT_OK;
+  const bool needs_scale = epilogue != MNMT_EPI_I32;
+  const bool needs_bias = epilogue != MNMT_EPI_I32 && epilogue != MNMT_EPI_LOGITS && epilogue != MNMT_EPI_ARGMAX;
+  if (!d_X || !d_W || !d_Y || (needs_scale && !d_scale) || (needs_bias && !d_bias))
+    return set_error(MNMT_E_INVALID_ARG, "null device pointer");
+  if (reinterpret_cast<uintptr_t>(d_X) % 16 || reinterpret_cast<uintptr_t>(d_W) % 16)
+    return set_error(MNMT_E_INVALID_ARG, "X and W must be 16-byte aligned");
+  EpiArgs e{epilogue, d_Y, N, gamma, nullptr};
+  if (epilogue == MNMT_EPI_ARGMAX) e = EpiArgs{EPI_LOGITS_ARGMAX, nullptr, N, 1.f, static_cast<unsigned long long*>(d_Y)};
+  const hipError_t h = launch_qlinear(d_X, K, d_W, d_scale, d_bias, M, K, N, e, static_cast<hipStream_t>(stream));
+  return h == hipSuccess ? MNMT_OK : hip_error(h, "qlinear launch");
+}
+
+extern "C" int mnmt_fold_requant(float s_in, const float* s_w, const float* b, float s_out, int N, float* scale,
+                                 float* bias) {
+  if (!s_w || !b || !scale || !bias || N < 1 || !(s_in > 0.0f) || !(s_out > 0.0f))
+    return set_error(MNMT_E_INVALID_ARG, "bad fold_requant arguments");
+  for (int n = 0; n < N; ++n) {
+    scale[n] = (float)((double)s_in * (double)s_w[n] / (double)s_out);
+    bias[n] = (float)((double)b[n] / (double)s_out);
+  }
+  return MNMT_OK;
+}
+
+extern "C" int mnmt_debug_canon(int fn, const float* d_x, int n, float* d_y, void* stream) {
+  if (fn < 0 || fn > 2 || n < 0 || !d_x || !d_y) return set_error(MNMT_E_INVALID_ARG, "bad debug_canon arguments");
+  const hipError_t h = launch_debug_canon(fn, d_x, n, d_y, static_cast<hipStream_t>(stream));
+  return h == hipSuccess ? MNMT_OK : hip_error(h, "debug_canon launch");
+}

@@ -1,0 +1,191 @@
+// internal.h -- host-side structures and kernel launchers of libmnmt.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "../../include/mnmt.h"
+
+namespace mnmt {
+
+// Status with message; set_error stores the thread-local text.
+int set_error(int status, const std::string& msg);
+int hip_error(hipError_t e, const char* what);
+
+#define MNMT_HIP(call)                                      \
+  do {                                                      \
+    hipError_t _e = (call);                                 \
+    if (_e != hipSuccess) return ::mnmt::hip_error(_e, #call); \
+  } while (0)
+
+// Epilogue kinds: the public MNMT_EPI_* values plus the fused arg-max.
+enum : int { EPI_LOGITS_ARGMAX = 16 };
+
+struct EpiArgs {
+  int kind;
+  void* out;          // [M, ldo] of the epilogue's type (may be null for ARGMAX)
+  int ldo;            // row stride of out, in elements
+  float gamma;        // residual weight for F32_RESID
+  unsigned long long* argmax;  // [M] packed (value, ~index) maxima for ARGMAX
+};
+
+// Y = epilogue(X[M,K] . W[N,K]^T); ldx = row stride of X in bytes.
+hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias,
+                          int M, int K, int N, const EpiArgs& e, hipStream_t s);
+
+// LayerNorm (optional) + quantization of rows of x [rows, d]:
+// do_ln: y = LN(x) with g, b, eps; else y = x.  q = quant(y, inv_s) if q;
+// x_out = y if x_out (post-LN writes the normalized row back).
+hipError_t launch_ln_quant(const float* x, int rows, int d, int do_ln, const float* g, const float* b, float eps,
+                           float inv_s, int8_t* q, float* x_out, hipStream_t s);
+
+// Token embedding + position table into x [rows, d]; row r of sentence
+// (r / S) position p: encoder (tok = src[r], p = r % S); decoder
+// (tok = tok[r], p = *step).
+hipError_t launch_embed(const int32_t* tok, int rows, int S_for_pos, const int* step, const int8_t* E,
+                        const float* c_emb, const float* pe, int d, int V, float* x, hipStream_t s);
+
+// Encoder self-attention over qkv [B*S, 3d] -> ctx [B*S, d].
+hipError_t launch_attn_enc(const int8_t* qkv, const int32_t* len, int B, int S, int d, int h, float c_qk,
+                           float c_pv, int8_t* ctx, hipStream_t s);
+
+// Decoder self-attention at position *step: stores this step's k, v of every
+// row into kcache/vcache [R][T][d] and attends over positions 0..step of the
+// row's hypothesis (hist: two [R][T] tables, position -> cache row, the one
+// of parity step & 1 is read; null = the row's own cache).
+hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, const int* step, int8_t* kcache,
+                                int8_t* vcache, const int32_t* hist, float c_qk, float c_pv, int8_t* ctx,
+                                hipStream_t s);
+
+// Decoder cross-attention: row r attends over the cross keys/values of
+// sentence r / W (kv [B*S, 2d]) limited to len[b].
+hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, const int8_t* kv, int S,
+                                 const int32_t* len, float c_qk, float c_pv, int8_t* ctx, hipStream_t s);
+
+// Greedy bookkeeping after the fused logits/arg-max of a step.
+hipError_t launch_greedy_commit(unsigned long long* slots, int R, int T, int32_t* cur_tok, int32_t* out_tok,
+                                int32_t* finished, int32_t* out_len, int* step, int stop_at_eos, int eos,
+                                int pad, hipStream_t s);
+hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
+                               int32_t* out_len, int* step, int bos, hipStream_t s);
+hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, int R, int T, int32_t* out,
+                                int32_t* out_len_dst, hipStream_t s);
+// Arg-max of fp32 rows [R, V] into packed slots (greedy when logits are
+// produced by the matrix-core path).
+hipError_t launch_row_argmax(const float* z, int R, int V, unsigned long long* slots, hipStream_t s);
+// Copy tokens into/out of the session (int32 vectors).
+hipError_t launch_copy_i32(const int32_t* src, int32_t* dst, int n, hipStream_t s);
+
+// Beam search kernels.
+struct BeamState {
+  int B, W, V, T;
+  float* score;          // [R] live scores
+  float* cand_score;     // [R][2W] per-row best expansions
+  int32_t* cand_tok;     // [R][2W]
+  int32_t* tok_hist;     // [T][R] token chosen into slot r at step t
+  int32_t* par_hist;     // [T][R] parent row of slot r at step t
+  int32_t* hist;         // [2][R][T] position -> cache row, double buffered by step parity
+  float* fin_score;      // [B][W]
+  int32_t* fin_len;      // [B][W]
+  int32_t* fin_row;      // [B][W] row of the EOS candidate's parent (hypothesis) at step len-1
+  int32_t* fin_count;    // [B]
+  int32_t* done;         // [B]
+  int32_t* cur_tok;      // [R]
+  const float* lp;       // [T + 1] length penalties
+  int eos, pad, bos;
+};
+hipError_t launch_beam_reset(const BeamState& st, int* step, hipStream_t s);
+hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int* step, hipStream_t s);
+hipError_t launch_beam_update(const BeamState& st, int* step, hipStream_t s);
+hipError_t launch_beam_finalize(const BeamState& st, int steps, int32_t* out, int32_t* out_len, float* out_score,
+                                hipStream_t s);
+
+// Model files (model.cpp).
+int model_size(const void* blob, size_t n, size_t* bytes, std::string& err);
+int model_create(const void* blob, size_t n, void* d_arena, size_t arena_bytes, hipStream_t s, mnmt_model** out,
+                 std::string& err);
+
+// Canonical-arithmetic self check.
+hipError_t launch_debug_canon(int fn, const float* x, int n, float* y, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Model and session structures.
+
+struct LinearDev {
+  const int8_t* w = nullptr;  // [N, K]
+  const float* scale = nullptr;
+  const float* bias = nullptr;
+  int N = 0, K = 0;
+  float inv_in = 0.f;  // 1 / input scale (quantization of this layer's input)
+};
+
+struct LnDev {
+  const float* g = nullptr;
+  const float* b = nullptr;
+};
+
+struct LayerDev {
+  LnDev sa_ln, ca_ln, ff_ln;
+  LinearDev qkv, o, cq, ckv, co, w1, w2;
+  float sa_gamma = 1.f, ca_gamma = 1.f, ff_gamma = 1.f;
+  float sa_cqk = 0.f, sa_cpv = 0.f, ca_cqk = 0.f, ca_cpv = 0.f;
+};
+
+}  // namespace mnmt
+
+struct mnmt_model {
+  mnmt_model_info info{};
+  int dh = 0;
+  int device = 0;
+  size_t arena_bytes = 0;
+  const int8_t* E = nullptr;     // [V, d]
+  const float* c_emb = nullptr;  // [V]
+  const float* c_out = nullptr;  // [V]
+  const float* pe = nullptr;     // [P, d]
+  std::vector<mnmt::LayerDev> enc, dec;
+  mnmt::LnDev enc_ln, dec_ln;
+  float s_enc = 0.f, inv_enc = 0.f, inv_fin = 0.f;
+};
+
+struct mnmt_session {
+  const mnmt_model* m = nullptr;
+  mnmt_session_cfg cfg{};
+  int R = 0;  // max rows = max_batch * beam
+  // current batch
+  int B = 0, S = 0, W = 1;
+  bool encoded = false;
+  int host_step = 0;
+  // buffers (device)
+  int32_t* src = nullptr;
+  int32_t* len = nullptr;
+  float* enc_x = nullptr;
+  int8_t* enc_a = nullptr;
+  int8_t* enc_qkv = nullptr;
+  int8_t* enc_h = nullptr;
+  int8_t* enc_out = nullptr;
+  float* logits = nullptr;  // shares memory with the encoder scratch
+  std::vector<int8_t*> cross_kv;
+  float* dec_x = nullptr;
+  int8_t* dec_a = nullptr;
+  int8_t* dec_qkv = nullptr;
+  int8_t* dec_q = nullptr;
+  int8_t* dec_h = nullptr;
+  std::vector<int8_t*> kcache, vcache;
+  int32_t* cur_tok = nullptr;
+  int* step = nullptr;
+  unsigned long long* slots = nullptr;
+  int32_t* out_tok = nullptr;
+  int32_t* finished = nullptr;
+  int32_t* out_len = nullptr;
+  float* lp = nullptr;
+  mnmt::BeamState beam{};
+  std::map<std::string, std::pair<void*, size_t>> named;
+  // graph cache
+  hipStream_t capture_stream = nullptr;
+  std::map<std::string, hipGraphExec_t> graphs;
+};

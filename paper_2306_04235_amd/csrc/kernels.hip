@@ -1,0 +1,658 @@
+// kernels.hip -- embedding, LayerNorm + quantization, int8 attention with an
+// int8 key/value cache, and the greedy / beam search bookkeeping.
+// All fp32 arithmetic follows the canonical order of canon.hpp.
+#include <cfloat>
+#include <climits>
+
+#include "canon.hpp"
+#include "internal.h"
+
+namespace mnmt {
+namespace {
+
+constexpr int kMaxAttnLen = 256;  // longest attended sequence (4 keys per lane)
+constexpr int kMaxHeadDim = 128;  // 8 x 16 bytes of query in registers
+constexpr int kMaxRowLen = 1024;  // LayerNorm width (16 values per lane)
+
+__device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
+  acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.z, b.z, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
+  return acc;
+}
+
+// ---------------------------------------------------------------------------
+// Embedding: x = fma(E[tok], c_emb[tok], PE[pos]).  One wave per row.
+__global__ __launch_bounds__(256) void k_embed(const int32_t* __restrict__ tok, int rows, int S, const int* step,
+                                               const int8_t* __restrict__ E, const float* __restrict__ c_emb,
+                                               const float* __restrict__ pe, int d, int V, float* __restrict__ x) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  int t = tok[r];
+  t = t < 0 ? 0 : (t >= V ? V - 1 : t);  // ids outside the vocabulary are clamped (memory safety)
+  const int pos = step ? *step : r % S;
+  const float c = c_emb[t];
+  for (int i = lane; i < d; i += 64)
+    x[(size_t)r * d + i] = fmaf((float)E[(size_t)t * d + i], c, pe[(size_t)pos * d + i]);
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm + quantization.  One wave per row; element i lives in lane i % 64
+// and is added to that lane's partial in ascending i (canonical order).
+__global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, int rows, int d, int do_ln,
+                                                  const float* __restrict__ g, const float* __restrict__ b,
+                                                  float eps, float inv_s, int8_t* __restrict__ q,
+                                                  float* __restrict__ x_out) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const float* xr = x + (size_t)r * d;
+  float v[kMaxRowLen / 64];
+  const int n = (d + 63) / 64;
+  if (do_ln) {
+    float p = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kMaxRowLen / 64; ++j) {
+      const int i = lane + 64 * j;
+      if (j < n && i < d) {
+        v[j] = xr[i];
+        p = p + v[j];
+      }
+    }
+    const float inv_d = 1.0f / (float)d;
+    const float mu = wave_sum(p) * inv_d;
+    float p2 = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kMaxRowLen / 64; ++j) {
+      const int i = lane + 64 * j;
+      if (j < n && i < d) {
+        v[j] = v[j] - mu;
+        p2 = fmaf(v[j], v[j], p2);
+      }
+    }
+    const float var = wave_sum(p2) * inv_d;
+    const float rstd = 1.0f / sqrtf(var + eps);
+#pragma unroll
+    for (int j = 0; j < kMaxRowLen / 64; ++j) {
+      const int i = lane + 64 * j;
+      if (j < n && i < d) v[j] = fmaf(v[j] * rstd, g[i], b[i]);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kMaxRowLen / 64; ++j) {
+      const int i = lane + 64 * j;
+      if (j < n && i < d) v[j] = xr[i];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kMaxRowLen / 64; ++j) {
+    const int i = lane + 64 * j;
+    if (j < n && i < d) {
+      if (q) q[(size_t)r * d + i] = code_of(v[j] * inv_s);
+      if (x_out) x_out[(size_t)r * d + i] = v[j];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Attention of one query row over n keys for one head, by one wave
+// (Appendix A self-weight / self-sum equations with the quantizer figure's
+// precisions): int8 scores, fp32 softmax in the canonical order, context
+// accumulated over ascending key index with one fma per key, requantized.
+// key(t) / val(t) give the head's dh codes of key / value t.
+template <class KeyFn, class ValFn>
+__device__ __forceinline__ void attend_wave(const int8_t* __restrict__ q, int n, int dh, KeyFn key, ValFn val,
+                                            float c_qk, float c_pv, int8_t* __restrict__ out, float* p_sh) {
+  const int lane = threadIdx.x & 63;
+  const int nc = dh / 16;
+  int4 qv[kMaxHeadDim / 16];
+#pragma unroll
+  for (int c = 0; c < kMaxHeadDim / 16; ++c) qv[c] = c < nc ? *(const int4*)(q + 16 * c) : make_int4(0, 0, 0, 0);
+  float sv[kMaxAttnLen / 64];
+  float mx = -FLT_MAX;
+#pragma unroll
+  for (int i = 0; i < kMaxAttnLen / 64; ++i) {
+    const int t = lane + 64 * i;
+    sv[i] = 0.0f;
+    if (t < n) {
+      const int8_t* kp = key(t);
+      int acc = 0;
+#pragma unroll
+      for (int c = 0; c < kMaxHeadDim / 16; ++c)
+        if (c < nc) acc = dot16(*(const int4*)(kp + 16 * c), qv[c], acc);
+      sv[i] = (float)acc * c_qk;
+      mx = fmaxf(mx, sv[i]);
+    }
+  }
+  mx = wave_max(mx);
+  float part = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kMaxAttnLen / 64; ++i) {
+    const int t = lane + 64 * i;
+    if (t < n) {
+      sv[i] = canon_exp(sv[i] - mx);
+      part = part + sv[i];
+    }
+  }
+  const float inv = 1.0f / wave_sum(part);
+#pragma unroll
+  for (int i = 0; i < kMaxAttnLen / 64; ++i) {
+    const int t = lane + 64 * i;
+    if (t < n) p_sh[t] = sv[i] * inv;
+  }
+  __syncthreads();  // the block is this one wave: publish p to every lane
+  for (int j = lane; j < dh; j += 64) {
+    float acc = 0.0f;
+    for (int t = 0; t < n; ++t) acc = fmaf(p_sh[t], (float)val(t)[j], acc);
+    out[j] = code_of(acc * c_pv);
+  }
+}
+
+// Encoder self-attention: block = one wave = (query s, head hd, sentence b).
+__global__ __launch_bounds__(64) void k_attn_enc(const int8_t* __restrict__ qkv, const int32_t* __restrict__ len,
+                                                 int S, int d, int dh, float c_qk, float c_pv,
+                                                 int8_t* __restrict__ ctx) {
+  __shared__ float p_sh[kMaxAttnLen];
+  const int s = blockIdx.x, hd = blockIdx.y, b = blockIdx.z;
+  int n = len[b];
+  n = n < 1 ? 1 : (n > S ? S : n);
+  const int8_t* base = qkv + (size_t)b * S * 3 * d;
+  const int8_t* q = base + (size_t)s * 3 * d + hd * dh;
+  auto key = [&](int t) { return base + (size_t)t * 3 * d + d + hd * dh; };
+  auto val = [&](int t) { return base + (size_t)t * 3 * d + 2 * d + hd * dh; };
+  attend_wave(q, n, dh, key, val, c_qk, c_pv, ctx + ((size_t)b * S + s) * d + hd * dh, p_sh);
+}
+
+// Decoder self-attention at position t = *step: block = one wave = (head, row).
+__global__ __launch_bounds__(64) void k_attn_dec_self(const int8_t* __restrict__ qkv, int d, int dh, int T,
+                                                      const int* __restrict__ step, int8_t* __restrict__ kcache,
+                                                      int8_t* __restrict__ vcache, const int32_t* __restrict__ hist,
+                                                      float c_qk, float c_pv, int8_t* __restrict__ ctx) {
+  __shared__ float p_sh[kMaxAttnLen];
+  const int hd = blockIdx.x, r = blockIdx.y;
+  const int lane = threadIdx.x;
+  int t = *step;
+  t = t < 0 ? 0 : (t >= T ? T - 1 : t);
+  const int8_t* row = qkv + (size_t)r * 3 * d;
+  const int8_t* knew = row + d + hd * dh;
+  const int8_t* vnew = row + 2 * d + hd * dh;
+  for (int j = lane; j < dh; j += 64) {
+    kcache[((size_t)r * T + t) * d + hd * dh + j] = knew[j];
+    vcache[((size_t)r * T + t) * d + hd * dh + j] = vnew[j];
+  }
+  // beam: hist holds two [R][T] tables used on alternate steps
+  const int R = gridDim.y;
+  const int32_t* hr = hist ? hist + ((size_t)(t & 1) * R + r) * T : nullptr;
+  auto key = [&](int tp) {
+    if (tp == t) return knew;
+    const int src = hr ? hr[tp] : r;
+    return (const int8_t*)kcache + ((size_t)src * T + tp) * d + hd * dh;
+  };
+  auto val = [&](int tp) {
+    if (tp == t) return vnew;
+    const int src = hr ? hr[tp] : r;
+    return (const int8_t*)vcache + ((size_t)src * T + tp) * d + hd * dh;
+  };
+  attend_wave(row + hd * dh, t + 1, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh, p_sh);
+}
+
+// Decoder cross-attention: row r attends over the source of sentence r / W.
+__global__ __launch_bounds__(64) void k_attn_dec_cross(const int8_t* __restrict__ q, int W, int d, int dh,
+                                                       const int8_t* __restrict__ kv, int S,
+                                                       const int32_t* __restrict__ len, float c_qk, float c_pv,
+                                                       int8_t* __restrict__ ctx) {
+  __shared__ float p_sh[kMaxAttnLen];
+  const int hd = blockIdx.x, r = blockIdx.y;
+  const int b = r / W;
+  int n = len[b];
+  n = n < 1 ? 1 : (n > S ? S : n);
+  const int8_t* base = kv + (size_t)b * S * 2 * d;
+  auto key = [&](int t) { return base + (size_t)t * 2 * d + hd * dh; };
+  auto val = [&](int t) { return base + (size_t)t * 2 * d + d + hd * dh; };
+  attend_wave(q + (size_t)r * d + hd * dh, n, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh, p_sh);
+}
+
+// ---------------------------------------------------------------------------
+// Greedy search bookkeeping.
+__global__ void k_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
+                               int32_t* out_len, int* step, int bos) {
+  for (int r = threadIdx.x; r < R; r += blockDim.x) {
+    slots[r] = 0ull;
+    cur_tok[r] = bos;
+    finished[r] = 0;
+    out_len[r] = steps;
+  }
+  if (threadIdx.x == 0) *step = 0;
+}
+
+// Reads the step's arg-max slots (and clears them for the next step), records
+// the tokens, applies the end-of-sentence rule and advances the step counter.
+__global__ void k_greedy_commit(unsigned long long* slots, int R, int T, int32_t* cur_tok, int32_t* out_tok,
+                                int32_t* finished, int32_t* out_len, int* step, int stop_at_eos, int eos,
+                                int pad) {
+  const int t = *step;
+  __syncthreads();  // every thread has read the step before it advances
+  for (int r = threadIdx.x; r < R; r += blockDim.x) {
+    const int tok = unpack_index(slots[r]);
+    slots[r] = 0ull;
+    const int fin = finished[r];
+    if (t < T) out_tok[(size_t)t * R + r] = fin ? pad : tok;
+    if (!fin && stop_at_eos && tok == eos) {
+      finished[r] = 1;
+      out_len[r] = t + 1;
+    }
+    cur_tok[r] = fin ? pad : tok;
+  }
+  if (threadIdx.x == 0) *step = t + 1;
+}
+
+__global__ void k_greedy_output(const int32_t* out_tok, const int32_t* out_len, int R, int T, int32_t* out,
+                                int32_t* out_len_dst) {
+  const int r = blockIdx.x;
+  for (int t = threadIdx.x; t < T; t += blockDim.x) out[(size_t)r * T + t] = out_tok[(size_t)t * R + r];
+  if (threadIdx.x == 0) out_len_dst[r] = out_len[r];
+}
+
+// Arg-max of fp32 rows (smallest index among equal maxima), one wave per row.
+__global__ __launch_bounds__(256) void k_row_argmax(const float* __restrict__ z, int R, int V,
+                                                    unsigned long long* slots) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= R) return;
+  unsigned long long best = 0ull;
+  for (int v = lane; v < V; v += 64) {
+    const unsigned long long k = pack_argmax(z[(size_t)r * V + v], v);
+    best = k > best ? k : best;
+  }
+  best = wave_max_u64(best);
+  if (lane == 0) slots[r] = best;
+}
+
+__global__ void k_copy_i32(const int32_t* src, int32_t* dst, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+}
+
+// ---------------------------------------------------------------------------
+// Beam search.  Rows r = b * W + j hold the W hypotheses of sentence b.
+
+// Candidate order: higher score first, then smaller index.
+__device__ __forceinline__ bool better(float c1, int i1, float c2, int i2) {
+  return c1 > c2 || (c1 == c2 && i1 < i2);
+}
+
+__global__ void k_beam_reset(BeamState st, int* step) {
+  const int R = st.B * st.W;
+  for (int r = threadIdx.x + blockIdx.x * blockDim.x; r < R; r += blockDim.x * gridDim.x) {
+    st.score[r] = 0.0f;
+    st.cur_tok[r] = st.bos;
+    for (int t = 0; t < st.T; ++t) {  // every position points at a valid cache row
+      st.hist[(size_t)r * st.T + t] = r;
+      st.hist[(size_t)(R + r) * st.T + t] = r;
+      st.tok_hist[(size_t)t * R + r] = st.pad;
+      st.par_hist[(size_t)t * R + r] = r;
+    }
+  }
+  for (int b = threadIdx.x + blockIdx.x * blockDim.x; b < st.B; b += blockDim.x * gridDim.x) {
+    st.fin_count[b] = 0;
+    st.done[b] = 0;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *step = 0;
+}
+
+// Per live row: log-softmax statistics of the logits (max, then the canonical
+// sum of exp(z - max), lse = max + ln sum) and the row's K = 2W best
+// expansions by (score + (z - lse) desc, token asc).  One wave per row.
+template <int K>
+__global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logits, BeamState st,
+                                                  const int* __restrict__ step) {
+  const int r = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int t = *step;
+  const int b = r / st.W, j = r % st.W;
+  if (st.done[b] || (t == 0 && j > 0)) return;
+  const int V = st.V;
+  const float* z = logits + (size_t)r * V;
+  float mx = -FLT_MAX;
+  for (int v = lane; v < V; v += 64) mx = fmaxf(mx, z[v]);
+  mx = wave_max(mx);
+  float part = 0.0f;
+  for (int v = lane; v < V; v += 64) part = part + canon_exp(z[v] - mx);
+  const float lse = mx + canon_log(wave_sum(part));
+  const float sc = st.score[r];
+  float ls[K];
+  int lv[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    ls[k] = -FLT_MAX;
+    lv[k] = INT_MAX;
+  }
+  for (int v = lane; v < V; v += 64) {
+    float c = sc + (z[v] - lse);
+    int cv = v;
+    if (!better(c, cv, ls[K - 1], lv[K - 1])) continue;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {  // insertion by swapping keeps the list sorted
+      if (better(c, cv, ls[k], lv[k])) {
+        const float tc = ls[k];
+        const int tv = lv[k];
+        ls[k] = c;
+        lv[k] = cv;
+        c = tc;
+        cv = tv;
+      }
+    }
+  }
+  // Merge the 64 sorted lists: K rounds of a wave-wide maximum of the heads.
+  for (int k = 0; k < K; ++k) {
+    const unsigned long long mine = lv[0] == INT_MAX ? 0ull : pack_argmax(ls[0], lv[0]);
+    const unsigned long long win = wave_max_u64(mine);
+    if (mine == win && win != 0ull) {
+#pragma unroll
+      for (int i = 0; i + 1 < K; ++i) {
+        ls[i] = ls[i + 1];
+        lv[i] = lv[i + 1];
+      }
+      ls[K - 1] = -FLT_MAX;
+      lv[K - 1] = INT_MAX;
+    }
+    if (lane == 0) {
+      const int v = win ? unpack_index(win) : 0;
+      st.cand_tok[(size_t)r * K + k] = v;
+      st.cand_score[(size_t)r * K + k] = win ? sc + (z[v] - lse) : -FLT_MAX;
+    }
+  }
+}
+
+// Per sentence: merge the W rows' candidates, finish EOS hypotheses, refill
+// the W live slots and advance the key/value history.  One wave per sentence.
+template <int W_MAX>
+__global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step) {
+  constexpr int NC = W_MAX * 2 * W_MAX;  // candidates per sentence
+  __shared__ float cs[NC];
+  __shared__ int cj[NC], cv[NC];
+  __shared__ int order[2 * W_MAX];
+  __shared__ int new_par[W_MAX], new_tok[W_MAX];
+  __shared__ float new_score[W_MAX];
+  __shared__ int n_live_sh, done_sh;
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int W = st.W, K = 2 * W, R = st.B * W, T = st.T, V = st.V;
+  const int t = *step;
+  const bool active = !st.done[b];
+  if (active) {
+    const int n_alive = t == 0 ? 1 : W;
+    const int n = n_alive * K;
+    for (int i = lane; i < NC; i += 64) {
+      if (i < n) {
+        const int jj = i / K, k = i % K;
+        const int r = b * W + jj;
+        cs[i] = st.cand_score[(size_t)r * K + k];
+        cv[i] = st.cand_tok[(size_t)r * K + k];
+        cj[i] = jj;
+      }
+    }
+    __syncthreads();
+    // rank of each candidate = number of better candidates (flat index j*V + v breaks ties)
+    for (int i = lane; i < n; i += 64) {
+      int rank = 0;
+      const long fi = (long)cj[i] * V + cv[i];
+      for (int o = 0; o < n; ++o) {
+        const long fo = (long)cj[o] * V + cv[o];
+        rank += (cs[o] > cs[i] || (cs[o] == cs[i] && fo < fi)) ? 1 : 0;
+      }
+      if (rank < K) order[rank] = i;
+    }
+    __syncthreads();
+    if (lane == 0) {
+      int n_live = 0;
+      int fc = st.fin_count[b];
+      const int n_top = n < K ? n : K;
+      for (int rk = 0; rk < n_top && n_live < W; ++rk) {
+        const int i = order[rk];
+        if (cv[i] == st.eos) {
+          if (rk < W && fc < W) {
+            st.fin_score[b * W + fc] = cs[i] / st.lp[t + 1];
+            st.fin_len[b * W + fc] = t + 1;
+            st.fin_row[b * W + fc] = b * W + cj[i];
+            ++fc;
+          }
+          continue;
+        }
+        new_par[n_live] = b * W + cj[i];
+        new_tok[n_live] = cv[i];
+        new_score[n_live] = cs[i];
+        ++n_live;
+      }
+      st.fin_count[b] = fc;
+      if (fc >= W) st.done[b] = 1;
+      n_live_sh = n_live;
+      done_sh = fc >= W;
+    }
+    __syncthreads();
+    if (!done_sh) {
+      const int n_live = n_live_sh;
+      const int32_t* hcur = st.hist + (size_t)(t & 1) * R * T;
+      int32_t* hnext = st.hist + (size_t)((t + 1) & 1) * R * T;
+      for (int s = 0; s < n_live; ++s) {
+        const int p = b * W + s, par = new_par[s];
+        for (int tp = lane; tp <= t && tp < T; tp += 64) hnext[(size_t)p * T + tp] = tp < t ? hcur[(size_t)par * T + tp] : par;
+        if (lane == 0) {
+          st.score[p] = new_score[s];
+          st.cur_tok[p] = new_tok[s];
+          if (t < T) {
+            st.tok_hist[(size_t)t * R + p] = new_tok[s];
+            st.par_hist[(size_t)t * R + p] = par;
+          }
+        }
+      }
+    }
+  }
+  // The step counter is advanced by k_step_advance after every sentence.
+}
+
+__global__ void k_step_advance(int* step) {
+  if (threadIdx.x == 0) *step = *step + 1;
+}
+
+// Backtrack the tokens of the hypothesis held by `row` after step `last`
+// (positions 0..last) into out[0..last].
+__device__ void backtrack(const BeamState& st, int row, int last, int32_t* out) {
+  const int R = st.B * st.W;
+  for (int t = last; t >= 0; --t) {
+    out[t] = st.tok_hist[(size_t)t * R + row];
+    row = st.par_hist[(size_t)t * R + row];
+  }
+}
+
+// Per sentence: finish the live hypotheses if the sentence never completed,
+// pick the best normalized score (the first finished among equals: EOS
+// hypotheses in the order they finished, then the live slots in slot order)
+// and write its tokens.  One thread per sentence.
+__global__ void k_beam_finalize(BeamState st, int steps, int32_t* out, int32_t* out_len, float* out_score) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= st.B) return;
+  const int W = st.W;
+  int kind = -1, idx = 0;  // kind 0: finished entry idx; kind 1: live slot idx
+  float best = 0.0f;
+  const int fc = st.fin_count[b];
+  for (int i = 0; i < fc; ++i) {
+    const float v = st.fin_score[b * W + i];
+    if (kind < 0 || v > best) {
+      best = v;
+      kind = 0;
+      idx = i;
+    }
+  }
+  if (!st.done[b]) {
+    for (int s = 0; s < W; ++s) {
+      const float v = st.score[b * W + s] / st.lp[steps];
+      if (kind < 0 || v > best) {
+        best = v;
+        kind = 1;
+        idx = s;
+      }
+    }
+  }
+  int32_t* o = out + (size_t)b * steps;
+  int L;
+  if (kind == 1) {
+    L = steps;
+    backtrack(st, b * W + idx, steps - 1, o);
+  } else {
+    L = st.fin_len[b * W + idx];
+    if (L > 1) backtrack(st, st.fin_row[b * W + idx], L - 2, o);
+    o[L - 1] = st.eos;
+  }
+  for (int t = L; t < steps; ++t) o[t] = st.pad;
+  out_len[b] = L;
+  if (out_score) out_score[b] = best;
+}
+
+// ---------------------------------------------------------------------------
+__global__ void k_debug_canon(int fn, const float* x, int n, float* y) {
+  const int lane = threadIdx.x & 63;
+  if (fn == 0 || fn == 1) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += blockDim.x * gridDim.x)
+      y[i] = fn == 0 ? canon_exp(x[i]) : canon_log(x[i]);
+    return;
+  }
+  if (blockIdx.x != 0 || threadIdx.x >= 64) return;
+  if (fn == 2) {
+    float p = 0.0f;
+    for (int i = lane; i < n; i += 64) p = p + x[i];
+    p = wave_sum(p);
+    if (lane == 0) y[0] = p;
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Launchers.
+
+hipError_t launch_embed(const int32_t* tok, int rows, int S_for_pos, const int* step, const int8_t* E,
+                        const float* c_emb, const float* pe, int d, int V, float* x, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_embed, dim3((rows + 3) / 4), dim3(256), 0, s, tok, rows, S_for_pos, step, E, c_emb, pe, d, V,
+                     x);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_quant(const float* x, int rows, int d, int do_ln, const float* g, const float* b, float eps,
+                           float inv_s, int8_t* q, float* x_out, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (d > kMaxRowLen) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_ln_quant, dim3((rows + 3) / 4), dim3(256), 0, s, x, rows, d, do_ln, g, b, eps, inv_s, q,
+                     x_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_enc(const int8_t* qkv, const int32_t* len, int B, int S, int d, int h, float c_qk, float c_pv,
+                           int8_t* ctx, hipStream_t s) {
+  const int dh = d / h;
+  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_attn_enc, dim3(S, h, B), dim3(64), 0, s, qkv, len, S, d, dh, c_qk, c_pv, ctx);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, const int* step, int8_t* kcache,
+                                int8_t* vcache, const int32_t* hist, float c_qk, float c_pv, int8_t* ctx,
+                                hipStream_t s) {
+  const int dh = d / h;
+  if (T > kMaxAttnLen || dh > kMaxHeadDim || dh % 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_attn_dec_self, dim3(h, R), dim3(64), 0, s, qkv, d, dh, T, step, kcache, vcache, hist, c_qk,
+                     c_pv, ctx);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, const int8_t* kv, int S,
+                                 const int32_t* len, float c_qk, float c_pv, int8_t* ctx, hipStream_t s) {
+  const int dh = d / h;
+  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_attn_dec_cross, dim3(h, R), dim3(64), 0, s, q, W, d, dh, kv, S, len, c_qk, c_pv, ctx);
+  return hipGetLastError();
+}
+
+hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
+                               int32_t* out_len, int* step, int bos, hipStream_t s) {
+  hipLaunchKernelGGL(k_greedy_reset, dim3(1), dim3(256), 0, s, slots, R, steps, cur_tok, finished, out_len, step,
+                     bos);
+  return hipGetLastError();
+}
+
+hipError_t launch_greedy_commit(unsigned long long* slots, int R, int T, int32_t* cur_tok, int32_t* out_tok,
+                                int32_t* finished, int32_t* out_len, int* step, int stop_at_eos, int eos, int pad,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(k_greedy_commit, dim3(1), dim3(256), 0, s, slots, R, T, cur_tok, out_tok, finished, out_len,
+                     step, stop_at_eos, eos, pad);
+  return hipGetLastError();
+}
+
+hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, int R, int T, int32_t* out,
+                                int32_t* out_len_dst, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_greedy_output, dim3(R), dim3(64), 0, s, out_tok, out_len, R, T, out, out_len_dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_row_argmax(const float* z, int R, int V, unsigned long long* slots, hipStream_t s) {
+  if (R <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_row_argmax, dim3((R + 3) / 4), dim3(256), 0, s, z, R, V, slots);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_i32(const int32_t* src, int32_t* dst, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_copy_i32, dim3((n + 255) / 256), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_beam_reset(const BeamState& st, int* step, hipStream_t s) {
+  const int R = st.B * st.W;
+  hipLaunchKernelGGL(k_beam_reset, dim3((R + 255) / 256), dim3(256), 0, s, st, step);
+  return hipGetLastError();
+}
+
+hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int* step, hipStream_t s) {
+  const int R = st.B * st.W;
+  switch (2 * st.W) {
+    case 2: hipLaunchKernelGGL(k_beam_topk<2>, dim3(R), dim3(64), 0, s, logits, st, step); break;
+    case 4: hipLaunchKernelGGL(k_beam_topk<4>, dim3(R), dim3(64), 0, s, logits, st, step); break;
+    case 6: hipLaunchKernelGGL(k_beam_topk<6>, dim3(R), dim3(64), 0, s, logits, st, step); break;
+    case 8: hipLaunchKernelGGL(k_beam_topk<8>, dim3(R), dim3(64), 0, s, logits, st, step); break;
+    case 10: hipLaunchKernelGGL(k_beam_topk<10>, dim3(R), dim3(64), 0, s, logits, st, step); break;
+    case 12: hipLaunchKernelGGL(k_beam_topk<12>, dim3(R), dim3(64), 0, s, logits, st, step); break;
+    case 14: hipLaunchKernelGGL(k_beam_topk<14>, dim3(R), dim3(64), 0, s, logits, st, step); break;
+    case 16: hipLaunchKernelGGL(k_beam_topk<16>, dim3(R), dim3(64), 0, s, logits, st, step); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_beam_update(const BeamState& st, int* step, hipStream_t s) {
+  if (st.W > 8) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_beam_update<8>, dim3(st.B), dim3(64), 0, s, st, step);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_step_advance, dim3(1), dim3(64), 0, s, step);
+  return hipGetLastError();
+}
+
+hipError_t launch_beam_finalize(const BeamState& st, int steps, int32_t* out, int32_t* out_len,
+                                      float* out_score, hipStream_t s) {
+  hipLaunchKernelGGL(k_beam_finalize, dim3((st.B + 63) / 64), dim3(64), 0, s, st, steps, out, out_len, out_score);
+  return hipGetLastError();
+}
+
+hipError_t launch_debug_canon(int fn, const float* x, int n, float* y, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (fn < 0 || fn > 2) return hipErrorInvalidValue;
+  const int blocks = (fn == 2) ? 1 : (n + 255) / 256 > 1024 ? 1024 : (n + 255) / 256;
+  hipLaunchKernelGGL(k_debug_canon, dim3(blocks), dim3(256), 0, s, fn, x, n, y);
+  return hipGetLastError();
+}
+
+}  // namespace mnmt

@@ -1,0 +1,284 @@
+// qlinear.hip -- int8 x int8 -> int32 linear layers with fused epilogues
+// (8-bit GEMM of Section 4.1; requantization, bias, ReLU, residual and
+// dequantization fused between GEMMs as in Section 4.2).
+//
+// Two kernels:
+//  * qgemv: M <= 8 rows (batch-1 decoding).  Bandwidth bound: every weight
+//    byte is read once.  A weight row of K bytes is split over LPR lanes that
+//    each load 16 contiguous bytes (one dwordx4) per step, so one wave
+//    instruction reads 64 * 16 = 1024 contiguous bytes; U independent row
+//    groups per wave keep several loads in flight.  Products use the 4-way
+//    int8 dot instruction; the LPR partial sums meet in an xor butterfly.
+//  * qgemm: M > 8.  i8 matrix cores (v_mfma_i32_32x32x32_i8) on 64-deep K
+//    slabs staged in LDS; each of the 4 waves owns a tile of 32x32 fragments.
+// Integer accumulation is exact, so neither kernel's order matters; the fp32
+// epilogue is the same single expression in both.
+#include "canon.hpp"
+#include "internal.h"
+
+namespace mnmt {
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
+  acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.z, b.z, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
+  return acc;
+}
+
+// The fused epilogue of one output element (row m, column n).
+__device__ __forceinline__ void epilogue_store(const EpiArgs& e, int m, int n, int acc, const float* scale,
+                                               const float* bias) {
+  const float a = (float)acc;
+  const size_t o = (size_t)m * e.ldo + n;
+  switch (e.kind) {
+    case MNMT_EPI_I32:
+      ((int*)e.out)[o] = acc;
+      break;
+    case MNMT_EPI_I8:
+      ((int8_t*)e.out)[o] = code_of(fmaf(a, scale[n], bias[n]));
+      break;
+    case MNMT_EPI_I8_RELU:
+      ((int8_t*)e.out)[o] = code_of(fmaxf(fmaf(a, scale[n], bias[n]), 0.0f));
+      break;
+    case MNMT_EPI_F32:
+      ((float*)e.out)[o] = fmaf(a, scale[n], bias[n]);
+      break;
+    case MNMT_EPI_F32_RESID: {
+      float* y = (float*)e.out + o;
+      *y = fmaf(e.gamma, *y, fmaf(a, scale[n], bias[n]));
+      break;
+    }
+    default:  // LOGITS
+      ((float*)e.out)[o] = a * scale[n];
+      break;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// qgemv: MR = max rows of X, LPR = lanes per weight row, U = row groups per wave
+template <int MR, int LPR, int U>
+__global__ __launch_bounds__(256) void k_qgemv(const int8_t* __restrict__ X, int ldx, const int8_t* __restrict__ W,
+                                               int M, int K, int N, const float* __restrict__ scale,
+                                               const float* __restrict__ bias, EpiArgs e) {
+  constexpr int RPI = 64 / LPR;  // weight rows per wave instruction
+  const int lane = threadIdx.x & 63;
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int sub = lane / LPR;
+  const int kl = lane % LPR;
+  const int row0 = wave * RPI * U;
+  int acc[U][MR];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int m = 0; m < MR; ++m) acc[u][m] = 0;
+
+  for (int k = kl * 16; k < K; k += LPR * 16) {
+    int4 wv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int n = row0 + u * RPI + sub;
+      wv[u] = n < N ? *(const int4*)(W + (size_t)n * K + k) : make_int4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int m = 0; m < MR; ++m) {
+      if (m < M) {
+        const int4 xv = *(const int4*)(X + (size_t)m * ldx + k);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc[u][m] = dot16(wv[u], xv, acc[u][m]);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = LPR / 2; off >= 1; off >>= 1)
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < MR; ++m) acc[u][m] += __shfl_xor(acc[u][m], off, 64);
+
+  if (e.kind == EPI_LOGITS_ARGMAX) {
+#pragma unroll
+    for (int m = 0; m < MR; ++m) {
+      if (m >= M) break;
+      unsigned long long best = 0ull;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int n = row0 + u * RPI + sub;
+        if (kl == 0 && n < N) {
+          const float z = (float)acc[u][m] * scale[n];
+          if (e.out) ((float*)e.out)[(size_t)m * e.ldo + n] = z;
+          const unsigned long long key = pack_argmax(z, n);
+          best = key > best ? key : best;
+        }
+      }
+      best = wave_max_u64(best);
+      if (lane == 0 && best != 0ull) atomicMax(e.argmax + m, best);
+    }
+    return;
+  }
+  if (kl != 0) return;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int n = row0 + u * RPI + sub;
+    if (n >= N) continue;
+#pragma unroll
+    for (int m = 0; m < MR; ++m)
+      if (m < M) epilogue_store(e, m, n, acc[u][m], scale, bias);
+  }
+}
+
+template <int MR, int LPR>
+hipError_t gemv_u(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
+                  int N, const EpiArgs& e, hipStream_t s) {
+  constexpr int RPI = 64 / LPR;
+  // Enough waves to cover the chip: fewer row groups per wave for small N.
+  const long waves4 = ((long)N + RPI * 4 - 1) / (RPI * 4);
+  if (waves4 >= 1024) {
+    const int blocks = (int)((waves4 + 3) / 4);
+    hipLaunchKernelGGL((k_qgemv<MR, LPR, 4>), dim3(blocks), dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, e);
+  } else if (waves4 * 2 >= 1024) {
+    const long waves = ((long)N + RPI * 2 - 1) / (RPI * 2);
+    hipLaunchKernelGGL((k_qgemv<MR, LPR, 2>), dim3((int)((waves + 3) / 4)), dim3(256), 0, s, X, ldx, W, M, K, N,
+                       scale, bias, e);
+  } else {
+    const long waves = ((long)N + RPI - 1) / RPI;
+    hipLaunchKernelGGL((k_qgemv<MR, LPR, 1>), dim3((int)((waves + 3) / 4)), dim3(256), 0, s, X, ldx, W, M, K, N,
+                       scale, bias, e);
+  }
+  return hipGetLastError();
+}
+
+template <int MR>
+hipError_t gemv_lpr(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
+                    int N, const EpiArgs& e, hipStream_t s) {
+  const int chunks = K / 16;
+  if (chunks >= 64) return gemv_u<MR, 64>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (chunks >= 32) return gemv_u<MR, 32>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (chunks >= 16) return gemv_u<MR, 16>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (chunks >= 8) return gemv_u<MR, 8>(X, ldx, W, scale, bias, M, K, N, e, s);
+  return gemv_u<MR, 4>(X, ldx, W, scale, bias, M, K, N, e, s);
+}
+
+// ---------------------------------------------------------------------------
+// qgemm: BM x BN output tile per 256-thread block, 64-deep K slabs in LDS.
+template <int BM, int BN, int WAVES_M>
+__global__ __launch_bounds__(256) void k_qgemm(const int8_t* __restrict__ X, int ldx, const int8_t* __restrict__ W,
+                                               int M, int K, int N, const float* __restrict__ scale,
+                                               const float* __restrict__ bias, EpiArgs e) {
+  constexpr int BK = 64;
+  constexpr int LDS_STRIDE = BK + 16;  // bytes; the pad spreads rows over LDS banks
+  constexpr int WAVES_N = 4 / WAVES_M;
+  constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
+  constexpr int FM = WTM / 32, FN = WTN / 32;
+  static_assert(FM >= 1 && FN >= 1, "wave tile must hold whole 32x32 fragments");
+  __shared__ __attribute__((aligned(16))) int8_t As[BM * LDS_STRIDE];
+  __shared__ __attribute__((aligned(16))) int8_t Bs[BN * LDS_STRIDE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  v16i acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
+
+  constexpr int A_CHUNKS = BM * (BK / 16), B_CHUNKS = BN * (BK / 16);
+  int4 ra[(A_CHUNKS + 255) / 256], rb[(B_CHUNKS + 255) / 256];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < (A_CHUNKS + 255) / 256; ++i) {
+      const int c = tid + i * 256;
+      const int r = c >> 2, kc = (c & 3) * 16;
+      ra[i] = (c < A_CHUNKS && m0 + r < M) ? *(const int4*)(X + (size_t)(m0 + r) * ldx + k0 + kc)
+                                            : make_int4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < (B_CHUNKS + 255) / 256; ++i) {
+      const int c = tid + i * 256;
+      const int r = c >> 2, kc = (c & 3) * 16;
+      rb[i] = (c < B_CHUNKS && n0 + r < N) ? *(const int4*)(W + (size_t)(n0 + r) * K + k0 + kc)
+                                            : make_int4(0, 0, 0, 0);
+    }
+  };
+  auto lstore = [&]() {
+#pragma unroll
+    for (int i = 0; i < (A_CHUNKS + 255) / 256; ++i) {
+      const int c = tid + i * 256;
+      if (c < A_CHUNKS) *(int4*)(As + (c >> 2) * LDS_STRIDE + (c & 3) * 16) = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < (B_CHUNKS + 255) / 256; ++i) {
+      const int c = tid + i * 256;
+      if (c < B_CHUNKS) *(int4*)(Bs + (c >> 2) * LDS_STRIDE + (c & 3) * 16) = rb[i];
+    }
+  };
+
+  gload(0);
+  for (int k0 = 0; k0 < K; k0 += BK) {
+    __syncthreads();  // previous slab fully consumed
+    lstore();
+    __syncthreads();
+    if (k0 + BK < K) gload(k0 + BK);  // prefetch the next slab while computing
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 32) {
+      v4i a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        a[i] = *(const v4i*)(As + (wm * WTM + i * 32 + (lane & 31)) * LDS_STRIDE + kk + (lane >> 5) * 16);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = *(const v4i*)(Bs + (wn * WTN + j * 32 + (lane & 31)) * LDS_STRIDE + kk + (lane >> 5) * 16);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // Fragment layout: element r of lane l sits at row 8*(r/4) + 4*(l/32) + r%4, column l%32.
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int col = n0 + wn * WTN + j * 32 + (lane & 31);
+      if (col >= N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (row < M) epilogue_store(e, row, col, acc[i][j][r], scale, bias);
+      }
+    }
+}
+
+template <int BM, int BN, int WAVES_M>
+hipError_t gemm_launch(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
+                       int K, int N, const EpiArgs& e, hipStream_t s) {
+  dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
+  hipLaunchKernelGGL((k_qgemm<BM, BN, WAVES_M>), grid, dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, e);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
+                          int K, int N, const EpiArgs& e, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (M <= 8) {
+    if (M == 1) return gemv_lpr<1>(X, ldx, W, scale, bias, M, K, N, e, s);
+    if (M == 2) return gemv_lpr<2>(X, ldx, W, scale, bias, M, K, N, e, s);
+    if (M <= 4) return gemv_lpr<4>(X, ldx, W, scale, bias, M, K, N, e, s);
+    return gemv_lpr<8>(X, ldx, W, scale, bias, M, K, N, e, s);
+  }
+  if (e.kind == EPI_LOGITS_ARGMAX) return hipErrorInvalidValue;  // arg-max fusion is a batch-1 path
+  if (M <= 32) return gemm_launch<32, 128, 1>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (M <= 64) return gemm_launch<64, 128, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+  return gemm_launch<128, 128, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+}
+
+}  // namespace mnmt

@@ -1,0 +1,459 @@
+// session.cpp -- workspace plan, encoder / decoder drivers, greedy and beam
+// search loops, and hipGraph capture of a whole search.
+//
+// Workspace plan (Section 4.2: buffers shared by operations that never live
+// at the same time): the encoder's activations (fp32 residual, int8 LN/context
+// buffer, int8 QKV, int8 FFN hidden, int8 output) share one region with the
+// decoder's fp32 logits, which are only needed after encoding has finished.
+// Each layer reuses the same few buffers: one fp32 residual stream and int8
+// buffers for the sublayer input, attention context and FFN hidden layer.
+#include <cmath>
+#include <cstring>
+#include <string>
+
+#include "internal.h"
+
+namespace mnmt {
+namespace {
+
+struct Bump {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = (off + 255) / 256 * 256;
+    off = o + bytes;
+    return o;
+  }
+};
+
+struct Plan {
+  size_t src, len, region, enc_x, enc_a, enc_qkv, enc_h, enc_out, logits;
+  std::vector<size_t> cross_kv, kc, vc;
+  size_t dec_x, dec_a, dec_qkv, dec_q, dec_h;
+  size_t cur_tok, step, slots, out_tok, finished, out_len, lp;
+  size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
+  size_t total;
+};
+
+int validate_cfg(const mnmt_model* m, const mnmt_session_cfg* c) {
+  if (!m || !c) return set_error(MNMT_E_INVALID_ARG, "null model or session config");
+  const int P = m->info.max_pos;
+  if (c->max_batch < 1 || c->max_batch > 65536 || c->max_src_len < 1 || c->max_src_len > 256 ||
+      c->max_src_len > P || c->max_tgt_len < 1 || c->max_tgt_len > 256 || c->max_tgt_len > P || c->beam < 1 ||
+      c->beam > 8 || 2 * c->beam > m->info.vocab)
+    return set_error(MNMT_E_INVALID_ARG,
+                     "session config out of range: need max_batch >= 1, 1 <= max_src_len, max_tgt_len <= "
+                     "min(256, max_pos), 1 <= beam <= 8 and 2*beam <= vocab");
+  return MNMT_OK;
+}
+
+Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
+  Plan p{};
+  Bump b;
+  const size_t d = m->info.d_model, F = m->info.d_ffn, V = m->info.vocab, Ld = m->info.n_dec;
+  const size_t B = c.max_batch, S = c.max_src_len, T = c.max_tgt_len, W = c.beam, R = B * W, BS = B * S;
+  p.src = b.take(4 * BS);
+  p.len = b.take(4 * B);
+  // shared region: encoder scratch | decoder logits
+  Bump r;
+  p.enc_x = r.take(4 * BS * d);
+  p.enc_a = r.take(BS * d);
+  p.enc_qkv = r.take(BS * 3 * d);
+  p.enc_h = r.take(BS * F);
+  p.enc_out = r.take(BS * d);
+  const size_t enc_bytes = r.off;
+  const size_t logit_bytes = 4 * R * V;
+  p.region = b.take(enc_bytes > logit_bytes ? enc_bytes : logit_bytes);
+  p.enc_x += p.region;
+  p.enc_a += p.region;
+  p.enc_qkv += p.region;
+  p.enc_h += p.region;
+  p.enc_out += p.region;
+  p.logits = p.region;
+  for (size_t l = 0; l < Ld; ++l) p.cross_kv.push_back(b.take(BS * 2 * d));
+  p.dec_x = b.take(4 * R * d);
+  p.dec_a = b.take(R * d);
+  p.dec_qkv = b.take(R * 3 * d);
+  p.dec_q = b.take(R * d);
+  p.dec_h = b.take(R * F);
+  for (size_t l = 0; l < Ld; ++l) {
+    p.kc.push_back(b.take(R * T * d));
+    p.vc.push_back(b.take(R * T * d));
+  }
+  p.cur_tok = b.take(4 * R);
+  p.step = b.take(4);
+  p.slots = b.take(8 * R);
+  p.out_tok = b.take(4 * T * R);
+  p.finished = b.take(4 * R);
+  p.out_len = b.take(4 * R);
+  p.lp = b.take(4 * (T + 1));
+  p.score = b.take(4 * R);
+  p.cand_score = b.take(4 * R * 2 * W);
+  p.cand_tok = b.take(4 * R * 2 * W);
+  p.tok_hist = b.take(4 * T * R);
+  p.par_hist = b.take(4 * T * R);
+  p.hist = b.take(4 * 2 * R * T);
+  p.fin_score = b.take(4 * B * W);
+  p.fin_len = b.take(4 * B * W);
+  p.fin_row = b.take(4 * B * W);
+  p.fin_count = b.take(4 * B);
+  p.done = b.take(4 * B);
+  p.total = (b.off + 255) / 256 * 256;
+  return p;
+}
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+#define LAUNCH(x)                                                   \
+  do {                                                              \
+    hipError_t _e = (x);                                            \
+    if (_e != hipSuccess) return hip_error(_e, #x);                 \
+  } while (0)
+
+int qlin(const LinearDev& L, const int8_t* X, int M, int kind, void* out, float gamma, hipStream_t s,
+         unsigned long long* argmax = nullptr) {
+  EpiArgs e{kind, out, L.N, gamma, argmax};
+  LAUNCH(launch_qlinear(X, L.K, L.w, L.scale, L.bias, M, L.K, L.N, e, s));
+  return MNMT_OK;
+}
+
+// Encoder over the session's current batch (rows = B * S, padded rows are
+// computed and ignored), then every decoder layer's cross keys/values.
+int run_encoder(mnmt_session* S, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  const int d = m->info.d_model, rows = S->B * S->S;
+  const bool post = m->info.ln_post;
+  const float eps = m->info.ln_eps;
+  LAUNCH(launch_embed(S->src, rows, S->S, nullptr, m->E, m->c_emb, m->pe, d, m->info.vocab, S->enc_x, s));
+  const LayerDev& L0 = m->enc[0];
+  LAUNCH(launch_ln_quant(S->enc_x, rows, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->enc_a, nullptr, s));
+  for (size_t l = 0; l < m->enc.size(); ++l) {
+    const LayerDev& L = m->enc[l];
+    int rc;
+    if ((rc = qlin(L.qkv, S->enc_a, rows, MNMT_EPI_I8, S->enc_qkv, 1.f, s))) return rc;
+    LAUNCH(launch_attn_enc(S->enc_qkv, S->len, S->B, S->S, d, m->info.n_heads, L.sa_cqk, L.sa_cpv, S->enc_a, s));
+    if ((rc = qlin(L.o, S->enc_a, rows, MNMT_EPI_F32_RESID, S->enc_x, L.sa_gamma, s))) return rc;
+    // input of the FFN: pre-LN normalizes with the FFN's LayerNorm; post-LN
+    // normalizes the residual with the attention sublayer's LayerNorm.
+    const LnDev& ln1 = post ? L.sa_ln : L.ff_ln;
+    LAUNCH(launch_ln_quant(S->enc_x, rows, d, 1, ln1.g, ln1.b, eps, L.w1.inv_in, S->enc_a, post ? S->enc_x : nullptr, s));
+    if ((rc = qlin(L.w1, S->enc_a, rows, MNMT_EPI_I8_RELU, S->enc_h, 1.f, s))) return rc;
+    if ((rc = qlin(L.w2, S->enc_h, rows, MNMT_EPI_F32_RESID, S->enc_x, L.ff_gamma, s))) return rc;
+    const bool last = l + 1 == m->enc.size();
+    int8_t* dst = last ? S->enc_out : S->enc_a;
+    const float inv = last ? m->inv_enc : m->enc[l + 1].qkv.inv_in;
+    const LnDev& ln2 = post ? L.ff_ln : (last ? m->enc_ln : m->enc[l + 1].sa_ln);
+    LAUNCH(launch_ln_quant(S->enc_x, rows, d, 1, ln2.g, ln2.b, eps, inv, dst, post ? S->enc_x : nullptr, s));
+  }
+  for (size_t l = 0; l < m->dec.size(); ++l) {
+    int rc;
+    if ((rc = qlin(m->dec[l].ckv, S->enc_out, rows, MNMT_EPI_I8, S->cross_kv[l], 1.f, s))) return rc;
+  }
+  return MNMT_OK;
+}
+
+// One decoder step for R rows (W hypotheses per sentence); ends with the
+// final sublayer input in dec_a, ready for the output projection.
+int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
+  const bool post = m->info.ln_post;
+  const float eps = m->info.ln_eps;
+  LAUNCH(launch_embed(S->cur_tok, R, 1, S->step, m->E, m->c_emb, m->pe, d, m->info.vocab, S->dec_x, s));
+  const LayerDev& L0 = m->dec[0];
+  LAUNCH(launch_ln_quant(S->dec_x, R, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->dec_a, nullptr, s));
+  for (size_t l = 0; l < m->dec.size(); ++l) {
+    const LayerDev& L = m->dec[l];
+    int rc;
+    if ((rc = qlin(L.qkv, S->dec_a, R, MNMT_EPI_I8, S->dec_qkv, 1.f, s))) return rc;
+    LAUNCH(launch_attn_dec_self(S->dec_qkv, R, d, h, T, S->step, S->kcache[l], S->vcache[l],
+                                beam ? S->beam.hist : nullptr, L.sa_cqk, L.sa_cpv, S->dec_a, s));
+    if ((rc = qlin(L.o, S->dec_a, R, MNMT_EPI_F32_RESID, S->dec_x, L.sa_gamma, s))) return rc;
+    const LnDev& lnc = post ? L.sa_ln : L.ca_ln;
+    LAUNCH(launch_ln_quant(S->dec_x, R, d, 1, lnc.g, lnc.b, eps, L.cq.inv_in, S->dec_a, post ? S->dec_x : nullptr, s));
+    if ((rc = qlin(L.cq, S->dec_a, R, MNMT_EPI_I8, S->dec_q, 1.f, s))) return rc;
+    LAUNCH(launch_attn_dec_cross(S->dec_q, R, W, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, S->dec_a, s));
+    if ((rc = qlin(L.co, S->dec_a, R, MNMT_EPI_F32_RESID, S->dec_x, L.ca_gamma, s))) return rc;
+    const LnDev& lnf = post ? L.ca_ln : L.ff_ln;
+    LAUNCH(launch_ln_quant(S->dec_x, R, d, 1, lnf.g, lnf.b, eps, L.w1.inv_in, S->dec_a, post ? S->dec_x : nullptr, s));
+    if ((rc = qlin(L.w1, S->dec_a, R, MNMT_EPI_I8_RELU, S->dec_h, 1.f, s))) return rc;
+    if ((rc = qlin(L.w2, S->dec_h, R, MNMT_EPI_F32_RESID, S->dec_x, L.ff_gamma, s))) return rc;
+    const bool last = l + 1 == m->dec.size();
+    const float inv = last ? m->inv_fin : m->dec[l + 1].qkv.inv_in;
+    const LnDev& ln2 = post ? L.ff_ln : (last ? m->dec_ln : m->dec[l + 1].sa_ln);
+    LAUNCH(launch_ln_quant(S->dec_x, R, d, 1, ln2.g, ln2.b, eps, inv, S->dec_a, post ? S->dec_x : nullptr, s));
+  }
+  return MNMT_OK;
+}
+
+// Greedy step: layers, tied output projection with fused arg-max (batch <= 8)
+// or logits + row arg-max, then bookkeeping.  logits_out: optional [R, V].
+int greedy_step(mnmt_session* S, int R, int stop_at_eos, float* logits_out, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  int rc = run_decoder_layers(S, R, 1, false, s);
+  if (rc) return rc;
+  const int d = m->info.d_model, V = m->info.vocab;
+  if (R <= 8) {
+    EpiArgs e{EPI_LOGITS_ARGMAX, logits_out, V, 1.f, S->slots};
+    LAUNCH(launch_qlinear(S->dec_a, d, m->E, m->c_out, nullptr, R, d, V, e, s));
+  } else {
+    float* z = logits_out ? logits_out : S->logits;
+    EpiArgs e{MNMT_EPI_LOGITS, z, V, 1.f, nullptr};
+    LAUNCH(launch_qlinear(S->dec_a, d, m->E, m->c_out, nullptr, R, d, V, e, s));
+    LAUNCH(launch_row_argmax(z, R, V, S->slots, s));
+  }
+  LAUNCH(launch_greedy_commit(S->slots, R, S->cfg.max_tgt_len, S->cur_tok, S->out_tok, S->finished, S->out_len,
+                              S->step, stop_at_eos, m->info.eos_id, m->info.pad_id, s));
+  return MNMT_OK;
+}
+
+int beam_step(mnmt_session* S, int R, int W, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  int rc = run_decoder_layers(S, R, W, true, s);
+  if (rc) return rc;
+  const int d = m->info.d_model, V = m->info.vocab;
+  EpiArgs e{MNMT_EPI_LOGITS, S->logits, V, 1.f, nullptr};
+  LAUNCH(launch_qlinear(S->dec_a, d, m->E, m->c_out, nullptr, R, d, V, e, s));
+  LAUNCH(launch_beam_topk(S->logits, S->beam, S->step, s));
+  LAUNCH(launch_beam_update(S->beam, S->step, s));
+  return MNMT_OK;
+}
+
+// All device work of a translate call after the inputs are in the session.
+int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
+  int rc = run_encoder(S, s);
+  if (rc) return rc;
+  const mnmt_model* m = S->m;
+  if (sc.beam == 1) {
+    const int R = S->B;
+    LAUNCH(launch_greedy_reset(S->slots, R, sc.max_steps, S->cur_tok, S->finished, S->out_len, S->step,
+                               m->info.bos_id, s));
+    for (int t = 0; t < sc.max_steps; ++t)
+      if ((rc = greedy_step(S, R, sc.stop_at_eos, nullptr, s))) return rc;
+  } else {
+    const int R = S->B * sc.beam;
+    LAUNCH(launch_beam_reset(S->beam, S->step, s));
+    for (int t = 0; t < sc.max_steps; ++t)
+      if ((rc = beam_step(S, R, sc.beam, s))) return rc;
+  }
+  return MNMT_OK;
+}
+
+int check_ptr(const void* p, const char* what) {
+  if (!p) return set_error(MNMT_E_INVALID_ARG, std::string(what) + " is null");
+  if (reinterpret_cast<uintptr_t>(p) % 16) return set_error(MNMT_E_INVALID_ARG, std::string(what) + " is not 16-byte aligned");
+  return MNMT_OK;
+}
+
+int load_batch(mnmt_session* S, const int32_t* d_src, const int32_t* d_len, int B, int S_max, hipStream_t s) {
+  if (!S || !S->m) return set_error(MNMT_E_INVALID_ARG, "null session");
+  int rc;
+  if ((rc = check_ptr(d_src, "d_src")) || (rc = check_ptr(d_len, "d_len"))) return rc;
+  if (B < 1 || S_max < 1) return set_error(MNMT_E_INVALID_ARG, "batch and source length must be positive");
+  if (B > S->cfg.max_batch || S_max > S->cfg.max_src_len)
+    return set_error(MNMT_E_CAPACITY, "batch or source length exceeds the session capacity");
+  S->B = B;
+  S->S = S_max;
+  MNMT_HIP(hipMemcpyAsync(S->src, d_src, sizeof(int32_t) * (size_t)B * S_max, hipMemcpyDeviceToDevice, s));
+  MNMT_HIP(hipMemcpyAsync(S->len, d_len, sizeof(int32_t) * (size_t)B, hipMemcpyDeviceToDevice, s));
+  return MNMT_OK;
+}
+
+}  // namespace
+}  // namespace mnmt
+
+using namespace mnmt;
+
+extern "C" int mnmt_session_bytes(const mnmt_model* model, const mnmt_session_cfg* cfg, size_t* bytes) {
+  int rc = validate_cfg(model, cfg);
+  if (rc) return rc;
+  if (!bytes) return set_error(MNMT_E_INVALID_ARG, "bytes is null");
+  *bytes = make_plan(model, *cfg).total;
+  return MNMT_OK;
+}
+
+extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_cfg* cfg, void* d_ws, size_t ws_bytes,
+                                   mnmt_session** out) {
+  int rc = validate_cfg(model, cfg);
+  if (rc) return rc;
+  if (!out) return set_error(MNMT_E_INVALID_ARG, "out is null");
+  if (!d_ws || reinterpret_cast<uintptr_t>(d_ws) % 256)
+    return set_error(MNMT_E_INVALID_ARG, "workspace must be non-null and 256-byte aligned");
+  const Plan p = make_plan(model, *cfg);
+  if (ws_bytes < p.total) return set_error(MNMT_E_INVALID_ARG, "workspace smaller than mnmt_session_bytes");
+  auto* S = new mnmt_session();
+  S->m = model;
+  S->cfg = *cfg;
+  S->R = cfg->max_batch * cfg->beam;
+  uint8_t* base = static_cast<uint8_t*>(d_ws);
+  auto at = [&](size_t off) { return static_cast<void*>(base + off); };
+  const size_t d = model->info.d_model, BS = (size_t)cfg->max_batch * cfg->max_src_len, R = S->R,
+               T = cfg->max_tgt_len, V = model->info.vocab;
+  S->src = (int32_t*)at(p.src);
+  S->len = (int32_t*)at(p.len);
+  S->enc_x = (float*)at(p.enc_x);
+  S->enc_a = (int8_t*)at(p.enc_a);
+  S->enc_qkv = (int8_t*)at(p.enc_qkv);
+  S->enc_h = (int8_t*)at(p.enc_h);
+  S->enc_out = (int8_t*)at(p.enc_out);
+  S->logits = (float*)at(p.logits);
+  for (size_t l = 0; l < p.cross_kv.size(); ++l) S->cross_kv.push_back((int8_t*)at(p.cross_kv[l]));
+  S->dec_x = (float*)at(p.dec_x);
+  S->dec_a = (int8_t*)at(p.dec_a);
+  S->dec_qkv = (int8_t*)at(p.dec_qkv);
+  S->dec_q = (int8_t*)at(p.dec_q);
+  S->dec_h = (int8_t*)at(p.dec_h);
+  for (size_t l = 0; l < p.kc.size(); ++l) {
+    S->kcache.push_back((int8_t*)at(p.kc[l]));
+    S->vcache.push_back((int8_t*)at(p.vc[l]));
+  }
+  S->cur_tok = (int32_t*)at(p.cur_tok);
+  S->step = (int*)at(p.step);
+  S->slots = (unsigned long long*)at(p.slots);
+  S->out_tok = (int32_t*)at(p.out_tok);
+  S->finished = (int32_t*)at(p.finished);
+  S->out_len = (int32_t*)at(p.out_len);
+  S->lp = (float*)at(p.lp);
+  BeamState& st = S->beam;
+  st.B = cfg->max_batch;
+  st.W = cfg->beam;
+  st.V = model->info.vocab;
+  st.T = cfg->max_tgt_len;
+  st.score = (float*)at(p.score);
+  st.cand_score = (float*)at(p.cand_score);
+  st.cand_tok = (int32_t*)at(p.cand_tok);
+  st.tok_hist = (int32_t*)at(p.tok_hist);
+  st.par_hist = (int32_t*)at(p.par_hist);
+  st.hist = (int32_t*)at(p.hist);
+  st.fin_score = (float*)at(p.fin_score);
+  st.fin_len = (int32_t*)at(p.fin_len);
+  st.fin_row = (int32_t*)at(p.fin_row);
+  st.fin_count = (int32_t*)at(p.fin_count);
+  st.done = (int32_t*)at(p.done);
+  st.cur_tok = S->cur_tok;
+  st.lp = S->lp;
+  st.eos = model->info.eos_id;
+  st.pad = model->info.pad_id;
+  st.bos = model->info.bos_id;
+  S->named["enc_out"] = {S->enc_out, BS * d};
+  S->named["dec_x"] = {S->dec_x, 4 * R * d};
+  S->named["logits"] = {S->logits, 4 * R * V};
+  S->named["step"] = {S->step, 4};
+  S->named["cur_tok"] = {S->cur_tok, 4 * R};
+  for (size_t l = 0; l < p.cross_kv.size(); ++l) {
+    S->named["cross_kv." + std::to_string(l)] = {S->cross_kv[l], BS * 2 * d};
+    S->named["kcache." + std::to_string(l)] = {S->kcache[l], R * T * d};
+    S->named["vcache." + std::to_string(l)] = {S->vcache[l], R * T * d};
+  }
+  if (hipStreamCreateWithFlags(&S->capture_stream, hipStreamNonBlocking) != hipSuccess) {
+    delete S;
+    return set_error(MNMT_E_HIP, "could not create the capture stream");
+  }
+  *out = S;
+  return MNMT_OK;
+}
+
+extern "C" void mnmt_session_free(mnmt_session* S) {
+  if (!S) return;
+  for (auto& g : S->graphs) (void)hipGraphExecDestroy(g.second);
+  if (S->capture_stream) (void)hipStreamDestroy(S->capture_stream);
+  delete S;
+}
+
+extern "C" int mnmt_session_tensor(const mnmt_session* S, const char* name, void** d_ptr, size_t* bytes) {
+  if (!S || !name || !d_ptr) return set_error(MNMT_E_INVALID_ARG, "null argument");
+  auto it = S->named.find(name);
+  if (it == S->named.end()) return set_error(MNMT_E_INVALID_ARG, std::string("no session tensor ") + name);
+  *d_ptr = it->second.first;
+  if (bytes) *bytes = it->second.second;
+  return MNMT_OK;
+}
+
+extern "C" int mnmt_encode(mnmt_session* S, const int32_t* d_src, const int32_t* d_len, int B, int S_max,
+                           void* stream) {
+  hipStream_t s = as_stream(stream);
+  int rc = load_batch(S, d_src, d_len, B, S_max, s);
+  if (rc) return rc;
+  S->W = 1;
+  if ((rc = run_encoder(S, s))) return rc;
+  const mnmt_model* m = S->m;
+  LAUNCH(launch_greedy_reset(S->slots, B, S->cfg.max_tgt_len, S->cur_tok, S->finished, S->out_len, S->step,
+                             m->info.bos_id, s));
+  S->encoded = true;
+  S->host_step = 0;
+  return MNMT_OK;
+}
+
+extern "C" int mnmt_decode_step(mnmt_session* S, const int32_t* d_prev, int32_t* d_next, float* d_logits,
+                                void* stream) {
+  if (!S || !S->encoded) return set_error(MNMT_E_INVALID_ARG, "decode_step needs a session after mnmt_encode");
+  if (S->host_step >= S->cfg.max_tgt_len) return set_error(MNMT_E_CAPACITY, "decode step beyond max_tgt_len");
+  int rc;
+  if (d_prev && (rc = check_ptr(d_prev, "d_prev"))) return rc;
+  if ((rc = check_ptr(d_next, "d_next"))) return rc;
+  if (d_logits && (rc = check_ptr(d_logits, "d_logits"))) return rc;
+  hipStream_t s = as_stream(stream);
+  const int R = S->B;
+  if (d_prev) LAUNCH(launch_copy_i32(d_prev, S->cur_tok, R, s));
+  if ((rc = greedy_step(S, R, 0, d_logits, s))) return rc;
+  LAUNCH(launch_copy_i32(S->cur_tok, d_next, R, s));
+  ++S->host_step;
+  return MNMT_OK;
+}
+
+extern "C" int mnmt_translate(mnmt_session* S, const int32_t* d_src, const int32_t* d_len, int B, int S_max,
+                              const mnmt_search_cfg* sc, int32_t* d_out, int32_t* d_out_len, float* d_score,
+                              void* stream) {
+  if (!S || !sc) return set_error(MNMT_E_INVALID_ARG, "null session or search config");
+  int rc;
+  if ((rc = check_ptr(d_out, "d_out")) || (rc = check_ptr(d_out_len, "d_out_len"))) return rc;
+  if (d_score && (rc = check_ptr(d_score, "d_score"))) return rc;
+  if (sc->beam < 1 || sc->beam > S->cfg.beam || sc->max_steps < 1 || sc->max_steps > S->cfg.max_tgt_len)
+    return set_error(MNMT_E_CAPACITY, "beam or max_steps exceeds the session capacity");
+  if (sc->beam > 1 && sc->beam != S->cfg.beam)
+    return set_error(MNMT_E_UNSUPPORTED, "beam search runs at the session's beam width");
+  if (sc->beam > 1 && !std::isfinite(sc->len_penalty_alpha))
+    return set_error(MNMT_E_INVALID_ARG, "length penalty exponent must be finite");
+  hipStream_t s = as_stream(stream);
+  if ((rc = load_batch(S, d_src, d_len, B, S_max, s))) return rc;
+  S->W = sc->beam;
+  S->encoded = false;  // decode_step state is not kept across a translate
+  if (sc->beam > 1) {
+    S->beam.B = B;  // sentences of this call
+    // length penalties ((5 + L) / 6)^alpha for L = 0..max_tgt_len, in double
+    std::vector<float> lp(S->cfg.max_tgt_len + 1);
+    for (size_t L = 0; L < lp.size(); ++L)
+      lp[L] = (float)std::pow((5.0 + (double)L) / 6.0, (double)sc->len_penalty_alpha);
+    MNMT_HIP(hipMemcpyAsync(S->lp, lp.data(), sizeof(float) * lp.size(), hipMemcpyHostToDevice, s));
+    MNMT_HIP(hipStreamSynchronize(s));  // the host vector is released on return
+  }
+  if (sc->use_graph) {
+    const std::string key = std::to_string(B) + "," + std::to_string(S_max) + "," + std::to_string(sc->beam) + "," +
+                            std::to_string(sc->max_steps) + "," + std::to_string(sc->stop_at_eos);
+    auto it = S->graphs.find(key);
+    if (it == S->graphs.end()) {
+      MNMT_HIP(hipStreamBeginCapture(S->capture_stream, hipStreamCaptureModeRelaxed));
+      rc = enqueue_search(S, *sc, S->capture_stream);
+      hipGraph_t graph = nullptr;
+      const hipError_t ec = hipStreamEndCapture(S->capture_stream, &graph);
+      if (rc != MNMT_OK) {
+        if (graph) (void)hipGraphDestroy(graph);
+        return rc;
+      }
+      if (ec != hipSuccess) return hip_error(ec, "hipStreamEndCapture");
+      hipGraphExec_t exec = nullptr;
+      const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      if (ei != hipSuccess) return hip_error(ei, "hipGraphInstantiate");
+      it = S->graphs.emplace(key, exec).first;
+    }
+    MNMT_HIP(hipGraphLaunch(it->second, s));
+  } else {
+    if ((rc = enqueue_search(S, *sc, s))) return rc;
+  }
+  if (sc->beam == 1) {
+    LAUNCH(launch_greedy_output(S->out_tok, S->out_len, B, sc->max_steps, d_out, d_out_len, s));
+  } else {
+    LAUNCH(launch_beam_finalize(S->beam, sc->max_steps, d_out, d_out_len, d_score, s));
+  }
+  return MNMT_OK;
+}

@@ -1,0 +1,77 @@
+"""Host-side checks of the C ABI library that need no GPU: it loads, exports
+every entry point declared in include/mnmt.h, and its host-only functions
+(model validation, constant folding, status strings) behave."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2306_04235_amd import mnmt
+from synth import generate as G
+from synth.modelfile import read_model, write_model
+
+from .conftest import ROOT, model_blob
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "mnmt.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(mnmt_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = mnmt.lib()
+    declared = _declared()
+    assert set(declared) == set(mnmt.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    L = mnmt.lib()
+    assert L.mnmt_status_str(0) == b"ok"
+    assert L.mnmt_status_str(mnmt.E_BAD_MODEL) == b"bad model file"
+    assert L.mnmt_status_str(12345) == b"unknown status"
+
+
+def test_model_bytes_accepts_the_generated_models():
+    for name in ("TINY", "MOBILE"):
+        blob = model_blob(name)
+        n = mnmt.mnmt_model_bytes(blob)
+        _, t = read_model(blob)
+        weights = sum(a.size for k, a in t.items() if k.endswith(".w"))
+        assert weights < n < 2 * len(blob)
+
+
+def test_model_bytes_rejects_bad_files():
+    blob = model_blob("TINY")
+    with pytest.raises(mnmt.MnmtError) as e:
+        mnmt.mnmt_model_bytes(b"XXXX" + blob[4:])
+    assert e.value.status == mnmt.E_BAD_MODEL
+    with pytest.raises(mnmt.MnmtError) as e:
+        mnmt.mnmt_model_bytes(blob[:1000])
+    assert e.value.status == mnmt.E_BAD_MODEL
+    hdr, t = read_model(blob)
+    t = dict(t)
+    t["dec.0.ff.w2.b"] = np.full(t["dec.0.ff.w2.b"].shape, np.nan, np.float32)
+    with pytest.raises(mnmt.MnmtError) as e:
+        mnmt.mnmt_model_bytes(write_model(hdr, t))
+    assert e.value.status == mnmt.E_BAD_MODEL
+    hdr.d_model = 48  # not a multiple of 64: shapes the kernels do not support
+    with pytest.raises(mnmt.MnmtError) as e:
+        mnmt.mnmt_model_bytes(write_model(hdr, dict(read_model(blob)[1])))
+    assert e.value.status in (mnmt.E_UNSUPPORTED, mnmt.E_BAD_MODEL)
+
+
+def test_fold_requant_matches_oracle_bitwise():
+    rng = np.random.default_rng(4)
+    for _ in range(5):
+        s_w = rng.uniform(1e-5, 1e-2, 1000).astype(np.float32)
+        b = rng.normal(0, 0.05, 1000).astype(np.float32)
+        s_in, s_out = np.float32(rng.uniform(0.01, 0.05)), np.float32(rng.uniform(0.01, 0.2))
+        a = mnmt.mnmt_fold_requant(s_in, s_w, b, s_out)
+        r = oracle.fold_requant(s_in, s_w, b, s_out)
+        assert np.array_equal(a[0].view(np.uint32), r[0].view(np.uint32))
+        assert np.array_equal(a[1].view(np.uint32), r[1].view(np.uint32))

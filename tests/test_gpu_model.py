@@ -1,0 +1,198 @@
+"""End-to-end GPU parity against the oracle: encoder output codes and cross
+keys/values bit-exact, decode-step logits (bar: 1e-3 relative; bit-exact
+expected), greedy token sequences identical on the tiny and mobile workloads,
+hipGraph replay identical to eager launches, beam search identical on small
+models and on sampled sentences of the batched beam workloads."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import generate as G
+
+from .conftest import model_blob
+
+pytestmark = pytest.mark.gpu
+RTOL = 1e-3
+
+SMALL_PRE = G.ModelConfig("small-preln", 64, 4, 128, 2, 2, 500, ln_post=0, seed=77, random_gamma=True)
+SMALL_POST = G.ModelConfig("small-postln", 64, 2, 128, 2, 2, 300, ln_post=1, seed=78, random_gamma=True,
+                           weight_std=0.1)
+DIVERSE = G.ModelConfig("diverse-preln", 128, 2, 256, 3, 2, 700, ln_post=0, seed=81, random_gamma=True,
+                        weight_std=0.1)
+
+
+@pytest.fixture(scope="module")
+def torch_dev():
+    import torch
+
+    assert torch.cuda.is_available(), "GPU tests need a visible GPU"
+    return torch, torch.device("cuda:0")
+
+
+_models = {}
+
+
+def _pair(name_or_cfg):
+    """(oracle model, GPU model) for a named workload model or a ModelConfig."""
+    from paper_2306_04235_amd import mnmt
+
+    key = name_or_cfg if isinstance(name_or_cfg, str) else name_or_cfg.name
+    if key not in _models:
+        blob = model_blob(name_or_cfg) if isinstance(name_or_cfg, str) else G.build_model(name_or_cfg)
+        _models[key] = (oracle.Model(blob), mnmt.Model(blob))
+    return _models[key]
+
+
+def _t(torch, dev, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def _greedy_check(torch, dev, cfg, src, lens, steps, stop_at_eos=False, check_logits=True):
+    from paper_2306_04235_amd import mnmt
+
+    om, gm = _pair(cfg)
+    B, S = src.shape
+    print(f"greedy {cfg if isinstance(cfg, str) else cfg.name} B={B} S={S} steps={steps}", flush=True)
+    sess = mnmt.Session(gm, B, S, steps, 1)
+    ts, tl = _t(torch, dev, src), _t(torch, dev, lens)
+    o_out, o_len, o_logits = om.greedy(src, lens, steps, stop_at_eos=stop_at_eos, want_logits=True)
+    # encoder output and cross keys/values, bit-exact on valid rows
+    sess.encode(ts, tl)
+    torch.cuda.synchronize()
+    enc = sess.tensor("enc_out", torch.int8, (B, S, gm.info.d_model)).cpu().numpy()
+    o_enc = om.encode(src, lens)
+    for b in range(B):
+        assert np.array_equal(enc[b, : lens[b]], o_enc[b, : lens[b]]), f"encoder output, sentence {b}"
+    for l in range(gm.info.n_dec):
+        kv = sess.tensor(f"cross_kv.{l}", torch.int8, (B, S, 2 * gm.info.d_model)).cpu().numpy()
+        o_kv = om.cross_kv(o_enc, lens, l)
+        for b in range(B):
+            assert np.array_equal(kv[b, : lens[b]], o_kv[b, : lens[b]]), f"cross kv layer {l} sentence {b}"
+    # teacher-forced decode steps through the C ABI: logits and tokens
+    if check_logits and not stop_at_eos:
+        prev = None
+        for t in range(steps):
+            nxt, logits = sess.decode_step(prev, want_logits=True)
+            z = logits.cpu().numpy()
+            ref = o_logits[:, t]
+            assert np.allclose(z, ref, rtol=RTOL, atol=RTOL * np.abs(ref).max()), f"logits step {t}"
+            assert np.array_equal(z.view(np.uint32), ref.view(np.uint32)), f"logits bits step {t}"
+            assert np.array_equal(nxt.cpu().numpy(), o_out[:, t]), f"tokens step {t}"
+            prev = _t(torch, dev, o_out[:, t])
+    # whole translation, eager and captured in a graph (replayed twice)
+    for use_graph in (False, True, True):
+        out, out_len, _ = sess.translate(ts, tl, beam=1, max_steps=steps, stop_at_eos=stop_at_eos,
+                                         use_graph=use_graph)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), o_out), f"greedy tokens (graph={use_graph})"
+        assert np.array_equal(out_len.cpu().numpy(), o_len)
+    sess.close()
+    return o_out
+
+
+def test_tiny_postln_greedy(torch_dev):
+    torch, dev = torch_dev
+    src, lens = G.workload_inputs(G.WORKLOADS["tiny"])
+    _greedy_check(torch, dev, "TINY", src, lens, 16)
+
+
+def test_small_models_batched_greedy(torch_dev):
+    torch, dev = torch_dev
+    for cfg in (SMALL_PRE, SMALL_POST, DIVERSE):
+        src, lens = G.make_sources(cfg.vocab, 5, [1, 7, 12, 3, 12], seed=21, s_max=12)
+        _greedy_check(torch, dev, cfg, src, lens, 10)
+        _greedy_check(torch, dev, cfg, src, lens, 10, stop_at_eos=True, check_logits=False)
+
+
+def test_greedy_batch_above_gemv_limit(torch_dev):
+    # 12 rows: the output projection runs on matrix cores, arg-max separately
+    torch, dev = torch_dev
+    src, lens = G.make_sources(DIVERSE.vocab, 12, (2, 20), seed=22, s_max=20)
+    _greedy_check(torch, dev, DIVERSE, src, lens, 9)
+
+
+def test_diverse_model_output_depends_on_the_source(torch_dev):
+    # the higher-variance test model's translations differ between sources
+    torch, dev = torch_dev
+    src, lens = G.make_sources(DIVERSE.vocab, 3, (8, 14), seed=23, s_max=14)
+    out = _greedy_check(torch, dev, DIVERSE, src, lens, 12, check_logits=False)
+    assert len({tuple(r) for r in out}) > 1
+
+
+def test_mobile_greedy_latency_workload(torch_dev):
+    torch, dev = torch_dev
+    src, lens = G.workload_inputs(G.WORKLOADS["mobile"])
+    _greedy_check(torch, dev, "MOBILE", src, lens, 30)
+
+
+def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None):
+    from paper_2306_04235_amd import mnmt
+
+    om, gm = _pair(cfg)
+    B, S = src.shape
+    print(f"beam {cfg if isinstance(cfg, str) else cfg.name} B={B} S={S} W={W} T={steps}", flush=True)
+    sess = mnmt.Session(gm, B, S, steps, W)
+    ts, tl = _t(torch, dev, src), _t(torch, dev, lens)
+    results = []
+    for use_graph in (False, True):
+        out, out_len, score = sess.translate(ts, tl, beam=W, max_steps=steps, alpha=alpha, use_graph=use_graph)
+        torch.cuda.synchronize()
+        results.append((out.cpu().numpy(), out_len.cpu().numpy(), score.cpu().numpy()))
+    assert all(np.array_equal(results[0][i], results[1][i]) for i in range(3)), "graph replay differs from eager"
+    out, out_len, score = results[0]
+    idx = np.arange(B) if sample is None else np.asarray(sample)
+    o_out, o_len, o_score = om.beam(src[idx], lens[idx], W, steps, alpha)
+    assert np.array_equal(out_len[idx], o_len)
+    assert np.array_equal(out[idx], o_out)
+    assert np.array_equal(score[idx].view(np.uint32), o_score.view(np.uint32))
+    sess.close()
+
+
+def test_small_models_beam(torch_dev):
+    torch, dev = torch_dev
+    for cfg in (SMALL_PRE, SMALL_POST, DIVERSE):
+        src, lens = G.make_sources(cfg.vocab, 4, [5, 1, 9, 9], seed=31, s_max=9)
+        for W in (2, 4):
+            _beam_check(torch, dev, cfg, src, lens, W, 8, 0.6)
+
+
+def test_mobile_beam_workload_sampled(torch_dev):
+    torch, dev = torch_dev
+    w = G.WORKLOADS["mobile_beam"]
+    src, lens = G.workload_inputs(w)
+    _beam_check(torch, dev, "MOBILE", src, lens, w.beam, w.steps, w.alpha, sample=[0, 17, 40, 63])
+
+
+def test_base_beam_workload_sampled(torch_dev):
+    torch, dev = torch_dev
+    w = G.WORKLOADS["base_beam"]
+    src, lens = G.workload_inputs(w)
+    _beam_check(torch, dev, "BASE", src, lens, w.beam, w.steps, w.alpha, sample=[0, 127])
+
+
+def test_session_capacity_errors(torch_dev):
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    _, gm = _pair("TINY")
+    sess = mnmt.Session(gm, 2, 8, 4, 1)
+    src = torch.full((3, 8), 5, dtype=torch.int32, device=dev)
+    lens = torch.full((3,), 8, dtype=torch.int32, device=dev)
+    with pytest.raises(mnmt.MnmtError) as e:
+        sess.translate(src, lens, max_steps=4)
+    assert e.value.status == mnmt.E_CAPACITY
+    with pytest.raises(mnmt.MnmtError) as e:
+        sess.translate(src[:2], lens[:2], max_steps=5)
+    assert e.value.status == mnmt.E_CAPACITY
+    with pytest.raises(mnmt.MnmtError) as e:
+        mnmt.Session(gm, 1, 8, 4, 9)  # beam above the supported width
+    assert e.value.status == mnmt.E_INVALID_ARG
+    sess.encode(src[:1], lens[:1])
+    for _ in range(4):
+        sess.decode_step()
+    with pytest.raises(mnmt.MnmtError) as e:
+        sess.decode_step()
+    assert e.value.status == mnmt.E_CAPACITY
+    sess.close()

@@ -16,7 +16,7 @@ from .conftest import model_blob
 
 # A pre-LN model small enough for exhaustive checks, with gamma != 1.
 SMALL_PRE = G.ModelConfig("small-preln", 64, 4, 128, 2, 2, 500, ln_post=0, seed=77, random_gamma=True)
-SMALL_POST = G.ModelConfig("small-postln", 64, 2, 96, 2, 2, 300, ln_post=1, seed=78, random_gamma=True,
+SMALL_POST = G.ModelConfig("small-postln", 64, 2, 128, 2, 2, 300, ln_post=1, seed=78, random_gamma=True,
                            weight_std=0.1)
 MICRO = G.ModelConfig("micro-v6", 16, 2, 32, 1, 1, 6, ln_post=0, seed=79, weight_std=0.3, emb_std=0.3)
 
