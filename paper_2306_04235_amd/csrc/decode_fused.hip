@@ -1,0 +1,248 @@
+// decode_fused.hip -- decoder-step kernels for up to 8 rows (the batch-1
+// latency path) with the element-wise work fused into the GEMVs (Section 4.2:
+// everything between two GEMMs is one fused operation):
+//   k_qgemv_ln : [embedding of the step's tokens |] LayerNorm | quantization
+//                of the input rows, then a slice of a linear layer with a
+//                requantizing (optionally ReLU) epilogue, or the tied output
+//                projection with the arg-max fused.  Each block issues its
+//                weight loads first and normalizes the (at most 8) input rows
+//                while those loads are in flight; the rows are recomputed per
+//                block, which costs less than a kernel boundary.
+//   k_greedy_commit_slots : reduces the arg-max slots, records the tokens,
+//                applies the end-of-sentence rule and advances the step.
+// The arg-max of a row is spread over kSlots slots (block b updates slot
+// b % kSlots) so that blocks do not serialize on one address; the commit
+// kernel (the next launch) sees every update and clears the slots.
+#include "blocks.hpp"
+#include "internal.h"
+
+namespace mnmt {
+namespace {
+
+constexpr int kRows = 8;    // rows per fused step (greedy batch <= 8)
+constexpr int kSlots = 32;  // arg-max slots per row
+
+// Input rows -> int8 rows in LDS; wave w prepares rows w, w + 4.
+__device__ __forceinline__ void prepare_rows(const FusedIn& in, int R, int d, int t, int8_t* a_lds) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const bool writer = blockIdx.x == 0 && in.x_out != nullptr;
+  const int n = (d + 63) / 64;
+  for (int r = wave; r < R; r += 4) {
+    float v[kMaxRowLen / 64];
+    if (in.embed) {
+      int tok = in.tok[r];
+      tok = tok < 0 ? 0 : (tok >= in.V ? in.V - 1 : tok);
+      const float c = in.c_emb[tok];
+#pragma unroll
+      for (int j = 0; j < kMaxRowLen / 64; ++j) {
+        const int i = lane + 64 * j;
+        v[j] = (j < n && i < d) ? fmaf((float)in.E[(size_t)tok * d + i], c, in.pe[(size_t)t * d + i]) : 0.0f;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kMaxRowLen / 64; ++j) {
+        const int i = lane + 64 * j;
+        v[j] = (j < n && i < d) ? in.x[(size_t)r * d + i] : 0.0f;
+      }
+    }
+    if (writer && in.wb_input) {
+#pragma unroll
+      for (int j = 0; j < kMaxRowLen / 64; ++j) {
+        const int i = lane + 64 * j;
+        if (j < n && i < d) in.x_out[(size_t)r * d + i] = v[j];
+      }
+    }
+    if (in.do_ln) {
+      float p = 0.0f;
+#pragma unroll
+      for (int j = 0; j < kMaxRowLen / 64; ++j)
+        if (j < n && lane + 64 * j < d) p = p + v[j];
+      const float inv_d = 1.0f / (float)d;
+      const float mu = wave_sum(p) * inv_d;
+      float p2 = 0.0f;
+#pragma unroll
+      for (int j = 0; j < kMaxRowLen / 64; ++j) {
+        if (j < n && lane + 64 * j < d) {
+          v[j] = v[j] - mu;
+          p2 = fmaf(v[j], v[j], p2);
+        }
+      }
+      const float var = wave_sum(p2) * inv_d;
+      const float rstd = 1.0f / sqrtf(var + in.eps);
+#pragma unroll
+      for (int j = 0; j < kMaxRowLen / 64; ++j) {
+        const int i = lane + 64 * j;
+        if (j < n && i < d) v[j] = fmaf(v[j] * rstd, in.g[i], in.b[i]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kMaxRowLen / 64; ++j) {
+      const int i = lane + 64 * j;
+      if (j < n && i < d) {
+        a_lds[r * d + i] = code_of(v[j] * in.inv_s);
+        if (writer && !in.wb_input) in.x_out[(size_t)r * d + i] = v[j];
+      }
+    }
+  }
+}
+
+// MR rows of input, LPR lanes per weight row, U row groups per wave, and at
+// most two 16-byte K chunks per lane (K <= 32 * LPR, i.e. d <= 1024).
+template <int MR, int LPR, int U>
+__global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
+  constexpr int RPI = 64 / LPR;
+  __shared__ __attribute__((aligned(16))) int8_t a_lds[MR * kMaxRowLen];
+  __shared__ unsigned long long wmax[4][MR];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane / LPR, kl = lane % LPR;
+  const int R = gv.R, K = gv.K, N = gv.N;
+  const int row0 = (blockIdx.x * 4 + wave) * RPI * U;
+  // 1. weight loads first
+  int4 wv[2][U];
+#pragma unroll
+  for (int ki = 0; ki < 2; ++ki) {
+    const int k = kl * 16 + ki * LPR * 16;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int n = row0 + u * RPI + sub;
+      wv[ki][u] = (k < K && n < N) ? *(const int4*)(gv.W + (size_t)n * K + k) : make_int4(0, 0, 0, 0);
+    }
+  }
+  // 2. input rows while the loads are in flight
+  prepare_rows(in, R, K, gv.t, a_lds);
+  __syncthreads();
+  // 3. dot products
+  int acc[U][MR];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int m = 0; m < MR; ++m) acc[u][m] = 0;
+#pragma unroll
+  for (int ki = 0; ki < 2; ++ki) {
+    const int k = kl * 16 + ki * LPR * 16;
+    if (k < K) {
+#pragma unroll
+      for (int m = 0; m < MR; ++m) {
+        if (m < R) {
+          const int4 xv = *(const int4*)(a_lds + m * K + k);
+#pragma unroll
+          for (int u = 0; u < U; ++u) acc[u][m] = dot16(wv[ki][u], xv, acc[u][m]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int off = LPR / 2; off >= 1; off >>= 1)
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < MR; ++m) acc[u][m] += __shfl_xor(acc[u][m], off, 64);
+  if (gv.epi != EPI_LOGITS_ARGMAX) {
+    if (kl != 0) return;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int n = row0 + u * RPI + sub;
+      if (n >= N) continue;
+#pragma unroll
+      for (int m = 0; m < MR; ++m) {
+        if (m < R) {
+          float y = fmaf((float)acc[u][m], gv.scale[n], gv.bias[n]);
+          if (gv.epi == MNMT_EPI_I8_RELU) y = fmaxf(y, 0.0f);
+          ((int8_t*)gv.out)[(size_t)m * N + n] = code_of(y);
+        }
+      }
+    }
+    return;
+  }
+  // logits z = acc * scale[n] and the row's arg-max
+#pragma unroll
+  for (int m = 0; m < MR; ++m) {
+    unsigned long long best = 0ull;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int n = row0 + u * RPI + sub;
+      if (kl == 0 && n < N && m < R) {
+        const float z = (float)acc[u][m] * gv.scale[n];
+        if (gv.out) ((float*)gv.out)[(size_t)m * N + n] = z;
+        const unsigned long long key = pack_argmax(z, n);
+        best = key > best ? key : best;
+      }
+    }
+    best = wave_max_u64(best);
+    if (lane == 0) wmax[wave][m] = best;
+  }
+  __syncthreads();
+  if (threadIdx.x < R) {
+    const int m = threadIdx.x;
+    unsigned long long b = wmax[0][m];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) b = wmax[w][m] > b ? wmax[w][m] : b;
+    if (b != 0ull) atomicMax(gv.slots + m * kSlots + blockIdx.x % kSlots, b);
+  }
+}
+
+__global__ void k_greedy_commit_slots(FusedGemv gv) {
+  const int t = gv.t;
+  for (int m = threadIdx.x; m < gv.R; m += blockDim.x) {
+    unsigned long long b = 0ull;
+    for (int i = 0; i < kSlots; ++i) {
+      const unsigned long long s = gv.slots[m * kSlots + i];
+      b = s > b ? s : b;
+      gv.slots[m * kSlots + i] = 0ull;
+    }
+    const int tok = unpack_index(b);
+    const int fin = gv.finished[m];
+    if (t < gv.T) gv.out_tok[(size_t)t * gv.R + m] = fin ? gv.pad : tok;
+    if (!fin && gv.stop_at_eos && tok == gv.eos) {
+      gv.finished[m] = 1;
+      gv.out_len[m] = t + 1;
+    }
+    gv.cur_tok[m] = fin ? gv.pad : tok;
+  }
+  if (threadIdx.x == 0) *gv.step = t + 1;
+}
+
+template <int MR, int LPR>
+hipError_t launch_u(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
+  constexpr int RPI = 64 / LPR;
+  const long waves4 = ((long)gv.N + RPI * 4 - 1) / (RPI * 4);
+  if (waves4 >= 1024) {
+    hipLaunchKernelGGL((k_qgemv_ln<MR, LPR, 4>), dim3((int)((waves4 + 3) / 4)), dim3(256), 0, s, in, gv);
+  } else {
+    const long waves = ((long)gv.N + RPI - 1) / RPI;
+    hipLaunchKernelGGL((k_qgemv_ln<MR, LPR, 1>), dim3((int)((waves + 3) / 4)), dim3(256), 0, s, in, gv);
+  }
+  return hipGetLastError();
+}
+
+template <int MR>
+hipError_t launch_lpr(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
+  // lanes per weight row: as many 16-byte chunks as the row has, up to 64
+  // (K <= 1024 then leaves each lane at most two chunks)
+  const int chunks = gv.K / 16;
+  if (chunks >= 64) return launch_u<MR, 64>(in, gv, s);
+  if (chunks >= 32) return launch_u<MR, 32>(in, gv, s);
+  if (chunks >= 16) return launch_u<MR, 16>(in, gv, s);
+  if (chunks >= 8) return launch_u<MR, 8>(in, gv, s);
+  return launch_u<MR, 4>(in, gv, s);
+}
+
+}  // namespace
+
+int fused_slots_per_row() { return kSlots; }
+
+hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
+  // K chunks per lane must be at most two: K <= 32 * LPR with LPR <= 64
+  if (gv.R < 1 || gv.R > kRows || gv.K > kMaxRowLen || gv.K % 16) return hipErrorInvalidValue;
+  if (gv.R == 1) return launch_lpr<1>(in, gv, s);
+  if (gv.R == 2) return launch_lpr<2>(in, gv, s);
+  if (gv.R <= 4) return launch_lpr<4>(in, gv, s);
+  return launch_lpr<8>(in, gv, s);
+}
+
+hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s) {
+  hipLaunchKernelGGL(k_greedy_commit_slots, dim3(1), dim3(64), 0, s, gv);
+  return hipGetLastError();
+}
+
+}  // namespace mnmt

@@ -72,7 +72,8 @@ hipError_t launch_greedy_commit(unsigned long long* slots, int R, int T, int32_t
                                 int32_t* finished, int32_t* out_len, int* step, int stop_at_eos, int eos,
                                 int pad, hipStream_t s);
 hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
-                               int32_t* out_len, int* step, int bos, hipStream_t s);
+                               int32_t* out_len, int* step, int bos, unsigned long long* fslots, int n_fslots,
+                               hipStream_t s);
 hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, int R, int T, int32_t* out,
                                 int32_t* out_len_dst, hipStream_t s);
 // Arg-max of fp32 rows [R, V] into packed slots (greedy when logits are
@@ -80,6 +81,43 @@ hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, 
 hipError_t launch_row_argmax(const float* z, int R, int V, unsigned long long* slots, hipStream_t s);
 // Copy tokens into/out of the session (int32 vectors).
 hipError_t launch_copy_i32(const int32_t* src, int32_t* dst, int n, hipStream_t s);
+
+// Fused decoder step for up to 8 rows (decode_fused.hip).
+struct FusedIn {           // how a kernel obtains its int8 input rows
+  const float* x;          // residual rows [R, d] (unused when embed)
+  float* x_out;            // block 0 writes the input (wb_input) or normalized rows here, or null
+  int wb_input;
+  int embed;               // 1: rows are the embeddings of tok[] at position *step
+  const int32_t* tok;
+  const int8_t* E;
+  const float* c_emb;
+  const float* pe;
+  int V;
+  int do_ln;               // LayerNorm before quantization
+  const float* g;
+  const float* b;
+  float eps;
+  float inv_s;             // 1 / input scale of the consuming linear layer
+};
+struct FusedGemv {         // a linear layer over the prepared rows, and greedy bookkeeping
+  int R, K, N;
+  int t;                   // decode step (position) of this launch
+  int epi;                 // MNMT_EPI_I8, MNMT_EPI_I8_RELU or EPI_LOGITS_ARGMAX
+  const int8_t* W;
+  const float* scale;
+  const float* bias;
+  void* out;               // int8 [R, N]; for the arg-max: fp32 logits [R, N] or null
+  unsigned long long* slots;  // arg-max: [R][fused_slots_per_row()], zero before the launch
+  int* step;               // commit: advanced to t + 1
+  int32_t* out_tok;
+  int32_t* cur_tok;
+  int32_t* finished;
+  int32_t* out_len;
+  int T, stop_at_eos, eos, pad;
+};
+hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s);
+hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s);
+int fused_slots_per_row();
 
 // Beam search kernels.
 struct BeamState {
@@ -171,6 +209,8 @@ struct mnmt_session {
   float* logits = nullptr;  // shares memory with the encoder scratch
   std::vector<int8_t*> cross_kv;
   float* dec_x = nullptr;
+  float* dec_x2 = nullptr;  // second residual buffer (post-LN ping-pong)
+  unsigned long long* fslots = nullptr;  // spread arg-max slots [8][fused_slots_per_row()]
   int8_t* dec_a = nullptr;
   int8_t* dec_qkv = nullptr;
   int8_t* dec_q = nullptr;

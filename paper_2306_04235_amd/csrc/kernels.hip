@@ -4,23 +4,11 @@
 #include <cfloat>
 #include <climits>
 
-#include "canon.hpp"
+#include "blocks.hpp"
 #include "internal.h"
 
 namespace mnmt {
 namespace {
-
-constexpr int kMaxAttnLen = 256;  // longest attended sequence (4 keys per lane)
-constexpr int kMaxHeadDim = 128;  // 8 x 16 bytes of query in registers
-constexpr int kMaxRowLen = 1024;  // LayerNorm width (16 values per lane)
-
-__device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
-  acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
-  acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
-  acc = __builtin_amdgcn_sdot4(a.z, b.z, acc, false);
-  acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
-  return acc;
-}
 
 // ---------------------------------------------------------------------------
 // Embedding: x = fma(E[tok], c_emb[tok], PE[pos]).  One wave per row.
@@ -96,65 +84,10 @@ __global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, i
   }
 }
 
-// ---------------------------------------------------------------------------
-// Attention of one query row over n keys for one head, by one wave
-// (Appendix A self-weight / self-sum equations with the quantizer figure's
-// precisions): int8 scores, fp32 softmax in the canonical order, context
-// accumulated over ascending key index with one fma per key, requantized.
-// key(t) / val(t) give the head's dh codes of key / value t.
-template <class KeyFn, class ValFn>
-__device__ __forceinline__ void attend_wave(const int8_t* __restrict__ q, int n, int dh, KeyFn key, ValFn val,
-                                            float c_qk, float c_pv, int8_t* __restrict__ out, float* p_sh) {
-  const int lane = threadIdx.x & 63;
-  const int nc = dh / 16;
-  int4 qv[kMaxHeadDim / 16];
-#pragma unroll
-  for (int c = 0; c < kMaxHeadDim / 16; ++c) qv[c] = c < nc ? *(const int4*)(q + 16 * c) : make_int4(0, 0, 0, 0);
-  float sv[kMaxAttnLen / 64];
-  float mx = -FLT_MAX;
-#pragma unroll
-  for (int i = 0; i < kMaxAttnLen / 64; ++i) {
-    const int t = lane + 64 * i;
-    sv[i] = 0.0f;
-    if (t < n) {
-      const int8_t* kp = key(t);
-      int acc = 0;
-#pragma unroll
-      for (int c = 0; c < kMaxHeadDim / 16; ++c)
-        if (c < nc) acc = dot16(*(const int4*)(kp + 16 * c), qv[c], acc);
-      sv[i] = (float)acc * c_qk;
-      mx = fmaxf(mx, sv[i]);
-    }
-  }
-  mx = wave_max(mx);
-  float part = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kMaxAttnLen / 64; ++i) {
-    const int t = lane + 64 * i;
-    if (t < n) {
-      sv[i] = canon_exp(sv[i] - mx);
-      part = part + sv[i];
-    }
-  }
-  const float inv = 1.0f / wave_sum(part);
-#pragma unroll
-  for (int i = 0; i < kMaxAttnLen / 64; ++i) {
-    const int t = lane + 64 * i;
-    if (t < n) p_sh[t] = sv[i] * inv;
-  }
-  __syncthreads();  // the block is this one wave: publish p to every lane
-  for (int j = lane; j < dh; j += 64) {
-    float acc = 0.0f;
-    for (int t = 0; t < n; ++t) acc = fmaf(p_sh[t], (float)val(t)[j], acc);
-    out[j] = code_of(acc * c_pv);
-  }
-}
-
 // Encoder self-attention: block = one wave = (query s, head hd, sentence b).
 __global__ __launch_bounds__(64) void k_attn_enc(const int8_t* __restrict__ qkv, const int32_t* __restrict__ len,
                                                  int S, int d, int dh, float c_qk, float c_pv,
                                                  int8_t* __restrict__ ctx) {
-  __shared__ float p_sh[kMaxAttnLen];
   const int s = blockIdx.x, hd = blockIdx.y, b = blockIdx.z;
   int n = len[b];
   n = n < 1 ? 1 : (n > S ? S : n);
@@ -162,7 +95,7 @@ __global__ __launch_bounds__(64) void k_attn_enc(const int8_t* __restrict__ qkv,
   const int8_t* q = base + (size_t)s * 3 * d + hd * dh;
   auto key = [&](int t) { return base + (size_t)t * 3 * d + d + hd * dh; };
   auto val = [&](int t) { return base + (size_t)t * 3 * d + 2 * d + hd * dh; };
-  attend_wave(q, n, dh, key, val, c_qk, c_pv, ctx + ((size_t)b * S + s) * d + hd * dh, p_sh);
+  attend_wave(q, n, dh, key, val, c_qk, c_pv, ctx + ((size_t)b * S + s) * d + hd * dh);
 }
 
 // Decoder self-attention at position t = *step: block = one wave = (head, row).
@@ -170,7 +103,6 @@ __global__ __launch_bounds__(64) void k_attn_dec_self(const int8_t* __restrict__
                                                       const int* __restrict__ step, int8_t* __restrict__ kcache,
                                                       int8_t* __restrict__ vcache, const int32_t* __restrict__ hist,
                                                       float c_qk, float c_pv, int8_t* __restrict__ ctx) {
-  __shared__ float p_sh[kMaxAttnLen];
   const int hd = blockIdx.x, r = blockIdx.y;
   const int lane = threadIdx.x;
   int t = *step;
@@ -185,17 +117,17 @@ __global__ __launch_bounds__(64) void k_attn_dec_self(const int8_t* __restrict__
   // beam: hist holds two [R][T] tables used on alternate steps
   const int R = gridDim.y;
   const int32_t* hr = hist ? hist + ((size_t)(t & 1) * R + r) * T : nullptr;
-  auto key = [&](int tp) {
+  auto key = [&](int tp) -> const int8_t* {
     if (tp == t) return knew;
     const int src = hr ? hr[tp] : r;
     return (const int8_t*)kcache + ((size_t)src * T + tp) * d + hd * dh;
   };
-  auto val = [&](int tp) {
+  auto val = [&](int tp) -> const int8_t* {
     if (tp == t) return vnew;
     const int src = hr ? hr[tp] : r;
     return (const int8_t*)vcache + ((size_t)src * T + tp) * d + hd * dh;
   };
-  attend_wave(row + hd * dh, t + 1, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh, p_sh);
+  attend_wave(row + hd * dh, t + 1, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh);
 }
 
 // Decoder cross-attention: row r attends over the source of sentence r / W.
@@ -203,7 +135,6 @@ __global__ __launch_bounds__(64) void k_attn_dec_cross(const int8_t* __restrict_
                                                        const int8_t* __restrict__ kv, int S,
                                                        const int32_t* __restrict__ len, float c_qk, float c_pv,
                                                        int8_t* __restrict__ ctx) {
-  __shared__ float p_sh[kMaxAttnLen];
   const int hd = blockIdx.x, r = blockIdx.y;
   const int b = r / W;
   int n = len[b];
@@ -211,19 +142,20 @@ __global__ __launch_bounds__(64) void k_attn_dec_cross(const int8_t* __restrict_
   const int8_t* base = kv + (size_t)b * S * 2 * d;
   auto key = [&](int t) { return base + (size_t)t * 2 * d + hd * dh; };
   auto val = [&](int t) { return base + (size_t)t * 2 * d + d + hd * dh; };
-  attend_wave(q + (size_t)r * d + hd * dh, n, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh, p_sh);
+  attend_wave(q + (size_t)r * d + hd * dh, n, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh);
 }
 
 // ---------------------------------------------------------------------------
 // Greedy search bookkeeping.
 __global__ void k_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
-                               int32_t* out_len, int* step, int bos) {
+                               int32_t* out_len, int* step, int bos, unsigned long long* fslots, int n_fslots) {
   for (int r = threadIdx.x; r < R; r += blockDim.x) {
     slots[r] = 0ull;
     cur_tok[r] = bos;
     finished[r] = 0;
     out_len[r] = steps;
   }
+  for (int i = threadIdx.x; i < n_fslots; i += blockDim.x) fslots[i] = 0ull;
   if (threadIdx.x == 0) *step = 0;
 }
 
@@ -577,9 +509,10 @@ hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, co
 }
 
 hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
-                               int32_t* out_len, int* step, int bos, hipStream_t s) {
+                               int32_t* out_len, int* step, int bos, unsigned long long* fslots, int n_fslots,
+                               hipStream_t s) {
   hipLaunchKernelGGL(k_greedy_reset, dim3(1), dim3(256), 0, s, slots, R, steps, cur_tok, finished, out_len, step,
-                     bos);
+                     bos, fslots, n_fslots);
   return hipGetLastError();
 }
 

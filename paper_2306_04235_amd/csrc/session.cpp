@@ -10,6 +10,7 @@
 #include <cmath>
 #include <cstring>
 #include <string>
+#include <utility>
 
 #include "internal.h"
 
@@ -28,7 +29,7 @@ struct Bump {
 struct Plan {
   size_t src, len, region, enc_x, enc_a, enc_qkv, enc_h, enc_out, logits;
   std::vector<size_t> cross_kv, kc, vc;
-  size_t dec_x, dec_a, dec_qkv, dec_q, dec_h;
+  size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots;
   size_t cur_tok, step, slots, out_tok, finished, out_len, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
   size_t total;
@@ -71,6 +72,8 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.logits = p.region;
   for (size_t l = 0; l < Ld; ++l) p.cross_kv.push_back(b.take(BS * 2 * d));
   p.dec_x = b.take(4 * R * d);
+  p.dec_x2 = b.take(4 * R * d);
+  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row());
   p.dec_a = b.take(R * d);
   p.dec_qkv = b.take(R * 3 * d);
   p.dec_q = b.take(R * d);
@@ -206,6 +209,96 @@ int greedy_step(mnmt_session* S, int R, int stop_at_eos, float* logits_out, hipS
   return MNMT_OK;
 }
 
+// Greedy step for at most 8 rows with LayerNorm (and the embedding) fused into
+// the GEMV that consumes it, per decoder layer:
+//   [LN + QKV] [self-attention] [W_o + residual] [LN + Q] [cross-attention]
+//   [W_oc + residual] [LN + W1 + ReLU] [W2 + residual]
+// then [LN + logits + arg-max] and [commit].  Post-LN models alternate between
+// two residual buffers: block 0 writes the normalized rows while the other
+// blocks still read the un-normalized ones.
+int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
+  const bool post = m->info.ln_post;
+  float* xc = S->dec_x;
+  float* xo = S->dec_x2;
+  auto input = [&](bool embed, bool do_ln, const LnDev& ln, float inv_s, bool write_norm) {
+    FusedIn in{};
+    in.x = xc;
+    in.embed = embed;
+    in.tok = S->cur_tok;
+    in.E = m->E;
+    in.c_emb = m->c_emb;
+    in.pe = m->pe;
+    in.V = m->info.vocab;
+    in.do_ln = do_ln;
+    in.g = ln.g;
+    in.b = ln.b;
+    in.eps = m->info.ln_eps;
+    in.inv_s = inv_s;
+    if (embed) {
+      in.x_out = xc;  // the embedding becomes the residual stream
+      in.wb_input = 1;
+    } else if (write_norm) {
+      in.x_out = xo;  // post-LN: the normalized rows become the residual stream
+      in.wb_input = 0;
+    }
+    return in;
+  };
+  auto gemv = [&](const LinearDev& L, int epi, void* out) {
+    FusedGemv gv{};
+    gv.R = R;
+    gv.K = L.K;
+    gv.N = L.N;
+    gv.t = t;
+    gv.epi = epi;
+    gv.W = L.w;
+    gv.scale = L.scale;
+    gv.bias = L.bias;
+    gv.out = out;
+    return gv;
+  };
+  int rc;
+  for (size_t l = 0; l < m->dec.size(); ++l) {
+    const LayerDev& L = m->dec[l];
+    {
+      const bool embed = l == 0;
+      const LnDev& ln = post ? (embed ? L.sa_ln : m->dec[l - 1].ff_ln) : L.sa_ln;
+      LAUNCH(launch_qgemv_ln(input(embed, post ? !embed : true, ln, L.qkv.inv_in, post && !embed),
+                             gemv(L.qkv, MNMT_EPI_I8, S->dec_qkv), s));
+      if (post && !embed) std::swap(xc, xo);
+    }
+    LAUNCH(launch_attn_dec_self(S->dec_qkv, R, d, h, T, S->step, S->kcache[l], S->vcache[l], nullptr, L.sa_cqk,
+                                L.sa_cpv, S->dec_a, s));
+    if ((rc = qlin(L.o, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.sa_gamma, s))) return rc;
+    LAUNCH(launch_qgemv_ln(input(false, true, post ? L.sa_ln : L.ca_ln, L.cq.inv_in, post),
+                           gemv(L.cq, MNMT_EPI_I8, S->dec_q), s));
+    if (post) std::swap(xc, xo);
+    LAUNCH(launch_attn_dec_cross(S->dec_q, R, 1, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, S->dec_a, s));
+    if ((rc = qlin(L.co, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.ca_gamma, s))) return rc;
+    LAUNCH(launch_qgemv_ln(input(false, true, post ? L.ca_ln : L.ff_ln, L.w1.inv_in, post),
+                           gemv(L.w1, MNMT_EPI_I8_RELU, S->dec_h), s));
+    if (post) std::swap(xc, xo);
+    if ((rc = qlin(L.w2, S->dec_h, R, MNMT_EPI_F32_RESID, xc, L.ff_gamma, s))) return rc;
+  }
+  // output projection over the shared embedding with the arg-max, then commit
+  LinearDev out_proj{m->E, m->c_out, nullptr, m->info.vocab, d, 0.f};
+  FusedGemv gv = gemv(out_proj, EPI_LOGITS_ARGMAX, logits_out);
+  gv.slots = S->fslots;
+  gv.step = S->step;
+  gv.out_tok = S->out_tok;
+  gv.cur_tok = S->cur_tok;
+  gv.finished = S->finished;
+  gv.out_len = S->out_len;
+  gv.T = T;
+  gv.stop_at_eos = stop_at_eos;
+  gv.eos = m->info.eos_id;
+  gv.pad = m->info.pad_id;
+  LAUNCH(launch_qgemv_ln(input(false, true, post ? m->dec.back().ff_ln : m->dec_ln, m->inv_fin, false), gv, s));
+  LAUNCH(launch_greedy_commit_slots(gv, s));
+  return MNMT_OK;
+}
+
 int beam_step(mnmt_session* S, int R, int W, hipStream_t s) {
   const mnmt_model* m = S->m;
   int rc = run_decoder_layers(S, R, W, true, s);
@@ -226,9 +319,11 @@ int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
   if (sc.beam == 1) {
     const int R = S->B;
     LAUNCH(launch_greedy_reset(S->slots, R, sc.max_steps, S->cur_tok, S->finished, S->out_len, S->step,
-                               m->info.bos_id, s));
+                               m->info.bos_id, S->fslots, 8 * fused_slots_per_row(), s));
     for (int t = 0; t < sc.max_steps; ++t)
-      if ((rc = greedy_step(S, R, sc.stop_at_eos, nullptr, s))) return rc;
+      if ((rc = R <= 8 ? greedy_step_fused(S, R, t, sc.stop_at_eos, nullptr, s)
+                       : greedy_step(S, R, sc.stop_at_eos, nullptr, s)))
+        return rc;
   } else {
     const int R = S->B * sc.beam;
     LAUNCH(launch_beam_reset(S->beam, S->step, s));
@@ -298,6 +393,8 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->logits = (float*)at(p.logits);
   for (size_t l = 0; l < p.cross_kv.size(); ++l) S->cross_kv.push_back((int8_t*)at(p.cross_kv[l]));
   S->dec_x = (float*)at(p.dec_x);
+  S->dec_x2 = (float*)at(p.dec_x2);
+  S->fslots = (unsigned long long*)at(p.fslots);
   S->dec_a = (int8_t*)at(p.dec_a);
   S->dec_qkv = (int8_t*)at(p.dec_qkv);
   S->dec_q = (int8_t*)at(p.dec_q);
@@ -377,7 +474,7 @@ extern "C" int mnmt_encode(mnmt_session* S, const int32_t* d_src, const int32_t*
   if ((rc = run_encoder(S, s))) return rc;
   const mnmt_model* m = S->m;
   LAUNCH(launch_greedy_reset(S->slots, B, S->cfg.max_tgt_len, S->cur_tok, S->finished, S->out_len, S->step,
-                             m->info.bos_id, s));
+                             m->info.bos_id, S->fslots, 8 * fused_slots_per_row(), s));
   S->encoded = true;
   S->host_step = 0;
   return MNMT_OK;
@@ -394,7 +491,8 @@ extern "C" int mnmt_decode_step(mnmt_session* S, const int32_t* d_prev, int32_t*
   hipStream_t s = as_stream(stream);
   const int R = S->B;
   if (d_prev) LAUNCH(launch_copy_i32(d_prev, S->cur_tok, R, s));
-  if ((rc = greedy_step(S, R, 0, d_logits, s))) return rc;
+  if ((rc = R <= 8 ? greedy_step_fused(S, R, S->host_step, 0, d_logits, s) : greedy_step(S, R, 0, d_logits, s)))
+    return rc;
   LAUNCH(launch_copy_i32(S->cur_tok, d_next, R, s));
   ++S->host_step;
   return MNMT_OK;
