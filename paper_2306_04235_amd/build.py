@@ -22,7 +22,7 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off", "-Wall", "-Wno-unus
           "-I" + os.path.join(os.path.dirname(HERE), "include")]
 DEVICE = [f"--offload-arch={ARCH}", "-fno-gpu-flush-denormals-to-zero", "-fhip-fp32-correctly-rounded-divide-sqrt",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-SOURCES = ["qlinear.hip", "kernels.hip", "decode_fused.hip", "model.cpp", "session.cpp", "api.cpp"]
+SOURCES = ["qlinear.hip", "kernels.hip", "decode_fused.hip", "decode_step.hip", "model.cpp", "session.cpp", "api.cpp"]
 
 
 def _compile(src: str, verbose: bool) -> str:

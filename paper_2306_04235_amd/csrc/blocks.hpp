@@ -6,6 +6,7 @@
 #include <cfloat>
 
 #include "canon.hpp"
+#include "internal.h"
 
 namespace mnmt {
 
@@ -21,33 +22,57 @@ __device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
   return acc;
 }
 
-// Attention of one query row over n keys for one head, by one wave
-// (Appendix A self-weight / self-sum equations with the quantizer figure's
-// precisions): int8 scores, fp32 softmax in the canonical order, context
-// accumulated over ascending key index with one fma per key, requantized.
-// key(t) / val(t) return the head's dh codes of key / value t (global or LDS
-// addresses).  Softmax weights are exchanged by lane shuffles, so the wave
-// needs no barrier and may share its block with other waves.
-template <class KeyFn, class ValFn>
+// LDS-visibility barrier for the lanes of one wave (the other waves of the
+// block are not involved).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// LDS one wave's attention needs: softmax weights and the value rows.
+template <int NMAX, int DHMAX>
+struct AttnLdsT {
+  float p[NMAX];
+  int8_t v[NMAX][DHMAX];
+};
+using AttnLds = AttnLdsT<kMaxAttnLen, kMaxHeadDim>;
+
+// Attention of one query row over n keys for one head, by one wave (Appendix
+// A self-weight / self-sum equations with the quantizer figure's precisions):
+// int8 scores, fp32 softmax in the canonical order, context accumulated over
+// ascending key index with one fma per key, requantized.  key(t) / val(t)
+// return the head's dh codes of key / value t (global or LDS addresses).
+// Lane t loads key t and value t together, so all global loads are in flight
+// at once; weights and values are then staged in the wave's own LDS for the
+// context loop.  Only this wave synchronizes, so other waves of the block may
+// be elsewhere.
+template <int NMAX, int DHMAX, class KeyFn, class ValFn>
 __device__ __forceinline__ void attend_wave(const int8_t* __restrict__ q, int n, int dh, KeyFn key, ValFn val,
-                                            float c_qk, float c_pv, int8_t* __restrict__ out) {
+                                            float c_qk, float c_pv, int8_t* __restrict__ out,
+                                            AttnLdsT<NMAX, DHMAX>& sh) {
   const int lane = threadIdx.x & 63;
   const int nc = dh / 16;
-  int4 qv[kMaxHeadDim / 16];
+  int4 qv[DHMAX / 16];
 #pragma unroll
-  for (int c = 0; c < kMaxHeadDim / 16; ++c) qv[c] = c < nc ? *(const int4*)(q + 16 * c) : make_int4(0, 0, 0, 0);
-  float sv[kMaxAttnLen / 64];
+  for (int c = 0; c < DHMAX / 16; ++c) qv[c] = c < nc ? *(const int4*)(q + 16 * c) : make_int4(0, 0, 0, 0);
+  float sv[(NMAX + 63) / 64];
   float mx = -FLT_MAX;
 #pragma unroll
-  for (int i = 0; i < kMaxAttnLen / 64; ++i) {
+  for (int i = 0; i < (NMAX + 63) / 64; ++i) {
     const int t = lane + 64 * i;
     sv[i] = 0.0f;
     if (t < n) {
       const int8_t* kp = key(t);
+      const int8_t* vp = val(t);
       int acc = 0;
 #pragma unroll
-      for (int c = 0; c < kMaxHeadDim / 16; ++c)
-        if (c < nc) acc = dot16(*(const int4*)(kp + 16 * c), qv[c], acc);
+      for (int c = 0; c < DHMAX / 16; ++c) {
+        if (c < nc) {
+          acc = dot16(*(const int4*)(kp + 16 * c), qv[c], acc);
+          *(int4*)&sh.v[t][16 * c] = *(const int4*)(vp + 16 * c);
+        }
+      }
       sv[i] = (float)acc * c_qk;
       mx = fmaxf(mx, sv[i]);
     }
@@ -55,7 +80,7 @@ __device__ __forceinline__ void attend_wave(const int8_t* __restrict__ q, int n,
   mx = wave_max(mx);
   float part = 0.0f;
 #pragma unroll
-  for (int i = 0; i < kMaxAttnLen / 64; ++i) {
+  for (int i = 0; i < (NMAX + 63) / 64; ++i) {
     const int t = lane + 64 * i;
     if (t < n) {
       sv[i] = canon_exp(sv[i] - mx);
@@ -64,66 +89,135 @@ __device__ __forceinline__ void attend_wave(const int8_t* __restrict__ q, int n,
   }
   const float inv = 1.0f / wave_sum(part);
 #pragma unroll
-  for (int i = 0; i < kMaxAttnLen / 64; ++i) sv[i] = sv[i] * inv;  // p_t for t = lane + 64 i
-  for (int j0 = 0; j0 < dh; j0 += 64) {
-    const int j = j0 + lane;
+  for (int i = 0; i < (NMAX + 63) / 64; ++i) {
+    const int t = lane + 64 * i;
+    if (t < n) sh.p[t] = sv[i] * inv;
+  }
+  wave_sync();  // p and v visible to every lane of this wave
+  for (int j = lane; j < dh; j += 64) {
     float acc = 0.0f;
-#pragma unroll
-    for (int i = 0; i < kMaxAttnLen / 64; ++i) {
-      const int tn = n - 64 * i < 64 ? n - 64 * i : 64;
-      for (int tl = 0; tl < tn; ++tl) {
-        const float p = __shfl(sv[i], tl, 64);
-        const int8_t* vp = val(64 * i + tl);
-        if (j < dh) acc = fmaf(p, (float)vp[j], acc);
-      }
-    }
-    if (j < dh) out[j] = code_of(acc * c_pv);
+    for (int t = 0; t < n; ++t) acc = fmaf(sh.p[t], (float)sh.v[t][j], acc);
+    out[j] = code_of(acc * c_pv);
   }
 }
 
-// LayerNorm of one row by one wave (element i in lane i % 64, ascending i),
-// optionally without the normalization (do_ln = 0: y = x).  Writes the int8
-// codes quant(y, inv_s) to q (any address space) and, if y_out, the fp32 y.
-__device__ __forceinline__ void ln_row_wave(const float* __restrict__ x, int d, int do_ln, const float* __restrict__ g,
-                                            const float* __restrict__ b, float eps, float inv_s, int8_t* q,
-                                            float* y_out) {
-  const int lane = threadIdx.x & 63;
-  float v[kMaxRowLen / 64];
+// Input rows -> int8 rows in LDS (Section 4.2 fusion of the element-wise work
+// in front of a GEMM): row r of the block is global row row0 + r, taken from
+// the residual stream or computed as the token embedding, optionally layer-
+// normalized, then quantized into a_lds + r * lds_stride.  `writer` blocks
+// also store the embedding (wb_input) or the normalized row (post-LN) to
+// in.x_out.  Wave w prepares rows w, w + 4, ...; each wave works on
+// kPrepGroup rows at once so that their loads and reductions overlap.
+constexpr int kPrepGroup = 4;
+
+// Row-width classes the fused kernels are compiled for (d <= class).
+__host__ __device__ constexpr int row_class(int d) {
+  return d <= 64 ? 64 : d <= 128 ? 128 : d <= 256 ? 256 : d <= 384 ? 384 : d <= 512 ? 512 : 1024;
+}
+// Lanes per weight row of a GEMV over rows of that width (a power of two,
+// leaving each lane at most two 16-byte chunks).
+__host__ __device__ constexpr int lanes_per_row(int dmax) {
+  return dmax >= 1024 ? 64 : dmax >= 512 ? 32 : dmax >= 256 ? 16 : dmax >= 128 ? 8 : 4;
+}
+
+template <int NJ>  // d <= 64 * NJ
+__device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int row0, int d, int t, int8_t* a_lds,
+                                             int lds_stride, bool writer) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  writer = writer && in.x_out != nullptr;
   const int n = (d + 63) / 64;
+  for (int r0 = wave; r0 < rows; r0 += 4 * kPrepGroup) {
+    float v[kPrepGroup][NJ];
 #pragma unroll
-  for (int j = 0; j < kMaxRowLen / 64; ++j) {
-    const int i = lane + 64 * j;
-    v[j] = (j < n && i < d) ? x[i] : 0.0f;
-  }
-  if (do_ln) {
-    float p = 0.0f;
+    for (int g = 0; g < kPrepGroup; ++g) {
+      const int r = r0 + 4 * g;
+      const size_t gr = (size_t)(row0 + (r < rows ? r : 0));
+      if (in.embed) {
+        int tok = in.tok[gr];
+        tok = tok < 0 ? 0 : (tok >= in.V ? in.V - 1 : tok);
+        const int pos = in.S_pos > 0 ? (int)(gr % (size_t)in.S_pos) : t;
+        const float c = in.c_emb[tok];
 #pragma unroll
-    for (int j = 0; j < kMaxRowLen / 64; ++j)
-      if (j < n && lane + 64 * j < d) p = p + v[j];
-    const float inv_d = 1.0f / (float)d;
-    const float mu = wave_sum(p) * inv_d;
-    float p2 = 0.0f;
+        for (int j = 0; j < NJ; ++j) {
+          const int i = lane + 64 * j;
+          v[g][j] = (r < rows && j < n && i < d) ? fmaf((float)in.E[(size_t)tok * d + i], c, in.pe[(size_t)pos * d + i])
+                                                 : 0.0f;
+        }
+      } else {
 #pragma unroll
-    for (int j = 0; j < kMaxRowLen / 64; ++j) {
-      if (j < n && lane + 64 * j < d) {
-        v[j] = v[j] - mu;
-        p2 = fmaf(v[j], v[j], p2);
+        for (int j = 0; j < NJ; ++j) {
+          const int i = lane + 64 * j;
+          v[g][j] = (r < rows && j < n && i < d) ? in.x[gr * d + i] : 0.0f;
+        }
       }
     }
-    const float var = wave_sum(p2) * inv_d;
-    const float rstd = 1.0f / sqrtf(var + eps);
+    if (writer && in.wb_input) {
 #pragma unroll
-    for (int j = 0; j < kMaxRowLen / 64; ++j) {
-      const int i = lane + 64 * j;
-      if (j < n && i < d) v[j] = fmaf(v[j] * rstd, g[i], b[i]);
+      for (int g = 0; g < kPrepGroup; ++g) {
+        const int r = r0 + 4 * g;
+        if (r >= rows) continue;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int i = lane + 64 * j;
+          if (j < n && i < d) in.x_out[(size_t)(row0 + r) * d + i] = v[g][j];
+        }
+      }
     }
-  }
+    if (in.do_ln) {
+      // mean: canonical sum of each row (lane partials over ascending i, butterfly)
+      float p[kPrepGroup];
 #pragma unroll
-  for (int j = 0; j < kMaxRowLen / 64; ++j) {
-    const int i = lane + 64 * j;
-    if (j < n && i < d) {
-      if (q) q[i] = code_of(v[j] * inv_s);
-      if (y_out) y_out[i] = v[j];
+      for (int g = 0; g < kPrepGroup; ++g) {
+        p[g] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          if (j < n && lane + 64 * j < d) p[g] = p[g] + v[g][j];
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+        for (int g = 0; g < kPrepGroup; ++g) p[g] = p[g] + __shfl_xor(p[g], off, 64);
+      const float inv_d = 1.0f / (float)d;
+      float p2[kPrepGroup];
+#pragma unroll
+      for (int g = 0; g < kPrepGroup; ++g) {
+        const float mu = p[g] * inv_d;
+        p2[g] = 0.0f;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          if (j < n && lane + 64 * j < d) {
+            v[g][j] = v[g][j] - mu;
+            p2[g] = fmaf(v[g][j], v[g][j], p2[g]);
+          }
+        }
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+        for (int g = 0; g < kPrepGroup; ++g) p2[g] = p2[g] + __shfl_xor(p2[g], off, 64);
+#pragma unroll
+      for (int g = 0; g < kPrepGroup; ++g) {
+        const float var = p2[g] * inv_d;
+        const float rstd = 1.0f / sqrtf(var + in.eps);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int i = lane + 64 * j;
+          if (j < n && i < d) v[g][j] = fmaf(v[g][j] * rstd, in.g[i], in.b[i]);
+        }
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < kPrepGroup; ++g) {
+      const int r = r0 + 4 * g;
+      if (r >= rows) continue;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int i = lane + 64 * j;
+        if (j < n && i < d) {
+          a_lds[r * lds_stride + i] = code_of(v[g][j] * in.inv_s);
+          if (writer && !in.wb_input) in.x_out[(size_t)(row0 + r) * d + i] = v[g][j];
+        }
+      }
     }
   }
 }

@@ -22,76 +22,13 @@ namespace {
 constexpr int kRows = 8;    // rows per fused step (greedy batch <= 8)
 constexpr int kSlots = 32;  // arg-max slots per row
 
-// Input rows -> int8 rows in LDS; wave w prepares rows w, w + 4.
-__device__ __forceinline__ void prepare_rows(const FusedIn& in, int R, int d, int t, int8_t* a_lds) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const bool writer = blockIdx.x == 0 && in.x_out != nullptr;
-  const int n = (d + 63) / 64;
-  for (int r = wave; r < R; r += 4) {
-    float v[kMaxRowLen / 64];
-    if (in.embed) {
-      int tok = in.tok[r];
-      tok = tok < 0 ? 0 : (tok >= in.V ? in.V - 1 : tok);
-      const float c = in.c_emb[tok];
-#pragma unroll
-      for (int j = 0; j < kMaxRowLen / 64; ++j) {
-        const int i = lane + 64 * j;
-        v[j] = (j < n && i < d) ? fmaf((float)in.E[(size_t)tok * d + i], c, in.pe[(size_t)t * d + i]) : 0.0f;
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < kMaxRowLen / 64; ++j) {
-        const int i = lane + 64 * j;
-        v[j] = (j < n && i < d) ? in.x[(size_t)r * d + i] : 0.0f;
-      }
-    }
-    if (writer && in.wb_input) {
-#pragma unroll
-      for (int j = 0; j < kMaxRowLen / 64; ++j) {
-        const int i = lane + 64 * j;
-        if (j < n && i < d) in.x_out[(size_t)r * d + i] = v[j];
-      }
-    }
-    if (in.do_ln) {
-      float p = 0.0f;
-#pragma unroll
-      for (int j = 0; j < kMaxRowLen / 64; ++j)
-        if (j < n && lane + 64 * j < d) p = p + v[j];
-      const float inv_d = 1.0f / (float)d;
-      const float mu = wave_sum(p) * inv_d;
-      float p2 = 0.0f;
-#pragma unroll
-      for (int j = 0; j < kMaxRowLen / 64; ++j) {
-        if (j < n && lane + 64 * j < d) {
-          v[j] = v[j] - mu;
-          p2 = fmaf(v[j], v[j], p2);
-        }
-      }
-      const float var = wave_sum(p2) * inv_d;
-      const float rstd = 1.0f / sqrtf(var + in.eps);
-#pragma unroll
-      for (int j = 0; j < kMaxRowLen / 64; ++j) {
-        const int i = lane + 64 * j;
-        if (j < n && i < d) v[j] = fmaf(v[j] * rstd, in.g[i], in.b[i]);
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < kMaxRowLen / 64; ++j) {
-      const int i = lane + 64 * j;
-      if (j < n && i < d) {
-        a_lds[r * d + i] = code_of(v[j] * in.inv_s);
-        if (writer && !in.wb_input) in.x_out[(size_t)r * d + i] = v[j];
-      }
-    }
-  }
-}
-
-// MR rows of input, LPR lanes per weight row, U row groups per wave, and at
-// most two 16-byte K chunks per lane (K <= 32 * LPR, i.e. d <= 1024).
-template <int MR, int LPR, int U>
+// MR rows of input, rows of width K <= DMAX (LPR lanes per weight row, at
+// most two 16-byte K chunks per lane), U row groups per wave.
+template <int MR, int DMAX, int U>
 __global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
+  constexpr int LPR = lanes_per_row(DMAX);
   constexpr int RPI = 64 / LPR;
-  __shared__ __attribute__((aligned(16))) int8_t a_lds[MR * kMaxRowLen];
+  __shared__ __attribute__((aligned(16))) int8_t a_lds[MR * DMAX];
   __shared__ unsigned long long wmax[4][MR];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int sub = lane / LPR, kl = lane % LPR;
@@ -109,7 +46,7 @@ __global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
     }
   }
   // 2. input rows while the loads are in flight
-  prepare_rows(in, R, K, gv.t, a_lds);
+  prepare_rows<(DMAX + 63) / 64>(in, R, 0, K, gv.t, a_lds, K, blockIdx.x == 0);
   __syncthreads();
   // 3. dot products
   int acc[U][MR];
@@ -199,32 +136,36 @@ __global__ void k_greedy_commit_slots(FusedGemv gv) {
     }
     gv.cur_tok[m] = fin ? gv.pad : tok;
   }
+  for (int i = threadIdx.x; gv.zero_acc && i < gv.zero_n; i += blockDim.x) gv.zero_acc[i] = 0;
   if (threadIdx.x == 0) *gv.step = t + 1;
 }
 
-template <int MR, int LPR>
+// Row groups per wave: large layers (the output projection) get 8 so that
+// one round of about one block per CU has the whole matrix in flight; small
+// layers get 1 for the most blocks.
+template <int MR, int DMAX>
 hipError_t launch_u(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
-  constexpr int RPI = 64 / LPR;
-  const long waves4 = ((long)gv.N + RPI * 4 - 1) / (RPI * 4);
-  if (waves4 >= 1024) {
-    hipLaunchKernelGGL((k_qgemv_ln<MR, LPR, 4>), dim3((int)((waves4 + 3) / 4)), dim3(256), 0, s, in, gv);
+  constexpr int RPI = 64 / lanes_per_row(DMAX);
+  const long blocks8 = ((long)gv.N + RPI * 32 - 1) / (RPI * 32);
+  if (blocks8 >= 128) {
+    hipLaunchKernelGGL((k_qgemv_ln<MR, DMAX, 8>), dim3((int)blocks8), dim3(256), 0, s, in, gv);
   } else {
-    const long waves = ((long)gv.N + RPI - 1) / RPI;
-    hipLaunchKernelGGL((k_qgemv_ln<MR, LPR, 1>), dim3((int)((waves + 3) / 4)), dim3(256), 0, s, in, gv);
+    const long blocks1 = ((long)gv.N + RPI * 4 - 1) / (RPI * 4);
+    hipLaunchKernelGGL((k_qgemv_ln<MR, DMAX, 1>), dim3((int)blocks1), dim3(256), 0, s, in, gv);
   }
   return hipGetLastError();
 }
 
 template <int MR>
-hipError_t launch_lpr(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
-  // lanes per weight row: as many 16-byte chunks as the row has, up to 64
-  // (K <= 1024 then leaves each lane at most two chunks)
-  const int chunks = gv.K / 16;
-  if (chunks >= 64) return launch_u<MR, 64>(in, gv, s);
-  if (chunks >= 32) return launch_u<MR, 32>(in, gv, s);
-  if (chunks >= 16) return launch_u<MR, 16>(in, gv, s);
-  if (chunks >= 8) return launch_u<MR, 8>(in, gv, s);
-  return launch_u<MR, 4>(in, gv, s);
+hipError_t launch_d(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
+  switch (row_class(gv.K)) {
+    case 64: return launch_u<MR, 64>(in, gv, s);
+    case 128: return launch_u<MR, 128>(in, gv, s);
+    case 256: return launch_u<MR, 256>(in, gv, s);
+    case 384: return launch_u<MR, 384>(in, gv, s);
+    case 512: return launch_u<MR, 512>(in, gv, s);
+    default: return launch_u<MR, 1024>(in, gv, s);
+  }
 }
 
 }  // namespace
@@ -234,10 +175,10 @@ int fused_slots_per_row() { return kSlots; }
 hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
   // K chunks per lane must be at most two: K <= 32 * LPR with LPR <= 64
   if (gv.R < 1 || gv.R > kRows || gv.K > kMaxRowLen || gv.K % 16) return hipErrorInvalidValue;
-  if (gv.R == 1) return launch_lpr<1>(in, gv, s);
-  if (gv.R == 2) return launch_lpr<2>(in, gv, s);
-  if (gv.R <= 4) return launch_lpr<4>(in, gv, s);
-  return launch_lpr<8>(in, gv, s);
+  if (gv.R == 1) return launch_d<1>(in, gv, s);
+  if (gv.R == 2) return launch_d<2>(in, gv, s);
+  if (gv.R <= 4) return launch_d<4>(in, gv, s);
+  return launch_d<8>(in, gv, s);
 }
 
 hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s) {

@@ -93,6 +93,7 @@ struct FusedIn {           // how a kernel obtains its int8 input rows
   const float* c_emb;
   const float* pe;
   int V;
+  int S_pos;               // > 0: embedding position = row % S_pos (encoder); 0: the decode step
   int do_ln;               // LayerNorm before quantization
   const float* g;
   const float* b;
@@ -114,8 +115,73 @@ struct FusedGemv {         // a linear layer over the prepared rows, and greedy 
   int32_t* finished;
   int32_t* out_len;
   int T, stop_at_eos, eos, pad;
+  int32_t* zero_acc;       // commit: cleared after the step (or null)
+  int zero_n;
 };
 hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s);
+
+// Decoder step in 3 kernels per layer for at most 2 rows (decode_step.hip).
+struct StepIn {            // the sublayer input rows of a step kernel
+  int t;                   // decode step (embedding position)
+  int embed;               // rows = embeddings of tok[]
+  const int32_t* tok;
+  const int8_t* E;
+  const float* c_emb;
+  const float* pe;
+  int V;
+  const float* x_in;       // residual rows [R, d]
+  float* x_out;            // block 0 stores the updated rows here (or null)
+  const int32_t* acc;      // pending update: x <- fma(gamma, x, fma(acc, scale, bias)), or null
+  const float* scale;
+  const float* bias;
+  float gamma;
+  const float* post_g;     // post-LN: LayerNorm of the updated residual stream (or null)
+  const float* post_b;
+  const float* pre_g;      // pre-LN: LayerNorm of the sublayer input (or null)
+  const float* pre_b;
+  float eps;
+  float inv_s;             // 1 / input scale of the consuming layer
+  int32_t* zero_acc;       // block 0 clears this accumulator (its consumer has finished)
+  int zero_n;
+};
+struct StepAttn {
+  int R, d, dh, T, S, t;
+  const int8_t* W;         // QKV [3d, d] (self) or Q [d, d] (cross)
+  const float* scale;
+  const float* bias;
+  const int8_t* Wo;        // output projection [d, d]
+  int8_t* kcache;
+  int8_t* vcache;
+  const int8_t* kv;        // cross keys|values [R][S][2d]
+  const int32_t* len;
+  float c_qk, c_pv;
+  int32_t* acc_out;        // [R, d] int32, zero on entry
+};
+struct StepFfn {
+  int R, d, F;
+  const int8_t* W1;
+  const float* scale1;
+  const float* bias1;
+  const int8_t* W2;        // [d, F]
+  int32_t* acc_out;
+};
+struct StepLogits {
+  int R, d, V;
+  const int8_t* E;
+  const float* c_out;
+  float* logits;           // [R, V] or null
+  unsigned long long* slots;
+  int nslots;
+};
+bool step_path_fits(int R, int d, int dh, int F, int T, int S);
+hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s);
+hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s);
+hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s);
+// Small-M GEMM (M <= 64, K <= 1024) on 16x16x64 matrix cores; with `in` the
+// rows are prepared (embedding / LayerNorm / quantization) in its prologue.
+bool qgemm_small_fits(int M, int K);
+hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
+                              const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s);
 hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s);
 int fused_slots_per_row();
 
@@ -206,11 +272,13 @@ struct mnmt_session {
   int8_t* enc_qkv = nullptr;
   int8_t* enc_h = nullptr;
   int8_t* enc_out = nullptr;
+  float* enc_x2 = nullptr;  // second encoder residual buffer (post-LN ping-pong)
   float* logits = nullptr;  // shares memory with the encoder scratch
   std::vector<int8_t*> cross_kv;
   float* dec_x = nullptr;
   float* dec_x2 = nullptr;  // second residual buffer (post-LN ping-pong)
   unsigned long long* fslots = nullptr;  // spread arg-max slots [8][fused_slots_per_row()]
+  int32_t* step_acc = nullptr;           // decode-step accumulators [3][2][d] int32
   int8_t* dec_a = nullptr;
   int8_t* dec_qkv = nullptr;
   int8_t* dec_q = nullptr;

@@ -88,6 +88,7 @@ __global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, i
 __global__ __launch_bounds__(64) void k_attn_enc(const int8_t* __restrict__ qkv, const int32_t* __restrict__ len,
                                                  int S, int d, int dh, float c_qk, float c_pv,
                                                  int8_t* __restrict__ ctx) {
+  __shared__ AttnLds sh;
   const int s = blockIdx.x, hd = blockIdx.y, b = blockIdx.z;
   int n = len[b];
   n = n < 1 ? 1 : (n > S ? S : n);
@@ -95,7 +96,7 @@ __global__ __launch_bounds__(64) void k_attn_enc(const int8_t* __restrict__ qkv,
   const int8_t* q = base + (size_t)s * 3 * d + hd * dh;
   auto key = [&](int t) { return base + (size_t)t * 3 * d + d + hd * dh; };
   auto val = [&](int t) { return base + (size_t)t * 3 * d + 2 * d + hd * dh; };
-  attend_wave(q, n, dh, key, val, c_qk, c_pv, ctx + ((size_t)b * S + s) * d + hd * dh);
+  attend_wave(q, n, dh, key, val, c_qk, c_pv, ctx + ((size_t)b * S + s) * d + hd * dh, sh);
 }
 
 // Decoder self-attention at position t = *step: block = one wave = (head, row).
@@ -103,6 +104,7 @@ __global__ __launch_bounds__(64) void k_attn_dec_self(const int8_t* __restrict__
                                                       const int* __restrict__ step, int8_t* __restrict__ kcache,
                                                       int8_t* __restrict__ vcache, const int32_t* __restrict__ hist,
                                                       float c_qk, float c_pv, int8_t* __restrict__ ctx) {
+  __shared__ AttnLds sh;
   const int hd = blockIdx.x, r = blockIdx.y;
   const int lane = threadIdx.x;
   int t = *step;
@@ -127,7 +129,7 @@ __global__ __launch_bounds__(64) void k_attn_dec_self(const int8_t* __restrict__
     const int src = hr ? hr[tp] : r;
     return (const int8_t*)vcache + ((size_t)src * T + tp) * d + hd * dh;
   };
-  attend_wave(row + hd * dh, t + 1, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh);
+  attend_wave(row + hd * dh, t + 1, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh, sh);
 }
 
 // Decoder cross-attention: row r attends over the source of sentence r / W.
@@ -135,6 +137,7 @@ __global__ __launch_bounds__(64) void k_attn_dec_cross(const int8_t* __restrict_
                                                        const int8_t* __restrict__ kv, int S,
                                                        const int32_t* __restrict__ len, float c_qk, float c_pv,
                                                        int8_t* __restrict__ ctx) {
+  __shared__ AttnLds sh;
   const int hd = blockIdx.x, r = blockIdx.y;
   const int b = r / W;
   int n = len[b];
@@ -142,7 +145,7 @@ __global__ __launch_bounds__(64) void k_attn_dec_cross(const int8_t* __restrict_
   const int8_t* base = kv + (size_t)b * S * 2 * d;
   auto key = [&](int t) { return base + (size_t)t * 2 * d + hd * dh; };
   auto val = [&](int t) { return base + (size_t)t * 2 * d + d + hd * dh; };
-  attend_wave(q + (size_t)r * d + hd * dh, n, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh);
+  attend_wave(q + (size_t)r * d + hd * dh, n, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh, sh);
 }
 
 // ---------------------------------------------------------------------------

@@ -13,7 +13,7 @@
 //    slabs staged in LDS; each of the 4 waves owns a tile of 32x32 fragments.
 // Integer accumulation is exact, so neither kernel's order matters; the fp32
 // epilogue is the same single expression in both.
-#include "canon.hpp"
+#include "blocks.hpp"
 #include "internal.h"
 
 namespace mnmt {
@@ -21,14 +21,6 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
-
-__device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
-  acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
-  acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
-  acc = __builtin_amdgcn_sdot4(a.z, b.z, acc, false);
-  acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
-  return acc;
-}
 
 // The fused epilogue of one output element (row m, column n).
 __device__ __forceinline__ void epilogue_store(const EpiArgs& e, int m, int n, int acc, const float* scale,
@@ -256,6 +248,64 @@ __global__ __launch_bounds__(256) void k_qgemm(const int8_t* __restrict__ X, int
     }
 }
 
+// ---------------------------------------------------------------------------
+// qgemm_small: M <= 64, K <= 1024 (the batch-1 encoder).  A 32x32 output tile
+// per block, one 16x16 tile per wave on v_mfma_i32_16x16x64_i8.  Each lane's
+// operand is 16 contiguous K bytes of one row, so weight fragments are loaded
+// straight from global memory, all of K at once (a single round trip).  The
+// input rows come from global int8 X or, with LN, from prepare_rows
+// (embedding / LayerNorm / quantization of fp32 rows) into LDS.
+constexpr int kSmallMaxK = 1024;
+
+template <bool LN, int KMAX>  // K <= KMAX
+__global__ __launch_bounds__(256) void k_qgemm_small(FusedIn in, const int8_t* __restrict__ X, int ldx,
+                                                     const int8_t* __restrict__ W, int M, int K, int N,
+                                                     const float* __restrict__ scale, const float* __restrict__ bias,
+                                                     EpiArgs e) {
+  constexpr int NK = (KMAX + 63) / 64;
+  __shared__ __attribute__((aligned(16))) int8_t As[LN ? 32 * (KMAX + 16) : 16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
+  const int nk = K / 64;
+  const int col = n0 + 16 * wn + (lane & 15);
+  const int koff = 16 * (lane >> 4);
+  v4i bf[NK];
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk)
+    bf[kk] = (kk < nk && col < N) ? *(const v4i*)(W + (size_t)col * K + kk * 64 + koff) : v4i{0, 0, 0, 0};
+  const int arow = m0 + 16 * wm + (lane & 15);
+  v4i acc = {0, 0, 0, 0};
+  if (LN) {
+    const int KP = K + 16;
+    const int rows = M - m0 < 32 ? M - m0 : 32;
+    prepare_rows<(KMAX + 63) / 64>(in, rows, m0, K, 0, As, KP, blockIdx.x == 0);
+    __syncthreads();
+    const int lr = 16 * wm + (lane & 15);
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      if (kk < nk) {
+        const v4i a = lr < rows ? *(const v4i*)(As + lr * KP + kk * 64 + koff) : v4i{0, 0, 0, 0};
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bf[kk], acc, 0, 0, 0);
+      }
+    }
+  } else {
+    v4i af[NK];
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk)
+      af[kk] = (kk < nk && arow < M) ? *(const v4i*)(X + (size_t)arow * ldx + kk * 64 + koff) : v4i{0, 0, 0, 0};
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk)
+      if (kk < nk) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[kk], bf[kk], acc, 0, 0, 0);
+  }
+  // 16x16 fragment: element i of lane l sits at row 4*(l/16) + i, column l%16
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = m0 + 16 * wm + 4 * (lane >> 4) + i;
+    if (row < M && col < N) epilogue_store(e, row, col, acc[i], scale, bias);
+  }
+}
+
 template <int BM, int BN, int WAVES_M>
 hipError_t gemm_launch(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
                        int K, int N, const EpiArgs& e, hipStream_t s) {
@@ -265,6 +315,30 @@ hipError_t gemm_launch(const int8_t* X, int ldx, const int8_t* W, const float* s
 }
 
 }  // namespace
+
+bool qgemm_small_fits(int M, int K) { return M >= 1 && M <= 64 && K <= kSmallMaxK && K % 64 == 0; }
+
+hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
+                              const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s) {
+  if (!qgemm_small_fits(M, K) || (in && K > kMaxRowLen)) return hipErrorInvalidValue;
+  dim3 grid((N + 31) / 32, (M + 31) / 32);
+  const FusedIn none{};
+#define MNMT_SMALL(KM)                                                                                      \
+  if (in)                                                                                                   \
+    hipLaunchKernelGGL((k_qgemm_small<true, KM>), grid, dim3(256), 0, s, *in, X, ldx, W, M, K, N, scale, bias, e); \
+  else                                                                                                      \
+    hipLaunchKernelGGL((k_qgemm_small<false, KM>), grid, dim3(256), 0, s, none, X, ldx, W, M, K, N, scale, bias, e);
+  switch (row_class(K)) {
+    case 64: MNMT_SMALL(64) break;
+    case 128: MNMT_SMALL(128) break;
+    case 256: MNMT_SMALL(256) break;
+    case 384: MNMT_SMALL(384) break;
+    case 512: MNMT_SMALL(512) break;
+    default: MNMT_SMALL(1024) break;
+  }
+#undef MNMT_SMALL
+  return hipGetLastError();
+}
 
 hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
                           int K, int N, const EpiArgs& e, hipStream_t s) {
@@ -276,6 +350,7 @@ hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float
     return gemv_lpr<8>(X, ldx, W, scale, bias, M, K, N, e, s);
   }
   if (e.kind == EPI_LOGITS_ARGMAX) return hipErrorInvalidValue;  // arg-max fusion is a batch-1 path
+  if (qgemm_small_fits(M, K)) return launch_qgemm_small(nullptr, X, ldx, W, scale, bias, M, K, N, e, s);
   if (M <= 32) return gemm_launch<32, 128, 1>(X, ldx, W, scale, bias, M, K, N, e, s);
   if (M <= 64) return gemm_launch<64, 128, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
   return gemm_launch<128, 128, 2>(X, ldx, W, scale, bias, M, K, N, e, s);

@@ -27,7 +27,7 @@ struct Bump {
 };
 
 struct Plan {
-  size_t src, len, region, enc_x, enc_a, enc_qkv, enc_h, enc_out, logits;
+  size_t src, len, region, enc_x, enc_x2, enc_a, enc_qkv, enc_h, enc_out, logits;
   std::vector<size_t> cross_kv, kc, vc;
   size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots;
   size_t cur_tok, step, slots, out_tok, finished, out_len, lp;
@@ -61,6 +61,7 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.enc_qkv = r.take(BS * 3 * d);
   p.enc_h = r.take(BS * F);
   p.enc_out = r.take(BS * d);
+  p.enc_x2 = r.take(4 * BS * d);
   const size_t enc_bytes = r.off;
   const size_t logit_bytes = 4 * R * V;
   p.region = b.take(enc_bytes > logit_bytes ? enc_bytes : logit_bytes);
@@ -69,11 +70,13 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.enc_qkv += p.region;
   p.enc_h += p.region;
   p.enc_out += p.region;
+  p.enc_x2 += p.region;
   p.logits = p.region;
   for (size_t l = 0; l < Ld; ++l) p.cross_kv.push_back(b.take(BS * 2 * d));
   p.dec_x = b.take(4 * R * d);
   p.dec_x2 = b.take(4 * R * d);
-  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row());
+  // fused arg-max slots, then the decode-step int32 accumulators (cleared together)
+  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row() + 4 * 3 * 2 * d);
   p.dec_a = b.take(R * d);
   p.dec_qkv = b.take(R * 3 * d);
   p.dec_q = b.take(R * d);
@@ -119,6 +122,64 @@ int qlin(const LinearDev& L, const int8_t* X, int M, int kind, void* out, float 
   return MNMT_OK;
 }
 
+// Encoder for at most 64 rows (the batch-1 latency path): the embedding and
+// every LayerNorm run in the prologue of the matrix-core GEMM that consumes
+// them; per layer [LN + QKV] [attention] [W_o + residual] [LN + W1 + ReLU]
+// [W2 + residual].  Post-LN models alternate between two residual buffers.
+int run_encoder_small(mnmt_session* S, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  const int d = m->info.d_model, rows = S->B * S->S;
+  const bool post = m->info.ln_post;
+  float* xc = S->enc_x;
+  float* xo = S->enc_x2;
+  auto input = [&](bool embed, bool do_ln, const LnDev& ln, float inv_s, bool write_norm) {
+    FusedIn in{};
+    in.x = xc;
+    in.embed = embed;
+    in.tok = S->src;
+    in.E = m->E;
+    in.c_emb = m->c_emb;
+    in.pe = m->pe;
+    in.V = m->info.vocab;
+    in.S_pos = S->S;
+    in.do_ln = do_ln;
+    in.g = ln.g;
+    in.b = ln.b;
+    in.eps = m->info.ln_eps;
+    in.inv_s = inv_s;
+    if (embed) {
+      in.x_out = xc;
+      in.wb_input = 1;
+    } else if (write_norm) {
+      in.x_out = xo;
+    }
+    return in;
+  };
+  auto small = [&](const FusedIn* in, const int8_t* X, const LinearDev& L, int kind, void* out, float gamma) {
+    EpiArgs e{kind, out, L.N, gamma, nullptr};
+    return launch_qgemm_small(in, X, L.K, L.w, L.scale, L.bias, rows, L.K, L.N, e, s);
+  };
+  for (size_t l = 0; l < m->enc.size(); ++l) {
+    const LayerDev& L = m->enc[l];
+    const bool embed = l == 0;
+    FusedIn in = input(embed, post ? !embed : true, post ? (embed ? L.sa_ln : m->enc[l - 1].ff_ln) : L.sa_ln,
+                       L.qkv.inv_in, post && !embed);
+    LAUNCH(small(&in, nullptr, L.qkv, MNMT_EPI_I8, S->enc_qkv, 1.f));
+    if (post && !embed) std::swap(xc, xo);
+    LAUNCH(launch_attn_enc(S->enc_qkv, S->len, S->B, S->S, d, m->info.n_heads, L.sa_cqk, L.sa_cpv, S->enc_a, s));
+    LAUNCH(small(nullptr, S->enc_a, L.o, MNMT_EPI_F32_RESID, xc, L.sa_gamma));
+    in = input(false, true, post ? L.sa_ln : L.ff_ln, L.w1.inv_in, post);
+    LAUNCH(small(&in, nullptr, L.w1, MNMT_EPI_I8_RELU, S->enc_h, 1.f));
+    if (post) std::swap(xc, xo);
+    LAUNCH(small(nullptr, S->enc_h, L.w2, MNMT_EPI_F32_RESID, xc, L.ff_gamma));
+  }
+  const LnDev& lnf = post ? m->enc.back().ff_ln : m->enc_ln;
+  LAUNCH(launch_ln_quant(xc, rows, d, 1, lnf.g, lnf.b, m->info.ln_eps, m->inv_enc, S->enc_out, nullptr, s));
+  for (size_t l = 0; l < m->dec.size(); ++l)
+    LAUNCH(small(nullptr, S->enc_out, m->dec[l].ckv, MNMT_EPI_I8, S->cross_kv[l], 1.f));
+  return MNMT_OK;
+}
+
 // Encoder over the session's current batch (rows = B * S, padded rows are
 // computed and ignored), then every decoder layer's cross keys/values.
 int run_encoder(mnmt_session* S, hipStream_t s) {
@@ -126,6 +187,7 @@ int run_encoder(mnmt_session* S, hipStream_t s) {
   const int d = m->info.d_model, rows = S->B * S->S;
   const bool post = m->info.ln_post;
   const float eps = m->info.ln_eps;
+  if (qgemm_small_fits(rows, d) && qgemm_small_fits(rows, m->info.d_ffn)) return run_encoder_small(S, s);
   LAUNCH(launch_embed(S->src, rows, S->S, nullptr, m->E, m->c_emb, m->pe, d, m->info.vocab, S->enc_x, s));
   const LayerDev& L0 = m->enc[0];
   LAUNCH(launch_ln_quant(S->enc_x, rows, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->enc_a, nullptr, s));
@@ -299,6 +361,165 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
   return MNMT_OK;
 }
 
+// Greedy step for at most 2 rows in 3 kernels per layer (decode_step.hip):
+// [attention block, self] [attention block, cross] [FFN block] per layer,
+// then [output projection + arg-max] and [commit].  Each kernel applies the
+// previous sublayer's residual update in its prologue; the three int32
+// accumulators (W_o, W_oc, W2 partial sums) are cleared by the kernel after
+// their consumer, and the residual rows alternate between two buffers.
+int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
+  const bool post = m->info.ln_post;
+  int32_t* acc_o = S->step_acc;
+  int32_t* acc_oc = S->step_acc + 2 * d;
+  int32_t* acc_w2 = S->step_acc + 4 * d;
+  const int nacc = R * d;
+  float* xa = S->dec_x;
+  float* xb = S->dec_x2;
+  auto base = [&](float inv_s) {
+    StepIn in{};
+    in.t = t;
+    in.tok = S->cur_tok;
+    in.E = m->E;
+    in.c_emb = m->c_emb;
+    in.pe = m->pe;
+    in.V = m->info.vocab;
+    in.x_in = xa;
+    in.x_out = xb;
+    in.eps = m->info.ln_eps;
+    in.inv_s = inv_s;
+    return in;
+  };
+  auto pending = [&](StepIn& in, const int32_t* acc, const LinearDev& L, float gamma, const LnDev& post_ln) {
+    in.acc = acc;
+    in.scale = L.scale;
+    in.bias = L.bias;
+    in.gamma = gamma;
+    if (post) {
+      in.post_g = post_ln.g;
+      in.post_b = post_ln.b;
+    }
+  };
+  auto pre = [&](StepIn& in, const LnDev& ln) {
+    if (!post) {
+      in.pre_g = ln.g;
+      in.pre_b = ln.b;
+    }
+  };
+  auto attn = [&](const LayerDev& L, bool self, int32_t* acc_out) {
+    StepAttn at{};
+    at.R = R;
+    at.d = d;
+    at.dh = m->dh;
+    at.T = T;
+    at.S = S->S;
+    at.t = t;
+    const LinearDev& P = self ? L.qkv : L.cq;
+    at.W = P.w;
+    at.scale = P.scale;
+    at.bias = P.bias;
+    at.Wo = self ? L.o.w : L.co.w;
+    at.len = S->len;
+    at.c_qk = self ? L.sa_cqk : L.ca_cqk;
+    at.c_pv = self ? L.sa_cpv : L.ca_cpv;
+    at.acc_out = acc_out;
+    return at;
+  };
+  for (size_t l = 0; l < m->dec.size(); ++l) {
+    const LayerDev& L = m->dec[l];
+    {  // self-attention block
+      StepIn in = base(L.qkv.inv_in);
+      if (l == 0) {
+        in.embed = 1;
+      } else {
+        const LayerDev& P = m->dec[l - 1];
+        pending(in, acc_w2, P.w2, P.ff_gamma, P.ff_ln);
+        in.zero_acc = acc_oc;
+        in.zero_n = nacc;
+      }
+      pre(in, L.sa_ln);
+      StepAttn at = attn(L, true, acc_o);
+      at.kcache = S->kcache[l];
+      at.vcache = S->vcache[l];
+      LAUNCH(launch_step_attn(in, at, 1, h, s));
+      std::swap(xa, xb);
+    }
+    {  // cross-attention block
+      StepIn in = base(L.cq.inv_in);
+      pending(in, acc_o, L.o, L.sa_gamma, L.sa_ln);
+      pre(in, L.ca_ln);
+      in.zero_acc = acc_w2;
+      in.zero_n = nacc;
+      StepAttn at = attn(L, false, acc_oc);
+      at.kv = S->cross_kv[l];
+      LAUNCH(launch_step_attn(in, at, 0, h, s));
+      std::swap(xa, xb);
+    }
+    {  // FFN block
+      StepIn in = base(L.w1.inv_in);
+      pending(in, acc_oc, L.co, L.ca_gamma, L.ca_ln);
+      pre(in, L.ff_ln);
+      in.zero_acc = acc_o;
+      in.zero_n = nacc;
+      StepFfn f{};
+      f.R = R;
+      f.d = d;
+      f.F = L.w1.N;
+      f.W1 = L.w1.w;
+      f.scale1 = L.w1.scale;
+      f.bias1 = L.w1.bias;
+      f.W2 = L.w2.w;
+      f.acc_out = acc_w2;
+      LAUNCH(launch_step_ffn(in, f, s));
+      std::swap(xa, xb);
+    }
+  }
+  const LayerDev& last = m->dec.back();
+  StepIn in = base(m->inv_fin);
+  in.x_out = nullptr;
+  pending(in, acc_w2, last.w2, last.ff_gamma, last.ff_ln);
+  pre(in, m->dec_ln);
+  in.zero_acc = acc_oc;
+  in.zero_n = nacc;
+  StepLogits g{};
+  g.R = R;
+  g.d = d;
+  g.V = m->info.vocab;
+  g.E = m->E;
+  g.c_out = m->c_out;
+  g.logits = logits_out;
+  g.slots = S->fslots;
+  g.nslots = fused_slots_per_row();
+  LAUNCH(launch_step_logits(in, g, s));
+  FusedGemv gv{};
+  gv.R = R;
+  gv.t = t;
+  gv.slots = S->fslots;
+  gv.step = S->step;
+  gv.out_tok = S->out_tok;
+  gv.cur_tok = S->cur_tok;
+  gv.finished = S->finished;
+  gv.out_len = S->out_len;
+  gv.T = T;
+  gv.stop_at_eos = stop_at_eos;
+  gv.eos = m->info.eos_id;
+  gv.pad = m->info.pad_id;
+  gv.zero_acc = acc_w2;
+  gv.zero_n = nacc;
+  LAUNCH(launch_greedy_commit_slots(gv, s));
+  return MNMT_OK;
+}
+
+// The greedy step for R rows on the fastest path that fits.
+int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  if (step_path_fits(R, m->info.d_model, m->dh, m->info.d_ffn, S->cfg.max_tgt_len, S->S))
+    return greedy_step_v3(S, R, t, stop_at_eos, logits_out, s);
+  if (R <= 8) return greedy_step_fused(S, R, t, stop_at_eos, logits_out, s);
+  return greedy_step(S, R, stop_at_eos, logits_out, s);
+}
+
 int beam_step(mnmt_session* S, int R, int W, hipStream_t s) {
   const mnmt_model* m = S->m;
   int rc = run_decoder_layers(S, R, W, true, s);
@@ -319,11 +540,9 @@ int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
   if (sc.beam == 1) {
     const int R = S->B;
     LAUNCH(launch_greedy_reset(S->slots, R, sc.max_steps, S->cur_tok, S->finished, S->out_len, S->step,
-                               m->info.bos_id, S->fslots, 8 * fused_slots_per_row(), s));
+                               m->info.bos_id, S->fslots, 8 * fused_slots_per_row() + 3 * 2 * m->info.d_model / 2, s));
     for (int t = 0; t < sc.max_steps; ++t)
-      if ((rc = R <= 8 ? greedy_step_fused(S, R, t, sc.stop_at_eos, nullptr, s)
-                       : greedy_step(S, R, sc.stop_at_eos, nullptr, s)))
-        return rc;
+      if ((rc = greedy_step_any(S, R, t, sc.stop_at_eos, nullptr, s))) return rc;
   } else {
     const int R = S->B * sc.beam;
     LAUNCH(launch_beam_reset(S->beam, S->step, s));
@@ -390,11 +609,13 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->enc_qkv = (int8_t*)at(p.enc_qkv);
   S->enc_h = (int8_t*)at(p.enc_h);
   S->enc_out = (int8_t*)at(p.enc_out);
+  S->enc_x2 = (float*)at(p.enc_x2);
   S->logits = (float*)at(p.logits);
   for (size_t l = 0; l < p.cross_kv.size(); ++l) S->cross_kv.push_back((int8_t*)at(p.cross_kv[l]));
   S->dec_x = (float*)at(p.dec_x);
   S->dec_x2 = (float*)at(p.dec_x2);
   S->fslots = (unsigned long long*)at(p.fslots);
+  S->step_acc = (int32_t*)(S->fslots + 8 * fused_slots_per_row());
   S->dec_a = (int8_t*)at(p.dec_a);
   S->dec_qkv = (int8_t*)at(p.dec_qkv);
   S->dec_q = (int8_t*)at(p.dec_q);
@@ -474,7 +695,7 @@ extern "C" int mnmt_encode(mnmt_session* S, const int32_t* d_src, const int32_t*
   if ((rc = run_encoder(S, s))) return rc;
   const mnmt_model* m = S->m;
   LAUNCH(launch_greedy_reset(S->slots, B, S->cfg.max_tgt_len, S->cur_tok, S->finished, S->out_len, S->step,
-                             m->info.bos_id, S->fslots, 8 * fused_slots_per_row(), s));
+                             m->info.bos_id, S->fslots, 8 * fused_slots_per_row() + 3 * 2 * m->info.d_model / 2, s));
   S->encoded = true;
   S->host_step = 0;
   return MNMT_OK;
@@ -491,8 +712,7 @@ extern "C" int mnmt_decode_step(mnmt_session* S, const int32_t* d_prev, int32_t*
   hipStream_t s = as_stream(stream);
   const int R = S->B;
   if (d_prev) LAUNCH(launch_copy_i32(d_prev, S->cur_tok, R, s));
-  if ((rc = R <= 8 ? greedy_step_fused(S, R, S->host_step, 0, d_logits, s) : greedy_step(S, R, 0, d_logits, s)))
-    return rc;
+  if ((rc = greedy_step_any(S, R, S->host_step, 0, d_logits, s))) return rc;
   LAUNCH(launch_copy_i32(S->cur_tok, d_next, R, s));
   ++S->host_step;
   return MNMT_OK;

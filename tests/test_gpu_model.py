@@ -106,6 +106,26 @@ def test_small_models_batched_greedy(torch_dev):
         _greedy_check(torch, dev, cfg, src, lens, 10, stop_at_eos=True, check_logits=False)
 
 
+def test_one_and_two_row_greedy(torch_dev):
+    # 1 or 2 rows take the three-kernels-per-layer decoder step
+    torch, dev = torch_dev
+    for cfg in (SMALL_PRE, SMALL_POST, DIVERSE):
+        for B in (1, 2):
+            src, lens = G.make_sources(cfg.vocab, B, (3, 12), seed=24 + B, s_max=12)
+            _greedy_check(torch, dev, cfg, src, lens, 10)
+            _greedy_check(torch, dev, cfg, src, lens, 10, stop_at_eos=True, check_logits=False)
+
+
+def test_two_row_greedy_longest_sequences(torch_dev):
+    # 128 source positions and 128 target steps: the longest attention of the
+    # 2-row step; one position more moves both lengths to the general path
+    torch, dev = torch_dev
+    src, lens = G.make_sources(SMALL_POST.vocab, 2, [128, 77], seed=26, s_max=128)
+    _greedy_check(torch, dev, SMALL_POST, src, lens, 128)
+    src, lens = G.make_sources(SMALL_POST.vocab, 2, [129, 5], seed=27, s_max=129)
+    _greedy_check(torch, dev, SMALL_POST, src, lens, 129, check_logits=False)
+
+
 def test_greedy_batch_above_gemv_limit(torch_dev):
     # 12 rows: the output projection runs on matrix cores, arg-max separately
     torch, dev = torch_dev
