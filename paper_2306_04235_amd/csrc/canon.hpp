@@ -13,22 +13,66 @@
 
 namespace mnmt {
 
+// The canonical butterfly without the LDS crossbar.  Step `off` gives lane i
+// op(x_i, x_{i^off}).  The 32 and 16 steps use gfx950's permlane swaps: after
+// v_permlane32_swap of a value with itself the two results hold, in every
+// lane, x_i and x_{i^32} (in some order), and likewise x_i and x_{i^16} after
+// v_permlane16_swap.  After those steps a lane's value depends only on i mod
+// 16, so the 8, 4, 2, 1 steps can take the partner from a rotation of the
+// lane's 16-lane row (DPP row_ror), whose source lane is congruent to i^off
+// modulo 2 off.  op is commutative (fp32 add and max, integer add and max),
+// so every lane computes exactly the value of the xor butterfly.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xf, 0xf, false);
+}
+constexpr int kRowRor8 = 0x128, kRowRor4 = 0x124, kRowRor2 = 0x122, kRowRor1 = 0x121;
+
+// Partner values of steps 32 and 16: returns {a, b} with {a, b} = {x_i, x_{i^off}}.
+__device__ __forceinline__ void swap32(uint32_t v, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  a = r[0];
+  b = r[1];
+}
+__device__ __forceinline__ void swap16(uint32_t v, uint32_t& a, uint32_t& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  a = r[0];
+  b = r[1];
+}
+
+template <class Op>
+__device__ __forceinline__ float butterfly_f32(float x, Op op) {
+  uint32_t a, b;
+  swap32(__float_as_uint(x), a, b);
+  x = op(__uint_as_float(a), __uint_as_float(b));
+  swap16(__float_as_uint(x), a, b);
+  x = op(__uint_as_float(a), __uint_as_float(b));
+  x = op(x, __uint_as_float(dpp_u32<kRowRor8>(__float_as_uint(x))));
+  x = op(x, __uint_as_float(dpp_u32<kRowRor4>(__float_as_uint(x))));
+  x = op(x, __uint_as_float(dpp_u32<kRowRor2>(__float_as_uint(x))));
+  x = op(x, __uint_as_float(dpp_u32<kRowRor1>(__float_as_uint(x))));
+  return x;
+}
+
 // Sum of the 64 lanes' partials in the canonical butterfly.
 __device__ __forceinline__ float wave_sum(float p) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) p = p + __shfl_xor(p, off, 64);
-  return p;
+  return butterfly_f32(p, [](float u, float v) { return u + v; });
 }
 
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-  return v;
+  return butterfly_f32(v, [](float u, float w) { return fmaxf(u, w); });
 }
 
 __device__ __forceinline__ int wave_isum(int v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  uint32_t a, b;
+  swap32((uint32_t)v, a, b);
+  v = (int)(a + b);
+  swap16((uint32_t)v, a, b);
+  v = (int)(a + b);
+  v += (int)dpp_u32<kRowRor8>((uint32_t)v);
+  v += (int)dpp_u32<kRowRor4>((uint32_t)v);
+  v += (int)dpp_u32<kRowRor2>((uint32_t)v);
+  v += (int)dpp_u32<kRowRor1>((uint32_t)v);
   return v;
 }
 
@@ -97,12 +141,19 @@ __device__ __forceinline__ int unpack_index(unsigned long long key) {
 }
 
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const unsigned long long o = __shfl_xor(v, off, 64);
-    v = o > v ? o : v;
-  }
+  auto mx = [](unsigned long long u, unsigned long long w) { return u > w ? u : w; };
+  auto join = [](uint32_t lo, uint32_t hi) { return ((unsigned long long)hi << 32) | lo; };
+  uint32_t a0, b0, a1, b1;
+  swap32((uint32_t)v, a0, b0);
+  swap32((uint32_t)(v >> 32), a1, b1);
+  v = mx(join(a0, a1), join(b0, b1));
+  swap16((uint32_t)v, a0, b0);
+  swap16((uint32_t)(v >> 32), a1, b1);
+  v = mx(join(a0, a1), join(b0, b1));
+  v = mx(v, join(dpp_u32<kRowRor8>((uint32_t)v), dpp_u32<kRowRor8>((uint32_t)(v >> 32))));
+  v = mx(v, join(dpp_u32<kRowRor4>((uint32_t)v), dpp_u32<kRowRor4>((uint32_t)(v >> 32))));
+  v = mx(v, join(dpp_u32<kRowRor2>((uint32_t)v), dpp_u32<kRowRor2>((uint32_t)(v >> 32))));
+  v = mx(v, join(dpp_u32<kRowRor1>((uint32_t)v), dpp_u32<kRowRor1>((uint32_t)(v >> 32))));
   return v;
 }
-
 }  // namespace mnmt

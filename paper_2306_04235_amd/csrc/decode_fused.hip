@@ -118,7 +118,8 @@ __global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
   }
 }
 
-__global__ void k_greedy_commit_slots(FusedGemv gv) {
+__global__ __launch_bounds__(256) void k_greedy_commit_slots(FusedGemv gv) {
+  __shared__ int next_tok[kRows];
   const int t = gv.t;
   for (int m = threadIdx.x; m < gv.R; m += blockDim.x) {
     unsigned long long b = 0ull;
@@ -135,9 +136,21 @@ __global__ void k_greedy_commit_slots(FusedGemv gv) {
       gv.out_len[m] = t + 1;
     }
     gv.cur_tok[m] = fin ? gv.pad : tok;
+    next_tok[m] = fin ? gv.pad : tok;
   }
   for (int i = threadIdx.x; gv.zero_acc && i < gv.zero_n; i += blockDim.x) gv.zero_acc[i] = 0;
   if (threadIdx.x == 0) *gv.step = t + 1;
+  // the next step's input rows: embedding of the new tokens at position t + 1
+  if (gv.emb_out && t + 1 < gv.P) {
+    __syncthreads();
+    const int d = gv.d;
+    for (int e = threadIdx.x; e < gv.R * d; e += blockDim.x) {
+      const int m = e / d, i = e % d;
+      int tok = next_tok[m];
+      tok = tok < 0 ? 0 : (tok >= gv.V ? gv.V - 1 : tok);
+      gv.emb_out[e] = fmaf((float)gv.E[(size_t)tok * d + i], gv.c_emb[tok], gv.pe[(size_t)(t + 1) * d + i]);
+    }
+  }
 }
 
 // Row groups per wave: large layers (the output projection) get 8 so that
@@ -182,7 +195,8 @@ hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s
 }
 
 hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s) {
-  hipLaunchKernelGGL(k_greedy_commit_slots, dim3(1), dim3(64), 0, s, gv);
+  if (gv.R > kRows) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_greedy_commit_slots, dim3(1), dim3(256), 0, s, gv);
   return hipGetLastError();
 }
 

@@ -20,6 +20,11 @@
 // consumer has finished.  This is the paper's fusion of everything between
 // two GEMMs (Section 4.2) extended across the GEMM boundaries through the
 // exact integer accumulators.
+//
+// At one or two rows every kernel is bound by memory latency, not bandwidth,
+// so each one issues all of its global loads (rows, parameters, weights, the
+// attention keys and values) before it waits for the first of them: the
+// kernel then pays about one memory round trip instead of one per phase.
 #include "blocks.hpp"
 #include "internal.h"
 
@@ -31,65 +36,74 @@ constexpr int kStepMaxLen = 128; // longest self / cross attention
 constexpr int kStepHeadDim = 64; // widest head
 constexpr int kFfnChunk = 64;    // hidden units per k_step_ffn block
 
-// The rows of a sublayer input: y (fp32, the updated residual stream) and
-// a = quant(LN(y)) or quant(y), in LDS.  Wave w prepares row w (R <= 2).
+// 16 bytes as a native vector (copied as a value, never through memory)
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// What the wave preparing one input row loads at kernel start.
 template <int NJ>
-__device__ __forceinline__ void step_rows(const StepIn& in, int R, int d, int8_t* a_lds) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (blockIdx.x == 0 && in.zero_acc)
-    for (int i = threadIdx.x; i < in.zero_n; i += blockDim.x) in.zero_acc[i] = 0;
-  if (wave >= R) return;
-  const int r = wave;
-  float v[NJ];
-  if (in.embed) {
-    int tok = in.tok[r];
-    tok = tok < 0 ? 0 : (tok >= in.V ? in.V - 1 : tok);
-    const float c = in.c_emb[tok];
+struct RowRegs {
+  float x[NJ];   // residual row
+  int a[NJ];     // pending accumulator
+  float sc[NJ];  // pending update scale and bias
+  float bi[NJ];
+  float g[NJ];   // the LayerNorm's gain and bias
+  float b[NJ];
+};
+
+// Issues the loads of input row r (element i = lane + 64 j in slot j; slots
+// past d repeat element d - 1 and are never used).  No load is conditional:
+// a branch around a load makes the compiler wait for it where the branches
+// join, which would serialize the kernel's memory round trips.
+template <int NJ>
+__device__ __forceinline__ void load_row(const StepIn& in, int r, int d, RowRegs<NJ>& q) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int i = lane + 64 * j;
-      v[j] = i < d ? fmaf((float)in.E[(size_t)tok * d + i], c, in.pe[(size_t)in.t * d + i]) : 0.0f;
-    }
-  } else if (in.acc) {
-    // pending residual update of the previous sublayer (its fp32 epilogue)
+  for (int j = 0; j < NJ; ++j) {
+    const int i = min(lane + 64 * j, d - 1);
+    q.x[j] = in.x_in[(size_t)r * d + i];
+    q.a[j] = in.acc[(size_t)r * d + i];
+    q.sc[j] = in.scale[i];
+    q.bi[j] = in.bias[i];
+    q.g[j] = in.ln_g[i];
+    q.b[j] = in.ln_b[i];
+  }
+}
+
+// LayerNorm of one row held by a wave (element i = lane + 64 j in v[j]) in
+// the canonical order: lane partials over ascending i, then the butterfly.
+template <int NJ>
+__device__ __forceinline__ void ln_row(float (&v)[NJ], const float (&g)[NJ], const float (&b)[NJ], int d, float eps) {
+  const int lane = threadIdx.x & 63;
+  const float inv_d = 1.0f / (float)d;
+  float p = 0.0f;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int i = lane + 64 * j;
-      v[j] = i < d ? fmaf(in.gamma, in.x_in[(size_t)r * d + i],
-                          fmaf((float)in.acc[(size_t)r * d + i], in.scale[i], in.bias[i]))
-                   : 0.0f;
-    }
-  } else {
+  for (int j = 0; j < NJ; ++j)
+    if (lane + 64 * j < d) p = p + v[j];
+  const float mu = wave_sum(p) * inv_d;
+  float p2 = 0.0f;
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int i = lane + 64 * j;
-      v[j] = i < d ? in.x_in[(size_t)r * d + i] : 0.0f;
+  for (int j = 0; j < NJ; ++j) {
+    if (lane + 64 * j < d) {
+      v[j] = v[j] - mu;
+      p2 = fmaf(v[j], v[j], p2);
     }
   }
-  const float inv_d = 1.0f / (float)d;
-  // LayerNorm in the canonical order (element i in lane i % 64, ascending i)
-  auto layer_norm = [&](const float* g, const float* b) {
-    float p = 0.0f;
+  const float rstd = 1.0f / sqrtf(wave_sum(p2) * inv_d + eps);
 #pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      if (lane + 64 * j < d) p = p + v[j];
-    const float mu = wave_sum(p) * inv_d;
-    float p2 = 0.0f;
+  for (int j = 0; j < NJ; ++j)
+    if (lane + 64 * j < d) v[j] = fmaf(v[j] * rstd, g[j], b[j]);
+}
+
+// Finishes row r from the loaded registers: the pending residual update, the LayerNorm, the store of the updated residual row
+// (block 0), and the int8 codes in a_lds + r * d.
+template <int NJ>
+__device__ __forceinline__ void finish_row(const StepIn& in, int r, int d, RowRegs<NJ>& q, int8_t* a_lds) {
+  const int lane = threadIdx.x & 63;
+  float v[NJ];
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      if (lane + 64 * j < d) {
-        v[j] = v[j] - mu;
-        p2 = fmaf(v[j], v[j], p2);
-      }
-    }
-    const float rstd = 1.0f / sqrtf(wave_sum(p2) * inv_d + in.eps);
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int i = lane + 64 * j;
-      if (i < d) v[j] = fmaf(v[j] * rstd, g[i], b[i]);
-    }
-  };
-  if (in.post_g) layer_norm(in.post_g, in.post_b);  // post-LN: normalize the residual stream
+  for (int j = 0; j < NJ; ++j)
+    v[j] = in.update ? fmaf(in.gamma, q.x[j], fmaf((float)q.a[j], q.sc[j], q.bi[j])) : q.x[j];
+  if (in.ln_mode == 1) ln_row<NJ>(v, q.g, q.b, d, in.eps);  // post-LN: normalize the residual stream
   if (blockIdx.x == 0 && in.x_out) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -97,7 +111,7 @@ __device__ __forceinline__ void step_rows(const StepIn& in, int R, int d, int8_t
       if (i < d) in.x_out[(size_t)r * d + i] = v[j];
     }
   }
-  if (in.pre_g) layer_norm(in.pre_g, in.pre_b);  // pre-LN: normalize the sublayer input
+  if (in.ln_mode == 2) ln_row<NJ>(v, q.g, q.b, d, in.eps);  // pre-LN: normalize the sublayer input
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     const int i = lane + 64 * j;
@@ -105,241 +119,319 @@ __device__ __forceinline__ void step_rows(const StepIn& in, int R, int d, int8_t
   }
 }
 
-// One block per head.  DMAX: model width class; rows of W are d bytes.
-template <int DMAX, bool SELF>
-__global__ __launch_bounds__(256) void k_step_attn(StepIn in, StepAttn at) {
-  constexpr int LPR = lanes_per_row(DMAX);
-  constexpr int RPI = 64 / LPR;
-  constexpr int KC = (DMAX / 16 + LPR - 1) / LPR;           // 16-byte chunks per lane
-  constexpr int NROWS = (SELF ? 3 : 1) * kStepHeadDim;       // projection rows per head (max)
-  constexpr int U = (NROWS + 4 * RPI - 1) / (4 * RPI);       // row groups per wave
-  constexpr int ND = (DMAX + 255) / 256;                     // W_o rows per thread
+constexpr int kStepThreads = 256;  // block size of every step kernel
+
+// (The loop stride is the compile-time block size: reading blockDim.x loads
+// the dispatch packet and waits for every load issued before it.)
+__device__ __forceinline__ void clear_acc(const StepIn& in) {
+  if (blockIdx.x == 0 && in.zero_acc)
+    for (int i = threadIdx.x; i < in.zero_n; i += kStepThreads) in.zero_acc[i] = 0;
+}
+
+// The projections run on v_mfma_i32_16x16x64_i8 even though only R <= 2 of
+// the 16 rows of its A operand are real: one matrix instruction yields 16
+// complete output dot products in lanes 0..15 (D[m] = row m), where the
+// vector form spends tens of instructions per 4 outputs on cross-lane
+// reductions, and these kernels are bound by instruction issue, not by
+// memory.  Fragment layout: lane l holds 16 bytes of K at 16 (l / 16) of
+// row l % 16 (of the activations for A, of the weights for B).
+__device__ __forceinline__ v4i mfma16(const v4i a, const v4i b, const v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
+// One block per head.  DMAX: model width class; NI: attended positions per
+// lane (n <= 64 NI).
+template <int DMAX, bool SELF, int NI>
+__global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn at) {
+  constexpr int NJ = DMAX / 64;
+  constexpr int KS = DMAX / 64;      // 64-deep K steps of the projection
+  constexpr int TPW = SELF ? 3 : 1;  // 16-row projection tiles per wave (12 or 4 per head)
+  constexpr int OT = DMAX / 64;      // 16-column W_o tiles per wave (d / 16 over 4 waves)
+  constexpr int HC = kStepHeadDim / 16;
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
   __shared__ __attribute__((aligned(16))) int8_t qkv[3][kStepRows][kStepHeadDim];
   __shared__ __attribute__((aligned(16))) int8_t ctx[kStepRows][kStepHeadDim];
-  __shared__ AttnLdsT<kStepMaxLen, kStepHeadDim> att[kStepRows];
+  __shared__ AttnLdsT<64 * NI, kStepHeadDim> att[kStepRows];
   const int hd = blockIdx.x;
-  const int R = at.R, d = at.d, dh = at.dh;
-  const int nrows = (SELF ? 3 : 1) * dh;
+  const int R = at.R, d = at.d, dh = at.dh, nc = dh / 16, ks = d / 64;
+  const int ntile = (SELF ? 3 : 1) * dh / 16;  // projection tiles of this head
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int sub = lane / LPR, kl = lane % LPR;
-  auto row_of = [&](int j) { return (j / dh) * d + hd * dh + (j % dh); };
-  // 1. weight loads: the head's projection rows and its W_o columns
-  int4 wv[U][KC];
+  const int l16 = lane & 15, kq = lane >> 4;
+  // 1. every global load, none conditional: the wave's input row, the
+  //    projection's weight fragments with their scales and biases, the W_o
+  //    fragments, the keys and values
+  RowRegs<NJ> rr;
+  load_row(in, min(wave, R - 1), d, rr);
+  v4i wf[TPW][KS];
+  float e_sc[TPW], e_bi[TPW];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int j = (u * 4 + wave) * RPI + sub;
+  for (int t = 0; t < TPW; ++t) {
+    const int j = 16 * min(wave + 4 * t, ntile - 1) + l16;  // row of the head's [q | k | v]
+    const int part = (j >= dh) + (j >= 2 * dh);
+    const size_t n = (size_t)part * d + hd * dh + (j - part * dh);
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int k = (kl + c * LPR) * 16;
-      wv[u][c] = (j < nrows && k < d) ? *(const int4*)(at.W + (size_t)row_of(j) * d + k) : make_int4(0, 0, 0, 0);
+    for (int kk = 0; kk < KS; ++kk) wf[t][kk] = *(const v4i*)(at.W + n * d + 64 * min(kk, ks - 1) + 16 * kq);
+    e_sc[t] = at.scale[n];
+    e_bi[t] = at.bias[n];
+  }
+  v4i of[OT];
+#pragma unroll
+  for (int t = 0; t < OT; ++t) {
+    const int n = min(16 * (wave + 4 * t) + l16, d - 1);
+    of[t] = *(const v4i*)(at.Wo + (size_t)n * d + hd * dh + 16 * min(kq, nc - 1));
+  }
+  // keys and values of row r in registers: position lane + 64 i (self: the
+  // cached positions before t; cross: every source position; positions at
+  // or past n_load repeat position n_load - 1, or 0, and are not used)
+  const int r = min(wave, R - 1);
+  const int n_load = SELF ? at.t : at.S;
+  const int8_t* kbase = SELF ? at.kcache + (size_t)r * at.T * d + hd * dh : at.kv + (size_t)r * at.S * 2 * d + hd * dh;
+  const int8_t* vbase = SELF ? at.vcache + (size_t)r * at.T * d + hd * dh : kbase + d;
+  const size_t pstride = SELF ? (size_t)d : (size_t)2 * d;
+  v4i kr[NI][HC], vr[NI][HC];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const size_t p = (size_t)max(min(lane + 64 * i, n_load - 1), 0);
+#pragma unroll
+    for (int c = 0; c < HC; ++c) {
+      const int off = 16 * min(c, nc - 1);
+      kr[i][c] = *(const v4i*)(kbase + p * pstride + off);
+      vr[i][c] = *(const v4i*)(vbase + p * pstride + off);
     }
   }
-  int4 wo[ND][kStepHeadDim / 16];
-#pragma unroll
-  for (int i = 0; i < ND; ++i) {
-    const int n = threadIdx.x + 256 * i;
-#pragma unroll
-    for (int c = 0; c < kStepHeadDim / 16; ++c)
-      wo[i][c] = (n < d && 16 * c < dh) ? *(const int4*)(at.Wo + (size_t)n * d + hd * dh + 16 * c)
-                                        : make_int4(0, 0, 0, 0);
-  }
+  int n_att = SELF ? at.t + 1 : at.len[r];
+  n_att = SELF ? n_att : (n_att < 1 ? 1 : (n_att > at.S ? at.S : n_att));
   // 2. the rows
-  step_rows<(DMAX + 63) / 64>(in, R, d, a_lds);
+  clear_acc(in);
+  if (wave < R) finish_row(in, wave, d, rr, a_lds);
   __syncthreads();
-  // 3. Q (K, V) of the head, requantized
+  // 3. Q (K, V) of the head on the matrix cores, requantized into LDS
+  {
+    const int arow = l16 < R ? l16 : 0;
+    v4i af[KS];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int j = (u * 4 + wave) * RPI + sub;
-    int acc[kStepRows] = {0, 0};
+    for (int kk = 0; kk < KS; ++kk) af[kk] = *(const v4i*)(a_lds + arow * d + 64 * kk + 16 * kq);
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int k = (kl + c * LPR) * 16;
-      if (k < d)
+    for (int t = 0; t < TPW; ++t) {
+      const int tile = wave + 4 * t;
+      if (tile < ntile) {
+        v4i acc = {0, 0, 0, 0};
 #pragma unroll
-        for (int m = 0; m < kStepRows; ++m)
-          if (m < R) acc[m] = dot16(wv[u][c], *(const int4*)(a_lds + m * d + k), acc[m]);
-    }
+        for (int kk = 0; kk < KS; ++kk)
+          if (kk < ks) acc = mfma16(af[kk], wf[t][kk], acc);
+        if (lane < 16) {
+          const int j = 16 * tile + lane;
+          const int part = (j >= dh) + (j >= 2 * dh);
 #pragma unroll
-    for (int off = LPR / 2; off >= 1; off >>= 1)
-#pragma unroll
-      for (int m = 0; m < kStepRows; ++m) acc[m] += __shfl_xor(acc[m], off, 64);
-    if (kl == 0 && j < nrows) {
-      const int n = row_of(j);
-#pragma unroll
-      for (int m = 0; m < kStepRows; ++m)
-        if (m < R) qkv[j / dh][m][j % dh] = code_of(fmaf((float)acc[m], at.scale[n], at.bias[n]));
-    }
-  }
-  __syncthreads();
-  // 4. attention, wave r for row r
-  if (wave < R) {
-    const int r = wave;
-    if (SELF) {
-      const int T = at.T, t = at.t;
-      const int8_t* knew = qkv[1][r];
-      const int8_t* vnew = qkv[2][r];
-      for (int j = lane; j < dh; j += 64) {
-        at.kcache[((size_t)r * T + t) * d + hd * dh + j] = knew[j];
-        at.vcache[((size_t)r * T + t) * d + hd * dh + j] = vnew[j];
+          for (int m = 0; m < kStepRows; ++m)
+            if (m < R) qkv[part][m][j - part * dh] = code_of(fmaf((float)acc[m], e_sc[t], e_bi[t]));
+        }
       }
-      auto key = [&](int tp) -> const int8_t* {
-        return tp == t ? knew : at.kcache + ((size_t)r * T + tp) * d + hd * dh;
-      };
-      auto val = [&](int tp) -> const int8_t* {
-        return tp == t ? vnew : at.vcache + ((size_t)r * T + tp) * d + hd * dh;
-      };
-      attend_wave(qkv[0][r], t + 1, dh, key, val, at.c_qk, at.c_pv, ctx[r], att[r]);
-    } else {
-      int n = at.len[r];
-      n = n < 1 ? 1 : (n > at.S ? at.S : n);
-      const int8_t* base = at.kv + (size_t)r * at.S * 2 * d;
-      auto key = [&](int s) -> const int8_t* { return base + (size_t)s * 2 * d + hd * dh; };
-      auto val = [&](int s) -> const int8_t* { return base + (size_t)s * 2 * d + d + hd * dh; };
-      attend_wave(qkv[0][r], n, dh, key, val, at.c_qk, at.c_pv, ctx[r], att[r]);
     }
   }
   __syncthreads();
-  // 5. this head's share of the output projection, exact int32 partial sums
+  // 4. attention of row `wave` (Appendix A with the quantizer figure's
+  //    precisions): int8 scores, fp32 softmax in the canonical order, context
+  //    accumulated over ascending positions with one fma each, requantized
+  if (wave < R) {
+    AttnLdsT<64 * NI, kStepHeadDim>& sh = att[r];
+    const int8_t* knew = qkv[1][r];
+    const int8_t* vnew = qkv[2][r];
+    if (SELF) {
+      int8_t* kc = at.kcache + ((size_t)r * at.T + at.t) * d + hd * dh;
+      int8_t* vc = at.vcache + ((size_t)r * at.T + at.t) * d + hd * dh;
+      for (int j = lane; j < dh; j += 64) {
+        kc[j] = knew[j];
+        vc[j] = vnew[j];
+      }
+    }
+    int4 qv[HC], kn[HC];
 #pragma unroll
-  for (int i = 0; i < ND; ++i) {
-    const int n = threadIdx.x + 256 * i;
-    if (n >= d) continue;
+    for (int c = 0; c < HC; ++c) {
+      qv[c] = c < nc ? *(const int4*)(qkv[0][r] + 16 * c) : make_int4(0, 0, 0, 0);
+      kn[c] = c < nc ? *(const int4*)(knew + 16 * c) : make_int4(0, 0, 0, 0);
+    }
+    int s_new = 0;  // score of the position appended at this step
 #pragma unroll
-    for (int m = 0; m < kStepRows; ++m) {
-      if (m >= R) continue;
-      int s = 0;
+    for (int c = 0; c < HC; ++c) s_new = dot16(kn[c], qv[c], s_new);
+    float sv[NI];
+    float mx = -FLT_MAX;
 #pragma unroll
-      for (int c = 0; c < kStepHeadDim / 16; ++c)
-        if (16 * c < dh) s = dot16(wo[i][c], *(const int4*)(ctx[m] + 16 * c), s);
-      atomicAdd(at.acc_out + (size_t)m * d + n, s);
+    for (int i = 0; i < NI; ++i) {
+      const int p = lane + 64 * i;
+      sv[i] = 0.0f;
+      if (p < n_att) {
+        const bool cur = SELF && p == at.t;
+        int acc = 0;
+#pragma unroll
+        for (int c = 0; c < HC; ++c) {
+          const int4 kk = make_int4(kr[i][c].x, kr[i][c].y, kr[i][c].z, kr[i][c].w);
+          acc = dot16(kk, qv[c], acc);
+        }
+        if (!cur)
+#pragma unroll
+          for (int c = 0; c < HC; ++c)
+            if (c < nc) *(v4i*)&sh.v[p][16 * c] = vr[i][c];
+        sv[i] = (float)(cur ? s_new : acc) * at.c_qk;
+        mx = fmaxf(mx, sv[i]);
+      }
+    }
+    if (SELF)
+      for (int j = lane; j < dh; j += 64) sh.v[at.t][j] = vnew[j];
+    mx = wave_max(mx);
+    float part = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      if (lane + 64 * i < n_att) {
+        sv[i] = canon_exp(sv[i] - mx);
+        part = part + sv[i];
+      }
+    }
+    const float inv = 1.0f / wave_sum(part);
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      if (lane + 64 * i < n_att) sh.p[lane + 64 * i] = sv[i] * inv;
+    wave_sync();  // p and v visible to every lane of this wave
+    for (int j = lane; j < dh; j += 64) {
+      float acc = 0.0f;
+      int p = 0;
+      for (; p + 4 <= n_att; p += 4) {
+        const float p0 = sh.p[p], p1 = sh.p[p + 1], p2 = sh.p[p + 2], p3 = sh.p[p + 3];
+        const float v0 = sh.v[p][j], v1 = sh.v[p + 1][j], v2 = sh.v[p + 2][j], v3 = sh.v[p + 3][j];
+        acc = fmaf(p0, v0, acc);
+        acc = fmaf(p1, v1, acc);
+        acc = fmaf(p2, v2, acc);
+        acc = fmaf(p3, v3, acc);
+      }
+      for (; p < n_att; ++p) acc = fmaf(sh.p[p], (float)sh.v[p][j], acc);
+      ctx[r][j] = code_of(acc * at.c_pv);
+    }
+  }
+  __syncthreads();
+  // 5. this head's share of the output projection (K = dh), exact int32
+  //    partial sums added to the accumulator
+  {
+    const int crow = l16 < R ? l16 : 0;
+    const v4i cf = kq < nc ? *(const v4i*)(ctx[crow] + 16 * kq) : v4i{0, 0, 0, 0};
+#pragma unroll
+    for (int t = 0; t < OT; ++t) {
+      const int n0 = 16 * (wave + 4 * t);
+      if (n0 < d) {
+        const v4i acc = mfma16(cf, of[t], v4i{0, 0, 0, 0});
+        if (lane < 16)
+#pragma unroll
+          for (int m = 0; m < kStepRows; ++m)
+            if (m < R) atomicAdd(at.acc_out + (size_t)m * d + n0 + lane, acc[m]);
+      }
     }
   }
 }
 
-// One block per kFfnChunk hidden units: W1 rows of the chunk (ReLU
-// requantization), then the chunk's W2 columns into the int32 accumulator.
+// One block per kFfnChunk hidden units (one 16-row W1 tile per wave): ReLU
+// requantization of the chunk, then the chunk's W2 columns (K = 64) into the
+// int32 accumulator.
 template <int DMAX>
-__global__ __launch_bounds__(256) void k_step_ffn(StepIn in, StepFfn f) {
-  constexpr int LPR = lanes_per_row(DMAX);
-  constexpr int RPI = 64 / LPR;
-  constexpr int KC = (DMAX / 16 + LPR - 1) / LPR;
-  constexpr int U = (kFfnChunk + 4 * RPI - 1) / (4 * RPI);
-  constexpr int ND = (DMAX + 255) / 256;
+__global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f) {
+  constexpr int NJ = DMAX / 64;
+  constexpr int KS = DMAX / 64;
+  constexpr int OT = DMAX / 64;
+  static_assert(kFfnChunk == 64, "one W1 tile per wave and one K step of W2");
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
   __shared__ __attribute__((aligned(16))) int8_t h[kStepRows][kFfnChunk];
-  const int R = f.R, d = f.d, F = f.F;
+  const int R = f.R, d = f.d, F = f.F, ks = d / 64;
   const int f0 = blockIdx.x * kFfnChunk;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int sub = lane / LPR, kl = lane % LPR;
-  int4 wv[U][KC];
+  const int l16 = lane & 15, kq = lane >> 4;
+  RowRegs<NJ> rr;
+  load_row(in, min(wave, R - 1), d, rr);
+  const size_t hrow = (size_t)min(f0 + 16 * wave + l16, F - 1);
+  v4i wf[KS];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int j = (u * 4 + wave) * RPI + sub;
+  for (int kk = 0; kk < KS; ++kk) wf[kk] = *(const v4i*)(f.W1 + hrow * d + 64 * min(kk, ks - 1) + 16 * kq);
+  const float e_sc = f.scale1[hrow], e_bi = f.bias1[hrow];
+  v4i of[OT];
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int k = (kl + c * LPR) * 16;
-      wv[u][c] = (j < kFfnChunk && f0 + j < F && k < d) ? *(const int4*)(f.W1 + (size_t)(f0 + j) * d + k)
-                                                         : make_int4(0, 0, 0, 0);
-    }
+  for (int t = 0; t < OT; ++t) {
+    const int n = min(16 * (wave + 4 * t) + l16, d - 1);
+    of[t] = *(const v4i*)(f.W2 + (size_t)n * F + f0 + 16 * kq);
   }
-  int4 w2[ND][kFfnChunk / 16];
-#pragma unroll
-  for (int i = 0; i < ND; ++i) {
-    const int n = threadIdx.x + 256 * i;
-#pragma unroll
-    for (int c = 0; c < kFfnChunk / 16; ++c)
-      w2[i][c] = (n < d && f0 + 16 * c < F) ? *(const int4*)(f.W2 + (size_t)n * F + f0 + 16 * c)
-                                            : make_int4(0, 0, 0, 0);
-  }
-  step_rows<(DMAX + 63) / 64>(in, R, d, a_lds);
+  clear_acc(in);
+  if (wave < R) finish_row(in, wave, d, rr, a_lds);
   __syncthreads();
+  {
+    const int arow = l16 < R ? l16 : 0;
+    v4i acc = {0, 0, 0, 0};
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int j = (u * 4 + wave) * RPI + sub;
-    int acc[kStepRows] = {0, 0};
-#pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int k = (kl + c * LPR) * 16;
-      if (k < d)
-#pragma unroll
-        for (int m = 0; m < kStepRows; ++m)
-          if (m < R) acc[m] = dot16(wv[u][c], *(const int4*)(a_lds + m * d + k), acc[m]);
-    }
-#pragma unroll
-    for (int off = LPR / 2; off >= 1; off >>= 1)
-#pragma unroll
-      for (int m = 0; m < kStepRows; ++m) acc[m] += __shfl_xor(acc[m], off, 64);
-    if (kl == 0 && j < kFfnChunk) {
-      const int n = f0 + j;
+    for (int kk = 0; kk < KS; ++kk)
+      if (kk < ks) acc = mfma16(*(const v4i*)(a_lds + arow * d + 64 * kk + 16 * kq), wf[kk], acc);
+    if (lane < 16)
 #pragma unroll
       for (int m = 0; m < kStepRows; ++m)
-        if (m < R) h[m][j] = n < F ? code_of(fmaxf(fmaf((float)acc[m], f.scale1[n], f.bias1[n]), 0.0f)) : 0;
-    }
+        if (m < R) h[m][16 * wave + lane] = code_of(fmaxf(fmaf((float)acc[m], e_sc, e_bi), 0.0f));
   }
   __syncthreads();
+  {
+    const int hr = l16 < R ? l16 : 0;
+    const v4i hf = *(const v4i*)(h[hr] + 16 * kq);
 #pragma unroll
-  for (int i = 0; i < ND; ++i) {
-    const int n = threadIdx.x + 256 * i;
-    if (n >= d) continue;
+    for (int t = 0; t < OT; ++t) {
+      const int n0 = 16 * (wave + 4 * t);
+      if (n0 < d) {
+        const v4i acc = mfma16(hf, of[t], v4i{0, 0, 0, 0});
+        if (lane < 16)
 #pragma unroll
-    for (int m = 0; m < kStepRows; ++m) {
-      if (m >= R) continue;
-      int s = 0;
-#pragma unroll
-      for (int c = 0; c < kFfnChunk / 16; ++c) s = dot16(w2[i][c], *(const int4*)(h[m] + 16 * c), s);
-      atomicAdd(f.acc_out + (size_t)m * d + n, s);
+          for (int m = 0; m < kStepRows; ++m)
+            if (m < R) atomicAdd(f.acc_out + (size_t)m * d + n0 + lane, acc[m]);
+      }
     }
   }
 }
 
-// Output projection over the shared embedding with the fused arg-max.
+// Output projection over the shared embedding with the fused arg-max: each
+// wave takes kLogitsTiles tiles of 16 vocabulary rows.
+constexpr int kLogitsTiles = 2;
 template <int DMAX>
-__global__ __launch_bounds__(256) void k_step_logits(StepIn in, StepLogits g) {
-  constexpr int LPR = lanes_per_row(DMAX);
-  constexpr int RPI = 64 / LPR;
-  constexpr int KC = (DMAX / 16 + LPR - 1) / LPR;
-  constexpr int U = 8;
+__global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLogits g) {
+  constexpr int NJ = DMAX / 64;
+  constexpr int KS = DMAX / 64;
+  constexpr int TPW = kLogitsTiles;
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
   __shared__ unsigned long long wmax[4][kStepRows];
-  const int R = g.R, d = g.d, N = g.V;
+  const int R = g.R, d = g.d, N = g.V, ks = d / 64;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int sub = lane / LPR, kl = lane % LPR;
-  const int row0 = (blockIdx.x * 4 + wave) * RPI * U;
-  int4 wv[U][KC];
+  const int l16 = lane & 15, kq = lane >> 4;
+  const int row0 = (blockIdx.x * 4 + wave) * TPW * 16;
+  RowRegs<NJ> rr;
+  load_row(in, min(wave, R - 1), d, rr);
+  v4i wf[TPW][KS];
+  float co[TPW];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int n = row0 + u * RPI + sub;
+  for (int t = 0; t < TPW; ++t) {
+    const size_t n = (size_t)min(row0 + 16 * t + l16, N - 1);
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int k = (kl + c * LPR) * 16;
-      wv[u][c] = (n < N && k < d) ? *(const int4*)(g.E + (size_t)n * d + k) : make_int4(0, 0, 0, 0);
-    }
+    for (int kk = 0; kk < KS; ++kk) wf[t][kk] = *(const v4i*)(g.E + n * d + 64 * min(kk, ks - 1) + 16 * kq);
+    co[t] = g.c_out[n];
   }
-  step_rows<(DMAX + 63) / 64>(in, R, d, a_lds);
+  clear_acc(in);
+  if (wave < R) finish_row(in, wave, d, rr, a_lds);
   __syncthreads();
+  const int arow = l16 < R ? l16 : 0;
+  v4i af[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) af[kk] = *(const v4i*)(a_lds + arow * d + 64 * kk + 16 * kq);
   unsigned long long best[kStepRows] = {0ull, 0ull};
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int n = row0 + u * RPI + sub;
-    int acc[kStepRows] = {0, 0};
+  for (int t = 0; t < TPW; ++t) {
+    v4i acc = {0, 0, 0, 0};
 #pragma unroll
-    for (int c = 0; c < KC; ++c) {
-      const int k = (kl + c * LPR) * 16;
-      if (k < d)
-#pragma unroll
-        for (int m = 0; m < kStepRows; ++m)
-          if (m < R) acc[m] = dot16(wv[u][c], *(const int4*)(a_lds + m * d + k), acc[m]);
-    }
-#pragma unroll
-    for (int off = LPR / 2; off >= 1; off >>= 1)
-#pragma unroll
-      for (int m = 0; m < kStepRows; ++m) acc[m] += __shfl_xor(acc[m], off, 64);
-    if (kl == 0 && n < N) {
+    for (int kk = 0; kk < KS; ++kk)
+      if (kk < ks) acc = mfma16(af[kk], wf[t][kk], acc);
+    const int n = row0 + 16 * t + lane;
+    if (lane < 16 && n < N) {
 #pragma unroll
       for (int m = 0; m < kStepRows; ++m) {
         if (m < R) {
-          const float z = (float)acc[m] * g.c_out[n];
+          const float z = (float)acc[m] * co[t];
           if (g.logits) g.logits[(size_t)m * N + n] = z;
           const unsigned long long key = pack_argmax(z, n);
           best[m] = key > best[m] ? key : best[m];
@@ -379,28 +471,35 @@ bool step_path_fits(int R, int d, int dh, int F, int T, int S) {
   }
 
 hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s) {
-#define MNMT_ATTN(DM)                                                                              \
-  if (self)                                                                                        \
-    hipLaunchKernelGGL((k_step_attn<DM, true>), dim3(heads), dim3(256), 0, s, in, at);              \
-  else                                                                                             \
-    hipLaunchKernelGGL((k_step_attn<DM, false>), dim3(heads), dim3(256), 0, s, in, at);
+  // positions attended: self t + 1 <= T, cross at most S
+  const int n_max = self ? at.t + 1 : at.S;
+#define MNMT_ATTN_NI(DM, SELF, NI) hipLaunchKernelGGL((k_step_attn<DM, SELF, NI>), dim3(heads), dim3(kStepThreads), 0, s, in, at)
+#define MNMT_ATTN(DM)                                   \
+  if (self) {                                           \
+    if (n_max <= 64) MNMT_ATTN_NI(DM, true, 1);         \
+    else MNMT_ATTN_NI(DM, true, 2);                     \
+  } else {                                              \
+    if (n_max <= 64) MNMT_ATTN_NI(DM, false, 1);        \
+    else MNMT_ATTN_NI(DM, false, 2);                    \
+  }
   MNMT_BY_D(at.d, MNMT_ATTN)
 #undef MNMT_ATTN
+#undef MNMT_ATTN_NI
   return hipGetLastError();
 }
 
 hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s) {
   const int blocks = (f.F + kFfnChunk - 1) / kFfnChunk;
-#define MNMT_FFN(DM) hipLaunchKernelGGL((k_step_ffn<DM>), dim3(blocks), dim3(256), 0, s, in, f);
+#define MNMT_FFN(DM) hipLaunchKernelGGL((k_step_ffn<DM>), dim3(blocks), dim3(kStepThreads), 0, s, in, f);
   MNMT_BY_D(f.d, MNMT_FFN)
 #undef MNMT_FFN
   return hipGetLastError();
 }
 
 hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s) {
-  const int rpb = 4 * (64 / lanes_per_row(row_class(g.d))) * 8;  // rows per block
+  const int rpb = 4 * kLogitsTiles * 16;  // rows per block
   const int blocks = (g.V + rpb - 1) / rpb;
-#define MNMT_LOGITS(DM) hipLaunchKernelGGL((k_step_logits<DM>), dim3(blocks), dim3(256), 0, s, in, g);
+#define MNMT_LOGITS(DM) hipLaunchKernelGGL((k_step_logits<DM>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);
   MNMT_BY_D(g.d, MNMT_LOGITS)
 #undef MNMT_LOGITS
   return hipGetLastError();

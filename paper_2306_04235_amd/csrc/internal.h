@@ -117,28 +117,28 @@ struct FusedGemv {         // a linear layer over the prepared rows, and greedy 
   int T, stop_at_eos, eos, pad;
   int32_t* zero_acc;       // commit: cleared after the step (or null)
   int zero_n;
+  float* emb_out;          // commit: embedding of the next input tokens at position t + 1 (or null)
+  const int8_t* E;
+  const float* c_emb;
+  const float* pe;
+  int d, V, P;
 };
 hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s);
 
 // Decoder step in 3 kernels per layer for at most 2 rows (decode_step.hip).
 struct StepIn {            // the sublayer input rows of a step kernel
-  int t;                   // decode step (embedding position)
-  int embed;               // rows = embeddings of tok[]
-  const int32_t* tok;
-  const int8_t* E;
-  const float* c_emb;
-  const float* pe;
-  int V;
+  // Every pointer is valid for the extent given even where its flag is off,
+  // so that the kernels load without branches.
   const float* x_in;       // residual rows [R, d]
   float* x_out;            // block 0 stores the updated rows here (or null)
-  const int32_t* acc;      // pending update: x <- fma(gamma, x, fma(acc, scale, bias)), or null
-  const float* scale;
-  const float* bias;
+  const int32_t* acc;      // [R, d]: pending update x <- fma(gamma, x, fma(acc, scale, bias))
+  const float* scale;      // [d]
+  const float* bias;       // [d]
   float gamma;
-  const float* post_g;     // post-LN: LayerNorm of the updated residual stream (or null)
-  const float* post_b;
-  const float* pre_g;      // pre-LN: LayerNorm of the sublayer input (or null)
-  const float* pre_b;
+  int update;              // apply the pending update
+  const float* ln_g;       // [d] LayerNorm gain and bias
+  const float* ln_b;
+  int ln_mode;             // 0 none, 1 post-LN (the residual stream), 2 pre-LN (the sublayer input)
   float eps;
   float inv_s;             // 1 / input scale of the consuming layer
   int32_t* zero_acc;       // block 0 clears this accumulator (its consumer has finished)

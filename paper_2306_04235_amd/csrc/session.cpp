@@ -363,10 +363,12 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
 
 // Greedy step for at most 2 rows in 3 kernels per layer (decode_step.hip):
 // [attention block, self] [attention block, cross] [FFN block] per layer,
-// then [output projection + arg-max] and [commit].  Each kernel applies the
-// previous sublayer's residual update in its prologue; the three int32
-// accumulators (W_o, W_oc, W2 partial sums) are cleared by the kernel after
-// their consumer, and the residual rows alternate between two buffers.
+// then [output projection + arg-max] and [commit].  The step's input rows
+// (the embeddings of the current tokens) are in dec_x on entry; the commit
+// writes the next step's.  Each kernel applies the previous sublayer's
+// residual update in its prologue; the three int32 accumulators (W_o, W_oc,
+// W2 partial sums) are cleared by the kernel after their consumer, and the
+// residual rows alternate between two buffers.
 int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s) {
   const mnmt_model* m = S->m;
   const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
@@ -377,34 +379,38 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   const int nacc = R * d;
   float* xa = S->dec_x;
   float* xb = S->dec_x2;
+  // a row input with no pending update and no LayerNorm; the pointers of the
+  // unused operands only need to be valid
   auto base = [&](float inv_s) {
     StepIn in{};
-    in.t = t;
-    in.tok = S->cur_tok;
-    in.E = m->E;
-    in.c_emb = m->c_emb;
-    in.pe = m->pe;
-    in.V = m->info.vocab;
     in.x_in = xa;
     in.x_out = xb;
+    in.acc = acc_o;
+    in.scale = m->dec_ln.g ? m->dec_ln.g : m->dec[0].sa_ln.g;
+    in.bias = in.scale;
+    in.gamma = 1.0f;
+    in.ln_g = in.scale;
+    in.ln_b = in.scale;
     in.eps = m->info.ln_eps;
     in.inv_s = inv_s;
     return in;
   };
-  auto pending = [&](StepIn& in, const int32_t* acc, const LinearDev& L, float gamma, const LnDev& post_ln) {
-    in.acc = acc;
-    in.scale = L.scale;
-    in.bias = L.bias;
-    in.gamma = gamma;
-    if (post) {
-      in.post_g = post_ln.g;
-      in.post_b = post_ln.b;
+  // the residual update of the sublayer whose partial sums are in acc (its
+  // post-LN LayerNorm in post-LN models), and the pre-LN LayerNorm of the next
+  auto rows = [&](StepIn& in, const int32_t* acc, const LinearDev* L, float gamma, const LnDev& post_ln,
+                  const LnDev& pre_ln) {
+    if (acc) {
+      in.acc = acc;
+      in.scale = L->scale;
+      in.bias = L->bias;
+      in.gamma = gamma;
+      in.update = 1;
     }
-  };
-  auto pre = [&](StepIn& in, const LnDev& ln) {
-    if (!post) {
-      in.pre_g = ln.g;
-      in.pre_b = ln.b;
+    const LnDev& ln = post ? post_ln : pre_ln;
+    if (ln.g && (acc || !post)) {
+      in.ln_g = ln.g;
+      in.ln_b = ln.b;
+      in.ln_mode = post ? 1 : 2;
     }
   };
   auto attn = [&](const LayerDev& L, bool self, int32_t* acc_out) {
@@ -426,29 +432,30 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     at.acc_out = acc_out;
     return at;
   };
+  const LnDev none{};
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
     {  // self-attention block
       StepIn in = base(L.qkv.inv_in);
       if (l == 0) {
-        in.embed = 1;
+        // the embeddings are the residual stream as they are
+        in.x_out = nullptr;
+        rows(in, nullptr, nullptr, 1.0f, none, L.sa_ln);
       } else {
         const LayerDev& P = m->dec[l - 1];
-        pending(in, acc_w2, P.w2, P.ff_gamma, P.ff_ln);
+        rows(in, acc_w2, &P.w2, P.ff_gamma, P.ff_ln, L.sa_ln);
         in.zero_acc = acc_oc;
         in.zero_n = nacc;
       }
-      pre(in, L.sa_ln);
       StepAttn at = attn(L, true, acc_o);
       at.kcache = S->kcache[l];
       at.vcache = S->vcache[l];
       LAUNCH(launch_step_attn(in, at, 1, h, s));
-      std::swap(xa, xb);
+      if (in.x_out) std::swap(xa, xb);
     }
     {  // cross-attention block
       StepIn in = base(L.cq.inv_in);
-      pending(in, acc_o, L.o, L.sa_gamma, L.sa_ln);
-      pre(in, L.ca_ln);
+      rows(in, acc_o, &L.o, L.sa_gamma, L.sa_ln, L.ca_ln);
       in.zero_acc = acc_w2;
       in.zero_n = nacc;
       StepAttn at = attn(L, false, acc_oc);
@@ -458,8 +465,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     }
     {  // FFN block
       StepIn in = base(L.w1.inv_in);
-      pending(in, acc_oc, L.co, L.ca_gamma, L.ca_ln);
-      pre(in, L.ff_ln);
+      rows(in, acc_oc, &L.co, L.ca_gamma, L.ca_ln, L.ff_ln);
       in.zero_acc = acc_o;
       in.zero_n = nacc;
       StepFfn f{};
@@ -478,8 +484,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   const LayerDev& last = m->dec.back();
   StepIn in = base(m->inv_fin);
   in.x_out = nullptr;
-  pending(in, acc_w2, last.w2, last.ff_gamma, last.ff_ln);
-  pre(in, m->dec_ln);
+  rows(in, acc_w2, &last.w2, last.ff_gamma, last.ff_ln, m->dec_ln);
   in.zero_acc = acc_oc;
   in.zero_n = nacc;
   StepLogits g{};
@@ -507,15 +512,34 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   gv.pad = m->info.pad_id;
   gv.zero_acc = acc_w2;
   gv.zero_n = nacc;
+  gv.emb_out = S->dec_x;
+  gv.E = m->E;
+  gv.c_emb = m->c_emb;
+  gv.pe = m->pe;
+  gv.d = d;
+  gv.V = m->info.vocab;
+  gv.P = m->info.max_pos;
   LAUNCH(launch_greedy_commit_slots(gv, s));
   return MNMT_OK;
 }
 
-// The greedy step for R rows on the fastest path that fits.
-int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s) {
+bool step_path_used(const mnmt_session* S, int R) {
   const mnmt_model* m = S->m;
-  if (step_path_fits(R, m->info.d_model, m->dh, m->info.d_ffn, S->cfg.max_tgt_len, S->S))
-    return greedy_step_v3(S, R, t, stop_at_eos, logits_out, s);
+  return step_path_fits(R, m->info.d_model, m->dh, m->info.d_ffn, S->cfg.max_tgt_len, S->S);
+}
+
+// The 1-2 row path's input rows: embeddings of cur_tok at the position held
+// by the device step counter.
+int embed_step_input(mnmt_session* S, int R, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  LAUNCH(launch_embed(S->cur_tok, R, 1, S->step, m->E, m->c_emb, m->pe, m->info.d_model, m->info.vocab, S->dec_x, s));
+  return MNMT_OK;
+}
+
+// The greedy step for R rows on the fastest path that fits.
+// On the 1-2 row path the input rows must be in dec_x (embed_step_input).
+int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s) {
+  if (step_path_used(S, R)) return greedy_step_v3(S, R, t, stop_at_eos, logits_out, s);
   if (R <= 8) return greedy_step_fused(S, R, t, stop_at_eos, logits_out, s);
   return greedy_step(S, R, stop_at_eos, logits_out, s);
 }
@@ -541,6 +565,7 @@ int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
     const int R = S->B;
     LAUNCH(launch_greedy_reset(S->slots, R, sc.max_steps, S->cur_tok, S->finished, S->out_len, S->step,
                                m->info.bos_id, S->fslots, 8 * fused_slots_per_row() + 3 * 2 * m->info.d_model / 2, s));
+    if (step_path_used(S, R) && (rc = embed_step_input(S, R, s))) return rc;
     for (int t = 0; t < sc.max_steps; ++t)
       if ((rc = greedy_step_any(S, R, t, sc.stop_at_eos, nullptr, s))) return rc;
   } else {
@@ -712,6 +737,7 @@ extern "C" int mnmt_decode_step(mnmt_session* S, const int32_t* d_prev, int32_t*
   hipStream_t s = as_stream(stream);
   const int R = S->B;
   if (d_prev) LAUNCH(launch_copy_i32(d_prev, S->cur_tok, R, s));
+  if (step_path_used(S, R) && (rc = embed_step_input(S, R, s))) return rc;
   if ((rc = greedy_step_any(S, R, S->host_step, 0, d_logits, s))) return rc;
   LAUNCH(launch_copy_i32(S->cur_tok, d_next, R, s));
   ++S->host_step;
