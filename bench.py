@@ -8,10 +8,16 @@ layers, int8 self/cross attention with the int8 key/value cache, fused
 logits + arg-max), replayed from a captured hipGraph, inputs already in HBM.
 
 Prints one JSON line: decoded tokens per second (value), ms per sentence,
-the roofline of the dominant kernel (the fused logits + arg-max pass over
-the 8.19 MB int8 embedding, HBM bound), the int8 GEMM throughput of the
-largest quantized-linear sweep shape against the i8 matrix-core peak, and the
-CPU oracle timed on the host as a baseline.
+the roofline of the dominant kernel (the decoder's fused logits + arg-max
+kernel over the 8.19 MB int8 embedding, HBM bound, launched alone through
+mnmt_qlinear on one int8 row), the int8 GEMM throughput of the largest
+quantized-linear sweep shape against the i8 matrix-core peak, and the CPU
+oracle timed on the host as a baseline.
+
+--counters runs only the roofline kernel (50 launches) and a 256 MiB device
+copy, for rocprofv3 --pmc passes; --ingest-counters FETCH.csv WRITE.csv turns
+the two passes' counter_collection files into profiles/counters.json (HBM
+bytes per launch, scaled by what the same counters read for the copy).
 """
 from __future__ import annotations
 
@@ -42,9 +48,30 @@ def _events_ms(torch, fn, reps, stream):
     return e0.elapsed_time(e1) / reps
 
 
+ROOF_TAG = "step_logits_raw_b1"
+ROOF_KERNEL = "k_step_logits<256, true>"
+COPY_BYTES = 256 << 20
+
+
+def _kernel_events_ms(torch, fn_ev, reps, stream):
+    """Mean kernel duration (ms) over reps back-to-back launches of
+    fn_ev(e0, e1), whose events take the kernel's own start and end times."""
+    pairs = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)  # creates the HIP events; the launch re-records them
+        e1.record(stream)
+        pairs.append((e0, e1))
+    for e0, e1 in pairs:
+        fn_ev(e0, e1)
+    pairs[-1][1].synchronize()
+    return sum(a.elapsed_time(b) for a, b in pairs) / reps
+
+
 def _source_hash():
     h = hashlib.sha256()
-    for f in ("qlinear.hip", "canon.hpp"):
+    for f in ("decode_step.hip", "canon.hpp", "blocks.hpp", "internal.h"):
         with open(os.path.join(ROOT, "paper_2306_04235_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -62,6 +89,92 @@ def _traffic(kernel_tag):
     if not rec or rec.get("source_hash") != _source_hash():
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def _roofline_kernel(torch, np, mnmt, WL, G, info, blob, dev, stream):
+    """The roofline kernel as a closure, and its algorithmic bytes per launch:
+    the int8 embedding [V, d], the fp32 output scales [V], one int8 row, one
+    8-byte arg-max slot."""
+    from synth.modelfile import read_model
+
+    dims = WL.Dims(info.d_model, info.n_heads, info.d_ffn, info.n_enc, info.n_dec, info.vocab)
+    alg_bytes = WL.logits_gemv_bytes(dims) + info.d_model + 8
+    _, tens = read_model(blob)
+    x = torch.randint(-127, 128, (1, info.d_model), dtype=torch.int8, device=dev)
+    E = torch.from_numpy(np.array(tens["emb.w"])).to(dev)
+    c_out = torch.from_numpy(np.array(tens["emb.s"])).to(dev)  # the values do not affect the timing
+    slot = torch.zeros(1, dtype=torch.int64, device=dev)
+
+    def fn(e0=None, e1=None):
+        if e0 is None:
+            mnmt.mnmt_qlinear(x, E, c_out, None, mnmt.EPI_ARGMAX, out=slot, stream=stream)
+        else:
+            mnmt.mnmt_qlinear_timed(x, E, c_out, None, mnmt.EPI_ARGMAX, e0, e1, out=slot, stream=stream)
+
+    return fn, alg_bytes
+
+
+def counters_run():
+    """Short run for rocprofv3 --pmc: the roofline kernel 50 times, then a
+    256 MiB device-to-device copy (the counters' calibration) 3 times."""
+    import numpy as np
+    import torch
+
+    from paper_2306_04235_amd import mnmt, workload as WL
+    from synth import generate as G
+
+    dev = torch.device("cuda:0")
+    blob = G.build_model(G.WORKLOADS["mobile"].model)
+    model = mnmt.Model(blob)
+    stream = torch.cuda.current_stream()
+    fn, _ = _roofline_kernel(torch, np, mnmt, WL, G, model.info, blob, dev, stream)
+    for _ in range(50):
+        fn()
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    model.close()
+    print("counters run done", flush=True)
+
+
+def ingest_counters(fetch_csv, write_csv, command):
+    """profiles/counters.json from the FETCH_SIZE and WRITE_SIZE passes."""
+    import csv
+
+    def per_kernel(path, counter):
+        vals = {}
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if row["Counter_Name"] != counter:
+                    continue
+                vals.setdefault(row["Kernel_Name"], []).append(float(row["Counter_Value"]))
+        return vals
+
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        vals = per_kernel(path, counter)
+        roof = [v for k, v in vals.items() if "k_step_logits" in k]
+        others = {k: v for k, v in vals.items() if "k_step_logits" not in k and "mnmt" not in k}
+        copy_name, copy_vals = max(others.items(), key=lambda kv: max(kv[1]))
+        factor = COPY_BYTES / max(copy_vals)  # bytes per counter unit
+        per_launch = sorted(roof[0])[len(roof[0]) // 2] * factor  # median over the launches
+        out[counter] = {"per_launch_bytes": per_launch, "bytes_per_unit": factor, "copy_kernel": copy_name,
+                        "copy_counter": max(copy_vals), "launches": len(roof[0])}
+    rec = {"source_hash": _source_hash(), "kernel": ROOF_KERNEL,
+           "hbm_bytes_per_launch": round(out["FETCH_SIZE"]["per_launch_bytes"] + out["WRITE_SIZE"]["per_launch_bytes"]),
+           "fetch": out["FETCH_SIZE"], "write": out["WRITE_SIZE"], "command": command}
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    data = {}
+    if os.path.exists(path):
+        with open(path) as f:
+            data = json.load(f)
+    data[ROOF_TAG] = rec
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w") as f:
+        json.dump(data, f, indent=1)
+    print(json.dumps(rec))
 
 
 def cpu_baseline(workload, min_seconds=10.0):
@@ -88,11 +201,20 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--counters", action="store_true", help="only the roofline kernel and the copy (for --pmc)")
+    ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--ingest-command", default="")
     args = ap.parse_args()
+    if args.ingest_counters:
+        ingest_counters(*args.ingest_counters, args.ingest_command)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the batch-1 path does not "
               "shard; larger batches shard by sentence, see the design notes)", file=sys.stderr)
         sys.exit(2)
+    if args.counters:
+        counters_run()
+        return
 
     import numpy as np
     import torch
@@ -128,25 +250,16 @@ def main():
     tokens = int(outs[1].sum().item()) * args.steps
     ms_per_sentence = elapsed * 1e3 / (args.steps * w.batch)
 
-    # Dominant kernel: fused logits + arg-max over the int8 embedding (batch 1).
-    dims = WL.Dims(info.d_model, info.n_heads, info.d_ffn, info.n_enc, info.n_dec, info.vocab)
-    alg_bytes = WL.logits_gemv_bytes(dims) + info.d_model + 8
-    from synth.modelfile import read_model
-
-    _, tens = read_model(blob)
-    x = torch.randint(-127, 128, (1, info.d_model), dtype=torch.int8, device=dev)
-    E = torch.from_numpy(np.ascontiguousarray(tens["emb.w"])).to(dev)
-    # per-row output scales (their values do not affect the timing)
-    c_out = torch.from_numpy(np.ascontiguousarray(tens["emb.s"])).to(dev)
-    slot = torch.zeros(1, dtype=torch.int64, device=dev)
-    fn = lambda: mnmt.mnmt_qlinear(x, E, c_out, None, mnmt.EPI_ARGMAX, out=slot, stream=stream)  # noqa: E731
+    # Dominant kernel: the decoder's fused logits + arg-max over the int8
+    # embedding (batch 1), launched alone on one int8 row.
+    fn, alg_bytes = _roofline_kernel(torch, np, mnmt, WL, G, info, blob, dev, stream)
     for _ in range(10):
         fn()
-    kern_ms = _events_ms(torch, fn, 400, stream)
+    kern_ms = _kernel_events_ms(torch, fn, 400, stream)
     achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": _traffic("logits_argmax_b1"),
-                "kernel": "k_qgemv<1,16,4> (fused logits + arg-max, M=1 K=256 N=32000)",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": _traffic(ROOF_TAG),
+                "kernel": ROOF_KERNEL + " (fused logits + arg-max, M=1 K=256 N=32000)",
                 "alg_bytes_per_launch": alg_bytes, "avg_us": round(kern_ms * 1e3, 3)}
 
     # Largest quantized-linear sweep shape on the matrix cores.

@@ -184,9 +184,20 @@ int mnmt_session_tensor(const mnmt_session* session, const char* name, void** d_
  * [N, K] row-major, d_scale/d_bias fp32 [N] (bias may be NULL for I32 and
  * LOGITS), d_Y [M, N] of the epilogue's type.  K must be a positive multiple
  * of 64 and at most 8192; M >= 0, N >= 1.  M <= 8 runs the wavefront
- * reduction kernel, larger M the i8 matrix-core kernel. */
+ * reduction kernel (the arg-max epilogue at M <= 2, K <= 512: the decoder's
+ * logits kernel on the matrix cores), larger M the i8 matrix-core kernels. */
 int mnmt_qlinear(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias,
                  int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream);
+
+/* mnmt_qlinear with timing events (hipEvent_t, created with timing enabled,
+ * or NULL).  On the fused arg-max path (MNMT_EPI_ARGMAX, M <= 2, K <= 512:
+ * the decoder's logits kernel on int8 rows) the two events take the kernel's
+ * own start and end times (hipExtLaunchKernel), so their elapsed time is the
+ * kernel's duration without launch gaps; on other paths they are recorded on
+ * the stream before and after the launch. */
+int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias,
+                       int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream,
+                       void* ev_start, void* ev_stop);
 
 /* Folded requantization constants (host): scale[n] = s_in*s_w[n]/s_out,
  * bias[n] = b[n]/s_out, each computed in double and rounded once to fp32. */

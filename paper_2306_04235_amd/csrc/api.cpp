@@ -61,8 +61,18 @@ extern "C" int mnmt_model_get_info(const mnmt_model* model, mnmt_model_info* out
 
 extern "C" void mnmt_model_free(mnmt_model* model) { delete model; }
 
+extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias,
+                                  int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream,
+                                  void* ev_start, void* ev_stop);
+
 extern "C" int mnmt_qlinear(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias, int M,
                             int K, int N, int epilogue, float gamma, void* d_Y, void* stream) {
+  return mnmt_qlinear_timed(d_X, d_W, d_scale, d_bias, M, K, N, epilogue, gamma, d_Y, stream, nullptr, nullptr);
+}
+
+extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias,
+                                  int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream,
+                                  void* ev_start, void* ev_stop) {
   if (M < 0 || N < 1 || K < 64 || K % 64 || K > 8192)
     return set_error(MNMT_E_INVALID_ARG, "need M >= 0, N >= 1 and K a multiple of 64 in [64, 8192]");
   if (epilogue < MNMT_EPI_I32 || epilogue > MNMT_EPI_ARGMAX) return set_error(MNMT_E_INVALID_ARG, "unknown epilogue");
@@ -75,10 +85,30 @@ extern "C" int mnmt_qlinear(const int8_t* d_X, const int8_t* d_W, const float* d
     return set_error(MNMT_E_INVALID_ARG, "null device pointer");
   if (reinterpret_cast<uintptr_t>(d_X) % 16 || reinterpret_cast<uintptr_t>(d_W) % 16)
     return set_error(MNMT_E_INVALID_ARG, "X and W must be 16-byte aligned");
+  if (epilogue == MNMT_EPI_ARGMAX && step_logits_fits(M, K)) {
+    // the decoder's fused logits + arg-max kernel on int8 rows, one slot per row
+    StepLogits g{};
+    g.R = M;
+    g.d = K;
+    g.V = N;
+    g.E = static_cast<const int8_t*>(d_W);
+    g.c_out = d_scale;
+    g.slots = static_cast<unsigned long long*>(d_Y);
+    g.nslots = 1;
+    g.x_i8 = static_cast<const int8_t*>(d_X);
+    const hipError_t h = launch_step_logits(StepIn{}, g, static_cast<hipStream_t>(stream),
+                                            static_cast<hipEvent_t>(ev_start), static_cast<hipEvent_t>(ev_stop));
+    return h == hipSuccess ? MNMT_OK : hip_error(h, "qlinear launch");
+  }
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t h = ev_start ? hipEventRecord(static_cast<hipEvent_t>(ev_start), s) : hipSuccess;
+  if (h != hipSuccess) return hip_error(h, "qlinear start event");
   EpiArgs e{epilogue, d_Y, N, gamma, nullptr};
   if (epilogue == MNMT_EPI_ARGMAX) e = EpiArgs{EPI_LOGITS_ARGMAX, nullptr, N, 1.f, static_cast<unsigned long long*>(d_Y)};
-  const hipError_t h = launch_qlinear(d_X, K, d_W, d_scale, d_bias, M, K, N, e, static_cast<hipStream_t>(stream));
-  return h == hipSuccess ? MNMT_OK : hip_error(h, "qlinear launch");
+  h = launch_qlinear(d_X, K, d_W, d_scale, d_bias, M, K, N, e, s);
+  if (h != hipSuccess) return hip_error(h, "qlinear launch");
+  h = ev_stop ? hipEventRecord(static_cast<hipEvent_t>(ev_stop), s) : hipSuccess;
+  return h == hipSuccess ? MNMT_OK : hip_error(h, "qlinear stop event");
 }
 
 extern "C" int mnmt_fold_requant(float s_in, const float* s_w, const float* b, float s_out, int N, float* scale,

@@ -25,6 +25,8 @@
 // so each one issues all of its global loads (rows, parameters, weights, the
 // attention keys and values) before it waits for the first of them: the
 // kernel then pays about one memory round trip instead of one per phase.
+#include <hip/hip_ext.h>
+
 #include "blocks.hpp"
 #include "internal.h"
 
@@ -388,9 +390,10 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
 }
 
 // Output projection over the shared embedding with the fused arg-max: each
-// wave takes kLogitsTiles tiles of 16 vocabulary rows.
+// wave takes kLogitsTiles tiles of 16 vocabulary rows.  RAW: the rows are
+// int8 codes already (g.x_i8) instead of the residual stream.
 constexpr int kLogitsTiles = 2;
-template <int DMAX>
+template <int DMAX, bool RAW>
 __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLogits g) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;
@@ -402,7 +405,9 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   const int l16 = lane & 15, kq = lane >> 4;
   const int row0 = (blockIdx.x * 4 + wave) * TPW * 16;
   RowRegs<NJ> rr;
-  load_row(in, min(wave, R - 1), d, rr);
+  if (!RAW) load_row(in, min(wave, R - 1), d, rr);
+  v4i xr = {0, 0, 0, 0};
+  if (RAW) xr = *(const v4i*)(g.x_i8 + (size_t)min(wave, R - 1) * d + 16 * min(lane, d / 16 - 1));
   v4i wf[TPW][KS];
   float co[TPW];
 #pragma unroll
@@ -412,8 +417,12 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     for (int kk = 0; kk < KS; ++kk) wf[t][kk] = *(const v4i*)(g.E + n * d + 64 * min(kk, ks - 1) + 16 * kq);
     co[t] = g.c_out[n];
   }
-  clear_acc(in);
-  if (wave < R) finish_row(in, wave, d, rr, a_lds);
+  if (!RAW) {
+    clear_acc(in);
+    if (wave < R) finish_row(in, wave, d, rr, a_lds);
+  } else if (wave < R && lane < d / 16) {
+    *(v4i*)(a_lds + wave * d + 16 * lane) = xr;
+  }
   __syncthreads();
   const int arow = l16 < R ? l16 : 0;
   v4i af[KS];
@@ -450,7 +459,9 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     unsigned long long b = wmax[0][m];
 #pragma unroll
     for (int w = 1; w < 4; ++w) b = wmax[w][m] > b ? wmax[w][m] : b;
-    if (b != 0ull) atomicMax(g.slots + m * g.nslots + blockIdx.x % g.nslots, b);
+    // the slot usually holds a larger key already: test before the atomic
+    unsigned long long* slot = g.slots + m * g.nslots + blockIdx.x % g.nslots;
+    if (b > __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(slot, b);
   }
 }
 
@@ -460,6 +471,8 @@ bool step_path_fits(int R, int d, int dh, int F, int T, int S) {
   return R >= 1 && R <= kStepRows && d <= 512 && d % 64 == 0 && dh <= kStepHeadDim && dh % 16 == 0 &&
          F % kFfnChunk == 0 && T <= kStepMaxLen && S <= kStepMaxLen;
 }
+
+bool step_logits_fits(int R, int d) { return R >= 1 && R <= kStepRows && d % 64 == 0 && d >= 64 && d <= 512; }
 
 #define MNMT_BY_D(d, CALL)            \
   switch (row_class(d)) {             \
@@ -496,10 +509,18 @@ hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s) {
+hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s, hipEvent_t ev_start,
+                              hipEvent_t ev_stop) {
   const int rpb = 4 * kLogitsTiles * 16;  // rows per block
   const int blocks = (g.V + rpb - 1) / rpb;
-#define MNMT_LOGITS(DM) hipLaunchKernelGGL((k_step_logits<DM>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);
+#define MNMT_LOGITS(DM)                                                                                       \
+  if (g.x_i8 && (ev_start || ev_stop))                                                                        \
+    hipExtLaunchKernelGGL((k_step_logits<DM, true>), dim3(blocks), dim3(kStepThreads), 0, s, ev_start, ev_stop, 0, \
+                          in, g);                                                                             \
+  else if (g.x_i8)                                                                                            \
+    hipLaunchKernelGGL((k_step_logits<DM, true>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);             \
+  else                                                                                                        \
+    hipLaunchKernelGGL((k_step_logits<DM, false>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);
   MNMT_BY_D(g.d, MNMT_LOGITS)
 #undef MNMT_LOGITS
   return hipGetLastError();

@@ -172,11 +172,15 @@ struct StepLogits {
   float* logits;           // [R, V] or null
   unsigned long long* slots;
   int nslots;
+  const int8_t* x_i8;      // int8 rows [R, d] instead of the StepIn rows (or null)
 };
 bool step_path_fits(int R, int d, int dh, int F, int T, int S);
+bool step_logits_fits(int R, int d);  // R <= 2, d a multiple of 64 up to 512
 hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s);
 hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s);
-hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s);
+// With ev_start / ev_stop the events take the kernel's own start and end times.
+hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s, hipEvent_t ev_start = nullptr,
+                              hipEvent_t ev_stop = nullptr);
 // Small-M GEMM (M <= 64, K <= 1024) on 16x16x64 matrix cores; with `in` the
 // rows are prepared (embedding / LayerNorm / quantization) in its prologue.
 bool qgemm_small_fits(int M, int K);

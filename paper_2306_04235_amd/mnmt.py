@@ -18,7 +18,7 @@ EPI_I32, EPI_I8, EPI_I8_RELU, EPI_F32, EPI_F32_RESID, EPI_LOGITS, EPI_ARGMAX = r
 
 EXPORTS = ("mnmt_model_bytes", "mnmt_model_load", "mnmt_model_get_info", "mnmt_model_free", "mnmt_session_bytes",
            "mnmt_session_create", "mnmt_session_free", "mnmt_encode", "mnmt_decode_step", "mnmt_translate",
-           "mnmt_session_tensor", "mnmt_qlinear", "mnmt_fold_requant", "mnmt_debug_canon", "mnmt_status_str",
+           "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed", "mnmt_fold_requant", "mnmt_debug_canon", "mnmt_status_str",
            "mnmt_last_error")
 
 
@@ -70,6 +70,7 @@ def lib():
         L.mnmt_translate.argtypes = [vp, vp, vp, i32, i32, C.POINTER(SearchCfg), vp, vp, vp, vp]
         L.mnmt_session_tensor.argtypes = [vp, C.c_char_p, C.POINTER(vp), C.POINTER(sz)]
         L.mnmt_qlinear.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp]
+        L.mnmt_qlinear_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp, vp, vp]
         L.mnmt_fold_requant.argtypes = [f32, vp, vp, f32, i32, vp, vp]
         L.mnmt_debug_canon.argtypes = [i32, vp, i32, vp, vp]
         L.mnmt_status_str.argtypes = [i32]
@@ -128,6 +129,21 @@ def mnmt_qlinear(X, W, scale, bias, epilogue, gamma=1.0, out=None, stream=None):
         out = torch.empty((M, N), dtype=dt, device=X.device)
     _check(lib().mnmt_qlinear(_ptr(X), _ptr(W), _ptr(scale), _ptr(bias), M, K, N, epilogue, float(gamma),
                               _ptr(out), _stream(stream)), "mnmt_qlinear")
+    return out
+
+
+def mnmt_qlinear_timed(X, W, scale, bias, epilogue, ev_start, ev_stop, gamma=1.0, out=None, stream=None):
+    """mnmt_qlinear bracketed by two torch.cuda.Event(enable_timing=True)
+    (recorded once beforehand so that their HIP events exist)."""
+    import torch
+
+    M, K = X.shape
+    N = W.shape[0]
+    if out is None:
+        out = torch.zeros(M, dtype=torch.int64, device=X.device)
+    _check(lib().mnmt_qlinear_timed(_ptr(X), _ptr(W), _ptr(scale), _ptr(bias), M, K, N, epilogue, float(gamma),
+                                    _ptr(out), _stream(stream), C.c_void_p(ev_start.cuda_event),
+                                    C.c_void_p(ev_stop.cuda_event)), "mnmt_qlinear_timed")
     return out
 
 

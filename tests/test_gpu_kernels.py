@@ -115,6 +115,52 @@ def test_qlinear_all_epilogues(torch_dev, M, K, N):
     assert np.array_equal(got[rows].view(np.uint32), ref.view(np.uint32))
 
 
+@pytest.mark.parametrize("M,K,N", [(1, 256, 32000), (2, 512, 32000), (1, 64, 1000), (2, 128, 33), (1, 384, 129),
+                                   (3, 256, 1000), (8, 1024, 4097), (2, 1024, 500)], ids=lambda v: str(v))
+def test_qlinear_fused_argmax(torch_dev, M, K, N):
+    # M <= 2 with K <= 512 runs the decoder's logits kernel (matrix cores, one
+    # slot per row); other shapes run the GEMV.  Rows of W are duplicated so
+    # that the maximum is tied and the smallest index must win.
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    print(f"qlinear ARGMAX M={M} K={K} N={N}", flush=True)
+    X, W, mult, _ = G.sweep_case(M, K, N, seed=7)
+    rng = np.random.default_rng(N)
+    dq = (mult * 1e-3).astype(np.float32)
+    ref_z = oracle.qlinear(X, W, dq, None, oracle.EPI_LOGITS)
+    for m in range(M):  # copy each row's winner to a later and an earlier index
+        best = int(np.argmax(ref_z[m]))
+        for dst in {int(rng.integers(0, N)), N - 1}:
+            W[dst] = W[best]
+            dq[dst] = dq[best]
+    ref_z = oracle.qlinear(X, W, dq, None, oracle.EPI_LOGITS)
+    got = _run(torch, dev, X, W, dq, None, mnmt.EPI_ARGMAX)
+    idx = mnmt.argmax_index(got)
+    assert np.array_equal(idx, np.argmax(ref_z, axis=1))  # numpy: the first maximum
+    # the key holds the maximum logit itself
+    keys = (got.astype(np.int64) >> 32) & 0xFFFFFFFF
+    bits = np.where(keys & 0x80000000, keys & 0x7FFFFFFF, ~keys & 0xFFFFFFFF).astype(np.uint32)
+    assert np.array_equal(bits.view(np.float32), ref_z.max(axis=1))
+
+
+def test_qlinear_timed_matches_and_times_the_kernel(torch_dev):
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    for M, K, N, epi in ((1, 256, 32000, mnmt.EPI_ARGMAX), (4, 256, 1024, mnmt.EPI_ARGMAX)):
+        X, W, mult, _ = G.sweep_case(M, K, N, seed=5)
+        tX, tW, ts = _gpu(torch, dev, X), _gpu(torch, dev, W), _gpu(torch, dev, (mult * 1e-3).astype(np.float32))
+        ref = mnmt.mnmt_qlinear(tX, tW, ts, None, epi)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        e1.record()
+        got = mnmt.mnmt_qlinear_timed(tX, tW, ts, None, epi, e0, e1)
+        e1.synchronize()
+        assert torch.equal(got, ref)
+        assert 0.0 < e0.elapsed_time(e1) < 100.0
+
+
 def test_qlinear_worst_case_accumulator(torch_dev):
     torch, dev = torch_dev
     from paper_2306_04235_amd import mnmt
