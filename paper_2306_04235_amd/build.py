@@ -22,13 +22,15 @@ COMMON = ["-O3", "-fPIC", "-std=c++17", "-ffp-contract=off", "-Wall", "-Wno-unus
           "-I" + os.path.join(os.path.dirname(HERE), "include")]
 DEVICE = [f"--offload-arch={ARCH}", "-fno-gpu-flush-denormals-to-zero", "-fhip-fp32-correctly-rounded-divide-sqrt",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-SOURCES = ["qlinear.hip", "kernels.hip", "decode_fused.hip", "decode_step.hip", "model.cpp", "session.cpp", "api.cpp"]
+# per-file device flags: the GEMM keeps its matrix-core accumulators in VGPRs
+EXTRA = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+SOURCES = ["qlinear.hip", "kernels.hip", "decode_fused.hip", "decode_step.hip", "gemm.hip", "model.cpp", "session.cpp", "api.cpp"]
 
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD, src + ".o")
     path = os.path.join(CSRC, src)
-    flags = COMMON + (DEVICE if src.endswith(".hip") else ["-D__HIP_PLATFORM_AMD__"])
+    flags = COMMON + (DEVICE + EXTRA.get(src, []) if src.endswith(".hip") else ["-D__HIP_PLATFORM_AMD__"])
     lang = ["-x", "hip"] if src.endswith(".hip") else []
     cmd = [HIPCC, *flags, *lang, "-c", path, "-o", obj]
     if verbose:

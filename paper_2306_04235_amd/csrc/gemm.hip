@@ -1,0 +1,290 @@
+// gemm.hip -- int8 GEMM with fused epilogues for more than 64 rows (the
+// batched encoder, beam decoding and the quantized-linear sweep), on the i8
+// matrix cores: Y[m, n] = epilogue(sum_k X[m, k] W[n, k]) (Section 4.1's 8-bit
+// GEMM; the epilogues of Section 4.2 applied as the tile is written).
+//
+// Tiles.  A 256-thread block owns a BN x BM tile of (output column n, row m);
+// its 4 waves split it WN x WM.  K is walked in 64-byte slabs staged through
+// LDS with double buffering: the next slab's global loads are in flight while
+// the current one feeds v_mfma_i32_32x32x32_i8, one LDS barrier per slab.
+// Loads clamp their row index instead of branching, so rows past M or N read
+// valid memory and produce outputs that are never stored.
+//
+// Operand order.  W is the MFMA A operand and X the B operand, so a 32x32
+// accumulator holds D[n][m]: element r of lane l is column n = 8 (r / 4) +
+// 4 (l / 32) + r % 4 of row m = l % 32, four consecutive columns per r / 4.
+// For int8 outputs two v_permlane32_swap exchanges between lanes l and l + 32
+// leave each lane with 16 consecutive columns of one row, written by one
+// 16-byte store; fp32 and int32 outputs are written 4 columns per store.
+//
+// Accumulators live in VGPRs (the file is built with the MFMA VGPR form), so
+// the epilogue reads them without accumulator-register moves.
+//
+// Placement.  Blocks are dispatched to the 8 XCDs round-robin; the linear
+// block id is remapped so that each XCD works through one contiguous range of
+// tiles (m fastest), which keeps the W and X tiles it shares in its own L2.
+#include "blocks.hpp"
+#include "internal.h"
+
+namespace mnmt {
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+constexpr int kBK = 64;            // K bytes per slab
+constexpr int kLdsRow = kBK + 16;  // padded LDS row (spreads rows over banks)
+constexpr int kXcds = 8;
+
+// clamp(rint(y), -127, 127) in the low byte: after the clamp, adding 1.5 * 2^23
+// rounds to an integer (round half to even, as rintf) and leaves it in the
+// low mantissa bits in two's complement.  NaN clamps to -127 as in code_of.
+__device__ __forceinline__ uint32_t code_bits(float y) {
+  return __float_as_uint(fminf(fmaxf(y, -127.0f), 127.0f) + 12582912.0f);
+}
+__device__ __forceinline__ uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  return (a & 0xffu) | ((b & 0xffu) << 8) | ((c & 0xffu) << 16) | (d << 24);
+}
+
+template <int EPI>
+__device__ __forceinline__ float epi_value(int acc, float sc, float bi) {
+  const float a = (float)acc;
+  if (EPI == MNMT_EPI_LOGITS) return a * sc;
+  const float y = fmaf(a, sc, bi);
+  return EPI == MNMT_EPI_I8_RELU ? fmaxf(y, 0.0f) : y;
+}
+
+// Writes one 32x32 accumulator fragment (columns nb .. nb + 31, this lane's
+// row m = row of lane l % 32).  FAST: the whole fragment is inside the output
+// and rows are 16-byte aligned, so no lane checks anything.
+template <int EPI, bool FAST>
+__device__ __forceinline__ void store_fragment(const EpiArgs& e, const v16i& c, const float (&sc)[4][4],
+                                               const float (&bi)[4][4], int m, int nb, int h, int M, int N) {
+  constexpr bool INT8_OUT = EPI == MNMT_EPI_I8 || EPI == MNMT_EPI_I8_RELU;
+  if (INT8_OUT) {
+    uint32_t w4[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      uint32_t q[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) q[t] = code_bits(epi_value<EPI>(c[4 * g + t], sc[g][t], bi[g][t]));
+      w4[g] = pack4(q[0], q[1], q[2], q[3]);
+    }
+    // lanes l and l + 32 trade groups (the upper half of the first operand
+    // with the lower half of the second): lane l ends with columns
+    // nb + 0..15, lane l + 32 with nb + 16..31, 4 columns per word
+    const auto s02 = __builtin_amdgcn_permlane32_swap(w4[0], w4[2], false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap(w4[1], w4[3], false, false);
+    const uint32_t o[4] = {s02[0], s02[1], s13[0], s13[1]};
+    const int n = nb + 16 * h;
+    int8_t* y = (int8_t*)e.out + (size_t)m * e.ldo + n;
+    if (FAST) {
+      *(v4i*)y = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
+    } else if (m < M) {
+#pragma unroll
+      for (int t = 0; t < 16; ++t)
+        if (n + t < N) y[t] = (int8_t)(o[t >> 2] >> (8 * (t & 3)));
+    }
+    return;
+  }
+  if (!FAST && m >= M) return;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int n = nb + 8 * g + 4 * h;
+    if (EPI == MNMT_EPI_I32) {
+      int* y = (int*)e.out + (size_t)m * e.ldo + n;
+      if (FAST) {
+        *(v4i*)y = v4i{c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]};
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          if (n + t < N) y[t] = c[4 * g + t];
+      }
+    } else {
+      float* y = (float*)e.out + (size_t)m * e.ldo + n;
+      v4f v;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) v[t] = epi_value<EPI>(c[4 * g + t], sc[g][t], bi[g][t]);
+      if (FAST) {
+        if (EPI == MNMT_EPI_F32_RESID) {
+          const v4f old = *(const v4f*)y;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = fmaf(e.gamma, old[t], v[t]);
+        }
+        *(v4f*)y = v;
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          if (n + t < N) y[t] = EPI == MNMT_EPI_F32_RESID ? fmaf(e.gamma, y[t], v[t]) : v[t];
+      }
+    }
+  }
+}
+
+template <int BN, int BM, int WN, int WM, int EPI>
+__global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int ldx, const int8_t* __restrict__ W,
+                                              int M, int K, int N, const float* __restrict__ scale,
+                                              const float* __restrict__ bias, EpiArgs e, int tiles_m, int tiles) {
+  static_assert(WN * WM == 4, "4 waves");
+  constexpr int TN = BN / WN, TM = BM / WM;  // wave tile
+  constexpr int FN = TN / 32, FM = TM / 32;  // 32x32 fragments per wave
+  static_assert(FN >= 1 && FM >= 1, "whole fragments");
+  constexpr int CW = BN * (kBK / 16) / 256, CX = BM * (kBK / 16) / 256;  // 16-byte chunks per thread
+  static_assert(CW >= 1 && CX >= 1, "every thread loads");
+  constexpr bool INT8_OUT = EPI == MNMT_EPI_I8 || EPI == MNMT_EPI_I8_RELU;
+  __shared__ __attribute__((aligned(16))) int8_t Ws[2][BN * kLdsRow];
+  __shared__ __attribute__((aligned(16))) int8_t Xs[2][BM * kLdsRow];
+  __shared__ float sc_lds[BN], bi_lds[BN];  // the tile's epilogue constants
+
+  // tile of this block: XCD x takes tiles [x * per, (x + 1) * per), m fastest
+  const int b = blockIdx.x;
+  const int per = (tiles + kXcds - 1) / kXcds;
+  const int tile = (b % kXcds) * per + b / kXcds;
+  if (tile >= tiles) return;  // the grid is rounded up to whole XCD ranges
+  const int m0 = (tile % tiles_m) * BM, n0 = (tile / tiles_m) * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn = wave / WM, wm = wave % WM;
+  const int l32 = lane & 31, h = lane >> 5;
+
+  if (EPI != MNMT_EPI_I32) {
+    for (int c = tid; c < BN; c += 256) {
+      const int n = min(n0 + c, N - 1);
+      sc_lds[c] = scale[n];
+      bi_lds[c] = EPI == MNMT_EPI_LOGITS ? 0.0f : bias[n];
+    }
+  }
+
+  // 32-bit offsets of this thread's 16-byte chunks (the slab adds k0)
+  uint32_t ow[CW], ox[CX];
+#pragma unroll
+  for (int i = 0; i < CW; ++i) {
+    const int c = tid + 256 * i;
+    ow[i] = (uint32_t)min(n0 + (c >> 2), N - 1) * (uint32_t)K + 16 * (c & 3);
+  }
+#pragma unroll
+  for (int i = 0; i < CX; ++i) {
+    const int c = tid + 256 * i;
+    ox[i] = (uint32_t)min(m0 + (c >> 2), M - 1) * (uint32_t)ldx + 16 * (c & 3);
+  }
+  v4i rw[CW], rx[CX];
+  auto gload = [&](int k0) {
+    const int8_t* wk = W + k0;
+    const int8_t* xk = X + k0;
+#pragma unroll
+    for (int i = 0; i < CW; ++i) rw[i] = *(const v4i*)(wk + ow[i]);
+#pragma unroll
+    for (int i = 0; i < CX; ++i) rx[i] = *(const v4i*)(xk + ox[i]);
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < CW; ++i) {
+      const int c = tid + 256 * i;
+      *(v4i*)(&Ws[buf][(c >> 2) * kLdsRow + 16 * (c & 3)]) = rw[i];
+    }
+#pragma unroll
+    for (int i = 0; i < CX; ++i) {
+      const int c = tid + 256 * i;
+      *(v4i*)(&Xs[buf][(c >> 2) * kLdsRow + 16 * (c & 3)]) = rx[i];
+    }
+  };
+
+  v16i acc[FN][FM];
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int i = 0; i < FM; ++i) acc[j][i] = v16i{};
+
+  const int slabs = K / kBK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int s = 0; s < slabs; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < slabs) gload((s + 1) * kBK);
+#pragma unroll
+    for (int kk = 0; kk < kBK; kk += 32) {
+      v4i a[FN], bx[FM];
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        a[j] = *(const v4i*)(&Ws[buf][(wn * TN + 32 * j + l32) * kLdsRow + kk + 16 * h]);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        bx[i] = *(const v4i*)(&Xs[buf][(wm * TM + 32 * i + l32) * kLdsRow + kk + 16 * h]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int i = 0; i < FM; ++i) acc[j][i] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[j], bx[i], acc[j][i], 0, 0, 0);
+    }
+    if (s + 1 < slabs) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  // epilogue: whole fragments take the check-free path
+  const bool aligned = INT8_OUT ? (e.ldo % 16 == 0 && (reinterpret_cast<uintptr_t>(e.out) & 15) == 0)
+                                : (e.ldo % 4 == 0 && (reinterpret_cast<uintptr_t>(e.out) & 15) == 0);
+#pragma unroll
+  for (int j = 0; j < FN; ++j) {
+    const int cb = wn * TN + 32 * j;  // fragment's first column within the tile
+    float sc[4][4], bi[4][4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const v4f s4 = *(const v4f*)(sc_lds + cb + 8 * g + 4 * h);
+      const v4f b4 = *(const v4f*)(bi_lds + cb + 8 * g + 4 * h);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        sc[g][t] = EPI == MNMT_EPI_I32 ? 0.0f : s4[t];
+        bi[g][t] = EPI == MNMT_EPI_I32 ? 0.0f : b4[t];
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int mb = m0 + wm * TM + 32 * i;
+      const bool fast = aligned && n0 + cb + 32 <= N && mb + 32 <= M;  // uniform over the wave
+      if (fast)
+        store_fragment<EPI, true>(e, acc[j][i], sc, bi, mb + l32, n0 + cb, h, M, N);
+      else
+        store_fragment<EPI, false>(e, acc[j][i], sc, bi, mb + l32, n0 + cb, h, M, N);
+    }
+  }
+}
+
+template <int BN, int BM, int WN, int WM>
+hipError_t launch_cfg(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
+                      int N, const EpiArgs& e, hipStream_t s) {
+  const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+  const int tiles = tiles_m * tiles_n;
+  const int grid = (tiles + kXcds - 1) / kXcds * kXcds;
+#define MNMT_GEMM(EPI)                                                                                          \
+  hipLaunchKernelGGL((k_gemm<BN, BM, WN, WM, EPI>), dim3(grid), dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, \
+                     e, tiles_m, tiles)
+  switch (e.kind) {
+    case MNMT_EPI_I32: MNMT_GEMM(MNMT_EPI_I32); break;
+    case MNMT_EPI_I8: MNMT_GEMM(MNMT_EPI_I8); break;
+    case MNMT_EPI_I8_RELU: MNMT_GEMM(MNMT_EPI_I8_RELU); break;
+    case MNMT_EPI_F32: MNMT_GEMM(MNMT_EPI_F32); break;
+    case MNMT_EPI_F32_RESID: MNMT_GEMM(MNMT_EPI_F32_RESID); break;
+    case MNMT_EPI_LOGITS: MNMT_GEMM(MNMT_EPI_LOGITS); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef MNMT_GEMM
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// The largest tile that still gives about two blocks per CU (256 CUs).
+hipError_t launch_gemm(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
+                       int N, const EpiArgs& e, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (K % kBK) return hipErrorInvalidValue;
+  auto tiles = [&](int bn, int bm) { return (long)((N + bn - 1) / bn) * ((M + bm - 1) / bm); };
+  constexpr long kFill = 512;
+  if (tiles(256, 128) >= kFill) return launch_cfg<256, 128, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (tiles(128, 128) >= kFill) return launch_cfg<128, 128, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (tiles(128, 64) >= kFill) return launch_cfg<128, 64, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+  return launch_cfg<64, 64, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+}
+
+}  // namespace mnmt

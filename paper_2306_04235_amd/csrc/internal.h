@@ -34,6 +34,9 @@ struct EpiArgs {
   unsigned long long* argmax;  // [M] packed (value, ~index) maxima for ARGMAX
 };
 
+// Tiled matrix-core GEMM for large M (gemm.hip); K a multiple of 64.
+hipError_t launch_gemm(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
+                       int N, const EpiArgs& e, hipStream_t s);
 // Y = epilogue(X[M,K] . W[N,K]^T); ldx = row stride of X in bytes.
 hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias,
                           int M, int K, int N, const EpiArgs& e, hipStream_t s);

@@ -9,8 +9,9 @@
 //    instruction reads 64 * 16 = 1024 contiguous bytes; U independent row
 //    groups per wave keep several loads in flight.  Products use the 4-way
 //    int8 dot instruction; the LPR partial sums meet in an xor butterfly.
-//  * qgemm: M > 8.  i8 matrix cores (v_mfma_i32_32x32x32_i8) on 64-deep K
-//    slabs staged in LDS; each of the 4 waves owns a tile of 32x32 fragments.
+//  * qgemm_small: 8 < M <= 64 and K <= 1024 (the batch-1 encoder), 16x16x64
+//    matrix-core fragments loaded straight from memory.
+// Larger M runs the tiled matrix-core GEMM of gemm.hip.
 // Integer accumulation is exact, so neither kernel's order matters; the fp32
 // epilogue is the same single expression in both.
 #include "blocks.hpp"
@@ -20,7 +21,6 @@ namespace mnmt {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
 
 // The fused epilogue of one output element (row m, column n).
 __device__ __forceinline__ void epilogue_store(const EpiArgs& e, int m, int n, int acc, const float* scale,
@@ -156,99 +156,6 @@ hipError_t gemv_lpr(const int8_t* X, int ldx, const int8_t* W, const float* scal
 }
 
 // ---------------------------------------------------------------------------
-// qgemm: BM x BN output tile per 256-thread block, 64-deep K slabs in LDS.
-template <int BM, int BN, int WAVES_M>
-__global__ __launch_bounds__(256) void k_qgemm(const int8_t* __restrict__ X, int ldx, const int8_t* __restrict__ W,
-                                               int M, int K, int N, const float* __restrict__ scale,
-                                               const float* __restrict__ bias, EpiArgs e) {
-  constexpr int BK = 64;
-  constexpr int LDS_STRIDE = BK + 16;  // bytes; the pad spreads rows over LDS banks
-  constexpr int WAVES_N = 4 / WAVES_M;
-  constexpr int WTM = BM / WAVES_M, WTN = BN / WAVES_N;
-  constexpr int FM = WTM / 32, FN = WTN / 32;
-  static_assert(FM >= 1 && FN >= 1, "wave tile must hold whole 32x32 fragments");
-  __shared__ __attribute__((aligned(16))) int8_t As[BM * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) int8_t Bs[BN * LDS_STRIDE];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  v16i acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0;
-
-  constexpr int A_CHUNKS = BM * (BK / 16), B_CHUNKS = BN * (BK / 16);
-  int4 ra[(A_CHUNKS + 255) / 256], rb[(B_CHUNKS + 255) / 256];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < (A_CHUNKS + 255) / 256; ++i) {
-      const int c = tid + i * 256;
-      const int r = c >> 2, kc = (c & 3) * 16;
-      ra[i] = (c < A_CHUNKS && m0 + r < M) ? *(const int4*)(X + (size_t)(m0 + r) * ldx + k0 + kc)
-                                            : make_int4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < (B_CHUNKS + 255) / 256; ++i) {
-      const int c = tid + i * 256;
-      const int r = c >> 2, kc = (c & 3) * 16;
-      rb[i] = (c < B_CHUNKS && n0 + r < N) ? *(const int4*)(W + (size_t)(n0 + r) * K + k0 + kc)
-                                            : make_int4(0, 0, 0, 0);
-    }
-  };
-  auto lstore = [&]() {
-#pragma unroll
-    for (int i = 0; i < (A_CHUNKS + 255) / 256; ++i) {
-      const int c = tid + i * 256;
-      if (c < A_CHUNKS) *(int4*)(As + (c >> 2) * LDS_STRIDE + (c & 3) * 16) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < (B_CHUNKS + 255) / 256; ++i) {
-      const int c = tid + i * 256;
-      if (c < B_CHUNKS) *(int4*)(Bs + (c >> 2) * LDS_STRIDE + (c & 3) * 16) = rb[i];
-    }
-  };
-
-  gload(0);
-  for (int k0 = 0; k0 < K; k0 += BK) {
-    __syncthreads();  // previous slab fully consumed
-    lstore();
-    __syncthreads();
-    if (k0 + BK < K) gload(k0 + BK);  // prefetch the next slab while computing
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 32) {
-      v4i a[FM], b[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        a[i] = *(const v4i*)(As + (wm * WTM + i * 32 + (lane & 31)) * LDS_STRIDE + kk + (lane >> 5) * 16);
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        b[j] = *(const v4i*)(Bs + (wn * WTN + j * 32 + (lane & 31)) * LDS_STRIDE + kk + (lane >> 5) * 16);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-  }
-  // Fragment layout: element r of lane l sits at row 8*(r/4) + 4*(l/32) + r%4, column l%32.
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-      const int col = n0 + wn * WTN + j * 32 + (lane & 31);
-      if (col >= N) continue;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < M) epilogue_store(e, row, col, acc[i][j][r], scale, bias);
-      }
-    }
-}
-
-// ---------------------------------------------------------------------------
 // qgemm_small: M <= 64, K <= 1024 (the batch-1 encoder).  A 32x32 output tile
 // per block, one 16x16 tile per wave on v_mfma_i32_16x16x64_i8.  Each lane's
 // operand is 16 contiguous K bytes of one row, so weight fragments are loaded
@@ -306,14 +213,6 @@ __global__ __launch_bounds__(256) void k_qgemm_small(FusedIn in, const int8_t* _
   }
 }
 
-template <int BM, int BN, int WAVES_M>
-hipError_t gemm_launch(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
-                       int K, int N, const EpiArgs& e, hipStream_t s) {
-  dim3 grid((N + BN - 1) / BN, (M + BM - 1) / BM);
-  hipLaunchKernelGGL((k_qgemm<BM, BN, WAVES_M>), grid, dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, e);
-  return hipGetLastError();
-}
-
 }  // namespace
 
 bool qgemm_small_fits(int M, int K) { return M >= 1 && M <= 64 && K <= kSmallMaxK && K % 64 == 0; }
@@ -351,9 +250,7 @@ hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float
   }
   if (e.kind == EPI_LOGITS_ARGMAX) return hipErrorInvalidValue;  // arg-max fusion is a batch-1 path
   if (qgemm_small_fits(M, K)) return launch_qgemm_small(nullptr, X, ldx, W, scale, bias, M, K, N, e, s);
-  if (M <= 32) return gemm_launch<32, 128, 1>(X, ldx, W, scale, bias, M, K, N, e, s);
-  if (M <= 64) return gemm_launch<64, 128, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
-  return gemm_launch<128, 128, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+  return launch_gemm(X, ldx, W, scale, bias, M, K, N, e, s);
 }
 
 }  // namespace mnmt
