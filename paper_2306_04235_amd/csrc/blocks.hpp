@@ -14,6 +14,15 @@ constexpr int kMaxAttnLen = 256;  // longest attended sequence (4 keys per lane)
 constexpr int kMaxHeadDim = 128;  // 8 x 16 bytes of query in registers
 constexpr int kMaxRowLen = 1024;  // LayerNorm width (16 values per lane)
 
+// 16 bytes as a native vector (copied as a value, never through memory)
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+// One v_mfma_i32_16x16x64_i8: lane l holds 16 bytes of K at 16 (l / 16) of
+// row l % 16 of A and of B; D[i] of lane l is row 4 (l / 16) + i, column l % 16.
+__device__ __forceinline__ v4i mfma16(const v4i a, const v4i b, const v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
   acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
   acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
@@ -28,6 +37,31 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// LayerNorm of one row held by a wave (element i = lane + 64 j in v[j]) in
+// the canonical order: lane partials over ascending i, then the butterfly.
+template <int NJ>
+__device__ __forceinline__ void ln_row(float (&v)[NJ], const float (&g)[NJ], const float (&b)[NJ], int d, float eps) {
+  const int lane = threadIdx.x & 63;
+  const float inv_d = 1.0f / (float)d;
+  float p = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    if (lane + 64 * j < d) p = p + v[j];
+  const float mu = wave_sum(p) * inv_d;
+  float p2 = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    if (lane + 64 * j < d) {
+      v[j] = v[j] - mu;
+      p2 = fmaf(v[j], v[j], p2);
+    }
+  }
+  const float rstd = 1.0f / sqrtf(wave_sum(p2) * inv_d + eps);
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+    if (lane + 64 * j < d) v[j] = fmaf(v[j] * rstd, g[j], b[j]);
 }
 
 // LDS one wave's attention needs: softmax weights and the value rows.

@@ -38,8 +38,6 @@ constexpr int kStepMaxLen = 128; // longest self / cross attention
 constexpr int kStepHeadDim = 64; // widest head
 constexpr int kFfnChunk = 64;    // hidden units per k_step_ffn block
 
-// 16 bytes as a native vector (copied as a value, never through memory)
-typedef int v4i __attribute__((ext_vector_type(4)));
 
 // What the wave preparing one input row loads at kernel start.
 template <int NJ>
@@ -69,31 +67,6 @@ __device__ __forceinline__ void load_row(const StepIn& in, int r, int d, RowRegs
     q.g[j] = in.ln_g[i];
     q.b[j] = in.ln_b[i];
   }
-}
-
-// LayerNorm of one row held by a wave (element i = lane + 64 j in v[j]) in
-// the canonical order: lane partials over ascending i, then the butterfly.
-template <int NJ>
-__device__ __forceinline__ void ln_row(float (&v)[NJ], const float (&g)[NJ], const float (&b)[NJ], int d, float eps) {
-  const int lane = threadIdx.x & 63;
-  const float inv_d = 1.0f / (float)d;
-  float p = 0.0f;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j)
-    if (lane + 64 * j < d) p = p + v[j];
-  const float mu = wave_sum(p) * inv_d;
-  float p2 = 0.0f;
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    if (lane + 64 * j < d) {
-      v[j] = v[j] - mu;
-      p2 = fmaf(v[j], v[j], p2);
-    }
-  }
-  const float rstd = 1.0f / sqrtf(wave_sum(p2) * inv_d + eps);
-#pragma unroll
-  for (int j = 0; j < NJ; ++j)
-    if (lane + 64 * j < d) v[j] = fmaf(v[j] * rstd, g[j], b[j]);
 }
 
 // Finishes row r from the loaded registers: the pending residual update, the LayerNorm, the store of the updated residual row
@@ -137,9 +110,6 @@ __device__ __forceinline__ void clear_acc(const StepIn& in) {
 // reductions, and these kernels are bound by instruction issue, not by
 // memory.  Fragment layout: lane l holds 16 bytes of K at 16 (l / 16) of
 // row l % 16 (of the activations for A, of the weights for B).
-__device__ __forceinline__ v4i mfma16(const v4i a, const v4i b, const v4i c) {
-  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
-}
 
 // One block per head.  DMAX: model width class; NI: attended positions per
 // lane (n <= 64 NI).
@@ -157,7 +127,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   const int hd = blockIdx.x;
   const int R = at.R, d = at.d, dh = at.dh, nc = dh / 16, ks = d / 64;
   const int ntile = (SELF ? 3 : 1) * dh / 16;  // projection tiles of this head
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
   // 1. every global load, none conditional: the wave's input row, the
   //    projection's weight fragments with their scales and biases, the W_o
@@ -342,7 +312,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
   __shared__ __attribute__((aligned(16))) int8_t h[kStepRows][kFfnChunk];
   const int R = f.R, d = f.d, F = f.F, ks = d / 64;
   const int f0 = blockIdx.x * kFfnChunk;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
   RowRegs<NJ> rr;
   load_row(in, min(wave, R - 1), d, rr);
@@ -401,7 +371,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
   __shared__ unsigned long long wmax[4][kStepRows];
   const int R = g.R, d = g.d, N = g.V, ks = d / 64;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
   const int row0 = (blockIdx.x * 4 + wave) * TPW * 16;
   RowRegs<NJ> rr;

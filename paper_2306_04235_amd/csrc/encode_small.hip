@@ -1,0 +1,482 @@
+// encode_small.hip -- the encoder for at most 64 rows (a batch-1 source, or a
+// few short ones) in 2 kernels per layer plus one for the output:
+//   k_enc_attn (one block per head): [pending residual update + LayerNorm +
+//       quantization of all rows] -> the head's Q, K, V rows on the matrix
+//       cores -> attention within each sentence -> the head's context times
+//       its columns of W_o, added to an int32 accumulator
+//   k_enc_ffn (one block per 64 hidden units): [pending update + LayerNorm +
+//       quantization] -> the chunk of W1 with the ReLU requantization -> the
+//       chunk's columns of W2 into an int32 accumulator
+//   k_enc_out (one block per 64 output columns of one decoder layer's cross
+//       K|V projection): [pending update + final LayerNorm + quantization with
+//       the encoder output scale] -> the cross keys and values
+// As in the batch-1 decoder (decode_step.hip): integer partial sums are
+// exact in any order, so the heads and FFN chunks add into shared int32
+// accumulators, and the next kernel applies the residual epilogue
+// x <- fma(gamma, x, fma(acc, scale, bias)) in its prologue.  Every block
+// recomputes the LayerNorm of all rows (a few KB) instead of paying a kernel
+// boundary.  Two accumulators per kind alternate by layer; the kernel after a
+// buffer's consumer clears it.
+//
+// Rows are r = b S + p (sentence b, position p < S, padded positions computed
+// and never used); attention keys of row r are its sentence's positions below
+// its length (Appendix A self-attention with the quantizer figure's
+// precisions, the same canonical arithmetic as the other attention kernels).
+#include "blocks.hpp"
+#include "internal.h"
+
+namespace mnmt {
+namespace {
+
+constexpr int kEncRows = 64;      // rows of this path (B * S)
+constexpr int kEncHeadDim = 64;   // widest head
+constexpr int kEncChunk = 64;     // hidden units per k_enc_ffn block, columns per k_enc_out block
+constexpr int kEncThreads = 256;  // block size (4 waves)
+
+// LayerNorm of G rows held by a wave (row q's element i = lane + 64 j in
+// v[q][j]), each in the canonical order (as ln_row), interleaved.
+template <int G, int NJ>
+__device__ __forceinline__ void ln_rows(float (&v)[G][NJ], const float (&g)[NJ], const float (&b)[NJ], int d,
+                                        float eps) {
+  const int lane = threadIdx.x & 63;
+  const float inv_d = 1.0f / (float)d;
+  float p[G], mu[G], p2[G], rstd[G];
+#pragma unroll
+  for (int q = 0; q < G; ++q) {
+    p[q] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (lane + 64 * j < d) p[q] = p[q] + v[q][j];
+  }
+#pragma unroll
+  for (int q = 0; q < G; ++q) mu[q] = wave_sum(p[q]) * inv_d;
+#pragma unroll
+  for (int q = 0; q < G; ++q) {
+    p2[q] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      if (lane + 64 * j < d) {
+        v[q][j] = v[q][j] - mu[q];
+        p2[q] = fmaf(v[q][j], v[q][j], p2[q]);
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < G; ++q) rstd[q] = 1.0f / sqrtf(wave_sum(p2[q]) * inv_d + eps);
+#pragma unroll
+  for (int q = 0; q < G; ++q)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+      if (lane + 64 * j < d) v[q][j] = fmaf(v[q][j] * rstd[q], g[j], b[j]);
+}
+
+// The sublayer input rows: the embedding or the pending residual update, the
+// LayerNorm, block 0's stores of the updated residual rows (x_out) and of the
+// int8 rows (q_out), and the int8 rows in a_lds (row stride D).  Wave w takes
+// rows w + 4 u, u < RPW, and issues all of their loads before it uses the
+// first (one memory round trip, two for the embedding's token lookup), then
+// calls issue_weights() to issue the kernel's other loads.  D is
+// the exact width, so no element needs a bounds check; EMBED is a template
+// flag so that no load sits behind a run-time branch.
+template <int D, bool EMBED, int RPW, class Issue>
+__device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue issue_weights) {
+  constexpr int NJ = D / 64;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int R = in.R;
+  float sc[NJ], bi[NJ], g[NJ], b[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int i = lane + 64 * j;
+    sc[j] = in.scale[i];
+    bi[j] = in.bias[i];
+    g[j] = in.ln_g[i];
+    b[j] = in.ln_b[i];
+  }
+  float x[RPW][NJ], a[RPW][NJ], ce[RPW];
+  if (EMBED) {
+    int tok[RPW];
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) {
+      const int t = in.tok[min(wave + 4 * u, R - 1)];
+      tok[u] = t < 0 ? 0 : (t >= in.V ? in.V - 1 : t);
+    }
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) {
+      const int pos = min(wave + 4 * u, R - 1) % in.S;
+      ce[u] = in.c_emb[tok[u]];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int i = lane + 64 * j;
+        x[u][j] = in.pe[pos * D + i];
+        a[u][j] = (float)in.E[tok[u] * D + i];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) {
+      const int r = min(wave + 4 * u, R - 1);
+      ce[u] = 0.0f;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int i = lane + 64 * j;
+        x[u][j] = in.x_in[r * D + i];
+        a[u][j] = (float)in.acc[r * D + i];
+      }
+    }
+  }
+  // the kernel's own loads go behind the rows' (the in-order memory counter
+  // then lets the rows be used before those arrive)
+  issue_weights();
+  // four rows at a time, so that their dependent chains (butterflies,
+  // square root, division) interleave
+  constexpr int G = 4;
+#pragma unroll
+  for (int u0 = 0; u0 < RPW; u0 += G) {
+    if (wave + 4 * u0 >= R) break;
+    float v[G][NJ];
+#pragma unroll
+    for (int q = 0; q < G; ++q)
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int u = u0 + q;
+        if (EMBED)
+          v[q][j] = fmaf(a[u][j], ce[u], x[u][j]);
+        else if (in.update)
+          v[q][j] = fmaf(in.gamma, x[u][j], fmaf(a[u][j], sc[j], bi[j]));
+        else
+          v[q][j] = x[u][j];
+      }
+    if (in.ln_mode == 1) ln_rows<G, NJ>(v, g, b, D, in.eps);  // post-LN: normalize the residual stream
+    if (blockIdx.x == 0 && in.x_out) {
+#pragma unroll
+      for (int q = 0; q < G; ++q) {
+        const int r = wave + 4 * (u0 + q);
+        if (r < R)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) in.x_out[r * D + lane + 64 * j] = v[q][j];
+      }
+    }
+    if (in.ln_mode == 2) ln_rows<G, NJ>(v, g, b, D, in.eps);  // pre-LN: normalize the sublayer input
+#pragma unroll
+    for (int q = 0; q < G; ++q) {
+      const int r = wave + 4 * (u0 + q);
+      if (r < R) {
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int8_t c = code_of(v[q][j] * in.inv_s);
+          a_lds[r * D + lane + 64 * j] = c;
+          if (blockIdx.x == 0 && in.q_out) in.q_out[r * D + lane + 64 * j] = c;
+        }
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ void enc_clear(const EncIn& in) {
+  if (blockIdx.x != 0) return;
+  for (int i = threadIdx.x; i < in.zero0_n; i += kEncThreads) in.zero0[i] = 0;
+  for (int i = threadIdx.x; i < in.zero1_n; i += kEncThreads) in.zero1[i] = 0;
+}
+
+// A fragment of int8 rows [rows, K] in LDS (row stride ld): rows m0 + l % 16,
+// K bytes k0 + 16 (l / 16) .. + 15, zero past K.
+__device__ __forceinline__ v4i lds_frag(const int8_t* base, int ld, int m0, int k0, int K) {
+  const int lane = threadIdx.x & 63;
+  const int k = k0 + 16 * (lane >> 4);
+  return k < K ? *(const v4i*)(base + (m0 + (lane & 15)) * ld + k) : v4i{0, 0, 0, 0};
+}
+
+// int32 fragment D (rows m0 + 4 (l / 16) + i, column n) added to out[R, ld].
+__device__ __forceinline__ void add_frag(int32_t* out, int ld, const v4i& acc, int m0, int n, int R) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + 4 * (lane >> 4) + i;
+    if (m < R) atomicAdd(out + (size_t)m * ld + n, acc[i]);
+  }
+}
+
+template <int DMAX, bool EMBED, int RPW>
+__global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) {
+  constexpr int KS = DMAX / 64;                   // 64-deep K steps over d
+  constexpr int PT = 3 * kEncHeadDim / 16 / 4;    // projection tiles per wave (3 dh / 16 over 4 waves)
+  constexpr int OT = DMAX / 64;                   // W_o column tiles per wave (d / 16 over 4 waves)
+  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
+  __shared__ __attribute__((aligned(16))) int8_t qkv[3][kEncRows][kEncHeadDim];
+  __shared__ __attribute__((aligned(16))) int8_t ctx[kEncRows][kEncHeadDim];
+  __shared__ float sc[kEncRows][kEncRows];        // scores, then probabilities
+  const int hd = blockIdx.x;
+  const int R = in.R, d = DMAX, dh = at.dh, S = in.S, ks = KS;
+  const int mt_n = (R + 15) / 16;
+  const int ntile = 3 * dh / 16;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l16 = lane & 15, kq = lane >> 4;
+  // 1. the rows, and behind their loads the weights: the head's Q|K|V rows
+  //    and its W_o columns, with the projection's scale and bias per lane
+  v4i wf[PT][KS];
+  float e_sc[PT], e_bi[PT];
+  v4i of[OT];
+  enc_clear(in);
+  enc_rows<DMAX, EMBED, RPW>(in, a_lds, [&]() {
+#pragma unroll
+    for (int u = 0; u < PT; ++u) {
+      const int j = 16 * min(wave + 4 * u, ntile - 1) + l16;  // row of the head's [q | k | v]
+      const int part = (j >= dh) + (j >= 2 * dh);
+      const int n = part * d + hd * dh + (j - part * dh);
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) wf[u][kk] = *(const v4i*)(at.W + n * d + 64 * kk + 16 * kq);
+      e_sc[u] = at.scale[n];
+      e_bi[u] = at.bias[n];
+    }
+#pragma unroll
+    for (int u = 0; u < OT; ++u) {
+      const int n = 16 * (wave + 4 * u) + l16;
+      of[u] = *(const v4i*)(at.Wo + n * d + hd * dh + 16 * min(kq, dh / 16 - 1));
+    }
+  });
+  __syncthreads();
+  // 3. Q, K, V of the head, requantized into LDS
+#pragma unroll
+  for (int u = 0; u < PT; ++u) {
+    const int tile = wave + 4 * u;
+    if (tile >= ntile) continue;
+    const int j = 16 * tile + l16;
+    const int part = (j >= dh) + (j >= 2 * dh);
+    for (int mt = 0; mt < mt_n; ++mt) {
+      v4i acc = {0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk)
+        if (kk < ks) acc = mfma16(lds_frag(a_lds, d, 16 * mt, 64 * kk, d), wf[u][kk], acc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = 16 * mt + 4 * kq + i;
+        if (m < R) qkv[part][m][j - part * dh] = code_of(fmaf((float)acc[i], e_sc[u], e_bi[u]));
+      }
+    }
+  }
+  __syncthreads();
+  // 4. scores q . k (int32 exact) scaled by c_qk, every (query, key) pair
+  for (int t = wave; t < mt_n * mt_n; t += 4) {
+    const int mt = t / mt_n, kt = t % mt_n;
+    const v4i acc = mfma16(lds_frag(&qkv[0][0][0], kEncHeadDim, 16 * mt, 0, dh),
+                           lds_frag(&qkv[1][0][0], kEncHeadDim, 16 * kt, 0, dh), v4i{0, 0, 0, 0});
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sc[16 * mt + 4 * kq + i][16 * kt + l16] = (float)acc[i] * at.c_qk;
+  }
+  __syncthreads();
+  // 5. softmax of each row over its sentence's keys (one key per lane: the
+  //    canonical order), probabilities in place at sc[m][0 .. n)
+  {
+    float sv[RPW], ex[RPW];
+    int nn[RPW];
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) {
+      const int m = min(wave + 4 * u, R - 1);
+      const int b = m / S;
+      int n = at.len[b];
+      nn[u] = n < 1 ? 1 : (n > S ? S : n);
+      sv[u] = lane < nn[u] ? sc[m][b * S + lane] : -FLT_MAX;
+    }
+    float mx[RPW], inv[RPW];
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) mx[u] = wave_max(sv[u]);
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) ex[u] = lane < nn[u] ? canon_exp(sv[u] - mx[u]) : 0.0f;
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) inv[u] = 1.0f / wave_sum(ex[u]);
+    wave_sync();  // every lane has read its scores before any probability is written
+    // keys n .. S - 1 get probability 0: fma(0, v, acc) leaves acc unchanged
+    // bit for bit, so the context loop may run over all S keys
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) {
+      const int m = wave + 4 * u;
+      if (m < R && lane < S) sc[m][lane] = lane < nn[u] ? ex[u] * inv[u] : 0.0f;
+    }
+  }
+  __syncthreads();
+  // 6. context: ascending keys, one fma each, requantized
+  {
+    // thread: column j = tid % dh of rows g0 + groups u (g0 = tid / dh), one
+    // fma chain per row over the keys of its sentence in ascending order
+    // (probability 0 past the sentence's length).  With one sentence the
+    // rows share each value load; rows past R repeat row R - 1, unstored.
+    constexpr int CPT = RPW;  // rows per thread at most (4 RPW rows over kEncThreads / dh >= 4 groups)
+    const int groups = kEncThreads / dh;
+    const int j = threadIdx.x % dh, g0 = threadIdx.x / dh;
+    if (S == R) {  // one sentence
+      const int8_t* vcol = &qkv[2][0][j];
+      float acc[CPT];
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) acc[u] = 0.0f;
+      for (int t = 0; t < S; ++t) {
+        const float v = (float)vcol[t * kEncHeadDim];
+#pragma unroll
+        for (int u = 0; u < CPT; ++u) acc[u] = fmaf(sc[min(g0 + groups * u, R - 1)][t], v, acc[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int m = g0 + groups * u;
+        if (m < R) ctx[m][j] = code_of(acc[u] * at.c_pv);
+      }
+    } else {
+      for (int m = g0; m < R; m += groups) {
+        const int base = (m / S) * S;
+        float acc = 0.0f;
+        for (int t = 0; t < S; ++t) acc = fmaf(sc[m][t], (float)qkv[2][base + t][j], acc);
+        ctx[m][j] = code_of(acc * at.c_pv);
+      }
+    }
+  }
+  __syncthreads();
+  // 7. the head's share of the output projection (K = dh), exact int32 sums
+#pragma unroll
+  for (int u = 0; u < OT; ++u) {
+    const int n0 = 16 * (wave + 4 * u);
+    if (n0 >= d) continue;
+    for (int mt = 0; mt < mt_n; ++mt) {
+      const v4i acc = mfma16(lds_frag(&ctx[0][0], kEncHeadDim, 16 * mt, 0, dh), of[u], v4i{0, 0, 0, 0});
+      add_frag(at.acc_out, d, acc, 16 * mt, n0 + l16, R);
+    }
+  }
+}
+
+// One block per kEncChunk hidden units, one 16-unit W1 tile per wave.
+template <int DMAX, int RPW>
+__global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
+  constexpr int KS = DMAX / 64;
+  constexpr int OT = DMAX / 64;
+  static_assert(kEncChunk == 64, "one W1 tile per wave and one K step of W2");
+  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
+  __shared__ __attribute__((aligned(16))) int8_t hb[kEncRows][kEncChunk];
+  const int R = in.R, d = DMAX, F = f.F, ks = KS;
+  const int mt_n = (R + 15) / 16;
+  const int f0 = blockIdx.x * kEncChunk;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l16 = lane & 15, kq = lane >> 4;
+  const int hrow = f0 + 16 * wave + l16;  // < F (F is a multiple of kEncChunk)
+  v4i wf[KS];
+  float e_sc, e_bi;
+  v4i of[OT];
+  enc_clear(in);
+  enc_rows<DMAX, false, RPW>(in, a_lds, [&]() {
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) wf[kk] = *(const v4i*)(f.W1 + hrow * d + 64 * kk + 16 * kq);
+    e_sc = f.scale1[hrow];
+    e_bi = f.bias1[hrow];
+#pragma unroll
+    for (int u = 0; u < OT; ++u) {
+      const int n = 16 * (wave + 4 * u) + l16;
+      of[u] = *(const v4i*)(f.W2 + n * F + f0 + 16 * kq);
+    }
+  });
+  __syncthreads();
+  for (int mt = 0; mt < mt_n; ++mt) {
+    v4i acc = {0, 0, 0, 0};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+      if (kk < ks) acc = mfma16(lds_frag(a_lds, d, 16 * mt, 64 * kk, d), wf[kk], acc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = 16 * mt + 4 * kq + i;
+      if (m < R) hb[m][16 * wave + l16] = code_of(fmaxf(fmaf((float)acc[i], e_sc, e_bi), 0.0f));
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < OT; ++u) {
+    const int n0 = 16 * (wave + 4 * u);
+    if (n0 >= d) continue;
+    for (int mt = 0; mt < mt_n; ++mt) {
+      const v4i acc = mfma16(lds_frag(&hb[0][0], kEncChunk, 16 * mt, 0, kEncChunk), of[u], v4i{0, 0, 0, 0});
+      add_frag(f.acc_out, d, acc, 16 * mt, n0 + l16, R);
+    }
+  }
+}
+
+// One block per kEncChunk columns of one decoder layer's cross K|V projection.
+template <int DMAX, int RPW>
+__global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
+  constexpr int KS = DMAX / 64;
+  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
+  const int R = in.R, d = DMAX, ks = KS;
+  const int mt_n = (R + 15) / 16;
+  const int per_layer = 2 * d / kEncChunk;
+  const int layer = blockIdx.x / per_layer;
+  const int c0 = (blockIdx.x - layer * per_layer) * kEncChunk;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int l16 = lane & 15, kq = lane >> 4;
+  const EncOut::Layer& L = o.layer[layer];
+  const int col = c0 + 16 * wave + l16;  // < 2 d
+  v4i wf[KS];
+  float e_sc, e_bi;
+  enc_clear(in);
+  enc_rows<DMAX, false, RPW>(in, a_lds, [&]() {
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) wf[kk] = *(const v4i*)(L.W + col * d + 64 * kk + 16 * kq);
+    e_sc = L.scale[col];
+    e_bi = L.bias[col];
+  });
+  __syncthreads();
+  for (int mt = 0; mt < mt_n; ++mt) {
+    v4i acc = {0, 0, 0, 0};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk)
+      if (kk < ks) acc = mfma16(lds_frag(a_lds, d, 16 * mt, 64 * kk, d), wf[kk], acc);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = 16 * mt + 4 * kq + i;
+      if (m < R) L.out[(size_t)m * 2 * d + col] = code_of(fmaf((float)acc[i], e_sc, e_bi));
+    }
+  }
+}
+
+}  // namespace
+
+bool enc_small_fits(int R, int S, int d, int dh, int F) {
+  return R >= 1 && R <= kEncRows && S <= kEncRows && d % 64 == 0 && d <= 256 && dh % 16 == 0 &&
+         dh <= kEncHeadDim && F % kEncChunk == 0;
+}
+
+// exact width x rows per wave (8 for up to 32 rows, else 16)
+#define MNMT_ENC_BY_D(d, R, CALL)                        \
+  switch ((d) * ((R) <= 32 ? 1 : -1)) {                 \
+    case 64: CALL(64, 8); break;                         \
+    case 128: CALL(128, 8); break;                       \
+    case 192: CALL(192, 8); break;                       \
+    case 256: CALL(256, 8); break;                       \
+    case -64: CALL(64, 16); break;                       \
+    case -128: CALL(128, 16); break;                     \
+    case -192: CALL(192, 16); break;                     \
+    case -256: CALL(256, 16); break;                     \
+    default: return hipErrorInvalidValue;                \
+  }
+
+hipError_t launch_enc_attn(const EncIn& in, const EncAttn& at, int heads, hipStream_t s) {
+#define MNMT_E(DM, RPW)                                                                          \
+  if (in.embed)                                                                                  \
+    hipLaunchKernelGGL((k_enc_attn<DM, true, RPW>), dim3(heads), dim3(kEncThreads), 0, s, in, at); \
+  else                                                                                           \
+    hipLaunchKernelGGL((k_enc_attn<DM, false, RPW>), dim3(heads), dim3(kEncThreads), 0, s, in, at);
+  MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
+#undef MNMT_E
+  return hipGetLastError();
+}
+
+hipError_t launch_enc_ffn(const EncIn& in, const EncFfn& f, hipStream_t s) {
+  const int blocks = f.F / kEncChunk;
+#define MNMT_E(DM, RPW) hipLaunchKernelGGL((k_enc_ffn<DM, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, f);
+  MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
+#undef MNMT_E
+  return hipGetLastError();
+}
+
+hipError_t launch_enc_out(const EncIn& in, const EncOut& o, hipStream_t s) {
+  if (o.layers < 1 || o.layers > EncOut::kMaxLayers) return hipErrorInvalidValue;
+  const int blocks = o.layers * (2 * in.d / kEncChunk);
+#define MNMT_E(DM, RPW) hipLaunchKernelGGL((k_enc_out<DM, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, o);
+  MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
+#undef MNMT_E
+  return hipGetLastError();
+}
+
+}  // namespace mnmt

@@ -184,6 +184,67 @@ hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s);
 // With ev_start / ev_stop the events take the kernel's own start and end times.
 hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s, hipEvent_t ev_start = nullptr,
                               hipEvent_t ev_stop = nullptr);
+// Encoder for at most 64 rows in 2 kernels per layer (encode_small.hip).
+struct EncIn {             // the sublayer input rows of an encoder kernel
+  // Every pointer is valid for the extent given even where its flag is off.
+  int R, d, S;             // rows (B * S), width, positions per sentence
+  int embed;               // rows = embeddings of tok[r] at position r % S
+  const int32_t* tok;
+  const int8_t* E;
+  const float* c_emb;
+  const float* pe;
+  int V;
+  const float* x_in;       // residual rows [R, d]
+  float* x_out;            // block 0 stores the updated rows here (or null)
+  const int32_t* acc;      // [R, d]: pending update x <- fma(gamma, x, fma(acc, scale, bias))
+  const float* scale;      // [d]
+  const float* bias;       // [d]
+  float gamma;
+  int update;
+  const float* ln_g;       // [d]
+  const float* ln_b;
+  int ln_mode;             // 0 none, 1 post-LN (the residual stream), 2 pre-LN (the sublayer input)
+  float eps;
+  float inv_s;             // 1 / input scale of the consuming layer
+  int8_t* q_out;           // block 0 stores the int8 rows here (or null)
+  int32_t* zero0;          // block 0 clears these accumulators (their consumers have finished)
+  int zero0_n;
+  int32_t* zero1;
+  int zero1_n;
+};
+struct EncAttn {
+  int dh;
+  const int8_t* W;         // QKV [3d, d]
+  const float* scale;
+  const float* bias;
+  const int8_t* Wo;        // [d, d]
+  const int32_t* len;      // [B]
+  float c_qk, c_pv;
+  int32_t* acc_out;        // [R, d], zero on entry
+};
+struct EncFfn {
+  int F;
+  const int8_t* W1;
+  const float* scale1;
+  const float* bias1;
+  const int8_t* W2;        // [d, F]
+  int32_t* acc_out;        // [R, d], zero on entry
+};
+struct EncOut {            // every decoder layer's cross K|V projection of the encoder output
+  static constexpr int kMaxLayers = 16;
+  struct Layer {
+    const int8_t* W;       // [2d, d]
+    const float* scale;
+    const float* bias;
+    int8_t* out;           // [R, 2d]
+  } layer[kMaxLayers];
+  int layers;
+};
+bool enc_small_fits(int R, int S, int d, int dh, int F);
+hipError_t launch_enc_attn(const EncIn& in, const EncAttn& at, int heads, hipStream_t s);
+hipError_t launch_enc_ffn(const EncIn& in, const EncFfn& f, hipStream_t s);
+hipError_t launch_enc_out(const EncIn& in, const EncOut& o, hipStream_t s);
+
 // Small-M GEMM (M <= 64, K <= 1024) on 16x16x64 matrix cores; with `in` the
 // rows are prepared (embedding / LayerNorm / quantization) in its prologue.
 bool qgemm_small_fits(int M, int K);
@@ -286,6 +347,7 @@ struct mnmt_session {
   float* dec_x2 = nullptr;  // second residual buffer (post-LN ping-pong)
   unsigned long long* fslots = nullptr;  // spread arg-max slots [8][fused_slots_per_row()]
   int32_t* step_acc = nullptr;           // decode-step accumulators [3][2][d] int32
+  int32_t* enc_acc = nullptr;            // small-batch encoder accumulators [2 W_o + 2 W2][64][d] int32
   int8_t* dec_a = nullptr;
   int8_t* dec_qkv = nullptr;
   int8_t* dec_q = nullptr;

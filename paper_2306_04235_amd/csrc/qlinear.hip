@@ -20,7 +20,6 @@
 namespace mnmt {
 namespace {
 
-typedef int v4i __attribute__((ext_vector_type(4)));
 
 // The fused epilogue of one output element (row m, column n).
 __device__ __forceinline__ void epilogue_store(const EpiArgs& e, int m, int n, int acc, const float* scale,

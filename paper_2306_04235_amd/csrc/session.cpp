@@ -26,10 +26,12 @@ struct Bump {
   }
 };
 
+constexpr size_t kEncAccRows = 64;  // rows of the small-batch encoder path
+
 struct Plan {
   size_t src, len, region, enc_x, enc_x2, enc_a, enc_qkv, enc_h, enc_out, logits;
   std::vector<size_t> cross_kv, kc, vc;
-  size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots;
+  size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots, enc_acc;
   size_t cur_tok, step, slots, out_tok, finished, out_len, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
   size_t total;
@@ -46,6 +48,8 @@ int validate_cfg(const mnmt_model* m, const mnmt_session_cfg* c) {
                      "min(256, max_pos), 1 <= beam <= 8 and 2*beam <= vocab");
   return MNMT_OK;
 }
+
+size_t enc_acc_bytes(size_t d) { return 4 * kEncAccRows * d * sizeof(int32_t); }
 
 Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   Plan p{};
@@ -73,6 +77,9 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.enc_x2 += p.region;
   p.logits = p.region;
   for (size_t l = 0; l < Ld; ++l) p.cross_kv.push_back(b.take(BS * 2 * d));
+  // int32 split-K accumulators of the small-batch encoder: W_o and W2 sums,
+  // two of each (zero at creation; every encode leaves them zero)
+  p.enc_acc = b.take(enc_acc_bytes(d));
   p.dec_x = b.take(4 * R * d);
   p.dec_x2 = b.take(4 * R * d);
   // fused arg-max slots, then the decode-step int32 accumulators (cleared together)
@@ -180,6 +187,129 @@ int run_encoder_small(mnmt_session* S, hipStream_t s) {
   return MNMT_OK;
 }
 
+// Encoder for at most 64 rows in 2 kernels per layer (encode_small.hip):
+// [attention block] [FFN block] per layer, then [final LayerNorm + encoder
+// output + every decoder layer's cross K|V].  Each kernel applies the
+// previous sublayer's residual update in its prologue; the W_o and W2 int32
+// accumulators alternate by layer parity and are cleared by the kernel after
+// their consumer, so that all four are zero again when the encode ends.
+int run_encoder_blocks(mnmt_session* S, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  const int d = m->info.d_model, h = m->info.n_heads, R = S->B * S->S;
+  const int L = (int)m->enc.size();
+  const bool post = m->info.ln_post;
+  int32_t* acc_o[2] = {S->enc_acc, S->enc_acc + kEncAccRows * d};
+  int32_t* acc_f[2] = {S->enc_acc + 2 * kEncAccRows * d, S->enc_acc + 3 * kEncAccRows * d};
+  const int n = R * d;
+  float* xa = S->enc_x;
+  float* xb = S->enc_x2;
+  const float* any_d = m->enc[0].sa_ln.g;  // a valid float[d] for operands a kernel does not use
+  auto base = [&](float inv_s) {
+    EncIn in{};
+    in.R = R;
+    in.d = d;
+    in.S = S->S;
+    in.tok = S->src;
+    in.E = m->E;
+    in.c_emb = m->c_emb;
+    in.pe = m->pe;
+    in.V = m->info.vocab;
+    in.x_in = xa;
+    in.x_out = xb;
+    in.acc = acc_o[0];
+    in.scale = any_d;
+    in.bias = any_d;
+    in.gamma = 1.0f;
+    in.ln_g = any_d;
+    in.ln_b = any_d;
+    in.eps = m->info.ln_eps;
+    in.inv_s = inv_s;
+    return in;
+  };
+  // the residual update of the sublayer whose partial sums are in acc (and
+  // its post-LN LayerNorm in post-LN models), then the next pre-LN LayerNorm
+  auto rows = [&](EncIn& in, const int32_t* acc, const LinearDev* Lp, float gamma, const LnDev& post_ln,
+                  const LnDev& pre_ln) {
+    if (acc) {
+      in.acc = acc;
+      in.scale = Lp->scale;
+      in.bias = Lp->bias;
+      in.gamma = gamma;
+      in.update = 1;
+    }
+    const LnDev& ln = post ? post_ln : pre_ln;
+    if (ln.g && (acc || !post)) {
+      in.ln_g = ln.g;
+      in.ln_b = ln.b;
+      in.ln_mode = post ? 1 : 2;
+    }
+  };
+  const LnDev none{};
+  for (int l = 0; l < L; ++l) {
+    const LayerDev& Ly = m->enc[l];
+    {  // self-attention block
+      EncIn in = base(Ly.qkv.inv_in);
+      if (l == 0) {
+        in.embed = 1;  // the embeddings become the residual stream
+        rows(in, nullptr, nullptr, 1.0f, none, Ly.sa_ln);
+        in.zero1 = acc_f[0];
+        in.zero1_n = n;
+      } else {
+        const LayerDev& P = m->enc[l - 1];
+        rows(in, acc_f[(l - 1) & 1], &P.w2, P.ff_gamma, P.ff_ln, Ly.sa_ln);
+      }
+      in.zero0 = acc_o[(l + 1) & 1];
+      in.zero0_n = n;
+      EncAttn at{};
+      at.dh = m->dh;
+      at.W = Ly.qkv.w;
+      at.scale = Ly.qkv.scale;
+      at.bias = Ly.qkv.bias;
+      at.Wo = Ly.o.w;
+      at.len = S->len;
+      at.c_qk = Ly.sa_cqk;
+      at.c_pv = Ly.sa_cpv;
+      at.acc_out = acc_o[l & 1];
+      LAUNCH(launch_enc_attn(in, at, h, s));
+      std::swap(xa, xb);
+    }
+    {  // FFN block
+      EncIn in = base(Ly.w1.inv_in);
+      rows(in, acc_o[l & 1], &Ly.o, Ly.sa_gamma, Ly.sa_ln, Ly.ff_ln);
+      in.zero0 = acc_f[(l + 1) & 1];
+      in.zero0_n = n;
+      EncFfn f{};
+      f.F = Ly.w1.N;
+      f.W1 = Ly.w1.w;
+      f.scale1 = Ly.w1.scale;
+      f.bias1 = Ly.w1.bias;
+      f.W2 = Ly.w2.w;
+      f.acc_out = acc_f[l & 1];
+      LAUNCH(launch_enc_ffn(in, f, s));
+      std::swap(xa, xb);
+    }
+  }
+  // final LayerNorm (post-LN: the last layer's), the int8 encoder output and
+  // the cross keys and values of every decoder layer
+  const LayerDev& last = m->enc.back();
+  EncIn in = base(m->inv_enc);
+  in.x_out = nullptr;
+  rows(in, acc_f[(L - 1) & 1], &last.w2, last.ff_gamma, last.ff_ln, m->enc_ln);
+  in.q_out = S->enc_out;
+  in.zero0 = acc_o[(L - 1) & 1];
+  in.zero0_n = n;
+  EncOut o{};
+  o.layers = (int)m->dec.size();
+  for (int l = 0; l < o.layers; ++l) {
+    o.layer[l].W = m->dec[l].ckv.w;
+    o.layer[l].scale = m->dec[l].ckv.scale;
+    o.layer[l].bias = m->dec[l].ckv.bias;
+    o.layer[l].out = S->cross_kv[l];
+  }
+  LAUNCH(launch_enc_out(in, o, s));
+  return MNMT_OK;
+}
+
 // Encoder over the session's current batch (rows = B * S, padded rows are
 // computed and ignored), then every decoder layer's cross keys/values.
 int run_encoder(mnmt_session* S, hipStream_t s) {
@@ -187,6 +317,8 @@ int run_encoder(mnmt_session* S, hipStream_t s) {
   const int d = m->info.d_model, rows = S->B * S->S;
   const bool post = m->info.ln_post;
   const float eps = m->info.ln_eps;
+  if (enc_small_fits(rows, S->S, d, m->dh, m->info.d_ffn) && (int)m->dec.size() <= EncOut::kMaxLayers)
+    return run_encoder_blocks(S, s);
   if (qgemm_small_fits(rows, d) && qgemm_small_fits(rows, m->info.d_ffn)) return run_encoder_small(S, s);
   LAUNCH(launch_embed(S->src, rows, S->S, nullptr, m->E, m->c_emb, m->pe, d, m->info.vocab, S->enc_x, s));
   const LayerDev& L0 = m->enc[0];
@@ -640,6 +772,7 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->dec_x = (float*)at(p.dec_x);
   S->dec_x2 = (float*)at(p.dec_x2);
   S->fslots = (unsigned long long*)at(p.fslots);
+  S->enc_acc = (int32_t*)at(p.enc_acc);
   S->step_acc = (int32_t*)(S->fslots + 8 * fused_slots_per_row());
   S->dec_a = (int8_t*)at(p.dec_a);
   S->dec_qkv = (int8_t*)at(p.dec_qkv);
@@ -690,6 +823,14 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   if (hipStreamCreateWithFlags(&S->capture_stream, hipStreamNonBlocking) != hipSuccess) {
     delete S;
     return set_error(MNMT_E_HIP, "could not create the capture stream");
+  }
+  // the encoder accumulators start at zero (each encode leaves them so)
+  hipError_t h = hipMemsetAsync(S->enc_acc, 0, enc_acc_bytes(d), S->capture_stream);
+  if (h == hipSuccess) h = hipStreamSynchronize(S->capture_stream);
+  if (h != hipSuccess) {
+    (void)hipStreamDestroy(S->capture_stream);
+    delete S;
+    return hip_error(h, "clearing the encoder accumulators");
   }
   *out = S;
   return MNMT_OK;
