@@ -114,35 +114,45 @@ __global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
     unsigned long long b = wmax[0][m];
 #pragma unroll
     for (int w = 1; w < 4; ++w) b = wmax[w][m] > b ? wmax[w][m] : b;
-    if (b != 0ull) atomicMax(gv.slots + m * kSlots + blockIdx.x % kSlots, b);
+    if (b != 0ull) atomicMax(gv.slots + (size_t)m * gv.nslots + blockIdx.x % kSlots, b);
   }
 }
 
 __global__ __launch_bounds__(256) void k_greedy_commit_slots(FusedGemv gv) {
   __shared__ int next_tok[kRows];
-  const int t = gv.t;
-  for (int m = threadIdx.x; m < gv.R; m += blockDim.x) {
+  __shared__ unsigned long long wbest[4];
+  const int t = gv.t, ns = gv.nslots;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int m = 0; m < gv.R; ++m) {
+    // every thread reduces a stride of the row's slots and clears them
     unsigned long long b = 0ull;
-    for (int i = 0; i < kSlots; ++i) {
-      const unsigned long long s = gv.slots[m * kSlots + i];
-      b = s > b ? s : b;
-      gv.slots[m * kSlots + i] = 0ull;
+    for (int i = threadIdx.x; i < ns; i += 256) {
+      const unsigned long long v = gv.slots[(size_t)m * ns + i];
+      b = v > b ? v : b;
     }
-    const int tok = unpack_index(b);
-    const int fin = gv.finished[m];
-    if (t < gv.T) gv.out_tok[(size_t)t * gv.R + m] = fin ? gv.pad : tok;
-    if (!fin && gv.stop_at_eos && tok == gv.eos) {
-      gv.finished[m] = 1;
-      gv.out_len[m] = t + 1;
+    for (int i = threadIdx.x; i < ns; i += 256) gv.slots[(size_t)m * ns + i] = 0ull;
+    b = wave_max_u64(b);
+    if (lane == 0) wbest[wave] = b;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      b = wbest[0];
+      for (int w = 1; w < 4; ++w) b = wbest[w] > b ? wbest[w] : b;
+      const int tok = unpack_index(b);
+      const int fin = gv.finished[m];
+      if (t < gv.T) gv.out_tok[(size_t)t * gv.R + m] = fin ? gv.pad : tok;
+      if (!fin && gv.stop_at_eos && tok == gv.eos) {
+        gv.finished[m] = 1;
+        gv.out_len[m] = t + 1;
+      }
+      gv.cur_tok[m] = fin ? gv.pad : tok;
+      next_tok[m] = fin ? gv.pad : tok;
     }
-    gv.cur_tok[m] = fin ? gv.pad : tok;
-    next_tok[m] = fin ? gv.pad : tok;
+    __syncthreads();
   }
   for (int i = threadIdx.x; gv.zero_acc && i < gv.zero_n; i += blockDim.x) gv.zero_acc[i] = 0;
   if (threadIdx.x == 0) *gv.step = t + 1;
   // the next step's input rows: embedding of the new tokens at position t + 1
   if (gv.emb_out && t + 1 < gv.P) {
-    __syncthreads();
     const int d = gv.d;
     for (int e = threadIdx.x; e < gv.R * d; e += blockDim.x) {
       const int m = e / d, i = e % d;
@@ -183,7 +193,7 @@ hipError_t launch_d(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
 
 }  // namespace
 
-int fused_slots_per_row() { return kSlots; }
+int fused_slots_per_row(int V) { return max(kSlots, step_logits_blocks(V)); }
 
 hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
   // K chunks per lane must be at most two: K <= 32 * LPR with LPR <= 64
@@ -195,7 +205,7 @@ hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s
 }
 
 hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s) {
-  if (gv.R > kRows) return hipErrorInvalidValue;
+  if (gv.R > kRows || gv.nslots < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_greedy_commit_slots, dim3(1), dim3(256), 0, s, gv);
   return hipGetLastError();
 }

@@ -429,9 +429,17 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     unsigned long long b = wmax[0][m];
 #pragma unroll
     for (int w = 1; w < 4; ++w) b = wmax[w][m] > b ? wmax[w][m] : b;
-    // the slot usually holds a larger key already: test before the atomic
-    unsigned long long* slot = g.slots + m * g.nslots + blockIdx.x % g.nslots;
-    if (b > __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(slot, b);
+    unsigned long long* slot = g.slots + (size_t)m * g.nslots;
+    if (g.nslots >= (int)gridDim.x) {
+      // one partial per block: a plain store, no atomic (atomics on one
+      // address serialize), reduced by the consumer
+      slot[blockIdx.x] = b;
+    } else {
+      // few slots: most blocks find a larger key already there, and the
+      // test spares them the serialized atomic
+      slot += blockIdx.x % g.nslots;
+      if (b > __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(slot, b);
+    }
   }
 }
 
@@ -443,6 +451,11 @@ bool step_path_fits(int R, int d, int dh, int F, int T, int S) {
 }
 
 bool step_logits_fits(int R, int d) { return R >= 1 && R <= kStepRows && d % 64 == 0 && d >= 64 && d <= 512; }
+
+int step_logits_blocks(int V) {
+  const int rpb = 4 * kLogitsTiles * 16;  // rows per block
+  return (V + rpb - 1) / rpb;
+}
 
 #define MNMT_BY_D(d, CALL)            \
   switch (row_class(d)) {             \
@@ -481,8 +494,7 @@ hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s) {
 
 hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s, hipEvent_t ev_start,
                               hipEvent_t ev_stop) {
-  const int rpb = 4 * kLogitsTiles * 16;  // rows per block
-  const int blocks = (g.V + rpb - 1) / rpb;
+  const int blocks = step_logits_blocks(g.V);
 #define MNMT_LOGITS(DM)                                                                                       \
   if (g.x_i8 && (ev_start || ev_stop))                                                                        \
     hipExtLaunchKernelGGL((k_step_logits<DM, true>), dim3(blocks), dim3(kStepThreads), 0, s, ev_start, ev_stop, 0, \

@@ -111,7 +111,8 @@ struct FusedGemv {         // a linear layer over the prepared rows, and greedy 
   const float* scale;
   const float* bias;
   void* out;               // int8 [R, N]; for the arg-max: fp32 logits [R, N] or null
-  unsigned long long* slots;  // arg-max: [R][fused_slots_per_row()], zero before the launch
+  unsigned long long* slots;  // arg-max: [R][nslots], zero before the launch
+  int nslots;              // arg-max slots per row (fused_slots_per_row(V))
   int* step;               // commit: advanced to t + 1
   int32_t* out_tok;
   int32_t* cur_tok;
@@ -179,6 +180,7 @@ struct StepLogits {
 };
 bool step_path_fits(int R, int d, int dh, int F, int T, int S);
 bool step_logits_fits(int R, int d);  // R <= 2, d a multiple of 64 up to 512
+int step_logits_blocks(int V);        // blocks (and arg-max partials per row) of launch_step_logits
 hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s);
 hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s);
 // With ev_start / ev_stop the events take the kernel's own start and end times.
@@ -251,7 +253,9 @@ bool qgemm_small_fits(int M, int K);
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
                               const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s);
 hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s);
-int fused_slots_per_row();
+// Arg-max slots per row of the greedy paths: the spread atomic slots of the
+// 3-8 row path and one partial per block of the 1-2 row logits kernel.
+int fused_slots_per_row(int V);
 
 // Beam search kernels.
 struct BeamState {
@@ -345,7 +349,7 @@ struct mnmt_session {
   std::vector<int8_t*> cross_kv;
   float* dec_x = nullptr;
   float* dec_x2 = nullptr;  // second residual buffer (post-LN ping-pong)
-  unsigned long long* fslots = nullptr;  // spread arg-max slots [8][fused_slots_per_row()]
+  unsigned long long* fslots = nullptr;  // arg-max slots [8][fused_slots_per_row(V)]
   int32_t* step_acc = nullptr;           // decode-step accumulators [3][2][d] int32
   int32_t* enc_acc = nullptr;            // small-batch encoder accumulators [2 W_o + 2 W2][64][d] int32
   int8_t* dec_a = nullptr;

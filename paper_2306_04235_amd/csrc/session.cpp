@@ -83,7 +83,7 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.dec_x = b.take(4 * R * d);
   p.dec_x2 = b.take(4 * R * d);
   // fused arg-max slots, then the decode-step int32 accumulators (cleared together)
-  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row() + 4 * 3 * 2 * d);
+  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row(m->info.vocab) + 4 * 3 * 2 * d);
   p.dec_a = b.take(R * d);
   p.dec_qkv = b.take(R * 3 * d);
   p.dec_q = b.take(R * d);
@@ -479,6 +479,7 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
   LinearDev out_proj{m->E, m->c_out, nullptr, m->info.vocab, d, 0.f};
   FusedGemv gv = gemv(out_proj, EPI_LOGITS_ARGMAX, logits_out);
   gv.slots = S->fslots;
+  gv.nslots = fused_slots_per_row(m->info.vocab);
   gv.step = S->step;
   gv.out_tok = S->out_tok;
   gv.cur_tok = S->cur_tok;
@@ -627,12 +628,13 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   g.c_out = m->c_out;
   g.logits = logits_out;
   g.slots = S->fslots;
-  g.nslots = fused_slots_per_row();
+  g.nslots = fused_slots_per_row(m->info.vocab);
   LAUNCH(launch_step_logits(in, g, s));
   FusedGemv gv{};
   gv.R = R;
   gv.t = t;
   gv.slots = S->fslots;
+  gv.nslots = fused_slots_per_row(m->info.vocab);
   gv.step = S->step;
   gv.out_tok = S->out_tok;
   gv.cur_tok = S->cur_tok;
@@ -696,7 +698,7 @@ int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
   if (sc.beam == 1) {
     const int R = S->B;
     LAUNCH(launch_greedy_reset(S->slots, R, sc.max_steps, S->cur_tok, S->finished, S->out_len, S->step,
-                               m->info.bos_id, S->fslots, 8 * fused_slots_per_row() + 3 * 2 * m->info.d_model / 2, s));
+                               m->info.bos_id, S->fslots, 8 * fused_slots_per_row(m->info.vocab) + 3 * 2 * m->info.d_model / 2, s));
     if (step_path_used(S, R) && (rc = embed_step_input(S, R, s))) return rc;
     for (int t = 0; t < sc.max_steps; ++t)
       if ((rc = greedy_step_any(S, R, t, sc.stop_at_eos, nullptr, s))) return rc;
@@ -773,7 +775,7 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->dec_x2 = (float*)at(p.dec_x2);
   S->fslots = (unsigned long long*)at(p.fslots);
   S->enc_acc = (int32_t*)at(p.enc_acc);
-  S->step_acc = (int32_t*)(S->fslots + 8 * fused_slots_per_row());
+  S->step_acc = (int32_t*)(S->fslots + 8 * (size_t)fused_slots_per_row((int)V));
   S->dec_a = (int8_t*)at(p.dec_a);
   S->dec_qkv = (int8_t*)at(p.dec_qkv);
   S->dec_q = (int8_t*)at(p.dec_q);
@@ -861,7 +863,7 @@ extern "C" int mnmt_encode(mnmt_session* S, const int32_t* d_src, const int32_t*
   if ((rc = run_encoder(S, s))) return rc;
   const mnmt_model* m = S->m;
   LAUNCH(launch_greedy_reset(S->slots, B, S->cfg.max_tgt_len, S->cur_tok, S->finished, S->out_len, S->step,
-                             m->info.bos_id, S->fslots, 8 * fused_slots_per_row() + 3 * 2 * m->info.d_model / 2, s));
+                             m->info.bos_id, S->fslots, 8 * fused_slots_per_row(m->info.vocab) + 3 * 2 * m->info.d_model / 2, s));
   S->encoded = true;
   S->host_step = 0;
   return MNMT_OK;
