@@ -15,8 +15,13 @@
 // accumulators, and the next kernel applies the residual epilogue
 // x <- fma(gamma, x, fma(acc, scale, bias)) in its prologue.  Every block
 // recomputes the LayerNorm of all rows (a few KB) instead of paying a kernel
-// boundary.  Two accumulators per kind alternate by layer; the kernel after a
-// buffer's consumer clears it.
+// boundary; the blocks share the stores of the updated rows.  Two
+// accumulators per kind alternate by layer; the blocks of the kernel after a
+// buffer's consumer clear it.
+//
+// The blocks have 8 waves: the per-row work (LayerNorm, softmax) and the
+// context sums are chains of dependent instructions, so more waves per block
+// shorten the kernel even though the few blocks leave most CUs idle.
 //
 // Rows are r = b S + p (sentence b, position p < S, padded positions computed
 // and never used); attention keys of row r are its sentence's positions below
@@ -28,10 +33,11 @@
 namespace mnmt {
 namespace {
 
-constexpr int kEncRows = 64;      // rows of this path (B * S)
-constexpr int kEncHeadDim = 64;   // widest head
-constexpr int kEncChunk = 64;     // hidden units per k_enc_ffn block, columns per k_enc_out block
-constexpr int kEncThreads = 256;  // block size (4 waves)
+constexpr int kEncRows = 64;                // rows of this path (B * S)
+constexpr int kEncHeadDim = 64;             // widest head
+constexpr int kEncChunk = 64;               // hidden units per k_enc_ffn block, columns per k_enc_out block
+constexpr int kEncWaves = 8;                // waves per block
+constexpr int kEncThreads = 64 * kEncWaves;
 
 // LayerNorm of G rows held by a wave (row q's element i = lane + 64 j in
 // v[q][j]), each in the canonical order (as ln_row), interleaved.
@@ -70,14 +76,26 @@ __device__ __forceinline__ void ln_rows(float (&v)[G][NJ], const float (&g)[NJ],
       if (lane + 64 * j < d) v[q][j] = fmaf(v[q][j] * rstd[q], g[j], b[j]);
 }
 
+// Clears this block's share of the accumulators whose consumers have
+// finished (16-byte stores; the counts are multiples of 64).
+__device__ __forceinline__ void enc_clear(const EncIn& in) {
+  const int b = blockIdx.x, nb = in.nblk;
+  const int n0 = in.zero0_n / 4, n1 = in.zero1_n / 4;
+  const int per0 = (n0 + nb - 1) / nb, per1 = (n1 + nb - 1) / nb;
+  const int e0 = min(n0, (b + 1) * per0), e1 = min(n1, (b + 1) * per1);
+  for (int i = b * per0 + threadIdx.x; i < e0; i += kEncThreads) ((v4i*)in.zero0)[i] = v4i{0, 0, 0, 0};
+  for (int i = b * per1 + threadIdx.x; i < e1; i += kEncThreads) ((v4i*)in.zero1)[i] = v4i{0, 0, 0, 0};
+}
+
 // The sublayer input rows: the embedding or the pending residual update, the
-// LayerNorm, block 0's stores of the updated residual rows (x_out) and of the
-// int8 rows (q_out), and the int8 rows in a_lds (row stride D).  Wave w takes
-// rows w + 4 u, u < RPW, and issues all of their loads before it uses the
-// first (one memory round trip, two for the embedding's token lookup), then
-// calls issue_weights() to issue the kernel's other loads.  D is
-// the exact width, so no element needs a bounds check; EMBED is a template
-// flag so that no load sits behind a run-time branch.
+// LayerNorm, the stores of the updated residual rows (x_out) and of the int8
+// rows (q_out) (row r by block r mod nblk), and the int8 rows in a_lds (row
+// stride D).  Wave w takes rows w + kEncWaves u, u < RPW, and issues all of
+// their loads before it uses the first (one memory round trip, two for the
+// embedding's token lookup), then calls issue_weights() to issue the
+// kernel's other loads, then clears its share of the finished accumulators.
+// D is the exact width, so no element needs a bounds check; EMBED is a
+// template flag so that no load sits behind a run-time branch.
 template <int D, bool EMBED, int RPW, class Issue>
 __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue issue_weights) {
   constexpr int NJ = D / 64;
@@ -97,12 +115,12 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
     int tok[RPW];
 #pragma unroll
     for (int u = 0; u < RPW; ++u) {
-      const int t = in.tok[min(wave + 4 * u, R - 1)];
+      const int t = in.tok[min(wave + kEncWaves * u, R - 1)];
       tok[u] = t < 0 ? 0 : (t >= in.V ? in.V - 1 : t);
     }
 #pragma unroll
     for (int u = 0; u < RPW; ++u) {
-      const int pos = min(wave + 4 * u, R - 1) % in.S;
+      const int pos = min(wave + kEncWaves * u, R - 1) % in.S;
       ce[u] = in.c_emb[tok[u]];
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
@@ -114,7 +132,7 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
   } else {
 #pragma unroll
     for (int u = 0; u < RPW; ++u) {
-      const int r = min(wave + 4 * u, R - 1);
+      const int r = min(wave + kEncWaves * u, R - 1);
       ce[u] = 0.0f;
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
@@ -125,14 +143,16 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
     }
   }
   // the kernel's own loads go behind the rows' (the in-order memory counter
-  // then lets the rows be used before those arrive)
+  // then lets the rows be used before those arrive), the clearing stores
+  // behind both
   issue_weights();
-  // four rows at a time, so that their dependent chains (butterflies,
+  enc_clear(in);
+  // up to four rows at a time, so that their dependent chains (butterflies,
   // square root, division) interleave
-  constexpr int G = 4;
+  constexpr int G = RPW < 4 ? RPW : 4;
 #pragma unroll
   for (int u0 = 0; u0 < RPW; u0 += G) {
-    if (wave + 4 * u0 >= R) break;
+    if (wave + kEncWaves * u0 >= R) break;
     float v[G][NJ];
 #pragma unroll
     for (int q = 0; q < G; ++q)
@@ -147,11 +167,11 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
           v[q][j] = x[u][j];
       }
     if (in.ln_mode == 1) ln_rows<G, NJ>(v, g, b, D, in.eps);  // post-LN: normalize the residual stream
-    if (blockIdx.x == 0 && in.x_out) {
+    if (in.x_out) {
 #pragma unroll
       for (int q = 0; q < G; ++q) {
-        const int r = wave + 4 * (u0 + q);
-        if (r < R)
+        const int r = wave + kEncWaves * (u0 + q);
+        if (r < R && r % in.nblk == (int)blockIdx.x)
 #pragma unroll
           for (int j = 0; j < NJ; ++j) in.x_out[r * D + lane + 64 * j] = v[q][j];
       }
@@ -159,23 +179,18 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
     if (in.ln_mode == 2) ln_rows<G, NJ>(v, g, b, D, in.eps);  // pre-LN: normalize the sublayer input
 #pragma unroll
     for (int q = 0; q < G; ++q) {
-      const int r = wave + 4 * (u0 + q);
+      const int r = wave + kEncWaves * (u0 + q);
       if (r < R) {
+        const bool qst = in.q_out && r % in.nblk == (int)blockIdx.x;
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
           const int8_t c = code_of(v[q][j] * in.inv_s);
           a_lds[r * D + lane + 64 * j] = c;
-          if (blockIdx.x == 0 && in.q_out) in.q_out[r * D + lane + 64 * j] = c;
+          if (qst) in.q_out[r * D + lane + 64 * j] = c;
         }
       }
     }
   }
-}
-
-__device__ __forceinline__ void enc_clear(const EncIn& in) {
-  if (blockIdx.x != 0) return;
-  for (int i = threadIdx.x; i < in.zero0_n; i += kEncThreads) in.zero0[i] = 0;
-  for (int i = threadIdx.x; i < in.zero1_n; i += kEncThreads) in.zero1[i] = 0;
 }
 
 // A fragment of int8 rows [rows, K] in LDS (row stride ld): rows m0 + l % 16,
@@ -196,31 +211,35 @@ __device__ __forceinline__ void add_frag(int32_t* out, int ld, const v4i& acc, i
   }
 }
 
+// One block per head.
 template <int DMAX, bool EMBED, int RPW>
 __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) {
-  constexpr int KS = DMAX / 64;                   // 64-deep K steps over d
-  constexpr int PT = 3 * kEncHeadDim / 16 / 4;    // projection tiles per wave (3 dh / 16 over 4 waves)
-  constexpr int OT = DMAX / 64;                   // W_o column tiles per wave (d / 16 over 4 waves)
+  constexpr int KS = DMAX / 64;                                   // 64-deep K steps over d
+  constexpr int NT = 3 * kEncHeadDim / 16;                        // projection tiles of the widest head
+  constexpr int PT = (NT + kEncWaves - 1) / kEncWaves;            // projection tiles per wave
+  constexpr int OT = (DMAX / 16 + kEncWaves - 1) / kEncWaves;     // W_o column tiles per wave
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
-  __shared__ __attribute__((aligned(16))) int8_t qkv[3][kEncRows][kEncHeadDim];
+  __shared__ __attribute__((aligned(16))) int8_t qk[2][kEncRows][kEncHeadDim];
+  __shared__ __attribute__((aligned(16))) int8_t vt[kEncHeadDim][kEncRows];  // values, transposed
   __shared__ __attribute__((aligned(16))) int8_t ctx[kEncRows][kEncHeadDim];
-  __shared__ float sc[kEncRows][kEncRows];        // scores, then probabilities
+  __shared__ __attribute__((aligned(16))) float sc[kEncRows][kEncRows];      // scores, then probabilities
   const int hd = blockIdx.x;
   const int R = in.R, d = DMAX, dh = at.dh, S = in.S, ks = KS;
   const int mt_n = (R + 15) / 16;
   const int ntile = 3 * dh / 16;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
-  // 1. the rows, and behind their loads the weights: the head's Q|K|V rows
-  //    and its W_o columns, with the projection's scale and bias per lane
+  // 1. the rows, and behind their loads the weights (the head's Q|K|V rows
+  //    and its W_o columns, with the projection's scale and bias per lane) and
+  //    the lengths of the sentences of the wave's softmax rows
   v4i wf[PT][KS];
   float e_sc[PT], e_bi[PT];
   v4i of[OT];
-  enc_clear(in);
+  int nn[RPW];
   enc_rows<DMAX, EMBED, RPW>(in, a_lds, [&]() {
 #pragma unroll
     for (int u = 0; u < PT; ++u) {
-      const int j = 16 * min(wave + 4 * u, ntile - 1) + l16;  // row of the head's [q | k | v]
+      const int j = 16 * min(wave + kEncWaves * u, ntile - 1) + l16;  // row of the head's [q | k | v]
       const int part = (j >= dh) + (j >= 2 * dh);
       const int n = part * d + hd * dh + (j - part * dh);
 #pragma unroll
@@ -230,18 +249,21 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
     }
 #pragma unroll
     for (int u = 0; u < OT; ++u) {
-      const int n = 16 * (wave + 4 * u) + l16;
+      const int n = min(16 * (wave + kEncWaves * u) + l16, d - 1);
       of[u] = *(const v4i*)(at.Wo + n * d + hd * dh + 16 * min(kq, dh / 16 - 1));
     }
+#pragma unroll
+    for (int u = 0; u < RPW; ++u) nn[u] = at.len[min(wave + kEncWaves * u, R - 1) / S];
   });
   __syncthreads();
-  // 3. Q, K, V of the head, requantized into LDS
+  // 2. Q, K, V of the head, requantized into LDS (V transposed)
 #pragma unroll
   for (int u = 0; u < PT; ++u) {
-    const int tile = wave + 4 * u;
+    const int tile = wave + kEncWaves * u;
     if (tile >= ntile) continue;
     const int j = 16 * tile + l16;
     const int part = (j >= dh) + (j >= 2 * dh);
+    const int c = j - part * dh;
     for (int mt = 0; mt < mt_n; ++mt) {
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
@@ -250,31 +272,35 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int m = 16 * mt + 4 * kq + i;
-        if (m < R) qkv[part][m][j - part * dh] = code_of(fmaf((float)acc[i], e_sc[u], e_bi[u]));
+        if (m < R) {
+          const int8_t code = code_of(fmaf((float)acc[i], e_sc[u], e_bi[u]));
+          if (part == 2) vt[c][m] = code;
+          else qk[part][m][c] = code;
+        }
       }
     }
   }
   __syncthreads();
-  // 4. scores q . k (int32 exact) scaled by c_qk, every (query, key) pair
-  for (int t = wave; t < mt_n * mt_n; t += 4) {
+  // 3. scores q . k (int32 exact) scaled by c_qk, every (query, key) pair
+  for (int t = wave; t < mt_n * mt_n; t += kEncWaves) {
     const int mt = t / mt_n, kt = t % mt_n;
-    const v4i acc = mfma16(lds_frag(&qkv[0][0][0], kEncHeadDim, 16 * mt, 0, dh),
-                           lds_frag(&qkv[1][0][0], kEncHeadDim, 16 * kt, 0, dh), v4i{0, 0, 0, 0});
+    const v4i acc = mfma16(lds_frag(&qk[0][0][0], kEncHeadDim, 16 * mt, 0, dh),
+                           lds_frag(&qk[1][0][0], kEncHeadDim, 16 * kt, 0, dh), v4i{0, 0, 0, 0});
 #pragma unroll
     for (int i = 0; i < 4; ++i) sc[16 * mt + 4 * kq + i][16 * kt + l16] = (float)acc[i] * at.c_qk;
   }
   __syncthreads();
-  // 5. softmax of each row over its sentence's keys (one key per lane: the
-  //    canonical order), probabilities in place at sc[m][0 .. n)
+  // 4. softmax of each row over its sentence's keys (one key per lane: the
+  //    canonical order), probabilities in place at sc[m][0 .. n); keys from
+  //    n up to S rounded up to 4 get probability 0: fma(0, v, acc) leaves acc
+  //    unchanged bit for bit, so the context loop may run over them
   {
     float sv[RPW], ex[RPW];
-    int nn[RPW];
 #pragma unroll
     for (int u = 0; u < RPW; ++u) {
-      const int m = min(wave + 4 * u, R - 1);
+      const int m = min(wave + kEncWaves * u, R - 1);
       const int b = m / S;
-      int n = at.len[b];
-      nn[u] = n < 1 ? 1 : (n > S ? S : n);
+      nn[u] = nn[u] < 1 ? 1 : (nn[u] > S ? S : nn[u]);
       sv[u] = lane < nn[u] ? sc[m][b * S + lane] : -FLT_MAX;
     }
     float mx[RPW], inv[RPW];
@@ -285,33 +311,40 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
 #pragma unroll
     for (int u = 0; u < RPW; ++u) inv[u] = 1.0f / wave_sum(ex[u]);
     wave_sync();  // every lane has read its scores before any probability is written
-    // keys n .. S - 1 get probability 0: fma(0, v, acc) leaves acc unchanged
-    // bit for bit, so the context loop may run over all S keys
+    const int s4 = (S + 3) & ~3;
 #pragma unroll
     for (int u = 0; u < RPW; ++u) {
-      const int m = wave + 4 * u;
-      if (m < R && lane < S) sc[m][lane] = lane < nn[u] ? ex[u] * inv[u] : 0.0f;
+      const int m = wave + kEncWaves * u;
+      if (m < R && lane < s4) sc[m][lane] = lane < nn[u] ? ex[u] * inv[u] : 0.0f;
     }
   }
   __syncthreads();
-  // 6. context: ascending keys, one fma each, requantized
+  // 5. context: ascending keys, one fma each, requantized
   {
     // thread: column j = tid % dh of rows g0 + groups u (g0 = tid / dh), one
-    // fma chain per row over the keys of its sentence in ascending order
-    // (probability 0 past the sentence's length).  With one sentence the
-    // rows share each value load; rows past R repeat row R - 1, unstored.
-    constexpr int CPT = RPW;  // rows per thread at most (4 RPW rows over kEncThreads / dh >= 4 groups)
+    // fma chain per row over the keys of its sentence in ascending order.
+    // With one sentence the rows share each load of four values and read
+    // four probabilities at once; rows past R repeat row R - 1, unstored.
+    constexpr int CPT = RPW;  // rows per thread at most (kEncThreads / dh >= kEncWaves groups)
     const int groups = kEncThreads / dh;
     const int j = threadIdx.x % dh, g0 = threadIdx.x / dh;
     if (S == R) {  // one sentence
-      const int8_t* vcol = &qkv[2][0][j];
       float acc[CPT];
 #pragma unroll
       for (int u = 0; u < CPT; ++u) acc[u] = 0.0f;
-      for (int t = 0; t < S; ++t) {
-        const float v = (float)vcol[t * kEncHeadDim];
+      for (int t = 0; t < S; t += 4) {
+        const int v4 = *(const int*)&vt[j][t];
+        float v[4];
 #pragma unroll
-        for (int u = 0; u < CPT; ++u) acc[u] = fmaf(sc[min(g0 + groups * u, R - 1)][t], v, acc[u]);
+        for (int e = 0; e < 4; ++e) v[e] = (float)(int)(int8_t)(v4 >> (8 * e));
+#pragma unroll
+        for (int u = 0; u < CPT; ++u) {
+          const float4 p = *(const float4*)&sc[min(g0 + groups * u, R - 1)][t];
+          acc[u] = fmaf(p.x, v[0], acc[u]);
+          acc[u] = fmaf(p.y, v[1], acc[u]);
+          acc[u] = fmaf(p.z, v[2], acc[u]);
+          acc[u] = fmaf(p.w, v[3], acc[u]);
+        }
       }
 #pragma unroll
       for (int u = 0; u < CPT; ++u) {
@@ -322,16 +355,16 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       for (int m = g0; m < R; m += groups) {
         const int base = (m / S) * S;
         float acc = 0.0f;
-        for (int t = 0; t < S; ++t) acc = fmaf(sc[m][t], (float)qkv[2][base + t][j], acc);
+        for (int t = 0; t < S; ++t) acc = fmaf(sc[m][t], (float)vt[j][base + t], acc);
         ctx[m][j] = code_of(acc * at.c_pv);
       }
     }
   }
   __syncthreads();
-  // 7. the head's share of the output projection (K = dh), exact int32 sums
+  // 6. the head's share of the output projection (K = dh), exact int32 sums
 #pragma unroll
   for (int u = 0; u < OT; ++u) {
-    const int n0 = 16 * (wave + 4 * u);
+    const int n0 = 16 * (wave + kEncWaves * u);
     if (n0 >= d) continue;
     for (int mt = 0; mt < mt_n; ++mt) {
       const v4i acc = mfma16(lds_frag(&ctx[0][0], kEncHeadDim, 16 * mt, 0, dh), of[u], v4i{0, 0, 0, 0});
@@ -340,12 +373,13 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   }
 }
 
-// One block per kEncChunk hidden units, one 16-unit W1 tile per wave.
+// One block per kEncChunk hidden units: wave w computes the 16-unit W1 tile
+// w % 4 for the 16-row tiles w / 4, w / 4 + 2, ...
 template <int DMAX, int RPW>
 __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
   constexpr int KS = DMAX / 64;
-  constexpr int OT = DMAX / 64;
-  static_assert(kEncChunk == 64, "one W1 tile per wave and one K step of W2");
+  constexpr int OT = (DMAX / 16 + kEncWaves - 1) / kEncWaves;  // W2 column tiles per wave
+  static_assert(kEncChunk == 64 && kEncWaves == 8, "four W1 tiles, two row-tile phases, one K step of W2");
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
   __shared__ __attribute__((aligned(16))) int8_t hb[kEncRows][kEncChunk];
   const int R = in.R, d = DMAX, F = f.F, ks = KS;
@@ -353,11 +387,11 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
   const int f0 = blockIdx.x * kEncChunk;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
-  const int hrow = f0 + 16 * wave + l16;  // < F (F is a multiple of kEncChunk)
+  const int ht = wave & 3, mt0 = wave >> 2;
+  const int hrow = f0 + 16 * ht + l16;  // < F (F is a multiple of kEncChunk)
   v4i wf[KS];
   float e_sc, e_bi;
   v4i of[OT];
-  enc_clear(in);
   enc_rows<DMAX, false, RPW>(in, a_lds, [&]() {
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) wf[kk] = *(const v4i*)(f.W1 + hrow * d + 64 * kk + 16 * kq);
@@ -365,12 +399,12 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
     e_bi = f.bias1[hrow];
 #pragma unroll
     for (int u = 0; u < OT; ++u) {
-      const int n = 16 * (wave + 4 * u) + l16;
+      const int n = min(16 * (wave + kEncWaves * u) + l16, d - 1);
       of[u] = *(const v4i*)(f.W2 + n * F + f0 + 16 * kq);
     }
   });
   __syncthreads();
-  for (int mt = 0; mt < mt_n; ++mt) {
+  for (int mt = mt0; mt < mt_n; mt += 2) {
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
@@ -378,13 +412,13 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = 16 * mt + 4 * kq + i;
-      if (m < R) hb[m][16 * wave + l16] = code_of(fmaxf(fmaf((float)acc[i], e_sc, e_bi), 0.0f));
+      if (m < R) hb[m][16 * ht + l16] = code_of(fmaxf(fmaf((float)acc[i], e_sc, e_bi), 0.0f));
     }
   }
   __syncthreads();
 #pragma unroll
   for (int u = 0; u < OT; ++u) {
-    const int n0 = 16 * (wave + 4 * u);
+    const int n0 = 16 * (wave + kEncWaves * u);
     if (n0 >= d) continue;
     for (int mt = 0; mt < mt_n; ++mt) {
       const v4i acc = mfma16(lds_frag(&hb[0][0], kEncChunk, 16 * mt, 0, kEncChunk), of[u], v4i{0, 0, 0, 0});
@@ -393,10 +427,13 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
   }
 }
 
-// One block per kEncChunk columns of one decoder layer's cross K|V projection.
+// One block per kEncChunk columns of one decoder layer's cross K|V
+// projection: wave w computes the 16-column tile w % 4 for the 16-row tiles
+// w / 4, w / 4 + 2, ...
 template <int DMAX, int RPW>
 __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
   constexpr int KS = DMAX / 64;
+  static_assert(kEncChunk == 64 && kEncWaves == 8, "four column tiles, two row-tile phases");
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
   const int R = in.R, d = DMAX, ks = KS;
   const int mt_n = (R + 15) / 16;
@@ -406,10 +443,10 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
   const EncOut::Layer& L = o.layer[layer];
-  const int col = c0 + 16 * wave + l16;  // < 2 d
+  const int col = c0 + 16 * (wave & 3) + l16;  // < 2 d
+  const int mt0 = wave >> 2;
   v4i wf[KS];
   float e_sc, e_bi;
-  enc_clear(in);
   enc_rows<DMAX, false, RPW>(in, a_lds, [&]() {
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) wf[kk] = *(const v4i*)(L.W + col * d + 64 * kk + 16 * kq);
@@ -417,7 +454,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
     e_bi = L.bias[col];
   });
   __syncthreads();
-  for (int mt = 0; mt < mt_n; ++mt) {
+  for (int mt = mt0; mt < mt_n; mt += 2) {
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
@@ -437,21 +474,23 @@ bool enc_small_fits(int R, int S, int d, int dh, int F) {
          dh <= kEncHeadDim && F % kEncChunk == 0;
 }
 
-// exact width x rows per wave (8 for up to 32 rows, else 16)
+// exact width x rows per wave (4 for up to 32 rows, else 8)
 #define MNMT_ENC_BY_D(d, R, CALL)                        \
   switch ((d) * ((R) <= 32 ? 1 : -1)) {                 \
-    case 64: CALL(64, 8); break;                         \
-    case 128: CALL(128, 8); break;                       \
-    case 192: CALL(192, 8); break;                       \
-    case 256: CALL(256, 8); break;                       \
-    case -64: CALL(64, 16); break;                       \
-    case -128: CALL(128, 16); break;                     \
-    case -192: CALL(192, 16); break;                     \
-    case -256: CALL(256, 16); break;                     \
+    case 64: CALL(64, 4); break;                         \
+    case 128: CALL(128, 4); break;                       \
+    case 192: CALL(192, 4); break;                       \
+    case 256: CALL(256, 4); break;                       \
+    case -64: CALL(64, 8); break;                        \
+    case -128: CALL(128, 8); break;                      \
+    case -192: CALL(192, 8); break;                      \
+    case -256: CALL(256, 8); break;                      \
     default: return hipErrorInvalidValue;                \
   }
 
-hipError_t launch_enc_attn(const EncIn& in, const EncAttn& at, int heads, hipStream_t s) {
+hipError_t launch_enc_attn(const EncIn& in0, const EncAttn& at, int heads, hipStream_t s) {
+  EncIn in = in0;
+  in.nblk = heads;
 #define MNMT_E(DM, RPW)                                                                          \
   if (in.embed)                                                                                  \
     hipLaunchKernelGGL((k_enc_attn<DM, true, RPW>), dim3(heads), dim3(kEncThreads), 0, s, in, at); \
@@ -462,17 +501,21 @@ hipError_t launch_enc_attn(const EncIn& in, const EncAttn& at, int heads, hipStr
   return hipGetLastError();
 }
 
-hipError_t launch_enc_ffn(const EncIn& in, const EncFfn& f, hipStream_t s) {
+hipError_t launch_enc_ffn(const EncIn& in0, const EncFfn& f, hipStream_t s) {
   const int blocks = f.F / kEncChunk;
+  EncIn in = in0;
+  in.nblk = blocks;
 #define MNMT_E(DM, RPW) hipLaunchKernelGGL((k_enc_ffn<DM, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, f);
   MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
 #undef MNMT_E
   return hipGetLastError();
 }
 
-hipError_t launch_enc_out(const EncIn& in, const EncOut& o, hipStream_t s) {
+hipError_t launch_enc_out(const EncIn& in0, const EncOut& o, hipStream_t s) {
   if (o.layers < 1 || o.layers > EncOut::kMaxLayers) return hipErrorInvalidValue;
-  const int blocks = o.layers * (2 * in.d / kEncChunk);
+  const int blocks = o.layers * (2 * in0.d / kEncChunk);
+  EncIn in = in0;
+  in.nblk = blocks;
 #define MNMT_E(DM, RPW) hipLaunchKernelGGL((k_enc_out<DM, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, o);
   MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
 #undef MNMT_E

@@ -197,7 +197,7 @@ struct EncIn {             // the sublayer input rows of an encoder kernel
   const float* pe;
   int V;
   const float* x_in;       // residual rows [R, d]
-  float* x_out;            // block 0 stores the updated rows here (or null)
+  float* x_out;            // the blocks store the updated rows here (or null)
   const int32_t* acc;      // [R, d]: pending update x <- fma(gamma, x, fma(acc, scale, bias))
   const float* scale;      // [d]
   const float* bias;       // [d]
@@ -208,8 +208,10 @@ struct EncIn {             // the sublayer input rows of an encoder kernel
   int ln_mode;             // 0 none, 1 post-LN (the residual stream), 2 pre-LN (the sublayer input)
   float eps;
   float inv_s;             // 1 / input scale of the consuming layer
-  int8_t* q_out;           // block 0 stores the int8 rows here (or null)
-  int32_t* zero0;          // block 0 clears these accumulators (their consumers have finished)
+  int8_t* q_out;           // the blocks store the int8 rows here (or null)
+  int32_t* zero0;          // the blocks clear these accumulators (their consumers have finished);
+                           // zero0_n, zero1_n: multiples of 64
+  int nblk;                // blocks of the launch (set by the launcher)
   int zero0_n;
   int32_t* zero1;
   int zero1_n;
