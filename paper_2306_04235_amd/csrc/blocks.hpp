@@ -31,6 +31,17 @@ __device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
   return acc;
 }
 
+// Workgroup barrier that orders LDS accesses only: the fences name the local
+// address space, so the barrier waits for the wave's LDS operations but not
+// for its global loads (__syncthreads would wait for every load in flight,
+// including prefetches meant for a later phase).  Every block-level exchange
+// in these kernels goes through LDS.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // LDS-visibility barrier for the lanes of one wave (the other waves of the
 // block are not involved).
 __device__ __forceinline__ void wave_sync() {

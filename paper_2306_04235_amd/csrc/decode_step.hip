@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   // 2. the rows
   clear_acc(in);
   if (wave < R) finish_row(in, wave, d, rr, a_lds);
-  __syncthreads();
+  lds_barrier();
   // 3. Q (K, V) of the head on the matrix cores, requantized into LDS
   {
     const int arow = l16 < R ? l16 : 0;
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   // 4. attention of row `wave` (Appendix A with the quantizer figure's
   //    precisions): int8 scores, fp32 softmax in the canonical order, context
   //    accumulated over ascending positions with one fma each, requantized
@@ -279,7 +279,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
       ctx[r][j] = code_of(acc * at.c_pv);
     }
   }
-  __syncthreads();
+  lds_barrier();
   // 5. this head's share of the output projection (K = dh), exact int32
   //    partial sums added to the accumulator
   {
@@ -329,7 +329,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
   }
   clear_acc(in);
   if (wave < R) finish_row(in, wave, d, rr, a_lds);
-  __syncthreads();
+  lds_barrier();
   {
     const int arow = l16 < R ? l16 : 0;
     v4i acc = {0, 0, 0, 0};
@@ -341,7 +341,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
       for (int m = 0; m < kStepRows; ++m)
         if (m < R) h[m][16 * wave + lane] = code_of(fmaxf(fmaf((float)acc[m], e_sc, e_bi), 0.0f));
   }
-  __syncthreads();
+  lds_barrier();
   {
     const int hr = l16 < R ? l16 : 0;
     const v4i hf = *(const v4i*)(h[hr] + 16 * kq);
@@ -393,7 +393,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   } else if (wave < R && lane < d / 16) {
     *(v4i*)(a_lds + wave * d + 16 * lane) = xr;
   }
-  __syncthreads();
+  lds_barrier();
   const int arow = l16 < R ? l16 : 0;
   v4i af[KS];
 #pragma unroll
@@ -423,7 +423,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     const unsigned long long w = wave_max_u64(best[m]);
     if (lane == 0) wmax[wave][m] = w;
   }
-  __syncthreads();
+  lds_barrier();
   if (threadIdx.x < R) {
     const int m = threadIdx.x;
     unsigned long long b = wmax[0][m];

@@ -255,7 +255,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
 #pragma unroll
     for (int u = 0; u < RPW; ++u) nn[u] = at.len[min(wave + kEncWaves * u, R - 1) / S];
   });
-  __syncthreads();
+  lds_barrier();
   // 2. Q, K, V of the head, requantized into LDS (V transposed)
 #pragma unroll
   for (int u = 0; u < PT; ++u) {
@@ -280,7 +280,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   // 3. scores q . k (int32 exact) scaled by c_qk, every (query, key) pair
   for (int t = wave; t < mt_n * mt_n; t += kEncWaves) {
     const int mt = t / mt_n, kt = t % mt_n;
@@ -289,7 +289,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
 #pragma unroll
     for (int i = 0; i < 4; ++i) sc[16 * mt + 4 * kq + i][16 * kt + l16] = (float)acc[i] * at.c_qk;
   }
-  __syncthreads();
+  lds_barrier();
   // 4. softmax of each row over its sentence's keys (one key per lane: the
   //    canonical order), probabilities in place at sc[m][0 .. n); keys from
   //    n up to S rounded up to 4 get probability 0: fma(0, v, acc) leaves acc
@@ -318,7 +318,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       if (m < R && lane < s4) sc[m][lane] = lane < nn[u] ? ex[u] * inv[u] : 0.0f;
     }
   }
-  __syncthreads();
+  lds_barrier();
   // 5. context: ascending keys, one fma each, requantized
   {
     // thread: column j = tid % dh of rows g0 + groups u (g0 = tid / dh), one
@@ -360,7 +360,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   // 6. the head's share of the output projection (K = dh), exact int32 sums
 #pragma unroll
   for (int u = 0; u < OT; ++u) {
@@ -403,7 +403,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
       of[u] = *(const v4i*)(f.W2 + n * F + f0 + 16 * kq);
     }
   });
-  __syncthreads();
+  lds_barrier();
   for (int mt = mt0; mt < mt_n; mt += 2) {
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
@@ -415,7 +415,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
       if (m < R) hb[m][16 * ht + l16] = code_of(fmaxf(fmaf((float)acc[i], e_sc, e_bi), 0.0f));
     }
   }
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int u = 0; u < OT; ++u) {
     const int n0 = 16 * (wave + kEncWaves * u);
@@ -453,7 +453,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
     e_sc = L.scale[col];
     e_bi = L.bias[col];
   });
-  __syncthreads();
+  lds_barrier();
   for (int mt = mt0; mt < mt_n; mt += 2) {
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
