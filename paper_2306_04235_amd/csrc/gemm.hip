@@ -42,8 +42,11 @@ constexpr int kXcds = 8;
 __device__ __forceinline__ uint32_t code_bits(float y) {
   return __float_as_uint(fminf(fmaxf(y, -127.0f), 127.0f) + 12582912.0f);
 }
+// Low bytes of a, b, c, d in bytes 0..3 (three byte permutes).
 __device__ __forceinline__ uint32_t pack4(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
-  return (a & 0xffu) | ((b & 0xffu) << 8) | ((c & 0xffu) << 16) | (d << 24);
+  const uint32_t ab = __builtin_amdgcn_perm(b, a, 0x0c0c0400u);  // [a0, b0, 0, 0]
+  const uint32_t cd = __builtin_amdgcn_perm(d, c, 0x0c0c0400u);  // [c0, d0, 0, 0]
+  return __builtin_amdgcn_perm(cd, ab, 0x05040100u);            // [a0, b0, c0, d0]
 }
 
 template <int EPI>
@@ -76,7 +79,8 @@ __device__ __forceinline__ void store_fragment(const EpiArgs& e, const v16i& c, 
     const auto s02 = __builtin_amdgcn_permlane32_swap(w4[0], w4[2], false, false);
     const auto s13 = __builtin_amdgcn_permlane32_swap(w4[1], w4[3], false, false);
     const uint32_t o[4] = {s02[0], s02[1], s13[0], s13[1]};
-    const int n = nb + 16 * h;
+    int n = nb + 16 * h;
+    if (!FAST) asm volatile("" : "+v"(n), "+v"(m));  // keeps the checks below inside this path
     int8_t* y = (int8_t*)e.out + (size_t)m * e.ldo + n;
     if (FAST) {
       *(v4i*)y = v4i{(int)o[0], (int)o[1], (int)o[2], (int)o[3]};
@@ -87,6 +91,7 @@ __device__ __forceinline__ void store_fragment(const EpiArgs& e, const v16i& c, 
     }
     return;
   }
+  if (!FAST) asm volatile("" : "+v"(nb), "+v"(m));
   if (!FAST && m >= M) return;
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
@@ -249,6 +254,145 @@ __global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int 
   }
 }
 
+// Persistent variant for whole BN x BM tiles (M and N multiples of the tile,
+// K = KC KCN) and many of them.  Each block (4 waves, 2 per CU) walks its
+// XCD's tiles with a stride; a tile's K is taken in KC-byte chunks, each held
+// whole in LDS, and the next chunk (of this tile or the next) is loaded into
+// registers while the current one feeds the matrix cores and while the
+// finished tile's epilogue runs, so the loads of a tile overlap the previous
+// tile's work instead of being exposed at its start.  The barriers order LDS
+// only, so the prefetch stays in flight across them.  The loop body is
+// straight-line (the chunk loop unrolled, the prefetch unconditional: after
+// the last tile it reloads that tile), so the wait for the prefetch before it
+// goes to LDS does not include the tile's output stores issued after it
+// (loads and stores share one in-order counter).
+template <int EPI, int BN, int BM, int KC, int KCN>
+__global__ __launch_bounds__(256) void k_gemm_p(const int8_t* X, int ldx, const int8_t* W, int M, int K, int N,
+                                                const float* scale, const float* bias, EpiArgs e, int tiles_m,
+                                                int tiles, int nblk) {
+  constexpr int ROW = KC + 16;                 // padded LDS row
+  constexpr int CPR = KC / 16;                 // 16-byte chunks per row
+  constexpr int LW = BN * CPR / 256, LX = BM * CPR / 256;  // loads per thread and chunk
+  constexpr int FN = BN / 64, FM = BM / 64;    // 32 x 32 fragments per wave (2 x 2 waves)
+  static_assert(LW >= 1 && LX >= 1 && BN * CPR % 256 == 0 && BM * CPR % 256 == 0, "whole loads");
+  static_assert(256 % CPR == 0, "a load step covers whole rows");
+  constexpr int RPS = 256 / CPR;               // rows per load step
+  __shared__ __attribute__((aligned(16))) int8_t Ws[BN * ROW];
+  __shared__ __attribute__((aligned(16))) int8_t Xs[BM * ROW];
+  __shared__ __attribute__((aligned(16))) float sc_lds[2][BN], bi_lds[2][BN];  // per tile, alternating
+
+  // tiles of this block: its XCD's contiguous range (m fastest), strided by
+  // the XCD's block count
+  const int xcd = blockIdx.x % kXcds, nbx = nblk / kXcds;
+  const int per = (tiles + kXcds - 1) / kXcds;
+  const int end = min((xcd + 1) * per, tiles);
+  int tile = xcd * per + blockIdx.x / kXcds;
+  if (tile >= end) return;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave >> 1, wm = wave & 1;
+  const int l32 = lane & 31, h = lane >> 5;
+  const int lrow = tid / CPR, lcol = 16 * (tid % CPR);  // this thread's loads: rows lrow + RPS i, 16 bytes at lcol
+
+  v4i rw[LW], rx[LX];
+  float rs[(2 * BN + 255) / 256];
+  auto gload = [&](int t, int c) {  // c: compile-time after unrolling
+    const int m0 = (t % tiles_m) * BM, n0 = (t / tiles_m) * BN;
+    const int k0 = c * KC + lcol;
+#pragma unroll
+    for (int i = 0; i < LW; ++i) rw[i] = *(const v4i*)(W + (size_t)(n0 + lrow + RPS * i) * K + k0);
+#pragma unroll
+    for (int i = 0; i < LX; ++i) rx[i] = *(const v4i*)(X + (size_t)(m0 + lrow + RPS * i) * ldx + k0);
+    if (c == 0 && EPI != MNMT_EPI_I32) {
+#pragma unroll
+      for (int i = 0; i < (2 * BN + 255) / 256; ++i) {
+        const int q = tid + 256 * i;  // scale[0..BN), then bias[0..BN)
+        if (q < 2 * BN) rs[i] = q < BN ? scale[n0 + q] : (EPI == MNMT_EPI_LOGITS ? 0.0f : bias[n0 + q - BN]);
+      }
+    }
+  };
+  auto lstore = [&](int c, int sb) {
+#pragma unroll
+    for (int i = 0; i < LW; ++i) *(v4i*)(&Ws[(lrow + RPS * i) * ROW + lcol]) = rw[i];
+#pragma unroll
+    for (int i = 0; i < LX; ++i) *(v4i*)(&Xs[(lrow + RPS * i) * ROW + lcol]) = rx[i];
+    if (c == 0 && EPI != MNMT_EPI_I32) {
+#pragma unroll
+      for (int i = 0; i < (2 * BN + 255) / 256; ++i) {
+        const int q = tid + 256 * i;
+        if (q < 2 * BN) (q < BN ? sc_lds[sb] : bi_lds[sb])[q % BN] = rs[i];
+      }
+    }
+  };
+
+  int sb = 0;
+  gload(tile, 0);
+  lstore(0, 0);
+  lds_barrier();
+  for (;;) {
+    const int ntile = tile + nbx;
+    const bool has_next = ntile < end;
+    v16i acc[FN][FM];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int i = 0; i < FM; ++i) acc[j][i] = v16i{};
+#pragma unroll
+    for (int c = 0; c < KCN; ++c) {
+      if (c + 1 < KCN) gload(tile, c + 1);
+      else gload(has_next ? ntile : tile, 0);
+      // keeps the prefetch here: the compiler would otherwise sink the loads
+      // to their use after the epilogue (the LDS-only barriers let it; the
+      // operands are not declared restrict, so the loads cannot pass this)
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int kk = 0; kk < KC; kk += 32) {
+        v4i a[FN], bx[FM];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) a[j] = *(const v4i*)(&Ws[(BN / 2 * wn + 32 * j + l32) * ROW + kk + 16 * h]);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) bx[i] = *(const v4i*)(&Xs[(BM / 2 * wm + 32 * i + l32) * ROW + kk + 16 * h]);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int i = 0; i < FM; ++i)
+            acc[j][i] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[j], bx[i], acc[j][i], 0, 0, 0);
+      }
+      lds_barrier();  // every wave is done with the chunk in LDS
+      if (c + 1 < KCN) {
+        lstore(c + 1, sb);
+        lds_barrier();
+      }
+    }
+    {
+      const int m0 = (tile % tiles_m) * BM, n0 = (tile / tiles_m) * BN;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int cb = BN / 2 * wn + 32 * j;  // fragment's first column within the tile
+        float sc[4][4], bi[4][4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const v4f s4 = *(const v4f*)(&sc_lds[sb][cb + 8 * g + 4 * h]);
+          const v4f b4 = *(const v4f*)(&bi_lds[sb][cb + 8 * g + 4 * h]);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            sc[g][t] = EPI == MNMT_EPI_I32 ? 0.0f : s4[t];
+            bi[g][t] = EPI == MNMT_EPI_I32 ? 0.0f : b4[t];
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+          store_fragment<EPI, true>(e, acc[j][i], sc, bi, m0 + BM / 2 * wm + 32 * i + l32, n0 + cb, h, M, N);
+      }
+    }
+    if (!has_next) break;
+    sb ^= 1;  // the next tile's constants go to the other buffer
+    lstore(0, sb);
+    lds_barrier();
+    tile = ntile;
+  }
+}
+
 template <int BN, int BM, int WN, int WM>
 hipError_t launch_cfg(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
                       int N, const EpiArgs& e, hipStream_t s) {
@@ -271,14 +415,56 @@ hipError_t launch_cfg(const int8_t* X, int ldx, const int8_t* W, const float* sc
   return hipGetLastError();
 }
 
+template <int BN, int BM, int KC, int KCN>
+hipError_t launch_persistent(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
+                             int K, int N, const EpiArgs& e, hipStream_t s) {
+  const int tiles_m = M / BM, tiles = tiles_m * (N / BN);
+  // two blocks per CU: 32 CUs per XCD
+  const int nblk = min(kXcds * 64, (tiles + kXcds - 1) / kXcds * kXcds);
+#define MNMT_GEMM(EPI)                                                                                    \
+  hipLaunchKernelGGL((k_gemm_p<EPI, BN, BM, KC, KCN>), dim3(nblk), dim3(256), 0, s, X, ldx, W, M, K, N, scale, \
+                     bias, e, tiles_m, tiles, nblk)
+  switch (e.kind) {
+    case MNMT_EPI_I32: MNMT_GEMM(MNMT_EPI_I32); break;
+    case MNMT_EPI_I8: MNMT_GEMM(MNMT_EPI_I8); break;
+    case MNMT_EPI_I8_RELU: MNMT_GEMM(MNMT_EPI_I8_RELU); break;
+    case MNMT_EPI_F32: MNMT_GEMM(MNMT_EPI_F32); break;
+    case MNMT_EPI_F32_RESID: MNMT_GEMM(MNMT_EPI_F32_RESID); break;
+    case MNMT_EPI_LOGITS: MNMT_GEMM(MNMT_EPI_LOGITS); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef MNMT_GEMM
+  return hipGetLastError();
+}
+
+// Persistent configuration: 256 x 128 tiles (waves of 128 x 64, the fewest
+// LDS reads per MFMA that fit two waves per SIMD), 128-byte K chunks.
+constexpr int kPBN = 256, kPBM = 128, kPKC = 128;
+
 }  // namespace
 
-// The largest tile that still gives about two blocks per CU (256 CUs).
+// The persistent kernel for whole tiles (16-byte aligned rows), K a power-of-two
+// number of chunks and enough tiles for every block; otherwise the
+// largest slab-pipelined tile that still gives about two blocks per CU (256
+// CUs).
 hipError_t launch_gemm(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
                        int N, const EpiArgs& e, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   if (K % kBK) return hipErrorInvalidValue;
   auto tiles = [&](int bn, int bm) { return (long)((N + bn - 1) / bn) * ((M + bm - 1) / bm); };
+  const bool int8_out = e.kind == MNMT_EPI_I8 || e.kind == MNMT_EPI_I8_RELU;
+  const bool aligned = (reinterpret_cast<uintptr_t>(e.out) & 15) == 0 && e.ldo % (int8_out ? 16 : 4) == 0;
+  if (aligned && M % kPBM == 0 && N % kPBN == 0 && tiles(kPBN, kPBM) >= kXcds * 64 && ldx % 16 == 0 &&
+      (reinterpret_cast<uintptr_t>(X) & 15) == 0 && (reinterpret_cast<uintptr_t>(W) & 15) == 0 && K % kPKC == 0) {
+    switch (K / kPKC) {
+      case 1: return launch_persistent<kPBN, kPBM, kPKC, 1>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 2: return launch_persistent<kPBN, kPBM, kPKC, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 4: return launch_persistent<kPBN, kPBM, kPKC, 4>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 8: return launch_persistent<kPBN, kPBM, kPKC, 8>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 16: return launch_persistent<kPBN, kPBM, kPKC, 16>(X, ldx, W, scale, bias, M, K, N, e, s);
+      default: break;
+    }
+  }
   constexpr long kFill = 512;
   if (tiles(256, 128) >= kFill) return launch_cfg<256, 128, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
   if (tiles(128, 128) >= kFill) return launch_cfg<128, 128, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);

@@ -115,6 +115,34 @@ def test_qlinear_all_epilogues(torch_dev, M, K, N):
     assert np.array_equal(got[rows].view(np.uint32), ref.view(np.uint32))
 
 
+@pytest.mark.parametrize("M,K,N", [(2048, 256, 8192), (1024, 1024, 16384), (768, 2048, 22016), (4096, 512, 4096)],
+                         ids=lambda v: str(v))
+def test_qlinear_persistent_gemm_epilogues(torch_dev, M, K, N):
+    """Whole 256 x 128 tiles and at least 512 of them: the persistent GEMM
+    (2, 8, 16 and 4 chunks of 128 bytes of K), every epilogue, sampled rows."""
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    print(f"persistent GEMM M={M} K={K} N={N}", flush=True)
+    X, W, mult, bias = G.sweep_case(M, K, N, seed=7)
+    rows = np.unique(np.concatenate([[0, 127, 128, M - 1], np.random.default_rng(3).choice(M, 28, replace=False)]))
+    acc = oracle.qgemm_i32(X[rows], W)
+    got = _run(torch, dev, X, W, mult, bias, mnmt.EPI_I32)
+    assert np.array_equal(got[rows], acc)
+    for epi, oepi in ((mnmt.EPI_I8, oracle.EPI_I8), (mnmt.EPI_I8_RELU, oracle.EPI_I8_RELU)):
+        got = _run(torch, dev, X, W, mult, bias, epi)
+        assert np.array_equal(got[rows], oracle.qlinear(X[rows], W, mult, bias, oepi))
+    dq = (mult * 1e-3).astype(np.float32)
+    for epi in (mnmt.EPI_F32, mnmt.EPI_LOGITS):
+        got = _run(torch, dev, X, W, dq, bias, epi)
+        ref = oracle.qlinear(X[rows], W, dq, bias, epi)
+        assert np.array_equal(got[rows].view(np.uint32), ref.view(np.uint32))
+    resid = np.random.default_rng(4).normal(0, 1, (M, N)).astype(np.float32)
+    got = _run(torch, dev, X, W, dq, bias, mnmt.EPI_F32_RESID, gamma=0.75, resid=resid)
+    ref = oracle.qlinear(X[rows], W, dq, bias, oracle.EPI_F32_RESID, gamma=0.75, resid=resid[rows])
+    assert np.array_equal(got[rows].view(np.uint32), ref.view(np.uint32))
+
+
 @pytest.mark.parametrize("M,K,N", [(1, 256, 32000), (2, 512, 32000), (1, 64, 1000), (2, 128, 33), (1, 384, 129),
                                    (3, 256, 1000), (8, 1024, 4097), (2, 1024, 500)], ids=lambda v: str(v))
 def test_qlinear_fused_argmax(torch_dev, M, K, N):
