@@ -277,6 +277,29 @@ def main():
     qgemm = {"shape": [M, K, N], "epilogue": "i8 requant", "tops": round(tops, 1), "peak": I8_PEAK_TOPS,
              "frac": round(tops / I8_PEAK_TOPS, 4), "avg_us": round(gemm_ms * 1e3, 2)}
 
+    # The paper's own MobileNMT-10MB / 20MB shapes on the same batch-1 path
+    # (context beside the paper's phone latencies, not the headline workload).
+    paper = {}
+    for cfg in (G.PAPER_10MB, G.PAPER_20MB):
+        pm = mnmt.Model(G.build_model(cfg))
+        psrc, plen = G.make_sources(cfg.vocab, 1, [30], seed=2010 + cfg.d_model, s_max=30)
+        ps = mnmt.Session(pm, 1, 30, 30, 1)
+        pt, pl = torch.from_numpy(psrc).to(dev), torch.from_numpy(plen).to(dev)
+        pouts = (torch.empty((1, 30), dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev),
+                 torch.empty(1, dtype=torch.float32, device=dev))
+        for _ in range(5):
+            ps.translate(pt, pl, beam=1, max_steps=30, use_graph=True, out=pouts)
+        torch.cuda.synchronize()
+        p0 = time.perf_counter()
+        for _ in range(20):
+            ps.translate(pt, pl, beam=1, max_steps=30, use_graph=True, out=pouts)
+        torch.cuda.synchronize()
+        pe = time.perf_counter() - p0
+        paper[cfg.name] = {"ms_per_sentence": round(pe * 1e3 / 20, 4),
+                           "tokens_per_s": round(int(pouts[1].sum().item()) * 20 / pe, 1)}
+        ps.close()
+        pm.close()
+
     line = {
         "metric": "decoded tokens/sec at batch 1 (greedy, 30-token sentences)",
         "value": round(tokens / elapsed, 1),
@@ -296,6 +319,7 @@ def main():
                    "dec_layers": info.n_dec, "vocab": info.vocab, "graph": True},
         "roofline": roofline,
         "qgemm": qgemm,
+        "paper_shapes_b1_greedy30": paper,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w)

@@ -147,6 +147,16 @@ def test_mobile_greedy_latency_workload(torch_dev):
     _greedy_check(torch, dev, "MOBILE", src, lens, 30)
 
 
+@pytest.mark.parametrize("cfg", [G.PAPER_10MB, G.PAPER_20MB], ids=lambda c: c.name)
+def test_paper_model_shapes_greedy(torch_dev, cfg):
+    """The paper's MobileNMT-10MB / 20MB settings (vocabulary 8000, width 256 /
+    384, 4 / 6 heads of 64, FFN 512 / 768, 12 + 2 layers): batch 1, 30 source
+    tokens, 30 greedy steps, tokens and logits against the oracle."""
+    torch, dev = torch_dev
+    src, lens = G.make_sources(cfg.vocab, 1, [30], seed=2010 + cfg.d_model, s_max=30)
+    _greedy_check(torch, dev, cfg, src, lens, 30)
+
+
 def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None):
     from paper_2306_04235_amd import mnmt
 
