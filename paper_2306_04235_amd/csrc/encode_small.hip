@@ -470,8 +470,10 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
 }  // namespace
 
 bool enc_small_fits(int R, int S, int d, int dh, int F) {
-  return R >= 1 && R <= kEncRows && S <= kEncRows && d % 64 == 0 && d <= 256 && dh % 16 == 0 &&
-         dh <= kEncHeadDim && F % kEncChunk == 0;
+  // (512 only up to 32 rows: with 8 rows per wave its attention kernel spills)
+  const bool width = d == 64 || d == 128 || d == 192 || d == 256 || d == 384 || (d == 512 && R <= 32);
+  return R >= 1 && R <= kEncRows && S <= kEncRows && width && dh % 16 == 0 && dh <= kEncHeadDim &&
+         F % kEncChunk == 0;
 }
 
 // exact width x rows per wave (4 for up to 32 rows, else 8)
@@ -481,10 +483,13 @@ bool enc_small_fits(int R, int S, int d, int dh, int F) {
     case 128: CALL(128, 4); break;                       \
     case 192: CALL(192, 4); break;                       \
     case 256: CALL(256, 4); break;                       \
+    case 384: CALL(384, 4); break;                       \
+    case 512: CALL(512, 4); break;                       \
     case -64: CALL(64, 8); break;                        \
     case -128: CALL(128, 8); break;                      \
     case -192: CALL(192, 8); break;                      \
     case -256: CALL(256, 8); break;                      \
+    case -384: CALL(384, 8); break;                      \
     default: return hipErrorInvalidValue;                \
   }
 

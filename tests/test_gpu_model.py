@@ -147,6 +147,20 @@ def test_mobile_greedy_latency_workload(torch_dev):
     _greedy_check(torch, dev, "MOBILE", src, lens, 30)
 
 
+WIDE384 = G.ModelConfig("wide-384", 384, 6, 768, 2, 1, 600, ln_post=0, seed=83, random_gamma=True, weight_std=0.05)
+WIDE512 = G.ModelConfig("wide-512", 512, 8, 1024, 2, 1, 600, ln_post=0, seed=84, random_gamma=True, weight_std=0.05)
+
+
+def test_small_encoder_wide_models(torch_dev):
+    """The batch-1 encoder kernels at widths 384 (two sentences, 50 rows: 8 rows
+    per wave, attention within each sentence) and 512 (one sentence of 20)."""
+    torch, dev = torch_dev
+    src, lens = G.make_sources(WIDE384.vocab, 2, [25, 19], seed=41, s_max=25)
+    _greedy_check(torch, dev, WIDE384, src, lens, 8)
+    src, lens = G.make_sources(WIDE512.vocab, 1, [20], seed=42, s_max=20)
+    _greedy_check(torch, dev, WIDE512, src, lens, 8)
+
+
 @pytest.mark.parametrize("cfg", [G.PAPER_10MB, G.PAPER_20MB], ids=lambda c: c.name)
 def test_paper_model_shapes_greedy(torch_dev, cfg):
     """The paper's MobileNMT-10MB / 20MB settings (vocabulary 8000, width 256 /
