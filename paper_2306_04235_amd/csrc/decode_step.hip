@@ -112,9 +112,11 @@ __device__ __forceinline__ void clear_acc(const StepIn& in) {
 // row l % 16 (of the activations for A, of the weights for B).
 
 // One block per head.  DMAX: model width class; NI: attended positions per
-// lane (n <= 64 NI).
-template <int DMAX, bool SELF, int NI>
-__global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn at) {
+// lane (n <= 64 NI).  MODE 1 (self, layer 0): the input rows are the
+// embeddings of the previous step's arg-max tokens, found from cm's partials;
+// MODE 2 (cross, layer 0): block 0 records those tokens.
+template <int DMAX, bool SELF, int NI, int MODE>
+__global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn at, StepCommit cm) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;      // 64-deep K steps of the projection
   constexpr int TPW = SELF ? 3 : 1;  // 16-row projection tiles per wave (12 or 4 per head)
@@ -133,7 +135,32 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   //    projection's weight fragments with their scales and biases, the W_o
   //    fragments, the keys and values
   RowRegs<NJ> rr;
-  load_row(in, min(wave, R - 1), d, rr);
+  // MODE 1 / 2: the arg-max partials of the wave's row (lane i: slots i + 64 k)
+  // and whether the row had finished
+  unsigned long long pk[4] = {0ull, 0ull, 0ull, 0ull};
+  int fin = 0;
+  if (MODE != 0) {
+    const int row = min(wave, R - 1);
+    const unsigned long long* sl = cm.slots + (size_t)row * cm.nslots;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pk[k] = sl[min(lane + 64 * k, cm.nslots - 1)];
+    fin = cm.finished[row];
+  }
+  if (MODE == 1) {
+    // the position term now, the token's embedding once the token is known
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = min(lane + 64 * j, d - 1);
+      rr.x[j] = cm.pe[(size_t)cm.t * d + i];
+      rr.a[j] = 0;
+      rr.sc[j] = 0.0f;
+      rr.bi[j] = 0.0f;
+      rr.g[j] = in.ln_g[i];
+      rr.b[j] = in.ln_b[i];
+    }
+  } else {
+    load_row(in, min(wave, R - 1), d, rr);
+  }
   v4i wf[TPW][KS];
   float e_sc[TPW], e_bi[TPW];
 #pragma unroll
@@ -173,9 +200,38 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   }
   int n_att = SELF ? at.t + 1 : at.len[r];
   n_att = SELF ? n_att : (n_att < 1 ? 1 : (n_att > at.S ? at.S : n_att));
+  int tok = 0;
+  if (MODE != 0) {
+    unsigned long long key = pk[0];
+#pragma unroll
+    for (int k = 1; k < 4; ++k) key = pk[k] > key ? pk[k] : key;
+    tok = unpack_index(wave_max_u64(key));
+  }
+  if (MODE == 1) {
+    // x = E[tok] c_emb[tok] + PE[t] (padding after the end of the sentence)
+    int te = fin ? cm.pad : tok;
+    te = te < 0 ? 0 : (te >= cm.V ? cm.V - 1 : te);
+    const float ce = cm.c_emb[te];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = min(lane + 64 * j, d - 1);
+      rr.x[j] = fmaf((float)cm.E[(size_t)te * d + i], ce, rr.x[j]);
+    }
+  }
   // 2. the rows
   clear_acc(in);
   if (wave < R) finish_row(in, wave, d, rr, a_lds);
+  if (MODE == 2 && blockIdx.x == 0 && wave < R && lane == 0) {
+    // step t - 1's token: output, end of sentence, current token, step counter
+    const int tc = cm.t - 1;
+    if (tc < cm.T) cm.out_tok[(size_t)tc * R + wave] = fin ? cm.pad : tok;
+    if (!fin && cm.stop_at_eos && tok == cm.eos) {
+      cm.finished[wave] = 1;
+      cm.out_len[wave] = tc + 1;
+    }
+    cm.cur_tok[wave] = fin ? cm.pad : tok;
+    if (wave == 0) *cm.step = cm.t;
+  }
   lds_barrier();
   // 3. Q (K, V) of the head on the matrix cores, requantized into LDS
   {
@@ -466,10 +522,20 @@ int step_logits_blocks(int V) {
     default: CALL(512); break;        \
   }
 
-hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s) {
+hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s,
+                            const StepCommit* cm) {
   // positions attended: self t + 1 <= T, cross at most S
   const int n_max = self ? at.t + 1 : at.S;
-#define MNMT_ATTN_NI(DM, SELF, NI) hipLaunchKernelGGL((k_step_attn<DM, SELF, NI>), dim3(heads), dim3(kStepThreads), 0, s, in, at)
+  if (cm && (cm->nslots < 1 || cm->nslots > 256 || cm->t < 1)) return hipErrorInvalidValue;
+  const StepCommit c = cm ? *cm : StepCommit{};
+#define MNMT_ATTN_NI(DM, SELF, NI)                                                                               \
+  do {                                                                                                           \
+    if (!cm)                                                                                                     \
+      hipLaunchKernelGGL((k_step_attn<DM, SELF, NI, 0>), dim3(heads), dim3(kStepThreads), 0, s, in, at, c);     \
+    else                                                                                                         \
+      hipLaunchKernelGGL((k_step_attn<DM, SELF, NI, SELF ? 1 : 2>), dim3(heads), dim3(kStepThreads), 0, s, in, at, \
+                         c);                                                                                     \
+  } while (0)
 #define MNMT_ATTN(DM)                                   \
   if (self) {                                           \
     if (n_max <= 64) MNMT_ATTN_NI(DM, true, 1);         \

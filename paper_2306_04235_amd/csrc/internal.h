@@ -161,6 +161,27 @@ struct StepAttn {
   float c_qk, c_pv;
   int32_t* acc_out;        // [R, d] int32, zero on entry
 };
+// The greedy commit of the previous step's token, folded into the next
+// step's first layer: the self-attention kernel of layer 0 reads the previous
+// logits kernel's per-block arg-max partials and embeds the token itself (at
+// position t), and block 0 of the cross-attention kernel of layer 0 records it
+// (the bookkeeping runs one kernel later, so no block reads `finished` while
+// another writes it).
+struct StepCommit {
+  const unsigned long long* slots;  // [R][nslots] arg-max partials of step t - 1
+  int nslots;                       // at most 256
+  const int8_t* E;                  // embedding [V, d], its scales, the position table
+  const float* c_emb;
+  const float* pe;
+  int V;
+  int t;                            // this step (the committed token is step t - 1's)
+  int32_t* finished;
+  int32_t* out_tok;                 // [T][R]
+  int32_t* out_len;
+  int32_t* cur_tok;
+  int* step;
+  int T, stop_at_eos, eos, pad;
+};
 struct StepFfn {
   int R, d, F;
   const int8_t* W1;
@@ -181,7 +202,10 @@ struct StepLogits {
 bool step_path_fits(int R, int d, int dh, int F, int T, int S);
 bool step_logits_fits(int R, int d);  // R <= 2, d a multiple of 64 up to 512
 int step_logits_blocks(int V);        // blocks (and arg-max partials per row) of launch_step_logits
-hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s);
+// cm (or null): self = 1 embeds the previous step's token from its partials
+// (layer 0, the rows' x_in unused); self = 0 records that token (block 0).
+hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s,
+                            const StepCommit* cm = nullptr);
 hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s);
 // With ev_start / ev_stop the events take the kernel's own start and end times.
 hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s, hipEvent_t ev_start = nullptr,

@@ -502,7 +502,15 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
 // residual update in its prologue; the three int32 accumulators (W_o, W_oc,
 // W2 partial sums) are cleared by the kernel after their consumer, and the
 // residual rows alternate between two buffers.
-int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s) {
+// The commit folds into the next step when every row's partials fit one
+// wave's four loads per lane.
+bool fold_ok(const mnmt_model* m) { return fused_slots_per_row(m->info.vocab) <= 256; }
+
+// fold (a whole translation's steps): step t > 0 embeds and records step t -
+// 1's token inside its first layer instead of a commit kernel after step t -
+// 1; the last step commits as usual.
+int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s, bool fold,
+                   bool last_step) {
   const mnmt_model* m = S->m;
   const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
   const bool post = m->info.ln_post;
@@ -566,13 +574,35 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     return at;
   };
   const LnDev none{};
+  const bool folded = fold && t > 0 && fold_ok(m);
+  StepCommit cm{};
+  if (folded) {
+    cm.slots = S->fslots;
+    cm.nslots = fused_slots_per_row(m->info.vocab);
+    cm.E = m->E;
+    cm.c_emb = m->c_emb;
+    cm.pe = m->pe;
+    cm.V = m->info.vocab;
+    cm.t = t;
+    cm.finished = S->finished;
+    cm.out_tok = S->out_tok;
+    cm.out_len = S->out_len;
+    cm.cur_tok = S->cur_tok;
+    cm.step = S->step;
+    cm.T = T;
+    cm.stop_at_eos = stop_at_eos;
+    cm.eos = m->info.eos_id;
+    cm.pad = m->info.pad_id;
+  }
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
+    const StepCommit* cml = folded && l == 0 ? &cm : nullptr;
     {  // self-attention block
       StepIn in = base(L.qkv.inv_in);
       if (l == 0) {
-        // the embeddings are the residual stream as they are
-        in.x_out = nullptr;
+        // the embeddings are the residual stream as they are (folded: the
+        // kernel computes them and block 0 stores them for the next kernel)
+        if (!cml) in.x_out = nullptr;
         rows(in, nullptr, nullptr, 1.0f, none, L.sa_ln);
       } else {
         const LayerDev& P = m->dec[l - 1];
@@ -583,7 +613,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       StepAttn at = attn(L, true, acc_o);
       at.kcache = S->kcache[l];
       at.vcache = S->vcache[l];
-      LAUNCH(launch_step_attn(in, at, 1, h, s));
+      LAUNCH(launch_step_attn(in, at, 1, h, s, cml));
       if (in.x_out) std::swap(xa, xb);
     }
     {  // cross-attention block
@@ -593,7 +623,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       in.zero_n = nacc;
       StepAttn at = attn(L, false, acc_oc);
       at.kv = S->cross_kv[l];
-      LAUNCH(launch_step_attn(in, at, 0, h, s));
+      LAUNCH(launch_step_attn(in, at, 0, h, s, cml));
       std::swap(xa, xb);
     }
     {  // FFN block
@@ -653,6 +683,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   gv.d = d;
   gv.V = m->info.vocab;
   gv.P = m->info.max_pos;
+  if (fold && !last_step && fold_ok(m)) return MNMT_OK;  // the next step's first layer commits
   LAUNCH(launch_greedy_commit_slots(gv, s));
   return MNMT_OK;
 }
@@ -672,8 +703,9 @@ int embed_step_input(mnmt_session* S, int R, hipStream_t s) {
 
 // The greedy step for R rows on the fastest path that fits.
 // On the 1-2 row path the input rows must be in dec_x (embed_step_input).
-int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s) {
-  if (step_path_used(S, R)) return greedy_step_v3(S, R, t, stop_at_eos, logits_out, s);
+int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s,
+                    bool fold = false, bool last = false) {
+  if (step_path_used(S, R)) return greedy_step_v3(S, R, t, stop_at_eos, logits_out, s, fold, last);
   if (R <= 8) return greedy_step_fused(S, R, t, stop_at_eos, logits_out, s);
   return greedy_step(S, R, stop_at_eos, logits_out, s);
 }
@@ -701,7 +733,7 @@ int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
                                m->info.bos_id, S->fslots, 8 * fused_slots_per_row(m->info.vocab) + 3 * 2 * m->info.d_model / 2, s));
     if (step_path_used(S, R) && (rc = embed_step_input(S, R, s))) return rc;
     for (int t = 0; t < sc.max_steps; ++t)
-      if ((rc = greedy_step_any(S, R, t, sc.stop_at_eos, nullptr, s))) return rc;
+      if ((rc = greedy_step_any(S, R, t, sc.stop_at_eos, nullptr, s, true, t + 1 == sc.max_steps))) return rc;
   } else {
     const int R = S->B * sc.beam;
     LAUNCH(launch_beam_reset(S->beam, S->step, s));
