@@ -201,6 +201,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-paper-shapes", action="store_true", help="skip the paper-shape side measurements")
     ap.add_argument("--counters", action="store_true", help="only the roofline kernel and the copy (for --pmc)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--ingest-command", default="")
@@ -280,7 +281,7 @@ def main():
     # The paper's own MobileNMT-10MB / 20MB shapes on the same batch-1 path
     # (context beside the paper's phone latencies, not the headline workload).
     paper = {}
-    for cfg in (G.PAPER_10MB, G.PAPER_20MB):
+    for cfg in () if args.no_paper_shapes else (G.PAPER_10MB, G.PAPER_20MB):
         pm = mnmt.Model(G.build_model(cfg))
         psrc, plen = G.make_sources(cfg.vocab, 1, [30], seed=2010 + cfg.d_model, s_max=30)
         ps = mnmt.Session(pm, 1, 30, 30, 1)

@@ -200,14 +200,11 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   }
   int n_att = SELF ? at.t + 1 : at.len[r];
   n_att = SELF ? n_att : (n_att < 1 ? 1 : (n_att > at.S ? at.S : n_att));
-  int tok = 0;
-  if (MODE != 0) {
+  if (MODE == 1) {
     unsigned long long key = pk[0];
 #pragma unroll
     for (int k = 1; k < 4; ++k) key = pk[k] > key ? pk[k] : key;
-    tok = unpack_index(wave_max_u64(key));
-  }
-  if (MODE == 1) {
+    const int tok = unpack_index(wave_max_u64(key));
     // x = E[tok] c_emb[tok] + PE[t] (padding after the end of the sentence)
     int te = fin ? cm.pad : tok;
     te = te < 0 ? 0 : (te >= cm.V ? cm.V - 1 : te);
@@ -221,17 +218,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   // 2. the rows
   clear_acc(in);
   if (wave < R) finish_row(in, wave, d, rr, a_lds);
-  if (MODE == 2 && blockIdx.x == 0 && wave < R && lane == 0) {
-    // step t - 1's token: output, end of sentence, current token, step counter
-    const int tc = cm.t - 1;
-    if (tc < cm.T) cm.out_tok[(size_t)tc * R + wave] = fin ? cm.pad : tok;
-    if (!fin && cm.stop_at_eos && tok == cm.eos) {
-      cm.finished[wave] = 1;
-      cm.out_len[wave] = tc + 1;
-    }
-    cm.cur_tok[wave] = fin ? cm.pad : tok;
-    if (wave == 0) *cm.step = cm.t;
-  }
+
   lds_barrier();
   // 3. Q (K, V) of the head on the matrix cores, requantized into LDS
   {
@@ -351,6 +338,24 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
           for (int m = 0; m < kStepRows; ++m)
             if (m < R) atomicAdd(at.acc_out + (size_t)m * d + n0 + lane, acc[m]);
       }
+    }
+  }
+  if (MODE == 2 && blockIdx.x == 0) {
+    // step t - 1's token (off the critical path, at the end): output, end of
+    // sentence, current token, step counter
+    unsigned long long key = pk[0];
+#pragma unroll
+    for (int k = 1; k < 4; ++k) key = pk[k] > key ? pk[k] : key;
+    const int tok = unpack_index(wave_max_u64(key));
+    if (wave < R && lane == 0) {
+      const int tc = cm.t - 1;
+      if (tc < cm.T) cm.out_tok[(size_t)tc * R + wave] = fin ? cm.pad : tok;
+      if (!fin && cm.stop_at_eos && tok == cm.eos) {
+        cm.finished[wave] = 1;
+        cm.out_len[wave] = tc + 1;
+      }
+      cm.cur_tok[wave] = fin ? cm.pad : tok;
+      if (wave == 0) *cm.step = cm.t;
     }
   }
 }
