@@ -127,7 +127,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   __shared__ __attribute__((aligned(16))) int8_t ctx[kStepRows][kStepHeadDim];
   __shared__ AttnLdsT<64 * NI, kStepHeadDim> att[kStepRows];
   const int hd = blockIdx.x;
-  const int R = at.R, d = at.d, dh = at.dh, nc = dh / 16, ks = d / 64;
+  const int R = at.R, d = DMAX, dh = at.dh, nc = dh / 16, ks = d / 64;  // DMAX is the exact width
   const int ntile = (SELF ? 3 : 1) * dh / 16;  // projection tiles of this head
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
@@ -371,7 +371,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
   static_assert(kFfnChunk == 64, "one W1 tile per wave and one K step of W2");
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
   __shared__ __attribute__((aligned(16))) int8_t h[kStepRows][kFfnChunk];
-  const int R = f.R, d = f.d, F = f.F, ks = d / 64;
+  const int R = f.R, d = DMAX, F = f.F, ks = d / 64;  // DMAX is the exact width
   const int f0 = blockIdx.x * kFfnChunk;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
@@ -431,7 +431,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   constexpr int TPW = kLogitsTiles;
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
   __shared__ unsigned long long wmax[4][kStepRows];
-  const int R = g.R, d = g.d, N = g.V, ks = d / 64;
+  const int R = g.R, d = DMAX, N = g.V, ks = d / 64;  // DMAX is the exact width
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
   const int row0 = (blockIdx.x * 4 + wave) * TPW * 16;
@@ -518,13 +518,19 @@ int step_logits_blocks(int V) {
   return (V + rpb - 1) / rpb;
 }
 
+// Kernels are instantiated on the exact width (a multiple of 64 up to 512),
+// so the row code carries no bounds checks.
 #define MNMT_BY_D(d, CALL)            \
-  switch (row_class(d)) {             \
+  switch (d) {                        \
     case 64: CALL(64); break;         \
     case 128: CALL(128); break;       \
+    case 192: CALL(192); break;       \
     case 256: CALL(256); break;       \
+    case 320: CALL(320); break;       \
     case 384: CALL(384); break;       \
-    default: CALL(512); break;        \
+    case 448: CALL(448); break;       \
+    case 512: CALL(512); break;       \
+    default: return hipErrorInvalidValue; \
   }
 
 hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s,
