@@ -93,23 +93,24 @@ def _traffic(kernel_tag):
 
 def _roofline_kernel(torch, np, mnmt, WL, G, info, blob, dev, stream):
     """The roofline kernel as a closure, and its algorithmic bytes per launch:
-    the int8 embedding [V, d], the fp32 output scales [V], one int8 row, one
-    8-byte arg-max slot."""
+    the int8 embedding [V, d], the fp32 output scales [V], one int8 row, and
+    the 8-byte arg-max partial of every block (the store pattern of the batch-1
+    decode step)."""
     from synth.modelfile import read_model
 
     dims = WL.Dims(info.d_model, info.n_heads, info.d_ffn, info.n_enc, info.n_dec, info.vocab)
-    alg_bytes = WL.logits_gemv_bytes(dims) + info.d_model + 8
+    alg_bytes = WL.logits_gemv_bytes(dims) + info.d_model + 8 * mnmt.argmax_partials(info.vocab)
     _, tens = read_model(blob)
     x = torch.randint(-127, 128, (1, info.d_model), dtype=torch.int8, device=dev)
     E = torch.from_numpy(np.array(tens["emb.w"])).to(dev)
     c_out = torch.from_numpy(np.array(tens["emb.s"])).to(dev)  # the values do not affect the timing
-    slot = torch.zeros(1, dtype=torch.int64, device=dev)
+    slot = torch.zeros((1, mnmt.argmax_partials(info.vocab)), dtype=torch.int64, device=dev)
 
     def fn(e0=None, e1=None):
         if e0 is None:
-            mnmt.mnmt_qlinear(x, E, c_out, None, mnmt.EPI_ARGMAX, out=slot, stream=stream)
+            mnmt.mnmt_qlinear(x, E, c_out, None, mnmt.EPI_ARGMAX_PARTIAL, out=slot, stream=stream)
         else:
-            mnmt.mnmt_qlinear_timed(x, E, c_out, None, mnmt.EPI_ARGMAX, e0, e1, out=slot, stream=stream)
+            mnmt.mnmt_qlinear_timed(x, E, c_out, None, mnmt.EPI_ARGMAX_PARTIAL, e0, e1, out=slot, stream=stream)
 
     return fn, alg_bytes
 

@@ -83,6 +83,11 @@ extern "C" {
  *                       z = acc * scale[n] and key() order-preserving on
  *                       floats: the arg max with the smallest index among
  *                       equal maxima, fused into the logits pass (M <= 8).
+ *   MNMT_EPI_ARGMAX_PARTIAL: Y uint64 [M, P], P = mnmt_argmax_partials(N): the
+ *                       same keys, one maximum per block of the logits kernel
+ *                       (plain stores, no zero-fill needed); the row's arg-max
+ *                       key is the largest of its P entries (M <= 2, K <= 512,
+ *                       as the decoder's batch-1 step writes it).
  * acc = sum_k X[m,k] W[n,k] in int32, converted to fp32 with round-to-nearest-even. */
 #define MNMT_EPI_I32 0
 #define MNMT_EPI_I8 1
@@ -91,6 +96,7 @@ extern "C" {
 #define MNMT_EPI_F32_RESID 4
 #define MNMT_EPI_LOGITS 5
 #define MNMT_EPI_ARGMAX 6
+#define MNMT_EPI_ARGMAX_PARTIAL 7
 
 typedef struct mnmt_model mnmt_model;
 typedef struct mnmt_session mnmt_session;
@@ -189,8 +195,13 @@ int mnmt_session_tensor(const mnmt_session* session, const char* name, void** d_
 int mnmt_qlinear(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias,
                  int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream);
 
+/* Number of partial keys per row that MNMT_EPI_ARGMAX_PARTIAL writes for N
+ * outputs (one per 128 outputs), or -1 for N < 1. */
+int mnmt_argmax_partials(int N);
+
 /* mnmt_qlinear with timing events (hipEvent_t, created with timing enabled,
- * or NULL).  On the fused arg-max path (MNMT_EPI_ARGMAX, M <= 2, K <= 512:
+ * or NULL).  On the fused arg-max path (MNMT_EPI_ARGMAX or
+ * MNMT_EPI_ARGMAX_PARTIAL, M <= 2, K <= 512:
  * the decoder's logits kernel on int8 rows) the two events take the kernel's
  * own start and end times (hipExtLaunchKernel), so their elapsed time is the
  * kernel's duration without launch gaps; on other paths they are recorded on

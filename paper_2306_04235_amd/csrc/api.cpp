@@ -75,18 +75,23 @@ extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const fl
                                   void* ev_start, void* ev_stop) {
   if (M < 0 || N < 1 || K < 64 || K % 64 || K > 8192)
     return set_error(MNMT_E_INVALID_ARG, "need M >= 0, N >= 1 and K a multiple of 64 in [64, 8192]");
-  if (epilogue < MNMT_EPI_I32 || epilogue > MNMT_EPI_ARGMAX) return set_error(MNMT_E_INVALID_ARG, "unknown epilogue");
+  if (epilogue < MNMT_EPI_I32 || epilogue > MNMT_EPI_ARGMAX_PARTIAL)
+    return set_error(MNMT_E_INVALID_ARG, "unknown epilogue");
+  if (epilogue == MNMT_EPI_ARGMAX_PARTIAL && !step_logits_fits(M == 0 ? 1 : M, K))
+    return set_error(MNMT_E_UNSUPPORTED, "the partial arg-max epilogue takes M <= 2 and K a multiple of 64 up to 512");
   if (epilogue == MNMT_EPI_ARGMAX && M > 8)
     return set_error(MNMT_E_UNSUPPORTED, "the fused arg-max epilogue takes at most 8 rows");
   if (M == 0) return MNMT_OK;
   const bool needs_scale = epilogue != MNMT_EPI_I32;
-  const bool needs_bias = epilogue != MNMT_EPI_I32 && epilogue != MNMT_EPI_LOGITS && epilogue != MNMT_EPI_ARGMAX;
+  const bool argmax = epilogue == MNMT_EPI_ARGMAX || epilogue == MNMT_EPI_ARGMAX_PARTIAL;
+  const bool needs_bias = epilogue != MNMT_EPI_I32 && epilogue != MNMT_EPI_LOGITS && !argmax;
   if (!d_X || !d_W || !d_Y || (needs_scale && !d_scale) || (needs_bias && !d_bias))
     return set_error(MNMT_E_INVALID_ARG, "null device pointer");
   if (reinterpret_cast<uintptr_t>(d_X) % 16 || reinterpret_cast<uintptr_t>(d_W) % 16)
     return set_error(MNMT_E_INVALID_ARG, "X and W must be 16-byte aligned");
-  if (epilogue == MNMT_EPI_ARGMAX && step_logits_fits(M, K)) {
-    // the decoder's fused logits + arg-max kernel on int8 rows, one slot per row
+  if (argmax && step_logits_fits(M, K)) {
+    // the decoder's fused logits + arg-max kernel on int8 rows: one slot per
+    // row (atomics), or one partial per block and row (plain stores)
     StepLogits g{};
     g.R = M;
     g.d = K;
@@ -94,7 +99,7 @@ extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const fl
     g.E = static_cast<const int8_t*>(d_W);
     g.c_out = d_scale;
     g.slots = static_cast<unsigned long long*>(d_Y);
-    g.nslots = 1;
+    g.nslots = epilogue == MNMT_EPI_ARGMAX ? 1 : step_logits_blocks(N);
     g.x_i8 = static_cast<const int8_t*>(d_X);
     const hipError_t h = launch_step_logits(StepIn{}, g, static_cast<hipStream_t>(stream),
                                             static_cast<hipEvent_t>(ev_start), static_cast<hipEvent_t>(ev_stop));
@@ -110,6 +115,8 @@ extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const fl
   h = ev_stop ? hipEventRecord(static_cast<hipEvent_t>(ev_stop), s) : hipSuccess;
   return h == hipSuccess ? MNMT_OK : hip_error(h, "qlinear stop event");
 }
+
+extern "C" int mnmt_argmax_partials(int N) { return N < 1 ? -1 : step_logits_blocks(N); }
 
 extern "C" int mnmt_fold_requant(float s_in, const float* s_w, const float* b, float s_out, int N, float* scale,
                                  float* bias) {

@@ -14,11 +14,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmnmt.so")
 
 OK, E_INVALID_ARG, E_BAD_MODEL, E_CAPACITY, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-EPI_I32, EPI_I8, EPI_I8_RELU, EPI_F32, EPI_F32_RESID, EPI_LOGITS, EPI_ARGMAX = range(7)
+EPI_I32, EPI_I8, EPI_I8_RELU, EPI_F32, EPI_F32_RESID, EPI_LOGITS, EPI_ARGMAX, EPI_ARGMAX_PARTIAL = range(8)
 
 EXPORTS = ("mnmt_model_bytes", "mnmt_model_load", "mnmt_model_get_info", "mnmt_model_free", "mnmt_session_bytes",
            "mnmt_session_create", "mnmt_session_free", "mnmt_encode", "mnmt_decode_step", "mnmt_translate",
-           "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed", "mnmt_fold_requant", "mnmt_debug_canon", "mnmt_status_str",
+           "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed", "mnmt_argmax_partials", "mnmt_fold_requant",
+           "mnmt_debug_canon", "mnmt_status_str",
            "mnmt_last_error")
 
 
@@ -71,6 +72,7 @@ def lib():
         L.mnmt_session_tensor.argtypes = [vp, C.c_char_p, C.POINTER(vp), C.POINTER(sz)]
         L.mnmt_qlinear.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp]
         L.mnmt_qlinear_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp, vp, vp]
+        L.mnmt_argmax_partials.argtypes = [i32]
         L.mnmt_fold_requant.argtypes = [f32, vp, vp, f32, i32, vp, vp]
         L.mnmt_debug_canon.argtypes = [i32, vp, i32, vp, vp]
         L.mnmt_status_str.argtypes = [i32]
@@ -124,6 +126,8 @@ def mnmt_qlinear(X, W, scale, bias, epilogue, gamma=1.0, out=None, stream=None):
     N = W.shape[0]
     if out is None and epilogue == EPI_ARGMAX:
         out = torch.zeros(M, dtype=torch.int64, device=X.device)  # packed (key, index) per row
+    elif out is None and epilogue == EPI_ARGMAX_PARTIAL:
+        out = torch.empty((M, argmax_partials(N)), dtype=torch.int64, device=X.device)
     elif out is None:
         dt = {EPI_I32: torch.int32, EPI_I8: torch.int8, EPI_I8_RELU: torch.int8}.get(epilogue, torch.float32)
         out = torch.empty((M, N), dtype=dt, device=X.device)
@@ -140,11 +144,20 @@ def mnmt_qlinear_timed(X, W, scale, bias, epilogue, ev_start, ev_stop, gamma=1.0
     M, K = X.shape
     N = W.shape[0]
     if out is None:
-        out = torch.zeros(M, dtype=torch.int64, device=X.device)
+        shape = (M, argmax_partials(N)) if epilogue == EPI_ARGMAX_PARTIAL else (M,)
+        out = torch.zeros(shape, dtype=torch.int64, device=X.device)
     _check(lib().mnmt_qlinear_timed(_ptr(X), _ptr(W), _ptr(scale), _ptr(bias), M, K, N, epilogue, float(gamma),
                                     _ptr(out), _stream(stream), C.c_void_p(ev_start.cuda_event),
                                     C.c_void_p(ev_stop.cuda_event)), "mnmt_qlinear_timed")
     return out
+
+
+def argmax_partials(N: int) -> int:
+    """Partial keys per row of an MNMT_EPI_ARGMAX_PARTIAL result for N outputs."""
+    p = lib().mnmt_argmax_partials(int(N))
+    if p < 1:
+        raise ValueError(f"no arg-max partials for N={N}")
+    return p
 
 
 def argmax_index(packed):

@@ -170,6 +170,16 @@ def test_qlinear_fused_argmax(torch_dev, M, K, N):
     keys = (got.astype(np.int64) >> 32) & 0xFFFFFFFF
     bits = np.where(keys & 0x80000000, keys & 0x7FFFFFFF, ~keys & 0xFFFFFFFF).astype(np.uint32)
     assert np.array_equal(bits.view(np.float32), ref_z.max(axis=1))
+    if M <= 2 and K <= 512:
+        # one key per block of 128 outputs: each is its block's arg-max key,
+        # and their maximum is the row's
+        part = _run(torch, dev, X, W, dq, None, mnmt.EPI_ARGMAX_PARTIAL)
+        P = mnmt.argmax_partials(N)
+        assert part.shape == (M, P)
+        assert np.array_equal(part.view(np.uint64).max(axis=1), got.view(np.uint64))
+        for p in sorted({0, P // 2, P - 1}):
+            blk = ref_z[:, 128 * p:128 * (p + 1)]
+            assert np.array_equal(mnmt.argmax_index(part[:, p]), 128 * p + np.argmax(blk, axis=1))
 
 
 def test_qlinear_timed_matches_and_times_the_kernel(torch_dev):
