@@ -301,6 +301,124 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
   }
 }
 
+// The same statistics and candidates with one 256-thread block per row, for
+// V <= kTopkMaxV: the maximum (order-free) over float4 loads, exp(z - max) of
+// every element computed by all threads into LDS, the canonical sum by wave 0
+// (lane l adds elements l, l + 64, ... in ascending order, then the
+// butterfly: the same order as the one-wave kernel), and the candidates by
+// per-thread sorted lists merged over the block.  The candidate order is
+// total (score, then index), so the split over threads does not change the
+// result.
+constexpr int kTopkMaxV = 32768;
+
+__device__ __forceinline__ unsigned long long block_max_u64(unsigned long long v, unsigned long long* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  v = wave_max_u64(v);
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  unsigned long long m = red[0];
+#pragma unroll
+  for (int w = 1; w < 4; ++w) m = red[w] > m ? red[w] : m;
+  __syncthreads();  // red is reused by the next call
+  return m;
+}
+
+template <int K>
+__global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict__ logits, BeamState st,
+                                                         const int* __restrict__ step) {
+  __shared__ float e_lds[kTopkMaxV];
+  __shared__ float redf[4];
+  __shared__ unsigned long long redk[4];
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = *step;
+  const int b = r / st.W, j = r % st.W;
+  if (st.done[b] || (t == 0 && j > 0)) return;
+  const int V = st.V;
+  const float* z = logits + (size_t)r * V;
+  const bool vec = (V & 3) == 0;  // rows are then 16-byte aligned
+  // 1. maximum
+  float mx = -FLT_MAX;
+  if (vec) {
+    const float4* z4 = reinterpret_cast<const float4*>(z);
+    for (int i = tid; i < V / 4; i += 256) {
+      const float4 q = z4[i];
+      mx = fmaxf(mx, fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w)));
+    }
+  } else {
+    for (int i = tid; i < V; i += 256) mx = fmaxf(mx, z[i]);
+  }
+  mx = wave_max(mx);
+  if (lane == 0) redf[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+  // 2. exp(z - max) of every element into LDS, then the canonical sum
+  if (vec) {
+    const float4* z4 = reinterpret_cast<const float4*>(z);
+    for (int i = tid; i < V / 4; i += 256) {
+      const float4 q = z4[i];
+      e_lds[4 * i] = canon_exp(q.x - mx);
+      e_lds[4 * i + 1] = canon_exp(q.y - mx);
+      e_lds[4 * i + 2] = canon_exp(q.z - mx);
+      e_lds[4 * i + 3] = canon_exp(q.w - mx);
+    }
+  } else {
+    for (int i = tid; i < V; i += 256) e_lds[i] = canon_exp(z[i] - mx);
+  }
+  __syncthreads();
+  if (wave == 0) {
+    float part = 0.0f;
+    for (int i = lane; i < V; i += 64) part = part + e_lds[i];
+    const float lse = mx + canon_log(wave_sum(part));
+    if (lane == 0) redf[0] = lse;
+  }
+  __syncthreads();
+  const float lse = redf[0];
+  const float sc = st.score[r];
+  // 3. per-thread sorted candidate lists, then K rounds of a block maximum
+  float ls[K];
+  int lv[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    ls[k] = -FLT_MAX;
+    lv[k] = INT_MAX;
+  }
+  for (int v = tid; v < V; v += 256) {
+    float c = sc + (z[v] - lse);
+    int cv = v;
+    if (!better(c, cv, ls[K - 1], lv[K - 1])) continue;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {  // insertion by swapping keeps the list sorted
+      if (better(c, cv, ls[k], lv[k])) {
+        const float tc = ls[k];
+        const int tv = lv[k];
+        ls[k] = c;
+        lv[k] = cv;
+        c = tc;
+        cv = tv;
+      }
+    }
+  }
+  for (int k = 0; k < K; ++k) {
+    const unsigned long long mine = lv[0] == INT_MAX ? 0ull : pack_argmax(ls[0], lv[0]);
+    const unsigned long long win = block_max_u64(mine, redk);
+    if (mine == win && win != 0ull) {
+#pragma unroll
+      for (int i = 0; i + 1 < K; ++i) {
+        ls[i] = ls[i + 1];
+        lv[i] = lv[i + 1];
+      }
+      ls[K - 1] = -FLT_MAX;
+      lv[K - 1] = INT_MAX;
+    }
+    if (tid == 0) {
+      const int v = win ? unpack_index(win) : 0;
+      st.cand_tok[(size_t)r * K + k] = v;
+      st.cand_score[(size_t)r * K + k] = win ? sc + (z[v] - lse) : -FLT_MAX;
+    }
+  }
+}
+
 // Per sentence: merge the W rows' candidates, finish EOS hypotheses, refill
 // the W live slots and advance the key/value history.  One wave per sentence.
 template <int W_MAX>
@@ -554,6 +672,22 @@ hipError_t launch_beam_reset(const BeamState& st, int* step, hipStream_t s) {
 
 hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int* step, hipStream_t s) {
   const int R = st.B * st.W;
+  if (st.V <= kTopkMaxV) {
+#define MNMT_TOPK(K) hipLaunchKernelGGL(k_beam_topk_block<K>, dim3(R), dim3(256), 0, s, logits, st, step)
+    switch (2 * st.W) {
+      case 2: MNMT_TOPK(2); break;
+      case 4: MNMT_TOPK(4); break;
+      case 6: MNMT_TOPK(6); break;
+      case 8: MNMT_TOPK(8); break;
+      case 10: MNMT_TOPK(10); break;
+      case 12: MNMT_TOPK(12); break;
+      case 14: MNMT_TOPK(14); break;
+      case 16: MNMT_TOPK(16); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef MNMT_TOPK
+    return hipGetLastError();
+  }
   switch (2 * st.W) {
     case 2: hipLaunchKernelGGL(k_beam_topk<2>, dim3(R), dim3(64), 0, s, logits, st, step); break;
     case 4: hipLaunchKernelGGL(k_beam_topk<4>, dim3(R), dim3(64), 0, s, logits, st, step); break;
