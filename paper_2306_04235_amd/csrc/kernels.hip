@@ -302,14 +302,23 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
 }
 
 // The same statistics and candidates with one 256-thread block per row, for
-// V <= kTopkMaxV: the maximum (order-free) over float4 loads, exp(z - max) of
-// every element computed by all threads into LDS, the canonical sum by wave 0
-// (lane l adds elements l, l + 64, ... in ascending order, then the
-// butterfly: the same order as the one-wave kernel), and the candidates by
-// per-thread sorted lists merged over the block.  The candidate order is
-// total (score, then index), so the split over threads does not change the
-// result.
+// V a multiple of 4 up to kTopkMaxV: the row is loaded once into registers
+// (every load in flight at once: 16 bytes per load, up to 32 per thread), the
+// maximum (order-free) taken from them, exp(z - max) of every element computed
+// by all threads into LDS, the canonical sum by wave 0 (lane l adds elements
+// l, l + 64, ... in ascending order, then the butterfly: the same order as the
+// one-wave kernel).  The candidates then come from a threshold: the score is
+// monotone in z, so each thread's best score is score + (its max z - lse), and
+// the K-th largest of these over the lanes of a wave has at least K scores of
+// the row at or above it; the largest such bound over the waves filters the
+// row down to a short list (about 4K entries on real logits), ranked by
+// pairwise comparison.  If ties push the list past kTopkCap the scores go to
+// LDS and per-thread sorted lists merged over the block take over.  The
+// candidate order is total (score, then index), so neither the filter nor the
+// split over threads changes the result.
 constexpr int kTopkMaxV = 32768;
+constexpr int kTopkV4 = kTopkMaxV / 4 / 256;  // float4 per thread
+constexpr int kTopkCap = 1024;                // entries of the filtered list
 
 __device__ __forceinline__ unsigned long long block_max_u64(unsigned long long v, unsigned long long* red) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -323,59 +332,12 @@ __device__ __forceinline__ unsigned long long block_max_u64(unsigned long long v
   return m;
 }
 
+// Per-thread sorted lists over the scores in LDS, merged over the block: the
+// path for rows whose filtered list overflows (large groups of equal scores).
 template <int K>
-__global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict__ logits, BeamState st,
-                                                         const int* __restrict__ step) {
-  __shared__ float e_lds[kTopkMaxV];
-  __shared__ float redf[4];
-  __shared__ unsigned long long redk[4];
-  const int r = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int t = *step;
-  const int b = r / st.W, j = r % st.W;
-  if (st.done[b] || (t == 0 && j > 0)) return;
-  const int V = st.V;
-  const float* z = logits + (size_t)r * V;
-  const bool vec = (V & 3) == 0;  // rows are then 16-byte aligned
-  // 1. maximum
-  float mx = -FLT_MAX;
-  if (vec) {
-    const float4* z4 = reinterpret_cast<const float4*>(z);
-    for (int i = tid; i < V / 4; i += 256) {
-      const float4 q = z4[i];
-      mx = fmaxf(mx, fmaxf(fmaxf(q.x, q.y), fmaxf(q.z, q.w)));
-    }
-  } else {
-    for (int i = tid; i < V; i += 256) mx = fmaxf(mx, z[i]);
-  }
-  mx = wave_max(mx);
-  if (lane == 0) redf[wave] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
-  // 2. exp(z - max) of every element into LDS, then the canonical sum
-  if (vec) {
-    const float4* z4 = reinterpret_cast<const float4*>(z);
-    for (int i = tid; i < V / 4; i += 256) {
-      const float4 q = z4[i];
-      e_lds[4 * i] = canon_exp(q.x - mx);
-      e_lds[4 * i + 1] = canon_exp(q.y - mx);
-      e_lds[4 * i + 2] = canon_exp(q.z - mx);
-      e_lds[4 * i + 3] = canon_exp(q.w - mx);
-    }
-  } else {
-    for (int i = tid; i < V; i += 256) e_lds[i] = canon_exp(z[i] - mx);
-  }
-  __syncthreads();
-  if (wave == 0) {
-    float part = 0.0f;
-    for (int i = lane; i < V; i += 64) part = part + e_lds[i];
-    const float lse = mx + canon_log(wave_sum(part));
-    if (lane == 0) redf[0] = lse;
-  }
-  __syncthreads();
-  const float lse = redf[0];
-  const float sc = st.score[r];
-  // 3. per-thread sorted candidate lists, then K rounds of a block maximum
+__device__ __forceinline__ void topk_lists(const float* c_lds, int V, unsigned long long* redk, int* cand_tok,
+                                        float* cand_score) {
+  const int tid = threadIdx.x;
   float ls[K];
   int lv[K];
 #pragma unroll
@@ -384,16 +346,16 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
     lv[k] = INT_MAX;
   }
   for (int v = tid; v < V; v += 256) {
-    float c = sc + (z[v] - lse);
+    float c = c_lds[v];
     int cv = v;
     if (!better(c, cv, ls[K - 1], lv[K - 1])) continue;
 #pragma unroll
-    for (int k = 0; k < K; ++k) {  // insertion by swapping keeps the list sorted
-      if (better(c, cv, ls[k], lv[k])) {
-        const float tc = ls[k];
-        const int tv = lv[k];
-        ls[k] = c;
-        lv[k] = cv;
+    for (int m = 0; m < K; ++m) {  // insertion by swapping keeps the list sorted
+      if (better(c, cv, ls[m], lv[m])) {
+        const float tc = ls[m];
+        const int tv = lv[m];
+        ls[m] = c;
+        lv[m] = cv;
         c = tc;
         cv = tv;
       }
@@ -402,7 +364,9 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
   for (int k = 0; k < K; ++k) {
     const unsigned long long mine = lv[0] == INT_MAX ? 0ull : pack_argmax(ls[0], lv[0]);
     const unsigned long long win = block_max_u64(mine, redk);
-    if (mine == win && win != 0ull) {
+    if (mine == win && win != 0ull) {  // the owner of the winner records and drops it
+      cand_tok[k] = lv[0];
+      cand_score[k] = ls[0];
 #pragma unroll
       for (int i = 0; i + 1 < K; ++i) {
         ls[i] = ls[i + 1];
@@ -411,12 +375,143 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
       ls[K - 1] = -FLT_MAX;
       lv[K - 1] = INT_MAX;
     }
-    if (tid == 0) {
-      const int v = win ? unpack_index(win) : 0;
-      st.cand_tok[(size_t)r * K + k] = v;
-      st.cand_score[(size_t)r * K + k] = win ? sc + (z[v] - lse) : -FLT_MAX;
+    if (win == 0ull && tid == 0) {
+      cand_tok[k] = 0;
+      cand_score[k] = -FLT_MAX;
     }
   }
+}
+
+template <int K>
+__global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict__ logits, BeamState st,
+                                                         const int* __restrict__ step) {
+  __shared__ float e_lds[kTopkMaxV];
+  __shared__ float list_c[kTopkCap];
+  __shared__ int list_v[kTopkCap];
+  __shared__ float redf[4];
+  __shared__ unsigned long long redk[4];
+  __shared__ int n_list;
+  const int r = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int t = *step;
+  const int b = r / st.W, j = r % st.W;
+  if (st.done[b] || (t == 0 && j > 0)) return;
+  const int V = st.V, n4 = V / 4;
+  const float4* z4 = reinterpret_cast<const float4*>(logits + (size_t)r * V);
+  int* cand_tok = st.cand_tok + (size_t)r * K;
+  float* cand_score = st.cand_score + (size_t)r * K;
+  if (tid == 0) n_list = 0;
+  // 1. the row in registers (element 4 (tid + 256 k) + q), the thread's
+  //    maximum and the row's
+  float4 zr[kTopkV4];
+#pragma unroll
+  for (int k = 0; k < kTopkV4; ++k) zr[k] = z4[min(tid + 256 * k, n4 - 1)];
+  float tmx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < kTopkV4; ++k)
+    if (tid + 256 * k < n4) tmx = fmaxf(tmx, fmaxf(fmaxf(zr[k].x, zr[k].y), fmaxf(zr[k].z, zr[k].w)));
+  float mx = wave_max(fmaxf(tmx, -FLT_MAX));
+  if (lane == 0) redf[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+  // 2. exp(z - max) of every element into LDS, then the canonical sum
+#pragma unroll
+  for (int k = 0; k < kTopkV4; ++k) {
+    const int i = tid + 256 * k;
+    if (i < n4) {
+      e_lds[4 * i] = canon_exp(zr[k].x - mx);
+      e_lds[4 * i + 1] = canon_exp(zr[k].y - mx);
+      e_lds[4 * i + 2] = canon_exp(zr[k].z - mx);
+      e_lds[4 * i + 3] = canon_exp(zr[k].w - mx);
+    }
+  }
+  __syncthreads();
+  if (wave == 0) {
+    // lane l: elements l, l + 64, ... in ascending order (eight reads in
+    // flight, the adds in order)
+    float part = 0.0f;
+    int i = lane;
+    for (; i + 7 * 64 < V; i += 8 * 64) {
+      float e[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) e[u] = e_lds[i + 64 * u];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) part = part + e[u];
+    }
+    for (; i < V; i += 64) part = part + e_lds[i];
+    const float lse = mx + canon_log(wave_sum(part));
+    if (lane == 0) redf[0] = lse;
+  }
+  __syncthreads();
+  const float lse = redf[0];
+  const float sc = st.score[r];
+  // 3. the bound: the K-th largest thread-best score of each wave (scores
+  //    below -FLT_MAX never qualify), the largest over the waves
+  const float cm = sc + (tmx - lse);
+  float v = cm >= -FLT_MAX ? cm : -INFINITY;
+  float kth = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    kth = wave_max(v);
+    const unsigned long long hold = __ballot(v == kth);
+    if (lane == __ffsll((long long)hold) - 1) v = -INFINITY;  // drop one holder
+  }
+  __syncthreads();  // every read of redf[0] is done
+  if (lane == 0) redf[wave] = fmaxf(kth, -FLT_MAX);
+  __syncthreads();
+  const float tau = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+  // 4. the filtered list: every score at or above the bound
+#pragma unroll
+  for (int k = 0; k < kTopkV4; ++k) {
+    const int i = tid + 256 * k;
+    if (i < n4) {
+      const float c4[4] = {sc + (zr[k].x - lse), sc + (zr[k].y - lse), sc + (zr[k].z - lse),
+                           sc + (zr[k].w - lse)};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (c4[q] >= tau) {
+          const int pos = atomicAdd(&n_list, 1);
+          if (pos < kTopkCap) {
+            list_c[pos] = c4[q];
+            list_v[pos] = 4 * i + q;
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int n = n_list;
+  if (n <= kTopkCap) {
+    // 5. rank = the number of list entries that beat the entry
+    for (int i = tid; i < n; i += 256) {
+      const float ci = list_c[i];
+      const int vi = list_v[i];
+      int rank = 0;
+      for (int o = 0; o < n; ++o) rank += better(list_c[o], list_v[o], ci, vi) ? 1 : 0;
+      if (rank < K) {
+        cand_tok[rank] = vi;
+        cand_score[rank] = ci;
+      }
+    }
+    for (int k = n + tid; k < K; k += 256) {  // fewer than K scores qualify
+      cand_tok[k] = 0;
+      cand_score[k] = -FLT_MAX;
+    }
+    return;
+  }
+  // 5'. the overflow path: all scores into LDS, sorted lists, block merge
+#pragma unroll
+  for (int k = 0; k < kTopkV4; ++k) {
+    const int i = tid + 256 * k;
+    if (i < n4) {
+      e_lds[4 * i] = sc + (zr[k].x - lse);
+      e_lds[4 * i + 1] = sc + (zr[k].y - lse);
+      e_lds[4 * i + 2] = sc + (zr[k].z - lse);
+      e_lds[4 * i + 3] = sc + (zr[k].w - lse);
+    }
+  }
+  __syncthreads();
+  topk_lists<K>(e_lds, V, redk, cand_tok, cand_score);
 }
 
 // Per sentence: merge the W rows' candidates, finish EOS hypotheses, refill
@@ -672,7 +767,7 @@ hipError_t launch_beam_reset(const BeamState& st, int* step, hipStream_t s) {
 
 hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int* step, hipStream_t s) {
   const int R = st.B * st.W;
-  if (st.V <= kTopkMaxV) {
+  if (st.V <= kTopkMaxV && st.V % 4 == 0) {
 #define MNMT_TOPK(K) hipLaunchKernelGGL(k_beam_topk_block<K>, dim3(R), dim3(256), 0, s, logits, st, step)
     switch (2 * st.W) {
       case 2: MNMT_TOPK(2); break;

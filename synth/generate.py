@@ -50,6 +50,7 @@ class ModelConfig:
     emb_std: float = WEIGHT_STD
     gamma_range: tuple = (0.5, 1.5)
     weight_std: float = WEIGHT_STD
+    emb_distinct: int = 0  # > 0: embedding row v repeats drawn row v mod emb_distinct (groups of equal logits)
 
 
 # The model shapes of the five workloads.
@@ -113,7 +114,9 @@ def build_model(cfg: ModelConfig) -> bytes:
     def gamma(name):
         t[name] = f32([rng.uniform(*cfg.gamma_range) if cfg.random_gamma else 1.0])
 
-    e = rng.normal(0.0, cfg.emb_std, size=(cfg.vocab, d))
+    e = rng.normal(0.0, cfg.emb_std, size=(cfg.emb_distinct or cfg.vocab, d))
+    if cfg.emb_distinct:
+        e = e[np.arange(cfg.vocab) % cfg.emb_distinct]
     t["emb.w"], t["emb.s"] = _quantize_rows(e)
     t["pe"] = positional_table(cfg.max_pos, d)
     s_enc = _act_scale(rng, 1.0)

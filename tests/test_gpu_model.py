@@ -194,12 +194,31 @@ def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None):
     sess.close()
 
 
+ODD_VOCAB = G.ModelConfig("odd-vocab", 64, 4, 128, 1, 1, 501, ln_post=0, seed=79, random_gamma=True, weight_std=0.1)
+
+
 def test_small_models_beam(torch_dev):
     torch, dev = torch_dev
-    for cfg in (SMALL_PRE, SMALL_POST, DIVERSE):
+    for cfg in (SMALL_PRE, SMALL_POST, DIVERSE, ODD_VOCAB):  # odd vocabulary: the one-wave-per-row top-k
         src, lens = G.make_sources(cfg.vocab, 4, [5, 1, 9, 9], seed=31, s_max=9)
-        for W in (2, 4):
+        for W in (2, 4, 6):
             _beam_check(torch, dev, cfg, src, lens, W, 8, 0.6)
+
+
+TIES3 = G.ModelConfig("ties-3", 64, 4, 128, 1, 1, 3000, ln_post=0, seed=86, emb_distinct=3)
+TIES1 = G.ModelConfig("ties-1", 64, 4, 128, 1, 1, 2048, ln_post=0, seed=87, emb_distinct=1)
+
+
+def test_beam_tied_logits(torch_dev):
+    """Embedding rows repeated so the logits come in groups of equal values:
+    1000 equal best scores per row (the filtered top-k list near its 1024
+    capacity) and 2048 (every score equal: the overflow path).  Ties go to the
+    lower flat index on both sides."""
+    torch, dev = torch_dev
+    for cfg in (TIES3, TIES1):
+        src, lens = G.make_sources(cfg.vocab, 3, [6, 2, 7], seed=33, s_max=7)
+        for W in (2, 4, 8):
+            _beam_check(torch, dev, cfg, src, lens, W, 6, 0.6)
 
 
 def test_mobile_beam_workload_sampled(torch_dev):
