@@ -53,6 +53,20 @@ ROOF_KERNEL = "k_step_logits<256, true>"
 COPY_BYTES = 256 << 20
 
 
+def _warm(torch, fn, seconds=0.05):
+    """Untimed calls for about ``seconds`` of wall time (at least 3): the GPU's
+    clocks settle under sustained load (a 60 us GEMM measured right after an
+    idle phase runs up to 20% slower)."""
+    t0 = time.perf_counter()
+    n = 0
+    while n < 3 or time.perf_counter() - t0 < seconds:
+        fn()
+        n += 1
+        if n % 16 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+
+
 def _kernel_events_ms(torch, fn_ev, reps, stream):
     """Mean kernel duration (ms) over reps back-to-back launches of
     fn_ev(e0, e1), whose events take the kernel's own start and end times."""
@@ -196,6 +210,107 @@ def cpu_baseline(workload, min_seconds=10.0):
                       f"{el:.1f} s, single-threaded scalar C"}
 
 
+def qlinear_sweep(torch, mnmt, G, dev, reps=100):
+    """The quantized-linear sweep: X int8 [M, K] x W int8 [N, K], int32
+    accumulation, folded per-channel requant to int8, for M in {1, 4, 64, 256,
+    4096} and (K, N) in {(256, 1024), (1024, 256), (512, 2048), (256, 32000)}.
+    Each shape: 3 untimed launches, then ``reps`` back to back between two
+    events (launch gaps included).  Roofline per shape: the larger of the i8
+    matrix-core time 2MKN / 5.0 POP/s and the memory time of its algorithmic
+    bytes (X, W, 8 B of constants per column, the int8 output) at 8 TB/s."""
+    stream = torch.cuda.current_stream()
+    mark = torch.empty(1, device=dev)
+    rows = []
+    for K, N in G.SWEEP_KN:
+        for M in G.SWEEP_M:
+            X, W, mult, bias = (torch.from_numpy(a).to(dev) for a in G.sweep_case(M, K, N))
+            mark.fill_(float(M))  # a fill kernel separates the shapes in a kernel trace
+            Y = torch.empty((M, N), dtype=torch.int8, device=dev)
+            g = lambda: mnmt.mnmt_qlinear(X, W, mult, bias, mnmt.EPI_I8, out=Y, stream=stream)  # noqa: E731
+            _warm(torch, g)
+            ms = _events_ms(torch, g, reps, stream)
+            ops = 2.0 * M * K * N
+            nbytes = M * K + N * K + 8 * N + M * N
+            t_mfma = ops / (I8_PEAK_TOPS * 1e12)
+            t_mem = nbytes / (HBM_PEAK_GBS * 1e9)
+            t_roof = _sweep_roofline_us(M, K, N) * 1e-6
+            rows.append({"M": M, "K": K, "N": N, "us": round(ms * 1e3, 3), "tops": round(ops / (ms * 1e-3) / 1e12, 2),
+                         "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "bound": "mfma" if t_mfma >= t_mem else "hbm",
+                         "roof_us": round(t_roof * 1e6, 3), "frac": round(t_roof / (ms * 1e-3), 4)})
+            print(f"sweep M={M} K={K} N={N}: {ms * 1e3:.2f} us, roofline {rows[-1]['bound']} "
+                  f"{t_roof * 1e6:.2f} us, frac {rows[-1]['frac']:.3f}", file=sys.stderr, flush=True)
+    return rows
+
+
+def _sweep_roofline_us(M, K, N):
+    ops = 2.0 * M * K * N
+    nbytes = M * K + N * K + 8 * N + M * N
+    return max(ops / (I8_PEAK_TOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e6
+
+
+def sweep_trace_summary(trace_csv, command):
+    """Per-shape kernel durations of ``--sweep`` from a rocprofv3 kernel trace
+    (the fill kernel before each shape splits the dispatches), as markdown."""
+    import csv
+
+    with open(trace_csv) as f:
+        recs = sorted(csv.DictReader(f), key=lambda r: int(r["Start_Timestamp"]))
+    groups = []
+    for r in recs:
+        name = r["Kernel_Name"]
+        if "Fill" in name or "fill" in name:
+            groups.append([])
+        elif groups and "mnmt::" in name:
+            groups[-1].append((name, (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3))
+    from synth import generate as G
+
+    shapes = [(M, K, N) for K, N in G.SWEEP_KN for M in G.SWEEP_M]
+    if len(groups) != len(shapes):
+        raise SystemExit(f"expected {len(shapes)} shape groups, found {len(groups)}")
+    out = ["| M | K | N | kernel(s) | launches | mean µs | roofline µs | frac |", "|---:|---:|---:|---|---:|---:|---:|---:|"]
+    for (M, K, N), g in zip(shapes, groups):
+        names = sorted({n.replace("void ", "").replace("mnmt::(anonymous namespace)::", "").split("(")[0] for n, _ in g})
+        timed = g[-100:]  # one kernel per call: the timed launches are the last 100
+        calls = len(timed)
+        mean_us = sum(d for _, d in timed) / max(1, calls)
+        roof = _sweep_roofline_us(M, K, N)
+        out.append(f"| {M} | {K} | {N} | `{'`, `'.join(names)}` | {calls} | {mean_us:.2f} | {roof:.2f} | {roof / mean_us:.3f} |")
+    print(f"Command: `{command}`\n" if command else "", end="")
+    print("\n".join(out))
+
+
+def beam_throughput(torch, mnmt, G, dev, names=("mobile_beam", "base_beam"), reps=3):
+    """The two batched beam-search workloads (mobile: 64 sentences, base: 128;
+    beam 4, length penalty 0.6), each translation one captured graph, inputs
+    resident on the device: one untimed translation, then ``reps`` timed."""
+    res = {}
+    for name in names:
+        w = G.WORKLOADS[name]
+        m = mnmt.Model(G.build_model(w.model))
+        src, lens = G.workload_inputs(w)
+        ts, tl = torch.from_numpy(src).to(dev), torch.from_numpy(lens).to(dev)
+        sess = mnmt.Session(m, w.batch, w.s_max, w.steps, w.beam)
+        outs = (torch.empty((w.batch, w.steps), dtype=torch.int32, device=dev),
+                torch.empty(w.batch, dtype=torch.int32, device=dev),
+                torch.empty(w.batch, dtype=torch.float32, device=dev))
+        run = lambda: sess.translate(ts, tl, beam=w.beam, max_steps=w.steps, alpha=w.alpha,  # noqa: E731
+                                     use_graph=True, out=outs)
+        run()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            run()
+        torch.cuda.synchronize()
+        el = (time.perf_counter() - t0) / reps
+        toks = int(outs[1].sum().item())
+        res[name] = {"workload": w.name, "ms_per_batch": round(el * 1e3, 3), "sentences_per_s": round(w.batch / el, 1),
+                     "output_tokens_per_s": round(toks / el, 1), "batch": w.batch, "beam": w.beam,
+                     "max_steps": w.steps}
+        sess.close()
+        m.close()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -203,10 +318,18 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paper-shapes", action="store_true", help="skip the paper-shape side measurements")
+    ap.add_argument("--no-beam", action="store_true", help="skip the batched beam-search side measurements")
+    ap.add_argument("--beam-only", nargs="?", const="all", choices=("all", "mobile_beam", "base_beam"),
+                    help="only the batched beam-search measurements (for profiling), optionally one workload")
+    ap.add_argument("--sweep", action="store_true", help="only the quantized-linear sweep (20 shapes, I8 epilogue)")
     ap.add_argument("--counters", action="store_true", help="only the roofline kernel and the copy (for --pmc)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--ingest-command", default="")
+    ap.add_argument("--sweep-trace", metavar="KERNEL_TRACE_CSV", help="summarize a kernel trace of --sweep")
     args = ap.parse_args()
+    if args.sweep_trace:
+        sweep_trace_summary(args.sweep_trace, args.ingest_command)
+        return
     if args.ingest_counters:
         ingest_counters(*args.ingest_counters, args.ingest_command)
         return
@@ -226,6 +349,13 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    if args.sweep:
+        print(json.dumps({"qlinear_sweep": qlinear_sweep(torch, mnmt, G, dev)}), flush=True)
+        return
+    if args.beam_only:
+        names = ("mobile_beam", "base_beam") if args.beam_only == "all" else (args.beam_only,)
+        print(json.dumps({"beam_throughput": beam_throughput(torch, mnmt, G, dev, names)}), flush=True)
+        return
     w = G.WORKLOADS["mobile"]
     blob = G.build_model(w.model)
     model = mnmt.Model(blob)
@@ -272,8 +402,7 @@ def main():
     bi = torch.zeros(N, dtype=torch.float32, device=dev)
     Yg = torch.empty((M, N), dtype=torch.int8, device=dev)
     g = lambda: mnmt.mnmt_qlinear(Xg, Wg, sc, bi, mnmt.EPI_I8, out=Yg, stream=stream)  # noqa: E731
-    for _ in range(3):
-        g()
+    _warm(torch, g)
     gemm_ms = _events_ms(torch, g, 20, stream)
     tops = 2.0 * M * K * N / (gemm_ms * 1e-3) / 1e12
     qgemm = {"shape": [M, K, N], "epilogue": "i8 requant", "tops": round(tops, 1), "peak": I8_PEAK_TOPS,
@@ -323,6 +452,8 @@ def main():
         "qgemm": qgemm,
         "paper_shapes_b1_greedy30": paper,
     }
+    if not args.no_beam:
+        line["beam_throughput"] = beam_throughput(torch, mnmt, G, dev)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(line), flush=True)
