@@ -441,6 +441,231 @@ hipError_t launch_persistent(const int8_t* X, int ldx, const int8_t* W, const fl
 // LDS reads per MFMA that fit two waves per SIMD), 128-byte K chunks.
 constexpr int kPBN = 256, kPBM = 128, kPKC = 128;
 
+// ---------------------------------------------------------------------------
+// Weight-stationary kernel for K = 256 and long runs of rows (the 4096-row
+// sweep shapes, large batched logits).  A 512-thread block owns 256 output
+// columns: wave w keeps the int8 weights of its 64 columns (w mod 4) for the
+// whole K in registers (16 KB per wave, 64 VGPRs), and its per-column
+// constants too, and walks a range of 64-row steps of X.  Waves w and w + 4
+// take rows 0-31 and 32-63 of each step, so all eight waves pass the same
+// barriers and finish together (with two independent blocks per CU the
+// hardware's preference for older waves let one block finish well before the
+// other).  Each step's X rows (16 KB) go through LDS, double buffered; they
+// are loaded into registers at the start of the previous step and stored to
+// LDS at its end.  The LDS then feeds only the X operand: 0.5 KB of LDS
+// reads per 32x32x32 MFMA instead of 0.75 KB with both operands staged.
+//
+// The epilogue of step t - 1 runs interleaved with the MFMAs of step t (two
+// accumulator sets), so its VALU work overlaps the matrix cores.  For a
+// uniform loop body the first step also runs an epilogue, of zeros, over its
+// own rows, which the real epilogue rewrites one step later (same wave, same
+// addresses, program order): every step then issues the same memory
+// operations, and each wait for the X prefetch counts exactly the output
+// stores issued after it (loads and stores share one in-order counter), so
+// no wait covers stores of the current step.
+constexpr int kWsK = 256, kWsRows = 64, kWsMinSteps = 16;
+
+template <int EPI>
+struct WsConst {
+  float sc[2][16], bi[2][16];  // [fragment][4 g + t]: column 32 f + 8 g + 4 h + t of the wave
+};
+
+// Group G (4 outputs) of fragment F: int8 outputs are packed into w4[G] and
+// written after group 3 (one 16-byte store of 16 consecutive columns per
+// lane, after two lane swaps); wider outputs are written per group.
+template <int EPI, int F, int G>
+__device__ __forceinline__ void ws_epi_group(const EpiArgs& e, const v16i (&P)[2], const WsConst<EPI>& c,
+                                             uint32_t (&w4)[4], int m, int nw, int h) {
+  constexpr bool INT8_OUT = EPI == MNMT_EPI_I8 || EPI == MNMT_EPI_I8_RELU;
+  if (INT8_OUT) {
+    uint32_t q[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) q[t] = code_bits(epi_value<EPI>(P[F][4 * G + t], c.sc[F][4 * G + t], c.bi[F][4 * G + t]));
+    w4[G] = pack4(q[0], q[1], q[2], q[3]);
+    if (G == 3) {
+      const auto s02 = __builtin_amdgcn_permlane32_swap(w4[0], w4[2], false, false);
+      const auto s13 = __builtin_amdgcn_permlane32_swap(w4[1], w4[3], false, false);
+      int8_t* y = (int8_t*)e.out + (size_t)m * e.ldo + nw + 32 * F + 16 * h;
+      *(v4i*)y = v4i{(int)s02[0], (int)s02[1], (int)s13[0], (int)s13[1]};
+    }
+  } else if (EPI == MNMT_EPI_I32) {
+    int* y = (int*)e.out + (size_t)m * e.ldo + nw + 32 * F + 8 * G + 4 * h;
+    *(v4i*)y = v4i{P[F][4 * G], P[F][4 * G + 1], P[F][4 * G + 2], P[F][4 * G + 3]};
+  } else {
+    static_assert(EPI != MNMT_EPI_F32_RESID, "the zero epilogue of the first step would overwrite the residual");
+    float* y = (float*)e.out + (size_t)m * e.ldo + nw + 32 * F + 8 * G + 4 * h;
+    v4f v;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) v[t] = epi_value<EPI>(P[F][4 * G + t], c.sc[F][4 * G + t], c.bi[F][4 * G + t]);
+    *(v4f*)y = v;
+  }
+}
+
+// The 8 groups (2 fragments x 4) of the epilogue spread over the K steps:
+// step KK takes groups [8 KK / NKK, 8 (KK + 1) / NKK).
+template <int EPI, int KK, int NKK>
+__device__ __forceinline__ void ws_epi_part(const EpiArgs& e, const v16i (&P)[2], const WsConst<EPI>& c,
+                                            uint32_t (&w4)[4], int m, int nw, int h) {
+#pragma unroll
+  for (int q = 8 * KK / NKK; q < 8 * (KK + 1) / NKK; ++q) {
+    if (q == 0) ws_epi_group<EPI, 0, 0>(e, P, c, w4, m, nw, h);
+    if (q == 1) ws_epi_group<EPI, 0, 1>(e, P, c, w4, m, nw, h);
+    if (q == 2) ws_epi_group<EPI, 0, 2>(e, P, c, w4, m, nw, h);
+    if (q == 3) ws_epi_group<EPI, 0, 3>(e, P, c, w4, m, nw, h);
+    if (q == 4) ws_epi_group<EPI, 1, 0>(e, P, c, w4, m, nw, h);
+    if (q == 5) ws_epi_group<EPI, 1, 1>(e, P, c, w4, m, nw, h);
+    if (q == 6) ws_epi_group<EPI, 1, 2>(e, P, c, w4, m, nw, h);
+    if (q == 7) ws_epi_group<EPI, 1, 3>(e, P, c, w4, m, nw, h);
+  }
+}
+
+// K step KK onward: two MFMAs into C (the wave's two 32-column fragments
+// against one 32-row X fragment from LDS), then part KK of P's epilogue.
+template <int EPI, int NKK, int KK = 0>
+__device__ __forceinline__ void ws_steps(const int8_t* xs, const v4i (&wr)[2][NKK], v16i (&C)[2], const EpiArgs& e,
+                                         const v16i (&P)[2], const WsConst<EPI>& c, uint32_t (&w4)[4], int m, int nw,
+                                         int h) {
+  if constexpr (KK < NKK) {
+    const v4i bx = *(const v4i*)(xs + 32 * KK);
+    C[0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wr[0][KK], bx, C[0], 0, 0, 0);
+    C[1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wr[1][KK], bx, C[1], 0, 0, 0);
+    ws_epi_part<EPI, KK, NKK>(e, P, c, w4, m, nw, h);
+    ws_steps<EPI, NKK, KK + 1>(xs, wr, C, e, P, c, w4, m, nw, h);
+  }
+}
+
+template <int EPI, int NKK, int KK = 0>
+__device__ __forceinline__ void ws_epilogue(const EpiArgs& e, const v16i (&P)[2], const WsConst<EPI>& c,
+                                            uint32_t (&w4)[4], int m, int nw, int h) {
+  if constexpr (KK < NKK) {
+    ws_epi_part<EPI, KK, NKK>(e, P, c, w4, m, nw, h);
+    ws_epilogue<EPI, NKK, KK + 1>(e, P, c, w4, m, nw, h);
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512, 1) void k_gemm_ws(const int8_t* X, int ldx, const int8_t* W, int M,
+                                                    const float* scale, const float* bias, EpiArgs e, int ncol,
+                                                    int steps_per_block) {
+  constexpr int KB = kWsK, TM = kWsRows, NKK = KB / 32, XROW = KB + 16;  // padded LDS row
+  constexpr int CPR = KB / 16, RPS = 512 / CPR, LX = TM / RPS;  // X loads: 16 bytes, rows per pass, passes
+  static_assert(TM % RPS == 0 && LX >= 1, "whole X loads");
+  __shared__ __attribute__((aligned(16))) int8_t Xs[2][TM * XROW];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5;
+  const int cb = blockIdx.x % ncol, ms = blockIdx.x / ncol;
+  const int nw = cb * 256 + 64 * (wave & 3);       // the wave's first column
+  const int row = (lane & 31) + 32 * (wave >> 2);  // the lane's row within a step
+  const int t0 = ms * steps_per_block, t1 = min(t0 + steps_per_block, M / TM);
+  if (t0 >= t1) return;
+  const int lrow = tid / CPR, lcol = 16 * (tid % CPR);  // this thread's X loads: rows lrow + RPS i
+
+  v4i px[LX];
+  auto xload = [&](int t) {
+#pragma unroll
+    for (int i = 0; i < LX; ++i) px[i] = *(const v4i*)(X + (size_t)(t * TM + lrow + RPS * i) * ldx + lcol);
+  };
+  auto xstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < LX; ++i) *(v4i*)(&Xs[buf][(lrow + RPS * i) * XROW + lcol]) = px[i];
+  };
+  xload(t0);
+  v4i wr[2][NKK];
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+      wr[f][kk] = *(const v4i*)(W + (size_t)(nw + 32 * f + (lane & 31)) * KB + 32 * kk + 16 * h);
+  WsConst<EPI> c;
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int n = nw + 32 * f + 8 * g + 4 * h;
+      const v4f s4 = EPI == MNMT_EPI_I32 ? v4f{} : *(const v4f*)(scale + n);
+      const v4f b4 = (EPI == MNMT_EPI_I32 || EPI == MNMT_EPI_LOGITS) ? v4f{} : *(const v4f*)(bias + n);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        c.sc[f][4 * g + t] = s4[t];
+        c.bi[f][4 * g + t] = b4[t];
+      }
+    }
+  xstore(0);
+  // the weights and constants arrive here, before the loop: a wait for them
+  // inside it would be counted from the loop entry on every step
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) asm volatile("" : "+v"(wr[f][kk]));
+#pragma unroll
+    for (int q = 0; q < 16; ++q) asm volatile("" : "+v"(c.sc[f][q]), "+v"(c.bi[f][q]));
+  }
+  lds_barrier();
+
+  uint32_t w4[4];
+  v16i A[2] = {v16i{}, v16i{}}, B[2] = {v16i{}, v16i{}};
+  const int xoff = row * XROW + 16 * h;
+  int t = t0, buf = 0;
+  for (;;) {
+    // step t into A, the epilogue of step t - 1 from B (zeros over step t0's
+    // rows the first time)
+    xload(min(t + 1, t1 - 1));
+    asm volatile("" ::: "memory");  // keeps the prefetch ahead of the step
+    A[0] = A[1] = v16i{};
+    ws_steps<EPI, NKK>(&Xs[buf][xoff], wr, A, e, B, c, w4, max(t - 1, t0) * TM + row, nw, h);
+    xstore(buf ^ 1);
+    lds_barrier();
+    if (t + 1 >= t1) {
+      ws_epilogue<EPI, NKK>(e, A, c, w4, t * TM + row, nw, h);
+      break;
+    }
+    ++t;
+    buf ^= 1;
+    // step t into B, the epilogue of step t - 1 from A
+    xload(min(t + 1, t1 - 1));
+    asm volatile("" ::: "memory");
+    B[0] = B[1] = v16i{};
+    ws_steps<EPI, NKK>(&Xs[buf][xoff], wr, B, e, A, c, w4, (t - 1) * TM + row, nw, h);
+    xstore(buf ^ 1);
+    lds_barrier();
+    if (t + 1 >= t1) {
+      ws_epilogue<EPI, NKK>(e, B, c, w4, t * TM + row, nw, h);
+      break;
+    }
+    ++t;
+    buf ^= 1;
+  }
+}
+
+// Blocks for the weight-stationary kernel: one per CU, the column blocks
+// times a split of the row steps.
+struct WsPlan {
+  int ncol, steps_per_block, nblk;
+};
+__host__ inline WsPlan ws_plan(int M, int N) {
+  const int ncol = N / 256, steps = M / kWsRows;
+  const int split = max(1, min(steps, 256 / max(1, ncol)));
+  const int spb = (steps + split - 1) / split;
+  return WsPlan{ncol, spb, ncol * ((steps + spb - 1) / spb)};
+}
+
+hipError_t launch_ws(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
+                     const EpiArgs& e, const WsPlan& p, hipStream_t s) {
+#define MNMT_GEMM(EPI)                                                                                          \
+  hipLaunchKernelGGL((k_gemm_ws<EPI>), dim3(p.nblk), dim3(512), 0, s, X, ldx, W, M, scale, bias, e, p.ncol, \
+                     p.steps_per_block)
+  switch (e.kind) {
+    case MNMT_EPI_I32: MNMT_GEMM(MNMT_EPI_I32); break;
+    case MNMT_EPI_I8: MNMT_GEMM(MNMT_EPI_I8); break;
+    case MNMT_EPI_I8_RELU: MNMT_GEMM(MNMT_EPI_I8_RELU); break;
+    case MNMT_EPI_F32: MNMT_GEMM(MNMT_EPI_F32); break;
+    case MNMT_EPI_LOGITS: MNMT_GEMM(MNMT_EPI_LOGITS); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef MNMT_GEMM
+  return hipGetLastError();
+}
+
 }  // namespace
 
 // The persistent kernel for whole tiles (16-byte aligned rows), K a power-of-two
@@ -454,6 +679,12 @@ hipError_t launch_gemm(const int8_t* X, int ldx, const int8_t* W, const float* s
   auto tiles = [&](int bn, int bm) { return (long)((N + bn - 1) / bn) * ((M + bm - 1) / bm); };
   const bool int8_out = e.kind == MNMT_EPI_I8 || e.kind == MNMT_EPI_I8_RELU;
   const bool aligned = (reinterpret_cast<uintptr_t>(e.out) & 15) == 0 && e.ldo % (int8_out ? 16 : 4) == 0;
+  const bool ops_aligned = ldx % 16 == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0 &&
+                           (reinterpret_cast<uintptr_t>(W) & 15) == 0;
+  if (aligned && ops_aligned && K == kWsK && N % 256 == 0 && M % kWsRows == 0 && e.kind != MNMT_EPI_F32_RESID) {
+    const WsPlan p = ws_plan(M, N);
+    if (p.steps_per_block >= kWsMinSteps) return launch_ws(X, ldx, W, scale, bias, M, e, p, s);
+  }
   if (aligned && M % kPBM == 0 && N % kPBN == 0 && tiles(kPBN, kPBM) >= kXcds * 64 && ldx % 16 == 0 &&
       (reinterpret_cast<uintptr_t>(X) & 15) == 0 && (reinterpret_cast<uintptr_t>(W) & 15) == 0 && K % kPKC == 0) {
     switch (K / kPKC) {

@@ -143,6 +143,35 @@ def test_qlinear_persistent_gemm_epilogues(torch_dev, M, K, N):
     assert np.array_equal(got[rows].view(np.uint32), ref.view(np.uint32))
 
 
+@pytest.mark.parametrize("M,K,N", [(4096, 256, 32000), (4096, 256, 16384), (8192, 256, 8192)], ids=lambda v: str(v))
+def test_qlinear_weight_stationary_gemm(torch_dev, M, K, N):
+    """K = 256 with at least 16 row steps of 64 per block: the weight-stationary
+    kernel (weights in registers, the epilogue of one step interleaved with the
+    next step's MFMAs).  Sampled rows include the first two rows of every
+    block's first step, which that kernel first fills with a placeholder and
+    then rewrites, and each block's last step; every epilogue it takes."""
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    print(f"weight-stationary GEMM M={M} K={K} N={N}", flush=True)
+    X, W, mult, bias = G.sweep_case(M, K, N, seed=11)
+    ncol, steps = N // 256, M // 64
+    spb = -(-steps // max(1, min(steps, 256 // ncol)))
+    starts = np.arange(0, steps, spb) * 64
+    rows = np.unique(np.concatenate([starts, starts + 33, np.minimum(starts + spb * 64, M) - 1,
+                                     np.random.default_rng(5).choice(M, 12, replace=False)]))
+    got = _run(torch, dev, X, W, mult, bias, mnmt.EPI_I32)
+    assert np.array_equal(got[rows], oracle.qgemm_i32(X[rows], W))
+    for epi, oepi in ((mnmt.EPI_I8, oracle.EPI_I8), (mnmt.EPI_I8_RELU, oracle.EPI_I8_RELU)):
+        got = _run(torch, dev, X, W, mult, bias, epi)
+        assert np.array_equal(got[rows], oracle.qlinear(X[rows], W, mult, bias, oepi))
+    dq = (mult * 1e-3).astype(np.float32)
+    for epi in (mnmt.EPI_F32, mnmt.EPI_LOGITS):
+        got = _run(torch, dev, X, W, dq, bias, epi)
+        ref = oracle.qlinear(X[rows], W, dq, bias, epi)
+        assert np.array_equal(got[rows].view(np.uint32), ref.view(np.uint32))
+
+
 @pytest.mark.parametrize("M,K,N", [(1, 256, 32000), (2, 512, 32000), (1, 64, 1000), (2, 128, 33), (1, 384, 129),
                                    (3, 256, 1000), (8, 1024, 4097), (2, 1024, 500)], ids=lambda v: str(v))
 def test_qlinear_fused_argmax(torch_dev, M, K, N):
