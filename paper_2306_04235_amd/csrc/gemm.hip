@@ -473,15 +473,33 @@ struct WsConst {
 // Group G (4 outputs) of fragment F: int8 outputs are packed into w4[G] and
 // written after group 3 (one 16-byte store of 16 consecutive columns per
 // lane, after two lane swaps); wider outputs are written per group.
+// Byte T of d = the low byte of (y + 1.5 * 2^23) for y already clamped to
+// [-127, 127]: the add rounds y to an integer (round half to even) and leaves
+// its two's complement code in the low byte (as code_bits), and the SDWA
+// destination select writes that byte alone (byte 0 clears the others), so
+// four codes are packed without byte permutes.
+template <int T>
+__device__ __forceinline__ void add_code_byte(uint32_t& d, float y) {
+  const float magic = 12582912.0f;
+  if (T == 0) asm("v_add_f32_sdwa %0, %1, %2 dst_sel:BYTE_0 dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:DWORD" : "=v"(d) : "v"(y), "v"(magic));
+  if (T == 1) asm("v_add_f32_sdwa %0, %1, %2 dst_sel:BYTE_1 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:DWORD" : "+v"(d) : "v"(y), "v"(magic));
+  if (T == 2) asm("v_add_f32_sdwa %0, %1, %2 dst_sel:BYTE_2 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:DWORD" : "+v"(d) : "v"(y), "v"(magic));
+  if (T == 3) asm("v_add_f32_sdwa %0, %1, %2 dst_sel:BYTE_3 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:DWORD" : "+v"(d) : "v"(y), "v"(magic));
+}
+
 template <int EPI, int F, int G>
 __device__ __forceinline__ void ws_epi_group(const EpiArgs& e, const v16i (&P)[2], const WsConst<EPI>& c,
                                              uint32_t (&w4)[4], int m, int nw, int h) {
   constexpr bool INT8_OUT = EPI == MNMT_EPI_I8 || EPI == MNMT_EPI_I8_RELU;
   if (INT8_OUT) {
-    uint32_t q[4];
+    float y[4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) q[t] = code_bits(epi_value<EPI>(P[F][4 * G + t], c.sc[F][4 * G + t], c.bi[F][4 * G + t]));
-    w4[G] = pack4(q[0], q[1], q[2], q[3]);
+    for (int t = 0; t < 4; ++t)
+      y[t] = fminf(fmaxf(epi_value<EPI>(P[F][4 * G + t], c.sc[F][4 * G + t], c.bi[F][4 * G + t]), -127.0f), 127.0f);
+    add_code_byte<0>(w4[G], y[0]);
+    add_code_byte<1>(w4[G], y[1]);
+    add_code_byte<2>(w4[G], y[2]);
+    add_code_byte<3>(w4[G], y[3]);
     if (G == 3) {
       const auto s02 = __builtin_amdgcn_permlane32_swap(w4[0], w4[2], false, false);
       const auto s13 = __builtin_amdgcn_permlane32_swap(w4[1], w4[3], false, false);
