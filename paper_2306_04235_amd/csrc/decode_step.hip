@@ -103,6 +103,41 @@ __device__ __forceinline__ void clear_acc(const StepIn& in) {
     for (int i = threadIdx.x; i < in.zero_n; i += kStepThreads) in.zero_acc[i] = 0;
 }
 
+// Waits for the previous kernel of a translation's chain (see StepChain):
+// thread i polls the flag word of block i (relaxed, agent scope), then each
+// polling wave takes an acquire fence and the block a barrier, after which
+// every thread sees the previous kernel's writes.  Called after the weight loads
+// are issued, so they arrive while the previous kernel still runs.
+__device__ __forceinline__ void chain_wait(const StepChain& c) {
+  if (!c.wait) return;
+  const int tid = threadIdx.x;
+  if (tid < c.nwait) {
+    const unsigned* w = c.wait + (blockIdx.x % chain_copies(c.nwait)) * kChainCopyStride + tid;
+    unsigned n = 0;
+    while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < c.want) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++n >= kChainSpinLimit) {  // never in a correct chain: record it and go on
+        __hip_atomic_fetch_or(c.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+    }
+  }
+  // the acquire (an invalidation of the CU's caches) once per polling wave;
+  // the barrier then orders every wave's loads after it
+  if ((int)(tid & ~63) < c.nwait) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  __syncthreads();
+}
+
+// The block's flag word (in every copy), stored (release, agent scope) after
+// every thread of the block has issued its last global write.
+__device__ __forceinline__ void chain_signal(const StepChain& c) {
+  if (!c.done) return;
+  __syncthreads();
+  if ((int)threadIdx.x < chain_copies(gridDim.x))
+    __hip_atomic_store(c.done + threadIdx.x * kChainCopyStride + blockIdx.x, c.val, __ATOMIC_RELEASE,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // The projections run on v_mfma_i32_16x16x64_i8 even though only R <= 2 of
 // the 16 rows of its A operand are real: one matrix instruction yields 16
 // complete output dot products in lanes 0..15 (D[m] = row m), where the
@@ -131,36 +166,10 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   const int ntile = (SELF ? 3 : 1) * dh / 16;  // projection tiles of this head
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
-  // 1. every global load, none conditional: the wave's input row, the
-  //    projection's weight fragments with their scales and biases, the W_o
-  //    fragments, the keys and values
-  RowRegs<NJ> rr;
-  // MODE 1 / 2: the arg-max partials of the wave's row (lane i: slots i + 64 k)
-  // and whether the row had finished
-  unsigned long long pk[4] = {0ull, 0ull, 0ull, 0ull};
-  int fin = 0;
-  if (MODE != 0) {
-    const int row = min(wave, R - 1);
-    const unsigned long long* sl = cm.slots + (size_t)row * cm.nslots;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) pk[k] = sl[min(lane + 64 * k, cm.nslots - 1)];
-    fin = cm.finished[row];
-  }
-  if (MODE == 1) {
-    // the position term now, the token's embedding once the token is known
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int i = min(lane + 64 * j, d - 1);
-      rr.x[j] = cm.pe[(size_t)cm.t * d + i];
-      rr.a[j] = 0;
-      rr.sc[j] = 0.0f;
-      rr.bi[j] = 0.0f;
-      rr.g[j] = in.ln_g[i];
-      rr.b[j] = in.ln_b[i];
-    }
-  } else {
-    load_row(in, min(wave, R - 1), d, rr);
-  }
+  // 1. every global load, none conditional: the projection's weight
+  //    fragments with their scales and biases, the W_o fragments, the keys
+  //    and values (all written before the previous kernel started), then,
+  //    after the chain wait, the wave's input row
   v4i wf[TPW][KS];
   float e_sc[TPW], e_bi[TPW];
 #pragma unroll
@@ -200,6 +209,35 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   }
   int n_att = SELF ? at.t + 1 : at.len[r];
   n_att = SELF ? n_att : (n_att < 1 ? 1 : (n_att > at.S ? at.S : n_att));
+  asm volatile("" ::: "memory");  // the loads above stay ahead of the wait
+  chain_wait(in.chain);
+  RowRegs<NJ> rr;
+  // MODE 1 / 2: the arg-max partials of the wave's row (lane i: slots i + 64 k)
+  // and whether the row had finished
+  unsigned long long pk[4] = {0ull, 0ull, 0ull, 0ull};
+  int fin = 0;
+  if (MODE != 0) {
+    const int row = min(wave, R - 1);
+    const unsigned long long* sl = cm.slots + (size_t)row * cm.nslots;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pk[k] = sl[min(lane + 64 * k, cm.nslots - 1)];
+    fin = cm.finished[row];
+  }
+  if (MODE == 1) {
+    // the position term now, the token's embedding once the token is known
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = min(lane + 64 * j, d - 1);
+      rr.x[j] = cm.pe[(size_t)cm.t * d + i];
+      rr.a[j] = 0;
+      rr.sc[j] = 0.0f;
+      rr.bi[j] = 0.0f;
+      rr.g[j] = in.ln_g[i];
+      rr.b[j] = in.ln_b[i];
+    }
+  } else {
+    load_row(in, min(wave, R - 1), d, rr);
+  }
   if (MODE == 1) {
     unsigned long long key = pk[0];
 #pragma unroll
@@ -358,6 +396,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
       if (wave == 0) *cm.step = cm.t;
     }
   }
+  chain_signal(in.chain);
 }
 
 // One block per kFfnChunk hidden units (one 16-row W1 tile per wave): ReLU
@@ -375,8 +414,6 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
   const int f0 = blockIdx.x * kFfnChunk;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
-  RowRegs<NJ> rr;
-  load_row(in, min(wave, R - 1), d, rr);
   const size_t hrow = (size_t)min(f0 + 16 * wave + l16, F - 1);
   v4i wf[KS];
 #pragma unroll
@@ -388,6 +425,10 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
     const int n = min(16 * (wave + 4 * t) + l16, d - 1);
     of[t] = *(const v4i*)(f.W2 + (size_t)n * F + f0 + 16 * kq);
   }
+  asm volatile("" ::: "memory");  // the weight loads stay ahead of the wait
+  chain_wait(in.chain);
+  RowRegs<NJ> rr;
+  load_row(in, min(wave, R - 1), d, rr);
   clear_acc(in);
   if (wave < R) finish_row(in, wave, d, rr, a_lds);
   lds_barrier();
@@ -418,6 +459,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
       }
     }
   }
+  chain_signal(in.chain);
 }
 
 // Output projection over the shared embedding with the fused arg-max: each
@@ -435,8 +477,6 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
   const int row0 = (blockIdx.x * 4 + wave) * TPW * 16;
-  RowRegs<NJ> rr;
-  if (!RAW) load_row(in, min(wave, R - 1), d, rr);
   v4i xr = {0, 0, 0, 0};
   if (RAW) xr = *(const v4i*)(g.x_i8 + (size_t)min(wave, R - 1) * d + 16 * min(lane, d / 16 - 1));
   v4i wf[TPW][KS];
@@ -447,6 +487,12 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) wf[t][kk] = *(const v4i*)(g.E + n * d + 64 * min(kk, ks - 1) + 16 * kq);
     co[t] = g.c_out[n];
+  }
+  RowRegs<NJ> rr;
+  if (!RAW) {
+    asm volatile("" ::: "memory");  // the weight loads stay ahead of the wait
+    chain_wait(in.chain);
+    load_row(in, min(wave, R - 1), d, rr);
   }
   if (!RAW) {
     clear_acc(in);
@@ -502,6 +548,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
       if (b > __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(slot, b);
     }
   }
+  if (!RAW) chain_signal(in.chain);
 }
 
 }  // namespace

@@ -130,6 +130,30 @@ struct FusedGemv {         // a linear layer over the prepared rows, and greedy 
 hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s);
 
 // Decoder step in 3 kernels per layer for at most 2 rows (decode_step.hip).
+// Hand-off between consecutive kernels of a batch-1 translation that run on
+// two alternating streams: a kernel loads its weights, then waits until every
+// block of the kernel before it has stored `want` (or more) into its flag
+// word, and its own blocks store `val` when done (release / acquire at agent
+// scope).  Null `wait` / `done`: no wait / no flag.  Waits are bounded: after
+// kChainSpinLimit polls the kernel sets *err and goes on.
+// A kernel of at most kChainCopyStride blocks stores its flag words in
+// kChainCopies copies kChainCopyStride words apart, and consumer block b
+// polls copy b mod kChainCopies: hundreds of blocks polling one cache line
+// serialize at the memory and delay everything around them.
+constexpr int kChainMaxBlocks = 256;   // blocks of one kernel of the chain
+constexpr int kChainCopies = 8, kChainCopyStride = 128;
+constexpr int kChainSlotWords = kChainCopies * kChainCopyStride;  // flag words per kernel slot
+constexpr unsigned kChainSpinLimit = 1u << 17;  // about 8 ms of polling
+__host__ __device__ constexpr int chain_copies(int blocks) { return blocks <= kChainCopyStride ? kChainCopies : 1; }
+struct StepChain {
+  const unsigned* wait;  // the previous kernel's flag words [nwait]
+  int nwait;
+  unsigned want;
+  unsigned* done;        // this kernel's flag words [gridDim.x]
+  unsigned val;
+  int* err;
+};
+
 struct StepIn {            // the sublayer input rows of a step kernel
   // Every pointer is valid for the extent given even where its flag is off,
   // so that the kernels load without branches.
@@ -147,6 +171,7 @@ struct StepIn {            // the sublayer input rows of a step kernel
   float inv_s;             // 1 / input scale of the consuming layer
   int32_t* zero_acc;       // block 0 clears this accumulator (its consumer has finished)
   int zero_n;
+  StepChain chain;
 };
 struct StepAttn {
   int R, d, dh, T, S, t;
@@ -394,5 +419,10 @@ struct mnmt_session {
   std::map<std::string, std::pair<void*, size_t>> named;
   // graph cache
   hipStream_t capture_stream = nullptr;
+  hipStream_t side_stream = nullptr;  // the second stream of the batch-1 kernel chain
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
+  unsigned* chain = nullptr;          // flag words [3 n_dec + 1][kChainSlotWords], cleared per translation
+  int* chain_err = nullptr;           // set by a wait that gave up (never cleared)
+  bool chain_on = true;               // off with MNMT_SERIAL_STEPS=1 in the environment
   std::map<std::string, hipGraphExec_t> graphs;
 };

@@ -8,6 +8,7 @@
 // Each layer reuses the same few buffers: one fp32 residual stream and int8
 // buffers for the sublayer input, attention context and FFN hidden layer.
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <utility>
@@ -34,6 +35,7 @@ struct Plan {
   size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots, enc_acc;
   size_t cur_tok, step, slots, out_tok, finished, out_len, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
+  size_t chain_err;
   size_t total;
 };
 
@@ -50,6 +52,16 @@ int validate_cfg(const mnmt_model* m, const mnmt_session_cfg* c) {
 }
 
 size_t enc_acc_bytes(size_t d) { return 4 * kEncAccRows * d * sizeof(int32_t); }
+
+// The chain's flag words: one slot of kChainSlotWords per kernel of a step
+// (self-attention, cross-attention, FFN per layer, then the logits).
+size_t chain_words(const mnmt_model* m) { return (3 * (size_t)m->info.n_dec + 1) * kChainSlotWords; }
+
+// 8-byte words cleared by the greedy reset: the fused arg-max slots, the
+// decode-step accumulators and the chain's flag words, which follow each other.
+int fslots_words(const mnmt_model* m) {
+  return 8 * fused_slots_per_row(m->info.vocab) + 3 * 2 * m->info.d_model / 2 + (int)(chain_words(m) / 2);
+}
 
 Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   Plan p{};
@@ -82,8 +94,9 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.enc_acc = b.take(enc_acc_bytes(d));
   p.dec_x = b.take(4 * R * d);
   p.dec_x2 = b.take(4 * R * d);
-  // fused arg-max slots, then the decode-step int32 accumulators (cleared together)
-  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row(m->info.vocab) + 4 * 3 * 2 * d);
+  // fused arg-max slots, the decode-step int32 accumulators and the chain's
+  // flag words (cleared together)
+  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row(m->info.vocab) + 4 * 3 * 2 * d + 4 * chain_words(m));
   p.dec_a = b.take(R * d);
   p.dec_qkv = b.take(R * 3 * d);
   p.dec_q = b.take(R * d);
@@ -110,6 +123,7 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.fin_row = b.take(4 * B * W);
   p.fin_count = b.take(4 * B);
   p.done = b.take(4 * B);
+  p.chain_err = b.take(4);
   p.total = (b.off + 255) / 256 * 256;
   return p;
 }
@@ -506,11 +520,43 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
 // wave's four loads per lane.
 bool fold_ok(const mnmt_model* m) { return fused_slots_per_row(m->info.vocab) <= 256; }
 
+// Host state of a translation's kernel chain: kernel j runs on stream j mod 2,
+// after kernel j - 2 (stream order), and waits on the flags of kernel j - 1.
+struct Chain {
+  hipStream_t st[2];
+  unsigned* flags;
+  int* err;
+  long j = 0;  // kernels launched so far
+  int prev_slot = 0, prev_blocks = 0;
+  unsigned prev_val = 0;
+  // The chain arguments of the next kernel (flag slot, block count, the value
+  // its blocks store) and the stream it goes on.
+  hipStream_t next(StepChain& c, int slot, int blocks, unsigned val) {
+    c.wait = j > 0 ? flags + (size_t)prev_slot * kChainSlotWords : nullptr;
+    c.nwait = prev_blocks;
+    c.want = prev_val;
+    c.done = flags + (size_t)slot * kChainSlotWords;
+    c.val = val;
+    c.err = err;
+    prev_slot = slot;
+    prev_blocks = blocks;
+    prev_val = val;
+    return st[j++ & 1];
+  }
+  hipStream_t last() const { return st[(j - 1) & 1]; }
+};
+
+// Every kernel of the 1-2 row step fits the flag slots.
+bool chain_ok(const mnmt_model* m) {
+  return fold_ok(m) && m->info.n_heads <= kChainMaxBlocks && m->info.d_ffn / 64 <= kChainMaxBlocks &&
+         step_logits_blocks(m->info.vocab) <= kChainMaxBlocks;
+}
+
 // fold (a whole translation's steps): step t > 0 embeds and records step t -
 // 1's token inside its first layer instead of a commit kernel after step t -
 // 1; the last step commits as usual.
 int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s, bool fold,
-                   bool last_step) {
+                   bool last_step, Chain* ch) {
   const mnmt_model* m = S->m;
   const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
   const bool post = m->info.ln_post;
@@ -613,7 +659,8 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       StepAttn at = attn(L, true, acc_o);
       at.kcache = S->kcache[l];
       at.vcache = S->vcache[l];
-      LAUNCH(launch_step_attn(in, at, 1, h, s, cml));
+      const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l, h, t + 1) : s;
+      LAUNCH(launch_step_attn(in, at, 1, h, ks, cml));
       if (in.x_out) std::swap(xa, xb);
     }
     {  // cross-attention block
@@ -623,7 +670,8 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       in.zero_n = nacc;
       StepAttn at = attn(L, false, acc_oc);
       at.kv = S->cross_kv[l];
-      LAUNCH(launch_step_attn(in, at, 0, h, s, cml));
+      const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 1, h, t + 1) : s;
+      LAUNCH(launch_step_attn(in, at, 0, h, ks, cml));
       std::swap(xa, xb);
     }
     {  // FFN block
@@ -640,7 +688,8 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       f.bias1 = L.w1.bias;
       f.W2 = L.w2.w;
       f.acc_out = acc_w2;
-      LAUNCH(launch_step_ffn(in, f, s));
+      const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 2, f.F / 64, t + 1) : s;
+      LAUNCH(launch_step_ffn(in, f, ks));
       std::swap(xa, xb);
     }
   }
@@ -659,7 +708,8 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   g.logits = logits_out;
   g.slots = S->fslots;
   g.nslots = fused_slots_per_row(m->info.vocab);
-  LAUNCH(launch_step_logits(in, g, s));
+  const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)m->dec.size(), step_logits_blocks(g.V), t + 1) : s;
+  LAUNCH(launch_step_logits(in, g, ks));
   FusedGemv gv{};
   gv.R = R;
   gv.t = t;
@@ -684,7 +734,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   gv.V = m->info.vocab;
   gv.P = m->info.max_pos;
   if (fold && !last_step && fold_ok(m)) return MNMT_OK;  // the next step's first layer commits
-  LAUNCH(launch_greedy_commit_slots(gv, s));
+  LAUNCH(launch_greedy_commit_slots(gv, ch ? ch->last() : s));  // after the logits on their stream
   return MNMT_OK;
 }
 
@@ -704,8 +754,8 @@ int embed_step_input(mnmt_session* S, int R, hipStream_t s) {
 // The greedy step for R rows on the fastest path that fits.
 // On the 1-2 row path the input rows must be in dec_x (embed_step_input).
 int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s,
-                    bool fold = false, bool last = false) {
-  if (step_path_used(S, R)) return greedy_step_v3(S, R, t, stop_at_eos, logits_out, s, fold, last);
+                    bool fold = false, bool last = false, Chain* ch = nullptr) {
+  if (step_path_used(S, R)) return greedy_step_v3(S, R, t, stop_at_eos, logits_out, s, fold, last, ch);
   if (R <= 8) return greedy_step_fused(S, R, t, stop_at_eos, logits_out, s);
   return greedy_step(S, R, stop_at_eos, logits_out, s);
 }
@@ -730,10 +780,24 @@ int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
   if (sc.beam == 1) {
     const int R = S->B;
     LAUNCH(launch_greedy_reset(S->slots, R, sc.max_steps, S->cur_tok, S->finished, S->out_len, S->step,
-                               m->info.bos_id, S->fslots, 8 * fused_slots_per_row(m->info.vocab) + 3 * 2 * m->info.d_model / 2, s));
+                               m->info.bos_id, S->fslots, fslots_words(m), s));
     if (step_path_used(S, R) && (rc = embed_step_input(S, R, s))) return rc;
-    for (int t = 0; t < sc.max_steps; ++t)
-      if ((rc = greedy_step_any(S, R, t, sc.stop_at_eos, nullptr, s, true, t + 1 == sc.max_steps))) return rc;
+    if (step_path_used(S, R) && chain_ok(m) && S->chain_on) {
+      // the step kernels alternate between the caller's stream and the side
+      // stream, each loading its weights while its predecessor runs
+      MNMT_HIP(hipEventRecord(S->fork_ev, s));
+      MNMT_HIP(hipStreamWaitEvent(S->side_stream, S->fork_ev, 0));
+      Chain ch{{s, S->side_stream}, S->chain, S->chain_err};
+      for (int t = 0; t < sc.max_steps && !rc; ++t)
+        rc = greedy_step_any(S, R, t, sc.stop_at_eos, nullptr, s, true, t + 1 == sc.max_steps, &ch);
+      // join the side stream whatever happened, so a capture can end cleanly
+      MNMT_HIP(hipEventRecord(S->join_ev, S->side_stream));
+      MNMT_HIP(hipStreamWaitEvent(s, S->join_ev, 0));
+      if (rc) return rc;
+    } else {
+      for (int t = 0; t < sc.max_steps; ++t)
+        if ((rc = greedy_step_any(S, R, t, sc.stop_at_eos, nullptr, s, true, t + 1 == sc.max_steps))) return rc;
+    }
   } else {
     const int R = S->B * sc.beam;
     LAUNCH(launch_beam_reset(S->beam, S->step, s));
@@ -808,6 +872,8 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->fslots = (unsigned long long*)at(p.fslots);
   S->enc_acc = (int32_t*)at(p.enc_acc);
   S->step_acc = (int32_t*)(S->fslots + 8 * (size_t)fused_slots_per_row((int)V));
+  S->chain = (unsigned*)(S->step_acc + 3 * 2 * d);
+  S->chain_err = (int*)at(p.chain_err);
   S->dec_a = (int8_t*)at(p.dec_a);
   S->dec_qkv = (int8_t*)at(p.dec_qkv);
   S->dec_q = (int8_t*)at(p.dec_q);
@@ -849,21 +915,31 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->named["logits"] = {S->logits, 4 * R * V};
   S->named["step"] = {S->step, 4};
   S->named["cur_tok"] = {S->cur_tok, 4 * R};
+  S->named["chain_err"] = {S->chain_err, 4};
   for (size_t l = 0; l < p.cross_kv.size(); ++l) {
     S->named["cross_kv." + std::to_string(l)] = {S->cross_kv[l], BS * 2 * d};
     S->named["kcache." + std::to_string(l)] = {S->kcache[l], R * T * d};
     S->named["vcache." + std::to_string(l)] = {S->vcache[l], R * T * d};
   }
-  if (hipStreamCreateWithFlags(&S->capture_stream, hipStreamNonBlocking) != hipSuccess) {
-    delete S;
-    return set_error(MNMT_E_HIP, "could not create the capture stream");
+  if (hipStreamCreateWithFlags(&S->capture_stream, hipStreamNonBlocking) != hipSuccess ||
+      hipStreamCreateWithFlags(&S->side_stream, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&S->fork_ev, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&S->join_ev, hipEventDisableTiming) != hipSuccess) {
+    mnmt_session_free(S);
+    return set_error(MNMT_E_HIP, "could not create the session's streams and events");
   }
-  // the encoder accumulators start at zero (each encode leaves them so)
+  // Tools that serialize kernel dispatches (a kernel tracer may) would leave
+  // each chained kernel polling for a predecessor queued behind it until its
+  // wait gives up; MNMT_SERIAL_STEPS=1 runs the steps in one stream instead.
+  const char* serial = std::getenv("MNMT_SERIAL_STEPS");
+  S->chain_on = !(serial && std::atoi(serial) != 0);
+  // the encoder accumulators start at zero (each encode leaves them so), the
+  // chain error word too
   hipError_t h = hipMemsetAsync(S->enc_acc, 0, enc_acc_bytes(d), S->capture_stream);
+  if (h == hipSuccess) h = hipMemsetAsync(S->chain_err, 0, sizeof(int), S->capture_stream);
   if (h == hipSuccess) h = hipStreamSynchronize(S->capture_stream);
   if (h != hipSuccess) {
-    (void)hipStreamDestroy(S->capture_stream);
-    delete S;
+    mnmt_session_free(S);
     return hip_error(h, "clearing the encoder accumulators");
   }
   *out = S;
@@ -874,6 +950,9 @@ extern "C" void mnmt_session_free(mnmt_session* S) {
   if (!S) return;
   for (auto& g : S->graphs) (void)hipGraphExecDestroy(g.second);
   if (S->capture_stream) (void)hipStreamDestroy(S->capture_stream);
+  if (S->side_stream) (void)hipStreamDestroy(S->side_stream);
+  if (S->fork_ev) (void)hipEventDestroy(S->fork_ev);
+  if (S->join_ev) (void)hipEventDestroy(S->join_ev);
   delete S;
 }
 
@@ -895,7 +974,7 @@ extern "C" int mnmt_encode(mnmt_session* S, const int32_t* d_src, const int32_t*
   if ((rc = run_encoder(S, s))) return rc;
   const mnmt_model* m = S->m;
   LAUNCH(launch_greedy_reset(S->slots, B, S->cfg.max_tgt_len, S->cur_tok, S->finished, S->out_len, S->step,
-                             m->info.bos_id, S->fslots, 8 * fused_slots_per_row(m->info.vocab) + 3 * 2 * m->info.d_model / 2, s));
+                             m->info.bos_id, S->fslots, fslots_words(m), s));
   S->encoded = true;
   S->host_step = 0;
   return MNMT_OK;

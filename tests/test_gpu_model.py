@@ -88,6 +88,8 @@ def _greedy_check(torch, dev, cfg, src, lens, steps, stop_at_eos=False, check_lo
         torch.cuda.synchronize()
         assert np.array_equal(out.cpu().numpy(), o_out), f"greedy tokens (graph={use_graph})"
         assert np.array_equal(out_len.cpu().numpy(), o_len)
+    # no kernel of the translation chain gave up waiting for its predecessor
+    assert int(sess.tensor("chain_err", torch.int32, (1,)).cpu().numpy()[0]) == 0
     sess.close()
     return o_out
 
@@ -145,6 +147,29 @@ def test_mobile_greedy_latency_workload(torch_dev):
     torch, dev = torch_dev
     src, lens = G.workload_inputs(G.WORKLOADS["mobile"])
     _greedy_check(torch, dev, "MOBILE", src, lens, 30)
+
+
+def test_serial_steps_match_the_kernel_chain(torch_dev, monkeypatch):
+    """The batch-1 steps run as a chain of kernels over two streams, each
+    waiting on its predecessor's flags; with MNMT_SERIAL_STEPS=1 (read at
+    session creation) they run in one stream.  Both give the oracle's tokens."""
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    om, gm = _pair("MOBILE")
+    src, lens = G.workload_inputs(G.WORKLOADS["mobile"])
+    o_out, o_len = om.greedy(src, lens, 30)[:2]
+    ts, tl = _t(torch, dev, src), _t(torch, dev, lens)
+    for serial in ("0", "1"):
+        monkeypatch.setenv("MNMT_SERIAL_STEPS", serial)
+        sess = mnmt.Session(gm, 1, src.shape[1], 30, 1)
+        for use_graph in (False, True):
+            out, out_len, _ = sess.translate(ts, tl, beam=1, max_steps=30, use_graph=use_graph)
+            torch.cuda.synchronize()
+            assert np.array_equal(out.cpu().numpy(), o_out), f"serial={serial} graph={use_graph}"
+            assert np.array_equal(out_len.cpu().numpy(), o_len)
+        assert int(sess.tensor("chain_err", torch.int32, (1,)).cpu().numpy()[0]) == 0
+        sess.close()
 
 
 WIDE384 = G.ModelConfig("wide-384", 384, 6, 768, 2, 1, 600, ln_post=0, seed=83, random_gamma=True, weight_std=0.05)
