@@ -463,14 +463,17 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
 }
 
 // Output projection over the shared embedding with the fused arg-max: each
-// wave takes kLogitsTiles tiles of 16 vocabulary rows.  RAW: the rows are
+// wave takes TPW tiles of 16 vocabulary rows (kLogitsTiles alone, more in a
+// kernel chain, where the weights load while the previous kernel runs and
+// fewer blocks mean fewer flags to store and to wait for).  RAW: the rows are
 // int8 codes already (g.x_i8) instead of the residual stream.
 constexpr int kLogitsTiles = 2;
-template <int DMAX, bool RAW>
+// in a chain: 4 tiles per wave once that still leaves about 100 blocks
+__host__ inline int chain_logits_tiles(int V) { return V >= 4 * 4 * 16 * 96 ? 4 : kLogitsTiles; }
+template <int DMAX, bool RAW, int TPW>
 __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLogits g) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;
-  constexpr int TPW = kLogitsTiles;
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
   __shared__ unsigned long long wmax[4][kStepRows];
   const int R = g.R, d = DMAX, N = g.V, ks = d / 64;  // DMAX is the exact width
@@ -565,6 +568,12 @@ int step_logits_blocks(int V) {
   return (V + rpb - 1) / rpb;
 }
 
+int step_logits_blocks_chained(int V, int d) {
+  (void)d;
+  const int rpb = 4 * chain_logits_tiles(V) * 16;
+  return (V + rpb - 1) / rpb;
+}
+
 // Kernels are instantiated on the exact width (a multiple of 64 up to 512),
 // so the row code carries no bounds checks.
 #define MNMT_BY_D(d, CALL)            \
@@ -619,14 +628,18 @@ hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s) {
 hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s, hipEvent_t ev_start,
                               hipEvent_t ev_stop) {
   const int blocks = step_logits_blocks(g.V);
+  const int cblocks = step_logits_blocks_chained(g.V, g.d);
+  if (in.chain.done && g.nslots < cblocks) return hipErrorInvalidValue;
 #define MNMT_LOGITS(DM)                                                                                       \
   if (g.x_i8 && (ev_start || ev_stop))                                                                        \
-    hipExtLaunchKernelGGL((k_step_logits<DM, true>), dim3(blocks), dim3(kStepThreads), 0, s, ev_start, ev_stop, 0, \
-                          in, g);                                                                             \
+    hipExtLaunchKernelGGL((k_step_logits<DM, true, kLogitsTiles>), dim3(blocks), dim3(kStepThreads), 0, s,    \
+                          ev_start, ev_stop, 0, in, g);                                                       \
   else if (g.x_i8)                                                                                            \
-    hipLaunchKernelGGL((k_step_logits<DM, true>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);             \
+    hipLaunchKernelGGL((k_step_logits<DM, true, kLogitsTiles>), dim3(blocks), dim3(kStepThreads), 0, s, in, g); \
+  else if (in.chain.done && chain_logits_tiles(g.V) == 4)                                                    \
+    hipLaunchKernelGGL((k_step_logits<DM, false, 4>), dim3(cblocks), dim3(kStepThreads), 0, s, in, g);        \
   else                                                                                                        \
-    hipLaunchKernelGGL((k_step_logits<DM, false>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);
+    hipLaunchKernelGGL((k_step_logits<DM, false, kLogitsTiles>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);
   MNMT_BY_D(g.d, MNMT_LOGITS)
 #undef MNMT_LOGITS
   return hipGetLastError();

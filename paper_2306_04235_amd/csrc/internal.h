@@ -227,6 +227,7 @@ struct StepLogits {
 bool step_path_fits(int R, int d, int dh, int F, int T, int S);
 bool step_logits_fits(int R, int d);  // R <= 2, d a multiple of 64 up to 512
 int step_logits_blocks(int V);        // blocks (and arg-max partials per row) of launch_step_logits
+int step_logits_blocks_chained(int V, int d);  // the same in a kernel chain (more rows per block)
 // cm (or null): self = 1 embeds the previous step's token from its partials
 // (layer 0, the rows' x_in unused); self = 0 records that token (block 0).
 hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s,

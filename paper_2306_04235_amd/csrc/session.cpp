@@ -549,7 +549,7 @@ struct Chain {
 // Every kernel of the 1-2 row step fits the flag slots.
 bool chain_ok(const mnmt_model* m) {
   return fold_ok(m) && m->info.n_heads <= kChainMaxBlocks && m->info.d_ffn / 64 <= kChainMaxBlocks &&
-         step_logits_blocks(m->info.vocab) <= kChainMaxBlocks;
+         step_logits_blocks_chained(m->info.vocab, m->info.d_model) <= kChainMaxBlocks;
 }
 
 // fold (a whole translation's steps): step t > 0 embeds and records step t -
@@ -708,7 +708,8 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   g.logits = logits_out;
   g.slots = S->fslots;
   g.nslots = fused_slots_per_row(m->info.vocab);
-  const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)m->dec.size(), step_logits_blocks(g.V), t + 1) : s;
+  const hipStream_t ks =
+      ch ? ch->next(in.chain, 3 * (int)m->dec.size(), step_logits_blocks_chained(g.V, d), t + 1) : s;
   LAUNCH(launch_step_logits(in, g, ks));
   FusedGemv gv{};
   gv.R = R;
