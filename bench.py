@@ -49,7 +49,7 @@ def _events_ms(torch, fn, reps, stream):
 
 
 ROOF_TAG = "step_logits_raw_b1"
-ROOF_KERNEL = "k_step_logits<256, true>"
+ROOF_KERNEL = "k_step_logits<256, true, 2>"
 COPY_BYTES = 256 << 20
 
 
