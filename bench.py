@@ -85,7 +85,7 @@ def _kernel_events_ms(torch, fn_ev, reps, stream):
 
 def _source_hash():
     h = hashlib.sha256()
-    for f in ("decode_step.hip", "canon.hpp", "blocks.hpp", "internal.h"):
+    for f in ("decode_step.hip", "canon.hpp", "blocks.hpp", "chain.hpp", "internal.h"):
         with open(os.path.join(ROOT, "paper_2306_04235_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

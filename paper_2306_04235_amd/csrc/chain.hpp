@@ -1,0 +1,46 @@
+// chain.hpp -- the hand-off between consecutive kernels of a translation
+// that run on two alternating streams (StepChain in internal.h): a kernel
+// issues the loads that do not depend on its predecessor, waits on the
+// predecessor's per-block flag words, and stores its own when done.
+#pragma once
+
+#include "internal.h"
+
+namespace mnmt {
+
+// Waits for the previous kernel of a translation's chain (see StepChain):
+// thread i polls the flag word of block i (relaxed, agent scope), then each
+// polling wave takes an acquire fence and the block a barrier, after which
+// every thread sees the previous kernel's writes.  Called after the weight loads
+// are issued, so they arrive while the previous kernel still runs.
+__device__ __forceinline__ void chain_wait(const StepChain& c) {
+  if (!c.wait) return;
+  const int tid = threadIdx.x;
+  if (tid < c.nwait) {
+    const unsigned* w = c.wait + (blockIdx.x % chain_copies(c.nwait)) * kChainCopyStride + tid;
+    unsigned n = 0;
+    while (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < c.want) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++n >= kChainSpinLimit) {  // never in a correct chain: record it and go on
+        __hip_atomic_fetch_or(c.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+    }
+  }
+  // the acquire (an invalidation of the CU's caches) once per polling wave;
+  // the barrier then orders every wave's loads after it
+  if ((int)(tid & ~63) < c.nwait) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  __syncthreads();
+}
+
+// The block's flag word (in every copy), stored (release, agent scope) after
+// every thread of the block has issued its last global write.
+__device__ __forceinline__ void chain_signal(const StepChain& c) {
+  if (!c.done) return;
+  __syncthreads();
+  if ((int)threadIdx.x < chain_copies(gridDim.x))
+    __hip_atomic_store(c.done + threadIdx.x * kChainCopyStride + blockIdx.x, c.val, __ATOMIC_RELEASE,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+}  // namespace mnmt

@@ -28,6 +28,7 @@
 // its length (Appendix A self-attention with the quantizer figure's
 // precisions, the same canonical arithmetic as the other attention kernels).
 #include "blocks.hpp"
+#include "chain.hpp"
 #include "internal.h"
 
 namespace mnmt {
@@ -101,6 +102,11 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
   constexpr int NJ = D / 64;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int R = in.R;
+  // the kernel's own loads first (weights, scales, lengths: none written by
+  // the previous kernel), then, in a kernel chain, the wait for it
+  issue_weights();
+  asm volatile("" ::: "memory");
+  chain_wait(in.chain);
   float sc[NJ], bi[NJ], g[NJ], b[NJ];
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
@@ -142,10 +148,7 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
       }
     }
   }
-  // the kernel's own loads go behind the rows' (the in-order memory counter
-  // then lets the rows be used before those arrive), the clearing stores
-  // behind both
-  issue_weights();
+  // the clearing stores behind the loads
   enc_clear(in);
   // up to four rows at a time, so that their dependent chains (butterflies,
   // square root, division) interleave
@@ -371,6 +374,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       add_frag(at.acc_out, d, acc, 16 * mt, n0 + l16, R);
     }
   }
+  chain_signal(in.chain);
 }
 
 // One block per kEncChunk hidden units: wave w computes the 16-unit W1 tile
@@ -425,6 +429,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
       add_frag(f.acc_out, d, acc, 16 * mt, n0 + l16, R);
     }
   }
+  chain_signal(in.chain);
 }
 
 // One block per kEncChunk columns of one decoder layer's cross K|V
@@ -465,6 +470,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
       if (m < R) L.out[(size_t)m * 2 * d + col] = code_of(fmaf((float)acc[i], e_sc, e_bi));
     }
   }
+  chain_signal(in.chain);
 }
 
 }  // namespace

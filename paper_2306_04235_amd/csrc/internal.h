@@ -83,6 +83,8 @@ hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, 
 // produced by the matrix-core path).
 hipError_t launch_row_argmax(const float* z, int R, int V, unsigned long long* slots, hipStream_t s);
 // Copy tokens into/out of the session (int32 vectors).
+hipError_t launch_load_batch(const int32_t* src_in, const int32_t* len_in, int32_t* src, int32_t* len, int n_src,
+                             int n_len, unsigned* zero, int n_zero, hipStream_t s);
 hipError_t launch_copy_i32(const int32_t* src, int32_t* dst, int n, hipStream_t s);
 
 // Fused decoder step for up to 8 rows (decode_fused.hip).
@@ -265,6 +267,7 @@ struct EncIn {             // the sublayer input rows of an encoder kernel
   int zero0_n;
   int32_t* zero1;
   int zero1_n;
+  StepChain chain;
 };
 struct EncAttn {
   int dh;
@@ -423,6 +426,7 @@ struct mnmt_session {
   hipStream_t side_stream = nullptr;  // the second stream of the batch-1 kernel chain
   hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   unsigned* chain = nullptr;          // flag words [3 n_dec + 1][kChainSlotWords], cleared per translation
+  unsigned* enc_chain = nullptr;      // the encoder's [2 n_enc][kChainSlotWords], cleared by the batch load
   int* chain_err = nullptr;           // set by a wait that gave up (never cleared)
   bool chain_on = true;               // off with MNMT_SERIAL_STEPS=1 in the environment
   std::map<std::string, hipGraphExec_t> graphs;

@@ -205,6 +205,16 @@ __global__ __launch_bounds__(256) void k_row_argmax(const float* __restrict__ z,
   if (lane == 0) slots[r] = best;
 }
 
+// The batch's source ids and lengths into the session, and the encoder
+// chain's flag words cleared for the translation that follows.
+__global__ void k_load_batch(const int32_t* src_in, const int32_t* len_in, int32_t* src, int32_t* len, int n_src,
+                             int n_len, unsigned* zero, int n_zero) {
+  const int stride = gridDim.x * blockDim.x;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n_src; i += stride) src[i] = src_in[i];
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n_len; i += stride) len[i] = len_in[i];
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n_zero; i += stride) zero[i] = 0u;
+}
+
 __global__ void k_copy_i32(const int32_t* src, int32_t* dst, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) dst[i] = src[i];
@@ -750,6 +760,14 @@ hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, 
 hipError_t launch_row_argmax(const float* z, int R, int V, unsigned long long* slots, hipStream_t s) {
   if (R <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_row_argmax, dim3((R + 3) / 4), dim3(256), 0, s, z, R, V, slots);
+  return hipGetLastError();
+}
+
+hipError_t launch_load_batch(const int32_t* src_in, const int32_t* len_in, int32_t* src, int32_t* len, int n_src,
+                             int n_len, unsigned* zero, int n_zero, hipStream_t s) {
+  const int n = max(max(n_src, n_len), n_zero);
+  const int blocks = min(256, max(1, (n + 255) / 256));
+  hipLaunchKernelGGL(k_load_batch, dim3(blocks), dim3(256), 0, s, src_in, len_in, src, len, n_src, n_len, zero, n_zero);
   return hipGetLastError();
 }
 

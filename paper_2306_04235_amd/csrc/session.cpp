@@ -35,7 +35,7 @@ struct Plan {
   size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots, enc_acc;
   size_t cur_tok, step, slots, out_tok, finished, out_len, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
-  size_t chain_err;
+  size_t chain_err, enc_chain;
   size_t total;
 };
 
@@ -124,6 +124,7 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.fin_count = b.take(4 * B);
   p.done = b.take(4 * B);
   p.chain_err = b.take(4);
+  p.enc_chain = b.take(4 * 2 * (size_t)m->info.n_enc * kChainSlotWords);
   p.total = (b.off + 255) / 256 * 256;
   return p;
 }
@@ -207,7 +208,33 @@ int run_encoder_small(mnmt_session* S, hipStream_t s) {
 // previous sublayer's residual update in its prologue; the W_o and W2 int32
 // accumulators alternate by layer parity and are cleared by the kernel after
 // their consumer, so that all four are zero again when the encode ends.
-int run_encoder_blocks(mnmt_session* S, hipStream_t s) {
+// Host state of a translation's kernel chain: kernel j runs on stream j mod 2,
+// after kernel j - 2 (stream order), and waits on the flags of kernel j - 1.
+struct Chain {
+  hipStream_t st[2];
+  unsigned* flags;
+  int* err;
+  long j = 0;  // kernels launched so far
+  int prev_slot = 0, prev_blocks = 0;
+  unsigned prev_val = 0;
+  // The chain arguments of the next kernel (flag slot, block count, the value
+  // its blocks store) and the stream it goes on.
+  hipStream_t next(StepChain& c, int slot, int blocks, unsigned val, bool signal = true) {
+    c.wait = j > 0 ? flags + (size_t)prev_slot * kChainSlotWords : nullptr;
+    c.nwait = prev_blocks;
+    c.want = prev_val;
+    c.done = signal ? flags + (size_t)slot * kChainSlotWords : nullptr;
+    c.val = val;
+    c.err = err;
+    prev_slot = slot;
+    prev_blocks = blocks;
+    prev_val = val;
+    return st[j++ & 1];
+  }
+  hipStream_t last() const { return st[(j - 1) & 1]; }
+};
+
+int run_encoder_blocks(mnmt_session* S, hipStream_t s, Chain* ch = nullptr) {
   const mnmt_model* m = S->m;
   const int d = m->info.d_model, h = m->info.n_heads, R = S->B * S->S;
   const int L = (int)m->enc.size();
@@ -284,7 +311,8 @@ int run_encoder_blocks(mnmt_session* S, hipStream_t s) {
       at.c_qk = Ly.sa_cqk;
       at.c_pv = Ly.sa_cpv;
       at.acc_out = acc_o[l & 1];
-      LAUNCH(launch_enc_attn(in, at, h, s));
+      const hipStream_t ks = ch ? ch->next(in.chain, 2 * l, h, 1) : s;
+      LAUNCH(launch_enc_attn(in, at, h, ks));
       std::swap(xa, xb);
     }
     {  // FFN block
@@ -299,7 +327,8 @@ int run_encoder_blocks(mnmt_session* S, hipStream_t s) {
       f.bias1 = Ly.w1.bias;
       f.W2 = Ly.w2.w;
       f.acc_out = acc_f[l & 1];
-      LAUNCH(launch_enc_ffn(in, f, s));
+      const hipStream_t ks = ch ? ch->next(in.chain, 2 * l + 1, f.F / 64, 1) : s;
+      LAUNCH(launch_enc_ffn(in, f, ks));
       std::swap(xa, xb);
     }
   }
@@ -320,7 +349,9 @@ int run_encoder_blocks(mnmt_session* S, hipStream_t s) {
     o.layer[l].bias = m->dec[l].ckv.bias;
     o.layer[l].out = S->cross_kv[l];
   }
-  LAUNCH(launch_enc_out(in, o, s));
+  // the last kernel of the chain: no flag (the caller joins the streams)
+  const hipStream_t ks = ch ? ch->next(in.chain, 0, o.layers * 2 * d / 64, 1, false) : s;
+  LAUNCH(launch_enc_out(in, o, ks));
   return MNMT_OK;
 }
 
@@ -331,8 +362,18 @@ int run_encoder(mnmt_session* S, hipStream_t s) {
   const int d = m->info.d_model, rows = S->B * S->S;
   const bool post = m->info.ln_post;
   const float eps = m->info.ln_eps;
-  if (enc_small_fits(rows, S->S, d, m->dh, m->info.d_ffn) && (int)m->dec.size() <= EncOut::kMaxLayers)
-    return run_encoder_blocks(S, s);
+  if (enc_small_fits(rows, S->S, d, m->dh, m->info.d_ffn) && (int)m->dec.size() <= EncOut::kMaxLayers) {
+    if (!S->chain_on || m->info.n_heads > kChainCopyStride || m->info.d_ffn / 64 > kChainCopyStride)
+      return run_encoder_blocks(S, s);
+    // the encoder's kernels as a chain over the two streams (see Chain)
+    MNMT_HIP(hipEventRecord(S->fork_ev, s));
+    MNMT_HIP(hipStreamWaitEvent(S->side_stream, S->fork_ev, 0));
+    Chain ch{{s, S->side_stream}, S->enc_chain, S->chain_err};
+    const int rc = run_encoder_blocks(S, s, &ch);
+    MNMT_HIP(hipEventRecord(S->join_ev, S->side_stream));
+    MNMT_HIP(hipStreamWaitEvent(s, S->join_ev, 0));
+    return rc;
+  }
   if (qgemm_small_fits(rows, d) && qgemm_small_fits(rows, m->info.d_ffn)) return run_encoder_small(S, s);
   LAUNCH(launch_embed(S->src, rows, S->S, nullptr, m->E, m->c_emb, m->pe, d, m->info.vocab, S->enc_x, s));
   const LayerDev& L0 = m->enc[0];
@@ -519,32 +560,6 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
 // The commit folds into the next step when every row's partials fit one
 // wave's four loads per lane.
 bool fold_ok(const mnmt_model* m) { return fused_slots_per_row(m->info.vocab) <= 256; }
-
-// Host state of a translation's kernel chain: kernel j runs on stream j mod 2,
-// after kernel j - 2 (stream order), and waits on the flags of kernel j - 1.
-struct Chain {
-  hipStream_t st[2];
-  unsigned* flags;
-  int* err;
-  long j = 0;  // kernels launched so far
-  int prev_slot = 0, prev_blocks = 0;
-  unsigned prev_val = 0;
-  // The chain arguments of the next kernel (flag slot, block count, the value
-  // its blocks store) and the stream it goes on.
-  hipStream_t next(StepChain& c, int slot, int blocks, unsigned val) {
-    c.wait = j > 0 ? flags + (size_t)prev_slot * kChainSlotWords : nullptr;
-    c.nwait = prev_blocks;
-    c.want = prev_val;
-    c.done = flags + (size_t)slot * kChainSlotWords;
-    c.val = val;
-    c.err = err;
-    prev_slot = slot;
-    prev_blocks = blocks;
-    prev_val = val;
-    return st[j++ & 1];
-  }
-  hipStream_t last() const { return st[(j - 1) & 1]; }
-};
 
 // Every kernel of the 1-2 row step fits the flag slots.
 bool chain_ok(const mnmt_model* m) {
@@ -823,8 +838,8 @@ int load_batch(mnmt_session* S, const int32_t* d_src, const int32_t* d_len, int 
     return set_error(MNMT_E_CAPACITY, "batch or source length exceeds the session capacity");
   S->B = B;
   S->S = S_max;
-  MNMT_HIP(hipMemcpyAsync(S->src, d_src, sizeof(int32_t) * (size_t)B * S_max, hipMemcpyDeviceToDevice, s));
-  MNMT_HIP(hipMemcpyAsync(S->len, d_len, sizeof(int32_t) * (size_t)B, hipMemcpyDeviceToDevice, s));
+  LAUNCH(launch_load_batch(d_src, d_len, S->src, S->len, B * S_max, B, S->enc_chain,
+                           2 * S->m->info.n_enc * kChainSlotWords, s));
   return MNMT_OK;
 }
 
@@ -875,6 +890,7 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->step_acc = (int32_t*)(S->fslots + 8 * (size_t)fused_slots_per_row((int)V));
   S->chain = (unsigned*)(S->step_acc + 3 * 2 * d);
   S->chain_err = (int*)at(p.chain_err);
+  S->enc_chain = (unsigned*)at(p.enc_chain);
   S->dec_a = (int8_t*)at(p.dec_a);
   S->dec_qkv = (int8_t*)at(p.dec_qkv);
   S->dec_q = (int8_t*)at(p.dec_q);
