@@ -40,7 +40,9 @@
  *   n_heads, d_ffn, n_enc, n_dec, vocab, max_pos, ln_post (0 pre-LN,
  *   1 post-LN); i32 pad_id, bos_id, eos_id, unk_id; f32 ln_eps; u32 n_tensors.
  *   n_tensors entries of 64 bytes: char name[40] (NUL padded); u32 dtype
- *   (1 int8, 2 fp32); u32 rank (1 or 2); u32 dim0; u32 dim1 (1 for rank 1);
+ *   (1 int8, 2 fp32, 3 packed 4-bit: linear weights only, dim1 a multiple of
+ *   16, dim0 * dim1 / 2 bytes); u32 rank (1 or 2); u32 dim0; u32 dim1 (1 for
+ *   rank 1);
  *   u64 offset (from file start, multiple of 256).  Tensors, d = d_model,
  *   F = d_ffn, V = vocab, P = max_pos; <e> = "enc.<l>", <t> = "dec.<l>":
  *     emb.w i8 [V,d], emb.s f32 [V] (per-row scale), pe f32 [P,d],
@@ -53,6 +55,10 @@
  *     <e|t>.ff.ln.{g,b}, .ff.w1.{w [F,d],sw,b,sin,sout [1]},
  *     .ff.w2.{w [d,F],sw,b} (input scale = ff.w1.sout), .ff.gamma.
  *   Weights are symmetric per-output-channel int8: w_real = sw[n] * w[n,k].
+ *   4-bit weights (the paper's W-E-A 4-8-8 setting) hold codes in [-7, 7]:
+ *   in each group of 16 codes of a row, byte i (i < 8) has code i + 8 in its
+ *   low nibble and code (i + 8) + 8 in its high nibble; the loader expands
+ *   them to their int8 codes, so every kernel runs on them unchanged.
  */
 #ifndef MNMT_H
 #define MNMT_H

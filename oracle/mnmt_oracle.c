@@ -32,6 +32,10 @@
  *   R6  attention scale 1/sqrt(d_head); masked keys are skipped.
  *   R7  exp/log from Cody-Waite reduction + truncated series (orc_exp/orc_log).
  *   R8  beam search rules in translate_one_beam().
+ *   R9  4-bit weights (the paper's W-E-A 4-8-8 setting, Table on quantization
+ *       bit widths): per-row symmetric codes in [-7, 7], stored packed in the
+ *       model file and unpacked here to the same int8 codes, so the integer
+ *       GEMM and everything after it are unchanged.
  */
 #include "mnmt_oracle.h"
 
@@ -294,6 +298,7 @@ int orc_log_softmax_stats(const float* z, int n, float* max_out, float* lse_out)
 
 typedef struct {
   const int8_t* w; /* [N, K] */
+  int8_t* w_own;   /* unpacked 4-bit weights (owned), else NULL */
   int N, K;
   const float* s_w;
   const float* b;
@@ -349,7 +354,8 @@ static uint32_t rd_u32(const unsigned char* p) {
   return v;
 }
 
-/* Look up a tensor by name; check dtype (1 int8, 2 fp32) and shape. */
+/* Look up a tensor by name; check dtype (1 int8, 2 fp32, 3 packed 4-bit)
+ * and shape. */
 static const void* find_tensor(const orc_model* m, const char* name, uint32_t dtype, uint32_t d0,
                                uint32_t d1) {
   for (int i = 0; i < m->n_tensors; ++i) {
@@ -362,7 +368,8 @@ static const void* find_tensor(const orc_model* m, const char* name, uint32_t dt
     uint64_t off;
     memcpy(&off, e + 56, 8);
     if (dt != dtype || a != d0 || b != d1) return NULL;
-    uint64_t bytes = (uint64_t)a * b * (dtype == 1 ? 1u : 4u);
+    if (dtype == 3 && b % 16 != 0) return NULL;
+    uint64_t bytes = dtype == 3 ? (uint64_t)a * b / 2 : (uint64_t)a * b * (dtype == 1 ? 1u : 4u);
     if (off % 256 != 0 || off + bytes > m->nbytes) return NULL;
     return m->blob + off;
   }
@@ -386,6 +393,23 @@ static int load_linear(orc_model* m, linear_t* L, const char* pfx, int N, int K,
   L->K = K;
   snprintf(nm, sizeof nm, "%s.w", pfx);
   L->w = (const int8_t*)find_tensor(m, nm, 1, (uint32_t)N, (uint32_t)K);
+  if (!L->w) {
+    /* 4-bit: in each group of 16 codes of a row, byte i (i < 8) holds code i
+     * in its low nibble and code i + 8 in its high nibble, each plus 8 */
+    const unsigned char* p = (const unsigned char*)find_tensor(m, nm, 3, (uint32_t)N, (uint32_t)K);
+    if (p) {
+      L->w_own = (int8_t*)malloc((size_t)N * K);
+      if (!L->w_own) return ORC_E_NOMEM;
+      for (size_t r = 0; r < (size_t)N; ++r)
+        for (int g = 0; g < K / 16; ++g)
+          for (int i = 0; i < 8; ++i) {
+            const unsigned char byte = p[r * (size_t)K / 2 + (size_t)g * 8 + i];
+            L->w_own[r * K + 16 * g + i] = (int8_t)((int)(byte & 15) - 8);
+            L->w_own[r * K + 16 * g + 8 + i] = (int8_t)((int)(byte >> 4) - 8);
+          }
+      L->w = L->w_own;
+    }
+  }
   snprintf(nm, sizeof nm, "%s.sw", pfx);
   L->s_w = (const float*)find_tensor(m, nm, 2, (uint32_t)N, 1);
   snprintf(nm, sizeof nm, "%s.b", pfx);
@@ -499,6 +523,7 @@ static int load_layer(orc_model* m, layer_t* L, const char* side, int l, int is_
 static void free_linear(linear_t* L) {
   free(L->scale);
   free(L->bias);
+  free(L->w_own);
 }
 
 void orc_model_free(orc_model* m) {

@@ -19,7 +19,7 @@
 namespace mnmt {
 namespace {
 
-constexpr uint32_t kI8 = 1, kF32 = 2;
+constexpr uint32_t kI8 = 1, kF32 = 2, kI4 = 3;  // kI4: packed 4-bit weight codes
 
 struct Entry {
   uint32_t dtype, rank, d0, d1;
@@ -97,18 +97,42 @@ float rd_f(const float* p, size_t i) {
   return v;
 }
 
-// Copy an int8 weight and compute its folded constants into the image.
+// Copy an int8 weight (4-bit weights: their int8 codes) and compute its
+// folded constants into the image.
 bool add_linear(Parser& P, Image& img, LinearDev& L, const std::string& pfx, int N, int K, float s_in,
                 const float* s_out, int n_blocks) {
-  const int8_t* w = P.i8(pfx + ".w", (uint32_t)N, (uint32_t)K);
+  auto it = P.t.find(pfx + ".w");
+  const bool four = it != P.t.end() && it->second.dtype == kI4;
+  const int8_t* w = four ? nullptr : P.i8(pfx + ".w", (uint32_t)N, (uint32_t)K);
+  const uint8_t* w4 = nullptr;
+  if (four) {
+    if (it->second.d0 != (uint32_t)N || it->second.d1 != (uint32_t)K) {
+      P.err = "tensor " + pfx + ".w has the wrong shape";
+      return false;
+    }
+    w4 = P.blob + it->second.off;
+  }
   const float* sw = P.f32(pfx + ".sw", (uint32_t)N);
   const float* b = P.f32(pfx + ".b", (uint32_t)N);
-  if (!w || !sw || !b) return false;
+  if ((!w && !w4) || !sw || !b) return false;
   L.N = N;
   L.K = K;
   L.inv_in = (float)(1.0 / (double)s_in);
   const size_t ow = img.alloc((size_t)N * K);
-  std::memcpy(img.buf.data() + ow, w, (size_t)N * K);
+  int8_t* dst = reinterpret_cast<int8_t*>(img.buf.data() + ow);
+  if (four) {
+    // in each group of 16 codes of a row, byte i (i < 8) holds code i in its
+    // low nibble and code i + 8 in its high nibble, each plus 8
+    for (size_t r = 0; r < (size_t)N; ++r)
+      for (int g = 0; g < K / 16; ++g)
+        for (int i = 0; i < 8; ++i) {
+          const uint8_t byte = w4[r * (size_t)K / 2 + (size_t)g * 8 + i];
+          dst[r * K + 16 * g + i] = (int8_t)((int)(byte & 15) - 8);
+          dst[r * K + 16 * g + 8 + i] = (int8_t)((int)(byte >> 4) - 8);
+        }
+  } else {
+    std::memcpy(dst, w, (size_t)N * K);
+  }
   const size_t os = img.alloc(sizeof(float) * N), ob = img.alloc(sizeof(float) * N);
   float* sc = reinterpret_cast<float*>(img.buf.data() + os);
   float* bi = reinterpret_cast<float*>(img.buf.data() + ob);
@@ -245,8 +269,9 @@ int build_model(const void* blob, size_t n, mnmt_model& m, Image*& out_img, std:
     name[40] = 0;
     Entry en{rd32(e + 40), rd32(e + 44), rd32(e + 48), rd32(e + 52), 0};
     std::memcpy(&en.off, e + 56, 8);
-    const uint64_t bytes = (uint64_t)en.d0 * en.d1 * (en.dtype == kI8 ? 1 : 4);
-    if ((en.dtype != kI8 && en.dtype != kF32) || en.off % 256 || en.off + bytes > n || en.off < 64 + (uint64_t)nt * 64) {
+    const uint64_t bytes = en.dtype == kI4 ? (uint64_t)en.d0 * en.d1 / 2 : (uint64_t)en.d0 * en.d1 * (en.dtype == kI8 ? 1 : 4);
+    if ((en.dtype != kI8 && en.dtype != kF32 && en.dtype != kI4) || (en.dtype == kI4 && en.d1 % 16) ||
+        en.off % 256 || en.off + bytes > n || en.off < 64 + (uint64_t)nt * 64) {
       err = std::string("tensor ") + name + " has an invalid dtype or lies outside the file";
       return MNMT_E_BAD_MODEL;
     }

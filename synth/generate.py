@@ -28,7 +28,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .modelfile import Header, write_model
+from .modelfile import Header, Int4Rows, write_model
 
 WEIGHT_STD = 0.02
 SPECIAL = 4  # ids 0..3 are PAD, BOS, EOS, UNK
@@ -51,6 +51,7 @@ class ModelConfig:
     gamma_range: tuple = (0.5, 1.5)
     weight_std: float = WEIGHT_STD
     emb_distinct: int = 0  # > 0: embedding row v repeats drawn row v mod emb_distinct (groups of equal logits)
+    w_bits: int = 8  # 4: linear weights as 4-bit codes (the paper's W-E-A 4-8-8; the embedding stays 8-bit)
 
 
 # The model shapes of the five workloads.
@@ -62,11 +63,12 @@ PAPER_10MB = ModelConfig("mobilenmt-10mb", 256, 4, 512, 12, 2, 8000, ln_post=0, 
 PAPER_20MB = ModelConfig("mobilenmt-20mb", 384, 6, 768, 12, 2, 8000, ln_post=0, seed=1020)
 
 
-def _quantize_rows(w: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
-    """Per-row symmetric int8 codes and float32 scales (offline preparation)."""
+def _quantize_rows(w: np.ndarray, qmax: int = 127) -> tuple[np.ndarray, np.ndarray]:
+    """Per-row symmetric codes in [-qmax, qmax] and float32 scales (offline
+    preparation): 127 for 8-bit, 7 for 4-bit weights."""
     amax = np.abs(w).max(axis=1)
-    s = np.where(amax > 0, amax / 127.0, 1.0)
-    codes = np.clip(np.rint(w / s[:, None]), -127, 127).astype(np.int8)
+    s = np.where(amax > 0, amax / float(qmax), 1.0)
+    codes = np.clip(np.rint(w / s[:, None]), -qmax, qmax).astype(np.int8)
     return codes, s.astype(np.float32)
 
 
@@ -98,8 +100,8 @@ def build_model(cfg: ModelConfig) -> bytes:
 
     def linear(pfx, n_out, n_in, s_in=None, s_out=None):
         w = rng.normal(0.0, wstd, size=(n_out, n_in))
-        codes, sw = _quantize_rows(w)
-        t[pfx + ".w"] = codes
+        codes, sw = _quantize_rows(w, 7 if cfg.w_bits == 4 else 127)
+        t[pfx + ".w"] = Int4Rows(codes) if cfg.w_bits == 4 else codes
         t[pfx + ".sw"] = sw
         t[pfx + ".b"] = f32(rng.normal(0.0, WEIGHT_STD, size=n_out))
         if s_in is not None:

@@ -8,8 +8,11 @@ inference arithmetic.
 Header (little endian): magic "MNMT", u32 version=1, u32 d_model, n_heads,
 d_ffn, n_enc, n_dec, vocab, max_pos, ln_post; i32 pad, bos, eos, unk;
 f32 ln_eps; u32 n_tensors.
-Entry: char name[40], u32 dtype (1 int8, 2 fp32), u32 rank, u32 dim0,
-u32 dim1, u64 offset.
+Entry: char name[40], u32 dtype (1 int8, 2 fp32, 3 packed 4-bit), u32 rank,
+u32 dim0, u32 dim1, u64 offset.  A packed 4-bit tensor [dim0, dim1] (dim1 a
+multiple of 16) holds codes in [-7, 7] as nibbles u = code + 8, dim0 * dim1 / 2
+bytes: in each group of 16 codes of a row, byte i (i < 8) holds code i in its
+low nibble and code i + 8 in its high nibble.
 """
 from __future__ import annotations
 
@@ -26,6 +29,30 @@ ALIGN = 256
 
 DT_I8 = 1
 DT_F32 = 2
+DT_I4 = 3
+
+
+class Int4Rows:
+    """int8 codes in [-7, 7] of a [rows, K] weight, to be stored packed (DT_I4)."""
+
+    def __init__(self, codes: np.ndarray):
+        codes = np.asarray(codes)
+        if codes.ndim != 2 or codes.shape[1] % 16 or codes.min() < -7 or codes.max() > 7:
+            raise ValueError("4-bit weights: [rows, K] codes in [-7, 7], K a multiple of 16")
+        self.codes = codes.astype(np.int8)
+
+
+def pack_int4(codes: np.ndarray) -> bytes:
+    """The DT_I4 payload of codes [rows, K]."""
+    u = (codes.astype(np.int16) + 8).astype(np.uint8).reshape(codes.shape[0], -1, 2, 8)
+    return (u[:, :, 0, :] | (u[:, :, 1, :] << 4)).astype(np.uint8).tobytes()
+
+
+def unpack_int4(data, rows: int, k: int) -> np.ndarray:
+    """Codes [rows, k] (int8) of a DT_I4 payload."""
+    b = np.frombuffer(data, dtype=np.uint8, count=rows * k // 2).reshape(rows, k // 16, 8)
+    u = np.stack([b & 15, b >> 4], axis=2).reshape(rows, k).astype(np.int16)
+    return (u - 8).astype(np.int8)
 
 
 @dataclass
@@ -54,6 +81,16 @@ def write_model(header: Header, tensors: dict[str, np.ndarray]) -> bytes:
     entries = []
     payload = []
     for name in names:
+        if isinstance(tensors[name], Int4Rows):
+            codes = tensors[name].codes
+            nb = name.encode()
+            if len(nb) >= 40:
+                raise ValueError(f"name too long: {name}")
+            data = pack_int4(codes)
+            entries.append(struct.pack(ENTRY_FMT, nb, DT_I4, 2, codes.shape[0], codes.shape[1], off))
+            payload.append((off, data))
+            off += (len(data) + ALIGN - 1) // ALIGN * ALIGN
+            continue
         a = np.ascontiguousarray(tensors[name])
         if a.dtype == np.int8:
             dt = DT_I8
@@ -94,6 +131,9 @@ def read_model(blob: bytes) -> tuple[Header, dict[str, np.ndarray]]:
     for i in range(f[15]):
         name, dt, rank, d0, d1, off = struct.unpack_from(ENTRY_FMT, blob, 64 + 64 * i)
         name = name.rstrip(b"\0").decode()
+        if dt == DT_I4:  # unpacked to int8 codes
+            out[name] = unpack_int4(blob[off: off + d0 * d1 // 2], d0, d1)
+            continue
         dtype = np.int8 if dt == DT_I8 else np.float32
         a = np.frombuffer(blob, dtype=dtype, count=d0 * d1, offset=off)
         out[name] = a.reshape(d0, d1) if rank == 2 else a

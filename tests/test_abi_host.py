@@ -45,6 +45,20 @@ def test_model_bytes_accepts_the_generated_models():
         assert weights < n < 2 * len(blob)
 
 
+def test_model_bytes_of_4bit_weights_equals_their_int8_form():
+    """4-bit weights (packed in the file) are expanded to their int8 codes on
+    the device: the arena size equals that of the same codes stored as int8."""
+    import dataclasses
+
+    from synth import generate as G
+
+    blob4 = G.build_model(dataclasses.replace(G.TINY, name="tiny-w4", w_bits=4))
+    hdr, t = read_model(blob4)
+    blob8 = write_model(hdr, {k: np.ascontiguousarray(v) for k, v in t.items()})
+    assert len(blob4) < len(blob8)
+    assert mnmt.mnmt_model_bytes(blob4) == mnmt.mnmt_model_bytes(blob8)
+
+
 def test_model_bytes_rejects_bad_files():
     blob = model_blob("TINY")
     with pytest.raises(mnmt.MnmtError) as e:

@@ -246,6 +246,24 @@ def test_beam_tied_logits(torch_dev):
             _beam_check(torch, dev, cfg, src, lens, W, 6, 0.6)
 
 
+def test_4bit_weight_models(torch_dev):
+    """The paper's W-E-A 4-8-8 setting (4-bit linear weights, 8-bit embedding
+    and activations): batch-1 greedy on the mobile shape and on a small model,
+    batched greedy and beam search on the small one, all against the oracle."""
+    import dataclasses
+
+    torch, dev = torch_dev
+    mob4 = dataclasses.replace(G.MOBILE, name="mobile-w4", w_bits=4)
+    src, lens = G.workload_inputs(G.WORKLOADS["mobile"])
+    _greedy_check(torch, dev, mob4, src, lens, 30)
+    div4 = dataclasses.replace(DIVERSE, name="diverse-w4", w_bits=4)
+    src, lens = G.make_sources(div4.vocab, 1, [9], seed=31, s_max=9)
+    _greedy_check(torch, dev, div4, src, lens, 10)
+    src, lens = G.make_sources(div4.vocab, 3, [9, 5, 7], seed=31, s_max=9)
+    _greedy_check(torch, dev, div4, src, lens, 10)
+    _beam_check(torch, dev, div4, src, lens, 2, 8, 0.6)
+
+
 def test_mobile_beam_workload_sampled(torch_dev):
     torch, dev = torch_dev
     w = G.WORKLOADS["mobile_beam"]

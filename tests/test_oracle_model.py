@@ -197,3 +197,42 @@ def test_activation_statistics_are_not_degenerate():
             assert (np.abs(codes) == 127).mean() < 0.01
             assert (codes == 0).mean() < 0.5
             assert codes.std() > 5
+
+
+def test_4bit_weights_quantizer_and_packing():
+    """The paper's W-E-A 4-8-8 setting: per-row symmetric 4-bit codes in
+    [-7, 7] with s = max|w| / 7, stored packed two codes per byte.  The
+    quantizer reproduces each weight within half a step, the extreme of every
+    row maps to +-7, and the packing round-trips."""
+    from synth.generate import _quantize_rows
+    from synth.modelfile import pack_int4, unpack_int4
+
+    rng = np.random.default_rng(41)
+    w = rng.normal(0.0, 0.02, size=(48, 64))
+    codes, s = _quantize_rows(w, 7)
+    assert codes.min() >= -7 and codes.max() <= 7
+    assert np.all(np.abs(codes).max(axis=1) == 7)
+    assert np.all(np.abs(codes * s[:, None].astype(np.float64) - w) <= s[:, None] / 2 * (1 + 1e-6))
+    assert np.array_equal(unpack_int4(pack_int4(codes), 48, 64), codes)
+    # the byte layout: byte i of a 16-code group holds codes i and i + 8, plus 8
+    one = np.arange(-7, 9, dtype=np.int8)[None, :16].clip(-7, 7)
+    packed = np.frombuffer(pack_int4(one), np.uint8)
+    assert [int(b) for b in packed] == [int(one[0, i] + 8) | (int(one[0, i + 8] + 8) << 4) for i in range(8)]
+
+
+def test_4bit_model_equals_its_int8_form():
+    """A model stored with 4-bit weights translates exactly as the same codes
+    stored as int8 (the oracle unpacks; nothing after the GEMM changes)."""
+    import dataclasses
+
+    from synth.modelfile import read_model, write_model
+
+    cfg = dataclasses.replace(G.TINY, name="tiny-w4", w_bits=4, seed=1101)
+    blob4 = G.build_model(cfg)
+    hdr, t = read_model(blob4)
+    blob8 = write_model(hdr, {k: np.ascontiguousarray(v) for k, v in t.items()})
+    src, lens = G.make_sources(cfg.vocab, 2, [9, 5], seed=7, s_max=9)
+    a = oracle.Model(blob4).greedy(src, lens, 10, want_logits=True)
+    b = oracle.Model(blob8).greedy(src, lens, 10, want_logits=True)
+    assert np.array_equal(a[0], b[0])
+    assert np.array_equal(a[2].view(np.uint32), b[2].view(np.uint32))
