@@ -56,9 +56,10 @@
  *     .ff.w2.{w [d,F],sw,b} (input scale = ff.w1.sout), .ff.gamma.
  *   Weights are symmetric per-output-channel int8: w_real = sw[n] * w[n,k].
  *   4-bit weights (the paper's W-E-A 4-8-8 setting) hold codes in [-7, 7]:
- *   in each group of 16 codes of a row, byte i (i < 8) has code i + 8 in its
- *   low nibble and code (i + 8) + 8 in its high nibble; the loader expands
- *   them to their int8 codes, so every kernel runs on them unchanged.
+ *   in each group of 16 codes of a row, byte i (i < 8) holds code i in its
+ *   low nibble and code i + 8 in its high nibble, each stored plus 8; the
+ *   loader expands them to their int8 codes, so every kernel runs on them
+ *   unchanged.
  */
 #ifndef MNMT_H
 #define MNMT_H
