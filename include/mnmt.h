@@ -95,6 +95,10 @@ extern "C" {
  *                       (plain stores, no zero-fill needed); the row's arg-max
  *                       key is the largest of its P entries (M <= 2, K <= 512,
  *                       as the decoder's batch-1 step writes it).
+ *   MNMT_EPI_ARGMAX_PARTIAL_PACKED: MNMT_EPI_ARGMAX_PARTIAL with d_W the
+ *                       fragment-order copy that mnmt_pack_weights writes
+ *                       (the layout the batch-1 decoder reads its tied
+ *                       output embedding in); same keys, same P.
  * acc = sum_k X[m,k] W[n,k] in int32, converted to fp32 with round-to-nearest-even. */
 #define MNMT_EPI_I32 0
 #define MNMT_EPI_I8 1
@@ -104,6 +108,7 @@ extern "C" {
 #define MNMT_EPI_LOGITS 5
 #define MNMT_EPI_ARGMAX 6
 #define MNMT_EPI_ARGMAX_PARTIAL 7
+#define MNMT_EPI_ARGMAX_PARTIAL_PACKED 8
 
 typedef struct mnmt_model mnmt_model;
 typedef struct mnmt_session mnmt_session;
@@ -205,6 +210,22 @@ int mnmt_qlinear(const int8_t* d_X, const int8_t* d_W, const float* d_scale, con
 /* Number of partial keys per row that MNMT_EPI_ARGMAX_PARTIAL writes for N
  * outputs (one per 128 outputs), or -1 for N < 1. */
 int mnmt_argmax_partials(int N);
+
+/* Bytes of the fragment-order copy of an int8 weight [N, K]:
+ * ceil(N / 16) * 16 * K, or 0 unless N >= 1 and K is a positive multiple of 64. */
+size_t mnmt_packed_bytes(int N, int K);
+
+/* Reorder d_W int8 [N, K] row-major (16-byte aligned, K a multiple of 64) into
+ * d_P (mnmt_packed_bytes(N, K) bytes, 16-byte aligned, caller-owned, not
+ * overlapping d_W), asynchronously on the stream: for tile t of 16 rows and
+ * slice j of 64 columns one contiguous kilobyte at offset (t * K/64 + j) * 1024
+ * whose 16-byte chunk l holds W[16t + l % 16, 64j + 16(l / 16) .. +15] (zeros
+ * for rows >= N) -- the operand each lane of an i8 16x16x64 matrix-core
+ * instruction takes, so the logits kernel reads each kilobyte with one
+ * coalesced load per wave.  This is a memory layout, not a change of the
+ * arithmetic: MNMT_EPI_ARGMAX_PARTIAL_PACKED on d_P gives the keys that
+ * MNMT_EPI_ARGMAX_PARTIAL gives on d_W. */
+int mnmt_pack_weights(const int8_t* d_W, int N, int K, int8_t* d_P, void* stream);
 
 /* mnmt_qlinear with timing events (hipEvent_t, created with timing enabled,
  * or NULL).  On the fused arg-max path (MNMT_EPI_ARGMAX or

@@ -75,15 +75,16 @@ extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const fl
                                   void* ev_start, void* ev_stop) {
   if (M < 0 || N < 1 || K < 64 || K % 64 || K > 8192)
     return set_error(MNMT_E_INVALID_ARG, "need M >= 0, N >= 1 and K a multiple of 64 in [64, 8192]");
-  if (epilogue < MNMT_EPI_I32 || epilogue > MNMT_EPI_ARGMAX_PARTIAL)
+  if (epilogue < MNMT_EPI_I32 || epilogue > MNMT_EPI_ARGMAX_PARTIAL_PACKED)
     return set_error(MNMT_E_INVALID_ARG, "unknown epilogue");
-  if (epilogue == MNMT_EPI_ARGMAX_PARTIAL && !step_logits_fits(M == 0 ? 1 : M, K))
+  const bool packed = epilogue == MNMT_EPI_ARGMAX_PARTIAL_PACKED;
+  if ((epilogue == MNMT_EPI_ARGMAX_PARTIAL || packed) && !step_logits_fits(M == 0 ? 1 : M, K))
     return set_error(MNMT_E_UNSUPPORTED, "the partial arg-max epilogue takes M <= 2 and K a multiple of 64 up to 512");
   if (epilogue == MNMT_EPI_ARGMAX && M > 8)
     return set_error(MNMT_E_UNSUPPORTED, "the fused arg-max epilogue takes at most 8 rows");
   if (M == 0) return MNMT_OK;
   const bool needs_scale = epilogue != MNMT_EPI_I32;
-  const bool argmax = epilogue == MNMT_EPI_ARGMAX || epilogue == MNMT_EPI_ARGMAX_PARTIAL;
+  const bool argmax = epilogue == MNMT_EPI_ARGMAX || epilogue == MNMT_EPI_ARGMAX_PARTIAL || packed;
   const bool needs_bias = epilogue != MNMT_EPI_I32 && epilogue != MNMT_EPI_LOGITS && !argmax;
   if (!d_X || !d_W || !d_Y || (needs_scale && !d_scale) || (needs_bias && !d_bias))
     return set_error(MNMT_E_INVALID_ARG, "null device pointer");
@@ -97,6 +98,7 @@ extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const fl
     g.d = K;
     g.V = N;
     g.E = static_cast<const int8_t*>(d_W);
+    g.frag = packed;
     g.c_out = d_scale;
     g.slots = static_cast<unsigned long long*>(d_Y);
     g.nslots = epilogue == MNMT_EPI_ARGMAX ? 1 : step_logits_blocks(N);
@@ -117,6 +119,17 @@ extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const fl
 }
 
 extern "C" int mnmt_argmax_partials(int N) { return N < 1 ? -1 : step_logits_blocks(N); }
+
+extern "C" size_t mnmt_packed_bytes(int N, int K) { return frag_bytes(N, K); }
+
+extern "C" int mnmt_pack_weights(const int8_t* d_W, int N, int K, int8_t* d_P, void* stream) {
+  if (!frag_bytes(N, K)) return set_error(MNMT_E_INVALID_ARG, "need N >= 1 and K a positive multiple of 64");
+  if (!d_W || !d_P) return set_error(MNMT_E_INVALID_ARG, "null device pointer");
+  if (reinterpret_cast<uintptr_t>(d_W) % 16 || reinterpret_cast<uintptr_t>(d_P) % 16)
+    return set_error(MNMT_E_INVALID_ARG, "W and P must be 16-byte aligned");
+  const hipError_t h = launch_pack_fragments(d_W, N, K, d_P, static_cast<hipStream_t>(stream));
+  return h == hipSuccess ? MNMT_OK : hip_error(h, "pack launch");
+}
 
 extern "C" int mnmt_fold_requant(float s_in, const float* s_w, const float* b, float s_out, int N, float* scale,
                                  float* bias) {

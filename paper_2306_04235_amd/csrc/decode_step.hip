@@ -432,11 +432,14 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
 // wave takes TPW tiles of 16 vocabulary rows (kLogitsTiles alone, more in a
 // kernel chain, where the weights load while the previous kernel runs and
 // fewer blocks mean fewer flags to store and to wait for).  RAW: the rows are
-// int8 codes already (g.x_i8) instead of the residual stream.
+// int8 codes already (g.x_i8) instead of the residual stream.  FRAG: the
+// embedding in fragment order (launch_pack_fragments), so that each of a
+// wave's weight loads reads one contiguous kilobyte; row-major, each load
+// gathers 64-byte pieces of 16 rows.
 constexpr int kLogitsTiles = 2;
 // in a chain: 4 tiles per wave once that still leaves about 100 blocks
 __host__ inline int chain_logits_tiles(int V) { return V >= 4 * 4 * 16 * 96 ? 4 : kLogitsTiles; }
-template <int DMAX, bool RAW, int TPW>
+template <int DMAX, bool RAW, int TPW, bool FRAG>
 __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLogits g) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;
@@ -453,8 +456,12 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     const size_t n = (size_t)min(row0 + 16 * t + l16, N - 1);
+    const size_t tile = (size_t)min(row0 / 16 + t, (N - 1) / 16);
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) wf[t][kk] = *(const v4i*)(g.E + n * d + 64 * min(kk, ks - 1) + 16 * kq);
+    for (int kk = 0; kk < KS; ++kk) {
+      if (FRAG) wf[t][kk] = *(const v4i*)(g.E + ((tile * KS + kk) * 64 + lane) * 16);
+      else wf[t][kk] = *(const v4i*)(g.E + n * d + 64 * min(kk, ks - 1) + 16 * kq);
+    }
     co[t] = g.c_out[n];
   }
   RowRegs<NJ> rr;
@@ -596,18 +603,27 @@ hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t
   const int blocks = step_logits_blocks(g.V);
   const int cblocks = step_logits_blocks_chained(g.V, g.d);
   if (in.chain.done && g.nslots < cblocks) return hipErrorInvalidValue;
-#define MNMT_LOGITS(DM)                                                                                       \
-  if (g.x_i8 && (ev_start || ev_stop))                                                                        \
-    hipExtLaunchKernelGGL((k_step_logits<DM, true, kLogitsTiles>), dim3(blocks), dim3(kStepThreads), 0, s,    \
-                          ev_start, ev_stop, 0, in, g);                                                       \
-  else if (g.x_i8)                                                                                            \
-    hipLaunchKernelGGL((k_step_logits<DM, true, kLogitsTiles>), dim3(blocks), dim3(kStepThreads), 0, s, in, g); \
-  else if (in.chain.done && chain_logits_tiles(g.V) == 4)                                                    \
-    hipLaunchKernelGGL((k_step_logits<DM, false, 4>), dim3(cblocks), dim3(kStepThreads), 0, s, in, g);        \
-  else                                                                                                        \
-    hipLaunchKernelGGL((k_step_logits<DM, false, kLogitsTiles>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);
+  if (!g.x_i8 && !g.frag) return hipErrorInvalidValue;  // the decoder reads the fragment-order copy
+#define MNMT_RAW(DM, FR)                                                                                          \
+  if (ev_start || ev_stop)                                                                                        \
+    hipExtLaunchKernelGGL((k_step_logits<DM, true, kLogitsTiles, FR>), dim3(blocks), dim3(kStepThreads), 0, s,    \
+                          ev_start, ev_stop, 0, in, g);                                                           \
+  else                                                                                                            \
+    hipLaunchKernelGGL((k_step_logits<DM, true, kLogitsTiles, FR>), dim3(blocks), dim3(kStepThreads), 0, s, in, g);
+#define MNMT_LOGITS(DM)                                                                                         \
+  if (g.x_i8 && g.frag) {                                                                                       \
+    MNMT_RAW(DM, true)                                                                                          \
+  } else if (g.x_i8) {                                                                                          \
+    MNMT_RAW(DM, false)                                                                                         \
+  } else if (in.chain.done && chain_logits_tiles(g.V) == 4) {                                                   \
+    hipLaunchKernelGGL((k_step_logits<DM, false, 4, true>), dim3(cblocks), dim3(kStepThreads), 0, s, in, g);    \
+  } else {                                                                                                      \
+    hipLaunchKernelGGL((k_step_logits<DM, false, kLogitsTiles, true>), dim3(blocks), dim3(kStepThreads), 0, s, in, \
+                       g);                                                                                      \
+  }
   MNMT_BY_D(g.d, MNMT_LOGITS)
 #undef MNMT_LOGITS
+#undef MNMT_RAW
   return hipGetLastError();
 }
 

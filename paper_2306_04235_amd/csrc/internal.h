@@ -86,6 +86,13 @@ hipError_t launch_row_argmax(const float* z, int R, int V, unsigned long long* s
 hipError_t launch_load_batch(const int32_t* src_in, const int32_t* len_in, int32_t* src, int32_t* len, int n_src,
                              int n_len, unsigned* zero, int n_zero, hipStream_t s);
 hipError_t launch_copy_i32(const int32_t* src, int32_t* dst, int n, hipStream_t s);
+// Fragment order of an int8 weight [N, K] (K a multiple of 64) for the batch-1
+// logits kernel: per tile t of 16 rows and slice j of 64 columns, one
+// contiguous kilobyte whose 16-byte chunk l holds row 16t + l % 16, columns
+// 64j + 16(l / 16) .. +15 (the i8 16x16x64 MFMA operand of lane l); rows past
+// N are zero.  frag_bytes = ceil(N / 16) * 16 * K (0 for bad sizes).
+size_t frag_bytes(int N, int K);
+hipError_t launch_pack_fragments(const int8_t* W, int N, int K, int8_t* out, hipStream_t s);
 
 // Fused decoder step for up to 8 rows (decode_fused.hip).
 struct FusedIn {           // how a kernel obtains its int8 input rows
@@ -225,6 +232,7 @@ struct StepLogits {
   unsigned long long* slots;
   int nslots;
   const int8_t* x_i8;      // int8 rows [R, d] instead of the StepIn rows (or null)
+  bool frag;               // E in fragment order (launch_pack_fragments), else row-major [V, d]
 };
 bool step_path_fits(int R, int d, int dh, int F, int T, int S);
 bool step_logits_fits(int R, int d);  // R <= 2, d a multiple of 64 up to 512
@@ -375,6 +383,7 @@ struct mnmt_model {
   int device = 0;
   size_t arena_bytes = 0;
   const int8_t* E = nullptr;     // [V, d]
+  const int8_t* E_frag = nullptr;  // E in fragment order, frag_bytes(V, d) (the batch-1 logits)
   const float* c_emb = nullptr;  // [V]
   const float* c_out = nullptr;  // [V]
   const float* pe = nullptr;     // [P, d]

@@ -220,6 +220,21 @@ __global__ void k_copy_i32(const int32_t* src, int32_t* dst, int n) {
   if (i < n) dst[i] = src[i];
 }
 
+// Fragment order (see frag_bytes): output chunk c of 16 bytes is lane
+// l = c % 64 of slice j = (c / 64) % (K / 64) of tile t = c / (64 * K / 64),
+// i.e. row 16t + l % 16, columns 64j + 16(l / 16) .. +15; rows past N are zero.
+__global__ __launch_bounds__(256) void k_pack_fragments(const int8_t* __restrict__ W, int N, int K, size_t chunks,
+                                                        int8_t* __restrict__ out) {
+  const size_t c = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= chunks) return;
+  const int ks = K / 64, lane = (int)(c % 64);
+  const size_t j = (c / 64) % ks, t = c / (64 * (size_t)ks);
+  const size_t row = 16 * t + (lane & 15);
+  int4 v = {0, 0, 0, 0};
+  if (row < (size_t)N) v = *(const int4*)(W + row * K + 64 * j + 16 * (lane >> 4));
+  *(int4*)(out + 16 * c) = v;
+}
+
 // ---------------------------------------------------------------------------
 // Beam search.  Rows r = b * W + j hold the W hypotheses of sentence b.
 
@@ -768,6 +783,17 @@ hipError_t launch_load_batch(const int32_t* src_in, const int32_t* len_in, int32
   const int n = max(max(n_src, n_len), n_zero);
   const int blocks = min(256, max(1, (n + 255) / 256));
   hipLaunchKernelGGL(k_load_batch, dim3(blocks), dim3(256), 0, s, src_in, len_in, src, len, n_src, n_len, zero, n_zero);
+  return hipGetLastError();
+}
+
+size_t frag_bytes(int N, int K) { return N < 1 || K < 64 || K % 64 ? 0 : (size_t)((N + 15) / 16) * 16 * K; }
+
+hipError_t launch_pack_fragments(const int8_t* W, int N, int K, int8_t* out, hipStream_t s) {
+  const size_t bytes = frag_bytes(N, K);
+  if (!bytes || !W || !out || reinterpret_cast<uintptr_t>(W) % 16 || reinterpret_cast<uintptr_t>(out) % 16)
+    return hipErrorInvalidValue;
+  const size_t chunks = bytes / 16;
+  hipLaunchKernelGGL(k_pack_fragments, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, W, N, K, chunks, out);
   return hipGetLastError();
 }
 

@@ -308,7 +308,9 @@ int build_model(const void* blob, size_t n, mnmt_model& m, Image*& out_img, std:
       }
       const size_t op = img->alloc(sizeof(float) * (size_t)Pn * d);
       std::memcpy(img->buf.data() + op, pe, sizeof(float) * (size_t)Pn * d);
+      const size_t of = img->alloc(frag_bytes(V, d));  // written on the device after the upload
       img->bind(&m.E, oE);
+      img->bind(&m.E_frag, of);
       img->bind(&m.c_emb, oc);
       img->bind(&m.c_out, oo);
       img->bind(&m.pe, op);
@@ -343,6 +345,8 @@ int finish_model(Image* img, mnmt_model& m, void* d_arena, size_t arena_bytes, h
   uint8_t* base = static_cast<uint8_t*>(d_arena);
   for (auto& f : img->fix) *f.first = base + f.second;
   hipError_t e = hipMemcpyAsync(d_arena, img->buf.data(), img->buf.size(), hipMemcpyHostToDevice, s);
+  if (e == hipSuccess)
+    e = launch_pack_fragments(m.E, m.info.vocab, m.info.d_model, const_cast<int8_t*>(m.E_frag), s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) {
     err = std::string("model upload failed: ") + hipGetErrorString(e);

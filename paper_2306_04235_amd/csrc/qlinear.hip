@@ -216,9 +216,20 @@ __global__ __launch_bounds__(256) void k_qgemm_small(FusedIn in, const int8_t* _
 
 bool qgemm_small_fits(int M, int K) { return M >= 1 && M <= 64 && K <= kSmallMaxK && K % 64 == 0; }
 
+// Up to 256 rows and N <= 1024 the one-round-trip kernel (every
+// block loads its weight fragments for all of K at once) also beats the
+// LDS-slab GEMM, whose 64x64 tiles leave such shapes with a few dozen blocks
+// (the batched decoder's projections and feed-forward layers).  At 512 rows
+// or N = 2048 the repeated weight loads make it the slower of the two.
+constexpr int kSmallMaxRows = 256;
+bool qgemm_rows_fit(int M, int K, int N) {
+  return M >= 1 && M <= kSmallMaxRows && N <= 1024 && K <= kSmallMaxK && K % 64 == 0;
+}
+
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
                               const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s) {
-  if (!qgemm_small_fits(M, K) || (in && K > kMaxRowLen)) return hipErrorInvalidValue;
+  if (M < 1 || M > (in ? 64 : kSmallMaxRows) || K > kSmallMaxK || K % 64 || (in && K > kMaxRowLen))
+    return hipErrorInvalidValue;
   dim3 grid((N + 31) / 32, (M + 31) / 32);
   const FusedIn none{};
 #define MNMT_SMALL(KM)                                                                                      \
@@ -248,7 +259,8 @@ hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float
     return gemv_lpr<8>(X, ldx, W, scale, bias, M, K, N, e, s);
   }
   if (e.kind == EPI_LOGITS_ARGMAX) return hipErrorInvalidValue;  // arg-max fusion is a batch-1 path
-  if (qgemm_small_fits(M, K)) return launch_qgemm_small(nullptr, X, ldx, W, scale, bias, M, K, N, e, s);
+  if (qgemm_small_fits(M, K) || qgemm_rows_fit(M, K, N))
+    return launch_qgemm_small(nullptr, X, ldx, W, scale, bias, M, K, N, e, s);
   return launch_gemm(X, ldx, W, scale, bias, M, K, N, e, s);
 }
 

@@ -718,7 +718,8 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   g.R = R;
   g.d = d;
   g.V = m->info.vocab;
-  g.E = m->E;
+  g.E = m->E_frag;
+  g.frag = true;
   g.c_out = m->c_out;
   g.logits = logits_out;
   g.slots = S->fslots;

@@ -14,11 +14,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmnmt.so")
 
 OK, E_INVALID_ARG, E_BAD_MODEL, E_CAPACITY, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
-EPI_I32, EPI_I8, EPI_I8_RELU, EPI_F32, EPI_F32_RESID, EPI_LOGITS, EPI_ARGMAX, EPI_ARGMAX_PARTIAL = range(8)
+(EPI_I32, EPI_I8, EPI_I8_RELU, EPI_F32, EPI_F32_RESID, EPI_LOGITS, EPI_ARGMAX, EPI_ARGMAX_PARTIAL,
+ EPI_ARGMAX_PARTIAL_PACKED) = range(9)
 
 EXPORTS = ("mnmt_model_bytes", "mnmt_model_load", "mnmt_model_get_info", "mnmt_model_free", "mnmt_session_bytes",
            "mnmt_session_create", "mnmt_session_free", "mnmt_encode", "mnmt_decode_step", "mnmt_translate",
-           "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed", "mnmt_argmax_partials", "mnmt_fold_requant",
+           "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed", "mnmt_argmax_partials", "mnmt_packed_bytes",
+           "mnmt_pack_weights", "mnmt_fold_requant",
            "mnmt_debug_canon", "mnmt_status_str",
            "mnmt_last_error")
 
@@ -73,6 +75,9 @@ def lib():
         L.mnmt_qlinear.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp]
         L.mnmt_qlinear_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp, vp, vp]
         L.mnmt_argmax_partials.argtypes = [i32]
+        L.mnmt_packed_bytes.argtypes = [i32, i32]
+        L.mnmt_packed_bytes.restype = sz
+        L.mnmt_pack_weights.argtypes = [vp, i32, i32, vp, vp]
         L.mnmt_fold_requant.argtypes = [f32, vp, vp, f32, i32, vp, vp]
         L.mnmt_debug_canon.argtypes = [i32, vp, i32, vp, vp]
         L.mnmt_status_str.argtypes = [i32]
@@ -118,15 +123,16 @@ def mnmt_fold_requant(s_in, s_w, b, s_out):
 
 
 # ---- device entry points ---------------------------------------------------------
-def mnmt_qlinear(X, W, scale, bias, epilogue, gamma=1.0, out=None, stream=None):
-    """Y = epilogue(X W^T) for int8 CUDA tensors X [M, K], W [N, K]."""
+def mnmt_qlinear(X, W, scale, bias, epilogue, gamma=1.0, out=None, stream=None, n_out=None):
+    """Y = epilogue(X W^T) for int8 CUDA tensors X [M, K], W [N, K] (for
+    EPI_ARGMAX_PARTIAL_PACKED, W is mnmt_pack_weights' output and n_out = N)."""
     import torch
 
     M, K = X.shape
-    N = W.shape[0]
+    N = W.shape[0] if n_out is None else int(n_out)
     if out is None and epilogue == EPI_ARGMAX:
         out = torch.zeros(M, dtype=torch.int64, device=X.device)  # packed (key, index) per row
-    elif out is None and epilogue == EPI_ARGMAX_PARTIAL:
+    elif out is None and epilogue in (EPI_ARGMAX_PARTIAL, EPI_ARGMAX_PARTIAL_PACKED):
         out = torch.empty((M, argmax_partials(N)), dtype=torch.int64, device=X.device)
     elif out is None:
         dt = {EPI_I32: torch.int32, EPI_I8: torch.int8, EPI_I8_RELU: torch.int8}.get(epilogue, torch.float32)
@@ -136,19 +142,38 @@ def mnmt_qlinear(X, W, scale, bias, epilogue, gamma=1.0, out=None, stream=None):
     return out
 
 
-def mnmt_qlinear_timed(X, W, scale, bias, epilogue, ev_start, ev_stop, gamma=1.0, out=None, stream=None):
+def mnmt_qlinear_timed(X, W, scale, bias, epilogue, ev_start, ev_stop, gamma=1.0, out=None, stream=None,
+                       n_out=None):
     """mnmt_qlinear bracketed by two torch.cuda.Event(enable_timing=True)
     (recorded once beforehand so that their HIP events exist)."""
     import torch
 
     M, K = X.shape
-    N = W.shape[0]
+    N = W.shape[0] if n_out is None else int(n_out)
     if out is None:
-        shape = (M, argmax_partials(N)) if epilogue == EPI_ARGMAX_PARTIAL else (M,)
+        partial = epilogue in (EPI_ARGMAX_PARTIAL, EPI_ARGMAX_PARTIAL_PACKED)
+        shape = (M, argmax_partials(N)) if partial else (M,)
         out = torch.zeros(shape, dtype=torch.int64, device=X.device)
     _check(lib().mnmt_qlinear_timed(_ptr(X), _ptr(W), _ptr(scale), _ptr(bias), M, K, N, epilogue, float(gamma),
                                     _ptr(out), _stream(stream), C.c_void_p(ev_start.cuda_event),
                                     C.c_void_p(ev_stop.cuda_event)), "mnmt_qlinear_timed")
+    return out
+
+
+def mnmt_pack_weights(W, stream=None):
+    """Fragment-order copy of an int8 CUDA tensor W [N, K] (K a multiple of
+    64): an int8 tensor [ceil(N / 16) * 16, K] whose bytes are in the order
+    mnmt_pack_weights documents (not a row-major matrix)."""
+    import torch
+
+    N, K = W.shape
+    if W.dtype != torch.int8 or not W.is_contiguous():
+        raise ValueError("W must be a contiguous int8 tensor")
+    nbytes = lib().mnmt_packed_bytes(int(N), int(K))
+    if nbytes == 0:
+        raise ValueError(f"cannot pack a [{N}, {K}] weight (K must be a positive multiple of 64)")
+    out = torch.empty((nbytes // K, K), dtype=torch.int8, device=W.device)
+    _check(lib().mnmt_pack_weights(_ptr(W), int(N), int(K), _ptr(out), _stream(stream)), "mnmt_pack_weights")
     return out
 
 

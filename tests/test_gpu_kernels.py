@@ -209,20 +209,49 @@ def test_qlinear_fused_argmax(torch_dev, M, K, N):
         for p in sorted({0, P // 2, P - 1}):
             blk = ref_z[:, 128 * p:128 * (p + 1)]
             assert np.array_equal(mnmt.argmax_index(part[:, p]), 128 * p + np.argmax(blk, axis=1))
+        # the same kernel on the fragment-order copy of W gives the same keys
+        tW = _gpu(torch, dev, W)
+        packed = mnmt.mnmt_pack_weights(tW)
+        got_p = mnmt.mnmt_qlinear(_gpu(torch, dev, X), packed, _gpu(torch, dev, dq), None,
+                                  mnmt.EPI_ARGMAX_PARTIAL_PACKED, n_out=N)
+        torch.cuda.synchronize()
+        assert np.array_equal(got_p.cpu().numpy().view(np.uint64), part.view(np.uint64))
+
+
+@pytest.mark.parametrize("N,K", [(33, 64), (1000, 256), (32000, 256), (129, 512), (16, 1024)], ids=lambda v: str(v))
+def test_pack_weights_layout(torch_dev, N, K):
+    # chunk l of kilobyte (t, j) holds W[16t + l % 16, 64j + 16(l // 16) .. +15], zero rows past N
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    print(f"pack_weights N={N} K={K}", flush=True)
+    W = np.random.default_rng(N + K).integers(-127, 128, (N, K)).astype(np.int8)
+    got = mnmt.mnmt_pack_weights(_gpu(torch, dev, W))
+    torch.cuda.synchronize()
+    tiles = (N + 15) // 16
+    assert mnmt.lib().mnmt_packed_bytes(N, K) == tiles * 16 * K == got.numel()
+    Wp = np.zeros((tiles * 16, K), np.int8)
+    Wp[:N] = W
+    # [t, r, j, q, b] -> [t, j, q, r, b]: lane l = 16 q + r
+    ref = Wp.reshape(tiles, 16, K // 64, 4, 16).transpose(0, 2, 3, 1, 4).reshape(-1)
+    assert np.array_equal(got.cpu().numpy().reshape(-1), ref)
 
 
 def test_qlinear_timed_matches_and_times_the_kernel(torch_dev):
     torch, dev = torch_dev
     from paper_2306_04235_amd import mnmt
 
-    for M, K, N, epi in ((1, 256, 32000, mnmt.EPI_ARGMAX), (4, 256, 1024, mnmt.EPI_ARGMAX)):
+    for M, K, N, epi in ((1, 256, 32000, mnmt.EPI_ARGMAX), (4, 256, 1024, mnmt.EPI_ARGMAX),
+                         (1, 256, 32000, mnmt.EPI_ARGMAX_PARTIAL_PACKED)):
         X, W, mult, _ = G.sweep_case(M, K, N, seed=5)
         tX, tW, ts = _gpu(torch, dev, X), _gpu(torch, dev, W), _gpu(torch, dev, (mult * 1e-3).astype(np.float32))
-        ref = mnmt.mnmt_qlinear(tX, tW, ts, None, epi)
+        if epi == mnmt.EPI_ARGMAX_PARTIAL_PACKED:
+            tW = mnmt.mnmt_pack_weights(tW)
+        ref = mnmt.mnmt_qlinear(tX, tW, ts, None, epi, n_out=N)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         e1.record()
-        got = mnmt.mnmt_qlinear_timed(tX, tW, ts, None, epi, e0, e1)
+        got = mnmt.mnmt_qlinear_timed(tX, tW, ts, None, epi, e0, e1, n_out=N)
         e1.synchronize()
         assert torch.equal(got, ref)
         assert 0.0 < e0.elapsed_time(e1) < 100.0
