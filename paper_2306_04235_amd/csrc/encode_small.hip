@@ -39,6 +39,14 @@ constexpr int kEncHeadDim = 64;             // widest head
 constexpr int kEncChunk = 64;               // hidden units per k_enc_ffn block, columns per k_enc_out block
 constexpr int kEncWaves = 8;                // waves per block
 constexpr int kEncThreads = 64 * kEncWaves;
+// LDS row strides of the int8 operands read as matrix-core fragments: 16
+// bytes past the row, so that the rows of a fragment (16 rows, the same 16
+// bytes of each) fall in different banks; at a stride of 256 (or 64) bytes
+// every row of a 128-bit read maps to the same four banks.
+template <int D>
+constexpr int lds_ld() { return D + 16; }
+constexpr int kHeadLd = kEncHeadDim + 16;   // q, k, context and hidden-unit rows
+constexpr int kVtLd = kEncRows + 4;         // transposed values: 4-byte reads by 64 consecutive rows
 
 // LayerNorm of G rows held by a wave (row q's element i = lane + 64 j in
 // v[q][j]), each in the canonical order (as ln_row), interleaved.
@@ -91,7 +99,7 @@ __device__ __forceinline__ void enc_clear(const EncIn& in) {
 // The sublayer input rows: the embedding or the pending residual update, the
 // LayerNorm, the stores of the updated residual rows (x_out) and of the int8
 // rows (q_out) (row r by block r mod nblk), and the int8 rows in a_lds (row
-// stride D).  Wave w takes rows w + kEncWaves u, u < RPW, and issues all of
+// stride lds_ld<D>()).  Wave w takes rows w + kEncWaves u, u < RPW, and issues all of
 // their loads before it uses the first (one memory round trip, two for the
 // embedding's token lookup), then calls issue_weights() to issue the
 // kernel's other loads, then clears its share of the finished accumulators.
@@ -188,7 +196,7 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
           const int8_t c = code_of(v[q][j] * in.inv_s);
-          a_lds[r * D + lane + 64 * j] = c;
+          a_lds[r * lds_ld<D>() + lane + 64 * j] = c;
           if (qst) in.q_out[r * D + lane + 64 * j] = c;
         }
       }
@@ -221,10 +229,10 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   constexpr int NT = 3 * kEncHeadDim / 16;                        // projection tiles of the widest head
   constexpr int PT = (NT + kEncWaves - 1) / kEncWaves;            // projection tiles per wave
   constexpr int OT = (DMAX / 16 + kEncWaves - 1) / kEncWaves;     // W_o column tiles per wave
-  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
-  __shared__ __attribute__((aligned(16))) int8_t qk[2][kEncRows][kEncHeadDim];
-  __shared__ __attribute__((aligned(16))) int8_t vt[kEncHeadDim][kEncRows];  // values, transposed
-  __shared__ __attribute__((aligned(16))) int8_t ctx[kEncRows][kEncHeadDim];
+  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * lds_ld<DMAX>()];
+  __shared__ __attribute__((aligned(16))) int8_t qk[2][kEncRows][kHeadLd];
+  __shared__ __attribute__((aligned(16))) int8_t vt[kEncHeadDim][kVtLd];  // values, transposed
+  __shared__ __attribute__((aligned(16))) int8_t ctx[kEncRows][kHeadLd];
   __shared__ __attribute__((aligned(16))) float sc[kEncRows][kEncRows];      // scores, then probabilities
   const int hd = blockIdx.x;
   const int R = in.R, d = DMAX, dh = at.dh, S = in.S, ks = KS;
@@ -271,7 +279,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk)
-        if (kk < ks) acc = mfma16(lds_frag(a_lds, d, 16 * mt, 64 * kk, d), wf[u][kk], acc);
+        if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), wf[u][kk], acc);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int m = 16 * mt + 4 * kq + i;
@@ -287,8 +295,8 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   // 3. scores q . k (int32 exact) scaled by c_qk, every (query, key) pair
   for (int t = wave; t < mt_n * mt_n; t += kEncWaves) {
     const int mt = t / mt_n, kt = t % mt_n;
-    const v4i acc = mfma16(lds_frag(&qk[0][0][0], kEncHeadDim, 16 * mt, 0, dh),
-                           lds_frag(&qk[1][0][0], kEncHeadDim, 16 * kt, 0, dh), v4i{0, 0, 0, 0});
+    const v4i acc = mfma16(lds_frag(&qk[0][0][0], kHeadLd, 16 * mt, 0, dh),
+                           lds_frag(&qk[1][0][0], kHeadLd, 16 * kt, 0, dh), v4i{0, 0, 0, 0});
 #pragma unroll
     for (int i = 0; i < 4; ++i) sc[16 * mt + 4 * kq + i][16 * kt + l16] = (float)acc[i] * at.c_qk;
   }
@@ -370,7 +378,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
     const int n0 = 16 * (wave + kEncWaves * u);
     if (n0 >= d) continue;
     for (int mt = 0; mt < mt_n; ++mt) {
-      const v4i acc = mfma16(lds_frag(&ctx[0][0], kEncHeadDim, 16 * mt, 0, dh), of[u], v4i{0, 0, 0, 0});
+      const v4i acc = mfma16(lds_frag(&ctx[0][0], kHeadLd, 16 * mt, 0, dh), of[u], v4i{0, 0, 0, 0});
       add_frag(at.acc_out, d, acc, 16 * mt, n0 + l16, R);
     }
   }
@@ -384,8 +392,8 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
   constexpr int KS = DMAX / 64;
   constexpr int OT = (DMAX / 16 + kEncWaves - 1) / kEncWaves;  // W2 column tiles per wave
   static_assert(kEncChunk == 64 && kEncWaves == 8, "four W1 tiles, two row-tile phases, one K step of W2");
-  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
-  __shared__ __attribute__((aligned(16))) int8_t hb[kEncRows][kEncChunk];
+  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * lds_ld<DMAX>()];
+  __shared__ __attribute__((aligned(16))) int8_t hb[kEncRows][kHeadLd];
   const int R = in.R, d = DMAX, F = f.F, ks = KS;
   const int mt_n = (R + 15) / 16;
   const int f0 = blockIdx.x * kEncChunk;
@@ -412,7 +420,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
-      if (kk < ks) acc = mfma16(lds_frag(a_lds, d, 16 * mt, 64 * kk, d), wf[kk], acc);
+      if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), wf[kk], acc);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = 16 * mt + 4 * kq + i;
@@ -425,7 +433,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
     const int n0 = 16 * (wave + kEncWaves * u);
     if (n0 >= d) continue;
     for (int mt = 0; mt < mt_n; ++mt) {
-      const v4i acc = mfma16(lds_frag(&hb[0][0], kEncChunk, 16 * mt, 0, kEncChunk), of[u], v4i{0, 0, 0, 0});
+      const v4i acc = mfma16(lds_frag(&hb[0][0], kHeadLd, 16 * mt, 0, kEncChunk), of[u], v4i{0, 0, 0, 0});
       add_frag(f.acc_out, d, acc, 16 * mt, n0 + l16, R);
     }
   }
@@ -439,7 +447,7 @@ template <int DMAX, int RPW>
 __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
   constexpr int KS = DMAX / 64;
   static_assert(kEncChunk == 64 && kEncWaves == 8, "four column tiles, two row-tile phases");
-  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * DMAX];
+  __shared__ __attribute__((aligned(16))) int8_t a_lds[kEncRows * lds_ld<DMAX>()];
   const int R = in.R, d = DMAX, ks = KS;
   const int mt_n = (R + 15) / 16;
   const int per_layer = 2 * d / kEncChunk;
@@ -463,7 +471,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
-      if (kk < ks) acc = mfma16(lds_frag(a_lds, d, 16 * mt, 64 * kk, d), wf[kk], acc);
+      if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), wf[kk], acc);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = 16 * mt + 4 * kq + i;
