@@ -33,13 +33,26 @@ __device__ __forceinline__ void chain_wait(const StepChain& c) {
   __syncthreads();
 }
 
-// The block's flag word (in every copy), stored (release, agent scope) after
-// every thread of the block has issued its last global write.
+// A global store that a later kernel of the chain reads: a relaxed
+// agent-scope atomic store, which goes through to the device's point of
+// coherence instead of staying in the writer's L2 (each XCD has its own).
+// With every such write made this way (and the accumulators' agent-scope
+// atomics), chain_signal only waits for the writes to complete and needs no
+// write-back of the L2, which an agent-scope release performs.
+template <class T>
+__device__ __forceinline__ void chain_store(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The block's flag word (in every copy), stored once every wave's writes
+// (chain_store, atomics) have completed.
 __device__ __forceinline__ void chain_signal(const StepChain& c) {
   if (!c.done) return;
-  __syncthreads();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's stores and atomics complete
+  __syncthreads();                // ... and every other wave's
   if ((int)threadIdx.x < chain_copies(gridDim.x))
-    __hip_atomic_store(c.done + threadIdx.x * kChainCopyStride + blockIdx.x, c.val, __ATOMIC_RELEASE,
+    __hip_atomic_store(c.done + threadIdx.x * kChainCopyStride + blockIdx.x, c.val, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
 }
 

@@ -51,22 +51,34 @@ struct RowRegs {
   float b[NJ];
 };
 
-// Issues the loads of input row r (element i = lane + 64 j in slot j; slots
-// past d repeat element d - 1 and are never used).  No load is conditional:
-// a branch around a load makes the compiler wait for it where the branches
-// join, which would serialize the kernel's memory round trips.
+// The loads of input row r (element i = lane + 64 j in slot j; slots past d
+// repeat element d - 1 and are never used), in two parts: the constants
+// (model parameters, issued before a chain wait together with the weights)
+// and the row data (written by the previous kernel, issued after it).  No
+// load is conditional on a lane: a branch around a load makes the compiler
+// wait for it where the branches join, which would serialize the kernel's
+// memory round trips.
 template <int NJ>
-__device__ __forceinline__ void load_row(const StepIn& in, int r, int d, RowRegs<NJ>& q) {
+__device__ __forceinline__ void load_row_consts(const StepIn& in, int d, RowRegs<NJ>& q) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int i = min(lane + 64 * j, d - 1);
+    q.sc[j] = in.scale[i];
+    q.bi[j] = in.bias[i];
+    q.g[j] = in.ln_g[i];
+    q.b[j] = in.ln_b[i];
+  }
+}
+
+template <int NJ>
+__device__ __forceinline__ void load_row_data(const StepIn& in, int r, int d, RowRegs<NJ>& q) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     const int i = min(lane + 64 * j, d - 1);
     q.x[j] = in.x_in[(size_t)r * d + i];
     q.a[j] = in.acc[(size_t)r * d + i];
-    q.sc[j] = in.scale[i];
-    q.bi[j] = in.bias[i];
-    q.g[j] = in.ln_g[i];
-    q.b[j] = in.ln_b[i];
   }
 }
 
@@ -84,7 +96,7 @@ __device__ __forceinline__ void finish_row(const StepIn& in, int r, int d, RowRe
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int i = lane + 64 * j;
-      if (i < d) in.x_out[(size_t)r * d + i] = v[j];
+      if (i < d) chain_store(in.x_out + (size_t)r * d + i, v[j]);
     }
   }
   if (in.ln_mode == 2) ln_row<NJ>(v, q.g, q.b, d, in.eps);  // pre-LN: normalize the sublayer input
@@ -101,7 +113,7 @@ constexpr int kStepThreads = 256;  // block size of every step kernel
 // the dispatch packet and waits for every load issued before it.)
 __device__ __forceinline__ void clear_acc(const StepIn& in) {
   if (blockIdx.x == 0 && in.zero_acc)
-    for (int i = threadIdx.x; i < in.zero_n; i += kStepThreads) in.zero_acc[i] = 0;
+    for (int i = threadIdx.x; i < in.zero_n; i += kStepThreads) chain_store(in.zero_acc + i, 0);
 }
 
 // The projections run on v_mfma_i32_16x16x64_i8 even though only R <= 2 of
@@ -175,20 +187,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   }
   int n_att = SELF ? at.t + 1 : at.len[r];
   n_att = SELF ? n_att : (n_att < 1 ? 1 : (n_att > at.S ? at.S : n_att));
-  asm volatile("" ::: "memory");  // the loads above stay ahead of the wait
-  chain_wait(in.chain);
   RowRegs<NJ> rr;
-  // MODE 1 / 2: the arg-max partials of the wave's row (lane i: slots i + 64 k)
-  // and whether the row had finished
-  unsigned long long pk[4] = {0ull, 0ull, 0ull, 0ull};
-  int fin = 0;
-  if (MODE != 0) {
-    const int row = min(wave, R - 1);
-    const unsigned long long* sl = cm.slots + (size_t)row * cm.nslots;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) pk[k] = sl[min(lane + 64 * k, cm.nslots - 1)];
-    fin = cm.finished[row];
-  }
   if (MODE == 1) {
     // the position term now, the token's embedding once the token is known
 #pragma unroll
@@ -202,8 +201,22 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
       rr.b[j] = in.ln_b[i];
     }
   } else {
-    load_row(in, min(wave, R - 1), d, rr);
+    load_row_consts(in, d, rr);
   }
+  asm volatile("" ::: "memory");  // the loads above stay ahead of the wait
+  chain_wait(in.chain);
+  // MODE 1 / 2: the arg-max partials of the wave's row (lane i: slots i + 64 k)
+  // and whether the row had finished
+  unsigned long long pk[4] = {0ull, 0ull, 0ull, 0ull};
+  int fin = 0;
+  if (MODE != 0) {
+    const int row = min(wave, R - 1);
+    const unsigned long long* sl = cm.slots + (size_t)row * cm.nslots;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pk[k] = sl[min(lane + 64 * k, cm.nslots - 1)];
+    fin = cm.finished[row];
+  }
+  if (MODE != 1) load_row_data(in, min(wave, R - 1), d, rr);
   if (MODE == 1) {
     unsigned long long key = pk[0];
 #pragma unroll
@@ -260,8 +273,8 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
       int8_t* kc = at.kcache + ((size_t)r * at.T + at.t) * d + hd * dh;
       int8_t* vc = at.vcache + ((size_t)r * at.T + at.t) * d + hd * dh;
       for (int j = lane; j < dh; j += 64) {
-        kc[j] = knew[j];
-        vc[j] = vnew[j];
+        chain_store(kc + j, knew[j]);
+        chain_store(vc + j, vnew[j]);
       }
     }
     int4 qv[HC], kn[HC];
@@ -353,13 +366,13 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
     const int tok = unpack_index(wave_max_u64(key));
     if (wave < R && lane == 0) {
       const int tc = cm.t - 1;
-      if (tc < cm.T) cm.out_tok[(size_t)tc * R + wave] = fin ? cm.pad : tok;
+      if (tc < cm.T) chain_store(cm.out_tok + (size_t)tc * R + wave, fin ? cm.pad : tok);
       if (!fin && cm.stop_at_eos && tok == cm.eos) {
-        cm.finished[wave] = 1;
-        cm.out_len[wave] = tc + 1;
+        chain_store(cm.finished + wave, 1);
+        chain_store(cm.out_len + wave, tc + 1);
       }
-      cm.cur_tok[wave] = fin ? cm.pad : tok;
-      if (wave == 0) *cm.step = cm.t;
+      chain_store(cm.cur_tok + wave, fin ? cm.pad : tok);
+      if (wave == 0) chain_store(cm.step, cm.t);
     }
   }
   chain_signal(in.chain);
@@ -391,10 +404,11 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
     const int n = min(16 * (wave + 4 * t) + l16, d - 1);
     of[t] = *(const v4i*)(f.W2 + (size_t)n * F + f0 + 16 * kq);
   }
+  RowRegs<NJ> rr;
+  load_row_consts(in, d, rr);
   asm volatile("" ::: "memory");  // the weight loads stay ahead of the wait
   chain_wait(in.chain);
-  RowRegs<NJ> rr;
-  load_row(in, min(wave, R - 1), d, rr);
+  load_row_data(in, min(wave, R - 1), d, rr);
   clear_acc(in);
   if (wave < R) finish_row(in, wave, d, rr, a_lds);
   lds_barrier();
@@ -466,9 +480,10 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   }
   RowRegs<NJ> rr;
   if (!RAW) {
+    load_row_consts(in, d, rr);
     asm volatile("" ::: "memory");  // the weight loads stay ahead of the wait
     chain_wait(in.chain);
-    load_row(in, min(wave, R - 1), d, rr);
+    load_row_data(in, min(wave, R - 1), d, rr);
   }
   if (!RAW) {
     clear_acc(in);
@@ -516,7 +531,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     if (g.nslots >= (int)gridDim.x) {
       // one partial per block: a plain store, no atomic (atomics on one
       // address serialize), reduced by the consumer
-      slot[blockIdx.x] = b;
+      chain_store(slot + blockIdx.x, b);
     } else {
       // few slots: most blocks find a larger key already there, and the
       // test spares them the serialized atomic

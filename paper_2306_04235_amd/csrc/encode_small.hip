@@ -86,14 +86,22 @@ __device__ __forceinline__ void ln_rows(float (&v)[G][NJ], const float (&g)[NJ],
 }
 
 // Clears this block's share of the accumulators whose consumers have
-// finished (16-byte stores; the counts are multiples of 64).
+// finished (8-byte write-through stores; the counts are multiples of 64).
 __device__ __forceinline__ void enc_clear(const EncIn& in) {
   const int b = blockIdx.x, nb = in.nblk;
   const int n0 = in.zero0_n / 4, n1 = in.zero1_n / 4;
   const int per0 = (n0 + nb - 1) / nb, per1 = (n1 + nb - 1) / nb;
   const int e0 = min(n0, (b + 1) * per0), e1 = min(n1, (b + 1) * per1);
-  for (int i = b * per0 + threadIdx.x; i < e0; i += kEncThreads) ((v4i*)in.zero0)[i] = v4i{0, 0, 0, 0};
-  for (int i = b * per1 + threadIdx.x; i < e1; i += kEncThreads) ((v4i*)in.zero1)[i] = v4i{0, 0, 0, 0};
+  unsigned long long* z0 = reinterpret_cast<unsigned long long*>(in.zero0);
+  unsigned long long* z1 = reinterpret_cast<unsigned long long*>(in.zero1);
+  for (int i = b * per0 + threadIdx.x; i < e0; i += kEncThreads) {
+    chain_store(z0 + 2 * i, 0ull);
+    chain_store(z0 + 2 * i + 1, 0ull);
+  }
+  for (int i = b * per1 + threadIdx.x; i < e1; i += kEncThreads) {
+    chain_store(z1 + 2 * i, 0ull);
+    chain_store(z1 + 2 * i + 1, 0ull);
+  }
 }
 
 // The sublayer input rows: the embedding or the pending residual update, the
@@ -184,7 +192,7 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
         const int r = wave + kEncWaves * (u0 + q);
         if (r < R && r % in.nblk == (int)blockIdx.x)
 #pragma unroll
-          for (int j = 0; j < NJ; ++j) in.x_out[r * D + lane + 64 * j] = v[q][j];
+          for (int j = 0; j < NJ; ++j) chain_store(in.x_out + r * D + lane + 64 * j, v[q][j]);
       }
     }
     if (in.ln_mode == 2) ln_rows<G, NJ>(v, g, b, D, in.eps);  // pre-LN: normalize the sublayer input
@@ -197,7 +205,7 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
         for (int j = 0; j < NJ; ++j) {
           const int8_t c = code_of(v[q][j] * in.inv_s);
           a_lds[r * lds_ld<D>() + lane + 64 * j] = c;
-          if (qst) in.q_out[r * D + lane + 64 * j] = c;
+          if (qst) chain_store(in.q_out + r * D + lane + 64 * j, c);
         }
       }
     }
