@@ -336,11 +336,29 @@ struct BeamState {
   int32_t* done;         // [B]
   int32_t* cur_tok;      // [R]
   const float* lp;       // [T + 1] length penalties
+  int32_t* count;        // [1] blocks of the update kernel finished this step (0 between steps)
   int eos, pad, bos;
+};
+// The next step's input rows, written by the beam update for every slot of
+// its sentence while t + 1 < steps: the embedding of the slot's token at
+// position t + 1 (x) and the first decoder layer's int8 input (a: LayerNorm
+// when do_ln, then quantization with inv_s).
+struct BeamNext {
+  float* x;        // [R, d]
+  int8_t* a;       // [R, d]
+  const int8_t* E;
+  const float* c_emb;
+  const float* pe;  // [P, d]
+  int d, V, P, steps;
+  int do_ln;
+  const float* g;
+  const float* b;
+  float eps, inv_s;
 };
 hipError_t launch_beam_reset(const BeamState& st, int* step, hipStream_t s);
 hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int* step, hipStream_t s);
-hipError_t launch_beam_update(const BeamState& st, int* step, hipStream_t s);
+// Also advances the step counter (the last block to finish).
+hipError_t launch_beam_update(const BeamState& st, int* step, const BeamNext& nx, hipStream_t s);
 hipError_t launch_beam_finalize(const BeamState& st, int steps, int32_t* out, int32_t* out_len, float* out_score,
                                 hipStream_t s);
 

@@ -28,26 +28,22 @@ __global__ __launch_bounds__(256) void k_embed(const int32_t* __restrict__ tok, 
 
 // ---------------------------------------------------------------------------
 // LayerNorm + quantization.  One wave per row; element i lives in lane i % 64
-// and is added to that lane's partial in ascending i (canonical order).
-__global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, int rows, int d, int do_ln,
-                                                  const float* __restrict__ g, const float* __restrict__ b,
-                                                  float eps, float inv_s, int8_t* __restrict__ q,
-                                                  float* __restrict__ x_out) {
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+// (slot j = i / 64 of v) and is added to that lane's partial in ascending i
+// (canonical order).  ln_quant_wave normalizes v in place (when do_ln) and
+// stores the codes (q_row) and the normalized row (x_out_row), either may be
+// null.
+__device__ __forceinline__ void ln_quant_wave(float (&v)[kMaxRowLen / 64], int d, int do_ln,
+                                              const float* __restrict__ g, const float* __restrict__ b, float eps,
+                                              float inv_s, int8_t* __restrict__ q_row,
+                                              float* __restrict__ x_out_row) {
   const int lane = threadIdx.x & 63;
-  if (r >= rows) return;
-  const float* xr = x + (size_t)r * d;
-  float v[kMaxRowLen / 64];
   const int n = (d + 63) / 64;
   if (do_ln) {
     float p = 0.0f;
 #pragma unroll
     for (int j = 0; j < kMaxRowLen / 64; ++j) {
       const int i = lane + 64 * j;
-      if (j < n && i < d) {
-        v[j] = xr[i];
-        p = p + v[j];
-      }
+      if (j < n && i < d) p = p + v[j];
     }
     const float inv_d = 1.0f / (float)d;
     const float mu = wave_sum(p) * inv_d;
@@ -67,21 +63,34 @@ __global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, i
       const int i = lane + 64 * j;
       if (j < n && i < d) v[j] = fmaf(v[j] * rstd, g[i], b[i]);
     }
-  } else {
-#pragma unroll
-    for (int j = 0; j < kMaxRowLen / 64; ++j) {
-      const int i = lane + 64 * j;
-      if (j < n && i < d) v[j] = xr[i];
-    }
   }
 #pragma unroll
   for (int j = 0; j < kMaxRowLen / 64; ++j) {
     const int i = lane + 64 * j;
     if (j < n && i < d) {
-      if (q) q[(size_t)r * d + i] = code_of(v[j] * inv_s);
-      if (x_out) x_out[(size_t)r * d + i] = v[j];
+      if (q_row) q_row[i] = code_of(v[j] * inv_s);
+      if (x_out_row) x_out_row[i] = v[j];
     }
   }
+}
+
+__global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, int rows, int d, int do_ln,
+                                                  const float* __restrict__ g, const float* __restrict__ b,
+                                                  float eps, float inv_s, int8_t* __restrict__ q,
+                                                  float* __restrict__ x_out) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  const float* xr = x + (size_t)r * d;
+  float v[kMaxRowLen / 64];
+  const int n = (d + 63) / 64;
+#pragma unroll
+  for (int j = 0; j < kMaxRowLen / 64; ++j) {
+    const int i = lane + 64 * j;
+    if (j < n && i < d) v[j] = xr[i];
+  }
+  ln_quant_wave(v, d, do_ln, g, b, eps, inv_s, q ? q + (size_t)r * d : nullptr,
+                x_out ? x_out + (size_t)r * d : nullptr);
 }
 
 // Encoder self-attention: block = one wave = (query s, head hd, sentence b).
@@ -259,7 +268,10 @@ __global__ void k_beam_reset(BeamState st, int* step) {
     st.fin_count[b] = 0;
     st.done[b] = 0;
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) *step = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    *step = 0;
+    *st.count = 0;
+  }
 }
 
 // Per live row: log-softmax statistics of the logits (max, then the canonical
@@ -540,9 +552,11 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
 }
 
 // Per sentence: merge the W rows' candidates, finish EOS hypotheses, refill
-// the W live slots and advance the key/value history.  One wave per sentence.
+// the W live slots and advance the key/value history; then the next step's
+// input rows of the sentence's slots (BeamNext), and the step counter
+// (advanced by the last block).  One wave per sentence.
 template <int W_MAX>
-__global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step) {
+__global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step, BeamNext nx) {
   constexpr int NC = W_MAX * 2 * W_MAX;  // candidates per sentence
   __shared__ float cs[NC];
   __shared__ int cj[NC], cv[NC];
@@ -550,11 +564,13 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step) {
   __shared__ int new_par[W_MAX], new_tok[W_MAX];
   __shared__ float new_score[W_MAX];
   __shared__ int n_live_sh, done_sh;
+  __shared__ int slot_tok[W_MAX];  // each slot's token after the update
   const int b = blockIdx.x;
   const int lane = threadIdx.x;
   const int W = st.W, K = 2 * W, R = st.B * W, T = st.T, V = st.V;
   const int t = *step;
   const bool active = !st.done[b];
+  if (lane < W) slot_tok[lane] = st.cur_tok[b * W + lane];
   if (active) {
     const int n_alive = t == 0 ? 1 : W;
     const int n = n_alive * K;
@@ -615,6 +631,7 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step) {
         if (lane == 0) {
           st.score[p] = new_score[s];
           st.cur_tok[p] = new_tok[s];
+          slot_tok[s] = new_tok[s];
           if (t < T) {
             st.tok_hist[(size_t)t * R + p] = new_tok[s];
             st.par_hist[(size_t)t * R + p] = par;
@@ -623,11 +640,32 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step) {
       }
     }
   }
-  // The step counter is advanced by k_step_advance after every sentence.
-}
-
-__global__ void k_step_advance(int* step) {
-  if (threadIdx.x == 0) *step = *step + 1;
+  __syncthreads();
+  // the next step's input rows: what k_embed and k_ln_quant compute, row by row
+  const int pos = t + 1;
+  if (pos < nx.steps && pos < nx.P) {
+    for (int s = 0; s < W; ++s) {
+      const int p = b * W + s;
+      int tk = slot_tok[s];
+      tk = tk < 0 ? 0 : (tk >= nx.V ? nx.V - 1 : tk);
+      const float c = nx.c_emb[tk];
+      float v[kMaxRowLen / 64];
+#pragma unroll
+      for (int j = 0; j < kMaxRowLen / 64; ++j) {
+        const int i = lane + 64 * j;
+        if (i < nx.d) {
+          v[j] = fmaf((float)nx.E[(size_t)tk * nx.d + i], c, nx.pe[(size_t)pos * nx.d + i]);
+          nx.x[(size_t)p * nx.d + i] = v[j];
+        }
+      }
+      ln_quant_wave(v, nx.d, nx.do_ln, nx.g, nx.b, nx.eps, nx.inv_s, nx.a + (size_t)p * nx.d, nullptr);
+    }
+  }
+  // the step counter, by the last block to get here (every block has read it)
+  if (lane == 0 && atomicAdd(st.count, 1) == (int)gridDim.x - 1) {
+    *st.count = 0;
+    *step = t + 1;
+  }
 }
 
 // Backtrack the tokens of the hypothesis held by `row` after step `last`
@@ -841,12 +879,9 @@ hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int*
   return hipGetLastError();
 }
 
-hipError_t launch_beam_update(const BeamState& st, int* step, hipStream_t s) {
-  if (st.W > 8) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_beam_update<8>, dim3(st.B), dim3(64), 0, s, st, step);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_step_advance, dim3(1), dim3(64), 0, s, step);
+hipError_t launch_beam_update(const BeamState& st, int* step, const BeamNext& nx, hipStream_t s) {
+  if (st.W > 8 || nx.d < 1 || nx.d > kMaxRowLen || !nx.x || !nx.a || !st.count) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_beam_update<8>, dim3(st.B), dim3(64), 0, s, st, step, nx);
   return hipGetLastError();
 }
 

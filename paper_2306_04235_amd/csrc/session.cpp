@@ -35,7 +35,7 @@ struct Plan {
   size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots, enc_acc;
   size_t cur_tok, step, slots, out_tok, finished, out_len, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
-  size_t chain_err, enc_chain;
+  size_t chain_err, enc_chain, beam_count;
   size_t total;
 };
 
@@ -124,6 +124,7 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.fin_count = b.take(4 * B);
   p.done = b.take(4 * B);
   p.chain_err = b.take(4);
+  p.beam_count = b.take(4);
   p.enc_chain = b.take(4 * 2 * (size_t)m->info.n_enc * kChainSlotWords);
   p.total = (b.off + 255) / 256 * 256;
   return p;
@@ -405,14 +406,18 @@ int run_encoder(mnmt_session* S, hipStream_t s) {
 
 // One decoder step for R rows (W hypotheses per sentence); ends with the
 // final sublayer input in dec_a, ready for the output projection.
-int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s) {
+// rows_ready: dec_x and dec_a already hold the step's input rows (written by
+// the previous step's beam update).
+int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, bool rows_ready = false) {
   const mnmt_model* m = S->m;
   const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
   const bool post = m->info.ln_post;
   const float eps = m->info.ln_eps;
-  LAUNCH(launch_embed(S->cur_tok, R, 1, S->step, m->E, m->c_emb, m->pe, d, m->info.vocab, S->dec_x, s));
   const LayerDev& L0 = m->dec[0];
-  LAUNCH(launch_ln_quant(S->dec_x, R, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->dec_a, nullptr, s));
+  if (!rows_ready) {
+    LAUNCH(launch_embed(S->cur_tok, R, 1, S->step, m->E, m->c_emb, m->pe, d, m->info.vocab, S->dec_x, s));
+    LAUNCH(launch_ln_quant(S->dec_x, R, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->dec_a, nullptr, s));
+  }
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
     int rc;
@@ -777,15 +782,33 @@ int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logit
   return greedy_step(S, R, stop_at_eos, logits_out, s);
 }
 
-int beam_step(mnmt_session* S, int R, int W, hipStream_t s) {
+// Step t of `steps`: from the second step on, the input rows come from the
+// previous step's beam update, which also prepares them for the next one.
+int beam_step(mnmt_session* S, int R, int W, int t, int steps, hipStream_t s) {
   const mnmt_model* m = S->m;
-  int rc = run_decoder_layers(S, R, W, true, s);
+  int rc = run_decoder_layers(S, R, W, true, s, t > 0);
   if (rc) return rc;
   const int d = m->info.d_model, V = m->info.vocab;
   EpiArgs e{MNMT_EPI_LOGITS, S->logits, V, 1.f, nullptr};
   LAUNCH(launch_qlinear(S->dec_a, d, m->E, m->c_out, nullptr, R, d, V, e, s));
   LAUNCH(launch_beam_topk(S->logits, S->beam, S->step, s));
-  LAUNCH(launch_beam_update(S->beam, S->step, s));
+  const LayerDev& L0 = m->dec[0];
+  BeamNext nx{};
+  nx.x = S->dec_x;
+  nx.a = S->dec_a;
+  nx.E = m->E;
+  nx.c_emb = m->c_emb;
+  nx.pe = m->pe;
+  nx.d = d;
+  nx.V = V;
+  nx.P = m->info.max_pos;
+  nx.steps = steps;
+  nx.do_ln = !m->info.ln_post;
+  nx.g = L0.sa_ln.g;
+  nx.b = L0.sa_ln.b;
+  nx.eps = m->info.ln_eps;
+  nx.inv_s = L0.qkv.inv_in;
+  LAUNCH(launch_beam_update(S->beam, S->step, nx, s));
   return MNMT_OK;
 }
 
@@ -819,7 +842,7 @@ int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
     const int R = S->B * sc.beam;
     LAUNCH(launch_beam_reset(S->beam, S->step, s));
     for (int t = 0; t < sc.max_steps; ++t)
-      if ((rc = beam_step(S, R, sc.beam, s))) return rc;
+      if ((rc = beam_step(S, R, sc.beam, t, sc.max_steps, s))) return rc;
   }
   return MNMT_OK;
 }
@@ -923,6 +946,7 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   st.fin_row = (int32_t*)at(p.fin_row);
   st.fin_count = (int32_t*)at(p.fin_count);
   st.done = (int32_t*)at(p.done);
+  st.count = (int32_t*)at(p.beam_count);
   st.cur_tok = S->cur_tok;
   st.lp = S->lp;
   st.eos = model->info.eos_id;
