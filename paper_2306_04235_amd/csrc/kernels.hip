@@ -554,9 +554,11 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
 // Per sentence: merge the W rows' candidates, finish EOS hypotheses, refill
 // the W live slots and advance the key/value history; then the next step's
 // input rows of the sentence's slots (BeamNext), and the step counter
-// (advanced by the last block).  One wave per sentence.
+// (advanced by the last block).  One block per sentence: wave 0 updates the
+// sentence, then wave w prepares slots w, w + kUpdWaves, ...
+constexpr int kUpdWaves = 4;
 template <int W_MAX>
-__global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step, BeamNext nx) {
+__global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, int* step, BeamNext nx) {
   constexpr int NC = W_MAX * 2 * W_MAX;  // candidates per sentence
   __shared__ float cs[NC];
   __shared__ int cj[NC], cv[NC];
@@ -566,15 +568,16 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step, Bea
   __shared__ int n_live_sh, done_sh;
   __shared__ int slot_tok[W_MAX];  // each slot's token after the update
   const int b = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const bool w0 = wv == 0;  // the wave that updates the sentence
   const int W = st.W, K = 2 * W, R = st.B * W, T = st.T, V = st.V;
   const int t = *step;
   const bool active = !st.done[b];
-  if (lane < W) slot_tok[lane] = st.cur_tok[b * W + lane];
+  if (threadIdx.x < W) slot_tok[threadIdx.x] = st.cur_tok[b * W + threadIdx.x];
   if (active) {
     const int n_alive = t == 0 ? 1 : W;
     const int n = n_alive * K;
-    for (int i = lane; i < NC; i += 64) {
+    for (int i = lane; w0 && i < NC; i += 64) {
       if (i < n) {
         const int jj = i / K, k = i % K;
         const int r = b * W + jj;
@@ -585,7 +588,7 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step, Bea
     }
     __syncthreads();
     // rank of each candidate = number of better candidates (flat index j*V + v breaks ties)
-    for (int i = lane; i < n; i += 64) {
+    for (int i = lane; w0 && i < n; i += 64) {
       int rank = 0;
       const long fi = (long)cj[i] * V + cv[i];
       for (int o = 0; o < n; ++o) {
@@ -595,7 +598,7 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step, Bea
       if (rank < K) order[rank] = i;
     }
     __syncthreads();
-    if (lane == 0) {
+    if (threadIdx.x == 0) {
       int n_live = 0;
       int fc = st.fin_count[b];
       const int n_top = n < K ? n : K;
@@ -621,7 +624,7 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step, Bea
       done_sh = fc >= W;
     }
     __syncthreads();
-    if (!done_sh) {
+    if (!done_sh && w0) {
       const int n_live = n_live_sh;
       const int32_t* hcur = st.hist + (size_t)(t & 1) * R * T;
       int32_t* hnext = st.hist + (size_t)((t + 1) & 1) * R * T;
@@ -641,10 +644,10 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step, Bea
     }
   }
   __syncthreads();
-  // the next step's input rows: what k_embed and k_ln_quant compute, row by row
+  // the next step's input rows: what k_embed and k_ln_quant compute, one wave per row
   const int pos = t + 1;
   if (pos < nx.steps && pos < nx.P) {
-    for (int s = 0; s < W; ++s) {
+    for (int s = wv; s < W; s += kUpdWaves) {
       const int p = b * W + s;
       int tk = slot_tok[s];
       tk = tk < 0 ? 0 : (tk >= nx.V ? nx.V - 1 : tk);
@@ -662,7 +665,8 @@ __global__ __launch_bounds__(64) void k_beam_update(BeamState st, int* step, Bea
     }
   }
   // the step counter, by the last block to get here (every block has read it)
-  if (lane == 0 && atomicAdd(st.count, 1) == (int)gridDim.x - 1) {
+  __syncthreads();
+  if (threadIdx.x == 0 && atomicAdd(st.count, 1) == (int)gridDim.x - 1) {
     *st.count = 0;
     *step = t + 1;
   }
@@ -881,7 +885,7 @@ hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int*
 
 hipError_t launch_beam_update(const BeamState& st, int* step, const BeamNext& nx, hipStream_t s) {
   if (st.W > 8 || nx.d < 1 || nx.d > kMaxRowLen || !nx.x || !nx.a || !st.count) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_beam_update<8>, dim3(st.B), dim3(64), 0, s, st, step, nx);
+  hipLaunchKernelGGL(k_beam_update<8>, dim3(st.B), dim3(64 * kUpdWaves), 0, s, st, step, nx);
   return hipGetLastError();
 }
 
