@@ -172,6 +172,39 @@ def test_serial_steps_match_the_kernel_chain(torch_dev, monkeypatch):
         sess.close()
 
 
+def test_kernel_chain_many_sentences(torch_dev, monkeypatch):
+    """Two dozen different batch-1 sentences (10-30 source tokens) through the
+    kernel chain, in graph replays as the benchmark runs them, against the
+    one-stream steps of the same kernels (about 5,000 flag hand-offs, each
+    consumer reading what its predecessors wrote on other compute units),
+    and the first four against the oracle."""
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    om, gm = _pair("MOBILE")
+    rng = np.random.default_rng(2024)
+    lens_all = rng.integers(10, 31, 24)
+    outs = {}
+    for serial in ("1", "0"):
+        monkeypatch.setenv("MNMT_SERIAL_STEPS", serial)
+        sess = mnmt.Session(gm, 1, 30, 30, 1)
+        got = []
+        for k, n in enumerate(lens_all):
+            src, lens = G.make_sources(G.MOBILE.vocab, 1, [int(n)], seed=500 + k, s_max=30)
+            out, out_len, _ = sess.translate(_t(torch, dev, src), _t(torch, dev, lens), beam=1, max_steps=30,
+                                             use_graph=True)
+            torch.cuda.synchronize()
+            got.append((out.cpu().numpy().copy(), out_len.cpu().numpy().copy()))
+            if serial == "0" and k < 4:
+                o_out, o_len = om.greedy(src, lens, 30)[:2]
+                assert np.array_equal(got[-1][0], o_out) and np.array_equal(got[-1][1], o_len), f"sentence {k}"
+        assert int(sess.tensor("chain_err", torch.int32, (1,)).cpu().numpy()[0]) == 0
+        sess.close()
+        outs[serial] = got
+    for k, (a, b) in enumerate(zip(outs["0"], outs["1"])):
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), f"sentence {k}"
+
+
 WIDE384 = G.ModelConfig("wide-384", 384, 6, 768, 2, 1, 600, ln_post=0, seed=83, random_gamma=True, weight_std=0.05)
 WIDE512 = G.ModelConfig("wide-512", 512, 8, 1024, 2, 1, 600, ln_post=0, seed=84, random_gamma=True, weight_std=0.05)
 
