@@ -531,7 +531,8 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     if (g.nslots >= (int)gridDim.x) {
       // one partial per block: a plain store, no atomic (atomics on one
       // address serialize), reduced by the consumer
-      chain_store(slot + blockIdx.x, b);
+      if (RAW) slot[blockIdx.x] = b;  // read after the launch, not by a chained kernel
+      else chain_store(slot + blockIdx.x, b);
     } else {
       // few slots: most blocks find a larger key already there, and the
       // test spares them the serialized atomic
