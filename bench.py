@@ -387,6 +387,20 @@ def main():
     tokens = int(outs[1].sum().item()) * args.steps
     ms_per_sentence = elapsed * 1e3 / (args.steps * w.batch)
 
+    # Latency distribution (outside the timed region): 50 translations, each
+    # between two events on the stream.
+    lat = []
+    cur = torch.cuda.current_stream()
+    for _ in range(50):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(cur)
+        step()
+        e1.record(cur)
+        e1.synchronize()
+        lat.append(e0.elapsed_time(e1))
+    lat_ms = {"median": round(float(np.median(lat)), 4), "p10": round(float(np.percentile(lat, 10)), 4),
+              "p90": round(float(np.percentile(lat, 90)), 4), "runs": len(lat)}
+
     # Dominant kernel: the decoder's fused logits + arg-max over the int8
     # embedding (batch 1), launched alone on one int8 row.
     fn, alg_bytes = _roofline_kernel(torch, np, mnmt, WL, G, info, blob, dev, None)  # the current stream
@@ -445,6 +459,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
         "ms_per_sentence": round(ms_per_sentence, 4),
+        "latency_ms_per_sentence": lat_ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -1084,6 +1084,12 @@ extern "C" int mnmt_translate(mnmt_session* S, const int32_t* d_src, const int32
       const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
       (void)hipGraphDestroy(graph);
       if (ei != hipSuccess) return hip_error(ei, "hipGraphInstantiate");
+      // the executable's device-side state now, not at its first launch
+      const hipError_t eu = hipGraphUpload(exec, s);
+      if (eu != hipSuccess) {
+        (void)hipGraphExecDestroy(exec);
+        return hip_error(eu, "hipGraphUpload");
+      }
       it = S->graphs.emplace(key, exec).first;
     }
     MNMT_HIP(hipGraphLaunch(it->second, s));
