@@ -216,14 +216,15 @@ __global__ __launch_bounds__(256) void k_qgemm_small(FusedIn in, const int8_t* _
 
 bool qgemm_small_fits(int M, int K) { return M >= 1 && M <= 64 && K <= kSmallMaxK && K % 64 == 0; }
 
-// Up to 256 rows and N <= 1024 the one-round-trip kernel (every
-// block loads its weight fragments for all of K at once) also beats the
-// LDS-slab GEMM, whose 64x64 tiles leave such shapes with a few dozen blocks
-// (the batched decoder's projections and feed-forward layers).  At 512 rows
-// or N = 2048 the repeated weight loads make it the slower of the two.
-constexpr int kSmallMaxRows = 256;
+// Up to 256 rows and N <= 1024, or 512 rows and N <= 512, the one-round-trip
+// kernel (every block loads its weight fragments for all of K at once) also
+// beats the LDS-slab GEMM, whose 64x64 tiles leave such shapes with a few
+// dozen blocks (the batched decoder's projections and feed-forward layers).
+// At 512 rows with N >= 1536, or N = 2048, the repeated weight loads make it
+// the slower of the two.
+constexpr int kSmallMaxRows = 512;
 bool qgemm_rows_fit(int M, int K, int N) {
-  return M >= 1 && M <= kSmallMaxRows && N <= 1024 && K <= kSmallMaxK && K % 64 == 0;
+  return M >= 1 && (M <= 256 ? N <= 1024 : M <= kSmallMaxRows && N <= 512) && K <= kSmallMaxK && K % 64 == 0;
 }
 
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
