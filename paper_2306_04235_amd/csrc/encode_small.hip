@@ -242,9 +242,13 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   __shared__ __attribute__((aligned(16))) int8_t vt[kEncHeadDim][kVtLd];  // values, transposed
   __shared__ __attribute__((aligned(16))) int8_t ctx[kEncRows][kHeadLd];
   __shared__ __attribute__((aligned(16))) float sc[kEncRows][kEncRows];      // scores, then probabilities
-  const int hd = blockIdx.x;
+  const int qs_n = at.qsplit, hd = blockIdx.x / qs_n, qs = blockIdx.x % qs_n;
   const int R = in.R, d = DMAX, dh = at.dh, S = in.S, ks = KS;
   const int mt_n = (R + 15) / 16;
+  // this block's query rows: the 16-row tiles qs, qs + qs_n, ... (keys and
+  // values of every row); row u of wave w is qrow(w + kEncWaves u)
+  const int q_rows = 16 * ((mt_n - qs + qs_n - 1) / qs_n);  // rows of its tiles (the last may be partial)
+  auto qrow = [&](int k) { return 16 * (qs + qs_n * (k / 16)) + (k % 16); };
   const int ntile = 3 * dh / 16;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
@@ -272,7 +276,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       of[u] = *(const v4i*)(at.Wo + n * d + hd * dh + 16 * min(kq, dh / 16 - 1));
     }
 #pragma unroll
-    for (int u = 0; u < RPW; ++u) nn[u] = at.len[min(wave + kEncWaves * u, R - 1) / S];
+    for (int u = 0; u < RPW; ++u) nn[u] = at.len[min(qrow(min(wave + kEncWaves * u, q_rows - 1)), R - 1) / S];
   });
   lds_barrier();
   // 2. Q, K, V of the head, requantized into LDS (V transposed)
@@ -284,6 +288,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
     const int part = (j >= dh) + (j >= 2 * dh);
     const int c = j - part * dh;
     for (int mt = 0; mt < mt_n; ++mt) {
+      if (part == 0 && mt % qs_n != qs) continue;  // queries of this block's rows only
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk)
@@ -301,8 +306,9 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   }
   lds_barrier();
   // 3. scores q . k (int32 exact) scaled by c_qk, every (query, key) pair
-  for (int t = wave; t < mt_n * mt_n; t += kEncWaves) {
-    const int mt = t / mt_n, kt = t % mt_n;
+  const int qt_n = q_rows / 16;  // this block's query tiles
+  for (int t = wave; t < qt_n * mt_n; t += kEncWaves) {
+    const int mt = qs + qs_n * (t / mt_n), kt = t % mt_n;
     const v4i acc = mfma16(lds_frag(&qk[0][0][0], kHeadLd, 16 * mt, 0, dh),
                            lds_frag(&qk[1][0][0], kHeadLd, 16 * kt, 0, dh), v4i{0, 0, 0, 0});
 #pragma unroll
@@ -314,40 +320,45 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   //    n up to S rounded up to 4 get probability 0: fma(0, v, acc) leaves acc
   //    unchanged bit for bit, so the context loop may run over them
   {
+    // rows of this wave: u < nu (the same count for every lane of the wave)
+    const int nu = (q_rows - wave + kEncWaves - 1) / kEncWaves;
     float sv[RPW], ex[RPW];
 #pragma unroll
     for (int u = 0; u < RPW; ++u) {
-      const int m = min(wave + kEncWaves * u, R - 1);
+      const int m = min(qrow(min(wave + kEncWaves * u, q_rows - 1)), R - 1);
       const int b = m / S;
       nn[u] = nn[u] < 1 ? 1 : (nn[u] > S ? S : nn[u]);
       sv[u] = lane < nn[u] ? sc[m][b * S + lane] : -FLT_MAX;
     }
     float mx[RPW], inv[RPW];
 #pragma unroll
-    for (int u = 0; u < RPW; ++u) mx[u] = wave_max(sv[u]);
+    for (int u = 0; u < RPW; ++u) mx[u] = u < nu ? wave_max(sv[u]) : 0.0f;
 #pragma unroll
-    for (int u = 0; u < RPW; ++u) ex[u] = lane < nn[u] ? canon_exp(sv[u] - mx[u]) : 0.0f;
+    for (int u = 0; u < RPW; ++u) ex[u] = u < nu && lane < nn[u] ? canon_exp(sv[u] - mx[u]) : 0.0f;
 #pragma unroll
-    for (int u = 0; u < RPW; ++u) inv[u] = 1.0f / wave_sum(ex[u]);
+    for (int u = 0; u < RPW; ++u) inv[u] = u < nu ? 1.0f / wave_sum(ex[u]) : 0.0f;
     wave_sync();  // every lane has read its scores before any probability is written
     const int s4 = (S + 3) & ~3;
 #pragma unroll
     for (int u = 0; u < RPW; ++u) {
-      const int m = wave + kEncWaves * u;
-      if (m < R && lane < s4) sc[m][lane] = lane < nn[u] ? ex[u] * inv[u] : 0.0f;
+      const int k = wave + kEncWaves * u, m = qrow(k);
+      if (k < q_rows && m < R && lane < s4) sc[m][lane] = lane < nn[u] ? ex[u] * inv[u] : 0.0f;
     }
   }
   lds_barrier();
   // 5. context: ascending keys, one fma each, requantized
   {
-    // thread: column j = tid % dh of rows g0 + groups u (g0 = tid / dh), one
-    // fma chain per row over the keys of its sentence in ascending order.
-    // With one sentence the rows share each load of four values and read
-    // four probabilities at once; rows past R repeat row R - 1, unstored.
+    // thread: column j = tid % dh of the block's rows qrow(g0 + groups u)
+    // (g0 = tid / dh), one fma chain per row over the keys of its sentence in
+    // ascending order.  With one sentence the rows share each load of four
+    // values and read four probabilities at once; rows past R repeat row
+    // R - 1, unstored.
     constexpr int CPT = RPW;  // rows per thread at most (kEncThreads / dh >= kEncWaves groups)
     const int groups = kEncThreads / dh;
     const int j = threadIdx.x % dh, g0 = threadIdx.x / dh;
     if (S == R) {  // one sentence
+      // rows of this thread: u < cu (as many as CPT at the widest)
+      const int cu = (q_rows - g0 + groups - 1) / groups;
       float acc[CPT];
 #pragma unroll
       for (int u = 0; u < CPT; ++u) acc[u] = 0.0f;
@@ -358,7 +369,8 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
         for (int e = 0; e < 4; ++e) v[e] = (float)(int)(int8_t)(v4 >> (8 * e));
 #pragma unroll
         for (int u = 0; u < CPT; ++u) {
-          const float4 p = *(const float4*)&sc[min(g0 + groups * u, R - 1)][t];
+          if (u >= cu) break;
+          const float4 p = *(const float4*)&sc[min(qrow(min(g0 + groups * u, q_rows - 1)), R - 1)][t];
           acc[u] = fmaf(p.x, v[0], acc[u]);
           acc[u] = fmaf(p.y, v[1], acc[u]);
           acc[u] = fmaf(p.z, v[2], acc[u]);
@@ -367,11 +379,13 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       }
 #pragma unroll
       for (int u = 0; u < CPT; ++u) {
-        const int m = g0 + groups * u;
-        if (m < R) ctx[m][j] = code_of(acc[u] * at.c_pv);
+        const int k = g0 + groups * u, m = qrow(k);
+        if (k < q_rows && m < R) ctx[m][j] = code_of(acc[u] * at.c_pv);
       }
     } else {
-      for (int m = g0; m < R; m += groups) {
+      for (int k = g0; k < q_rows; k += groups) {
+        const int m = qrow(k);
+        if (m >= R) break;  // rows ascend with k
         const int base = (m / S) * S;
         float acc = 0.0f;
         for (int t = 0; t < S; ++t) acc = fmaf(sc[m][t], (float)vt[j][base + t], acc);
@@ -385,7 +399,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   for (int u = 0; u < OT; ++u) {
     const int n0 = 16 * (wave + kEncWaves * u);
     if (n0 >= d) continue;
-    for (int mt = 0; mt < mt_n; ++mt) {
+    for (int mt = qs; mt < mt_n; mt += qs_n) {
       const v4i acc = mfma16(lds_frag(&ctx[0][0], kHeadLd, 16 * mt, 0, dh), of[u], v4i{0, 0, 0, 0});
       add_frag(at.acc_out, d, acc, 16 * mt, n0 + l16, R);
     }
@@ -515,14 +529,19 @@ bool enc_small_fits(int R, int S, int d, int dh, int F) {
     default: return hipErrorInvalidValue;                \
   }
 
-hipError_t launch_enc_attn(const EncIn& in0, const EncAttn& at, int heads, hipStream_t s) {
+int enc_attn_qsplit(int R) { return R > 16 ? 2 : 1; }
+
+hipError_t launch_enc_attn(const EncIn& in0, const EncAttn& at0, int heads, hipStream_t s) {
   EncIn in = in0;
-  in.nblk = heads;
+  EncAttn at = at0;
+  at.qsplit = enc_attn_qsplit(in.R);
+  const int blocks = heads * at.qsplit;
+  in.nblk = blocks;
 #define MNMT_E(DM, RPW)                                                                          \
   if (in.embed)                                                                                  \
-    hipLaunchKernelGGL((k_enc_attn<DM, true, RPW>), dim3(heads), dim3(kEncThreads), 0, s, in, at); \
-  else                                                                                           \
-    hipLaunchKernelGGL((k_enc_attn<DM, false, RPW>), dim3(heads), dim3(kEncThreads), 0, s, in, at);
+    hipLaunchKernelGGL((k_enc_attn<DM, true, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, at); \
+  else                                                                                            \
+    hipLaunchKernelGGL((k_enc_attn<DM, false, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, at);
   MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
 #undef MNMT_E
   return hipGetLastError();

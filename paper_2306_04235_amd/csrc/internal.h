@@ -286,6 +286,7 @@ struct EncAttn {
   const int32_t* len;      // [B]
   float c_qk, c_pv;
   int32_t* acc_out;        // [R, d], zero on entry
+  int qsplit;              // blocks per head (set by the launcher): each takes every qsplit-th 16-row query tile
 };
 struct EncFfn {
   int F;
@@ -306,6 +307,7 @@ struct EncOut {            // every decoder layer's cross K|V projection of the 
   int layers;
 };
 bool enc_small_fits(int R, int S, int d, int dh, int F);
+int enc_attn_qsplit(int R);  // blocks per head of launch_enc_attn for R rows
 hipError_t launch_enc_attn(const EncIn& in, const EncAttn& at, int heads, hipStream_t s);
 hipError_t launch_enc_ffn(const EncIn& in, const EncFfn& f, hipStream_t s);
 hipError_t launch_enc_out(const EncIn& in, const EncOut& o, hipStream_t s);

@@ -312,7 +312,7 @@ int run_encoder_blocks(mnmt_session* S, hipStream_t s, Chain* ch = nullptr) {
       at.c_qk = Ly.sa_cqk;
       at.c_pv = Ly.sa_cpv;
       at.acc_out = acc_o[l & 1];
-      const hipStream_t ks = ch ? ch->next(in.chain, 2 * l, h, 1) : s;
+      const hipStream_t ks = ch ? ch->next(in.chain, 2 * l, h * enc_attn_qsplit(R), 1) : s;
       LAUNCH(launch_enc_attn(in, at, h, ks));
       std::swap(xa, xb);
     }
