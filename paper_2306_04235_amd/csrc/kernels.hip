@@ -338,9 +338,9 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
   }
 }
 
-// The same statistics and candidates with one 256-thread block per row, for
+// The same statistics and candidates with one 512-thread block per row, for
 // V a multiple of 4 up to kTopkMaxV: the row is loaded once into registers
-// (every load in flight at once: 16 bytes per load, up to 32 per thread), the
+// (every load in flight at once: 16 bytes per load, up to 16 per thread), the
 // maximum (order-free) taken from them, exp(z - max) of every element computed
 // by all threads into LDS, the canonical sum by wave 0 (lane l adds elements
 // l, l + 64, ... in ascending order, then the butterfly: the same order as the
@@ -354,7 +354,8 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
 // candidate order is total (score, then index), so neither the filter nor the
 // split over threads changes the result.
 constexpr int kTopkMaxV = 32768;
-constexpr int kTopkV4 = kTopkMaxV / 4 / 256;  // float4 per thread
+constexpr int kTopkThreads = 512, kTopkWaves = kTopkThreads / 64;
+constexpr int kTopkV4 = kTopkMaxV / 4 / kTopkThreads;  // float4 per thread
 constexpr int kTopkCap = 1024;                // entries of the filtered list
 
 __device__ __forceinline__ unsigned long long block_max_u64(unsigned long long v, unsigned long long* red) {
@@ -364,7 +365,7 @@ __device__ __forceinline__ unsigned long long block_max_u64(unsigned long long v
   __syncthreads();
   unsigned long long m = red[0];
 #pragma unroll
-  for (int w = 1; w < 4; ++w) m = red[w] > m ? red[w] : m;
+  for (int w = 1; w < kTopkWaves; ++w) m = red[w] > m ? red[w] : m;
   __syncthreads();  // red is reused by the next call
   return m;
 }
@@ -382,7 +383,7 @@ __device__ __forceinline__ void topk_lists(const float* c_lds, int V, unsigned l
     ls[k] = -FLT_MAX;
     lv[k] = INT_MAX;
   }
-  for (int v = tid; v < V; v += 256) {
+  for (int v = tid; v < V; v += kTopkThreads) {
     float c = c_lds[v];
     int cv = v;
     if (!better(c, cv, ls[K - 1], lv[K - 1])) continue;
@@ -420,13 +421,13 @@ __device__ __forceinline__ void topk_lists(const float* c_lds, int V, unsigned l
 }
 
 template <int K>
-__global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict__ logits, BeamState st,
+__global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* __restrict__ logits, BeamState st,
                                                          const int* __restrict__ step) {
   __shared__ float e_lds[kTopkMaxV];
   __shared__ float list_c[kTopkCap];
   __shared__ int list_v[kTopkCap];
-  __shared__ float redf[4];
-  __shared__ unsigned long long redk[4];
+  __shared__ float redf[kTopkWaves];
+  __shared__ unsigned long long redk[kTopkWaves];
   __shared__ int n_list;
   const int r = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -438,23 +439,25 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
   int* cand_tok = st.cand_tok + (size_t)r * K;
   float* cand_score = st.cand_score + (size_t)r * K;
   if (tid == 0) n_list = 0;
-  // 1. the row in registers (element 4 (tid + 256 k) + q), the thread's
+  // 1. the row in registers (element 4 (tid + kTopkThreads k) + q), the thread's
   //    maximum and the row's
   float4 zr[kTopkV4];
 #pragma unroll
-  for (int k = 0; k < kTopkV4; ++k) zr[k] = z4[min(tid + 256 * k, n4 - 1)];
+  for (int k = 0; k < kTopkV4; ++k) zr[k] = z4[min(tid + kTopkThreads * k, n4 - 1)];
   float tmx = -INFINITY;
 #pragma unroll
   for (int k = 0; k < kTopkV4; ++k)
-    if (tid + 256 * k < n4) tmx = fmaxf(tmx, fmaxf(fmaxf(zr[k].x, zr[k].y), fmaxf(zr[k].z, zr[k].w)));
+    if (tid + kTopkThreads * k < n4) tmx = fmaxf(tmx, fmaxf(fmaxf(zr[k].x, zr[k].y), fmaxf(zr[k].z, zr[k].w)));
   float mx = wave_max(fmaxf(tmx, -FLT_MAX));
   if (lane == 0) redf[wave] = mx;
   __syncthreads();
-  mx = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+  mx = redf[0];
+#pragma unroll
+  for (int w = 1; w < kTopkWaves; ++w) mx = fmaxf(mx, redf[w]);
   // 2. exp(z - max) of every element into LDS, then the canonical sum
 #pragma unroll
   for (int k = 0; k < kTopkV4; ++k) {
-    const int i = tid + 256 * k;
+    const int i = tid + kTopkThreads * k;
     if (i < n4) {
       e_lds[4 * i] = canon_exp(zr[k].x - mx);
       e_lds[4 * i + 1] = canon_exp(zr[k].y - mx);
@@ -496,11 +499,13 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
   __syncthreads();  // every read of redf[0] is done
   if (lane == 0) redf[wave] = fmaxf(kth, -FLT_MAX);
   __syncthreads();
-  const float tau = fmaxf(fmaxf(redf[0], redf[1]), fmaxf(redf[2], redf[3]));
+  float tau = redf[0];
+#pragma unroll
+  for (int w = 1; w < kTopkWaves; ++w) tau = fmaxf(tau, redf[w]);
   // 4. the filtered list: every score at or above the bound
 #pragma unroll
   for (int k = 0; k < kTopkV4; ++k) {
-    const int i = tid + 256 * k;
+    const int i = tid + kTopkThreads * k;
     if (i < n4) {
       const float c4[4] = {sc + (zr[k].x - lse), sc + (zr[k].y - lse), sc + (zr[k].z - lse),
                            sc + (zr[k].w - lse)};
@@ -520,7 +525,7 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
   const int n = n_list;
   if (n <= kTopkCap) {
     // 5. rank = the number of list entries that beat the entry
-    for (int i = tid; i < n; i += 256) {
+    for (int i = tid; i < n; i += kTopkThreads) {
       const float ci = list_c[i];
       const int vi = list_v[i];
       int rank = 0;
@@ -530,7 +535,7 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
         cand_score[rank] = ci;
       }
     }
-    for (int k = n + tid; k < K; k += 256) {  // fewer than K scores qualify
+    for (int k = n + tid; k < K; k += kTopkThreads) {  // fewer than K scores qualify
       cand_tok[k] = 0;
       cand_score[k] = -FLT_MAX;
     }
@@ -539,7 +544,7 @@ __global__ __launch_bounds__(256) void k_beam_topk_block(const float* __restrict
   // 5'. the overflow path: all scores into LDS, sorted lists, block merge
 #pragma unroll
   for (int k = 0; k < kTopkV4; ++k) {
-    const int i = tid + 256 * k;
+    const int i = tid + kTopkThreads * k;
     if (i < n4) {
       e_lds[4 * i] = sc + (zr[k].x - lse);
       e_lds[4 * i + 1] = sc + (zr[k].y - lse);
@@ -854,7 +859,7 @@ hipError_t launch_beam_reset(const BeamState& st, int* step, hipStream_t s) {
 hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int* step, hipStream_t s) {
   const int R = st.B * st.W;
   if (st.V <= kTopkMaxV && st.V % 4 == 0) {
-#define MNMT_TOPK(K) hipLaunchKernelGGL(k_beam_topk_block<K>, dim3(R), dim3(256), 0, s, logits, st, step)
+#define MNMT_TOPK(K) hipLaunchKernelGGL(k_beam_topk_block<K>, dim3(R), dim3(kTopkThreads), 0, s, logits, st, step)
     switch (2 * st.W) {
       case 2: MNMT_TOPK(2); break;
       case 4: MNMT_TOPK(4); break;
