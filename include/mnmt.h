@@ -199,8 +199,9 @@ int mnmt_session_tensor(const mnmt_session* session, const char* name, void** d_
 /* ---- single quantized linear layer --------------------------------------- */
 
 /* Y = epilogue(X W^T): d_X int8 [M, K] row-major (row stride K), d_W int8
- * [N, K] row-major, d_scale/d_bias fp32 [N] (bias may be NULL for I32 and
- * LOGITS), d_Y [M, N] of the epilogue's type.  K must be a positive multiple
+ * [N, K] row-major (for MNMT_EPI_ARGMAX_PARTIAL_PACKED: mnmt_pack_weights'
+ * copy of it), d_scale/d_bias fp32 [N] (bias may be NULL for I32, LOGITS and
+ * the arg-max epilogues), d_Y [M, N] of the epilogue's type.  K must be a positive multiple
  * of 64 and at most 8192; M >= 0, N >= 1.  M <= 8 runs the wavefront
  * reduction kernel (the arg-max epilogue at M <= 2, K <= 512: the decoder's
  * logits kernel on the matrix cores), larger M the i8 matrix-core kernels. */
@@ -228,8 +229,8 @@ size_t mnmt_packed_bytes(int N, int K);
 int mnmt_pack_weights(const int8_t* d_W, int N, int K, int8_t* d_P, void* stream);
 
 /* mnmt_qlinear with timing events (hipEvent_t, created with timing enabled,
- * or NULL).  On the fused arg-max path (MNMT_EPI_ARGMAX or
- * MNMT_EPI_ARGMAX_PARTIAL, M <= 2, K <= 512:
+ * or NULL).  On the fused arg-max path (MNMT_EPI_ARGMAX,
+ * MNMT_EPI_ARGMAX_PARTIAL or MNMT_EPI_ARGMAX_PARTIAL_PACKED, M <= 2, K <= 512:
  * the decoder's logits kernel on int8 rows) the two events take the kernel's
  * own start and end times (hipExtLaunchKernel), so their elapsed time is the
  * kernel's duration without launch gaps; on other paths they are recorded on
