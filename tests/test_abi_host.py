@@ -89,3 +89,24 @@ def test_fold_requant_matches_oracle_bitwise():
         r = oracle.fold_requant(s_in, s_w, b, s_out)
         assert np.array_equal(a[0].view(np.uint32), r[0].view(np.uint32))
         assert np.array_equal(a[1].view(np.uint32), r[1].view(np.uint32))
+
+
+def test_packed_bytes_sizes():
+    """The fragment-order copy of an int8 [N, K] weight takes whole 16-row
+    tiles; sizes that cannot be packed give 0."""
+    L = mnmt.lib()
+    assert L.mnmt_packed_bytes(32000, 256) == 32000 * 256
+    assert L.mnmt_packed_bytes(33, 64) == 48 * 64
+    assert L.mnmt_packed_bytes(1, 512) == 16 * 512
+    for N, K in ((0, 64), (-1, 64), (16, 0), (16, 100), (16, -64)):
+        assert L.mnmt_packed_bytes(N, K) == 0
+
+
+def test_model_arena_holds_the_packed_embedding():
+    """The arena holds every weight plus the fragment-order copy of the tied
+    embedding that the batch-1 logits kernel reads."""
+    blob = model_blob("MOBILE")
+    hdr, t = read_model(blob)
+    V, d = np.asarray(t["emb.w"]).shape
+    weights = sum(np.asarray(a).size for k, a in t.items() if k.endswith(".w"))
+    assert mnmt.mnmt_model_bytes(blob) >= weights + mnmt.lib().mnmt_packed_bytes(V, d)
