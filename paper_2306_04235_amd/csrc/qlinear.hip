@@ -163,16 +163,20 @@ hipError_t gemv_lpr(const int8_t* X, int ldx, const int8_t* W, const float* scal
 // (embedding / LayerNorm / quantization of fp32 rows) into LDS.
 constexpr int kSmallMaxK = 1024;
 
-template <bool LN, int KMAX>  // K <= KMAX
-__global__ __launch_bounds__(256) void k_qgemm_small(FusedIn in, const int8_t* __restrict__ X, int ldx,
-                                                     const int8_t* __restrict__ W, int M, int K, int N,
-                                                     const float* __restrict__ scale, const float* __restrict__ bias,
-                                                     EpiArgs e) {
+// WAVES 4: a 32x32 tile per block; WAVES 1 (no LN): a 16x16 tile per
+// one-wave block, four times the blocks over the same waves.
+template <bool LN, int KMAX, int WAVES = 4>  // K <= KMAX
+__global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const int8_t* __restrict__ X, int ldx,
+                                                            const int8_t* __restrict__ W, int M, int K, int N,
+                                                            const float* __restrict__ scale,
+                                                            const float* __restrict__ bias, EpiArgs e) {
+  static_assert(WAVES == 4 || (WAVES == 1 && !LN), "32x32 tiles, or 16x16 without the row prologue");
   constexpr int NK = (KMAX + 63) / 64;
+  constexpr int TILE = WAVES == 4 ? 32 : 16;
   __shared__ __attribute__((aligned(16))) int8_t As[LN ? 32 * (KMAX + 16) : 16];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = WAVES == 4 ? threadIdx.x >> 6 : 0;
   const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
+  const int m0 = blockIdx.y * TILE, n0 = blockIdx.x * TILE;
   const int nk = K / 64;
   const int col = n0 + 16 * wn + (lane & 15);
   const int koff = 16 * (lane >> 4);
@@ -231,12 +235,18 @@ hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const
                               const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s) {
   if (M < 1 || M > (in ? 64 : kSmallMaxRows) || K > kSmallMaxK || K % 64 || (in && K > kMaxRowLen))
     return hipErrorInvalidValue;
-  dim3 grid((N + 31) / 32, (M + 31) / 32);
+  // 65-256 rows (the mobile beam decoder): one-wave blocks of 16x16 (at 512
+  // rows their four-fold block count made the base beam step slower)
+  const bool one = !in && M > 64 && M <= 256;
+  const dim3 grid = one ? dim3((N + 15) / 16, (M + 15) / 16) : dim3((N + 31) / 32, (M + 31) / 32);
   const FusedIn none{};
-#define MNMT_SMALL(KM)                                                                                      \
-  if (in)                                                                                                   \
+#define MNMT_SMALL(KM)                                                                                       \
+  if (in)                                                                                                    \
     hipLaunchKernelGGL((k_qgemm_small<true, KM>), grid, dim3(256), 0, s, *in, X, ldx, W, M, K, N, scale, bias, e); \
-  else                                                                                                      \
+  else if (one)                                                                                              \
+    hipLaunchKernelGGL((k_qgemm_small<false, KM, 1>), grid, dim3(64), 0, s, none, X, ldx, W, M, K, N, scale, bias, \
+                       e);                                                                                   \
+  else                                                                                                       \
     hipLaunchKernelGGL((k_qgemm_small<false, KM>), grid, dim3(256), 0, s, none, X, ldx, W, M, K, N, scale, bias, e);
   switch (row_class(K)) {
     case 64: MNMT_SMALL(64) break;
