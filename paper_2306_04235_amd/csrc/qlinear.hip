@@ -9,7 +9,8 @@
 //    instruction reads 64 * 16 = 1024 contiguous bytes; U independent row
 //    groups per wave keep several loads in flight.  Products use the 4-way
 //    int8 dot instruction; the LPR partial sums meet in an xor butterfly.
-//  * qgemm_small: 8 < M <= 64 and K <= 1024 (the batch-1 encoder), 16x16x64
+//  * qgemm_small: 8 < M <= 64 and K <= 1024 (the batch-1 encoder), and the
+//    batched decoder's 65-512-row projections of moderate N, 16x16x64
 //    matrix-core fragments loaded straight from memory.
 // Larger M runs the tiled matrix-core GEMM of gemm.hip.
 // Integer accumulation is exact, so neither kernel's order matters; the fp32
@@ -155,7 +156,7 @@ hipError_t gemv_lpr(const int8_t* X, int ldx, const int8_t* W, const float* scal
 }
 
 // ---------------------------------------------------------------------------
-// qgemm_small: M <= 64, K <= 1024 (the batch-1 encoder).  A 32x32 output tile
+// qgemm_small: K <= 1024, up to 512 rows (see qgemm_rows_fit).  A 32x32 output tile
 // per block, one 16x16 tile per wave on v_mfma_i32_16x16x64_i8.  Each lane's
 // operand is 16 contiguous K bytes of one row, so weight fragments are loaded
 // straight from global memory, all of K at once (a single round trip).  The
