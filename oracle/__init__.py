@@ -32,6 +32,8 @@ def lib():
         L.orc_log.argtypes = [f32]
         L.orc_canon_sum.restype = f32
         L.orc_canon_sum.argtypes = [vp, i32]
+        L.orc_canon_sum_squares.restype = f32
+        L.orc_canon_sum_squares.argtypes = [vp, i32]
         L.orc_quantize.restype = C.c_int8
         L.orc_quantize.argtypes = [f32, f32]
         L.orc_length_penalty.restype = f32
@@ -55,6 +57,8 @@ def lib():
         L.orc_decoder_logits.argtypes = [vp, vp, i32, vp, i32, vp]
         L.orc_decoder_logits_full.argtypes = [vp, vp, i32, vp, i32, vp]
         L.orc_translate_beam.argtypes = [vp, vp, vp, i32, i32, i32, i32, f32, vp, vp, vp]
+        L.orc_encode_trace.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp]
+        L.orc_decoder_trace.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -98,6 +102,18 @@ def log_array(x):
 def canon_sum(x) -> np.float32:
     x = _c(x, np.float32)
     return np.float32(lib().orc_canon_sum(_p(x), x.size))
+
+
+def canon_sum_squares(x) -> np.float32:
+    x = _c(x, np.float32)
+    return np.float32(lib().orc_canon_sum_squares(_p(x), x.size))
+
+
+def fold_dequant(s_in, s_w):
+    s_w = _c(s_w, np.float32)
+    out = np.empty_like(s_w)
+    lib().orc_fold_dequant(float(s_in), _p(s_w), s_w.size, _p(out))
+    return out
 
 
 def quantize(y: float, inv_s: float) -> int:
@@ -233,6 +249,34 @@ class Model:
         _check(lib().orc_decoder_logits_full(self._h, _p(src_row), src_row.size, _p(tokens), tokens.size,
                                              _p(z)), "decoder_logits_full")
         return z
+
+    def encode_trace(self, src_row):
+        """One sentence's encoder with its intermediate values: dict with x [U+1, S, d]
+        fp32, a [U, S, d], pj [U, S, P], ctx [U, S, d] int8 (U = 2 n_enc,
+        P = max(3d, F); FFN sublayers leave ctx zero) and enc [S, d]."""
+        src_row = _c(src_row, np.int32)
+        S, d, U = src_row.size, self.d, 2 * self.n_enc
+        P = max(3 * d, self.F)
+        t = dict(x=np.zeros((U + 1, S, d), np.float32), a=np.zeros((U, S, d), np.int8),
+                 pj=np.zeros((U, S, P), np.int8), ctx=np.zeros((U, S, d), np.int8), enc=np.zeros((S, d), np.int8))
+        _check(lib().orc_encode_trace(self._h, _p(src_row), S, _p(t["x"]), _p(t["a"]), _p(t["pj"]), _p(t["ctx"]),
+                                      _p(t["enc"])), "encode_trace")
+        return t
+
+    def decoder_trace(self, src_row, tokens):
+        """Teacher-forced decoding (inputs BOS, tokens[:-1]) with each step's
+        intermediate values: x [U+1, n, d], a, pj, ctx as in encode_trace
+        (U = 3 n_dec), fin [n, d] (int8 input of the output projection) and
+        z [n, V] logits."""
+        src_row, tokens = _c(src_row, np.int32), _c(tokens, np.int32)
+        n, d, U = tokens.size, self.d, 3 * self.n_dec
+        P = max(3 * d, self.F)
+        t = dict(x=np.zeros((U + 1, n, d), np.float32), a=np.zeros((U, n, d), np.int8),
+                 pj=np.zeros((U, n, P), np.int8), ctx=np.zeros((U, n, d), np.int8), fin=np.zeros((n, d), np.int8),
+                 z=np.zeros((n, self.V), np.float32))
+        _check(lib().orc_decoder_trace(self._h, _p(src_row), src_row.size, _p(tokens), n, _p(t["x"]), _p(t["a"]),
+                                       _p(t["pj"]), _p(t["ctx"]), _p(t["fin"]), _p(t["z"])), "decoder_trace")
+        return t
 
     def beam(self, src, lens, beam, max_steps, alpha=0.6):
         src, lens = _c(src, np.int32), _c(lens, np.int32)

@@ -59,7 +59,7 @@ float orc_canon_sum(const float* x, int n) {
 }
 
 /* Sum of squares in the same order; each partial accumulates with one fma. */
-static float canon_sum_squares(const float* x, int n) {
+float orc_canon_sum_squares(const float* x, int n) {
   float p[64];
   for (int l = 0; l < 64; ++l) p[l] = 0.0f;
   for (int i = 0; i < n; ++i) p[i % 64] = fmaf(x[i], x[i], p[i % 64]);
@@ -220,7 +220,7 @@ static void layer_norm_row(const float* x, int d, const float* g, const float* b
   float inv_d = 1.0f / (float)d;
   float mu = orc_canon_sum(x, d) * inv_d;
   for (int i = 0; i < d; ++i) delta[i] = x[i] - mu;
-  float var = canon_sum_squares(delta, d) * inv_d;
+  float var = orc_canon_sum_squares(delta, d) * inv_d;
   float rstd = 1.0f / sqrtf(var + eps);
   for (int i = 0; i < d; ++i) y[i] = fmaf(delta[i] * rstd, g[i], b[i]);
   free(delta);
@@ -701,6 +701,33 @@ static void linear_i8(const linear_t* L, const int8_t* a, int rows, int relu, in
   orc_qlinear(a, L->w, rows, L->K, L->N, L->scale, L->bias, 1.0f, relu ? ORC_EPI_I8_RELU : ORC_EPI_I8, y);
 }
 
+/* Copies of a forward pass's intermediate values (orc_encode_trace,
+ * orc_decoder_trace): the sublayers u = 0, 1, ... of all layers in order
+ * (encoder: self-attention, FFN; decoder: self-attention, cross-attention,
+ * FFN), each traced for `rows` rows starting at row `row0`.  Slots:
+ *   x   [U + 1][rows][d]  residual stream entering sublayer u; slot U after the last
+ *   a   [U][rows][d]      int8 input of the sublayer's first linear layer
+ *   pj  [U][rows][P]      QKV codes (self-attention, 3d), Q codes (cross, d) or the
+ *                         ReLU hidden codes (FFN, F); P = max(3d, F)
+ *   ctx [U][rows][d]      attention context codes (FFN sublayers: not written)
+ * Any pointer may be NULL.  Copying changes none of the arithmetic. */
+typedef struct {
+  float* x;
+  int8_t* a;
+  int8_t* pj;
+  int8_t* ctx;
+  int rows, row0, P;
+} trace_t;
+
+static void tr_x(const orc_model* m, const trace_t* tr, int u, const float* x, int n) {
+  if (tr && tr->x) memcpy(tr->x + ((size_t)u * tr->rows + tr->row0) * m->d, x, sizeof(float) * (size_t)n * m->d);
+}
+
+static void tr_i8(const trace_t* tr, int8_t* base, int u, int width, const int8_t* v, int n) {
+  if (!tr || !base) return;
+  for (int r = 0; r < n; ++r) memcpy(base + ((size_t)u * tr->rows + tr->row0 + r) * width, v + (size_t)r * width, (size_t)width);
+}
+
 /* Token embedding (shared matrix, scaled by sqrt(d)) plus the sinusoidal
  * position table stored in the model file: x = fma(E[tok], c_emb[tok], PE[pos]). */
 static void embed(const orc_model* m, int tok, int pos, float* x) {
@@ -709,18 +736,24 @@ static void embed(const orc_model* m, int tok, int pos, float* x) {
   for (int j = 0; j < m->d; ++j) x[j] = fmaf((float)e[j], m->c_emb[tok], pe[j]);
 }
 
-static void ffn_sublayer(const orc_model* m, const ffn_t* f, float* x, int rows) {
+static void ffn_sublayer(const orc_model* m, const ffn_t* f, float* x, int rows, const trace_t* tr, int u) {
   int8_t* a = (int8_t*)malloc((size_t)rows * m->d);
   int8_t* hb = (int8_t*)malloc((size_t)rows * m->F);
+  tr_x(m, tr, u, x, rows);
   sublayer_input(m, &f->ln, x, rows, f->w1.inv_in, a);
   linear_i8(&f->w1, a, rows, 1, hb);
+  if (tr) {
+    tr_i8(tr, tr->a, u, m->d, a, rows);
+    for (int r = 0; r < rows && tr->pj; ++r)
+      memcpy(tr->pj + ((size_t)u * tr->rows + tr->row0 + r) * tr->P, hb + (size_t)r * m->F, (size_t)m->F);
+  }
   residual_linear(m, &f->w2, &f->ln, f->gamma, hb, rows, x);
   free(a);
   free(hb);
 }
 
 /* Encoder of one sentence of S tokens -> enc codes [S, d] (scale s_enc). */
-static void encode_sentence(const orc_model* m, const int32_t* src, int S, int8_t* enc) {
+static void encode_sentence(const orc_model* m, const int32_t* src, int S, int8_t* enc, const trace_t* tr) {
   int d = m->d, dh = m->dh;
   float* x = (float*)malloc(sizeof(float) * (size_t)S * d);
   int8_t* a = (int8_t*)malloc((size_t)S * d);
@@ -729,15 +762,23 @@ static void encode_sentence(const orc_model* m, const int32_t* src, int S, int8_
   for (int t = 0; t < S; ++t) embed(m, src[t], t, x + (size_t)t * d);
   for (int l = 0; l < m->Le; ++l) {
     const layer_t* L = &m->enc[l];
+    tr_x(m, tr, 2 * l, x, S);
     sublayer_input(m, &L->sa.ln, x, S, L->sa.qkv.inv_in, a);
     linear_i8(&L->sa.qkv, a, S, 0, qkv);
     for (int t = 0; t < S; ++t)
       for (int hd = 0; hd < m->h; ++hd)
         orc_attend(qkv + (size_t)t * 3 * d + hd * dh, qkv + d + hd * dh, qkv + 2 * d + hd * dh, S, dh, 3 * d,
                    L->sa.c_qk, L->sa.c_pv, ctx + (size_t)t * d + hd * dh);
+    if (tr) {
+      tr_i8(tr, tr->a, 2 * l, d, a, S);
+      tr_i8(tr, tr->ctx, 2 * l, d, ctx, S);
+      for (int t = 0; t < S && tr->pj; ++t)
+        memcpy(tr->pj + ((size_t)(2 * l) * tr->rows + t) * tr->P, qkv + (size_t)t * 3 * d, (size_t)3 * d);
+    }
     residual_linear(m, &L->sa.o, &L->sa.ln, L->sa.gamma, ctx, S, x);
-    ffn_sublayer(m, &L->ff, x, S);
+    ffn_sublayer(m, &L->ff, x, S, tr, 2 * l + 1);
   }
+  tr_x(m, tr, 2 * m->Le, x, S);
   if (!m->post)
     orc_layernorm_quant(x, S, d, m->enc_ln.g, m->enc_ln.b, m->eps, m->inv_enc, enc, NULL);
   else
@@ -762,7 +803,7 @@ int orc_encode(const orc_model* m, const int32_t* src, const int32_t* len, int B
   int rc = check_batch(m, src, len, B, S_max);
   if (rc) return rc;
   memset(enc, 0, (size_t)B * S_max * m->d);
-  for (int b = 0; b < B; ++b) encode_sentence(m, src + (size_t)b * S_max, len[b], enc + (size_t)b * S_max * m->d);
+  for (int b = 0; b < B; ++b) encode_sentence(m, src + (size_t)b * S_max, len[b], enc + (size_t)b * S_max * m->d, NULL);
   return ORC_OK;
 }
 
@@ -814,7 +855,7 @@ static void cache_free(const orc_model* m, kv_cache_t* c) {
  * the cache, attends over positions 0..t (self) and over the S source
  * positions (cross), and writes the logits z[V]. */
 static void decoder_step(const orc_model* m, int tok, int t, kv_cache_t* c, int8_t* const* cross_kv, int S,
-                         float* z) {
+                         float* z, const trace_t* tr, int8_t* fin) {
   int d = m->d, dh = m->dh;
   float* x = (float*)malloc(sizeof(float) * (size_t)d);
   int8_t* a = (int8_t*)malloc((size_t)d);
@@ -824,7 +865,9 @@ static void decoder_step(const orc_model* m, int tok, int t, kv_cache_t* c, int8
   embed(m, tok, t, x);
   for (int l = 0; l < m->Ld; ++l) {
     const layer_t* L = &m->dec[l];
+    const int u = 3 * l;
     /* self-attention over the cache (causal: positions 0..t) */
+    tr_x(m, tr, u, x, 1);
     sublayer_input(m, &L->sa.ln, x, 1, L->sa.qkv.inv_in, a);
     linear_i8(&L->sa.qkv, a, 1, 0, qkv);
     memcpy(c->k[l] + (size_t)t * d, qkv + d, (size_t)d);
@@ -832,20 +875,33 @@ static void decoder_step(const orc_model* m, int tok, int t, kv_cache_t* c, int8
     for (int hd = 0; hd < m->h; ++hd)
       orc_attend(qkv + hd * dh, c->k[l] + hd * dh, c->v[l] + hd * dh, t + 1, dh, d, L->sa.c_qk, L->sa.c_pv,
                  ctx + hd * dh);
+    if (tr) {
+      tr_i8(tr, tr->a, u, d, a, 1);
+      tr_i8(tr, tr->ctx, u, d, ctx, 1);
+      if (tr->pj) memcpy(tr->pj + ((size_t)u * tr->rows + tr->row0) * tr->P, qkv, (size_t)3 * d);
+    }
     residual_linear(m, &L->sa.o, &L->sa.ln, L->sa.gamma, ctx, 1, x);
     /* cross-attention over the encoder output */
+    tr_x(m, tr, u + 1, x, 1);
     sublayer_input(m, &L->ca.ln, x, 1, L->ca.q.inv_in, a);
     linear_i8(&L->ca.q, a, 1, 0, q);
     for (int hd = 0; hd < m->h; ++hd)
       orc_attend(q + hd * dh, cross_kv[l] + hd * dh, cross_kv[l] + d + hd * dh, S, dh, 2 * d, L->ca.c_qk,
                  L->ca.c_pv, ctx + hd * dh);
+    if (tr) {
+      tr_i8(tr, tr->a, u + 1, d, a, 1);
+      tr_i8(tr, tr->ctx, u + 1, d, ctx, 1);
+      if (tr->pj) memcpy(tr->pj + ((size_t)(u + 1) * tr->rows + tr->row0) * tr->P, q, (size_t)d);
+    }
     residual_linear(m, &L->ca.o, &L->ca.ln, L->ca.gamma, ctx, 1, x);
-    ffn_sublayer(m, &L->ff, x, 1);
+    ffn_sublayer(m, &L->ff, x, 1, tr, u + 2);
   }
+  tr_x(m, tr, 3 * m->Ld, x, 1);
   if (!m->post)
     orc_layernorm_quant(x, 1, d, m->dec_ln.g, m->dec_ln.b, m->eps, m->inv_fin, a, NULL);
   else
     for (int j = 0; j < d; ++j) a[j] = orc_quantize(x[j], m->inv_fin);
+  if (fin) memcpy(fin, a, (size_t)d);
   /* tied output projection over the shared embedding */
   orc_qlinear(a, m->E, 1, d, m->V, m->c_out, NULL, 1.0f, ORC_EPI_LOGITS, z);
   free(x);
@@ -857,7 +913,7 @@ static void decoder_step(const orc_model* m, int tok, int t, kv_cache_t* c, int8
 
 static int8_t** build_cross(const orc_model* m, const int32_t* src, int S) {
   int8_t* enc = (int8_t*)malloc((size_t)S * m->d);
-  encode_sentence(m, src, S, enc);
+  encode_sentence(m, src, S, enc, NULL);
   int8_t** kv = (int8_t**)malloc(sizeof(int8_t*) * (size_t)m->Ld);
   for (int l = 0; l < m->Ld; ++l) {
     kv[l] = (int8_t*)malloc((size_t)S * 2 * m->d);
@@ -890,7 +946,7 @@ int orc_translate_greedy(const orc_model* m, const int32_t* src, const int32_t* 
         out[(size_t)b * steps + t] = m->pad_id;
         continue;
       }
-      decoder_step(m, tok, t, &c, cross, len[b], z);
+      decoder_step(m, tok, t, &c, cross, len[b], z, NULL, NULL);
       if (logits) memcpy(logits + ((size_t)b * steps + t) * m->V, z, sizeof(float) * (size_t)m->V);
       int best = 0;
       for (int v = 1; v < m->V; ++v)
@@ -921,7 +977,44 @@ int orc_decoder_logits(const orc_model* m, const int32_t* src, int S, const int3
   int8_t** cross = build_cross(m, src, S);
   kv_cache_t c;
   cache_alloc(m, &c, n);
-  for (int t = 0; t < n; ++t) decoder_step(m, t == 0 ? m->bos_id : tok[t - 1], t, &c, cross, S, z + (size_t)t * m->V);
+  for (int t = 0; t < n; ++t)
+    decoder_step(m, t == 0 ? m->bos_id : tok[t - 1], t, &c, cross, S, z + (size_t)t * m->V, NULL, NULL);
+  cache_free(m, &c);
+  free_cross(m, cross);
+  return ORC_OK;
+}
+
+/* The encoder of one sentence with its intermediate values copied out (see
+ * trace_t; U = 2 n_enc sublayers, rows = S) and its output codes enc [S, d]. */
+int orc_encode_trace(const orc_model* m, const int32_t* src, int S, float* x, int8_t* a, int8_t* pj, int8_t* ctx,
+                     int8_t* enc) {
+  if (!m || !src || !enc || S < 1 || S > m->P) return ORC_E_ARG;
+  for (int t = 0; t < S; ++t)
+    if (src[t] < 0 || src[t] >= m->V) return ORC_E_ARG;
+  trace_t tr = {x, a, pj, ctx, S, 0, 3 * m->d > m->F ? 3 * m->d : m->F};
+  encode_sentence(m, src, S, enc, &tr);
+  return ORC_OK;
+}
+
+/* Teacher-forced decoding (as orc_decoder_logits) with each step's
+ * intermediate values copied out: trace_t with U = 3 n_dec sublayers and one
+ * row per step; fin [n, d] receives each step's int8 input of the output
+ * projection, z [n, V] the logits. */
+int orc_decoder_trace(const orc_model* m, const int32_t* src, int S, const int32_t* tok, int n, float* x, int8_t* a,
+                      int8_t* pj, int8_t* ctx, int8_t* fin, float* z) {
+  if (!m || !src || !tok || !z || S < 1 || S > m->P || n < 1 || n > m->P) return ORC_E_ARG;
+  for (int t = 0; t < S; ++t)
+    if (src[t] < 0 || src[t] >= m->V) return ORC_E_ARG;
+  for (int t = 0; t < n; ++t)
+    if (tok[t] < 0 || tok[t] >= m->V) return ORC_E_ARG;
+  int8_t** cross = build_cross(m, src, S);
+  kv_cache_t c;
+  cache_alloc(m, &c, n);
+  for (int t = 0; t < n; ++t) {
+    trace_t tr = {x, a, pj, ctx, n, t, 3 * m->d > m->F ? 3 * m->d : m->F};
+    decoder_step(m, t == 0 ? m->bos_id : tok[t - 1], t, &c, cross, S, z + (size_t)t * m->V, &tr,
+                 fin ? fin + (size_t)t * m->d : NULL);
+  }
   cache_free(m, &c);
   free_cross(m, cross);
   return ORC_OK;
@@ -960,7 +1053,7 @@ int orc_decoder_logits_full(const orc_model* m, const int32_t* src, int S, const
         orc_attend(q + (size_t)t * d + hd * dh, cross[l] + hd * dh, cross[l] + d + hd * dh, S, dh, 2 * d,
                    L->ca.c_qk, L->ca.c_pv, ctx + (size_t)t * d + hd * dh);
     residual_linear(m, &L->ca.o, &L->ca.ln, L->ca.gamma, ctx, n, x);
-    ffn_sublayer(m, &L->ff, x, n);
+    ffn_sublayer(m, &L->ff, x, n, NULL, 0);
   }
   if (!m->post)
     orc_layernorm_quant(x, n, d, m->dec_ln.g, m->dec_ln.b, m->eps, m->inv_fin, a, NULL);
@@ -1030,7 +1123,7 @@ static void translate_one_beam(const orc_model* m, const int32_t* src, int S, in
     for (int j = 0; j < W; ++j) {
       if (!alive[j]) continue;
       int tok = t == 0 ? m->bos_id : toks[(size_t)j * T + t - 1];
-      decoder_step(m, tok, t, &cache[j], cross, S, z);
+      decoder_step(m, tok, t, &cache[j], cross, S, z, NULL, NULL);
       float lse;
       orc_log_softmax_stats(z, V, NULL, &lse);
       for (int v = 0; v < V; ++v) {

@@ -43,6 +43,7 @@ typedef struct orc_model orc_model;
 float orc_exp(float x);                       /* e^x for x <= 0 */
 float orc_log(float x);                       /* ln x for normal x > 0 */
 float orc_canon_sum(const float* x, int n);   /* 64 interleaved partial sums, halving combine */
+float orc_canon_sum_squares(const float* x, int n); /* the same order, partials p = fma(x, x, p) */
 int8_t orc_quantize(float y, float inv_s);    /* clamp(rne(y * inv_s), -127, 127) */
 float orc_length_penalty(int L, float alpha); /* ((5 + L) / 6)^alpha */
 int orc_map(int fn, const float* x, int n, float* y); /* fn 0: orc_exp, 1: orc_log */
@@ -82,6 +83,20 @@ int orc_decoder_logits(const orc_model* m, const int32_t* src, int S, const int3
 /* The same logits from a cache-free block computation with a causal mask. */
 int orc_decoder_logits_full(const orc_model* m, const int32_t* src, int S, const int32_t* tok, int n,
                             float* z);
+/* Intermediate values for stage-by-stage tests.  Sublayers u in order
+ * (encoder: self-attention, FFN; decoder: self-attention, cross-attention,
+ * FFN), U of them; P = max(3d, F).  Any of x, a, pj, ctx may be NULL.
+ *   x [U+1][rows][d] fp32 residual stream entering sublayer u (slot U: after the last)
+ *   a [U][rows][d] int8 input of the sublayer's first linear layer
+ *   pj [U][rows][P] int8 QKV (3d), cross Q (d) or FFN hidden (F) codes
+ *   ctx [U][rows][d] int8 attention context codes
+ * Encoder of one sentence: rows = S, enc [S, d] output codes. */
+int orc_encode_trace(const orc_model* m, const int32_t* src, int S, float* x, int8_t* a, int8_t* pj, int8_t* ctx,
+                     int8_t* enc);
+/* Teacher-forced decoding with rows = n steps; fin [n, d] the int8 input of
+ * the output projection at each step (or NULL); z [n, V] logits. */
+int orc_decoder_trace(const orc_model* m, const int32_t* src, int S, const int32_t* tok, int n, float* x, int8_t* a,
+                      int8_t* pj, int8_t* ctx, int8_t* fin, float* z);
 /* Beam search: out [B, max_steps] (PAD-filled), out_len [B], score [B]. */
 int orc_translate_beam(const orc_model* m, const int32_t* src, const int32_t* len, int B, int S_max,
                        int beam, int max_steps, float alpha, int32_t* out, int32_t* out_len,

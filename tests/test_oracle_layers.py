@@ -198,3 +198,45 @@ def test_log_softmax_stats_vs_float64():
         assert mx == z.max()
         ref = np.log(np.exp(z.astype(F64) - F64(mx)).sum()) + F64(mx)
         assert abs(F64(lse) - ref) <= 4e-7 * max(1.0, abs(ref))
+
+
+def _round_f32_exact(fr):
+    """The fp32 value nearest to the exact rational fr (ties to even)."""
+    import fractions
+
+    f = float(fr)  # nearest double
+    lo = np.float32(f)
+    # step to the neighbour whose exact distance to fr is smallest
+    cands = [np.nextafter(lo, np.float32(-np.inf)), lo, np.nextafter(lo, np.float32(np.inf))]
+    best = min(cands, key=lambda c: (abs(fractions.Fraction(float(c)) - fr), int(np.float32(c).view(np.uint32)) & 1))
+    return np.float32(best)
+
+
+def test_folded_constants_are_once_rounded():
+    """Folded requant and dequant constants (Section 3.2 quantizers folded into
+    one multiplier and one bias per channel) are the fp32 values nearest to the
+    exact s_in s_w / s_out, b / s_out and s_in s_w: compared with exact rational
+    arithmetic; a double intermediate may rarely differ by one fp32 ulp."""
+    import fractions
+
+    rng = np.random.default_rng(17)
+    N = 2000
+    s_in, s_out = F32(0.0313), F32(0.0471)
+    s_w = rng.uniform(1e-4, 5e-4, N).astype(F32)
+    b = rng.normal(0, 0.02, N).astype(F32)
+    sc, bi = oracle.fold_requant(s_in, s_w, b, s_out)
+    dq = oracle.fold_dequant(s_in, s_w)
+    Fr = fractions.Fraction
+    off = 0
+    for n in range(N):
+        e_sc = _round_f32_exact(Fr(float(s_in)) * Fr(float(s_w[n])) / Fr(float(s_out)))
+        e_bi = _round_f32_exact(Fr(float(b[n])) / Fr(float(s_out)))
+        for got, exp in ((sc[n], e_sc), (bi[n], e_bi)):
+            d = abs(int(np.float32(got).view(np.int32)) - int(np.float32(exp).view(np.int32)))
+            assert d <= 1
+            off += d
+        # the product of two fp32 values is exact in double: one rounding, so
+        # it equals the correctly rounded fp32 product
+        assert dq[n] == np.float32(s_in) * np.float32(s_w[n])
+        assert dq[n] == _round_f32_exact(Fr(float(s_in)) * Fr(float(s_w[n])))
+    assert off <= 4

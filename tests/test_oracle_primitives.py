@@ -135,3 +135,24 @@ def test_length_penalty_closed_form():
             a32 = float(np.float32(a))  # alpha travels as fp32
             assert v == np.float32(((5.0 + L) / 6.0) ** a32)
     assert oracle.length_penalty(1, 0.6) == 1.0  # ((5 + 1) / 6)^a = 1
+
+
+@pytest.mark.parametrize("row", _rows("canon_sum_squares.txt"), ids=lambda r: r[0])
+def test_canon_sum_squares_worked_examples(row):
+    # the variance sum accumulates each square with one fused multiply-add
+    n, x0, xm, xl, expected = int(row[1]), float(row[2]), float(row[3]), float(row[4]), float(row[5])
+    x = np.full(n, xm, np.float32)
+    x[0], x[-1] = x0, xl
+    assert oracle.canon_sum_squares(x) == np.float32(expected)
+
+
+def test_length_penalty_exact_values():
+    # ((5 + L) / 6)^alpha at points where the closed form is known exactly
+    for L, a, v in ((1, 0.6, 1.0), (7, 1.0, 2.0), (13, 1.0, 3.0), (19, 0.5, 2.0), (31, 0.5, math.sqrt(6.0)),
+                    (91, 0.25, 2.0), (187, 0.2, 2.0), (40, 0.0, 1.0)):
+        assert oracle.length_penalty(L, a) == np.float32(v), (L, a)
+    # 2^0.6 = exp(0.6 ln 2) = 1.51571656651039808...: L = 7 gives base 2
+    assert oracle.length_penalty(7, 0.6) == np.float32(1.5157165665103981)
+    # monotone in L for alpha > 0
+    vals = [oracle.length_penalty(L, 0.6) for L in range(1, 100)]
+    assert all(b > a for a, b in zip(vals, vals[1:]))
