@@ -134,6 +134,19 @@ def _roofline_kernel(torch, np, mnmt, WL, G, info, blob, dev, stream):
     return fn, alg_bytes
 
 
+def _trace_avg_us(kernel_tag):
+    """Average kernel-trace duration (us) of the roofline kernel from the
+    committed rocprofv3 summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f).get(kernel_tag + "_trace")
+    if not rec or rec.get("source_hash") != _source_hash():
+        return None
+    return rec.get("avg_us")
+
+
 def counters_run():
     """Short run for rocprofv3 --pmc: the roofline kernel 50 times, then a
     256 MiB device-to-device copy (the counters' calibration) 3 times."""
@@ -197,7 +210,21 @@ def ingest_counters(fetch_csv, write_csv, command):
     print(json.dumps(rec))
 
 
+def _host_cpu():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(workload, min_seconds=10.0):
+    """The oracle (scalar C, one thread) translating the workload's batch
+    repeatedly for about min_seconds; also returns its output, which the GPU
+    translations must equal."""
     import oracle
     from synth import generate as G
 
@@ -205,14 +232,60 @@ def cpu_baseline(workload, min_seconds=10.0):
     src, lens = G.workload_inputs(workload)
     n, t0 = 0, time.perf_counter()
     while True:
-        m.greedy(src, lens, workload.steps)
+        ref = m.greedy(src, lens, workload.steps)
         n += 1
         el = time.perf_counter() - t0
         if el >= min_seconds and n >= 2:
             break
-    return {"value": n * workload.steps * workload.batch / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{n} sentences of the same workload (batch 1, 30 source tokens, 30 greedy steps), "
-                      f"{el:.1f} s, single-threaded scalar C"}
+    rec = {"value": n * workload.steps * workload.batch / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+           "host_cpu": _host_cpu(), "host_cpus_visible": os.cpu_count(),
+           "sample": f"{n} sentences of the same workload (batch 1, 30 source tokens, 30 greedy steps), "
+                     f"{el:.1f} s, single-threaded scalar C"}
+    return rec, ref
+
+
+def oracle_greedy(workload):
+    import oracle
+    from synth import generate as G
+
+    src, lens = G.workload_inputs(workload)
+    return oracle.Model(G.build_model(workload.model)).greedy(src, lens, workload.steps)
+
+
+def check_tokens(what, got_out, got_len, ref):
+    """Exit non-zero unless the GPU's tokens and lengths equal the oracle's."""
+    import numpy as np
+
+    if not (np.array_equal(got_out, ref[0]) and np.array_equal(got_len, ref[1])):
+        print(f"bench.py: {what}: the GPU output differs from the oracle's; no figure is reported",
+              file=sys.stderr, flush=True)
+        sys.exit(3)
+
+
+def memory_read_gbs(torch, mnmt, dev):
+    """Read bandwidth of the probe kernel: a 64 MiB buffer read 32 times per
+    launch (per XCD 8 MiB, twice its L2: the data streams from the 256 MB
+    last-level cache) and a 4 GiB buffer read once (HBM).  Median of 5 timed
+    launches after 2 untimed ones, each between two events."""
+    import numpy as np
+
+    sink = torch.empty(mnmt.DEBUG_READ_BLOCKS, dtype=torch.int32, device=dev)
+    out = {}
+    for name, nbytes, reps in (("llc_64MiB", 64 << 20, 32), ("hbm_4GiB", 4 << 30, 1)):
+        x = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+        ts = []
+        for i in range(7):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            mnmt.mnmt_debug_read(x, sink, reps)
+            e1.record()
+            e1.synchronize()
+            if i >= 2:
+                ts.append(e0.elapsed_time(e1))
+        out[name] = round(nbytes * reps / (float(np.median(ts)) * 1e-3) / 1e9, 1)
+        del x
+    torch.cuda.synchronize()
+    return out
 
 
 def qlinear_sweep(torch, mnmt, G, dev, reps=100):
@@ -284,10 +357,18 @@ def sweep_trace_summary(trace_csv, command):
     print("\n".join(out))
 
 
-def beam_throughput(torch, mnmt, G, dev, names=("mobile_beam", "base_beam"), reps=3):
+def beam_throughput(torch, mnmt, G, dev, names=("mobile_beam", "base_beam"), reps=3, check=True):
     """The two batched beam-search workloads (mobile: 64 sentences, base: 128;
     beam 4, length penalty 0.6), each translation one captured graph, inputs
-    resident on the device: one untimed translation, then ``reps`` timed."""
+    resident on the device: one untimed translation, then ``reps`` timed.
+    The last translation's shortest sentence is compared with the oracle, and
+    a composite roofline (the sum over phases of max(ops / i8 peak, bytes /
+    HBM peak), paper_2306_04235_amd.workload.beam_roofline_s) over the steps
+    the batch ran gives the fraction."""
+    import numpy as np
+
+    from paper_2306_04235_amd import workload as WL
+
     res = {}
     for name in names:
         w = G.WORKLOADS[name]
@@ -307,10 +388,26 @@ def beam_throughput(torch, mnmt, G, dev, names=("mobile_beam", "base_beam"), rep
             run()
         torch.cuda.synchronize()
         el = (time.perf_counter() - t0) / reps
+        sess.status()
         toks = int(outs[1].sum().item())
+        out_np, len_np = outs[0].cpu().numpy(), outs[1].cpu().numpy()
+        if check:  # the shortest source against the oracle
+            import oracle
+
+            i = int(np.argmin(lens))
+            om = oracle.Model(G.build_model(w.model))
+            ref = om.beam(src[i:i + 1], lens[i:i + 1], w.beam, w.steps, w.alpha)
+            check_tokens(f"{name} sentence {i}", out_np[i:i + 1], len_np[i:i + 1], ref)
+        steps_run = int(len_np.max())
+        m_dims = WL.Dims(m.info.d_model, m.info.n_heads, m.info.d_ffn, m.info.n_enc, m.info.n_dec, m.info.vocab)
+        roof = WL.beam_roofline_s(m_dims, lens, w.beam, steps_run, I8_PEAK_TOPS * 1e12, HBM_PEAK_GBS * 1e9)
         res[name] = {"workload": w.name, "ms_per_batch": round(el * 1e3, 3), "sentences_per_s": round(w.batch / el, 1),
                      "output_tokens_per_s": round(toks / el, 1), "batch": w.batch, "beam": w.beam,
-                     "max_steps": w.steps}
+                     "max_steps": w.steps, "steps_run": steps_run,
+                     "composite_roofline": {"ms": round(roof["seconds"] * 1e3, 4),
+                                            "frac": round(roof["seconds"] / el, 4),
+                                            "parts_ms": {k: round(v["seconds"] * 1e3, 4)
+                                                         for k, v in roof["parts"].items()}}}
         sess.close()
         m.close()
     return res
@@ -376,6 +473,11 @@ def main():
     def step():
         sess.translate(tsrc, tlen, beam=1, max_steps=w.steps, use_graph=True, out=outs)
 
+    # the oracle's translation of the same sentence, which the timed ones must equal
+    if args.no_cpu_baseline:
+        ref = oracle_greedy(w)
+    else:
+        cpu_rec, ref = cpu_baseline(w)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -384,8 +486,15 @@ def main():
         step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    sess.status()  # raises if a chained kernel's wait gave up during the timed translations
+    check_tokens("timed translations", outs[0].cpu().numpy(), outs[1].cpu().numpy(), ref)
     tokens = int(outs[1].sum().item()) * args.steps
     ms_per_sentence = elapsed * 1e3 / (args.steps * w.batch)
+    dims = WL.Dims(info.d_model, info.n_heads, info.d_ffn, info.n_enc, info.n_dec, info.vocab)
+    sent_bytes = WL.greedy_sentence_bytes(dims, int(lens[0]), w.steps)
+    sent_gbs = sent_bytes / (ms_per_sentence * 1e-3) / 1e9
+    sentence_roofline = {"bound": "hbm", "alg_bytes": sent_bytes, "achieved": round(sent_gbs, 1),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(sent_gbs / HBM_PEAK_GBS, 4)}
 
     # Latency distribution (outside the timed region): 50 translations, each
     # between two events on the stream.
@@ -398,6 +507,8 @@ def main():
         e1.record(cur)
         e1.synchronize()
         lat.append(e0.elapsed_time(e1))
+    sess.status()
+    check_tokens("latency translations", outs[0].cpu().numpy(), outs[1].cpu().numpy(), ref)
     lat_ms = {"median": round(float(np.median(lat)), 4), "p10": round(float(np.percentile(lat, 10)), 4),
               "p90": round(float(np.percentile(lat, 90)), 4), "runs": len(lat)}
 
@@ -411,7 +522,17 @@ def main():
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": _traffic(ROOF_TAG),
                 "kernel": ROOF_KERNEL + " (fused logits + arg-max, M=1 K=256 N=32000)",
-                "alg_bytes_per_launch": alg_bytes, "avg_us": round(kern_ms * 1e3, 3)}
+                "alg_bytes_per_launch": alg_bytes, "avg_us": round(kern_ms * 1e3, 3),
+                "data": "the 8.19 MB embedding stays in the last-level cache across back-to-back launches; "
+                        "peak is the HBM figure, see llc_read_gbs for the cache's measured rate"}
+    trace = _trace_avg_us(ROOF_TAG)
+    if trace:
+        roofline["trace_avg_us"] = trace
+        roofline["trace_frac"] = round(alg_bytes / (trace * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+    mem = memory_read_gbs(torch, mnmt, dev)
+    roofline["llc_read_gbs"] = mem["llc_64MiB"]
+    roofline["hbm_read_gbs"] = mem["hbm_4GiB"]
+    roofline["frac_of_measured_llc"] = round(achieved / mem["llc_64MiB"], 4)
 
     # Largest quantized-linear sweep shape on the matrix cores.
     M, K, N = 4096, 256, 32000
@@ -469,13 +590,14 @@ def main():
                    "d_model": info.d_model, "heads": info.n_heads, "ffn": info.d_ffn, "enc_layers": info.n_enc,
                    "dec_layers": info.n_dec, "vocab": info.vocab, "graph": True},
         "roofline": roofline,
+        "sentence_roofline": sentence_roofline,
         "qgemm": qgemm,
         "paper_shapes_b1_greedy30": paper,
     }
     if not args.no_beam:
         line["beam_throughput"] = beam_throughput(torch, mnmt, G, dev)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(w)
+        line["cpu_baseline"] = cpu_rec
     print(json.dumps(line), flush=True)
     sess.close()
     model.close()

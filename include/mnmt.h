@@ -77,6 +77,7 @@ extern "C" {
 #define MNMT_E_CAPACITY (-3)     /* request exceeds the session's capacity */
 #define MNMT_E_HIP (-4)          /* a HIP runtime call failed (text in last_error) */
 #define MNMT_E_UNSUPPORTED (-5)  /* valid but not supported by this build */
+#define MNMT_E_TIMEOUT (-6)      /* a kernel's bounded wait for another kernel gave up (see mnmt_session_status) */
 
 /* Linear-layer epilogues (quantizer figure, Section 3.2), y = acc*scale+bias:
  *   MNMT_EPI_I32:       Y int32 = acc
@@ -177,23 +178,42 @@ int mnmt_encode(mnmt_session* session, const int32_t* d_src, const int32_t* d_le
  * d_prev [B] (NULL: the session's device-resident tokens, BOS at step 0 or
  * the previous step's outputs), output d_next [B] = arg max of the logits
  * (smallest id among equal maxima), optional d_logits [B, V] fp32.  The step
- * index lives in device memory.  Errors: MNMT_E_CAPACITY past max_tgt_len. */
+ * index lives in device memory.  Errors: MNMT_E_CAPACITY past max_tgt_len;
+ * MNMT_E_UNSUPPORTED on a session created with beam > 1 (beam search keeps
+ * its hypotheses, parents and finished list across steps and runs only as a
+ * whole search through mnmt_translate). */
 int mnmt_decode_step(mnmt_session* session, const int32_t* d_prev, int32_t* d_next, float* d_logits,
                      void* stream);
 
 /* Encode and search.  d_out [B, max_steps] int32 (PAD after the end),
  * d_out_len [B] int32, d_score [B] fp32 (beam: normalized score of the
- * returned hypothesis; greedy: unused, may be NULL).  Asynchronous; results
+ * returned hypothesis; greedy: unused, may be NULL).  Asynchronous: only
+ * device work is enqueued (no host wait, no copy; capturable), and results
  * are valid after `stream` synchronizes.  Greedy with stop_at_eos = 0 runs
- * exactly max_steps steps. */
+ * exactly max_steps steps.
+ * Batch-1 greedy searches (and encoders of at most 64 rows) run as a chain of
+ * kernels alternating between `stream` and a second session stream, each
+ * kernel waiting in a bounded spin on its predecessor's flags: the chain
+ * needs the two streams' kernels to run concurrently, which a tool that
+ * serializes dispatches prevents (set MNMT_SERIAL_STEPS=1 in the environment
+ * before creating the session to run them in one stream).  A wait that gives
+ * up sets a session error word: every later translate writes -1 into
+ * d_out_len until mnmt_session_status reports and clears it. */
 int mnmt_translate(mnmt_session* session, const int32_t* d_src, const int32_t* d_len, int B,
                    int S_max, const mnmt_search_cfg* search, int32_t* d_out, int32_t* d_out_len,
                    float* d_score, void* stream);
 
+/* Synchronizes `stream`, then reports (and clears) the session's error word:
+ * MNMT_E_TIMEOUT if a chained kernel's wait gave up since the last call
+ * (those translations' outputs are invalid), else MNMT_OK. */
+int mnmt_session_status(mnmt_session* session, void* stream);
+
 /* Device pointer and size of a session buffer, for inspection by tests:
  * "enc_out" int8 [B*S_max, d] (encoder output codes, padded rows undefined),
  * "cross_kv.<l>" int8 [B*S_max, 2d], "dec_x" fp32 [R, d], "logits" fp32 [R, V],
- * "step" int32 [1]. */
+ * "step" int32 [1], "chain_err" int32 [1], "out_key" uint64 [max_tgt_len][R]
+ * (greedy: each step's winning arg-max key, key(z) << 32 | (0xFFFFFFFF - id)
+ * as MNMT_EPI_ARGMAX packs it), "kcache.<l>", "vcache.<l>" int8 [R][T][d]. */
 int mnmt_session_tensor(const mnmt_session* session, const char* name, void** d_ptr, size_t* bytes);
 
 /* ---- single quantized linear layer --------------------------------------- */
@@ -250,6 +270,14 @@ int mnmt_fold_requant(float s_in, const float* h_s_w, const float* h_b, float s_
  * (x <= 0), 1 natural log (x > 0), 2 canonical-order sum of all n values
  * into d_y[0].  For tests of the canonical arithmetic. */
 int mnmt_debug_canon(int fn, const float* d_x, int n, float* d_y, void* stream);
+
+/* Read bandwidth probe (not part of inference): 2048 blocks of 256 threads
+ * read d_x [bytes] (16-byte aligned, bytes a multiple of 16) `reps` >= 1
+ * times with 16-byte loads, each block the same share every time, and each
+ * block stores one word into d_sink [2048].  Over a buffer that fits the
+ * last-level cache but not the L2 caches, read many times, it measures the
+ * last-level cache's bandwidth; over a buffer far larger than it, HBM's. */
+int mnmt_debug_read(const void* d_x, size_t bytes, int reps, unsigned* d_sink, void* stream);
 
 /* ---- errors ---------------------------------------------------------------- */
 const char* mnmt_status_str(int status);

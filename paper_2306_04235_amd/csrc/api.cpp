@@ -32,6 +32,7 @@ extern "C" const char* mnmt_status_str(int status) {
     case MNMT_E_CAPACITY: return "capacity exceeded";
     case MNMT_E_HIP: return "HIP runtime error";
     case MNMT_E_UNSUPPORTED: return "unsupported";
+    case MNMT_E_TIMEOUT: return "device-side wait timed out";
     default: return "unknown status";
   }
 }
@@ -146,4 +147,12 @@ extern "C" int mnmt_debug_canon(int fn, const float* d_x, int n, float* d_y, voi
   if (fn < 0 || fn > 2 || n < 0 || !d_x || !d_y) return set_error(MNMT_E_INVALID_ARG, "bad debug_canon arguments");
   const hipError_t h = launch_debug_canon(fn, d_x, n, d_y, static_cast<hipStream_t>(stream));
   return h == hipSuccess ? MNMT_OK : hip_error(h, "debug_canon launch");
+}
+
+extern "C" int mnmt_debug_read(const void* d_x, size_t bytes, int reps, unsigned* d_sink, void* stream) {
+  if (!d_x || !d_sink || bytes % 16 || reinterpret_cast<uintptr_t>(d_x) % 16 || reps < 1)
+    return set_error(MNMT_E_INVALID_ARG,
+                     "debug_read needs a 16-byte aligned buffer of a multiple of 16 bytes and reps >= 1");
+  const hipError_t h = launch_debug_read(d_x, bytes, reps, d_sink, static_cast<hipStream_t>(stream));
+  return h == hipSuccess ? MNMT_OK : hip_error(h, "debug_read launch");
 }

@@ -140,6 +140,7 @@ __global__ __launch_bounds__(256) void k_greedy_commit_slots(FusedGemv gv) {
       const int tok = unpack_index(b);
       const int fin = gv.finished[m];
       if (t < gv.T) gv.out_tok[(size_t)t * gv.R + m] = fin ? gv.pad : tok;
+      if (t < gv.T && gv.out_key) gv.out_key[(size_t)t * gv.R + m] = b;
       if (!fin && gv.stop_at_eos && tok == gv.eos) {
         gv.finished[m] = 1;
         gv.out_len[m] = t + 1;

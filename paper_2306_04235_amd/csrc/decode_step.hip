@@ -363,10 +363,12 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
     unsigned long long key = pk[0];
 #pragma unroll
     for (int k = 1; k < 4; ++k) key = pk[k] > key ? pk[k] : key;
-    const int tok = unpack_index(wave_max_u64(key));
+    const unsigned long long best = wave_max_u64(key);
+    const int tok = unpack_index(best);
     if (wave < R && lane == 0) {
       const int tc = cm.t - 1;
       if (tc < cm.T) chain_store(cm.out_tok + (size_t)tc * R + wave, fin ? cm.pad : tok);
+      if (cm.out_key && tc < cm.T) cm.out_key[(size_t)tc * R + wave] = best;
       if (!fin && cm.stop_at_eos && tok == cm.eos) {
         chain_store(cm.finished + wave, 1);
         chain_store(cm.out_len + wave, tc + 1);

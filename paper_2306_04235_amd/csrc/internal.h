@@ -71,14 +71,25 @@ hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, co
                                  const int32_t* len, float c_qk, float c_pv, int8_t* ctx, hipStream_t s);
 
 // Greedy bookkeeping after the fused logits/arg-max of a step.
+// out_key [T][R] (or null) receives each step's winning arg-max key.
 hipError_t launch_greedy_commit(unsigned long long* slots, int R, int T, int32_t* cur_tok, int32_t* out_tok,
                                 int32_t* finished, int32_t* out_len, int* step, int stop_at_eos, int eos,
-                                int pad, hipStream_t s);
+                                int pad, unsigned long long* out_key, hipStream_t s);
 hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
                                int32_t* out_len, int* step, int bos, unsigned long long* fslots, int n_fslots,
                                hipStream_t s);
+// A nonzero *chain_err (a chained kernel's wait gave up) marks every row's
+// length -1 instead of copying it.
 hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, int R, int T, int32_t* out,
-                                int32_t* out_len_dst, hipStream_t s);
+                                int32_t* out_len_dst, const int* chain_err, hipStream_t s);
+// The length penalties ((5 + L) / 6)^alpha, L = 0 .. n - 1, computed on the
+// host and passed by value in the kernel's arguments, into dst [n].
+struct LpTable {
+  static constexpr int kMax = 257;  // max_tgt_len <= 256
+  float v[kMax];
+  int n;
+};
+hipError_t launch_fill_lp(const LpTable& tab, float* dst, hipStream_t s);
 // Arg-max of fp32 rows [R, V] into packed slots (greedy when logits are
 // produced by the matrix-core path).
 hipError_t launch_row_argmax(const float* z, int R, int V, unsigned long long* slots, hipStream_t s);
@@ -127,6 +138,7 @@ struct FusedGemv {         // a linear layer over the prepared rows, and greedy 
   int32_t* cur_tok;
   int32_t* finished;
   int32_t* out_len;
+  unsigned long long* out_key;  // commit: [T][R] the step's winning arg-max key (or null)
   int T, stop_at_eos, eos, pad;
   int32_t* zero_acc;       // commit: cleared after the step (or null)
   int zero_n;
@@ -213,6 +225,7 @@ struct StepCommit {
   int32_t* out_tok;                 // [T][R]
   int32_t* out_len;
   int32_t* cur_tok;
+  unsigned long long* out_key;      // [T][R] the winning arg-max key of each step (or null)
   int* step;
   int T, stop_at_eos, eos, pad;
 };
@@ -361,8 +374,9 @@ hipError_t launch_beam_reset(const BeamState& st, int* step, hipStream_t s);
 hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int* step, hipStream_t s);
 // Also advances the step counter (the last block to finish).
 hipError_t launch_beam_update(const BeamState& st, int* step, const BeamNext& nx, hipStream_t s);
+// A nonzero *chain_err marks every sentence's length -1 (see launch_greedy_output).
 hipError_t launch_beam_finalize(const BeamState& st, int steps, int32_t* out, int32_t* out_len, float* out_score,
-                                hipStream_t s);
+                                const int* chain_err, hipStream_t s);
 
 // Model files (model.cpp).
 int model_size(const void* blob, size_t n, size_t* bytes, std::string& err);
@@ -371,6 +385,11 @@ int model_create(const void* blob, size_t n, void* d_arena, size_t arena_bytes, 
 
 // Canonical-arithmetic self check.
 hipError_t launch_debug_canon(int fn, const float* x, int n, float* y, hipStream_t s);
+// Read bandwidth probe: kDebugReadBlocks blocks read `bytes` (a multiple of
+// 16) `reps` times, each block the same share every time, and each stores one
+// word of sink [kDebugReadBlocks].
+constexpr int kDebugReadBlocks = 2048;
+hipError_t launch_debug_read(const void* x, size_t bytes, int reps, unsigned* sink, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Model and session structures.
@@ -447,6 +466,7 @@ struct mnmt_session {
   int32_t* out_tok = nullptr;
   int32_t* finished = nullptr;
   int32_t* out_len = nullptr;
+  unsigned long long* out_key = nullptr;  // [T][R] greedy: each step's winning arg-max key
   float* lp = nullptr;
   mnmt::BeamState beam{};
   std::map<std::string, std::pair<void*, size_t>> named;

@@ -175,14 +175,16 @@ __global__ void k_greedy_reset(unsigned long long* slots, int R, int steps, int3
 // the tokens, applies the end-of-sentence rule and advances the step counter.
 __global__ void k_greedy_commit(unsigned long long* slots, int R, int T, int32_t* cur_tok, int32_t* out_tok,
                                 int32_t* finished, int32_t* out_len, int* step, int stop_at_eos, int eos,
-                                int pad) {
+                                int pad, unsigned long long* out_key) {
   const int t = *step;
   __syncthreads();  // every thread has read the step before it advances
   for (int r = threadIdx.x; r < R; r += blockDim.x) {
-    const int tok = unpack_index(slots[r]);
+    const unsigned long long key = slots[r];
+    const int tok = unpack_index(key);
     slots[r] = 0ull;
     const int fin = finished[r];
     if (t < T) out_tok[(size_t)t * R + r] = fin ? pad : tok;
+    if (t < T && out_key) out_key[(size_t)t * R + r] = key;
     if (!fin && stop_at_eos && tok == eos) {
       finished[r] = 1;
       out_len[r] = t + 1;
@@ -193,10 +195,14 @@ __global__ void k_greedy_commit(unsigned long long* slots, int R, int T, int32_t
 }
 
 __global__ void k_greedy_output(const int32_t* out_tok, const int32_t* out_len, int R, int T, int32_t* out,
-                                int32_t* out_len_dst) {
+                                int32_t* out_len_dst, const int* chain_err) {
   const int r = blockIdx.x;
   for (int t = threadIdx.x; t < T; t += blockDim.x) out[(size_t)r * T + t] = out_tok[(size_t)t * R + r];
-  if (threadIdx.x == 0) out_len_dst[r] = out_len[r];
+  if (threadIdx.x == 0) out_len_dst[r] = (chain_err && *chain_err) ? -1 : out_len[r];
+}
+
+__global__ void k_fill_lp(LpTable tab, float* dst) {
+  for (int i = threadIdx.x; i < tab.n; i += blockDim.x) dst[i] = tab.v[i];
 }
 
 // Arg-max of fp32 rows (smallest index among equal maxima), one wave per row.
@@ -691,7 +697,8 @@ __device__ void backtrack(const BeamState& st, int row, int last, int32_t* out) 
 // pick the best normalized score (the first finished among equals: EOS
 // hypotheses in the order they finished, then the live slots in slot order)
 // and write its tokens.  One thread per sentence.
-__global__ void k_beam_finalize(BeamState st, int steps, int32_t* out, int32_t* out_len, float* out_score) {
+__global__ void k_beam_finalize(BeamState st, int steps, int32_t* out, int32_t* out_len, float* out_score,
+                                const int* chain_err) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= st.B) return;
   const int W = st.W;
@@ -726,12 +733,46 @@ __global__ void k_beam_finalize(BeamState st, int steps, int32_t* out, int32_t* 
     if (L > 1) backtrack(st, st.fin_row[b * W + idx], L - 2, o);
     o[L - 1] = st.eos;
   }
-  for (int t = L; t < steps; ++t) o[t] = st.pad;
-  out_len[b] = L;
+    for (int t = L; t < steps; ++t) o[t] = st.pad;
+  out_len[b] = (chain_err && *chain_err) ? -1 : L;
   if (out_score) out_score[b] = best;
 }
 
 // ---------------------------------------------------------------------------
+// A plain read of n16 16-byte words (each block XOR-folds its share into one
+// word of sink): the memory system's read bandwidth for the data's location
+// (last-level cache when the buffer was just read and fits, HBM otherwise).
+__global__ __launch_bounds__(256) void k_debug_read(const uint4* __restrict__ x, size_t n16, int reps,
+                                                    unsigned* sink) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  uint4 acc = {0u, 0u, 0u, 0u};
+  for (int rep = 0; rep < reps; ++rep) {
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n16; i += 4 * stride) {
+      const uint4 a = x[i], b = x[i + stride], c = x[i + 2 * stride], e = x[i + 3 * stride];
+      acc.x ^= a.x ^ b.x ^ c.x ^ e.x;
+      acc.y ^= a.y ^ b.y ^ c.y ^ e.y;
+      acc.z ^= a.z ^ b.z ^ c.z ^ e.z;
+      acc.w ^= a.w ^ b.w ^ c.w ^ e.w;
+    }
+    for (; i < n16; i += stride) {
+      const uint4 a = x[i];
+      acc.x ^= a.x;
+      acc.y ^= a.y;
+      acc.z ^= a.z;
+      acc.w ^= a.w;
+    }
+    // keep each pass a real read (no folding of identical passes)
+    asm volatile("" : "+v"(acc.x), "+v"(acc.y), "+v"(acc.z), "+v"(acc.w));
+  }
+  unsigned v = acc.x ^ acc.y ^ acc.z ^ acc.w;
+  for (int off = 32; off >= 1; off /= 2) v ^= __shfl_xor(v, off);
+  __shared__ unsigned part[4];
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
+}
+
 __global__ void k_debug_canon(int fn, const float* x, int n, float* y) {
   const int lane = threadIdx.x & 63;
   if (fn == 0 || fn == 1) {
@@ -806,16 +847,22 @@ hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int3
 
 hipError_t launch_greedy_commit(unsigned long long* slots, int R, int T, int32_t* cur_tok, int32_t* out_tok,
                                 int32_t* finished, int32_t* out_len, int* step, int stop_at_eos, int eos, int pad,
-                                hipStream_t s) {
+                                unsigned long long* out_key, hipStream_t s) {
   hipLaunchKernelGGL(k_greedy_commit, dim3(1), dim3(256), 0, s, slots, R, T, cur_tok, out_tok, finished, out_len,
-                     step, stop_at_eos, eos, pad);
+                     step, stop_at_eos, eos, pad, out_key);
   return hipGetLastError();
 }
 
 hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, int R, int T, int32_t* out,
-                                int32_t* out_len_dst, hipStream_t s) {
+                                int32_t* out_len_dst, const int* chain_err, hipStream_t s) {
   if (R <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_greedy_output, dim3(R), dim3(64), 0, s, out_tok, out_len, R, T, out, out_len_dst);
+  hipLaunchKernelGGL(k_greedy_output, dim3(R), dim3(64), 0, s, out_tok, out_len, R, T, out, out_len_dst, chain_err);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_lp(const LpTable& tab, float* dst, hipStream_t s) {
+  if (tab.n < 1 || tab.n > LpTable::kMax) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_fill_lp, dim3(1), dim3(256), 0, s, tab, dst);
   return hipGetLastError();
 }
 
@@ -894,9 +941,17 @@ hipError_t launch_beam_update(const BeamState& st, int* step, const BeamNext& nx
   return hipGetLastError();
 }
 
-hipError_t launch_beam_finalize(const BeamState& st, int steps, int32_t* out, int32_t* out_len,
-                                      float* out_score, hipStream_t s) {
-  hipLaunchKernelGGL(k_beam_finalize, dim3((st.B + 63) / 64), dim3(64), 0, s, st, steps, out, out_len, out_score);
+hipError_t launch_beam_finalize(const BeamState& st, int steps, int32_t* out, int32_t* out_len, float* out_score,
+                                const int* chain_err, hipStream_t s) {
+  hipLaunchKernelGGL(k_beam_finalize, dim3((st.B + 63) / 64), dim3(64), 0, s, st, steps, out, out_len, out_score,
+                     chain_err);
+  return hipGetLastError();
+}
+
+hipError_t launch_debug_read(const void* x, size_t bytes, int reps, unsigned* sink, hipStream_t s) {
+  if (bytes == 0 || reps < 1) return hipSuccess;
+  hipLaunchKernelGGL(k_debug_read, dim3(kDebugReadBlocks), dim3(256), 0, s, static_cast<const uint4*>(x), bytes / 16,
+                     reps, sink);
   return hipGetLastError();
 }
 

@@ -33,7 +33,7 @@ struct Plan {
   size_t src, len, region, enc_x, enc_x2, enc_a, enc_qkv, enc_h, enc_out, logits;
   std::vector<size_t> cross_kv, kc, vc;
   size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots, enc_acc;
-  size_t cur_tok, step, slots, out_tok, finished, out_len, lp;
+  size_t cur_tok, step, slots, out_tok, finished, out_len, out_key, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
   size_t chain_err, enc_chain, beam_count;
   size_t total;
@@ -110,7 +110,8 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.slots = b.take(8 * R);
   p.out_tok = b.take(4 * T * R);
   p.finished = b.take(4 * R);
-  p.out_len = b.take(4 * R);
+    p.out_len = b.take(4 * R);
+  p.out_key = b.take(8 * T * R);
   p.lp = b.take(4 * (T + 1));
   p.score = b.take(4 * R);
   p.cand_score = b.take(4 * R * 2 * W);
@@ -458,8 +459,8 @@ int greedy_step(mnmt_session* S, int R, int stop_at_eos, float* logits_out, hipS
     LAUNCH(launch_qlinear(S->dec_a, d, m->E, m->c_out, nullptr, R, d, V, e, s));
     LAUNCH(launch_row_argmax(z, R, V, S->slots, s));
   }
-  LAUNCH(launch_greedy_commit(S->slots, R, S->cfg.max_tgt_len, S->cur_tok, S->out_tok, S->finished, S->out_len,
-                              S->step, stop_at_eos, m->info.eos_id, m->info.pad_id, s));
+    LAUNCH(launch_greedy_commit(S->slots, R, S->cfg.max_tgt_len, S->cur_tok, S->out_tok, S->finished, S->out_len,
+                              S->step, stop_at_eos, m->info.eos_id, m->info.pad_id, S->out_key, s));
   return MNMT_OK;
 }
 
@@ -544,7 +545,8 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
   gv.out_tok = S->out_tok;
   gv.cur_tok = S->cur_tok;
   gv.finished = S->finished;
-  gv.out_len = S->out_len;
+    gv.out_len = S->out_len;
+  gv.out_key = S->out_key;
   gv.T = T;
   gv.stop_at_eos = stop_at_eos;
   gv.eos = m->info.eos_id;
@@ -653,6 +655,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     cm.finished = S->finished;
     cm.out_tok = S->out_tok;
     cm.out_len = S->out_len;
+    cm.out_key = S->out_key;
     cm.cur_tok = S->cur_tok;
     cm.step = S->step;
     cm.T = T;
@@ -741,7 +744,8 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   gv.out_tok = S->out_tok;
   gv.cur_tok = S->cur_tok;
   gv.finished = S->finished;
-  gv.out_len = S->out_len;
+    gv.out_len = S->out_len;
+  gv.out_key = S->out_key;
   gv.T = T;
   gv.stop_at_eos = stop_at_eos;
   gv.eos = m->info.eos_id;
@@ -928,7 +932,8 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->slots = (unsigned long long*)at(p.slots);
   S->out_tok = (int32_t*)at(p.out_tok);
   S->finished = (int32_t*)at(p.finished);
-  S->out_len = (int32_t*)at(p.out_len);
+    S->out_len = (int32_t*)at(p.out_len);
+  S->out_key = (unsigned long long*)at(p.out_key);
   S->lp = (float*)at(p.lp);
   BeamState& st = S->beam;
   st.B = cfg->max_batch;
@@ -957,7 +962,8 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->named["logits"] = {S->logits, 4 * R * V};
   S->named["step"] = {S->step, 4};
   S->named["cur_tok"] = {S->cur_tok, 4 * R};
-  S->named["chain_err"] = {S->chain_err, 4};
+    S->named["chain_err"] = {S->chain_err, 4};
+  S->named["out_key"] = {S->out_key, 8 * T * R};
   for (size_t l = 0; l < p.cross_kv.size(); ++l) {
     S->named["cross_kv." + std::to_string(l)] = {S->cross_kv[l], BS * 2 * d};
     S->named["kcache." + std::to_string(l)] = {S->kcache[l], R * T * d};
@@ -998,6 +1004,20 @@ extern "C" void mnmt_session_free(mnmt_session* S) {
   delete S;
 }
 
+extern "C" int mnmt_session_status(mnmt_session* S, void* stream) {
+  if (!S) return set_error(MNMT_E_INVALID_ARG, "null session");
+  hipStream_t s = as_stream(stream);
+  int err = 0;
+  MNMT_HIP(hipMemcpyAsync(&err, S->chain_err, sizeof(int), hipMemcpyDeviceToHost, s));
+  MNMT_HIP(hipStreamSynchronize(s));
+  if (!err) return MNMT_OK;
+  MNMT_HIP(hipMemsetAsync(S->chain_err, 0, sizeof(int), s));
+  MNMT_HIP(hipStreamSynchronize(s));
+  return set_error(MNMT_E_TIMEOUT,
+                   "a kernel of a chained batch-1 translation gave up waiting for its predecessor; the results "
+                   "since the last status check are invalid (their lengths read -1)");
+}
+
 extern "C" int mnmt_session_tensor(const mnmt_session* S, const char* name, void** d_ptr, size_t* bytes) {
   if (!S || !name || !d_ptr) return set_error(MNMT_E_INVALID_ARG, "null argument");
   auto it = S->named.find(name);
@@ -1024,7 +1044,10 @@ extern "C" int mnmt_encode(mnmt_session* S, const int32_t* d_src, const int32_t*
 
 extern "C" int mnmt_decode_step(mnmt_session* S, const int32_t* d_prev, int32_t* d_next, float* d_logits,
                                 void* stream) {
-  if (!S || !S->encoded) return set_error(MNMT_E_INVALID_ARG, "decode_step needs a session after mnmt_encode");
+    if (!S) return set_error(MNMT_E_INVALID_ARG, "null session");
+  if (S->cfg.beam > 1)
+    return set_error(MNMT_E_UNSUPPORTED, "decode_step is the greedy step; beam sessions search through mnmt_translate");
+  if (!S->encoded) return set_error(MNMT_E_INVALID_ARG, "decode_step needs a session after mnmt_encode");
   if (S->host_step >= S->cfg.max_tgt_len) return set_error(MNMT_E_CAPACITY, "decode step beyond max_tgt_len");
   int rc;
   if (d_prev && (rc = check_ptr(d_prev, "d_prev"))) return rc;
@@ -1059,12 +1082,13 @@ extern "C" int mnmt_translate(mnmt_session* S, const int32_t* d_src, const int32
   S->encoded = false;  // decode_step state is not kept across a translate
   if (sc->beam > 1) {
     S->beam.B = B;  // sentences of this call
-    // length penalties ((5 + L) / 6)^alpha for L = 0..max_tgt_len, in double
-    std::vector<float> lp(S->cfg.max_tgt_len + 1);
-    for (size_t L = 0; L < lp.size(); ++L)
-      lp[L] = (float)std::pow((5.0 + (double)L) / 6.0, (double)sc->len_penalty_alpha);
-    MNMT_HIP(hipMemcpyAsync(S->lp, lp.data(), sizeof(float) * lp.size(), hipMemcpyHostToDevice, s));
-    MNMT_HIP(hipStreamSynchronize(s));  // the host vector is released on return
+    // length penalties ((5 + L) / 6)^alpha for L = 0..max_tgt_len, in double,
+    // handed to the device in a kernel's arguments (no copy, no host wait)
+    LpTable lp{};
+    lp.n = S->cfg.max_tgt_len + 1;
+    for (int L = 0; L < lp.n; ++L)
+      lp.v[L] = (float)std::pow((5.0 + (double)L) / 6.0, (double)sc->len_penalty_alpha);
+    LAUNCH(launch_fill_lp(lp, S->lp, s));
   }
   if (sc->use_graph) {
     const std::string key = std::to_string(B) + "," + std::to_string(S_max) + "," + std::to_string(sc->beam) + "," +
@@ -1097,9 +1121,9 @@ extern "C" int mnmt_translate(mnmt_session* S, const int32_t* d_src, const int32
     if ((rc = enqueue_search(S, *sc, s))) return rc;
   }
   if (sc->beam == 1) {
-    LAUNCH(launch_greedy_output(S->out_tok, S->out_len, B, sc->max_steps, d_out, d_out_len, s));
+    LAUNCH(launch_greedy_output(S->out_tok, S->out_len, B, sc->max_steps, d_out, d_out_len, S->chain_err, s));
   } else {
-    LAUNCH(launch_beam_finalize(S->beam, sc->max_steps, d_out, d_out_len, d_score, s));
+    LAUNCH(launch_beam_finalize(S->beam, sc->max_steps, d_out, d_out_len, d_score, S->chain_err, s));
   }
   return MNMT_OK;
 }

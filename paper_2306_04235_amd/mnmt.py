@@ -13,15 +13,15 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmnmt.so")
 
-OK, E_INVALID_ARG, E_BAD_MODEL, E_CAPACITY, E_HIP, E_UNSUPPORTED = 0, -1, -2, -3, -4, -5
+OK, E_INVALID_ARG, E_BAD_MODEL, E_CAPACITY, E_HIP, E_UNSUPPORTED, E_TIMEOUT = 0, -1, -2, -3, -4, -5, -6
 (EPI_I32, EPI_I8, EPI_I8_RELU, EPI_F32, EPI_F32_RESID, EPI_LOGITS, EPI_ARGMAX, EPI_ARGMAX_PARTIAL,
  EPI_ARGMAX_PARTIAL_PACKED) = range(9)
 
 EXPORTS = ("mnmt_model_bytes", "mnmt_model_load", "mnmt_model_get_info", "mnmt_model_free", "mnmt_session_bytes",
            "mnmt_session_create", "mnmt_session_free", "mnmt_encode", "mnmt_decode_step", "mnmt_translate",
-           "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed", "mnmt_argmax_partials", "mnmt_packed_bytes",
+                      "mnmt_session_status", "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed", "mnmt_argmax_partials", "mnmt_packed_bytes",
            "mnmt_pack_weights", "mnmt_fold_requant",
-           "mnmt_debug_canon", "mnmt_status_str",
+           "mnmt_debug_canon", "mnmt_debug_read", "mnmt_status_str",
            "mnmt_last_error")
 
 
@@ -72,6 +72,7 @@ def lib():
         L.mnmt_decode_step.argtypes = [vp, vp, vp, vp, vp]
         L.mnmt_translate.argtypes = [vp, vp, vp, i32, i32, C.POINTER(SearchCfg), vp, vp, vp, vp]
         L.mnmt_session_tensor.argtypes = [vp, C.c_char_p, C.POINTER(vp), C.POINTER(sz)]
+        L.mnmt_session_status.argtypes = [vp, vp]
         L.mnmt_qlinear.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp]
         L.mnmt_qlinear_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp, vp, vp]
         L.mnmt_argmax_partials.argtypes = [i32]
@@ -80,6 +81,7 @@ def lib():
         L.mnmt_pack_weights.argtypes = [vp, i32, i32, vp, vp]
         L.mnmt_fold_requant.argtypes = [f32, vp, vp, f32, i32, vp, vp]
         L.mnmt_debug_canon.argtypes = [i32, vp, i32, vp, vp]
+        L.mnmt_debug_read.argtypes = [vp, sz, i32, vp, vp]
         L.mnmt_status_str.argtypes = [i32]
         L.mnmt_status_str.restype = C.c_char_p
         L.mnmt_last_error.argtypes = []
@@ -201,6 +203,17 @@ def mnmt_debug_canon(fn: int, x, stream=None):
     return y
 
 
+DEBUG_READ_BLOCKS = 2048
+
+
+def mnmt_debug_read(x, sink, reps=1, stream=None):
+    """Read every byte of the device tensor x `reps` times (bandwidth probe); sink: int32 [2048]."""
+    if sink.numel() * sink.element_size() < 4 * DEBUG_READ_BLOCKS:
+        raise ValueError("sink needs 2048 32-bit words")
+    _check(lib().mnmt_debug_read(_ptr(x), x.numel() * x.element_size(), int(reps), _ptr(sink), _stream(stream)),
+           "mnmt_debug_read")
+
+
 class Model:
     """A model loaded into a torch-allocated device arena."""
 
@@ -281,6 +294,10 @@ class Session:
         _check(lib().mnmt_translate(self.handle, _ptr(src), _ptr(lens), B, S, C.byref(sc), _ptr(out[0]),
                                     _ptr(out[1]), _ptr(out[2]), _stream(stream)), "mnmt_translate")
         return out
+
+    def status(self, stream=None):
+        """Synchronize and raise MnmtError(E_TIMEOUT) if a chained kernel's wait gave up."""
+        _check(lib().mnmt_session_status(self.handle, _stream(stream)), "mnmt_session_status")
 
     def tensor(self, name: str, dtype, shape):
         """A view of a session buffer (inside the workspace tensor)."""

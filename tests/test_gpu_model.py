@@ -88,10 +88,26 @@ def _greedy_check(torch, dev, cfg, src, lens, steps, stop_at_eos=False, check_lo
         torch.cuda.synchronize()
         assert np.array_equal(out.cpu().numpy(), o_out), f"greedy tokens (graph={use_graph})"
         assert np.array_equal(out_len.cpu().numpy(), o_len)
+    # each step's winning arg-max key (recorded by the step that commits the
+    # token): the high word is the order-preserving key of the maximum logit
+    if not stop_at_eos:
+        keys = sess.tensor("out_key", torch.int64, (steps, B)).cpu().numpy().view(np.uint64)
+        assert np.array_equal(keys.T, _argmax_keys(o_logits)), "arg-max keys (maximum logit bits and index)"
     # no kernel of the translation chain gave up waiting for its predecessor
     assert int(sess.tensor("chain_err", torch.int32, (1,)).cpu().numpy()[0]) == 0
+    sess.status()
     sess.close()
     return o_out
+
+
+def _argmax_keys(z):
+    """Packed arg-max keys of fp32 logits [..., V]: order-preserving 32-bit key of
+    the maximum << 32 | (0xFFFFFFFF - index of its first occurrence)."""
+    idx = z.argmax(axis=-1)
+    m = np.take_along_axis(z, idx[..., None], axis=-1)[..., 0]
+    u = m.astype(np.float32).view(np.uint32).astype(np.uint64)
+    hi = np.where(u & 0x80000000, ~u & 0xFFFFFFFF, u | 0x80000000)
+    return (hi << np.uint64(32)) | (np.uint64(0xFFFFFFFF) - idx.astype(np.uint64))
 
 
 def test_tiny_postln_greedy(torch_dev):
@@ -229,8 +245,11 @@ def test_paper_model_shapes_greedy(torch_dev, cfg):
     _greedy_check(torch, dev, cfg, src, lens, 30)
 
 
-def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None):
+def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None, parallel=False):
     from paper_2306_04235_amd import mnmt
+
+    from .oracle_pool import beam_many
+
 
     om, gm = _pair(cfg)
     B, S = src.shape
@@ -245,7 +264,11 @@ def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None):
     assert all(np.array_equal(results[0][i], results[1][i]) for i in range(3)), "graph replay differs from eager"
     out, out_len, score = results[0]
     idx = np.arange(B) if sample is None else np.asarray(sample)
-    o_out, o_len, o_score = om.beam(src[idx], lens[idx], W, steps, alpha)
+    if parallel:  # one oracle process per sentence, up to 16 at a time
+        mcfg = getattr(G, cfg) if isinstance(cfg, str) else cfg
+        o_out, o_len, o_score = beam_many(mcfg, src, lens, idx, W, steps, alpha)
+    else:
+        o_out, o_len, o_score = om.beam(src[idx], lens[idx], W, steps, alpha)
     assert np.array_equal(out_len[idx], o_len)
     assert np.array_equal(out[idx], o_out)
     assert np.array_equal(score[idx].view(np.uint32), o_score.view(np.uint32))
@@ -297,18 +320,92 @@ def test_4bit_weight_models(torch_dev):
     _beam_check(torch, dev, div4, src, lens, 2, 8, 0.6)
 
 
-def test_mobile_beam_workload_sampled(torch_dev):
+def test_mobile_beam_workload_all_sentences(torch_dev):
+    """The batched beam workload on the mobile model: all 64 sentences (10-60
+    source tokens, beam 4, 64 steps) against the oracle, run one sentence per
+    host process."""
     torch, dev = torch_dev
     w = G.WORKLOADS["mobile_beam"]
     src, lens = G.workload_inputs(w)
-    _beam_check(torch, dev, "MOBILE", src, lens, w.beam, w.steps, w.alpha, sample=[0, 17, 40, 63])
+    _beam_check(torch, dev, "MOBILE", src, lens, w.beam, w.steps, w.alpha, parallel=True)
 
 
-def test_base_beam_workload_sampled(torch_dev):
+def test_base_beam_workload_sentences(torch_dev):
+    """The base-model beam workload (128 sentences of 20-64 tokens, beam 4, 80
+    steps): the shortest and longest sources and 22 more spread over the
+    batch, against the oracle in host processes."""
     torch, dev = torch_dev
     w = G.WORKLOADS["base_beam"]
     src, lens = G.workload_inputs(w)
-    _beam_check(torch, dev, "BASE", src, lens, w.beam, w.steps, w.alpha, sample=[0, 127])
+    order = np.argsort(lens, kind="stable")
+    idx = sorted({int(order[0]), int(order[-1]), *range(0, 128, 6)})
+    assert len(idx) >= 16
+    _beam_check(torch, dev, "BASE", src, lens, w.beam, w.steps, w.alpha, sample=idx, parallel=True)
+
+
+VARIED = G.ModelConfig("varied-256", 256, 4, 1024, 2, 2, 32000, ln_post=0, seed=1102, random_gamma=True,
+                       weight_std=0.2)
+
+
+@pytest.mark.parametrize("B", [1, 2])
+def test_varied_output_chained_translate(torch_dev, B):
+    """The path the latency benchmark times -- width 256, vocabulary 32000, two
+    decoder layers: the two-stream kernel chain, the commit folded into the
+    next step and the 4-tile logits kernel of the chain, replayed from a graph
+    -- on a model whose greedy outputs vary from step to step (the workload
+    model repeats its input token), against the oracle's tokens and the bits
+    of every step's maximum logit."""
+    torch, dev = torch_dev
+    src, lens = G.make_sources(VARIED.vocab, B, [30, 17][:B], seed=90 + B, s_max=30)
+    out = _greedy_check(torch, dev, VARIED, src, lens, 30)
+    for b in range(B):
+        assert len(set(out[b].tolist())) >= 4, "the varied model should not repeat one token"
+
+
+def test_beam_session_rejects_decode_step(torch_dev):
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    _, gm = _pair("TINY")
+    sess = mnmt.Session(gm, 2, 8, 4, 2)
+    src = torch.full((2, 8), 5, dtype=torch.int32, device=dev)
+    lens = torch.full((2,), 8, dtype=torch.int32, device=dev)
+    sess.encode(src, lens)
+    with pytest.raises(mnmt.MnmtError) as e:
+        sess.decode_step()
+    assert e.value.status == mnmt.E_UNSUPPORTED
+    sess.close()
+
+
+def test_chain_error_word_marks_outputs(torch_dev):
+    """A chained kernel whose bounded wait gives up sets the session's error
+    word; here the host sets that word itself (no kernel waits in vain).  The
+    next translations report length -1 until mnmt_session_status raises
+    E_TIMEOUT and clears it."""
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    om, gm = _pair("TINY")
+    src, lens = G.workload_inputs(G.WORKLOADS["tiny"])
+    o_out, o_len = om.greedy(src, lens, 16)
+    sess = mnmt.Session(gm, 1, src.shape[1], 16, 1)
+    ts, tl = _t(torch, dev, src), _t(torch, dev, lens)
+    sess.status()
+    err = sess.tensor("chain_err", torch.int32, (1,))
+    err.fill_(1)
+    torch.cuda.synchronize()
+    for use_graph in (False, True):
+        out, out_len, _ = sess.translate(ts, tl, beam=1, max_steps=16, use_graph=use_graph)
+        torch.cuda.synchronize()
+        assert int(out_len.cpu()[0]) == -1
+    with pytest.raises(mnmt.MnmtError) as e:
+        sess.status()
+    assert e.value.status == mnmt.E_TIMEOUT
+    out, out_len, _ = sess.translate(ts, tl, beam=1, max_steps=16, use_graph=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(out.cpu().numpy(), o_out) and np.array_equal(out_len.cpu().numpy(), o_len)
+    sess.status()
+    sess.close()
 
 
 def test_session_capacity_errors(torch_dev):
