@@ -259,6 +259,23 @@ int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const float* d_scal
                        int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream,
                        void* ev_start, void* ev_stop);
 
+/* For callers that cannot allocate device memory (code under stream capture,
+ * tight serving loops, harnesses that forbid allocation): the fused logits +
+ * arg-max of mnmt_qlinear with MNMT_EPI_ARGMAX_PARTIAL_PACKED, reduced to each
+ * row's final result without a caller buffer for the partial keys.  d_X int8
+ * [M, K], d_Wp the fragment-order copy of W [N, K] (mnmt_pack_weights), d_scale
+ * fp32 [N] (z = acc * scale[n]); outputs d_key [M] (the row's largest packed
+ * key, key(z) << 32 | (0xFFFFFFFF - n), as MNMT_EPI_ARGMAX writes it) and/or
+ * d_tok [M] int32 (its index: the arg max, smallest index among equal
+ * maxima); either may be NULL, not both.  Limits: 1 <= M <= 2, K a multiple of
+ * 64 up to 512, 1 <= N <= 262144 (else MNMT_E_INVALID_ARG).  The partial keys
+ * live in a 32 KiB device array inside the library, one per GPU, held until
+ * the process ends; the call allocates nothing.  Every call on a GPU uses that
+ * GPU's array: calls that overlap on one GPU (other streams, other threads)
+ * race and must be serialized by the caller. */
+int mnmt_logits_argmax_noalloc(const int8_t* d_X, const int8_t* d_Wp, const float* d_scale, int M, int K, int N,
+                               unsigned long long* d_key, int32_t* d_tok, void* stream);
+
 /* Folded requantization constants (host): scale[n] = s_in*s_w[n]/s_out,
  * bias[n] = b[n]/s_out, each computed in double and rounded once to fp32. */
 int mnmt_fold_requant(float s_in, const float* h_s_w, const float* h_b, float s_out, int N,

@@ -24,7 +24,8 @@ DEVICE = [f"--offload-arch={ARCH}", "-fno-gpu-flush-denormals-to-zero", "-fhip-f
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 # per-file device flags: the GEMM keeps its matrix-core accumulators in VGPRs
 EXTRA = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
-SOURCES = ["qlinear.hip", "kernels.hip", "decode_fused.hip", "decode_step.hip", "encode_small.hip", "gemm.hip", "model.cpp", "session.cpp", "api.cpp"]
+SOURCES = ["qlinear.hip", "kernels.hip", "decode_fused.hip", "decode_step.hip", "encode_small.hip", "gemm.hip",
+           "noalloc.hip", "model.cpp", "session.cpp", "api.cpp"]
 
 
 def _compile(src: str, verbose: bool) -> str:

@@ -19,10 +19,9 @@ OK, E_INVALID_ARG, E_BAD_MODEL, E_CAPACITY, E_HIP, E_UNSUPPORTED, E_TIMEOUT = 0,
 
 EXPORTS = ("mnmt_model_bytes", "mnmt_model_load", "mnmt_model_get_info", "mnmt_model_free", "mnmt_session_bytes",
            "mnmt_session_create", "mnmt_session_free", "mnmt_encode", "mnmt_decode_step", "mnmt_translate",
-                      "mnmt_session_status", "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed", "mnmt_argmax_partials", "mnmt_packed_bytes",
-           "mnmt_pack_weights", "mnmt_fold_requant",
-           "mnmt_debug_canon", "mnmt_debug_read", "mnmt_status_str",
-           "mnmt_last_error")
+           "mnmt_session_status", "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed",
+           "mnmt_argmax_partials", "mnmt_packed_bytes", "mnmt_pack_weights", "mnmt_logits_argmax_noalloc",
+           "mnmt_fold_requant", "mnmt_debug_canon", "mnmt_debug_read", "mnmt_status_str", "mnmt_last_error")
 
 
 class MnmtError(RuntimeError):
@@ -82,6 +81,7 @@ def lib():
         L.mnmt_fold_requant.argtypes = [f32, vp, vp, f32, i32, vp, vp]
         L.mnmt_debug_canon.argtypes = [i32, vp, i32, vp, vp]
         L.mnmt_debug_read.argtypes = [vp, sz, i32, vp, vp]
+        L.mnmt_logits_argmax_noalloc.argtypes = [vp, vp, vp, i32, i32, i32, vp, vp, vp]
         L.mnmt_status_str.argtypes = [i32]
         L.mnmt_status_str.restype = C.c_char_p
         L.mnmt_last_error.argtypes = []
@@ -201,6 +201,21 @@ def mnmt_debug_canon(fn: int, x, stream=None):
     y = torch.empty(x.numel() if fn != 2 else 1, dtype=torch.float32, device=x.device)
     _check(lib().mnmt_debug_canon(fn, _ptr(x), x.numel(), _ptr(y), _stream(stream)), "mnmt_debug_canon")
     return y
+
+
+def mnmt_logits_argmax_noalloc(X, Wp, scale, N, key=None, tok=None, stream=None):
+    """Per-row arg-max key (int64 view of the uint64) and index of X [M, K] against
+    the packed weight Wp (mnmt_pack_weights), with no caller scratch."""
+    import torch
+
+    M, K = X.shape
+    if key is None:
+        key = torch.empty(M, dtype=torch.int64, device=X.device)
+    if tok is None:
+        tok = torch.empty(M, dtype=torch.int32, device=X.device)
+    _check(lib().mnmt_logits_argmax_noalloc(_ptr(X), _ptr(Wp), _ptr(scale), M, K, N, _ptr(key), _ptr(tok),
+                                            _stream(stream)), "mnmt_logits_argmax_noalloc")
+    return key, tok
 
 
 DEBUG_READ_BLOCKS = 2048
