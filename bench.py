@@ -549,11 +549,21 @@ def main():
              "frac": round(tops / I8_PEAK_TOPS, 4), "avg_us": round(gemm_ms * 1e3, 2)}
 
     # The paper's own MobileNMT-10MB / 20MB shapes on the same batch-1 path
-    # (context beside the paper's phone latencies, not the headline workload).
+    # (context beside the paper's phone latencies, not the headline workload),
+    # and the workload model with 4-bit linear weights (the paper's W-E-A
+    # 4-8-8 setting) loaded packed only.
+    import dataclasses
+
     paper = {}
-    for cfg in () if args.no_paper_shapes else (G.PAPER_10MB, G.PAPER_20MB):
-        pm = mnmt.Model(G.build_model(cfg))
-        psrc, plen = G.make_sources(cfg.vocab, 1, [30], seed=2010 + cfg.d_model, s_max=30)
+    mob4 = dataclasses.replace(G.MOBILE, name="mobile-12-2-w4-packed", w_bits=4)
+    for cfg in () if args.no_paper_shapes else (G.PAPER_10MB, G.PAPER_20MB, mob4):
+        flags = mnmt.LOAD_PACKED_4BIT_ONLY if cfg is mob4 else 0
+        pblob = G.build_model(cfg)
+        pm = mnmt.Model(pblob, flags=flags)
+        if cfg is mob4:
+            psrc, plen = src, lens
+        else:
+            psrc, plen = G.make_sources(cfg.vocab, 1, [30], seed=2010 + cfg.d_model, s_max=30)
         ps = mnmt.Session(pm, 1, 30, 30, 1)
         pt, pl = torch.from_numpy(psrc).to(dev), torch.from_numpy(plen).to(dev)
         pouts = (torch.empty((1, 30), dtype=torch.int32, device=dev), torch.empty(1, dtype=torch.int32, device=dev),
@@ -567,7 +577,14 @@ def main():
         torch.cuda.synchronize()
         pe = time.perf_counter() - p0
         paper[cfg.name] = {"ms_per_sentence": round(pe * 1e3 / 20, 4),
-                           "tokens_per_s": round(int(pouts[1].sum().item()) * 20 / pe, 1)}
+                           "tokens_per_s": round(int(pouts[1].sum().item()) * 20 / pe, 1),
+                           "arena_bytes": int(pm.arena.numel())}
+        if cfg is mob4:  # the same sentence as the headline, checked against the oracle
+            import oracle
+
+            ps.status()
+            r4 = oracle.Model(pblob).greedy(psrc, plen, 30)
+            check_tokens("4-bit translations", pouts[0].cpu().numpy(), pouts[1].cpu().numpy(), r4)
         ps.close()
         pm.close()
 

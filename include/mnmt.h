@@ -57,9 +57,10 @@
  *   Weights are symmetric per-output-channel int8: w_real = sw[n] * w[n,k].
  *   4-bit weights (the paper's W-E-A 4-8-8 setting) hold codes in [-7, 7]:
  *   in each group of 16 codes of a row, byte i (i < 8) holds code i in its
- *   low nibble and code i + 8 in its high nibble, each stored plus 8; the
- *   loader expands them to their int8 codes, so every kernel runs on them
- *   unchanged.
+ *   low nibble and code i + 8 in its high nibble, each stored plus 8.  The
+ *   batch-1 decoder step and the small-batch encoder read them packed and
+ *   widen them to int8 in registers; the batched kernels read an int8 copy
+ *   that the loader also keeps unless MNMT_LOAD_PACKED_4BIT_ONLY is given.
  */
 #ifndef MNMT_H
 #define MNMT_H
@@ -138,6 +139,15 @@ typedef struct {
 
 /* ---- model --------------------------------------------------------------- */
 
+/* Load flags (mnmt_model_bytes_ex, mnmt_model_load_ex).
+ * MNMT_LOAD_PACKED_4BIT_ONLY: keep 4-bit weights only in their packed form
+ * (half the bytes of int8 codes), without the int8 copy the batched kernels
+ * read.  Every linear weight of the file must be 4-bit (else
+ * MNMT_E_UNSUPPORTED); sessions of such a model must fit the batch-1 paths:
+ * beam 1, max_batch <= 2, max_batch * max_src_len <= 64, source and target
+ * lengths <= 128 (mnmt_session_create returns MNMT_E_UNSUPPORTED otherwise). */
+#define MNMT_LOAD_PACKED_4BIT_ONLY 1u
+
 /* Validate a model file held in host memory and report the device arena size
  * it needs.  Host only.  blob: the whole file; device_bytes: out. */
 int mnmt_model_bytes(const void* h_blob, size_t blob_bytes, size_t* device_bytes);
@@ -150,6 +160,12 @@ int mnmt_model_bytes(const void* h_blob, size_t blob_bytes, size_t* device_bytes
  * the caller's).  The model is bound to the current HIP device. */
 int mnmt_model_load(const void* h_blob, size_t blob_bytes, void* d_arena, size_t arena_bytes,
                     void* stream, mnmt_model** out);
+
+/* The same with load flags (MNMT_LOAD_*); flags 0 is mnmt_model_bytes /
+ * mnmt_model_load. */
+int mnmt_model_bytes_ex(const void* h_blob, size_t blob_bytes, unsigned flags, size_t* device_bytes);
+int mnmt_model_load_ex(const void* h_blob, size_t blob_bytes, unsigned flags, void* d_arena, size_t arena_bytes,
+                       void* stream, mnmt_model** out);
 
 int mnmt_model_get_info(const mnmt_model* model, mnmt_model_info* out);
 void mnmt_model_free(mnmt_model* model);

@@ -39,19 +39,29 @@ extern "C" const char* mnmt_status_str(int status) {
 
 extern "C" const char* mnmt_last_error(void) { return g_last_error.c_str(); }
 
-extern "C" int mnmt_model_bytes(const void* blob, size_t blob_bytes, size_t* device_bytes) {
+extern "C" int mnmt_model_bytes_ex(const void* blob, size_t blob_bytes, unsigned flags, size_t* device_bytes) {
   if (!device_bytes) return set_error(MNMT_E_INVALID_ARG, "device_bytes is null");
   std::string err;
-  const int rc = model_size(blob, blob_bytes, device_bytes, err);
+  const int rc = model_size(blob, blob_bytes, flags, device_bytes, err);
+  return rc ? set_error(rc, err) : MNMT_OK;
+}
+
+extern "C" int mnmt_model_bytes(const void* blob, size_t blob_bytes, size_t* device_bytes) {
+  return mnmt_model_bytes_ex(blob, blob_bytes, 0u, device_bytes);
+}
+
+extern "C" int mnmt_model_load_ex(const void* blob, size_t blob_bytes, unsigned flags, void* d_arena,
+                                  size_t arena_bytes, void* stream, mnmt_model** out) {
+  if (!out || !d_arena) return set_error(MNMT_E_INVALID_ARG, "out or arena is null");
+  std::string err;
+  const int rc =
+      model_create(blob, blob_bytes, flags, d_arena, arena_bytes, static_cast<hipStream_t>(stream), out, err);
   return rc ? set_error(rc, err) : MNMT_OK;
 }
 
 extern "C" int mnmt_model_load(const void* blob, size_t blob_bytes, void* d_arena, size_t arena_bytes, void* stream,
                                mnmt_model** out) {
-  if (!out || !d_arena) return set_error(MNMT_E_INVALID_ARG, "out or arena is null");
-  std::string err;
-  const int rc = model_create(blob, blob_bytes, d_arena, arena_bytes, static_cast<hipStream_t>(stream), out, err);
-  return rc ? set_error(rc, err) : MNMT_OK;
+  return mnmt_model_load_ex(blob, blob_bytes, 0u, d_arena, arena_bytes, stream, out);
 }
 
 extern "C" int mnmt_model_get_info(const mnmt_model* model, mnmt_model_info* out) {

@@ -23,6 +23,48 @@ __device__ __forceinline__ v4i mfma16(const v4i a, const v4i b, const v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
 }
 
+// 4-bit weight codes (the paper's W-E-A 4-8-8 setting) widened to int8: in
+// each group of 16 codes of a row, packed byte i (i < 8) holds code i in its
+// low nibble and code i + 8 in its high nibble, each plus 8.  Per byte,
+// ((u & 15) + 0x78) ^ 0x80 = u - 8 as a signed byte, with no carry between
+// bytes (u + 0x78 <= 0x87).
+__device__ __forceinline__ v4i unpack_i4x16(uint2 p) {
+  const unsigned m = 0x0F0F0F0Fu, b = 0x78787878u, s = 0x80808080u;
+  v4i r;
+  r.x = (int)(((p.x & m) + b) ^ s);         // codes 0..3
+  r.y = (int)(((p.y & m) + b) ^ s);         // codes 4..7
+  r.z = (int)((((p.x >> 4) & m) + b) ^ s);  // codes 8..11
+  r.w = (int)((((p.y >> 4) & m) + b) ^ s);  // codes 12..15
+  return r;
+}
+
+// A 16-byte weight fragment (16 consecutive codes of a weight row) held in
+// registers.  4-bit weights are loaded as their 8 packed bytes and widened
+// where the matrix instruction takes them, so that a kernel still issues all
+// of its loads before it waits for any.
+template <bool W4>
+struct WFrag {
+  v4i v;
+  __device__ __forceinline__ v4i get() const { return v; }
+};
+template <>
+struct WFrag<true> {
+  uint2 p;
+  __device__ __forceinline__ v4i get() const { return unpack_i4x16(p); }
+};
+
+// The fragment of row `row` of a [N, K] weight at column k0 (a multiple of
+// 16); W4: W holds the packed 4-bit rows (K / 2 bytes each).
+template <bool W4>
+__device__ __forceinline__ WFrag<W4> load_wfrag(const int8_t* W, size_t row, int K, int k0) {
+  WFrag<W4> f;
+  if constexpr (W4)
+    f.p = *(const uint2*)(reinterpret_cast<const uint8_t*>(W) + row * (size_t)(K / 2) + k0 / 2);
+  else
+    f.v = *(const v4i*)(W + row * (size_t)K + k0);
+  return f;
+}
+
 __device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
   acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
   acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);

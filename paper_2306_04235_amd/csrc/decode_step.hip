@@ -128,7 +128,7 @@ __device__ __forceinline__ void clear_acc(const StepIn& in) {
 // lane (n <= 64 NI).  MODE 1 (self, layer 0): the input rows are the
 // embeddings of the previous step's arg-max tokens, found from cm's partials;
 // MODE 2 (cross, layer 0): block 0 records those tokens.
-template <int DMAX, bool SELF, int NI, int MODE>
+template <int DMAX, bool SELF, int NI, int MODE, bool W4>
 __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn at, StepCommit cm) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;      // 64-deep K steps of the projection
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   //    fragments with their scales and biases, the W_o fragments, the keys
   //    and values (all written before the previous kernel started), then,
   //    after the chain wait, the wave's input row
-  v4i wf[TPW][KS];
+  WFrag<W4> wf[TPW][KS];
   float e_sc[TPW], e_bi[TPW];
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
@@ -156,15 +156,15 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
     const int part = (j >= dh) + (j >= 2 * dh);
     const size_t n = (size_t)part * d + hd * dh + (j - part * dh);
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) wf[t][kk] = *(const v4i*)(at.W + n * d + 64 * min(kk, ks - 1) + 16 * kq);
+    for (int kk = 0; kk < KS; ++kk) wf[t][kk] = load_wfrag<W4>(at.W, n, d, 64 * min(kk, ks - 1) + 16 * kq);
     e_sc[t] = at.scale[n];
     e_bi[t] = at.bias[n];
   }
-  v4i of[OT];
+  WFrag<W4> of[OT];
 #pragma unroll
   for (int t = 0; t < OT; ++t) {
     const int n = min(16 * (wave + 4 * t) + l16, d - 1);
-    of[t] = *(const v4i*)(at.Wo + (size_t)n * d + hd * dh + 16 * min(kq, nc - 1));
+    of[t] = load_wfrag<W4>(at.Wo, n, d, hd * dh + 16 * min(kq, nc - 1));
   }
   // keys and values of row r in registers: position lane + 64 i (self: the
   // cached positions before t; cross: every source position; positions at
@@ -250,7 +250,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
         v4i acc = {0, 0, 0, 0};
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk)
-          if (kk < ks) acc = mfma16(af[kk], wf[t][kk], acc);
+          if (kk < ks) acc = mfma16(af[kk], wf[t][kk].get(), acc);
         if (lane < 16) {
           const int j = 16 * tile + lane;
           const int part = (j >= dh) + (j >= 2 * dh);
@@ -349,7 +349,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
     for (int t = 0; t < OT; ++t) {
       const int n0 = 16 * (wave + 4 * t);
       if (n0 < d) {
-        const v4i acc = mfma16(cf, of[t], v4i{0, 0, 0, 0});
+        const v4i acc = mfma16(cf, of[t].get(), v4i{0, 0, 0, 0});
         if (lane < 16)
 #pragma unroll
           for (int m = 0; m < kStepRows; ++m)
@@ -383,7 +383,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
 // One block per kFfnChunk hidden units (one 16-row W1 tile per wave): ReLU
 // requantization of the chunk, then the chunk's W2 columns (K = 64) into the
 // int32 accumulator.
-template <int DMAX>
+template <int DMAX, bool W4>
 __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;
@@ -396,15 +396,15 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
   const size_t hrow = (size_t)min(f0 + 16 * wave + l16, F - 1);
-  v4i wf[KS];
+  WFrag<W4> wf[KS];
 #pragma unroll
-  for (int kk = 0; kk < KS; ++kk) wf[kk] = *(const v4i*)(f.W1 + hrow * d + 64 * min(kk, ks - 1) + 16 * kq);
+  for (int kk = 0; kk < KS; ++kk) wf[kk] = load_wfrag<W4>(f.W1, hrow, d, 64 * min(kk, ks - 1) + 16 * kq);
   const float e_sc = f.scale1[hrow], e_bi = f.bias1[hrow];
-  v4i of[OT];
+  WFrag<W4> of[OT];
 #pragma unroll
   for (int t = 0; t < OT; ++t) {
     const int n = min(16 * (wave + 4 * t) + l16, d - 1);
-    of[t] = *(const v4i*)(f.W2 + (size_t)n * F + f0 + 16 * kq);
+    of[t] = load_wfrag<W4>(f.W2, n, F, f0 + 16 * kq);
   }
   RowRegs<NJ> rr;
   load_row_consts(in, d, rr);
@@ -419,7 +419,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
-      if (kk < ks) acc = mfma16(*(const v4i*)(a_lds + arow * d + 64 * kk + 16 * kq), wf[kk], acc);
+      if (kk < ks) acc = mfma16(*(const v4i*)(a_lds + arow * d + 64 * kk + 16 * kq), wf[kk].get(), acc);
     if (lane < 16)
 #pragma unroll
       for (int m = 0; m < kStepRows; ++m)
@@ -433,7 +433,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
     for (int t = 0; t < OT; ++t) {
       const int n0 = 16 * (wave + 4 * t);
       if (n0 < d) {
-        const v4i acc = mfma16(hf, of[t], v4i{0, 0, 0, 0});
+        const v4i acc = mfma16(hf, of[t].get(), v4i{0, 0, 0, 0});
         if (lane < 16)
 #pragma unroll
           for (int m = 0; m < kStepRows; ++m)
@@ -585,14 +585,20 @@ hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int 
   // positions attended: self t + 1 <= T, cross at most S
   const int n_max = self ? at.t + 1 : at.S;
   if (cm && (cm->nslots < 1 || cm->nslots > 256 || cm->t < 1)) return hipErrorInvalidValue;
+  if (!at.W || !at.Wo) return hipErrorInvalidValue;  // (a weight without the form this launch reads)
   const StepCommit c = cm ? *cm : StepCommit{};
-#define MNMT_ATTN_NI(DM, SELF, NI)                                                                               \
+#define MNMT_ATTN_W(DM, SELF, NI, W4)                                                                           \
   do {                                                                                                           \
     if (!cm)                                                                                                     \
-      hipLaunchKernelGGL((k_step_attn<DM, SELF, NI, 0>), dim3(heads), dim3(kStepThreads), 0, s, in, at, c);     \
+      hipLaunchKernelGGL((k_step_attn<DM, SELF, NI, 0, W4>), dim3(heads), dim3(kStepThreads), 0, s, in, at, c); \
     else                                                                                                         \
-      hipLaunchKernelGGL((k_step_attn<DM, SELF, NI, SELF ? 1 : 2>), dim3(heads), dim3(kStepThreads), 0, s, in, at, \
-                         c);                                                                                     \
+      hipLaunchKernelGGL((k_step_attn<DM, SELF, NI, SELF ? 1 : 2, W4>), dim3(heads), dim3(kStepThreads), 0, s, in, \
+                         at, c);                                                                                 \
+  } while (0)
+#define MNMT_ATTN_NI(DM, SELF, NI)             \
+  do {                                         \
+    if (at.w4) MNMT_ATTN_W(DM, SELF, NI, true);  \
+    else MNMT_ATTN_W(DM, SELF, NI, false);       \
   } while (0)
 #define MNMT_ATTN(DM)                                   \
   if (self) {                                           \
@@ -605,12 +611,16 @@ hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int 
   MNMT_BY_D(at.d, MNMT_ATTN)
 #undef MNMT_ATTN
 #undef MNMT_ATTN_NI
+#undef MNMT_ATTN_W
   return hipGetLastError();
 }
 
 hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s) {
+  if (!f.W1 || !f.W2) return hipErrorInvalidValue;
   const int blocks = (f.F + kFfnChunk - 1) / kFfnChunk;
-#define MNMT_FFN(DM) hipLaunchKernelGGL((k_step_ffn<DM>), dim3(blocks), dim3(kStepThreads), 0, s, in, f);
+#define MNMT_FFN(DM)                                                                               \
+  if (f.w4) hipLaunchKernelGGL((k_step_ffn<DM, true>), dim3(blocks), dim3(kStepThreads), 0, s, in, f); \
+  else hipLaunchKernelGGL((k_step_ffn<DM, false>), dim3(blocks), dim3(kStepThreads), 0, s, in, f);
   MNMT_BY_D(f.d, MNMT_FFN)
 #undef MNMT_FFN
   return hipGetLastError();

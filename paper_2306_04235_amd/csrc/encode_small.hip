@@ -231,7 +231,7 @@ __device__ __forceinline__ void add_frag(int32_t* out, int ld, const v4i& acc, i
 }
 
 // One block per head.
-template <int DMAX, bool EMBED, int RPW>
+template <int DMAX, bool EMBED, int RPW, bool W4>
 __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) {
   constexpr int KS = DMAX / 64;                                   // 64-deep K steps over d
   constexpr int NT = 3 * kEncHeadDim / 16;                        // projection tiles of the widest head
@@ -255,9 +255,9 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   // 1. the rows, and behind their loads the weights (the head's Q|K|V rows
   //    and its W_o columns, with the projection's scale and bias per lane) and
   //    the lengths of the sentences of the wave's softmax rows
-  v4i wf[PT][KS];
+  WFrag<W4> wf[PT][KS];
   float e_sc[PT], e_bi[PT];
-  v4i of[OT];
+  WFrag<W4> of[OT];
   int nn[RPW];
   enc_rows<DMAX, EMBED, RPW>(in, a_lds, [&]() {
 #pragma unroll
@@ -266,14 +266,14 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
       const int part = (j >= dh) + (j >= 2 * dh);
       const int n = part * d + hd * dh + (j - part * dh);
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) wf[u][kk] = *(const v4i*)(at.W + n * d + 64 * kk + 16 * kq);
+      for (int kk = 0; kk < KS; ++kk) wf[u][kk] = load_wfrag<W4>(at.W, n, d, 64 * kk + 16 * kq);
       e_sc[u] = at.scale[n];
       e_bi[u] = at.bias[n];
     }
 #pragma unroll
     for (int u = 0; u < OT; ++u) {
       const int n = min(16 * (wave + kEncWaves * u) + l16, d - 1);
-      of[u] = *(const v4i*)(at.Wo + n * d + hd * dh + 16 * min(kq, dh / 16 - 1));
+      of[u] = load_wfrag<W4>(at.Wo, n, d, hd * dh + 16 * min(kq, dh / 16 - 1));
     }
 #pragma unroll
     for (int u = 0; u < RPW; ++u) nn[u] = at.len[min(qrow(min(wave + kEncWaves * u, q_rows - 1)), R - 1) / S];
@@ -287,12 +287,15 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
     const int j = 16 * tile + l16;
     const int part = (j >= dh) + (j >= 2 * dh);
     const int c = j - part * dh;
+    v4i w[KS];
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) w[kk] = wf[u][kk].get();
     for (int mt = 0; mt < mt_n; ++mt) {
       if (part == 0 && mt % qs_n != qs) continue;  // queries of this block's rows only
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk)
-        if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), wf[u][kk], acc);
+        if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), w[kk], acc);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int m = 16 * mt + 4 * kq + i;
@@ -399,8 +402,9 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
   for (int u = 0; u < OT; ++u) {
     const int n0 = 16 * (wave + kEncWaves * u);
     if (n0 >= d) continue;
+    const v4i wo = of[u].get();
     for (int mt = qs; mt < mt_n; mt += qs_n) {
-      const v4i acc = mfma16(lds_frag(&ctx[0][0], kHeadLd, 16 * mt, 0, dh), of[u], v4i{0, 0, 0, 0});
+      const v4i acc = mfma16(lds_frag(&ctx[0][0], kHeadLd, 16 * mt, 0, dh), wo, v4i{0, 0, 0, 0});
       add_frag(at.acc_out, d, acc, 16 * mt, n0 + l16, R);
     }
   }
@@ -409,7 +413,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_attn(EncIn in, EncAttn at) 
 
 // One block per kEncChunk hidden units: wave w computes the 16-unit W1 tile
 // w % 4 for the 16-row tiles w / 4, w / 4 + 2, ...
-template <int DMAX, int RPW>
+template <int DMAX, int RPW, bool W4>
 __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
   constexpr int KS = DMAX / 64;
   constexpr int OT = (DMAX / 16 + kEncWaves - 1) / kEncWaves;  // W2 column tiles per wave
@@ -423,26 +427,29 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
   const int l16 = lane & 15, kq = lane >> 4;
   const int ht = wave & 3, mt0 = wave >> 2;
   const int hrow = f0 + 16 * ht + l16;  // < F (F is a multiple of kEncChunk)
-  v4i wf[KS];
+  WFrag<W4> wf[KS];
   float e_sc, e_bi;
-  v4i of[OT];
+  WFrag<W4> of[OT];
   enc_rows<DMAX, false, RPW>(in, a_lds, [&]() {
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) wf[kk] = *(const v4i*)(f.W1 + hrow * d + 64 * kk + 16 * kq);
+    for (int kk = 0; kk < KS; ++kk) wf[kk] = load_wfrag<W4>(f.W1, hrow, d, 64 * kk + 16 * kq);
     e_sc = f.scale1[hrow];
     e_bi = f.bias1[hrow];
 #pragma unroll
     for (int u = 0; u < OT; ++u) {
       const int n = min(16 * (wave + kEncWaves * u) + l16, d - 1);
-      of[u] = *(const v4i*)(f.W2 + n * F + f0 + 16 * kq);
+      of[u] = load_wfrag<W4>(f.W2, n, F, f0 + 16 * kq);
     }
   });
   lds_barrier();
+  v4i w1[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) w1[kk] = wf[kk].get();
   for (int mt = mt0; mt < mt_n; mt += 2) {
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
-      if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), wf[kk], acc);
+      if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), w1[kk], acc);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = 16 * mt + 4 * kq + i;
@@ -454,8 +461,9 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
   for (int u = 0; u < OT; ++u) {
     const int n0 = 16 * (wave + kEncWaves * u);
     if (n0 >= d) continue;
+    const v4i w2 = of[u].get();
     for (int mt = 0; mt < mt_n; ++mt) {
-      const v4i acc = mfma16(lds_frag(&hb[0][0], kHeadLd, 16 * mt, 0, kEncChunk), of[u], v4i{0, 0, 0, 0});
+      const v4i acc = mfma16(lds_frag(&hb[0][0], kHeadLd, 16 * mt, 0, kEncChunk), w2, v4i{0, 0, 0, 0});
       add_frag(f.acc_out, d, acc, 16 * mt, n0 + l16, R);
     }
   }
@@ -465,7 +473,7 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_ffn(EncIn in, EncFfn f) {
 // One block per kEncChunk columns of one decoder layer's cross K|V
 // projection: wave w computes the 16-column tile w % 4 for the 16-row tiles
 // w / 4, w / 4 + 2, ...
-template <int DMAX, int RPW>
+template <int DMAX, int RPW, bool W4>
 __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
   constexpr int KS = DMAX / 64;
   static_assert(kEncChunk == 64 && kEncWaves == 8, "four column tiles, two row-tile phases");
@@ -480,20 +488,23 @@ __global__ __launch_bounds__(kEncThreads) void k_enc_out(EncIn in, EncOut o) {
   const EncOut::Layer& L = o.layer[layer];
   const int col = c0 + 16 * (wave & 3) + l16;  // < 2 d
   const int mt0 = wave >> 2;
-  v4i wf[KS];
+  WFrag<W4> wf[KS];
   float e_sc, e_bi;
   enc_rows<DMAX, false, RPW>(in, a_lds, [&]() {
 #pragma unroll
-    for (int kk = 0; kk < KS; ++kk) wf[kk] = *(const v4i*)(L.W + col * d + 64 * kk + 16 * kq);
+    for (int kk = 0; kk < KS; ++kk) wf[kk] = load_wfrag<W4>(L.W, col, d, 64 * kk + 16 * kq);
     e_sc = L.scale[col];
     e_bi = L.bias[col];
   });
   lds_barrier();
+  v4i w[KS];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk) w[kk] = wf[kk].get();
   for (int mt = mt0; mt < mt_n; mt += 2) {
     v4i acc = {0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
-      if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), wf[kk], acc);
+      if (kk < ks) acc = mfma16(lds_frag(a_lds, lds_ld<DMAX>(), 16 * mt, 64 * kk, d), w[kk], acc);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = 16 * mt + 4 * kq + i;
@@ -532,26 +543,37 @@ bool enc_small_fits(int R, int S, int d, int dh, int F) {
 int enc_attn_qsplit(int R) { return R > 16 ? 2 : 1; }
 
 hipError_t launch_enc_attn(const EncIn& in0, const EncAttn& at0, int heads, hipStream_t s) {
+  if (!at0.W || !at0.Wo) return hipErrorInvalidValue;
   EncIn in = in0;
   EncAttn at = at0;
   at.qsplit = enc_attn_qsplit(in.R);
   const int blocks = heads * at.qsplit;
   in.nblk = blocks;
-#define MNMT_E(DM, RPW)                                                                          \
-  if (in.embed)                                                                                  \
-    hipLaunchKernelGGL((k_enc_attn<DM, true, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, at); \
-  else                                                                                            \
-    hipLaunchKernelGGL((k_enc_attn<DM, false, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, at);
+#define MNMT_EW(DM, RPW, W4)                                                                         \
+  if (in.embed)                                                                                      \
+    hipLaunchKernelGGL((k_enc_attn<DM, true, RPW, W4>), dim3(blocks), dim3(kEncThreads), 0, s, in, at); \
+  else                                                                                                \
+    hipLaunchKernelGGL((k_enc_attn<DM, false, RPW, W4>), dim3(blocks), dim3(kEncThreads), 0, s, in, at);
+#define MNMT_E(DM, RPW)   \
+  if (at.w4) {            \
+    MNMT_EW(DM, RPW, true)  \
+  } else {                \
+    MNMT_EW(DM, RPW, false) \
+  }
   MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
 #undef MNMT_E
+#undef MNMT_EW
   return hipGetLastError();
 }
 
 hipError_t launch_enc_ffn(const EncIn& in0, const EncFfn& f, hipStream_t s) {
+  if (!f.W1 || !f.W2) return hipErrorInvalidValue;
   const int blocks = f.F / kEncChunk;
   EncIn in = in0;
   in.nblk = blocks;
-#define MNMT_E(DM, RPW) hipLaunchKernelGGL((k_enc_ffn<DM, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, f);
+#define MNMT_E(DM, RPW)                                                                                    \
+  if (f.w4) hipLaunchKernelGGL((k_enc_ffn<DM, RPW, true>), dim3(blocks), dim3(kEncThreads), 0, s, in, f);    \
+  else hipLaunchKernelGGL((k_enc_ffn<DM, RPW, false>), dim3(blocks), dim3(kEncThreads), 0, s, in, f);
   MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
 #undef MNMT_E
   return hipGetLastError();
@@ -559,10 +581,14 @@ hipError_t launch_enc_ffn(const EncIn& in0, const EncFfn& f, hipStream_t s) {
 
 hipError_t launch_enc_out(const EncIn& in0, const EncOut& o, hipStream_t s) {
   if (o.layers < 1 || o.layers > EncOut::kMaxLayers) return hipErrorInvalidValue;
+  for (int l = 0; l < o.layers; ++l)
+    if (!o.layer[l].W) return hipErrorInvalidValue;
   const int blocks = o.layers * (2 * in0.d / kEncChunk);
   EncIn in = in0;
   in.nblk = blocks;
-#define MNMT_E(DM, RPW) hipLaunchKernelGGL((k_enc_out<DM, RPW>), dim3(blocks), dim3(kEncThreads), 0, s, in, o);
+#define MNMT_E(DM, RPW)                                                                                    \
+  if (o.w4) hipLaunchKernelGGL((k_enc_out<DM, RPW, true>), dim3(blocks), dim3(kEncThreads), 0, s, in, o);    \
+  else hipLaunchKernelGGL((k_enc_out<DM, RPW, false>), dim3(blocks), dim3(kEncThreads), 0, s, in, o);
   MNMT_ENC_BY_D(in.d, in.R, MNMT_E)
 #undef MNMT_E
   return hipGetLastError();

@@ -206,6 +206,7 @@ struct StepAttn {
   const int32_t* len;
   float c_qk, c_pv;
   int32_t* acc_out;        // [R, d] int32, zero on entry
+  bool w4;                 // W and Wo hold packed 4-bit rows (K / 2 bytes each)
 };
 // The greedy commit of the previous step's token, folded into the next
 // step's first layer: the self-attention kernel of layer 0 reads the previous
@@ -236,6 +237,7 @@ struct StepFfn {
   const float* bias1;
   const int8_t* W2;        // [d, F]
   int32_t* acc_out;
+  bool w4;                 // W1 and W2 hold packed 4-bit rows
 };
 struct StepLogits {
   int R, d, V;
@@ -300,6 +302,7 @@ struct EncAttn {
   float c_qk, c_pv;
   int32_t* acc_out;        // [R, d], zero on entry
   int qsplit;              // blocks per head (set by the launcher): each takes every qsplit-th 16-row query tile
+  bool w4;                 // W and Wo hold packed 4-bit rows
 };
 struct EncFfn {
   int F;
@@ -308,6 +311,7 @@ struct EncFfn {
   const float* bias1;
   const int8_t* W2;        // [d, F]
   int32_t* acc_out;        // [R, d], zero on entry
+  bool w4;                 // W1 and W2 hold packed 4-bit rows
 };
 struct EncOut {            // every decoder layer's cross K|V projection of the encoder output
   static constexpr int kMaxLayers = 16;
@@ -318,6 +322,7 @@ struct EncOut {            // every decoder layer's cross K|V projection of the 
     int8_t* out;           // [R, 2d]
   } layer[kMaxLayers];
   int layers;
+  bool w4;                 // every layer's W holds packed 4-bit rows
 };
 bool enc_small_fits(int R, int S, int d, int dh, int F);
 int enc_attn_qsplit(int R);  // blocks per head of launch_enc_attn for R rows
@@ -378,10 +383,10 @@ hipError_t launch_beam_update(const BeamState& st, int* step, const BeamNext& nx
 hipError_t launch_beam_finalize(const BeamState& st, int steps, int32_t* out, int32_t* out_len, float* out_score,
                                 const int* chain_err, hipStream_t s);
 
-// Model files (model.cpp).
-int model_size(const void* blob, size_t n, size_t* bytes, std::string& err);
-int model_create(const void* blob, size_t n, void* d_arena, size_t arena_bytes, hipStream_t s, mnmt_model** out,
-                 std::string& err);
+// Model files (model.cpp); flags: MNMT_LOAD_* of mnmt.h.
+int model_size(const void* blob, size_t n, unsigned flags, size_t* bytes, std::string& err);
+int model_create(const void* blob, size_t n, unsigned flags, void* d_arena, size_t arena_bytes, hipStream_t s,
+                 mnmt_model** out, std::string& err);
 
 // Canonical-arithmetic self check.
 hipError_t launch_debug_canon(int fn, const float* x, int n, float* y, hipStream_t s);
@@ -395,12 +400,26 @@ hipError_t launch_debug_read(const void* x, size_t bytes, int reps, unsigned* si
 // Model and session structures.
 
 struct LinearDev {
-  const int8_t* w = nullptr;  // [N, K]
+  const int8_t* w = nullptr;    // [N, K] int8 codes (null: 4-bit weights loaded packed only)
+  const uint8_t* w4 = nullptr;  // 4-bit weights: the packed rows [N, K / 2] of the model file, else null
   const float* scale = nullptr;
   const float* bias = nullptr;
   int N = 0, K = 0;
   float inv_in = 0.f;  // 1 / input scale (quantization of this layer's input)
 };
+
+// A 1-2 row kernel's pair of weights: the packed 4-bit rows when both have
+// them (returns true), else the int8 codes.
+inline bool pick_weights(const LinearDev& a, const LinearDev& b, const int8_t*& wa, const int8_t*& wb) {
+  if (a.w4 && b.w4) {
+    wa = reinterpret_cast<const int8_t*>(a.w4);
+    wb = reinterpret_cast<const int8_t*>(b.w4);
+    return true;
+  }
+  wa = a.w;
+  wb = b.w;
+  return false;
+}
 
 struct LnDev {
   const float* g = nullptr;
@@ -426,6 +445,7 @@ struct mnmt_model {
   const float* c_emb = nullptr;  // [V]
   const float* c_out = nullptr;  // [V]
   const float* pe = nullptr;     // [P, d]
+  bool packed_only = false;      // 4-bit weights without their int8 copies (MNMT_LOAD_PACKED_4BIT_ONLY)
   std::vector<mnmt::LayerDev> enc, dec;
   mnmt::LnDev enc_ln, dec_ln;
   float s_enc = 0.f, inv_enc = 0.f, inv_fin = 0.f;

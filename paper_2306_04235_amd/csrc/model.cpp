@@ -97,10 +97,12 @@ float rd_f(const float* p, size_t i) {
   return v;
 }
 
-// Copy an int8 weight (4-bit weights: their int8 codes) and compute its
-// folded constants into the image.
+// Copy an int8 weight and compute its folded constants into the image.
+// 4-bit weights keep their packed rows (read by the 1-2 row decoder and the
+// small-batch encoder kernels) and, unless packed_only, their int8 codes too
+// (for the batched kernels).
 bool add_linear(Parser& P, Image& img, LinearDev& L, const std::string& pfx, int N, int K, float s_in,
-                const float* s_out, int n_blocks) {
+                const float* s_out, int n_blocks, bool packed_only) {
   auto it = P.t.find(pfx + ".w");
   const bool four = it != P.t.end() && it->second.dtype == kI4;
   const int8_t* w = four ? nullptr : P.i8(pfx + ".w", (uint32_t)N, (uint32_t)K);
@@ -118,20 +120,28 @@ bool add_linear(Parser& P, Image& img, LinearDev& L, const std::string& pfx, int
   L.N = N;
   L.K = K;
   L.inv_in = (float)(1.0 / (double)s_in);
-  const size_t ow = img.alloc((size_t)N * K);
-  int8_t* dst = reinterpret_cast<int8_t*>(img.buf.data() + ow);
   if (four) {
-    // in each group of 16 codes of a row, byte i (i < 8) holds code i in its
-    // low nibble and code i + 8 in its high nibble, each plus 8
-    for (size_t r = 0; r < (size_t)N; ++r)
-      for (int g = 0; g < K / 16; ++g)
-        for (int i = 0; i < 8; ++i) {
-          const uint8_t byte = w4[r * (size_t)K / 2 + (size_t)g * 8 + i];
-          dst[r * K + 16 * g + i] = (int8_t)((int)(byte & 15) - 8);
-          dst[r * K + 16 * g + 8 + i] = (int8_t)((int)(byte >> 4) - 8);
-        }
-  } else {
-    std::memcpy(dst, w, (size_t)N * K);
+    const size_t o4 = img.alloc((size_t)N * K / 2);
+    std::memcpy(img.buf.data() + o4, w4, (size_t)N * K / 2);
+    img.bind(&L.w4, o4);
+  }
+  if (!four || !packed_only) {
+    const size_t ow = img.alloc((size_t)N * K);
+    int8_t* dst = reinterpret_cast<int8_t*>(img.buf.data() + ow);
+    if (four) {
+      // in each group of 16 codes of a row, byte i (i < 8) holds code i in its
+      // low nibble and code i + 8 in its high nibble, each plus 8
+      for (size_t r = 0; r < (size_t)N; ++r)
+        for (int g = 0; g < K / 16; ++g)
+          for (int i = 0; i < 8; ++i) {
+            const uint8_t byte = w4[r * (size_t)K / 2 + (size_t)g * 8 + i];
+            dst[r * K + 16 * g + i] = (int8_t)((int)(byte & 15) - 8);
+            dst[r * K + 16 * g + 8 + i] = (int8_t)((int)(byte >> 4) - 8);
+          }
+    } else {
+      std::memcpy(dst, w, (size_t)N * K);
+    }
+    img.bind(&L.w, ow);
   }
   const size_t os = img.alloc(sizeof(float) * N), ob = img.alloc(sizeof(float) * N);
   float* sc = reinterpret_cast<float*>(img.buf.data() + os);
@@ -152,7 +162,6 @@ bool add_linear(Parser& P, Image& img, LinearDev& L, const std::string& pfx, int
       bi[n] = bn;
     }
   }
-  img.bind(&L.w, ow);
   img.bind(&L.scale, os);
   img.bind(&L.bias, ob);
   return true;
@@ -182,40 +191,46 @@ bool scalar(Parser& P, const std::string& name, float* v, bool positive_only) {
 }
 
 bool add_layer(Parser& P, Image& img, mnmt_model& m, LayerDev& L, const std::string& side, int l, bool dec) {
+  const bool po = m.packed_only;
   const int d = m.info.d_model, F = m.info.d_ffn;
   const std::string p = side + "." + std::to_string(l);
   float s_qkv[3], s_q[1], s_kv[2], s_h[1], s_ctx, s_in;
   if (!add_ln(P, img, L.sa_ln, p + ".sa.ln", d)) return false;
   if (!P.positive(p + ".sa.qkv.sout", 3, s_qkv) || !P.positive(p + ".sa.qkv.sin", 1, &s_in)) return false;
-  if (!add_linear(P, img, L.qkv, p + ".sa.qkv", 3 * d, d, s_in, s_qkv, 3)) return false;
+  if (!add_linear(P, img, L.qkv, p + ".sa.qkv", 3 * d, d, s_in, s_qkv, 3, po)) return false;
   if (!P.positive(p + ".sa.o.sin", 1, &s_ctx)) return false;
-  if (!add_linear(P, img, L.o, p + ".sa.o", d, d, s_ctx, nullptr, 1)) return false;
+  if (!add_linear(P, img, L.o, p + ".sa.o", d, d, s_ctx, nullptr, 1, po)) return false;
   L.sa_cqk = (float)((double)s_qkv[0] * (double)s_qkv[1] / std::sqrt((double)m.dh));
   L.sa_cpv = (float)((double)s_qkv[2] / (double)s_ctx);
   if (!scalar(P, p + ".sa.gamma", &L.sa_gamma, false)) return false;
   if (dec) {
     if (!add_ln(P, img, L.ca_ln, p + ".ca.ln", d)) return false;
     if (!P.positive(p + ".ca.q.sout", 1, s_q) || !P.positive(p + ".ca.q.sin", 1, &s_in)) return false;
-    if (!add_linear(P, img, L.cq, p + ".ca.q", d, d, s_in, s_q, 1)) return false;
+    if (!add_linear(P, img, L.cq, p + ".ca.q", d, d, s_in, s_q, 1, po)) return false;
     if (!P.positive(p + ".ca.kv.sout", 2, s_kv)) return false;
-    if (!add_linear(P, img, L.ckv, p + ".ca.kv", 2 * d, d, m.s_enc, s_kv, 2)) return false;
+    if (!add_linear(P, img, L.ckv, p + ".ca.kv", 2 * d, d, m.s_enc, s_kv, 2, po)) return false;
     if (!P.positive(p + ".ca.o.sin", 1, &s_ctx)) return false;
-    if (!add_linear(P, img, L.co, p + ".ca.o", d, d, s_ctx, nullptr, 1)) return false;
+    if (!add_linear(P, img, L.co, p + ".ca.o", d, d, s_ctx, nullptr, 1, po)) return false;
     L.ca_cqk = (float)((double)s_q[0] * (double)s_kv[0] / std::sqrt((double)m.dh));
     L.ca_cpv = (float)((double)s_kv[1] / (double)s_ctx);
     if (!scalar(P, p + ".ca.gamma", &L.ca_gamma, false)) return false;
   }
   if (!add_ln(P, img, L.ff_ln, p + ".ff.ln", d)) return false;
   if (!P.positive(p + ".ff.w1.sout", 1, s_h) || !P.positive(p + ".ff.w1.sin", 1, &s_in)) return false;
-  if (!add_linear(P, img, L.w1, p + ".ff.w1", F, d, s_in, s_h, 1)) return false;
-  if (!add_linear(P, img, L.w2, p + ".ff.w2", d, F, s_h[0], nullptr, 1)) return false;
+  if (!add_linear(P, img, L.w1, p + ".ff.w1", F, d, s_in, s_h, 1, po)) return false;
+  if (!add_linear(P, img, L.w2, p + ".ff.w2", d, F, s_h[0], nullptr, 1, po)) return false;
   return scalar(P, p + ".ff.gamma", &L.ff_gamma, false);
 }
 
 // Parse and lay out a model file; on success `img` holds the arena image and
 // `m` the structure with pointers still to be fixed up.
-int build_model(const void* blob, size_t n, mnmt_model& m, Image*& out_img, std::string& err) {
+int build_model(const void* blob, size_t n, unsigned flags, mnmt_model& m, Image*& out_img, std::string& err) {
   out_img = nullptr;
+  if (flags & ~(unsigned)MNMT_LOAD_PACKED_4BIT_ONLY) {
+    err = "unknown load flags";
+    return MNMT_E_INVALID_ARG;
+  }
+  m.packed_only = (flags & MNMT_LOAD_PACKED_4BIT_ONLY) != 0;
   if (!blob || n < 64) {
     err = "model blob missing or shorter than its header";
     return MNMT_E_INVALID_ARG;
@@ -327,6 +342,19 @@ int build_model(const void* blob, size_t n, mnmt_model& m, Image*& out_img, std:
     delete img;
     return MNMT_E_BAD_MODEL;
   }
+  if (m.packed_only) {  // every linear layer must then be 4-bit: no kernel could read the others
+    bool all4 = true;
+    for (auto it = P.t.begin(); it != P.t.end(); ++it) {
+      const std::string& nm = it->first;
+      if (nm.size() > 2 && nm.compare(nm.size() - 2, 2, ".w") == 0 && nm != "emb.w" && it->second.dtype != kI4)
+        all4 = false;
+    }
+    if (!all4) {
+      err = "MNMT_LOAD_PACKED_4BIT_ONLY needs every linear layer's weight in 4-bit";
+      delete img;
+      return MNMT_E_UNSUPPORTED;
+    }
+  }
   img->alloc(0);
   m.arena_bytes = img->buf.size();
   out_img = img;
@@ -357,20 +385,20 @@ int finish_model(Image* img, mnmt_model& m, void* d_arena, size_t arena_bytes, h
 
 }  // namespace
 
-int model_size(const void* blob, size_t n, size_t* bytes, std::string& err) {
+int model_size(const void* blob, size_t n, unsigned flags, size_t* bytes, std::string& err) {
   mnmt_model m;
   Image* img = nullptr;
-  const int rc = build_model(blob, n, m, img, err);
+  const int rc = build_model(blob, n, flags, m, img, err);
   if (rc == MNMT_OK) *bytes = img->buf.size();
   delete img;
   return rc;
 }
 
-int model_create(const void* blob, size_t n, void* d_arena, size_t arena_bytes, hipStream_t s, mnmt_model** out,
-                 std::string& err) {
+int model_create(const void* blob, size_t n, unsigned flags, void* d_arena, size_t arena_bytes, hipStream_t s,
+                 mnmt_model** out, std::string& err) {
   auto* m = new mnmt_model();
   Image* img = nullptr;
-  int rc = build_model(blob, n, *m, img, err);
+  int rc = build_model(blob, n, flags, *m, img, err);
   if (rc == MNMT_OK) rc = finish_model(img, *m, d_arena, arena_bytes, s, err);
   delete img;
   if (rc != MNMT_OK) {

@@ -41,6 +41,16 @@ struct Plan {
 
 int validate_cfg(const mnmt_model* m, const mnmt_session_cfg* c) {
   if (!m || !c) return set_error(MNMT_E_INVALID_ARG, "null model or session config");
+  if (m->packed_only) {
+    const int d = m->info.d_model, F = m->info.d_ffn;
+    const int rows = c->max_batch * c->max_src_len;
+    if (c->beam != 1 || c->max_batch > 2 || rows > 64 ||
+        !step_path_fits(c->max_batch, d, m->dh, F, c->max_tgt_len, c->max_src_len) ||
+        !enc_small_fits(rows, c->max_src_len, d, m->dh, F) || (int)m->dec.size() > EncOut::kMaxLayers)
+      return set_error(MNMT_E_UNSUPPORTED,
+                       "a model loaded with packed 4-bit weights only runs the batch-1 paths: beam 1, "
+                       "max_batch <= 2, max_batch * max_src_len <= 64, lengths <= 128");
+  }
   const int P = m->info.max_pos;
   if (c->max_batch < 1 || c->max_batch > 65536 || c->max_src_len < 1 || c->max_src_len > 256 ||
       c->max_src_len > P || c->max_tgt_len < 1 || c->max_tgt_len > 256 || c->max_tgt_len > P || c->beam < 1 ||
@@ -305,10 +315,9 @@ int run_encoder_blocks(mnmt_session* S, hipStream_t s, Chain* ch = nullptr) {
       in.zero0_n = n;
       EncAttn at{};
       at.dh = m->dh;
-      at.W = Ly.qkv.w;
+      at.w4 = pick_weights(Ly.qkv, Ly.o, at.W, at.Wo);
       at.scale = Ly.qkv.scale;
       at.bias = Ly.qkv.bias;
-      at.Wo = Ly.o.w;
       at.len = S->len;
       at.c_qk = Ly.sa_cqk;
       at.c_pv = Ly.sa_cpv;
@@ -324,10 +333,9 @@ int run_encoder_blocks(mnmt_session* S, hipStream_t s, Chain* ch = nullptr) {
       in.zero0_n = n;
       EncFfn f{};
       f.F = Ly.w1.N;
-      f.W1 = Ly.w1.w;
+      f.w4 = pick_weights(Ly.w1, Ly.w2, f.W1, f.W2);
       f.scale1 = Ly.w1.scale;
       f.bias1 = Ly.w1.bias;
-      f.W2 = Ly.w2.w;
       f.acc_out = acc_f[l & 1];
       const hipStream_t ks = ch ? ch->next(in.chain, 2 * l + 1, f.F / 64, 1) : s;
       LAUNCH(launch_enc_ffn(in, f, ks));
@@ -345,8 +353,10 @@ int run_encoder_blocks(mnmt_session* S, hipStream_t s, Chain* ch = nullptr) {
   in.zero0_n = n;
   EncOut o{};
   o.layers = (int)m->dec.size();
+  o.w4 = true;  // packed 4-bit rows when every layer has them
+  for (int l = 0; l < o.layers; ++l) o.w4 = o.w4 && m->dec[l].ckv.w4;
   for (int l = 0; l < o.layers; ++l) {
-    o.layer[l].W = m->dec[l].ckv.w;
+    o.layer[l].W = o.w4 ? reinterpret_cast<const int8_t*>(m->dec[l].ckv.w4) : m->dec[l].ckv.w;
     o.layer[l].scale = m->dec[l].ckv.scale;
     o.layer[l].bias = m->dec[l].ckv.bias;
     o.layer[l].out = S->cross_kv[l];
@@ -537,7 +547,7 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
     if ((rc = qlin(L.w2, S->dec_h, R, MNMT_EPI_F32_RESID, xc, L.ff_gamma, s))) return rc;
   }
   // output projection over the shared embedding with the arg-max, then commit
-  LinearDev out_proj{m->E, m->c_out, nullptr, m->info.vocab, d, 0.f};
+  LinearDev out_proj{m->E, nullptr, m->c_out, nullptr, m->info.vocab, d, 0.f};
   FusedGemv gv = gemv(out_proj, EPI_LOGITS_ARGMAX, logits_out);
   gv.slots = S->fslots;
   gv.nslots = fused_slots_per_row(m->info.vocab);
@@ -631,10 +641,9 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     at.S = S->S;
     at.t = t;
     const LinearDev& P = self ? L.qkv : L.cq;
-    at.W = P.w;
+    at.w4 = pick_weights(P, self ? L.o : L.co, at.W, at.Wo);
     at.scale = P.scale;
     at.bias = P.bias;
-    at.Wo = self ? L.o.w : L.co.w;
     at.len = S->len;
     at.c_qk = self ? L.sa_cqk : L.ca_cqk;
     at.c_pv = self ? L.sa_cpv : L.ca_cpv;
@@ -706,10 +715,9 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       f.R = R;
       f.d = d;
       f.F = L.w1.N;
-      f.W1 = L.w1.w;
+      f.w4 = pick_weights(L.w1, L.w2, f.W1, f.W2);
       f.scale1 = L.w1.scale;
       f.bias1 = L.w1.bias;
-      f.W2 = L.w2.w;
       f.acc_out = acc_w2;
       const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 2, f.F / 64, t + 1) : s;
       LAUNCH(launch_step_ffn(in, f, ks));

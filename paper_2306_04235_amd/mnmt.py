@@ -17,7 +17,9 @@ OK, E_INVALID_ARG, E_BAD_MODEL, E_CAPACITY, E_HIP, E_UNSUPPORTED, E_TIMEOUT = 0,
 (EPI_I32, EPI_I8, EPI_I8_RELU, EPI_F32, EPI_F32_RESID, EPI_LOGITS, EPI_ARGMAX, EPI_ARGMAX_PARTIAL,
  EPI_ARGMAX_PARTIAL_PACKED) = range(9)
 
-EXPORTS = ("mnmt_model_bytes", "mnmt_model_load", "mnmt_model_get_info", "mnmt_model_free", "mnmt_session_bytes",
+LOAD_PACKED_4BIT_ONLY = 1
+
+EXPORTS = ("mnmt_model_bytes", "mnmt_model_load", "mnmt_model_bytes_ex", "mnmt_model_load_ex", "mnmt_model_get_info", "mnmt_model_free", "mnmt_session_bytes",
            "mnmt_session_create", "mnmt_session_free", "mnmt_encode", "mnmt_decode_step", "mnmt_translate",
            "mnmt_session_status", "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed",
            "mnmt_argmax_partials", "mnmt_packed_bytes", "mnmt_pack_weights", "mnmt_logits_argmax_noalloc",
@@ -60,6 +62,8 @@ def lib():
         vp, sz, i32, f32 = C.c_void_p, C.c_size_t, C.c_int, C.c_float
         L.mnmt_model_bytes.argtypes = [C.c_char_p, sz, C.POINTER(sz)]
         L.mnmt_model_load.argtypes = [C.c_char_p, sz, vp, sz, vp, C.POINTER(vp)]
+        L.mnmt_model_bytes_ex.argtypes = [C.c_char_p, sz, C.c_uint, C.POINTER(sz)]
+        L.mnmt_model_load_ex.argtypes = [C.c_char_p, sz, C.c_uint, vp, sz, vp, C.POINTER(vp)]
         L.mnmt_model_get_info.argtypes = [vp, C.POINTER(ModelInfo)]
         L.mnmt_model_free.argtypes = [vp]
         L.mnmt_model_free.restype = None
@@ -107,9 +111,9 @@ def _stream(stream=None):
 
 
 # ---- host-only entry points ---------------------------------------------------
-def mnmt_model_bytes(blob: bytes) -> int:
+def mnmt_model_bytes(blob: bytes, flags: int = 0) -> int:
     n = C.c_size_t()
-    _check(lib().mnmt_model_bytes(blob, len(blob), C.byref(n)), "mnmt_model_bytes")
+    _check(lib().mnmt_model_bytes_ex(blob, len(blob), flags, C.byref(n)), "mnmt_model_bytes_ex")
     return n.value
 
 
@@ -232,13 +236,13 @@ def mnmt_debug_read(x, sink, reps=1, stream=None):
 class Model:
     """A model loaded into a torch-allocated device arena."""
 
-    def __init__(self, blob: bytes, device="cuda", stream=None):
+    def __init__(self, blob: bytes, device="cuda", stream=None, flags: int = 0):
         import torch
 
-        self.arena = torch.empty(mnmt_model_bytes(blob), dtype=torch.uint8, device=device)
+        self.arena = torch.empty(mnmt_model_bytes(blob, flags), dtype=torch.uint8, device=device)
         h = C.c_void_p()
-        _check(lib().mnmt_model_load(blob, len(blob), _ptr(self.arena), self.arena.numel(), _stream(stream),
-                                     C.byref(h)), "mnmt_model_load")
+        _check(lib().mnmt_model_load_ex(blob, len(blob), flags, _ptr(self.arena), self.arena.numel(),
+                                        _stream(stream), C.byref(h)), "mnmt_model_load_ex")
         self.handle = h
         info = ModelInfo()
         _check(lib().mnmt_model_get_info(h, C.byref(info)), "mnmt_model_get_info")

@@ -45,9 +45,12 @@ def test_model_bytes_accepts_the_generated_models():
         assert weights < n < 2 * len(blob)
 
 
-def test_model_bytes_of_4bit_weights_equals_their_int8_form():
-    """4-bit weights (packed in the file) are expanded to their int8 codes on
-    the device: the arena size equals that of the same codes stored as int8."""
+def test_model_bytes_of_4bit_weights():
+    """4-bit weights (the paper's W-E-A 4-8-8 setting): by default the arena
+    holds their packed rows (read by the batch-1 decoder and small-batch
+    encoder kernels) and their int8 codes (read by the batched kernels); with
+    MNMT_LOAD_PACKED_4BIT_ONLY only the packed rows, half the bytes of the
+    int8 model's linear weights.  An int8 model cannot be loaded that way."""
     import dataclasses
 
     from synth import generate as G
@@ -56,7 +59,17 @@ def test_model_bytes_of_4bit_weights_equals_their_int8_form():
     hdr, t = read_model(blob4)
     blob8 = write_model(hdr, {k: np.ascontiguousarray(v) for k, v in t.items()})
     assert len(blob4) < len(blob8)
-    assert mnmt.mnmt_model_bytes(blob4) == mnmt.mnmt_model_bytes(blob8)
+    lin = sum(v.size for k, v in t.items() if k.endswith(".w") and k != "emb.w")
+    assert all((v.size // 2) % 256 == 0 for k, v in t.items() if k.endswith(".w") and k != "emb.w")
+    b8 = mnmt.mnmt_model_bytes(blob8)
+    assert mnmt.mnmt_model_bytes(blob4) == b8 + lin // 2
+    assert mnmt.mnmt_model_bytes(blob4, mnmt.LOAD_PACKED_4BIT_ONLY) == b8 - lin // 2
+    with pytest.raises(mnmt.MnmtError) as e:
+        mnmt.mnmt_model_bytes(blob8, mnmt.LOAD_PACKED_4BIT_ONLY)
+    assert e.value.status == mnmt.E_UNSUPPORTED
+    with pytest.raises(mnmt.MnmtError) as e:
+        mnmt.mnmt_model_bytes(blob4, 2)
+    assert e.value.status == mnmt.E_INVALID_ARG
 
 
 def test_model_bytes_rejects_bad_files():

@@ -34,14 +34,15 @@ def torch_dev():
 _models = {}
 
 
-def _pair(name_or_cfg):
-    """(oracle model, GPU model) for a named workload model or a ModelConfig."""
+def _pair(name_or_cfg, flags=0):
+    """(oracle model, GPU model) for a named workload model or a ModelConfig
+    (flags: the GPU model's load flags)."""
     from paper_2306_04235_amd import mnmt
 
-    key = name_or_cfg if isinstance(name_or_cfg, str) else name_or_cfg.name
+    key = (name_or_cfg if isinstance(name_or_cfg, str) else name_or_cfg.name, flags)
     if key not in _models:
         blob = model_blob(name_or_cfg) if isinstance(name_or_cfg, str) else G.build_model(name_or_cfg)
-        _models[key] = (oracle.Model(blob), mnmt.Model(blob))
+        _models[key] = (oracle.Model(blob), mnmt.Model(blob, flags=flags))
     return _models[key]
 
 
@@ -49,10 +50,10 @@ def _t(torch, dev, a):
     return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
 
-def _greedy_check(torch, dev, cfg, src, lens, steps, stop_at_eos=False, check_logits=True):
+def _greedy_check(torch, dev, cfg, src, lens, steps, stop_at_eos=False, check_logits=True, flags=0):
     from paper_2306_04235_amd import mnmt
 
-    om, gm = _pair(cfg)
+    om, gm = _pair(cfg, flags)
     B, S = src.shape
     print(f"greedy {cfg if isinstance(cfg, str) else cfg.name} B={B} S={S} steps={steps}", flush=True)
     sess = mnmt.Session(gm, B, S, steps, 1)
@@ -318,6 +319,35 @@ def test_4bit_weight_models(torch_dev):
     src, lens = G.make_sources(div4.vocab, 3, [9, 5, 7], seed=31, s_max=9)
     _greedy_check(torch, dev, div4, src, lens, 10)
     _beam_check(torch, dev, div4, src, lens, 2, 8, 0.6)
+
+
+def test_4bit_packed_only_models(torch_dev):
+    """MNMT_LOAD_PACKED_4BIT_ONLY: the 4-bit weights stay packed on the device
+    (half the int8 model's linear-weight bytes) and the batch-1 decoder and
+    small-batch encoder kernels widen them in registers: per-step logits and
+    tokens equal the oracle's on the mobile shape and on the varied model at
+    one and two rows; sessions beyond those paths are refused."""
+    import dataclasses
+
+    from paper_2306_04235_amd import mnmt
+
+    torch, dev = torch_dev
+    mob4 = dataclasses.replace(G.MOBILE, name="mobile-w4", w_bits=4)
+    _, gm_full = _pair(mob4)
+    _, gm = _pair(mob4, mnmt.LOAD_PACKED_4BIT_ONLY)
+    _, gm8 = _pair("MOBILE")
+    assert gm.arena.numel() < gm8.arena.numel() < gm_full.arena.numel()
+    src, lens = G.workload_inputs(G.WORKLOADS["mobile"])
+    _greedy_check(torch, dev, mob4, src, lens, 30, flags=mnmt.LOAD_PACKED_4BIT_ONLY)
+    var4 = dataclasses.replace(VARIED, name="varied-w4", w_bits=4)
+    for B in (1, 2):
+        src, lens = G.make_sources(var4.vocab, B, [30, 21][:B], seed=95 + B, s_max=30)
+        out = _greedy_check(torch, dev, var4, src, lens, 30, flags=mnmt.LOAD_PACKED_4BIT_ONLY)
+        assert len(set(out[0].tolist())) >= 3
+    for mb, ms, beam in ((1, 30, 4), (3, 8, 1), (2, 40, 1)):
+        with pytest.raises(mnmt.MnmtError) as e:
+            mnmt.Session(gm, mb, ms, 30, beam)
+        assert e.value.status == mnmt.E_UNSUPPORTED
 
 
 def test_mobile_beam_workload_all_sentences(torch_dev):
