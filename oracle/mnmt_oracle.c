@@ -17,6 +17,8 @@
  *     Q/K/V; biases, residual stream, attention scores and softmax output in
  *     full precision; a learnable weight gamma on each sublayer's residual.
  *   - 8-bit integer GEMM (Section 4.1).
+ *   - Cross-layer parameter sharing as a model-file option (Section 2.2,
+ *     Encoder/Decoder Compression).
  *   - Greedy search as used by the paper's engine (Appendix D); beam search
  *     as the paper's default evaluation decoder (ablation table).
  *
@@ -328,6 +330,7 @@ typedef struct {
 typedef struct {
   attn_t sa, ca;
   ffn_t ff;
+  int alias; /* this layer reuses another layer's parameters (owns nothing) */
 } layer_t;
 
 struct orc_model {
@@ -462,6 +465,20 @@ static int load_layer(orc_model* m, layer_t* L, const char* side, int l, int is_
   char pfx[64], nm[64];
   int d = m->d, F = m->F;
   float s3[3], s_ctx;
+  /* Cross-layer parameter sharing (Section 2.2, Encoder/Decoder Compression):
+   * an int8 tensor "<side>.<l>.share" = j (0 <= j < l) makes layer l run with
+   * every parameter of layer j of the same stack. */
+  snprintf(nm, sizeof nm, "%s.%d.share", side, l);
+  {
+    const int8_t* sh = (const int8_t*)find_tensor(m, nm, 1, 1, 1);
+    if (sh) {
+      const int j = sh[0];
+      if (j < 0 || j >= l) return ORC_E_MODEL;
+      *L = (is_dec ? m->dec : m->enc)[j];
+      L->alias = 1;
+      return ORC_OK;
+    }
+  }
   /* self-attention */
   snprintf(pfx, sizeof pfx, "%s.%d.sa.ln", side, l);
   if (load_ln(m, &L->sa.ln, pfx)) return ORC_E_MODEL;
@@ -529,12 +546,14 @@ static void free_linear(linear_t* L) {
 void orc_model_free(orc_model* m) {
   if (!m) return;
   for (int l = 0; m->enc && l < m->Le; ++l) {
+    if (m->enc[l].alias) continue;
     free_linear(&m->enc[l].sa.qkv);
     free_linear(&m->enc[l].sa.o);
     free_linear(&m->enc[l].ff.w1);
     free_linear(&m->enc[l].ff.w2);
   }
   for (int l = 0; m->dec && l < m->Ld; ++l) {
+    if (m->dec[l].alias) continue;
     free_linear(&m->dec[l].sa.qkv);
     free_linear(&m->dec[l].sa.o);
     free_linear(&m->dec[l].ca.q);

@@ -447,6 +447,7 @@ struct mnmt_model {
   const float* pe = nullptr;     // [P, d]
   bool packed_only = false;      // 4-bit weights without their int8 copies (MNMT_LOAD_PACKED_4BIT_ONLY)
   std::vector<mnmt::LayerDev> enc, dec;
+  std::vector<int> enc_alias, dec_alias;  // layer l reuses layer alias[l]'s parameters (-1: its own)
   mnmt::LnDev enc_ln, dec_ln;
   float s_enc = 0.f, inv_enc = 0.f, inv_fin = 0.f;
 };

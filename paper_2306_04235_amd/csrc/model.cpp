@@ -334,8 +334,27 @@ int build_model(const void* blob, size_t n, unsigned flags, mnmt_model& m, Image
   // The layer vectors must not reallocate after bind() recorded addresses.
   m.enc.assign(I.n_enc, LayerDev{});
   m.dec.assign(I.n_dec, LayerDev{});
-  for (int l = 0; ok && l < I.n_enc; ++l) ok = add_layer(P, *img, m, m.enc[l], "enc", l, false);
-  for (int l = 0; ok && l < I.n_dec; ++l) ok = add_layer(P, *img, m, m.dec[l], "dec", l, true);
+  m.enc_alias.assign(I.n_enc, -1);
+  m.dec_alias.assign(I.n_dec, -1);
+  // Cross-layer parameter sharing (Section 2.2): an int8 tensor
+  // "<side>.<l>.share" = j < l makes layer l run on layer j's parameters,
+  // which the arena then holds once (the copy is made after the fix-up).
+  auto shared = [&](const char* side, int l, std::vector<int>& alias) {
+    const std::string nm = std::string(side) + "." + std::to_string(l) + ".share";
+    if (P.t.find(nm) == P.t.end()) return false;
+    const int8_t* v = P.i8(nm, 1, 1);
+    if (!v || v[0] < 0 || v[0] >= l) {
+      if (P.err.empty() || v) P.err = nm + " must name an earlier layer";
+      ok = false;
+      return true;
+    }
+    alias[l] = v[0];
+    return true;
+  };
+  for (int l = 0; ok && l < I.n_enc; ++l)
+    if (!shared("enc", l, m.enc_alias)) ok = add_layer(P, *img, m, m.enc[l], "enc", l, false);
+  for (int l = 0; ok && l < I.n_dec; ++l)
+    if (!shared("dec", l, m.dec_alias)) ok = add_layer(P, *img, m, m.dec[l], "dec", l, true);
   if (ok && !I.ln_post) ok = add_ln(P, *img, m.enc_ln, "enc.ln", d) && add_ln(P, *img, m.dec_ln, "dec.ln", d);
   if (!ok) {
     err = P.err.empty() ? "model file is inconsistent" : P.err;
@@ -372,6 +391,10 @@ int finish_model(Image* img, mnmt_model& m, void* d_arena, size_t arena_bytes, h
   }
   uint8_t* base = static_cast<uint8_t*>(d_arena);
   for (auto& f : img->fix) *f.first = base + f.second;
+  for (size_t l = 0; l < m.enc.size(); ++l)  // shared layers: in increasing l, so chains resolve
+    if (m.enc_alias[l] >= 0) m.enc[l] = m.enc[m.enc_alias[l]];
+  for (size_t l = 0; l < m.dec.size(); ++l)
+    if (m.dec_alias[l] >= 0) m.dec[l] = m.dec[m.dec_alias[l]];
   hipError_t e = hipMemcpyAsync(d_arena, img->buf.data(), img->buf.size(), hipMemcpyHostToDevice, s);
   if (e == hipSuccess)
     e = launch_pack_fragments(m.E, m.info.vocab, m.info.d_model, const_cast<int8_t*>(m.E_frag), s);

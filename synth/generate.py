@@ -52,6 +52,7 @@ class ModelConfig:
     weight_std: float = WEIGHT_STD
     emb_distinct: int = 0  # > 0: embedding row v repeats drawn row v mod emb_distinct (groups of equal logits)
     w_bits: int = 8  # 4: linear weights as 4-bit codes (the paper's W-E-A 4-8-8; the embedding stays 8-bit)
+    share_every: int = 0  # > 0: layer l >= share_every reuses the parameters of layer l % share_every (per stack)
 
 
 # The model shapes of the five workloads.
@@ -128,6 +129,10 @@ def build_model(cfg: ModelConfig) -> bytes:
     for side, n_layers in (("enc", cfg.n_enc), ("dec", cfg.n_dec)):
         for l in range(n_layers):
             p = f"{side}.{l}"
+            if cfg.share_every and l >= cfg.share_every:  # cross-layer parameter sharing
+                t[p + ".share"] = np.array([l % cfg.share_every], np.int8)
+                continue
+
             ln(p + ".sa.ln")
             s_qkv = [_act_scale(rng, sig_proj) for _ in range(3)]
             linear(p + ".sa.qkv", 3 * d, d, s_in=_act_scale(rng, 1.0), s_out=s_qkv)

@@ -15,7 +15,9 @@ and computes every stage in float64 straight from the paper's definitions:
 * layer normalization at each sublayer input (pre-LN, Appendix D) or after
   each residual add (post-LN files), biased variance, the file's epsilon;
 * one shared embedding for input and output (Appendix D), input rows scaled
-  by sqrt(d) plus the stored position table, output projection tied.
+  by sqrt(d) plus the stored position table, output projection tied;
+* cross-layer parameter sharing (Section 2.2): a layer whose file entry
+  "<side>.<l>.share" names layer j runs on layer j's parameters.
 
 Quantizer (the paper's rounding to the nearest integer, symmetric reading):
 code = clamp(round(value / s), -127, 127).  The stage functions return the
@@ -43,6 +45,12 @@ class FakeQuantModel:
         self.eps = float(np.float32(h.ln_eps))
 
     # --- parameters ---------------------------------------------------------
+    def layer(self, side: str, l: int) -> str:
+        """Tensor-name prefix of layer l of a stack, following shared layers."""
+        while f"{side}.{l}.share" in self.t:
+            l = int(self.t[f"{side}.{l}.share"][0])
+        return f"{side}.{l}"
+
     def scalar(self, name: str) -> float:
         return float(self.t[name][0])
 
@@ -148,7 +156,7 @@ class FakeQuantModel:
         return (np.asarray(x, F64) if self.post else self.layer_norm(x, "dec.ln")) / s
 
     def cross_kv(self, enc_codes, layer: int) -> np.ndarray:
-        pfx = f"dec.{layer}.ca.kv"
+        pfx = self.layer("dec", layer) + ".ca.kv"
         y = self.linear(enc_codes, self.scalar("enc.sout"), pfx)
         s = self.vec(pfx + ".sout")
         return np.concatenate([y[:, :self.d] / s[0], y[:, self.d:] / s[1]], axis=1)
@@ -166,7 +174,7 @@ class FakeQuantModel:
         S = len(src)
         x = self.embed(src, np.arange(S))
         for l in range(self.n_enc):
-            p = f"enc.{l}"
+            p = self.layer("enc", l)
             a = x if self.post else self.layer_norm(x, p + ".sa.ln")
             y = (a @ self.weight(p + ".sa.qkv").T) + self.vec(p + ".sa.qkv.b")
             ctx = self.attention(y[:, :d], y[:, d:2 * d], y[:, 2 * d:], 1.0, 1.0, 1.0, 1.0)
@@ -182,7 +190,7 @@ class FakeQuantModel:
         inp = np.concatenate([[bos], np.asarray(tokens[:-1])]).astype(np.int64)
         x = self.embed(inp, np.arange(n))
         for l in range(self.n_dec):
-            p = f"dec.{l}"
+            p = self.layer("dec", l)
             a = x if self.post else self.layer_norm(x, p + ".sa.ln")
             y = (a @ self.weight(p + ".sa.qkv").T) + self.vec(p + ".sa.qkv.b")
             ctx = np.zeros((n, d))

@@ -123,3 +123,21 @@ def test_model_arena_holds_the_packed_embedding():
     V, d = np.asarray(t["emb.w"]).shape
     weights = sum(np.asarray(a).size for k, a in t.items() if k.endswith(".w"))
     assert mnmt.mnmt_model_bytes(blob) >= weights + mnmt.lib().mnmt_packed_bytes(V, d)
+
+
+def test_shared_layers_are_stored_once():
+    """Cross-layer parameter sharing: the arena holds a shared layer's
+    parameters once; the loader rejects a layer that names itself or a later
+    layer."""
+    from tests.test_oracle_model import SHARED, _unshare
+
+    blob = G.build_model(SHARED)
+    full = _unshare(blob)
+    per_layer_enc = 4 * 64 * 64 + 2 * 64 * 128
+    assert mnmt.mnmt_model_bytes(full) - mnmt.mnmt_model_bytes(blob) >= (3 + 2) * per_layer_enc
+    hdr, t = read_model(blob)
+    t2 = {k: np.ascontiguousarray(v) for k, v in t.items()}
+    t2["dec.1.share"] = np.array([1], np.int8)
+    with pytest.raises(mnmt.MnmtError) as e:
+        mnmt.mnmt_model_bytes(write_model(hdr, t2))
+    assert e.value.status == mnmt.E_BAD_MODEL

@@ -350,6 +350,27 @@ def test_4bit_packed_only_models(torch_dev):
         assert e.value.status == mnmt.E_UNSUPPORTED
 
 
+SHARED = G.ModelConfig("shared-preln", 64, 4, 128, 4, 3, 500, ln_post=0, seed=82, random_gamma=True,
+                       weight_std=0.1, share_every=1)
+SHARED_256 = G.ModelConfig("shared-256", 256, 4, 1024, 6, 2, 32000, ln_post=0, seed=1103, random_gamma=True,
+                           weight_std=0.2, share_every=2)
+
+
+def test_cross_layer_sharing_models(torch_dev):
+    """Cross-layer parameter sharing (Section 2.2): layers that reuse another
+    layer's parameters (aliased device pointers, stored once) on every path --
+    the batch-1 chained step and encoder, the 3-8 row and matrix-core paths,
+    beam search -- against the oracle."""
+    torch, dev = torch_dev
+    for B in (1, 2, 5, 12):
+        src, lens = G.make_sources(SHARED.vocab, B, (3, 12), seed=60 + B, s_max=12)
+        _greedy_check(torch, dev, SHARED, src, lens, 9)
+    src, lens = G.make_sources(SHARED.vocab, 4, [5, 1, 9, 9], seed=31, s_max=9)
+    _beam_check(torch, dev, SHARED, src, lens, 4, 8, 0.6)
+    src, lens = G.make_sources(SHARED_256.vocab, 1, [30], seed=64, s_max=30)
+    _greedy_check(torch, dev, SHARED_256, src, lens, 30)
+
+
 def test_mobile_beam_workload_all_sentences(torch_dev):
     """The batched beam workload on the mobile model: all 64 sentences (10-60
     source tokens, beam 4, 64 steps) against the oracle, run one sentence per

@@ -40,6 +40,8 @@ SMALL_POST = G.ModelConfig("small-postln", 64, 2, 128, 2, 2, 300, ln_post=1, see
 VARIED = G.ModelConfig("varied-256", 256, 4, 1024, 2, 2, 32000, ln_post=0, seed=1102, random_gamma=True,
                        weight_std=0.2)
 SMALL_W4 = dataclasses.replace(SMALL_PRE, name="small-preln-w4", w_bits=4, seed=80)
+SHARED = G.ModelConfig("shared-preln", 64, 4, 128, 4, 3, 500, ln_post=0, seed=82, random_gamma=True,
+                       weight_std=0.1, share_every=1)
 
 MODELS = {
     "tiny": lambda: model_blob("TINY"),
@@ -47,6 +49,7 @@ MODELS = {
     "small_post_gamma": lambda: G.build_model(SMALL_POST),
     "small_pre_w4": lambda: G.build_model(SMALL_W4),
     "varied_256": lambda: G.build_model(VARIED),
+    "shared_layers": lambda: G.build_model(SHARED),
     "mobile": lambda: model_blob("MOBILE"),
 }
 
@@ -87,7 +90,7 @@ def encoder_stages(ref: FakeQuantModel, om, src, st: Stats):
     d, F = ref.d, ref.F
     check_f32(tr["x"][0], ref.embed(src, np.arange(S)), "embedding + positions", rtol=1e-6)
     for l in range(ref.n_enc):
-        p, u = f"enc.{l}", 2 * l
+        p, u = ref.layer("enc", l), 2 * l
         x = tr["x"][u].astype(np.float64)
         a_val, qkv_val, ctx_val, x_next = ref.self_attention_sublayer(
             p, x, tr["a"][u], tr["pj"][u][:, : 3 * d], tr["ctx"][u], lambda i: np.arange(S))
@@ -115,7 +118,7 @@ def decoder_stages(ref: FakeQuantModel, om, src, tokens, st: Stats):
     inp = np.concatenate([[ref.hdr.bos_id], tokens[:-1]])
     check_f32(tr["x"][0], ref.embed(inp, np.arange(n)), "decoder embedding + positions", rtol=1e-6)
     for l in range(ref.n_dec):
-        p, u = f"dec.{l}", 3 * l
+        p, u = ref.layer("dec", l), 3 * l
         x = tr["x"][u].astype(np.float64)
         a_val, qkv_val, ctx_val, x_next = ref.self_attention_sublayer(
             p, x, tr["a"][u], tr["pj"][u][:, : 3 * d], tr["ctx"][u], lambda i: np.arange(i + 1))
