@@ -54,6 +54,16 @@
  *     sout [2]} (input scale = enc.sout), .ca.o.{w,sw,b,sin}, .ca.gamma,
  *     <e|t>.ff.ln.{g,b}, .ff.w1.{w [F,d],sw,b,sin,sout [1]},
  *     .ff.w2.{w [d,F],sw,b} (input scale = ff.w1.sout), .ff.gamma.
+ *   Optional, cross-layer parameter sharing (Section 2.2): an int8 tensor
+ *   <e|t>.share [1] = j < l replaces all of layer l's tensors: layer l runs
+ *   on layer j's parameters (stored once).
+ *   Optional, embedding factorization (Section 2.1, "Scaling E"): emb.w is
+ *   [V, E] (E a multiple of 64, E <= d) with emb.proj.w i8 [d, E], emb.proj.sw
+ *   f32 [1] (one scale: the matrix is used in both orientations) and
+ *   emb.proj.sout f32 [1] (scale s_u of the output projection's int8 input):
+ *   input rows x = (float)(E[tok] . P[n]) * sw * c_emb[tok] + PE; output
+ *   u = requant(a P, s_fin * sw / s_u), logits z[v] = (u . E[v]) * s_u * s_E[v].
+ *   Such models run on the general (unfused) decode paths.
  *   Weights are symmetric per-output-channel int8: w_real = sw[n] * w[n,k].
  *   4-bit weights (the paper's W-E-A 4-8-8 setting) hold codes in [-7, 7]:
  *   in each group of 16 codes of a row, byte i (i < 8) holds code i in its
@@ -119,6 +129,7 @@ typedef struct {
   int32_t d_model, n_heads, d_ffn, n_enc, n_dec, vocab, max_pos, ln_post;
   int32_t pad_id, bos_id, eos_id, unk_id;
   float ln_eps;
+  int32_t emb_dim; /* factorized embedding width (0: the embedding has width d_model) */
 } mnmt_model_info;
 
 /* Capacity of a session: batch, source and target lengths, beam width. */

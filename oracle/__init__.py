@@ -58,7 +58,7 @@ def lib():
         L.orc_decoder_logits_full.argtypes = [vp, vp, i32, vp, i32, vp]
         L.orc_translate_beam.argtypes = [vp, vp, vp, i32, i32, i32, i32, f32, vp, vp, vp]
         L.orc_encode_trace.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp]
-        L.orc_decoder_trace.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp]
+        L.orc_decoder_trace.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -198,7 +198,7 @@ class Model:
         dims = np.zeros(16, np.int32)
         lib().orc_model_dims(self._h, _p(dims))
         (self.d, self.h, self.F, self.n_enc, self.n_dec, self.V, self.max_pos, self.ln_post, self.pad_id,
-         self.bos_id, self.eos_id, self.unk_id) = [int(v) for v in dims[:12]]
+         self.bos_id, self.eos_id, self.unk_id, self.emb_dim) = [int(v) for v in dims[:13]]
 
     def __del__(self):
         if getattr(self, "_h", None) and _lib is not None:
@@ -266,16 +266,17 @@ class Model:
     def decoder_trace(self, src_row, tokens):
         """Teacher-forced decoding (inputs BOS, tokens[:-1]) with each step's
         intermediate values: x [U+1, n, d], a, pj, ctx as in encode_trace
-        (U = 3 n_dec), fin [n, d] (int8 input of the output projection) and
-        z [n, V] logits."""
+        (U = 3 n_dec), fin [n, d] (int8 final rows), fin_u [n, emb_dim] (a
+        factorized embedding's projection of them) and z [n, V] logits."""
         src_row, tokens = _c(src_row, np.int32), _c(tokens, np.int32)
         n, d, U = tokens.size, self.d, 3 * self.n_dec
         P = max(3 * d, self.F)
         t = dict(x=np.zeros((U + 1, n, d), np.float32), a=np.zeros((U, n, d), np.int8),
                  pj=np.zeros((U, n, P), np.int8), ctx=np.zeros((U, n, d), np.int8), fin=np.zeros((n, d), np.int8),
-                 z=np.zeros((n, self.V), np.float32))
+                 fin_u=np.zeros((n, max(self.emb_dim, 1)), np.int8), z=np.zeros((n, self.V), np.float32))
         _check(lib().orc_decoder_trace(self._h, _p(src_row), src_row.size, _p(tokens), n, _p(t["x"]), _p(t["a"]),
-                                       _p(t["pj"]), _p(t["ctx"]), _p(t["fin"]), _p(t["z"])), "decoder_trace")
+                                       _p(t["pj"]), _p(t["ctx"]), _p(t["fin"]), _p(t["fin_u"]), _p(t["z"])),
+               "decoder_trace")
         return t
 
     def beam(self, src, lens, beam, max_steps, alpha=0.6):

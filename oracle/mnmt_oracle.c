@@ -17,8 +17,9 @@
  *     Q/K/V; biases, residual stream, attention scores and softmax output in
  *     full precision; a learnable weight gamma on each sublayer's residual.
  *   - 8-bit integer GEMM (Section 4.1).
- *   - Cross-layer parameter sharing as a model-file option (Section 2.2,
- *     Encoder/Decoder Compression).
+ *   - Cross-layer parameter sharing (Section 2.2, Encoder/Decoder
+ *     Compression) and embedding factorization (Section 2.1, Embedding
+ *     Compression) as model-file options.
  *   - Greedy search as used by the paper's engine (Appendix D); beam search
  *     as the paper's default evaluation decoder (ablation table).
  *
@@ -349,12 +350,34 @@ struct orc_model {
   layer_t* dec;
   ln_t enc_ln, dec_ln;
   float s_enc, s_fin, inv_enc, inv_fin;
+  /* factorized embedding (Section 2.1): E is [V, Ef], P [d, Ef] maps it to the
+   * model width; Ef = 0 when the embedding has the model width */
+  int Ef;
+  const int8_t* Pw;
+  linear_t proj_out; /* Pw transposed [Ef, d]: the final rows back to Ef codes */
+  float s_P;
+  float s_emb_out; /* scale of the output projection's int8 input: s_fin, or s_u when factorized */
 };
 
 static uint32_t rd_u32(const unsigned char* p) {
   uint32_t v;
   memcpy(&v, p, 4);
   return v;
+}
+
+/* The dimensions of a tensor of any type (0 if absent). */
+static void tensor_dims(const orc_model* m, const char* name, uint32_t* d0, uint32_t* d1) {
+  *d0 = *d1 = 0;
+  for (int i = 0; i < m->n_tensors; ++i) {
+    const unsigned char* e = m->blob + 64 + (size_t)i * 64;
+    char nm[41];
+    memcpy(nm, e, 40);
+    nm[40] = 0;
+    if (strcmp(nm, name) != 0) continue;
+    memcpy(d0, e + 48, 4);
+    memcpy(d1, e + 52, 4);
+    return;
+  }
 }
 
 /* Look up a tensor by name; check dtype (1 int8, 2 fp32, 3 packed 4-bit)
@@ -562,6 +585,9 @@ void orc_model_free(orc_model* m) {
     free_linear(&m->dec[l].ff.w1);
     free_linear(&m->dec[l].ff.w2);
   }
+  free(m->proj_out.scale);
+  free(m->proj_out.bias);
+  free(m->proj_out.w_own);
   free(m->enc);
   free(m->dec);
   free(m->c_emb);
@@ -606,11 +632,44 @@ int orc_model_load(const void* blob, size_t nbytes, orc_model** out) {
       m->eos_id >= m->V || m->unk_id < 0 || m->unk_id >= m->V)
     goto fail;
   m->dh = m->d / m->h;
-  m->E = (const int8_t*)find_tensor(m, "emb.w", 1, (uint32_t)m->V, (uint32_t)m->d);
+  if (scalar(m, "enc.sout", &m->s_enc) || scalar(m, "dec.sout", &m->s_fin)) goto fail;
+  m->s_emb_out = m->s_fin;
+  {
+    /* factorized embedding: emb.proj.w [d, Ef] with a per-tensor scale (the
+     * matrix serves in both orientations) and the output side's scale s_u */
+    uint32_t p0, p1;
+    tensor_dims(m, "emb.proj.w", &p0, &p1);
+    if (p0 || p1) {
+      float s_u;
+      m->Pw = (const int8_t*)find_tensor(m, "emb.proj.w", 1, (uint32_t)m->d, p1);
+      if (!m->Pw || p1 < 4 || p1 % 4 || p1 > (uint32_t)m->d) goto fail;
+      if (scalar(m, "emb.proj.sw", &m->s_P) || scalar(m, "emb.proj.sout", &s_u)) goto fail;
+      m->Ef = (int)p1;
+      linear_t* L = &m->proj_out;
+      L->N = m->Ef;
+      L->K = m->d;
+      L->w_own = (int8_t*)malloc((size_t)m->d * m->Ef);
+      L->scale = (float*)malloc(sizeof(float) * (size_t)m->Ef);
+      L->bias = (float*)malloc(sizeof(float) * (size_t)m->Ef);
+      if (!L->w_own || !L->scale || !L->bias) {
+        rc = ORC_E_NOMEM;
+        goto fail;
+      }
+      for (int n = 0; n < m->d; ++n)
+        for (int k = 0; k < m->Ef; ++k) L->w_own[(size_t)k * m->d + n] = m->Pw[(size_t)n * m->Ef + k];
+      L->w = L->w_own;
+      /* u = requant(a . P) with a = s_fin codes, P = s_P codes, u = s_u codes */
+      for (int k = 0; k < m->Ef; ++k) {
+        L->scale[k] = (float)((double)m->s_fin * (double)m->s_P / (double)s_u);
+        L->bias[k] = 0.0f;
+      }
+      m->s_emb_out = s_u;
+    }
+  }
+  m->E = (const int8_t*)find_tensor(m, "emb.w", 1, (uint32_t)m->V, (uint32_t)(m->Ef ? m->Ef : m->d));
   m->s_E = (const float*)find_tensor(m, "emb.s", 2, (uint32_t)m->V, 1);
   m->pe = (const float*)find_tensor(m, "pe", 2, (uint32_t)m->P, (uint32_t)m->d);
   if (!m->E || !m->s_E || !m->pe) goto fail;
-  if (scalar(m, "enc.sout", &m->s_enc) || scalar(m, "dec.sout", &m->s_fin)) goto fail;
   m->inv_enc = (float)(1.0 / (double)m->s_enc);
   m->inv_fin = (float)(1.0 / (double)m->s_fin);
   if (!m->post) {
@@ -625,11 +684,12 @@ int orc_model_load(const void* blob, size_t nbytes, orc_model** out) {
     goto fail;
   }
   /* Shared embedding (Appendix D): input rows scaled by sqrt(d) (reading),
-   * output projection dequantized by the final activation scale. */
+   * output projection dequantized by the scale of its int8 input (the final
+   * activation scale, or s_u after a factorized embedding's projection). */
   for (int v = 0; v < m->V; ++v) {
     if (!(m->s_E[v] > 0.0f) || !isfinite(m->s_E[v])) goto fail;
     m->c_emb[v] = (float)((double)m->s_E[v] * sqrt((double)m->d));
-    m->c_out[v] = (float)((double)m->s_fin * (double)m->s_E[v]);
+    m->c_out[v] = (float)((double)m->s_emb_out * (double)m->s_E[v]);
   }
   for (int l = 0; l < m->Le; ++l)
     if (load_layer(m, &m->enc[l], "enc", l, 0)) goto fail;
@@ -645,7 +705,7 @@ fail:
 int orc_model_dims(const orc_model* m, int32_t* dims) {
   if (!m || !dims) return ORC_E_ARG;
   int32_t v[16] = {m->d, m->h, m->F, m->Le, m->Ld, m->V, m->P, m->post,
-                   m->pad_id, m->bos_id, m->eos_id, m->unk_id, 0, 0, 0, 0};
+                   m->pad_id, m->bos_id, m->eos_id, m->unk_id, m->Ef, 0, 0, 0};
   memcpy(dims, v, sizeof v);
   return ORC_OK;
 }
@@ -750,9 +810,35 @@ static void tr_i8(const trace_t* tr, int8_t* base, int u, int width, const int8_
 /* Token embedding (shared matrix, scaled by sqrt(d)) plus the sinusoidal
  * position table stored in the model file: x = fma(E[tok], c_emb[tok], PE[pos]). */
 static void embed(const orc_model* m, int tok, int pos, float* x) {
-  const int8_t* e = m->E + (size_t)tok * m->d;
   const float* pe = m->pe + (size_t)pos * m->d;
+  if (m->Ef) {
+    /* factorized (Section 2.1): the token's Ef codes times the projection
+     * Pw [d, Ef], dequantized by s_P, then scaled and positioned as above */
+    const int8_t* ef = m->E + (size_t)tok * m->Ef;
+    for (int n = 0; n < m->d; ++n) {
+      int32_t acc = 0;
+      for (int k = 0; k < m->Ef; ++k) acc += (int32_t)ef[k] * (int32_t)m->Pw[(size_t)n * m->Ef + k];
+      x[n] = fmaf((float)acc * m->s_P, m->c_emb[tok], pe[n]);
+    }
+    return;
+  }
+  const int8_t* e = m->E + (size_t)tok * m->d;
   for (int j = 0; j < m->d; ++j) x[j] = fmaf((float)e[j], m->c_emb[tok], pe[j]);
+}
+
+/* Tied output projection (Appendix D) of the final int8 rows a [rows, d];
+ * a factorized embedding first maps them back to its width Ef (Section 2.1):
+ * u = requant(a . Pw, s_fin s_P / s_u), z = (u . E[v]) * s_u * s_E[v]. */
+static void output_logits(const orc_model* m, const int8_t* a, int rows, float* z, int8_t* u_out) {
+  if (!m->Ef) {
+    orc_qlinear(a, m->E, rows, m->d, m->V, m->c_out, NULL, 1.0f, ORC_EPI_LOGITS, z);
+    return;
+  }
+  int8_t* u = (int8_t*)malloc((size_t)rows * m->Ef);
+  linear_i8(&m->proj_out, a, rows, 0, u);
+  orc_qlinear(u, m->E, rows, m->Ef, m->V, m->c_out, NULL, 1.0f, ORC_EPI_LOGITS, z);
+  if (u_out) memcpy(u_out, u, (size_t)rows * m->Ef);
+  free(u);
 }
 
 static void ffn_sublayer(const orc_model* m, const ffn_t* f, float* x, int rows, const trace_t* tr, int u) {
@@ -874,7 +960,7 @@ static void cache_free(const orc_model* m, kv_cache_t* c) {
  * the cache, attends over positions 0..t (self) and over the S source
  * positions (cross), and writes the logits z[V]. */
 static void decoder_step(const orc_model* m, int tok, int t, kv_cache_t* c, int8_t* const* cross_kv, int S,
-                         float* z, const trace_t* tr, int8_t* fin) {
+                         float* z, const trace_t* tr, int8_t* fin, int8_t* fin_u) {
   int d = m->d, dh = m->dh;
   float* x = (float*)malloc(sizeof(float) * (size_t)d);
   int8_t* a = (int8_t*)malloc((size_t)d);
@@ -922,7 +1008,7 @@ static void decoder_step(const orc_model* m, int tok, int t, kv_cache_t* c, int8
     for (int j = 0; j < d; ++j) a[j] = orc_quantize(x[j], m->inv_fin);
   if (fin) memcpy(fin, a, (size_t)d);
   /* tied output projection over the shared embedding */
-  orc_qlinear(a, m->E, 1, d, m->V, m->c_out, NULL, 1.0f, ORC_EPI_LOGITS, z);
+  output_logits(m, a, 1, z, fin_u);
   free(x);
   free(a);
   free(qkv);
@@ -965,7 +1051,7 @@ int orc_translate_greedy(const orc_model* m, const int32_t* src, const int32_t* 
         out[(size_t)b * steps + t] = m->pad_id;
         continue;
       }
-      decoder_step(m, tok, t, &c, cross, len[b], z, NULL, NULL);
+      decoder_step(m, tok, t, &c, cross, len[b], z, NULL, NULL, NULL);
       if (logits) memcpy(logits + ((size_t)b * steps + t) * m->V, z, sizeof(float) * (size_t)m->V);
       int best = 0;
       for (int v = 1; v < m->V; ++v)
@@ -997,7 +1083,7 @@ int orc_decoder_logits(const orc_model* m, const int32_t* src, int S, const int3
   kv_cache_t c;
   cache_alloc(m, &c, n);
   for (int t = 0; t < n; ++t)
-    decoder_step(m, t == 0 ? m->bos_id : tok[t - 1], t, &c, cross, S, z + (size_t)t * m->V, NULL, NULL);
+    decoder_step(m, t == 0 ? m->bos_id : tok[t - 1], t, &c, cross, S, z + (size_t)t * m->V, NULL, NULL, NULL);
   cache_free(m, &c);
   free_cross(m, cross);
   return ORC_OK;
@@ -1017,10 +1103,11 @@ int orc_encode_trace(const orc_model* m, const int32_t* src, int S, float* x, in
 
 /* Teacher-forced decoding (as orc_decoder_logits) with each step's
  * intermediate values copied out: trace_t with U = 3 n_dec sublayers and one
- * row per step; fin [n, d] receives each step's int8 input of the output
- * projection, z [n, V] the logits. */
+ * row per step; fin [n, d] receives each step's int8 final rows, fin_u [n, Ef]
+ * (factorized embeddings) their projection back to the embedding width, z
+ * [n, V] the logits. */
 int orc_decoder_trace(const orc_model* m, const int32_t* src, int S, const int32_t* tok, int n, float* x, int8_t* a,
-                      int8_t* pj, int8_t* ctx, int8_t* fin, float* z) {
+                      int8_t* pj, int8_t* ctx, int8_t* fin, int8_t* fin_u, float* z) {
   if (!m || !src || !tok || !z || S < 1 || S > m->P || n < 1 || n > m->P) return ORC_E_ARG;
   for (int t = 0; t < S; ++t)
     if (src[t] < 0 || src[t] >= m->V) return ORC_E_ARG;
@@ -1032,7 +1119,7 @@ int orc_decoder_trace(const orc_model* m, const int32_t* src, int S, const int32
   for (int t = 0; t < n; ++t) {
     trace_t tr = {x, a, pj, ctx, n, t, 3 * m->d > m->F ? 3 * m->d : m->F};
     decoder_step(m, t == 0 ? m->bos_id : tok[t - 1], t, &c, cross, S, z + (size_t)t * m->V, &tr,
-                 fin ? fin + (size_t)t * m->d : NULL);
+                 fin ? fin + (size_t)t * m->d : NULL, fin_u && m->Ef ? fin_u + (size_t)t * m->Ef : NULL);
   }
   cache_free(m, &c);
   free_cross(m, cross);
@@ -1078,7 +1165,7 @@ int orc_decoder_logits_full(const orc_model* m, const int32_t* src, int S, const
     orc_layernorm_quant(x, n, d, m->dec_ln.g, m->dec_ln.b, m->eps, m->inv_fin, a, NULL);
   else
     for (size_t i = 0; i < (size_t)n * d; ++i) a[i] = orc_quantize(x[i], m->inv_fin);
-  orc_qlinear(a, m->E, n, d, m->V, m->c_out, NULL, 1.0f, ORC_EPI_LOGITS, z);
+  output_logits(m, a, n, z, NULL);
   free(x);
   free(a);
   free(qkv);
@@ -1142,7 +1229,7 @@ static void translate_one_beam(const orc_model* m, const int32_t* src, int S, in
     for (int j = 0; j < W; ++j) {
       if (!alive[j]) continue;
       int tok = t == 0 ? m->bos_id : toks[(size_t)j * T + t - 1];
-      decoder_step(m, tok, t, &cache[j], cross, S, z, NULL, NULL);
+      decoder_step(m, tok, t, &cache[j], cross, S, z, NULL, NULL, NULL);
       float lse;
       orc_log_softmax_stats(z, V, NULL, &lse);
       for (int v = 0; v < V; ++v) {

@@ -93,10 +93,11 @@ int orc_decoder_logits_full(const orc_model* m, const int32_t* src, int S, const
  * Encoder of one sentence: rows = S, enc [S, d] output codes. */
 int orc_encode_trace(const orc_model* m, const int32_t* src, int S, float* x, int8_t* a, int8_t* pj, int8_t* ctx,
                      int8_t* enc);
-/* Teacher-forced decoding with rows = n steps; fin [n, d] the int8 input of
- * the output projection at each step (or NULL); z [n, V] logits. */
+/* Teacher-forced decoding with rows = n steps; fin [n, d] the int8 final rows
+ * at each step (or NULL), fin_u [n, Ef] their projection back to the width Ef
+ * of a factorized embedding (or NULL); z [n, V] logits. */
 int orc_decoder_trace(const orc_model* m, const int32_t* src, int S, const int32_t* tok, int n, float* x, int8_t* a,
-                      int8_t* pj, int8_t* ctx, int8_t* fin, float* z);
+                      int8_t* pj, int8_t* ctx, int8_t* fin, int8_t* fin_u, float* z);
 /* Beam search: out [B, max_steps] (PAD-filled), out_len [B], score [B]. */
 int orc_translate_beam(const orc_model* m, const int32_t* src, const int32_t* len, int B, int S_max,
                        int beam, int max_steps, float alpha, int32_t* out, int32_t* out_len,

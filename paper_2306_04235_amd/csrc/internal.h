@@ -52,6 +52,13 @@ hipError_t launch_ln_quant(const float* x, int rows, int d, int do_ln, const flo
 // (tok = tok[r], p = *step).
 hipError_t launch_embed(const int32_t* tok, int rows, int S_for_pos, const int* step, const int8_t* E,
                         const float* c_emb, const float* pe, int d, int V, float* x, hipStream_t s);
+// The same rows for a factorized embedding (Section 2.1): E [V, Ef] int8
+// rows projected to d by P [d, Ef] (per-tensor scale s_proj):
+// x = fma((float)(E[tok] . P[n]) * s_proj, c_emb[tok], PE[pos][n]).
+constexpr int kMaxEmbDim = 1024;
+hipError_t launch_embed_proj(const int32_t* tok, int rows, int S_for_pos, const int* step, const int8_t* E, int Ef,
+                             const int8_t* P, float s_proj, const float* c_emb, const float* pe, int d, int V,
+                             float* x, hipStream_t s);
 
 // Encoder self-attention over qkv [B*S, 3d] -> ctx [B*S, d].
 hipError_t launch_attn_enc(const int8_t* qkv, const int32_t* len, int B, int S, int d, int h, float c_qk,
@@ -446,6 +453,12 @@ struct mnmt_model {
   const float* c_out = nullptr;  // [V]
   const float* pe = nullptr;     // [P, d]
   bool packed_only = false;      // 4-bit weights without their int8 copies (MNMT_LOAD_PACKED_4BIT_ONLY)
+  // factorized embedding (info.emb_dim > 0): E is [V, emb_dim], proj [d,
+  // emb_dim] maps it to the model width, proj_out (its transpose, requantized
+  // with s_fin * s_proj / s_u) maps the final rows back to emb_dim
+  const int8_t* proj = nullptr;
+  float s_proj = 0.f;
+  mnmt::LinearDev proj_out;
   std::vector<mnmt::LayerDev> enc, dec;
   std::vector<int> enc_alias, dec_alias;  // layer l reuses layer alias[l]'s parameters (-1: its own)
   mnmt::LnDev enc_ln, dec_ln;
@@ -480,6 +493,7 @@ struct mnmt_session {
   int8_t* dec_qkv = nullptr;
   int8_t* dec_q = nullptr;
   int8_t* dec_h = nullptr;
+  int8_t* dec_u = nullptr;  // factorized embedding: the output projection's int8 input [R, emb_dim]
   std::vector<int8_t*> kcache, vcache;
   int32_t* cur_tok = nullptr;
   int* step = nullptr;

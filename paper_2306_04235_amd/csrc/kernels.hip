@@ -26,6 +26,30 @@ __global__ __launch_bounds__(256) void k_embed(const int32_t* __restrict__ tok, 
     x[(size_t)r * d + i] = fmaf((float)E[(size_t)t * d + i], c, pe[(size_t)pos * d + i]);
 }
 
+// Factorized embedding rows (one block per row): the token's Ef codes in LDS,
+// thread n computes the exact int32 dot product with row n of P (4 codes per
+// sdot4), then x = fma((float)acc * s_proj, c_emb[tok], PE[pos][n]).
+__global__ __launch_bounds__(256) void k_embed_proj(const int32_t* __restrict__ tok, int S, const int* step,
+                                                    const int8_t* __restrict__ E, int Ef, const int8_t* __restrict__ P,
+                                                    float s_proj, const float* __restrict__ c_emb,
+                                                    const float* __restrict__ pe, int d, int V, float* __restrict__ x) {
+  __shared__ __attribute__((aligned(16))) int8_t e[kMaxEmbDim];
+  const int r = blockIdx.x;
+  int t = tok[r];
+  t = t < 0 ? 0 : (t >= V ? V - 1 : t);
+  const int pos = step ? *step : r % S;
+  for (int k = threadIdx.x; k < Ef; k += blockDim.x) e[k] = E[(size_t)t * Ef + k];
+  __syncthreads();
+  const float c = c_emb[t];
+  const int* er = reinterpret_cast<const int*>(e);
+  for (int n = threadIdx.x; n < d; n += blockDim.x) {
+    const int* pr = reinterpret_cast<const int*>(P + (size_t)n * Ef);
+    int acc = 0;
+    for (int k = 0; k < Ef / 4; ++k) acc = __builtin_amdgcn_sdot4(er[k], pr[k], acc, false);
+    x[(size_t)r * d + n] = fmaf((float)acc * s_proj, c, pe[(size_t)pos * d + n]);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // LayerNorm + quantization.  One wave per row; element i lives in lane i % 64
 // (slot j = i / 64 of v) and is added to that lane's partial in ascending i
@@ -799,6 +823,16 @@ hipError_t launch_embed(const int32_t* tok, int rows, int S_for_pos, const int* 
   if (rows <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_embed, dim3((rows + 3) / 4), dim3(256), 0, s, tok, rows, S_for_pos, step, E, c_emb, pe, d, V,
                      x);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed_proj(const int32_t* tok, int rows, int S_for_pos, const int* step, const int8_t* E, int Ef,
+                             const int8_t* P, float s_proj, const float* c_emb, const float* pe, int d, int V,
+                             float* x, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (Ef < 4 || Ef % 4 || Ef > kMaxEmbDim) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_embed_proj, dim3(rows), dim3(256), 0, s, tok, S_for_pos, step, E, Ef, P, s_proj, c_emb, pe, d,
+                     V, x);
   return hipGetLastError();
 }
 

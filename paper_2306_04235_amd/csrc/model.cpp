@@ -301,13 +301,30 @@ int build_model(const void* blob, size_t n, unsigned flags, mnmt_model& m, Image
     m.s_enc = s_enc;
     m.inv_enc = (float)(1.0 / (double)s_enc);
     m.inv_fin = (float)(1.0 / (double)s_fin);
-    const int8_t* E = P.i8("emb.w", (uint32_t)V, (uint32_t)d);
+    // factorized embedding (Section 2.1): E [V, Ef] and the projection P [d, Ef]
+    int Ef = d;
+    float s_proj = 0.f, s_u = 0.f;
+    const int8_t* Pw = nullptr;
+    const auto itp = P.t.find("emb.proj.w");
+    if (itp != P.t.end()) {
+      Ef = (int)itp->second.d1;
+      Pw = P.i8("emb.proj.w", (uint32_t)d, (uint32_t)Ef);
+      if (!Pw || Ef < 64 || Ef % 64 || Ef > d || !scalar(P, "emb.proj.sw", &s_proj, true) ||
+          !scalar(P, "emb.proj.sout", &s_u, true)) {
+        if (P.err.empty() || Pw) P.err = "factorized embedding: emb.proj.w [d, E] with E a multiple of 64 <= d, "
+                                         "positive emb.proj.sw and emb.proj.sout";
+        ok = false;
+      }
+      I.emb_dim = Ef;
+      m.s_proj = s_proj;
+    }
+    const int8_t* E = ok ? P.i8("emb.w", (uint32_t)V, (uint32_t)Ef) : nullptr;
     const float* sE = P.f32("emb.s", (uint32_t)V);
     const float* pe = P.f32("pe", (uint32_t)Pn, (uint32_t)d);
-    ok = E && sE && pe;
+    ok = ok && E && sE && pe;
     if (ok) {
-      const size_t oE = img->alloc((size_t)V * d);
-      std::memcpy(img->buf.data() + oE, E, (size_t)V * d);
+      const size_t oE = img->alloc((size_t)V * Ef);
+      std::memcpy(img->buf.data() + oE, E, (size_t)V * Ef);
       const size_t oc = img->alloc(sizeof(float) * V), oo = img->alloc(sizeof(float) * V);
       float* ce = reinterpret_cast<float*>(img->buf.data() + oc);
       float* co = reinterpret_cast<float*>(img->buf.data() + oo);
@@ -319,13 +336,34 @@ int build_model(const void* blob, size_t n, unsigned flags, mnmt_model& m, Image
           break;
         }
         ce[v] = (float)((double)s * std::sqrt((double)d));
-        co[v] = (float)((double)s_fin * (double)s);
+        co[v] = (float)((double)(Pw ? s_u : s_fin) * (double)s);
       }
       const size_t op = img->alloc(sizeof(float) * (size_t)Pn * d);
       std::memcpy(img->buf.data() + op, pe, sizeof(float) * (size_t)Pn * d);
-      const size_t of = img->alloc(frag_bytes(V, d));  // written on the device after the upload
+      if (!Pw) {
+        const size_t of = img->alloc(frag_bytes(V, d));  // written on the device after the upload
+        img->bind(&m.E_frag, of);
+      } else {
+        // P [d, Ef] for the input rows; its transpose [Ef, d] with the folded
+        // requantization s_fin * s_proj / s_u (no bias) for the output side
+        const size_t oP = img->alloc((size_t)d * Ef), oT = img->alloc((size_t)d * Ef);
+        std::memcpy(img->buf.data() + oP, Pw, (size_t)d * Ef);
+        int8_t* tr = reinterpret_cast<int8_t*>(img->buf.data() + oT);
+        for (int n = 0; n < d; ++n)
+          for (int k = 0; k < Ef; ++k) tr[(size_t)k * d + n] = Pw[(size_t)n * Ef + k];
+        const size_t os = img->alloc(sizeof(float) * Ef), ob = img->alloc(sizeof(float) * Ef);
+        float* sc = reinterpret_cast<float*>(img->buf.data() + os);
+        const float mu = (float)((double)s_fin * (double)s_proj / (double)s_u);
+        for (int k = 0; k < Ef; ++k) sc[k] = mu;  // the bias stays zero
+        img->bind(&m.proj, oP);
+        img->bind(&m.proj_out.w, oT);
+        img->bind(&m.proj_out.scale, os);
+        img->bind(&m.proj_out.bias, ob);
+        m.proj_out.N = Ef;
+        m.proj_out.K = d;
+        m.proj_out.inv_in = (float)(1.0 / (double)s_fin);
+      }
       img->bind(&m.E, oE);
-      img->bind(&m.E_frag, of);
       img->bind(&m.c_emb, oc);
       img->bind(&m.c_out, oo);
       img->bind(&m.pe, op);
@@ -396,7 +434,7 @@ int finish_model(Image* img, mnmt_model& m, void* d_arena, size_t arena_bytes, h
   for (size_t l = 0; l < m.dec.size(); ++l)
     if (m.dec_alias[l] >= 0) m.dec[l] = m.dec[m.dec_alias[l]];
   hipError_t e = hipMemcpyAsync(d_arena, img->buf.data(), img->buf.size(), hipMemcpyHostToDevice, s);
-  if (e == hipSuccess)
+  if (e == hipSuccess && m.E_frag)
     e = launch_pack_fragments(m.E, m.info.vocab, m.info.d_model, const_cast<int8_t*>(m.E_frag), s);
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) {

@@ -32,7 +32,7 @@ constexpr size_t kEncAccRows = 64;  // rows of the small-batch encoder path
 struct Plan {
   size_t src, len, region, enc_x, enc_x2, enc_a, enc_qkv, enc_h, enc_out, logits;
   std::vector<size_t> cross_kv, kc, vc;
-  size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, fslots, enc_acc;
+  size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, dec_u, fslots, enc_acc;
   size_t cur_tok, step, slots, out_tok, finished, out_len, out_key, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
   size_t chain_err, enc_chain, beam_count;
@@ -111,6 +111,7 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.dec_qkv = b.take(R * 3 * d);
   p.dec_q = b.take(R * d);
   p.dec_h = b.take(R * F);
+  p.dec_u = b.take(R * d);  // factorized embedding: emb_dim <= d codes per row
   for (size_t l = 0; l < Ld; ++l) {
     p.kc.push_back(b.take(R * T * d));
     p.vc.push_back(b.take(R * T * d));
@@ -154,6 +155,36 @@ int qlin(const LinearDev& L, const int8_t* X, int M, int kind, void* out, float 
   EpiArgs e{kind, out, L.N, gamma, argmax};
   LAUNCH(launch_qlinear(X, L.K, L.w, L.scale, L.bias, M, L.K, L.N, e, s));
   return MNMT_OK;
+}
+
+// A factorized embedding (Section 2.1) runs on the general decode paths only:
+// the fused batch-1 kernels embed and project over rows of the model width.
+bool factored(const mnmt_model* m) { return m->info.emb_dim > 0; }
+
+// Embedding rows x [rows, d] of tok (position r % S_for_pos, or *step).
+int embed_rows(const mnmt_session* S, const int32_t* tok, int rows, int S_for_pos, const int* step, float* x,
+               hipStream_t s) {
+  const mnmt_model* m = S->m;
+  const int d = m->info.d_model, V = m->info.vocab;
+  if (factored(m))
+    LAUNCH(launch_embed_proj(tok, rows, S_for_pos, step, m->E, m->info.emb_dim, m->proj, m->s_proj, m->c_emb, m->pe,
+                             d, V, x, s));
+  else
+    LAUNCH(launch_embed(tok, rows, S_for_pos, step, m->E, m->c_emb, m->pe, d, V, x, s));
+  return MNMT_OK;
+}
+
+// The int8 rows [R, K] the tied output projection takes: the final rows a
+// [R, d], or for a factorized embedding their projection back to emb_dim.
+int logits_input(mnmt_session* S, int R, const int8_t** X, int* K, hipStream_t s) {
+  const mnmt_model* m = S->m;
+  *X = S->dec_a;
+  *K = m->info.d_model;
+  if (!factored(m)) return MNMT_OK;
+  const int rc = qlin(m->proj_out, S->dec_a, R, MNMT_EPI_I8, S->dec_u, 1.f, s);
+  *X = S->dec_u;
+  *K = m->info.emb_dim;
+  return rc;
 }
 
 // Encoder for at most 64 rows (the batch-1 latency path): the embedding and
@@ -374,7 +405,7 @@ int run_encoder(mnmt_session* S, hipStream_t s) {
   const int d = m->info.d_model, rows = S->B * S->S;
   const bool post = m->info.ln_post;
   const float eps = m->info.ln_eps;
-  if (enc_small_fits(rows, S->S, d, m->dh, m->info.d_ffn) && (int)m->dec.size() <= EncOut::kMaxLayers) {
+  if (!factored(m) && enc_small_fits(rows, S->S, d, m->dh, m->info.d_ffn) && (int)m->dec.size() <= EncOut::kMaxLayers) {
     if (!S->chain_on || m->info.n_heads > kChainCopyStride || m->info.d_ffn / 64 > kChainCopyStride)
       return run_encoder_blocks(S, s);
     // the encoder's kernels as a chain over the two streams (see Chain)
@@ -386,8 +417,10 @@ int run_encoder(mnmt_session* S, hipStream_t s) {
     MNMT_HIP(hipStreamWaitEvent(s, S->join_ev, 0));
     return rc;
   }
-  if (qgemm_small_fits(rows, d) && qgemm_small_fits(rows, m->info.d_ffn)) return run_encoder_small(S, s);
-  LAUNCH(launch_embed(S->src, rows, S->S, nullptr, m->E, m->c_emb, m->pe, d, m->info.vocab, S->enc_x, s));
+  if (!factored(m) && qgemm_small_fits(rows, d) && qgemm_small_fits(rows, m->info.d_ffn))
+    return run_encoder_small(S, s);
+  int rc0 = embed_rows(S, S->src, rows, S->S, nullptr, S->enc_x, s);
+  if (rc0) return rc0;
   const LayerDev& L0 = m->enc[0];
   LAUNCH(launch_ln_quant(S->enc_x, rows, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->enc_a, nullptr, s));
   for (size_t l = 0; l < m->enc.size(); ++l) {
@@ -426,7 +459,8 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
   const float eps = m->info.ln_eps;
   const LayerDev& L0 = m->dec[0];
   if (!rows_ready) {
-    LAUNCH(launch_embed(S->cur_tok, R, 1, S->step, m->E, m->c_emb, m->pe, d, m->info.vocab, S->dec_x, s));
+    const int rc0 = embed_rows(S, S->cur_tok, R, 1, S->step, S->dec_x, s);
+    if (rc0) return rc0;
     LAUNCH(launch_ln_quant(S->dec_x, R, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->dec_a, nullptr, s));
   }
   for (size_t l = 0; l < m->dec.size(); ++l) {
@@ -459,14 +493,17 @@ int greedy_step(mnmt_session* S, int R, int stop_at_eos, float* logits_out, hipS
   const mnmt_model* m = S->m;
   int rc = run_decoder_layers(S, R, 1, false, s);
   if (rc) return rc;
-  const int d = m->info.d_model, V = m->info.vocab;
+  const int V = m->info.vocab;
+  const int8_t* X;
+  int K;
+  if ((rc = logits_input(S, R, &X, &K, s))) return rc;
   if (R <= 8) {
     EpiArgs e{EPI_LOGITS_ARGMAX, logits_out, V, 1.f, S->slots};
-    LAUNCH(launch_qlinear(S->dec_a, d, m->E, m->c_out, nullptr, R, d, V, e, s));
+    LAUNCH(launch_qlinear(X, K, m->E, m->c_out, nullptr, R, K, V, e, s));
   } else {
     float* z = logits_out ? logits_out : S->logits;
     EpiArgs e{MNMT_EPI_LOGITS, z, V, 1.f, nullptr};
-    LAUNCH(launch_qlinear(S->dec_a, d, m->E, m->c_out, nullptr, R, d, V, e, s));
+    LAUNCH(launch_qlinear(X, K, m->E, m->c_out, nullptr, R, K, V, e, s));
     LAUNCH(launch_row_argmax(z, R, V, S->slots, s));
   }
     LAUNCH(launch_greedy_commit(S->slots, R, S->cfg.max_tgt_len, S->cur_tok, S->out_tok, S->finished, S->out_len,
@@ -774,7 +811,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
 
 bool step_path_used(const mnmt_session* S, int R) {
   const mnmt_model* m = S->m;
-  return step_path_fits(R, m->info.d_model, m->dh, m->info.d_ffn, S->cfg.max_tgt_len, S->S);
+  return !factored(m) && step_path_fits(R, m->info.d_model, m->dh, m->info.d_ffn, S->cfg.max_tgt_len, S->S);
 }
 
 // The 1-2 row path's input rows: embeddings of cur_tok at the position held
@@ -790,7 +827,7 @@ int embed_step_input(mnmt_session* S, int R, hipStream_t s) {
 int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logits_out, hipStream_t s,
                     bool fold = false, bool last = false, Chain* ch = nullptr) {
   if (step_path_used(S, R)) return greedy_step_v3(S, R, t, stop_at_eos, logits_out, s, fold, last, ch);
-  if (R <= 8) return greedy_step_fused(S, R, t, stop_at_eos, logits_out, s);
+  if (R <= 8 && !factored(S->m)) return greedy_step_fused(S, R, t, stop_at_eos, logits_out, s);
   return greedy_step(S, R, stop_at_eos, logits_out, s);
 }
 
@@ -798,11 +835,16 @@ int greedy_step_any(mnmt_session* S, int R, int t, int stop_at_eos, float* logit
 // previous step's beam update, which also prepares them for the next one.
 int beam_step(mnmt_session* S, int R, int W, int t, int steps, hipStream_t s) {
   const mnmt_model* m = S->m;
-  int rc = run_decoder_layers(S, R, W, true, s, t > 0);
+  // factorized embeddings embed their rows in the decoder (the beam update
+  // prepares rows of the model width only)
+  int rc = run_decoder_layers(S, R, W, true, s, t > 0 && !factored(m));
   if (rc) return rc;
   const int d = m->info.d_model, V = m->info.vocab;
+  const int8_t* X;
+  int K;
+  if ((rc = logits_input(S, R, &X, &K, s))) return rc;
   EpiArgs e{MNMT_EPI_LOGITS, S->logits, V, 1.f, nullptr};
-  LAUNCH(launch_qlinear(S->dec_a, d, m->E, m->c_out, nullptr, R, d, V, e, s));
+  LAUNCH(launch_qlinear(X, K, m->E, m->c_out, nullptr, R, K, V, e, s));
   LAUNCH(launch_beam_topk(S->logits, S->beam, S->step, s));
   const LayerDev& L0 = m->dec[0];
   BeamNext nx{};
@@ -814,7 +856,7 @@ int beam_step(mnmt_session* S, int R, int W, int t, int steps, hipStream_t s) {
   nx.d = d;
   nx.V = V;
   nx.P = m->info.max_pos;
-  nx.steps = steps;
+  nx.steps = factored(m) ? 0 : steps;
   nx.do_ln = !m->info.ln_post;
   nx.g = L0.sa_ln.g;
   nx.b = L0.sa_ln.b;
@@ -931,6 +973,7 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->dec_qkv = (int8_t*)at(p.dec_qkv);
   S->dec_q = (int8_t*)at(p.dec_q);
   S->dec_h = (int8_t*)at(p.dec_h);
+  S->dec_u = (int8_t*)at(p.dec_u);
   for (size_t l = 0; l < p.kc.size(); ++l) {
     S->kcache.push_back((int8_t*)at(p.kc[l]));
     S->vcache.push_back((int8_t*)at(p.vc[l]));

@@ -35,7 +35,8 @@ class MnmtError(RuntimeError):
 
 class ModelInfo(C.Structure):
     _fields_ = [(n, C.c_int32) for n in ("d_model", "n_heads", "d_ffn", "n_enc", "n_dec", "vocab", "max_pos",
-                                         "ln_post", "pad_id", "bos_id", "eos_id", "unk_id")] + [("ln_eps", C.c_float)]
+                                         "ln_post", "pad_id", "bos_id", "eos_id", "unk_id")] + [
+        ("ln_eps", C.c_float), ("emb_dim", C.c_int32)]
 
 
 class SessionCfg(C.Structure):

@@ -10,6 +10,9 @@ The recipe:
 * the shared embedding E[V, d] is drawn and quantized the same way (per row);
 * biases N(0, 0.02), LayerNorm gains N(1, 0.02), shifts N(0, 0.02);
 * residual weights gamma = 1 unless ``random_gamma`` (then U[0.5, 1.5]);
+* optional: cross-layer parameter sharing (``share_every``) and a factorized
+  embedding (``emb_dim``: E [V, emb_dim] rows N(0, emb_std) and a [d, emb_dim]
+  projection N(0, 1 / emb_dim) with one per-tensor scale);
 * static per-tensor activation scales "drawn from the seed": each is
   4 sigma / 127 times U[0.9, 1.1], where sigma is the standard deviation the
   activation has under this weight distribution (1 for LayerNorm outputs,
@@ -53,6 +56,7 @@ class ModelConfig:
     emb_distinct: int = 0  # > 0: embedding row v repeats drawn row v mod emb_distinct (groups of equal logits)
     w_bits: int = 8  # 4: linear weights as 4-bit codes (the paper's W-E-A 4-8-8; the embedding stays 8-bit)
     share_every: int = 0  # > 0: layer l >= share_every reuses the parameters of layer l % share_every (per stack)
+    emb_dim: int = 0  # > 0: factorized embedding [V, emb_dim] with a [d_model, emb_dim] projection
 
 
 # The model shapes of the five workloads.
@@ -117,10 +121,17 @@ def build_model(cfg: ModelConfig) -> bytes:
     def gamma(name):
         t[name] = f32([rng.uniform(*cfg.gamma_range) if cfg.random_gamma else 1.0])
 
-    e = rng.normal(0.0, cfg.emb_std, size=(cfg.emb_distinct or cfg.vocab, d))
+    ef = cfg.emb_dim or d
+    e = rng.normal(0.0, cfg.emb_std, size=(cfg.emb_distinct or cfg.vocab, ef))
     if cfg.emb_distinct:
         e = e[np.arange(cfg.vocab) % cfg.emb_distinct]
     t["emb.w"], t["emb.s"] = _quantize_rows(e)
+    if cfg.emb_dim:  # factorized: P [d, E] with entries N(0, 1/E), one per-tensor scale
+        pw = rng.normal(0.0, 1.0 / np.sqrt(ef), size=(d, ef))
+        s_p = float(np.abs(pw).max()) / 127.0
+        t["emb.proj.w"] = np.clip(np.rint(pw / s_p), -127, 127).astype(np.int8)
+        t["emb.proj.sw"] = f32([s_p])
+        t["emb.proj.sout"] = f32([_act_scale(rng, np.sqrt(d / ef))])  # u = a P has variance d / E
     t["pe"] = positional_table(cfg.max_pos, d)
     s_enc = _act_scale(rng, 1.0)
     s_fin = _act_scale(rng, 1.0)

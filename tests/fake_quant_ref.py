@@ -17,7 +17,10 @@ and computes every stage in float64 straight from the paper's definitions:
 * one shared embedding for input and output (Appendix D), input rows scaled
   by sqrt(d) plus the stored position table, output projection tied;
 * cross-layer parameter sharing (Section 2.2): a layer whose file entry
-  "<side>.<l>.share" names layer j runs on layer j's parameters.
+  "<side>.<l>.share" names layer j runs on layer j's parameters;
+* embedding factorization (Section 2.1): embedding rows of width E times a
+  transformation P [d, E] on the way in, the final rows times P on the way
+  out (an int8 edge like every linear input), then the tied embedding.
 
 Quantizer (the paper's rounding to the nearest integer, symmetric reading):
 code = clamp(round(value / s), -127, 127).  The stage functions return the
@@ -72,10 +75,21 @@ class FakeQuantModel:
         var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
         return (x - mu) / np.sqrt(var + self.eps) * self.vec(pfx + ".g") + self.vec(pfx + ".b")
 
+    @property
+    def factorized(self) -> bool:
+        return "emb.proj.w" in self.t
+
+    def proj(self) -> np.ndarray:
+        """Factorized embedding (Section 2.1): the real transformation P [d, E]."""
+        return self.t["emb.proj.w"].astype(F64) * self.scalar("emb.proj.sw")
+
     def embed(self, tokens, positions) -> np.ndarray:
         E = self.t["emb.w"].astype(F64) * self.vec("emb.s")[:, None]
         pe = self.t["pe"].astype(F64)
-        return E[np.asarray(tokens)] * np.sqrt(self.d) + pe[np.asarray(positions)]
+        e = E[np.asarray(tokens)]
+        if self.factorized:
+            e = e @ self.proj().T
+        return e * np.sqrt(self.d) + pe[np.asarray(positions)]
 
     def sublayer_input(self, x, ln_pfx: str, s_in: float) -> np.ndarray:
         """Code-unit value of the sublayer's int8 input: pre-LN normalizes the
@@ -161,8 +175,17 @@ class FakeQuantModel:
         s = self.vec(pfx + ".sout")
         return np.concatenate([y[:, :self.d] / s[0], y[:, self.d:] / s[1]], axis=1)
 
-    def logits(self, fin_codes) -> np.ndarray:
+    def proj_back(self, fin_codes) -> np.ndarray:
+        """Factorized embedding: code-unit value of the final rows mapped back to
+        the embedding width, u = (a P) / s_u."""
+        return (np.asarray(fin_codes, F64) * self.scalar("dec.sout")) @ self.proj() / self.scalar("emb.proj.sout")
+
+    def logits(self, fin_codes, u_codes=None) -> np.ndarray:
+        """Tied output projection of the final rows (or, factorized, of their
+        int8 projection u_codes)."""
         E = self.t["emb.w"].astype(F64) * self.vec("emb.s")[:, None]
+        if self.factorized:
+            return (np.asarray(u_codes, F64) * self.scalar("emb.proj.sout")) @ E.T
         return (np.asarray(fin_codes, F64) * self.scalar("dec.sout")) @ E.T
 
     # --- the whole model without activation quantization ------------------------
@@ -211,4 +234,6 @@ class FakeQuantModel:
                               self.scalar(p + ".ff.gamma"), p + ".ff.ln")
         fin = x if self.post else self.layer_norm(x, "dec.ln")
         E = self.t["emb.w"].astype(F64) * self.vec("emb.s")[:, None]
+        if self.factorized:
+            fin = fin @ self.proj()
         return fin @ E.T

@@ -141,3 +141,26 @@ def test_shared_layers_are_stored_once():
     with pytest.raises(mnmt.MnmtError) as e:
         mnmt.mnmt_model_bytes(write_model(hdr, t2))
     assert e.value.status == mnmt.E_BAD_MODEL
+
+
+def test_factorized_embedding_arena_and_validation():
+    """A factorized embedding (Section 2.1) stores E [V, emb_dim], the
+    projection [d, emb_dim] and its transpose; a projection whose width is not
+    a multiple of 64 or exceeds d is rejected."""
+    import dataclasses
+
+    from tests.test_oracle_assembly import FACTOR
+
+    blob = G.build_model(FACTOR)
+    plain = G.build_model(dataclasses.replace(FACTOR, emb_dim=0))
+    d, V, E = FACTOR.d_model, FACTOR.vocab, FACTOR.emb_dim
+    # smaller embedding, no fragment-order copy, plus P and its transpose with E scales and biases
+    assert mnmt.mnmt_model_bytes(plain) - mnmt.mnmt_model_bytes(blob) >= 2 * V * (d - E) - 2 * d * E - 4096
+    hdr, t = read_model(blob)
+    for bad in (np.zeros((d, 96), np.int8), np.zeros((d, 512), np.int8)):
+        t2 = {k: np.ascontiguousarray(v) for k, v in t.items()}
+        t2["emb.proj.w"] = bad
+        t2["emb.w"] = np.zeros((V, bad.shape[1]), np.int8)
+        with pytest.raises(mnmt.MnmtError) as e:
+            mnmt.mnmt_model_bytes(write_model(hdr, t2))
+        assert e.value.status == mnmt.E_BAD_MODEL

@@ -371,6 +371,29 @@ def test_cross_layer_sharing_models(torch_dev):
     _greedy_check(torch, dev, SHARED_256, src, lens, 30)
 
 
+FACTOR = G.ModelConfig("factorized-256", 256, 4, 512, 2, 2, 2000, ln_post=0, seed=83, random_gamma=True,
+                       weight_std=0.2, emb_dim=128)
+FACTOR_POST = G.ModelConfig("factorized-post", 128, 2, 256, 2, 1, 700, ln_post=1, seed=84, weight_std=0.1,
+                            emb_dim=64)
+
+
+def test_factorized_embedding_models(torch_dev):
+    """Embedding factorization (Section 2.1): rows of width E projected to the
+    model width on the way in (k_embed_proj) and the final rows projected back
+    (an int8 linear layer over the transposed matrix) before the tied logits,
+    on the general greedy path at 1, 5 and 12 rows (per-step logits bits via
+    mnmt_decode_step) and in beam search, against the oracle."""
+    torch, dev = torch_dev
+    for cfg in (FACTOR, FACTOR_POST):
+        om, gm = _pair(cfg)
+        assert gm.info.emb_dim == cfg.emb_dim and om.emb_dim == cfg.emb_dim
+        for B in (1, 5, 12):
+            src, lens = G.make_sources(cfg.vocab, B, (3, 16), seed=70 + B, s_max=16)
+            _greedy_check(torch, dev, cfg, src, lens, 10)
+        src, lens = G.make_sources(cfg.vocab, 4, [5, 1, 9, 9], seed=31, s_max=9)
+        _beam_check(torch, dev, cfg, src, lens, 4, 8, 0.6)
+
+
 def test_mobile_beam_workload_all_sentences(torch_dev):
     """The batched beam workload on the mobile model: all 64 sentences (10-60
     source tokens, beam 4, 64 steps) against the oracle, run one sentence per

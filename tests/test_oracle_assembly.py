@@ -42,6 +42,10 @@ VARIED = G.ModelConfig("varied-256", 256, 4, 1024, 2, 2, 32000, ln_post=0, seed=
 SMALL_W4 = dataclasses.replace(SMALL_PRE, name="small-preln-w4", w_bits=4, seed=80)
 SHARED = G.ModelConfig("shared-preln", 64, 4, 128, 4, 3, 500, ln_post=0, seed=82, random_gamma=True,
                        weight_std=0.1, share_every=1)
+FACTOR = G.ModelConfig("factorized-256", 256, 4, 512, 2, 2, 2000, ln_post=0, seed=83, random_gamma=True,
+                       weight_std=0.2, emb_dim=128)
+FACTOR_POST = G.ModelConfig("factorized-post", 128, 2, 256, 2, 1, 700, ln_post=1, seed=84, weight_std=0.1,
+                            emb_dim=64)
 
 MODELS = {
     "tiny": lambda: model_blob("TINY"),
@@ -50,6 +54,8 @@ MODELS = {
     "small_pre_w4": lambda: G.build_model(SMALL_W4),
     "varied_256": lambda: G.build_model(VARIED),
     "shared_layers": lambda: G.build_model(SHARED),
+    "factorized_embedding": lambda: G.build_model(FACTOR),
+    "factorized_post_ln": lambda: G.build_model(FACTOR_POST),
     "mobile": lambda: model_blob("MOBILE"),
 }
 
@@ -139,7 +145,9 @@ def decoder_stages(ref: FakeQuantModel, om, src, tokens, st: Stats):
         check_codes(tr["pj"][u + 2][:, :F], h_val, f"{p} FFN hidden (ReLU)", st)
         check_f32(tr["x"][u + 3], x_next, f"{p} residual after FFN")
     check_codes(tr["fin"], ref.final_input(tr["x"][3 * ref.n_dec]), "output projection input", st)
-    check_f32(tr["z"], ref.logits(tr["fin"]), "logits (tied embedding, no bias)")
+    if ref.factorized:
+        check_codes(tr["fin_u"], ref.proj_back(tr["fin"]), "factorized embedding: final rows projected back", st)
+    check_f32(tr["z"], ref.logits(tr["fin"], tr["fin_u"]), "logits (tied embedding, no bias)")
     return tr
 
 
