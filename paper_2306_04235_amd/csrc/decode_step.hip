@@ -78,14 +78,58 @@ __device__ __forceinline__ void load_row_data(const StepIn& in, int r, int d, Ro
   for (int j = 0; j < NJ; ++j) {
     const int i = min(lane + 64 * j, d - 1);
     q.x[j] = in.x_in[(size_t)r * d + i];
-    q.a[j] = in.acc[(size_t)r * d + i];
+    q.a[j] = (int)(unsigned)in.acc[(size_t)r * d + i];  // the sum's low half (StepCount)
   }
 }
 
-// Finishes row r from the loaded registers: the pending residual update, the LayerNorm, the store of the updated residual row
-// (block 0), and the int8 codes in a_lds + r * d.
+// Counted hand-off (StepCount) words: relaxed agent-scope 64-bit atomics.
+__device__ __forceinline__ unsigned long long count_load(const unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void tag_store(unsigned long long* p, unsigned tag, unsigned bits) {
+  __hip_atomic_store(p, ((unsigned long long)tag << 32) | bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// One block's int32 partial sum into a counted word: the value (mod 2^32)
+// plus one count.
+__device__ __forceinline__ void count_add(unsigned long long* p, int v) {
+  atomicAdd(p, (unsigned long long)(unsigned)v + kCountUnit);
+}
+
+// Row r from the previous kernel through the counted hand-off: lane l polls
+// its elements' tagged row words and counted sums until every tag is `want`
+// and every count in.cnt.count_in, which leaves the row and the exact sums
+// in q.  Bounded like chain_wait: a poll that gives up records it in *err.
 template <int NJ>
-__device__ __forceinline__ void finish_row(const StepIn& in, int r, int d, RowRegs<NJ>& q, int8_t* a_lds) {
+__device__ __forceinline__ void poll_row_data(const StepIn& in, int r, int d, RowRegs<NJ>& q, unsigned want) {
+  const int lane = threadIdx.x & 63;
+  const unsigned long long need = (unsigned long long)in.cnt.count_in;
+  unsigned spins = 0;
+  while (true) {
+    bool ok = true;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = min(lane + 64 * j, d - 1);
+      const unsigned long long wx = count_load(in.cnt.x_in64 + (size_t)r * d + i);
+      const unsigned long long wa = count_load(in.acc + (size_t)r * d + i);
+      ok &= (unsigned)(wx >> 32) == want && (wa >> 40) == need;
+      q.x[j] = __uint_as_float((unsigned)wx);
+      q.a[j] = (int)(unsigned)wa;
+    }
+    if (ok) break;
+    if (++spins >= kChainSpinLimit) {
+      if (in.chain.err) __hip_atomic_fetch_or(in.chain.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+// Finishes row r from the loaded registers: the pending residual update, the
+// LayerNorm, the store of the updated residual row (block 0: plain, or tagged
+// with out_tag for the counted hand-off), and the int8 codes in a_lds + r * d.
+template <int NJ>
+__device__ __forceinline__ void finish_row(const StepIn& in, int r, int d, RowRegs<NJ>& q, int8_t* a_lds,
+                                           unsigned out_tag = 0) {
   const int lane = threadIdx.x & 63;
   float v[NJ];
 #pragma unroll
@@ -97,6 +141,13 @@ __device__ __forceinline__ void finish_row(const StepIn& in, int r, int d, RowRe
     for (int j = 0; j < NJ; ++j) {
       const int i = lane + 64 * j;
       if (i < d) chain_store(in.x_out + (size_t)r * d + i, v[j]);
+    }
+  }
+  if (blockIdx.x == 0 && in.cnt.x_out64) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = lane + 64 * j;
+      if (i < d) tag_store(in.cnt.x_out64 + (size_t)r * d + i, out_tag, __float_as_uint(v[j]));
     }
   }
   if (in.ln_mode == 2) ln_row<NJ>(v, q.g, q.b, d, in.eps);  // pre-LN: normalize the sublayer input
@@ -113,7 +164,14 @@ constexpr int kStepThreads = 256;  // block size of every step kernel
 // the dispatch packet and waits for every load issued before it.)
 __device__ __forceinline__ void clear_acc(const StepIn& in) {
   if (blockIdx.x == 0 && in.zero_acc)
-    for (int i = threadIdx.x; i < in.zero_n; i += kStepThreads) chain_store(in.zero_acc + i, 0);
+    for (int i = threadIdx.x; i < in.zero_n; i += kStepThreads) chain_store(in.zero_acc + i, 0ull);
+}
+
+// Before block 0 adds its partial sums: its clear of an accumulator must have
+// landed, since the next kernel's counted poll (not a flag stored after a
+// full wait) is all that orders that accumulator's next producer after it.
+__device__ __forceinline__ void clear_done(const StepIn& in) {
+  if (blockIdx.x == 0 && in.zero_acc) __builtin_amdgcn_s_waitcnt(0);
 }
 
 // The projections run on v_mfma_i32_16x16x64_i8 even though only R <= 2 of
@@ -187,6 +245,8 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   }
   int n_att = SELF ? at.t + 1 : at.len[r];
   n_att = SELF ? n_att : (n_att < 1 ? 1 : (n_att > at.S ? at.S : n_att));
+  const unsigned ep = *in.cnt.epoch;  // row tags of the counted hand-off (StepCount)
+  const unsigned want = ep * kTagSpan + in.cnt.tag_in, otag = ep * kTagSpan + in.cnt.tag_out;
   RowRegs<NJ> rr;
   if (MODE == 1) {
     // the position term now, the token's embedding once the token is known
@@ -216,7 +276,14 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
     for (int k = 0; k < 4; ++k) pk[k] = sl[min(lane + 64 * k, cm.nslots - 1)];
     fin = cm.finished[row];
   }
-  if (MODE != 1) load_row_data(in, min(wave, R - 1), d, rr);
+  if (MODE != 1) {
+    if (in.cnt.count_in > 0) {
+      if (wave < R) poll_row_data(in, wave, d, rr, want);
+      lds_barrier();  // the accumulator clear below comes after every wave's poll
+    } else {
+      load_row_data(in, min(wave, R - 1), d, rr);
+    }
+  }
   if (MODE == 1) {
     unsigned long long key = pk[0];
 #pragma unroll
@@ -234,7 +301,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   }
   // 2. the rows
   clear_acc(in);
-  if (wave < R) finish_row(in, wave, d, rr, a_lds);
+  if (wave < R) finish_row(in, wave, d, rr, a_lds, otag);
 
   lds_barrier();
   // 3. Q (K, V) of the head on the matrix cores, requantized into LDS
@@ -342,6 +409,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   lds_barrier();
   // 5. this head's share of the output projection (K = dh), exact int32
   //    partial sums added to the accumulator
+  clear_done(in);
   {
     const int crow = l16 < R ? l16 : 0;
     const v4i cf = kq < nc ? *(const v4i*)(ctx[crow] + 16 * kq) : v4i{0, 0, 0, 0};
@@ -353,7 +421,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
         if (lane < 16)
 #pragma unroll
           for (int m = 0; m < kStepRows; ++m)
-            if (m < R) atomicAdd(at.acc_out + (size_t)m * d + n0 + lane, acc[m]);
+            if (m < R) count_add(at.acc_out + (size_t)m * d + n0 + lane, acc[m]);
       }
     }
   }
@@ -406,13 +474,20 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
     const int n = min(16 * (wave + 4 * t) + l16, d - 1);
     of[t] = load_wfrag<W4>(f.W2, n, F, f0 + 16 * kq);
   }
+  const unsigned ep = *in.cnt.epoch;  // row tags of the counted hand-off (StepCount)
+  const unsigned want = ep * kTagSpan + in.cnt.tag_in, otag = ep * kTagSpan + in.cnt.tag_out;
   RowRegs<NJ> rr;
   load_row_consts(in, d, rr);
   asm volatile("" ::: "memory");  // the weight loads stay ahead of the wait
   chain_wait(in.chain);
-  load_row_data(in, min(wave, R - 1), d, rr);
+  if (in.cnt.count_in > 0) {
+    if (wave < R) poll_row_data(in, wave, d, rr, want);
+    lds_barrier();  // the accumulator clear below comes after every wave's poll
+  } else {
+    load_row_data(in, min(wave, R - 1), d, rr);
+  }
   clear_acc(in);
-  if (wave < R) finish_row(in, wave, d, rr, a_lds);
+  if (wave < R) finish_row(in, wave, d, rr, a_lds, otag);
   lds_barrier();
   {
     const int arow = l16 < R ? l16 : 0;
@@ -426,6 +501,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
         if (m < R) h[m][16 * wave + lane] = code_of(fmaxf(fmaf((float)acc[m], e_sc, e_bi), 0.0f));
   }
   lds_barrier();
+  clear_done(in);
   {
     const int hr = l16 < R ? l16 : 0;
     const v4i hf = *(const v4i*)(h[hr] + 16 * kq);
@@ -437,7 +513,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
         if (lane < 16)
 #pragma unroll
           for (int m = 0; m < kStepRows; ++m)
-            if (m < R) atomicAdd(f.acc_out + (size_t)m * d + n0 + lane, acc[m]);
+            if (m < R) count_add(f.acc_out + (size_t)m * d + n0 + lane, acc[m]);
       }
     }
   }

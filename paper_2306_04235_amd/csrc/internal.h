@@ -82,9 +82,10 @@ hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, co
 hipError_t launch_greedy_commit(unsigned long long* slots, int R, int T, int32_t* cur_tok, int32_t* out_tok,
                                 int32_t* finished, int32_t* out_len, int* step, int stop_at_eos, int eos,
                                 int pad, unsigned long long* out_key, hipStream_t s);
+// Also advances the counted hand-off's translation counter *epoch (if not null).
 hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
                                int32_t* out_len, int* step, int bos, unsigned long long* fslots, int n_fslots,
-                               hipStream_t s);
+                               unsigned* epoch, hipStream_t s);
 // A nonzero *chain_err (a chained kernel's wait gave up) marks every row's
 // length -1 instead of copying it.
 hipError_t launch_greedy_output(const int32_t* out_tok, const int32_t* out_len, int R, int T, int32_t* out,
@@ -182,12 +183,32 @@ struct StepChain {
   int* err;
 };
 
+// Counted hand-off between consecutive step kernels (instead of flags):
+// the int32 partial sums of a kernel's blocks are added into 64-bit words,
+// the sum modulo 2^32 in the low half and one count of 2^40 per adding block
+// (at most 255 blocks: the low half's carries stay below bit 40), so a
+// consumer polls the very words it needs until their count equals the
+// producer's block count; block 0 of the producer stores its updated fp32
+// rows as 64-bit words tagged with (translation, step, kernel).  The
+// producer needs no wait for its atomics and no flag, the consumer no cache
+// invalidation and no second load.
+constexpr unsigned kTagSpan = 8192;  // row tag = epoch * kTagSpan + step * 32 + kernel index in the step
+constexpr unsigned long long kCountUnit = 1ull << 40;
+struct StepCount {
+  int count_in;                       // > 0: poll acc until this many blocks added, rows from x_in64
+  const unsigned long long* x_in64;   // [R][d] the previous kernel's tagged rows
+  unsigned tag_in;                    // their tag offset
+  unsigned long long* x_out64;        // [R][d] this kernel's rows, tagged (block 0), or null
+  unsigned tag_out;
+  const unsigned* epoch;              // translation counter (advanced by each reset)
+};
+
 struct StepIn {            // the sublayer input rows of a step kernel
   // Every pointer is valid for the extent given even where its flag is off,
   // so that the kernels load without branches.
   const float* x_in;       // residual rows [R, d]
   float* x_out;            // block 0 stores the updated rows here (or null)
-  const int32_t* acc;      // [R, d]: pending update x <- fma(gamma, x, fma(acc, scale, bias))
+  const unsigned long long* acc;  // [R, d] counted sums (StepCount): pending x <- fma(gamma, x, fma(acc, scale, bias))
   const float* scale;      // [d]
   const float* bias;       // [d]
   float gamma;
@@ -197,9 +218,10 @@ struct StepIn {            // the sublayer input rows of a step kernel
   int ln_mode;             // 0 none, 1 post-LN (the residual stream), 2 pre-LN (the sublayer input)
   float eps;
   float inv_s;             // 1 / input scale of the consuming layer
-  int32_t* zero_acc;       // block 0 clears this accumulator (its consumer has finished)
+  unsigned long long* zero_acc;  // block 0 clears this accumulator (its consumer has finished)
   int zero_n;
   StepChain chain;
+  StepCount cnt;
 };
 struct StepAttn {
   int R, d, dh, T, S, t;
@@ -212,7 +234,7 @@ struct StepAttn {
   const int8_t* kv;        // cross keys|values [R][S][2d]
   const int32_t* len;
   float c_qk, c_pv;
-  int32_t* acc_out;        // [R, d] int32, zero on entry
+  unsigned long long* acc_out;  // [R, d] counted sums (StepCount), zero on entry
   bool w4;                 // W and Wo hold packed 4-bit rows (K / 2 bytes each)
 };
 // The greedy commit of the previous step's token, folded into the next
@@ -243,7 +265,7 @@ struct StepFfn {
   const float* scale1;
   const float* bias1;
   const int8_t* W2;        // [d, F]
-  int32_t* acc_out;
+  unsigned long long* acc_out;  // [R, d] counted sums (StepCount)
   bool w4;                 // W1 and W2 hold packed 4-bit rows
 };
 struct StepLogits {
@@ -487,7 +509,7 @@ struct mnmt_session {
   float* dec_x = nullptr;
   float* dec_x2 = nullptr;  // second residual buffer (post-LN ping-pong)
   unsigned long long* fslots = nullptr;  // arg-max slots [8][fused_slots_per_row(V)]
-  int32_t* step_acc = nullptr;           // decode-step accumulators [3][2][d] int32
+  unsigned long long* step_acc = nullptr;  // decode-step accumulators [3][2][d], counted 64-bit words
   int32_t* enc_acc = nullptr;            // small-batch encoder accumulators [2 W_o + 2 W2][64][d] int32
   int8_t* dec_a = nullptr;
   int8_t* dec_qkv = nullptr;
@@ -511,7 +533,10 @@ struct mnmt_session {
   hipEvent_t fork_ev = nullptr, join_ev = nullptr;
   unsigned* chain = nullptr;          // flag words [3 n_dec + 1][kChainSlotWords], cleared per translation
   unsigned* enc_chain = nullptr;      // the encoder's [2 n_enc][kChainSlotWords], cleared by the batch load
-  int* chain_err = nullptr;           // set by a wait that gave up (never cleared)
+  int* chain_err = nullptr;           // set by a wait that gave up (cleared by mnmt_session_status)
+  unsigned* epoch = nullptr;          // translation counter of the counted hand-off's row tags
+  unsigned long long* step_x64 = nullptr;  // tagged rows of the step kernels [3 n_dec][2][d]
+  bool counted_on = true;             // off with MNMT_COUNTED=0: flags between all step kernels
   bool chain_on = true;               // off with MNMT_SERIAL_STEPS=1 in the environment
   std::map<std::string, hipGraphExec_t> graphs;
 };

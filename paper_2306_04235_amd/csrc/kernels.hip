@@ -184,7 +184,8 @@ __global__ __launch_bounds__(64) void k_attn_dec_cross(const int8_t* __restrict_
 // ---------------------------------------------------------------------------
 // Greedy search bookkeeping.
 __global__ void k_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
-                               int32_t* out_len, int* step, int bos, unsigned long long* fslots, int n_fslots) {
+                               int32_t* out_len, int* step, int bos, unsigned long long* fslots, int n_fslots,
+                               unsigned* epoch) {
   for (int r = threadIdx.x; r < R; r += blockDim.x) {
     slots[r] = 0ull;
     cur_tok[r] = bos;
@@ -192,7 +193,10 @@ __global__ void k_greedy_reset(unsigned long long* slots, int R, int steps, int3
     out_len[r] = steps;
   }
   for (int i = threadIdx.x; i < n_fslots; i += blockDim.x) fslots[i] = 0ull;
-  if (threadIdx.x == 0) *step = 0;
+  if (threadIdx.x == 0) {
+    *step = 0;
+    if (epoch) *epoch = *epoch + 1u;
+  }
 }
 
 // Reads the step's arg-max slots (and clears them for the next step), records
@@ -873,9 +877,9 @@ hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, co
 
 hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
                                int32_t* out_len, int* step, int bos, unsigned long long* fslots, int n_fslots,
-                               hipStream_t s) {
+                               unsigned* epoch, hipStream_t s) {
   hipLaunchKernelGGL(k_greedy_reset, dim3(1), dim3(256), 0, s, slots, R, steps, cur_tok, finished, out_len, step,
-                     bos, fslots, n_fslots);
+                     bos, fslots, n_fslots, epoch);
   return hipGetLastError();
 }
 

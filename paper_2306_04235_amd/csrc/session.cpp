@@ -35,7 +35,7 @@ struct Plan {
   size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, dec_u, fslots, enc_acc;
   size_t cur_tok, step, slots, out_tok, finished, out_len, out_key, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
-  size_t chain_err, enc_chain, beam_count;
+  size_t chain_err, enc_chain, beam_count, epoch, step_x64;
   size_t total;
 };
 
@@ -70,7 +70,7 @@ size_t chain_words(const mnmt_model* m) { return (3 * (size_t)m->info.n_dec + 1)
 // 8-byte words cleared by the greedy reset: the fused arg-max slots, the
 // decode-step accumulators and the chain's flag words, which follow each other.
 int fslots_words(const mnmt_model* m) {
-  return 8 * fused_slots_per_row(m->info.vocab) + 3 * 2 * m->info.d_model / 2 + (int)(chain_words(m) / 2);
+  return 8 * fused_slots_per_row(m->info.vocab) + 3 * 2 * m->info.d_model + (int)(chain_words(m) / 2);
 }
 
 Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
@@ -106,7 +106,7 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.dec_x2 = b.take(4 * R * d);
   // fused arg-max slots, the decode-step int32 accumulators and the chain's
   // flag words (cleared together)
-  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row(m->info.vocab) + 4 * 3 * 2 * d + 4 * chain_words(m));
+  p.fslots = b.take(8 * 8 * (size_t)fused_slots_per_row(m->info.vocab) + 8 * 3 * 2 * d + 4 * chain_words(m));
   p.dec_a = b.take(R * d);
   p.dec_qkv = b.take(R * 3 * d);
   p.dec_q = b.take(R * d);
@@ -138,6 +138,8 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.chain_err = b.take(4);
   p.beam_count = b.take(4);
   p.enc_chain = b.take(4 * 2 * (size_t)m->info.n_enc * kChainSlotWords);
+  p.epoch = b.take(4);
+  p.step_x64 = b.take(8 * 3 * Ld * 2 * d);
   p.total = (b.off + 255) / 256 * 256;
   return p;
 }
@@ -629,9 +631,9 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   const mnmt_model* m = S->m;
   const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
   const bool post = m->info.ln_post;
-  int32_t* acc_o = S->step_acc;
-  int32_t* acc_oc = S->step_acc + 2 * d;
-  int32_t* acc_w2 = S->step_acc + 4 * d;
+  unsigned long long* acc_o = S->step_acc;
+  unsigned long long* acc_oc = S->step_acc + 2 * d;
+  unsigned long long* acc_w2 = S->step_acc + 4 * d;
   const int nacc = R * d;
   float* xa = S->dec_x;
   float* xb = S->dec_x2;
@@ -653,7 +655,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   };
   // the residual update of the sublayer whose partial sums are in acc (its
   // post-LN LayerNorm in post-LN models), and the pre-LN LayerNorm of the next
-  auto rows = [&](StepIn& in, const int32_t* acc, const LinearDev* L, float gamma, const LnDev& post_ln,
+  auto rows = [&](StepIn& in, const unsigned long long* acc, const LinearDev* L, float gamma, const LnDev& post_ln,
                   const LnDev& pre_ln) {
     if (acc) {
       in.acc = acc;
@@ -669,7 +671,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       in.ln_mode = post ? 1 : 2;
     }
   };
-  auto attn = [&](const LayerDev& L, bool self, int32_t* acc_out) {
+  auto attn = [&](const LayerDev& L, bool self, unsigned long long* acc_out) {
     StepAttn at{};
     at.R = R;
     at.d = d;
@@ -688,6 +690,34 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     return at;
   };
   const LnDev none{};
+  // Counted hand-off (StepCount) between the step's kernels: kernel k of the
+  // step (3 per layer, then the logits) polls kernel k - 1's counted sums and
+  // tagged rows (0 < k < 3 L) and leaves its own the same way (k < 3 L - 1);
+  // the last FFN still stores its rows plainly and flags its blocks, since
+  // the logits kernel's hundred-odd blocks would all poll the same words, and
+  // the step's first kernel waits on the logits kernel's flags.
+  const int nk = 3 * (int)m->dec.size();
+  const bool counted = S->counted_on && nk < 32;  // tag offsets t * 32 + k
+  int prev_blocks = 0;
+  auto count_io = [&](StepIn& in, int k, int blocks) {
+    in.cnt.epoch = S->epoch;
+    if (counted) {
+      if (k > 0) {
+        in.cnt.count_in = prev_blocks;
+        in.cnt.x_in64 = S->step_x64 + (size_t)(k - 1) * 2 * d;
+        in.cnt.tag_in = (unsigned)(t * 32 + k - 1);
+        in.chain.wait = nullptr;
+        in.chain.nwait = 0;
+      }
+      if (k < nk - 1) {
+        in.cnt.x_out64 = S->step_x64 + (size_t)k * 2 * d;
+        in.cnt.tag_out = (unsigned)(t * 32 + k);
+        in.x_out = nullptr;
+        in.chain.done = nullptr;
+      }
+    }
+    prev_blocks = blocks;
+  };
   const bool folded = fold && t > 0 && fold_ok(m);
   StepCommit cm{};
   if (folded) {
@@ -729,6 +759,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       at.kcache = S->kcache[l];
       at.vcache = S->vcache[l];
       const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l, h, t + 1) : s;
+      count_io(in, 3 * (int)l, h);
       LAUNCH(launch_step_attn(in, at, 1, h, ks, cml));
       if (in.x_out) std::swap(xa, xb);
     }
@@ -740,6 +771,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       StepAttn at = attn(L, false, acc_oc);
       at.kv = S->cross_kv[l];
       const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 1, h, t + 1) : s;
+      count_io(in, 3 * (int)l + 1, h);
       LAUNCH(launch_step_attn(in, at, 0, h, ks, cml));
       std::swap(xa, xb);
     }
@@ -757,6 +789,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       f.bias1 = L.w1.bias;
       f.acc_out = acc_w2;
       const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 2, f.F / 64, t + 1) : s;
+      count_io(in, 3 * (int)l + 2, f.F / 64);
       LAUNCH(launch_step_ffn(in, f, ks));
       std::swap(xa, xb);
     }
@@ -795,8 +828,8 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   gv.stop_at_eos = stop_at_eos;
   gv.eos = m->info.eos_id;
   gv.pad = m->info.pad_id;
-  gv.zero_acc = acc_w2;
-  gv.zero_n = nacc;
+  gv.zero_acc = reinterpret_cast<int32_t*>(acc_w2);  // cleared as 2 nacc int32 words
+  gv.zero_n = 2 * nacc;
   gv.emb_out = S->dec_x;
   gv.E = m->E;
   gv.c_emb = m->c_emb;
@@ -874,7 +907,7 @@ int enqueue_search(mnmt_session* S, const mnmt_search_cfg& sc, hipStream_t s) {
   if (sc.beam == 1) {
     const int R = S->B;
     LAUNCH(launch_greedy_reset(S->slots, R, sc.max_steps, S->cur_tok, S->finished, S->out_len, S->step,
-                               m->info.bos_id, S->fslots, fslots_words(m), s));
+                               m->info.bos_id, S->fslots, fslots_words(m), S->epoch, s));
     if (step_path_used(S, R) && (rc = embed_step_input(S, R, s))) return rc;
     if (step_path_used(S, R) && chain_ok(m) && S->chain_on) {
       // the step kernels alternate between the caller's stream and the side
@@ -965,9 +998,11 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->dec_x2 = (float*)at(p.dec_x2);
   S->fslots = (unsigned long long*)at(p.fslots);
   S->enc_acc = (int32_t*)at(p.enc_acc);
-  S->step_acc = (int32_t*)(S->fslots + 8 * (size_t)fused_slots_per_row((int)V));
+  S->step_acc = (unsigned long long*)(S->fslots + 8 * (size_t)fused_slots_per_row((int)V));
   S->chain = (unsigned*)(S->step_acc + 3 * 2 * d);
   S->chain_err = (int*)at(p.chain_err);
+  S->epoch = (unsigned*)at(p.epoch);
+  S->step_x64 = (unsigned long long*)at(p.step_x64);
   S->enc_chain = (unsigned*)at(p.enc_chain);
   S->dec_a = (int8_t*)at(p.dec_a);
   S->dec_qkv = (int8_t*)at(p.dec_qkv);
@@ -1032,10 +1067,18 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   // wait gives up; MNMT_SERIAL_STEPS=1 runs the steps in one stream instead.
   const char* serial = std::getenv("MNMT_SERIAL_STEPS");
   S->chain_on = !(serial && std::atoi(serial) != 0);
+  // MNMT_COUNTED=0: flags and one-word accumulators between all the 1-2 row
+  // step kernels instead of the counted hand-off (for comparison)
+  const char* counted = std::getenv("MNMT_COUNTED");
+  S->counted_on = !(counted && std::atoi(counted) == 0);
   // the encoder accumulators start at zero (each encode leaves them so), the
   // chain error word too
   hipError_t h = hipMemsetAsync(S->enc_acc, 0, enc_acc_bytes(d), S->capture_stream);
   if (h == hipSuccess) h = hipMemsetAsync(S->chain_err, 0, sizeof(int), S->capture_stream);
+  // row tags start at epoch 1, so the zeroed words never match
+  if (h == hipSuccess) h = hipMemsetAsync(S->epoch, 0, sizeof(unsigned), S->capture_stream);
+  if (h == hipSuccess)
+    h = hipMemsetAsync(S->step_x64, 0, 8 * 3 * (size_t)model->info.n_dec * 2 * d, S->capture_stream);
   if (h == hipSuccess) h = hipStreamSynchronize(S->capture_stream);
   if (h != hipSuccess) {
     mnmt_session_free(S);
@@ -1087,7 +1130,7 @@ extern "C" int mnmt_encode(mnmt_session* S, const int32_t* d_src, const int32_t*
   if ((rc = run_encoder(S, s))) return rc;
   const mnmt_model* m = S->m;
   LAUNCH(launch_greedy_reset(S->slots, B, S->cfg.max_tgt_len, S->cur_tok, S->finished, S->out_len, S->step,
-                             m->info.bos_id, S->fslots, fslots_words(m), s));
+                             m->info.bos_id, S->fslots, fslots_words(m), S->epoch, s));
   S->encoded = true;
   S->host_step = 0;
   return MNMT_OK;
