@@ -220,7 +220,9 @@ int mnmt_decode_step(mnmt_session* session, const int32_t* d_prev, int32_t* d_ne
  * exactly max_steps steps.
  * Batch-1 greedy searches (and encoders of at most 64 rows) run as a chain of
  * kernels alternating between `stream` and a second session stream, each
- * kernel waiting in a bounded spin on its predecessor's flags: the chain
+ * kernel waiting in a bounded spin on its predecessor's flags or partial
+ * sums (a decoder step is one launch per layer, its attention and FFN blocks
+ * handing off the same way inside it, then the output projection): the chain
  * needs the two streams' kernels to run concurrently, which a tool that
  * serializes dispatches prevents (set MNMT_SERIAL_STEPS=1 in the environment
  * before creating the session to run them in one stream).  A wait that gives

@@ -1,6 +1,7 @@
 // decode_step.hip -- the decoder step for at most 2 rows (the batch-1 latency
-// path) in 3 kernels per decoder layer plus the output projection and the
-// commit, instead of one kernel per operation:
+// path) in 3 block roles per decoder layer plus the output projection and the
+// commit, instead of one kernel per operation.  The roles run as one launch
+// per layer (k_step_layer) or as three kernels:
 //   k_step_attn<SELF> (one block per head):
 //       [pending residual update + LayerNorm + quantization of the rows]
 //       -> the head's rows of Q (and K, V) -> [append K, V to the int8 cache]
@@ -129,21 +130,21 @@ __device__ __forceinline__ void poll_row_data(const StepIn& in, int r, int d, Ro
 // with out_tag for the counted hand-off), and the int8 codes in a_lds + r * d.
 template <int NJ>
 __device__ __forceinline__ void finish_row(const StepIn& in, int r, int d, RowRegs<NJ>& q, int8_t* a_lds,
-                                           unsigned out_tag = 0) {
+                                           unsigned out_tag, int bid) {
   const int lane = threadIdx.x & 63;
   float v[NJ];
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
     v[j] = in.update ? fmaf(in.gamma, q.x[j], fmaf((float)q.a[j], q.sc[j], q.bi[j])) : q.x[j];
   if (in.ln_mode == 1) ln_row<NJ>(v, q.g, q.b, d, in.eps);  // post-LN: normalize the residual stream
-  if (blockIdx.x == 0 && in.x_out) {
+  if (bid == 0 && in.x_out) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int i = lane + 64 * j;
       if (i < d) chain_store(in.x_out + (size_t)r * d + i, v[j]);
     }
   }
-  if (blockIdx.x == 0 && in.cnt.x_out64) {
+  if (bid == 0 && in.cnt.x_out64) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int i = lane + 64 * j;
@@ -162,16 +163,16 @@ constexpr int kStepThreads = 256;  // block size of every step kernel
 
 // (The loop stride is the compile-time block size: reading blockDim.x loads
 // the dispatch packet and waits for every load issued before it.)
-__device__ __forceinline__ void clear_acc(const StepIn& in) {
-  if (blockIdx.x == 0 && in.zero_acc)
+__device__ __forceinline__ void clear_acc(const StepIn& in, int bid) {
+  if (bid == 0 && in.zero_acc)
     for (int i = threadIdx.x; i < in.zero_n; i += kStepThreads) chain_store(in.zero_acc + i, 0ull);
 }
 
 // Before block 0 adds its partial sums: its clear of an accumulator must have
 // landed, since the next kernel's counted poll (not a flag stored after a
 // full wait) is all that orders that accumulator's next producer after it.
-__device__ __forceinline__ void clear_done(const StepIn& in) {
-  if (blockIdx.x == 0 && in.zero_acc) __builtin_amdgcn_s_waitcnt(0);
+__device__ __forceinline__ void clear_done(const StepIn& in, int bid) {
+  if (bid == 0 && in.zero_acc) __builtin_amdgcn_s_waitcnt(0);
 }
 
 // The projections run on v_mfma_i32_16x16x64_i8 even though only R <= 2 of
@@ -186,8 +187,10 @@ __device__ __forceinline__ void clear_done(const StepIn& in) {
 // lane (n <= 64 NI).  MODE 1 (self, layer 0): the input rows are the
 // embeddings of the previous step's arg-max tokens, found from cm's partials;
 // MODE 2 (cross, layer 0): block 0 records those tokens.
+// The attention step of block `bid` (head bid); the kernel's chain signal is
+// left to the caller.
 template <int DMAX, bool SELF, int NI, int MODE, bool W4>
-__global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn at, StepCommit cm) {
+__device__ __forceinline__ void step_attn_body(const StepIn& in, const StepAttn& at, const StepCommit& cm, int bid) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;      // 64-deep K steps of the projection
   constexpr int TPW = SELF ? 3 : 1;  // 16-row projection tiles per wave (12 or 4 per head)
@@ -197,7 +200,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   __shared__ __attribute__((aligned(16))) int8_t qkv[3][kStepRows][kStepHeadDim];
   __shared__ __attribute__((aligned(16))) int8_t ctx[kStepRows][kStepHeadDim];
   __shared__ AttnLdsT<64 * NI, kStepHeadDim> att[kStepRows];
-  const int hd = blockIdx.x;
+  const int hd = bid;
   const int R = at.R, d = DMAX, dh = at.dh, nc = dh / 16, ks = d / 64;  // DMAX is the exact width
   const int ntile = (SELF ? 3 : 1) * dh / 16;  // projection tiles of this head
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -300,8 +303,8 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
     }
   }
   // 2. the rows
-  clear_acc(in);
-  if (wave < R) finish_row(in, wave, d, rr, a_lds, otag);
+  clear_acc(in, bid);
+  if (wave < R) finish_row(in, wave, d, rr, a_lds, otag, bid);
 
   lds_barrier();
   // 3. Q (K, V) of the head on the matrix cores, requantized into LDS
@@ -409,7 +412,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
   lds_barrier();
   // 5. this head's share of the output projection (K = dh), exact int32
   //    partial sums added to the accumulator
-  clear_done(in);
+  clear_done(in, bid);
   {
     const int crow = l16 < R ? l16 : 0;
     const v4i cf = kq < nc ? *(const v4i*)(ctx[crow] + 16 * kq) : v4i{0, 0, 0, 0};
@@ -425,7 +428,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
       }
     }
   }
-  if (MODE == 2 && blockIdx.x == 0) {
+  if (MODE == 2 && bid == 0) {
     // step t - 1's token (off the critical path, at the end): output, end of
     // sentence, current token, step counter
     unsigned long long key = pk[0];
@@ -445,6 +448,11 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
       if (wave == 0) chain_store(cm.step, cm.t);
     }
   }
+}
+
+template <int DMAX, bool SELF, int NI, int MODE, bool W4>
+__global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn at, StepCommit cm) {
+  step_attn_body<DMAX, SELF, NI, MODE, W4>(in, at, cm, blockIdx.x);
   chain_signal(in.chain);
 }
 
@@ -452,7 +460,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_attn(StepIn in, StepAttn 
 // requantization of the chunk, then the chunk's W2 columns (K = 64) into the
 // int32 accumulator.
 template <int DMAX, bool W4>
-__global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f) {
+__device__ __forceinline__ void step_ffn_body(const StepIn& in, const StepFfn& f, int bid) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;
   constexpr int OT = DMAX / 64;
@@ -460,7 +468,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
   __shared__ __attribute__((aligned(16))) int8_t h[kStepRows][kFfnChunk];
   const int R = f.R, d = DMAX, F = f.F, ks = d / 64;  // DMAX is the exact width
-  const int f0 = blockIdx.x * kFfnChunk;
+  const int f0 = bid * kFfnChunk;
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
   const size_t hrow = (size_t)min(f0 + 16 * wave + l16, F - 1);
@@ -486,8 +494,8 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
   } else {
     load_row_data(in, min(wave, R - 1), d, rr);
   }
-  clear_acc(in);
-  if (wave < R) finish_row(in, wave, d, rr, a_lds, otag);
+  clear_acc(in, bid);
+  if (wave < R) finish_row(in, wave, d, rr, a_lds, otag, bid);
   lds_barrier();
   {
     const int arow = l16 < R ? l16 : 0;
@@ -501,7 +509,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
         if (m < R) h[m][16 * wave + lane] = code_of(fmaxf(fmaf((float)acc[m], e_sc, e_bi), 0.0f));
   }
   lds_barrier();
-  clear_done(in);
+  clear_done(in, bid);
   {
     const int hr = l16 < R ? l16 : 0;
     const v4i hf = *(const v4i*)(h[hr] + 16 * kq);
@@ -517,7 +525,34 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
       }
     }
   }
+}
+
+template <int DMAX, bool W4>
+__global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f) {
+  step_ffn_body<DMAX, W4>(in, f, blockIdx.x);
   chain_signal(in.chain);
+}
+
+// One decoder layer of the step in one launch: blocks [0, heads) run the
+// self-attention step (head = block), blocks [heads, 2 heads) the
+// cross-attention step, the rest the FFN chunks; the phases hand off through
+// the counted words inside the launch, exactly as separate kernels would.  A
+// layer costs one kernel node instead of three (the decode graph shrinks by
+// two thirds).  FOLD: the first layer of a folded step (the self-attention
+// blocks embed the previous step's token, the first cross-attention block
+// records it).
+template <int DMAX, int NIS, int NIC, bool FOLD, bool W4>
+__global__ __launch_bounds__(kStepThreads) void k_step_layer(StepIn ia, StepAttn sa, StepIn ib, StepAttn ca,
+                                                             StepIn ic, StepFfn f, StepCommit cm) {
+  const int heads = sa.d / sa.dh;
+  const int b = blockIdx.x;
+  if (b < heads)
+    step_attn_body<DMAX, true, NIS, FOLD ? 1 : 0, W4>(ia, sa, cm, b);
+  else if (b < 2 * heads)
+    step_attn_body<DMAX, false, NIC, FOLD ? 2 : 0, W4>(ib, ca, cm, b - heads);
+  else
+    step_ffn_body<DMAX, W4>(ic, f, b - 2 * heads);
+  chain_signal(ic.chain);  // every block (when the next kernel waits on flags)
 }
 
 // Output projection over the shared embedding with the fused arg-max: each
@@ -564,8 +599,8 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     load_row_data(in, min(wave, R - 1), d, rr);
   }
   if (!RAW) {
-    clear_acc(in);
-    if (wave < R) finish_row(in, wave, d, rr, a_lds);
+    clear_acc(in, blockIdx.x);
+    if (wave < R) finish_row(in, wave, d, rr, a_lds, 0u, blockIdx.x);
   } else if (wave < R && lane < d / 16) {
     *(v4i*)(a_lds + wave * d + 16 * lane) = xr;
   }
@@ -688,6 +723,47 @@ hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int 
 #undef MNMT_ATTN
 #undef MNMT_ATTN_NI
 #undef MNMT_ATTN_W
+  return hipGetLastError();
+}
+
+int step_layer_blocks(int heads, int F) { return 2 * heads + F / kFfnChunk; }
+
+hipError_t launch_step_layer(const StepIn& ia, const StepAttn& sa, const StepIn& ib, const StepAttn& ca,
+                             const StepIn& ic, const StepFfn& f, hipStream_t s, const StepCommit* cm) {
+  const int heads = sa.d / sa.dh;
+  if (sa.w4 != ca.w4 || sa.w4 != f.w4) return hipErrorInvalidValue;  // one weight form per launch
+  if (!sa.W || !sa.Wo || !ca.W || !ca.Wo || !f.W1 || !f.W2) return hipErrorInvalidValue;
+  if (cm && (cm->nslots < 1 || cm->nslots > 256 || cm->t < 1)) return hipErrorInvalidValue;
+  const StepCommit c = cm ? *cm : StepCommit{};
+  const int blocks = step_layer_blocks(heads, f.F);
+  const int ns = sa.t + 1 <= 64 ? 1 : 2, nc = ca.S <= 64 ? 1 : 2;
+#define MNMT_LAYER_K(DM, NS, NC, FO, W)                                                                       \
+  hipLaunchKernelGGL((k_step_layer<DM, NS, NC, FO, W>), dim3(blocks), dim3(kStepThreads), 0, s, ia, sa, ib, ca, \
+                     ic, f, c)
+#define MNMT_LAYER_W(DM, NS, NC, FO)               \
+  if (sa.w4) MNMT_LAYER_K(DM, NS, NC, FO, true);   \
+  else MNMT_LAYER_K(DM, NS, NC, FO, false);
+#define MNMT_LAYER_F(DM, NS, NC)       \
+  if (cm) {                            \
+    MNMT_LAYER_W(DM, NS, NC, true)     \
+  } else {                             \
+    MNMT_LAYER_W(DM, NS, NC, false)    \
+  }
+#define MNMT_LAYER(DM)                                              \
+  if (ns == 1 && nc == 1) {                                         \
+    MNMT_LAYER_F(DM, 1, 1)                                          \
+  } else if (ns == 1) {                                             \
+    MNMT_LAYER_F(DM, 1, 2)                                          \
+  } else if (nc == 1) {                                             \
+    MNMT_LAYER_F(DM, 2, 1)                                          \
+  } else {                                                          \
+    MNMT_LAYER_F(DM, 2, 2)                                          \
+  }
+  MNMT_BY_D(sa.d, MNMT_LAYER)
+#undef MNMT_LAYER
+#undef MNMT_LAYER_F
+#undef MNMT_LAYER_W
+#undef MNMT_LAYER_K
   return hipGetLastError();
 }
 

@@ -287,6 +287,13 @@ int step_logits_blocks_chained(int V, int d);  // the same in a kernel chain (mo
 hipError_t launch_step_attn(const StepIn& in, const StepAttn& at, int self, int heads, hipStream_t s,
                             const StepCommit* cm = nullptr);
 hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s);
+// One whole decoder layer (self attention, cross attention, FFN) in one
+// launch of step_layer_blocks(heads, F) blocks, the phases handing off through
+// the counted words (ib and ic take counted input); cm: the folded commit of
+// the first layer (as launch_step_attn).  ic.chain carries the launch's flags.
+int step_layer_blocks(int heads, int F);
+hipError_t launch_step_layer(const StepIn& ia, const StepAttn& sa, const StepIn& ib, const StepAttn& ca,
+                             const StepIn& ic, const StepFfn& f, hipStream_t s, const StepCommit* cm = nullptr);
 // With ev_start / ev_stop the events take the kernel's own start and end times.
 hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s, hipEvent_t ev_start = nullptr,
                               hipEvent_t ev_stop = nullptr);
@@ -537,6 +544,7 @@ struct mnmt_session {
   unsigned* epoch = nullptr;          // translation counter of the counted hand-off's row tags
   unsigned long long* step_x64 = nullptr;  // tagged rows of the step kernels [3 n_dec][2][d]
   bool counted_on = true;             // off with MNMT_COUNTED=0: flags between all step kernels
+  bool merged_on = true;              // off with MNMT_MERGED_LAYERS=0: three launches per decoder layer
   bool chain_on = true;               // off with MNMT_SERIAL_STEPS=1 in the environment
   std::map<std::string, hipGraphExec_t> graphs;
 };

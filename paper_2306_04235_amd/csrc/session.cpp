@@ -739,9 +739,17 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     cm.eos = m->info.eos_id;
     cm.pad = m->info.pad_id;
   }
+  // merged: each layer's three phases in one launch (launch_step_layer), the
+  // phases handing off through the counted words inside it
+  // (the logits kernel's 256 threads poll one flag word per block of the
+  // last layer's launch)
+  const bool merged = S->merged_on && counted && step_layer_blocks(h, m->info.d_ffn) <= 256;
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
     const StepCommit* cml = folded && l == 0 ? &cm : nullptr;
+    StepIn ia{}, ib{}, ic{};
+    StepAttn sa{}, ca{};
+    StepFfn f{};
     {  // self-attention block
       StepIn in = base(L.qkv.inv_in);
       if (l == 0) {
@@ -758,9 +766,15 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       StepAttn at = attn(L, true, acc_o);
       at.kcache = S->kcache[l];
       at.vcache = S->vcache[l];
-      const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l, h, t + 1) : s;
-      count_io(in, 3 * (int)l, h);
-      LAUNCH(launch_step_attn(in, at, 1, h, ks, cml));
+      if (merged) {
+        count_io(in, 3 * (int)l, h);
+        ia = in;
+        sa = at;
+      } else {
+        const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l, h, t + 1) : s;
+        count_io(in, 3 * (int)l, h);
+        LAUNCH(launch_step_attn(in, at, 1, h, ks, cml));
+      }
       if (in.x_out) std::swap(xa, xb);
     }
     {  // cross-attention block
@@ -770,9 +784,15 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       in.zero_n = nacc;
       StepAttn at = attn(L, false, acc_oc);
       at.kv = S->cross_kv[l];
-      const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 1, h, t + 1) : s;
-      count_io(in, 3 * (int)l + 1, h);
-      LAUNCH(launch_step_attn(in, at, 0, h, ks, cml));
+      if (merged) {
+        count_io(in, 3 * (int)l + 1, h);
+        ib = in;
+        ca = at;
+      } else {
+        const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 1, h, t + 1) : s;
+        count_io(in, 3 * (int)l + 1, h);
+        LAUNCH(launch_step_attn(in, at, 0, h, ks, cml));
+      }
       std::swap(xa, xb);
     }
     {  // FFN block
@@ -780,7 +800,6 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       rows(in, acc_oc, &L.co, L.ca_gamma, L.ca_ln, L.ff_ln);
       in.zero_acc = acc_o;
       in.zero_n = nacc;
-      StepFfn f{};
       f.R = R;
       f.d = d;
       f.F = L.w1.N;
@@ -788,10 +807,38 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       f.scale1 = L.w1.scale;
       f.bias1 = L.w1.bias;
       f.acc_out = acc_w2;
-      const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 2, f.F / 64, t + 1) : s;
-      count_io(in, 3 * (int)l + 2, f.F / 64);
-      LAUNCH(launch_step_ffn(in, f, ks));
+      if (merged) {
+        count_io(in, 3 * (int)l + 2, f.F / 64);
+        ic = in;
+      } else {
+        const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l + 2, f.F / 64, t + 1) : s;
+        count_io(in, 3 * (int)l + 2, f.F / 64);
+        LAUNCH(launch_step_ffn(in, f, ks));
+      }
       std::swap(xa, xb);
+    }
+    if (merged) {
+      // the launch's chain: in the first layer the self- and cross-attention
+      // blocks wait on the previous kernel's flags (the cross blocks of a
+      // folded step read the previous step's arg-max partials, which only
+      // that wait orders after the logits kernel that writes them; as
+      // separate kernels, stream order did); every block of the last layer
+      // flags its end for the logits kernel (the next layer instead polls the
+      // counted words); polls that give up report through err
+      const bool last = l + 1 == m->dec.size();
+      StepChain c{};
+      const hipStream_t ks = ch ? ch->next(c, 3 * (int)l, step_layer_blocks(h, L.w1.N), t + 1, last) : s;
+      if (l == 0) {
+        for (StepIn* p : {&ia, &ib}) {
+          p->chain.wait = c.wait;
+          p->chain.nwait = c.nwait;
+          p->chain.want = c.want;
+        }
+      }
+      ia.chain.err = ib.chain.err = ic.chain.err = c.err;
+      ic.chain.done = c.done;
+      ic.chain.val = c.val;
+      LAUNCH(launch_step_layer(ia, sa, ib, ca, ic, f, ks, cml));
     }
   }
   const LayerDev& last = m->dec.back();
@@ -1071,6 +1118,10 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   // step kernels instead of the counted hand-off (for comparison)
   const char* counted = std::getenv("MNMT_COUNTED");
   S->counted_on = !(counted && std::atoi(counted) == 0);
+  // MNMT_MERGED_LAYERS=0: three launches per decoder layer of the 1-2 row
+  // step instead of one (for comparison)
+  const char* merged = std::getenv("MNMT_MERGED_LAYERS");
+  S->merged_on = !(merged && std::atoi(merged) == 0);
   // the encoder accumulators start at zero (each encode leaves them so), the
   // chain error word too
   hipError_t h = hipMemsetAsync(S->enc_acc, 0, enc_acc_bytes(d), S->capture_stream);

@@ -222,6 +222,61 @@ def test_kernel_chain_many_sentences(torch_dev, monkeypatch):
         assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), f"sentence {k}"
 
 
+@pytest.mark.parametrize("merged", ["1", "0"])
+def test_layer_launch_forms(torch_dev, monkeypatch, merged):
+    """Each decoder layer of the batch-1 step is one launch whose
+    self-attention, cross-attention and FFN blocks hand off through the
+    counted words inside it, or with MNMT_MERGED_LAYERS=0 (read at session
+    creation) three launches.  Per-step logits bits and tokens equal the
+    oracle's at one and two rows, pre- and post-LN, with 4-bit weights, shared
+    layers and widths 64-512, eager and in graph replays."""
+    import dataclasses
+
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    monkeypatch.setenv("MNMT_MERGED_LAYERS", merged)
+    src, lens = G.workload_inputs(G.WORKLOADS["mobile"])
+    _greedy_check(torch, dev, "MOBILE", src, lens, 30)
+    mob4 = dataclasses.replace(G.MOBILE, name="mobile-w4", w_bits=4)
+    _greedy_check(torch, dev, mob4, src, lens, 30, flags=mnmt.LOAD_PACKED_4BIT_ONLY)
+    for cfg, B, n, seed in ((SMALL_POST, 2, [9, 4], 121), (DIVERSE, 2, [14, 11], 122), (SHARED, 1, [12], 123),
+                            (WIDE512, 1, [20], 124), (WIDE384, 2, [25, 19], 125), (VARIED, 2, [30, 21], 126)):
+        src, lens = G.make_sources(cfg.vocab, B, n, seed=seed, s_max=max(n))
+        _greedy_check(torch, dev, cfg, src, lens, 12)
+
+
+def test_merged_layers_many_sentences(torch_dev, monkeypatch):
+    """Two dozen batch-1 sentences in graph replays through the merged layer
+    launches against the three-kernel layers (both on the counted hand-off),
+    the first four also against the oracle."""
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    om, gm = _pair("MOBILE")
+    rng = np.random.default_rng(2025)
+    lens_all = rng.integers(10, 31, 24)
+    outs = {}
+    for merged in ("1", "0"):
+        monkeypatch.setenv("MNMT_MERGED_LAYERS", merged)
+        sess = mnmt.Session(gm, 1, 30, 30, 1)
+        got = []
+        for k, n in enumerate(lens_all):
+            src, lens = G.make_sources(G.MOBILE.vocab, 1, [int(n)], seed=700 + k, s_max=30)
+            out, out_len, _ = sess.translate(_t(torch, dev, src), _t(torch, dev, lens), beam=1, max_steps=30,
+                                             use_graph=True)
+            torch.cuda.synchronize()
+            got.append((out.cpu().numpy().copy(), out_len.cpu().numpy().copy()))
+            if merged == "1" and k < 4:
+                o_out, o_len = om.greedy(src, lens, 30)[:2]
+                assert np.array_equal(got[-1][0], o_out) and np.array_equal(got[-1][1], o_len), f"sentence {k}"
+        assert int(sess.tensor("chain_err", torch.int32, (1,)).cpu().numpy()[0]) == 0
+        sess.close()
+        outs[merged] = got
+    for k, (a, b) in enumerate(zip(outs["0"], outs["1"])):
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), f"sentence {k}"
+
+
 WIDE384 = G.ModelConfig("wide-384", 384, 6, 768, 2, 1, 600, ln_post=0, seed=83, random_gamma=True, weight_std=0.05)
 WIDE512 = G.ModelConfig("wide-512", 512, 8, 1024, 2, 1, 600, ln_post=0, seed=84, random_gamma=True, weight_std=0.05)
 
