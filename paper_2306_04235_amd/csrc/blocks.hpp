@@ -207,12 +207,26 @@ __host__ __device__ constexpr int lanes_per_row(int dmax) {
   return dmax >= 1024 ? 64 : dmax >= 512 ? 32 : dmax >= 256 ? 16 : dmax >= 128 ? 8 : 4;
 }
 
+// Every global load is unconditional, with clamped indexes (rows past `rows`
+// read row row0, elements past d read element d - 1; neither is used), and
+// the LayerNorm's gain and bias are loaded once before the rows: a load under
+// a lane condition makes the compiler wait for it where the paths join, which
+// would turn the loads of a row group into one memory round trip each.
 template <int NJ>  // d <= 64 * NJ
 __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int row0, int d, int t, int8_t* a_lds,
                                              int lds_stride, bool writer) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   writer = writer && in.x_out != nullptr;
   const int n = (d + 63) / 64;
+  float gj[NJ], bj[NJ];
+  if (in.do_ln) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = min(lane + 64 * j, d - 1);
+      gj[j] = in.g[i];
+      bj[j] = in.b[i];
+    }
+  }
   for (int r0 = wave; r0 < rows; r0 += 4 * kPrepGroup) {
     float v[kPrepGroup][NJ];
 #pragma unroll
@@ -226,16 +240,12 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
         const float c = in.c_emb[tok];
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
-          const int i = lane + 64 * j;
-          v[g][j] = (r < rows && j < n && i < d) ? fmaf((float)in.E[(size_t)tok * d + i], c, in.pe[(size_t)pos * d + i])
-                                                 : 0.0f;
+          const int i = min(lane + 64 * j, d - 1);
+          v[g][j] = fmaf((float)in.E[(size_t)tok * d + i], c, in.pe[(size_t)pos * d + i]);
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-          const int i = lane + 64 * j;
-          v[g][j] = (r < rows && j < n && i < d) ? in.x[gr * d + i] : 0.0f;
-        }
+        for (int j = 0; j < NJ; ++j) v[g][j] = in.x[gr * d + min(lane + 64 * j, d - 1)];
       }
     }
     if (writer && in.wb_input) {
@@ -287,10 +297,8 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
         const float var = p2[g] * inv_d;
         const float rstd = 1.0f / sqrtf(var + in.eps);
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-          const int i = lane + 64 * j;
-          if (j < n && i < d) v[g][j] = fmaf(v[g][j] * rstd, in.g[i], in.b[i]);
-        }
+        for (int j = 0; j < NJ; ++j)
+          if (j < n && lane + 64 * j < d) v[g][j] = fmaf(v[g][j] * rstd, gj[j], bj[j]);
       }
     }
 #pragma unroll

@@ -56,16 +56,25 @@ __global__ __launch_bounds__(256) void k_embed_proj(const int32_t* __restrict__ 
 // (canonical order).  ln_quant_wave normalizes v in place (when do_ln) and
 // stores the codes (q_row) and the normalized row (x_out_row), either may be
 // null.
-__device__ __forceinline__ void ln_quant_wave(float (&v)[kMaxRowLen / 64], int d, int do_ln,
-                                              const float* __restrict__ g, const float* __restrict__ b, float eps,
-                                              float inv_s, int8_t* __restrict__ q_row,
-                                              float* __restrict__ x_out_row) {
+// The LayerNorm's gain and bias are loaded (clamped indexes, unconditional)
+// before the reductions, so they arrive while the sums run.
+template <int NJ>
+__device__ __forceinline__ void ln_quant_wave(float (&v)[NJ], int d, int do_ln, const float* __restrict__ g,
+                                              const float* __restrict__ b, float eps, float inv_s,
+                                              int8_t* __restrict__ q_row, float* __restrict__ x_out_row) {
   const int lane = threadIdx.x & 63;
   const int n = (d + 63) / 64;
   if (do_ln) {
+    float gj[NJ], bj[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int i = min(lane + 64 * j, d - 1);
+      gj[j] = g[i];
+      bj[j] = b[i];
+    }
     float p = 0.0f;
 #pragma unroll
-    for (int j = 0; j < kMaxRowLen / 64; ++j) {
+    for (int j = 0; j < NJ; ++j) {
       const int i = lane + 64 * j;
       if (j < n && i < d) p = p + v[j];
     }
@@ -73,7 +82,7 @@ __device__ __forceinline__ void ln_quant_wave(float (&v)[kMaxRowLen / 64], int d
     const float mu = wave_sum(p) * inv_d;
     float p2 = 0.0f;
 #pragma unroll
-    for (int j = 0; j < kMaxRowLen / 64; ++j) {
+    for (int j = 0; j < NJ; ++j) {
       const int i = lane + 64 * j;
       if (j < n && i < d) {
         v[j] = v[j] - mu;
@@ -83,13 +92,13 @@ __device__ __forceinline__ void ln_quant_wave(float (&v)[kMaxRowLen / 64], int d
     const float var = wave_sum(p2) * inv_d;
     const float rstd = 1.0f / sqrtf(var + eps);
 #pragma unroll
-    for (int j = 0; j < kMaxRowLen / 64; ++j) {
+    for (int j = 0; j < NJ; ++j) {
       const int i = lane + 64 * j;
-      if (j < n && i < d) v[j] = fmaf(v[j] * rstd, g[i], b[i]);
+      if (j < n && i < d) v[j] = fmaf(v[j] * rstd, gj[j], bj[j]);
     }
   }
 #pragma unroll
-  for (int j = 0; j < kMaxRowLen / 64; ++j) {
+  for (int j = 0; j < NJ; ++j) {
     const int i = lane + 64 * j;
     if (j < n && i < d) {
       if (q_row) q_row[i] = code_of(v[j] * inv_s);
@@ -98,6 +107,8 @@ __device__ __forceinline__ void ln_quant_wave(float (&v)[kMaxRowLen / 64], int d
   }
 }
 
+// NJ = row_class(d) / 64; the row's loads are unconditional (clamped index).
+template <int NJ>
 __global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, int rows, int d, int do_ln,
                                                   const float* __restrict__ g, const float* __restrict__ b,
                                                   float eps, float inv_s, int8_t* __restrict__ q,
@@ -106,15 +117,11 @@ __global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, i
   const int lane = threadIdx.x & 63;
   if (r >= rows) return;
   const float* xr = x + (size_t)r * d;
-  float v[kMaxRowLen / 64];
-  const int n = (d + 63) / 64;
+  float v[NJ];
 #pragma unroll
-  for (int j = 0; j < kMaxRowLen / 64; ++j) {
-    const int i = lane + 64 * j;
-    if (j < n && i < d) v[j] = xr[i];
-  }
-  ln_quant_wave(v, d, do_ln, g, b, eps, inv_s, q ? q + (size_t)r * d : nullptr,
-                x_out ? x_out + (size_t)r * d : nullptr);
+  for (int j = 0; j < NJ; ++j) v[j] = xr[min(lane + 64 * j, d - 1)];
+  ln_quant_wave<NJ>(v, d, do_ln, g, b, eps, inv_s, q ? q + (size_t)r * d : nullptr,
+                    x_out ? x_out + (size_t)r * d : nullptr);
 }
 
 // Encoder self-attention: block = one wave = (query s, head hd, sentence b).
@@ -844,8 +851,18 @@ hipError_t launch_ln_quant(const float* x, int rows, int d, int do_ln, const flo
                            float inv_s, int8_t* q, float* x_out, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (d > kMaxRowLen) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_ln_quant, dim3((rows + 3) / 4), dim3(256), 0, s, x, rows, d, do_ln, g, b, eps, inv_s, q,
-                     x_out);
+  const dim3 grid((rows + 3) / 4);
+#define MNMT_LNQ(NJ) \
+  hipLaunchKernelGGL(k_ln_quant<NJ>, grid, dim3(256), 0, s, x, rows, d, do_ln, g, b, eps, inv_s, q, x_out)
+  switch (row_class(d)) {
+    case 64: MNMT_LNQ(1); break;
+    case 128: MNMT_LNQ(2); break;
+    case 256: MNMT_LNQ(4); break;
+    case 384: MNMT_LNQ(6); break;
+    case 512: MNMT_LNQ(8); break;
+    default: MNMT_LNQ(16); break;
+  }
+#undef MNMT_LNQ
   return hipGetLastError();
 }
 

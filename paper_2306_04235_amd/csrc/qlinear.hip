@@ -22,6 +22,31 @@ namespace mnmt {
 namespace {
 
 
+// The epilogue operands of one lane's column (and, for the residual, of its
+// rows), loaded before the matrix product so that they arrive with the
+// operands instead of one round trip after it.
+struct EpiPre {
+  float sc = 0.0f, bi = 0.0f;
+  float y[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+};
+
+// Whether epilogue kind k is one that epilogue_pre handles.
+__device__ __forceinline__ bool epi_pre_kind(int k) {
+  return k == MNMT_EPI_I8 || k == MNMT_EPI_I8_RELU || k == MNMT_EPI_F32_RESID;
+}
+
+// The same expressions as epilogue_store, from the preloaded operands.
+__device__ __forceinline__ void epilogue_pre(const EpiArgs& e, int m, int n, int acc, const EpiPre& p, int i) {
+  const float a = (float)acc;
+  const size_t o = (size_t)m * e.ldo + n;
+  if (e.kind == MNMT_EPI_I8)
+    ((int8_t*)e.out)[o] = code_of(fmaf(a, p.sc, p.bi));
+  else if (e.kind == MNMT_EPI_I8_RELU)
+    ((int8_t*)e.out)[o] = code_of(fmaxf(fmaf(a, p.sc, p.bi), 0.0f));
+  else
+    ((float*)e.out)[o] = fmaf(e.gamma, p.y[i], fmaf(a, p.sc, p.bi));
+}
+
 // The fused epilogue of one output element (row m, column n).
 __device__ __forceinline__ void epilogue_store(const EpiArgs& e, int m, int n, int acc, const float* scale,
                                                const float* bias) {
@@ -186,6 +211,21 @@ __global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const in
   for (int kk = 0; kk < NK; ++kk)
     bf[kk] = (kk < nk && col < N) ? *(const v4i*)(W + (size_t)col * K + kk * 64 + koff) : v4i{0, 0, 0, 0};
   const int arow = m0 + 16 * wm + (lane & 15);
+  // the epilogue's operands (clamped indexes, unused past M or N)
+  EpiPre pre;
+  const bool pre_ok = epi_pre_kind(e.kind);
+  if (pre_ok) {
+    const int cc = col < N ? col : N - 1;
+    pre.sc = scale[cc];
+    pre.bi = bias[cc];
+    if (e.kind == MNMT_EPI_F32_RESID) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = m0 + 16 * wm + 4 * (lane >> 4) + i;
+        pre.y[i] = ((const float*)e.out)[(size_t)(row < M ? row : M - 1) * e.ldo + cc];
+      }
+    }
+  }
   v4i acc = {0, 0, 0, 0};
   if (LN) {
     const int KP = K + 16;
@@ -213,7 +253,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const in
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = m0 + 16 * wm + 4 * (lane >> 4) + i;
-    if (row < M && col < N) epilogue_store(e, row, col, acc[i], scale, bias);
+    if (row < M && col < N) {
+      if (pre_ok)
+        epilogue_pre(e, row, col, acc[i], pre, i);
+      else
+        epilogue_store(e, row, col, acc[i], scale, bias);
+    }
   }
 }
 

@@ -460,32 +460,40 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
   const bool post = m->info.ln_post;
   const float eps = m->info.ln_eps;
   const LayerDev& L0 = m->dec[0];
+  float* xc = S->dec_x;
   if (!rows_ready) {
     const int rc0 = embed_rows(S, S->cur_tok, R, 1, S->step, S->dec_x, s);
     if (rc0) return rc0;
     LAUNCH(launch_ln_quant(S->dec_x, R, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->dec_a, nullptr, s));
   }
+  // the linear layer L over the rows LN(x) quantized with L's input scale
+  // (post-LN: the normalized rows also replace x)
+  auto ln_linear = [&](const LinearDev& L, const LnDev& ln, int kind, void* out) -> int {
+    LAUNCH(launch_ln_quant(xc, R, d, 1, ln.g, ln.b, eps, L.inv_in, S->dec_a, post ? xc : nullptr, s));
+    return qlin(L, S->dec_a, R, kind, out, 1.f, s);
+  };
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
     int rc;
-    if ((rc = qlin(L.qkv, S->dec_a, R, MNMT_EPI_I8, S->dec_qkv, 1.f, s))) return rc;
+    if (l == 0)  // the step's input rows, quantized by the embedding step or the beam update
+      rc = qlin(L.qkv, S->dec_a, R, MNMT_EPI_I8, S->dec_qkv, 1.f, s);
+    else  // pre-LN: the layer's own LayerNorm; post-LN: the previous FFN's
+      rc = ln_linear(L.qkv, post ? m->dec[l - 1].ff_ln : L.sa_ln, MNMT_EPI_I8, S->dec_qkv);
+    if (rc) return rc;
     LAUNCH(launch_attn_dec_self(S->dec_qkv, R, d, h, T, S->step, S->kcache[l], S->vcache[l],
                                 beam ? S->beam.hist : nullptr, L.sa_cqk, L.sa_cpv, S->dec_a, s));
-    if ((rc = qlin(L.o, S->dec_a, R, MNMT_EPI_F32_RESID, S->dec_x, L.sa_gamma, s))) return rc;
-    const LnDev& lnc = post ? L.sa_ln : L.ca_ln;
-    LAUNCH(launch_ln_quant(S->dec_x, R, d, 1, lnc.g, lnc.b, eps, L.cq.inv_in, S->dec_a, post ? S->dec_x : nullptr, s));
-    if ((rc = qlin(L.cq, S->dec_a, R, MNMT_EPI_I8, S->dec_q, 1.f, s))) return rc;
+    if ((rc = qlin(L.o, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.sa_gamma, s))) return rc;
+    if ((rc = ln_linear(L.cq, post ? L.sa_ln : L.ca_ln, MNMT_EPI_I8, S->dec_q))) return rc;
     LAUNCH(launch_attn_dec_cross(S->dec_q, R, W, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, S->dec_a, s));
-    if ((rc = qlin(L.co, S->dec_a, R, MNMT_EPI_F32_RESID, S->dec_x, L.ca_gamma, s))) return rc;
-    const LnDev& lnf = post ? L.ca_ln : L.ff_ln;
-    LAUNCH(launch_ln_quant(S->dec_x, R, d, 1, lnf.g, lnf.b, eps, L.w1.inv_in, S->dec_a, post ? S->dec_x : nullptr, s));
-    if ((rc = qlin(L.w1, S->dec_a, R, MNMT_EPI_I8_RELU, S->dec_h, 1.f, s))) return rc;
-    if ((rc = qlin(L.w2, S->dec_h, R, MNMT_EPI_F32_RESID, S->dec_x, L.ff_gamma, s))) return rc;
-    const bool last = l + 1 == m->dec.size();
-    const float inv = last ? m->inv_fin : m->dec[l + 1].qkv.inv_in;
-    const LnDev& ln2 = post ? L.ff_ln : (last ? m->dec_ln : m->dec[l + 1].sa_ln);
-    LAUNCH(launch_ln_quant(S->dec_x, R, d, 1, ln2.g, ln2.b, eps, inv, S->dec_a, post ? S->dec_x : nullptr, s));
+    if ((rc = qlin(L.co, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.ca_gamma, s))) return rc;
+    if ((rc = ln_linear(L.w1, post ? L.ca_ln : L.ff_ln, MNMT_EPI_I8_RELU, S->dec_h))) return rc;
+    if ((rc = qlin(L.w2, S->dec_h, R, MNMT_EPI_F32_RESID, xc, L.ff_gamma, s))) return rc;
   }
+  // the final LayerNorm (post-LN: the last FFN's) into dec_a for the output
+  // projection
+  const LayerDev& last = m->dec.back();
+  const LnDev& lnf = post ? last.ff_ln : m->dec_ln;
+  LAUNCH(launch_ln_quant(xc, R, d, 1, lnf.g, lnf.b, eps, m->inv_fin, S->dec_a, nullptr, s));
   return MNMT_OK;
 }
 
