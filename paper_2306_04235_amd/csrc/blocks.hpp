@@ -120,72 +120,67 @@ __device__ __forceinline__ void ln_row(float (&v)[NJ], const float (&g)[NJ], con
 // LDS one wave's attention needs: softmax weights and the value rows.
 template <int NMAX, int DHMAX>
 struct AttnLdsT {
-  float p[NMAX];
+  alignas(16) float p[NMAX];
   int8_t v[NMAX][DHMAX];
 };
-using AttnLds = AttnLdsT<kMaxAttnLen, kMaxHeadDim>;
 
-// Attention of one query row over n keys for one head, by one wave (Appendix
-// A self-weight / self-sum equations with the quantizer figure's precisions):
-// int8 scores, fp32 softmax in the canonical order, context accumulated over
-// ascending key index with one fma per key, requantized.  key(t) / val(t)
-// return the head's dh codes of key / value t (global or LDS addresses).
-// Lane t loads key t and value t together, so all global loads are in flight
-// at once; weights and values are then staged in the wave's own LDS for the
-// context loop.  Only this wave synchronizes, so other waves of the block may
-// be elsewhere.
-template <int NMAX, int DHMAX, class KeyFn, class ValFn>
-__device__ __forceinline__ void attend_wave(const int8_t* __restrict__ q, int n, int dh, KeyFn key, ValFn val,
-                                            float c_qk, float c_pv, int8_t* __restrict__ out,
-                                            AttnLdsT<NMAX, DHMAX>& sh) {
+// The softmax and context of one query row for one head, by one wave
+// (Appendix A self-weight / self-sum equations with the quantizer figure's
+// precisions): sv[i] holds the scaled int8 score (float)(q . k_t) * c_qk of
+// key t = lane + 64 i (valid for t < n); fp32 softmax in the canonical order
+// (lane partials over ascending i, then the butterfly); context accumulated
+// over ascending key index with one fma per key from the values in LDS
+// (value t's codes at v + t * v_stride), requantized into out[0, dh).  p is
+// the wave's LDS row of at least n weights, 16-byte aligned.
+template <int NI>
+__device__ __forceinline__ void softmax_context(float (&sv)[NI], int n, int dh, float c_pv, float* p,
+                                                const int8_t* v, int v_stride, int8_t* __restrict__ out) {
   const int lane = threadIdx.x & 63;
-  const int nc = dh / 16;
-  int4 qv[DHMAX / 16];
-#pragma unroll
-  for (int c = 0; c < DHMAX / 16; ++c) qv[c] = c < nc ? *(const int4*)(q + 16 * c) : make_int4(0, 0, 0, 0);
-  float sv[(NMAX + 63) / 64];
   float mx = -FLT_MAX;
 #pragma unroll
-  for (int i = 0; i < (NMAX + 63) / 64; ++i) {
-    const int t = lane + 64 * i;
-    sv[i] = 0.0f;
-    if (t < n) {
-      const int8_t* kp = key(t);
-      const int8_t* vp = val(t);
-      int acc = 0;
-#pragma unroll
-      for (int c = 0; c < DHMAX / 16; ++c) {
-        if (c < nc) {
-          acc = dot16(*(const int4*)(kp + 16 * c), qv[c], acc);
-          *(int4*)&sh.v[t][16 * c] = *(const int4*)(vp + 16 * c);
-        }
-      }
-      sv[i] = (float)acc * c_qk;
-      mx = fmaxf(mx, sv[i]);
-    }
-  }
+  for (int i = 0; i < NI; ++i)
+    if (lane + 64 * i < n) mx = fmaxf(mx, sv[i]);
   mx = wave_max(mx);
   float part = 0.0f;
 #pragma unroll
-  for (int i = 0; i < (NMAX + 63) / 64; ++i) {
-    const int t = lane + 64 * i;
-    if (t < n) {
+  for (int i = 0; i < NI; ++i) {
+    if (lane + 64 * i < n) {
       sv[i] = canon_exp(sv[i] - mx);
       part = part + sv[i];
     }
   }
   const float inv = 1.0f / wave_sum(part);
 #pragma unroll
-  for (int i = 0; i < (NMAX + 63) / 64; ++i) {
+  for (int i = 0; i < NI; ++i) {
     const int t = lane + 64 * i;
-    if (t < n) sh.p[t] = sv[i] * inv;
+    if (t < n) p[t] = sv[i] * inv;
   }
-  wave_sync();  // p and v visible to every lane of this wave
+  wave_sync();  // the weights visible to every lane of this wave
+  // (8 keys per group: their weights and values are read from LDS before the
+  // group's chain of fmas, so the chain does not wait on each read)
   for (int j = lane; j < dh; j += 64) {
     float acc = 0.0f;
-    for (int t = 0; t < n; ++t) acc = fmaf(sh.p[t], (float)sh.v[t][j], acc);
+    int t = 0;
+#pragma unroll 2
+    for (; t + 8 <= n; t += 8) {
+      const float4 pa = *(const float4*)(p + t);
+      const float4 pb = *(const float4*)(p + t + 4);
+      float vv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) vv[k] = (float)v[(t + k) * v_stride + j];
+      acc = fmaf(pa.x, vv[0], acc);
+      acc = fmaf(pa.y, vv[1], acc);
+      acc = fmaf(pa.z, vv[2], acc);
+      acc = fmaf(pa.w, vv[3], acc);
+      acc = fmaf(pb.x, vv[4], acc);
+      acc = fmaf(pb.y, vv[5], acc);
+      acc = fmaf(pb.z, vv[6], acc);
+      acc = fmaf(pb.w, vv[7], acc);
+    }
+    for (; t < n; ++t) acc = fmaf(p[t], (float)v[t * v_stride + j], acc);
     out[j] = code_of(acc * c_pv);
   }
+  wave_sync();  // every lane done with p and v before the wave reuses them
 }
 
 // Input rows -> int8 rows in LDS (Section 4.2 fusion of the element-wise work

@@ -124,68 +124,172 @@ __global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, i
                     x_out ? x_out + (size_t)r * d : nullptr);
 }
 
-// Encoder self-attention: block = one wave = (query s, head hd, sentence b).
-__global__ __launch_bounds__(64) void k_attn_enc(const int8_t* __restrict__ qkv, const int32_t* __restrict__ len,
-                                                 int S, int d, int dh, float c_qk, float c_pv,
-                                                 int8_t* __restrict__ ctx) {
-  __shared__ AttnLds sh;
-  const int s = blockIdx.x, hd = blockIdx.y, b = blockIdx.z;
-  int n = len[b];
-  n = n < 1 ? 1 : (n > S ? S : n);
-  const int8_t* base = qkv + (size_t)b * S * 3 * d;
-  const int8_t* q = base + (size_t)s * 3 * d + hd * dh;
-  auto key = [&](int t) { return base + (size_t)t * 3 * d + d + hd * dh; };
-  auto val = [&](int t) { return base + (size_t)t * 3 * d + 2 * d + hd * dh; };
-  attend_wave(q, n, dh, key, val, c_qk, c_pv, ctx + ((size_t)b * S + s) * d + hd * dh, sh);
+__device__ __forceinline__ int dot16v(const v4i a, const v4i b, int acc) {
+  acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.z, b.z, acc, false);
+  acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
+  return acc;
 }
 
-// Decoder self-attention at position t = *step: block = one wave = (head, row).
-__global__ __launch_bounds__(64) void k_attn_dec_self(const int8_t* __restrict__ qkv, int d, int dh, int T,
-                                                      const int* __restrict__ step, int8_t* __restrict__ kcache,
-                                                      int8_t* __restrict__ vcache, const int32_t* __restrict__ hist,
-                                                      float c_qk, float c_pv, int8_t* __restrict__ ctx) {
-  __shared__ AttnLds sh;
-  const int hd = blockIdx.x, r = blockIdx.y;
-  const int lane = threadIdx.x;
+// Attention for query rows that share one key/value set (the rows of one
+// sentence in the encoder, the W hypotheses of one sentence over its source
+// in the decoder's cross attention).  Block = (head, group): the block stages
+// the group's keys and values of the head in LDS once (16-byte loads over all
+// threads, issued together: positions and chunks past the valid ones repeat
+// the last valid one and are never used), then each wave attends for its
+// query rows, loading the next row's query while it works on the current one.
+struct SharedAttn {
+  const int8_t* q;       // query row r of the head at q + r * ldq + head * dh
+  int ldq;
+  int rows;              // query rows per group (row r = group * rows + i)
+  const int8_t* kv;      // group g's key t of the head at kv + g * kv_group + k_off + t * ldkv + head * dh
+  size_t kv_group;
+  int ldkv, k_off, v_off;
+  const int32_t* len;    // valid keys of group g: len[g] clamped to [1, S]
+  int S, d, dh;
+  float c_qk, c_pv;
+  int8_t* ctx;           // context row r at ctx + r * d + head * dh
+};
+
+template <int NMAX, int DHMAX, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_attn_shared(SharedAttn a) {
+  constexpr int DHC = DHMAX / 16, KS = DHMAX + 16, NI = NMAX / 64;
+  constexpr int CH = NMAX * DHC, PER = (CH + 64 * WAVES - 1) / (64 * WAVES);
+  __shared__ __attribute__((aligned(16))) int8_t kl[NMAX * KS];
+  __shared__ __attribute__((aligned(16))) int8_t vl[NMAX * DHMAX];
+  __shared__ __attribute__((aligned(16))) float pl[WAVES][NMAX];
+  const int hd = blockIdx.x, g = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int dh = a.dh, nc = dh / 16;
+  int n = a.len[g];
+  n = n < 1 ? 1 : (n > a.S ? a.S : n);
+  const int8_t* kb = a.kv + (size_t)g * a.kv_group + a.k_off + hd * dh;
+  const int8_t* vb = a.kv + (size_t)g * a.kv_group + a.v_off + hd * dh;
+  v4i kr[PER], vr[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int c = tid + u * 64 * WAVES;
+    const int t = min(c / DHC, n - 1), cc = min(c % DHC, nc - 1);
+    kr[u] = *(const v4i*)(kb + (size_t)t * a.ldkv + 16 * cc);
+    vr[u] = *(const v4i*)(vb + (size_t)t * a.ldkv + 16 * cc);
+  }
+  const int rows = a.rows;
+  auto qrow = [&](int i) { return a.q + ((size_t)g * rows + min(i, rows - 1)) * a.ldq + hd * dh; };
+  v4i qn[DHC];
+#pragma unroll
+  for (int c = 0; c < DHC; ++c) qn[c] = *(const v4i*)(qrow(wave) + 16 * min(c, nc - 1));
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int c = tid + u * 64 * WAVES;
+    if (c < CH) {
+      const int t = c / DHC, cc = c % DHC;
+      *(v4i*)(kl + t * KS + 16 * cc) = kr[u];
+      *(v4i*)(vl + t * DHMAX + 16 * cc) = vr[u];
+    }
+  }
+  lds_barrier();
+  for (int i = wave; i < rows; i += WAVES) {
+    v4i qv[DHC];
+#pragma unroll
+    for (int c = 0; c < DHC; ++c) {
+      qv[c] = qn[c];
+      qn[c] = *(const v4i*)(qrow(i + WAVES) + 16 * min(c, nc - 1));
+    }
+    float sv[NI];
+#pragma unroll
+    for (int ii = 0; ii < NI; ++ii) {
+      const int t = lane + 64 * ii;
+      sv[ii] = 0.0f;
+      if (t < n) {
+        int acc = 0;
+#pragma unroll
+        for (int c = 0; c < DHC; ++c)
+          if (c < nc) acc = dot16v(*(const v4i*)(kl + t * KS + 16 * c), qv[c], acc);
+        sv[ii] = (float)acc * a.c_qk;
+      }
+    }
+    softmax_context<NI>(sv, n, dh, a.c_pv, pl[wave], vl, DHMAX, a.ctx + ((size_t)g * rows + i) * a.d + hd * dh);
+  }
+}
+
+// Decoder self-attention at position t = *step, block = row r: wave w takes
+// heads w, w + WAVES, ...  It appends the row's new key and value of the head
+// to the int8 cache and attends over positions 0..t (with beam search through
+// the row's history of parent rows, hist[t & 1]; the key and value of
+// position t are the new ones, read from qkv).  Loads are coalesced: CPP
+// lanes take one position's dh codes (16 bytes each), so one load
+// instruction covers 64 / CPP positions, and each position's score is the sum
+// of its lanes' partial dot products (exact); the scores then pass through
+// LDS into the one-key-per-lane layout of the canonical softmax.  Keys and
+// values are loaded in batches of at most 8 instructions each, all of a batch
+// issued together.
+template <int NMAX, int DHMAX, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __restrict__ qkv, int d, int h, int dh,
+                                                              int T, const int* __restrict__ step,
+                                                              int8_t* __restrict__ kcache, int8_t* __restrict__ vcache,
+                                                              const int32_t* __restrict__ hist, float c_qk,
+                                                              float c_pv, int8_t* __restrict__ ctx) {
+  constexpr int CPP = DHMAX / 16;  // lanes per position
+  constexpr int PPI = 64 / CPP;    // positions per load instruction
+  constexpr int NL = NMAX / PPI;   // load instructions per operand
+  constexpr int NB = NL < 8 ? NL : 8;
+  constexpr int NI = NMAX / 64;
+  __shared__ AttnLdsT<NMAX, DHMAX> sh[WAVES];
+  const int r = blockIdx.x, R = gridDim.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nc = dh / 16;
+  const int c = lane % CPP, pp = lane / CPP, cc = min(c, nc - 1);
   int t = *step;
   t = t < 0 ? 0 : (t >= T ? T - 1 : t);
+  const int n = t + 1;
   const int8_t* row = qkv + (size_t)r * 3 * d;
-  const int8_t* knew = row + d + hd * dh;
-  const int8_t* vnew = row + 2 * d + hd * dh;
-  for (int j = lane; j < dh; j += 64) {
-    kcache[((size_t)r * T + t) * d + hd * dh + j] = knew[j];
-    vcache[((size_t)r * T + t) * d + hd * dh + j] = vnew[j];
-  }
-  // beam: hist holds two [R][T] tables used on alternate steps
-  const int R = gridDim.y;
+  // the rows that hold each position's key and value (beam: the parents)
   const int32_t* hr = hist ? hist + ((size_t)(t & 1) * R + r) * T : nullptr;
-  auto key = [&](int tp) -> const int8_t* {
-    if (tp == t) return knew;
-    const int src = hr ? hr[tp] : r;
-    return (const int8_t*)kcache + ((size_t)src * T + tp) * d + hd * dh;
-  };
-  auto val = [&](int tp) -> const int8_t* {
-    if (tp == t) return vnew;
-    const int src = hr ? hr[tp] : r;
-    return (const int8_t*)vcache + ((size_t)src * T + tp) * d + hd * dh;
-  };
-  attend_wave(row + hd * dh, t + 1, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh, sh);
-}
-
-// Decoder cross-attention: row r attends over the source of sentence r / W.
-__global__ __launch_bounds__(64) void k_attn_dec_cross(const int8_t* __restrict__ q, int W, int d, int dh,
-                                                       const int8_t* __restrict__ kv, int S,
-                                                       const int32_t* __restrict__ len, float c_qk, float c_pv,
-                                                       int8_t* __restrict__ ctx) {
-  __shared__ AttnLds sh;
-  const int hd = blockIdx.x, r = blockIdx.y;
-  const int b = r / W;
-  int n = len[b];
-  n = n < 1 ? 1 : (n > S ? S : n);
-  const int8_t* base = kv + (size_t)b * S * 2 * d;
-  auto key = [&](int t) { return base + (size_t)t * 2 * d + hd * dh; };
-  auto val = [&](int t) { return base + (size_t)t * 2 * d + d + hd * dh; };
-  attend_wave(q + (size_t)r * d + hd * dh, n, dh, key, val, c_qk, c_pv, ctx + (size_t)r * d + hd * dh, sh);
+  int src[NL];
+#pragma unroll
+  for (int u = 0; u < NL; ++u) src[u] = hr ? hr[min(u * PPI + pp, t)] : r;
+  for (int hd = wave; hd < h; hd += WAVES) {
+    const int8_t* knew = row + d + hd * dh;
+    const int8_t* vnew = row + 2 * d + hd * dh;
+    const v4i qc = *(const v4i*)(row + hd * dh + 16 * cc);
+    AttnLdsT<NMAX, DHMAX>& w = sh[wave];
+#pragma unroll
+    for (int u0 = 0; u0 < NL; u0 += NB) {
+      v4i kr[NB], vr[NB];
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int tp = min((u0 + u) * PPI + pp, t);
+        const size_t off = ((size_t)src[u0 + u] * T + tp) * d + hd * dh + 16 * cc;
+        kr[u] = *(const v4i*)(tp == t ? knew + 16 * cc : kcache + off);
+        vr[u] = *(const v4i*)(tp == t ? vnew + 16 * cc : vcache + off);
+      }
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        int acc = c < nc ? dot16v(kr[u], qc, 0) : 0;
+#pragma unroll
+        for (int o = 1; o < CPP; o <<= 1) acc += __shfl_xor(acc, o, 64);
+        const int tp = (u0 + u) * PPI + pp;
+        if (c == 0 && tp < n) w.p[tp] = (float)acc * c_qk;
+        *(v4i*)&w.v[tp][16 * c] = vr[u];
+      }
+    }
+    // the new key and value into the cache (no other block reads position t
+    // of this step)
+    if (lane < nc) {
+      const size_t o = ((size_t)r * T + t) * d + hd * dh + 16 * lane;
+      *(v4i*)(kcache + o) = *(const v4i*)(knew + 16 * lane);
+      *(v4i*)(vcache + o) = *(const v4i*)(vnew + 16 * lane);
+    }
+    wave_sync();  // the scores and values visible to every lane
+    float sv[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int tp = lane + 64 * i;
+      sv[i] = tp < n ? w.p[tp] : 0.0f;
+    }
+    softmax_context<NI>(sv, n, dh, c_pv, w.p, &w.v[0][0], DHMAX, ctx + (size_t)r * d + hd * dh);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -866,30 +970,105 @@ hipError_t launch_ln_quant(const float* x, int rows, int d, int do_ln, const flo
   return hipGetLastError();
 }
 
+// Key-length class of the attention kernels (the LDS and registers they
+// reserve), head-width class.
+int attn_len_class(int n) { return n <= 64 ? 64 : n <= 128 ? 128 : 256; }
+int attn_dh_class(int dh) { return dh <= 64 ? 64 : 128; }
+
+template <int WAVES>
+hipError_t launch_shared(const SharedAttn& a, int groups, int h, hipStream_t s) {
+  const dim3 grid(h, groups);
+  const int nm = attn_len_class(a.S), dm = attn_dh_class(a.dh);
+#define MNMT_SH(NM, DM) hipLaunchKernelGGL((k_attn_shared<NM, DM, WAVES>), grid, dim3(64 * WAVES), 0, s, a)
+  if (dm == 64) {
+    if (nm == 64) MNMT_SH(64, 64);
+    else if (nm == 128) MNMT_SH(128, 64);
+    else MNMT_SH(256, 64);
+  } else {
+    if (nm == 64) MNMT_SH(64, 128);
+    else if (nm == 128) MNMT_SH(128, 128);
+    else MNMT_SH(256, 128);
+  }
+#undef MNMT_SH
+  return hipGetLastError();
+}
+
 hipError_t launch_attn_enc(const int8_t* qkv, const int32_t* len, int B, int S, int d, int h, float c_qk, float c_pv,
                            int8_t* ctx, hipStream_t s) {
   const int dh = d / h;
-  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_attn_enc, dim3(S, h, B), dim3(64), 0, s, qkv, len, S, d, dh, c_qk, c_pv, ctx);
-  return hipGetLastError();
+  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16 || B < 1 || S < 1) return hipErrorInvalidValue;
+  SharedAttn a{};
+  a.q = qkv;
+  a.ldq = 3 * d;
+  a.rows = S;
+  a.kv = qkv;
+  a.kv_group = (size_t)S * 3 * d;
+  a.ldkv = 3 * d;
+  a.k_off = d;
+  a.v_off = 2 * d;
+  a.len = len;
+  a.S = S;
+  a.d = d;
+  a.dh = dh;
+  a.c_qk = c_qk;
+  a.c_pv = c_pv;
+  a.ctx = ctx;
+  return launch_shared<8>(a, B, h, s);
 }
 
 hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, const int* step, int8_t* kcache,
                                 int8_t* vcache, const int32_t* hist, float c_qk, float c_pv, int8_t* ctx,
                                 hipStream_t s) {
   const int dh = d / h;
-  if (T > kMaxAttnLen || dh > kMaxHeadDim || dh % 16) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_attn_dec_self, dim3(h, R), dim3(64), 0, s, qkv, d, dh, T, step, kcache, vcache, hist, c_qk,
-                     c_pv, ctx);
+  if (T > kMaxAttnLen || dh > kMaxHeadDim || dh % 16 || R < 1) return hipErrorInvalidValue;
+  const int nm = attn_len_class(T), dm = attn_dh_class(dh);
+  // a block per row, a wave per head (up to 8, fewer for the widest LDS)
+#define MNMT_SELF(NM, DM, WV)                                                                                      \
+  hipLaunchKernelGGL((k_attn_dec_self<NM, DM, WV>), dim3(R), dim3(64 * WV), 0, s, qkv, d, h, dh, T, step, kcache, \
+                     vcache, hist, c_qk, c_pv, ctx)
+#define MNMT_SELF_W(NM, DM)                  \
+  if (h >= 8) MNMT_SELF(NM, DM, 8);         \
+  else if (h >= 4) MNMT_SELF(NM, DM, 4);    \
+  else if (h >= 2) MNMT_SELF(NM, DM, 2);    \
+  else MNMT_SELF(NM, DM, 1);
+  if (dm == 64) {
+    if (nm == 64) { MNMT_SELF_W(64, 64) }
+    else if (nm == 128) { MNMT_SELF_W(128, 64) }
+    else if (h >= 4) MNMT_SELF(256, 64, 4);
+    else if (h >= 2) MNMT_SELF(256, 64, 2);
+    else MNMT_SELF(256, 64, 1);
+  } else {
+    if (nm == 64) { MNMT_SELF_W(64, 128) }
+    else if (nm == 128) MNMT_SELF(128, 128, 2);
+    else if (h >= 2) MNMT_SELF(256, 128, 2);
+    else MNMT_SELF(256, 128, 1);
+  }
+#undef MNMT_SELF_W
+#undef MNMT_SELF
   return hipGetLastError();
 }
 
 hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, const int8_t* kv, int S,
                                  const int32_t* len, float c_qk, float c_pv, int8_t* ctx, hipStream_t s) {
   const int dh = d / h;
-  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_attn_dec_cross, dim3(h, R), dim3(64), 0, s, q, W, d, dh, kv, S, len, c_qk, c_pv, ctx);
-  return hipGetLastError();
+  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16 || W < 1 || R % W) return hipErrorInvalidValue;
+  SharedAttn a{};
+  a.q = q;
+  a.ldq = d;
+  a.rows = W;
+  a.kv = kv;
+  a.kv_group = (size_t)S * 2 * d;
+  a.ldkv = 2 * d;
+  a.k_off = 0;
+  a.v_off = d;
+  a.len = len;
+  a.S = S;
+  a.d = d;
+  a.dh = dh;
+  a.c_qk = c_qk;
+  a.c_pv = c_pv;
+  a.ctx = ctx;
+  return launch_shared<4>(a, R / W, h, s);
 }
 
 hipError_t launch_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
