@@ -34,6 +34,8 @@ def lib():
         L.orc_canon_sum.argtypes = [vp, i32]
         L.orc_canon_sum_squares.restype = f32
         L.orc_canon_sum_squares.argtypes = [vp, i32]
+        L.orc_canon_vocab_sum.restype = f32
+        L.orc_canon_vocab_sum.argtypes = [vp, i32]
         L.orc_quantize.restype = C.c_int8
         L.orc_quantize.argtypes = [f32, f32]
         L.orc_length_penalty.restype = f32
@@ -102,6 +104,11 @@ def log_array(x):
 def canon_sum(x) -> np.float32:
     x = _c(x, np.float32)
     return np.float32(lib().orc_canon_sum(_p(x), x.size))
+
+
+def canon_vocab_sum(x) -> np.float32:
+    x = _c(x, np.float32)
+    return np.float32(lib().orc_canon_vocab_sum(_p(x), x.size))
 
 
 def canon_sum_squares(x) -> np.float32:

@@ -28,7 +28,10 @@
  *   R1  fp32 everywhere outside the integer GEMMs; RNE; no contraction.
  *   R2  every fp32 sum over n terms is "wave64 order": 64 interleaved partial
  *       sums (term i goes to partial i mod 64, ascending i, starting at +0),
- *       then combined by halving: p[l] += p[l + off] for off = 32..1.
+ *       then combined by halving: p[l] += p[l + off] for off = 32..1 --
+ *       except the sum over the vocabulary in beam search's log-sum-exp
+ *       (R2b, orc_canon_vocab_sum): 512 partials fed four consecutive terms
+ *       at a time, halving within each run of 64, then a fixed tree of 8.
  *   R3  quantize: q = clamp(rint(y * (1/s)), -127, 127), 1/s rounded once.
  *   R4  folded constants computed in double, rounded once to fp32.
  *   R5  LayerNorm: biased variance, eps from the model file, affine g/b.
@@ -69,6 +72,25 @@ float orc_canon_sum_squares(const float* x, int n) {
   for (int off = 32; off >= 1; off /= 2)
     for (int l = 0; l < off; ++l) p[l] = p[l] + p[l + off];
   return p[0];
+}
+
+/* R2b: the sum over the vocabulary in the log-sum-exp of beam search.  The
+ * terms are dealt to 512 partial sums in groups of four consecutive terms
+ * (term i goes to partial (i / 4) mod 512, ascending i, partials start at
+ * +0); each run of 64 partials (64 w .. 64 w + 63) is combined by halving as
+ * in R2, giving g_w; then ((g0 + g1) + (g2 + g3)) + ((g4 + g5) + (g6 + g7)). */
+float orc_canon_vocab_sum(const float* x, int n) {
+  float p[512];
+  for (int j = 0; j < 512; ++j) p[j] = 0.0f;
+  for (int i = 0; i < n; ++i) p[(i / 4) % 512] = p[(i / 4) % 512] + x[i];
+  float g[8];
+  for (int w = 0; w < 8; ++w) {
+    float* q = p + 64 * w;
+    for (int off = 32; off >= 1; off /= 2)
+      for (int l = 0; l < off; ++l) q[l] = q[l] + q[l + off];
+    g[w] = q[0];
+  }
+  return ((g[0] + g[1]) + (g[2] + g[3])) + ((g[4] + g[5]) + (g[6] + g[7]));
 }
 
 /* R3: uniform symmetric 8-bit quantization (Section 3.2; rounding to the
@@ -280,7 +302,8 @@ int orc_attend(const int8_t* q, const int8_t* K, const int8_t* V, int n, int dh,
   return ORC_OK;
 }
 
-/* log-sum-exp of a row: max m, then m + ln(sum_v e^(z_v - m)). */
+/* log-sum-exp of a row: max m, then m + ln(sum_v e^(z_v - m)), the sum over
+ * the vocabulary in the R2b order. */
 int orc_log_softmax_stats(const float* z, int n, float* max_out, float* lse_out) {
   if (n <= 0) return ORC_E_ARG;
   float mx = z[0];
@@ -288,7 +311,7 @@ int orc_log_softmax_stats(const float* z, int n, float* max_out, float* lse_out)
     if (z[v] > mx) mx = z[v];
   float* e = (float*)malloc(sizeof(float) * (size_t)n);
   for (int v = 0; v < n; ++v) e[v] = orc_exp(z[v] - mx);
-  float sum = orc_canon_sum(e, n);
+  float sum = orc_canon_vocab_sum(e, n);
   free(e);
   if (max_out) *max_out = mx;
   if (lse_out) *lse_out = mx + orc_log(sum);

@@ -44,6 +44,7 @@ float orc_exp(float x);                       /* e^x for x <= 0 */
 float orc_log(float x);                       /* ln x for normal x > 0 */
 float orc_canon_sum(const float* x, int n);   /* 64 interleaved partial sums, halving combine */
 float orc_canon_sum_squares(const float* x, int n); /* the same order, partials p = fma(x, x, p) */
+float orc_canon_vocab_sum(const float* x, int n);   /* vocabulary sums: 512 partials, 4 terms a turn, tree of 8 */
 int8_t orc_quantize(float y, float inv_s);    /* clamp(rne(y * inv_s), -127, 127) */
 float orc_length_penalty(int L, float alpha); /* ((5 + L) / 6)^alpha */
 int orc_map(int fn, const float* x, int n, float* y); /* fn 0: orc_exp, 1: orc_log */

@@ -435,9 +435,28 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
   float mx = -FLT_MAX;
   for (int v = lane; v < V; v += 64) mx = fmaxf(mx, z[v]);
   mx = wave_max(mx);
-  float part = 0.0f;
-  for (int v = lane; v < V; v += 64) part = part + canon_exp(z[v] - mx);
-  const float lse = mx + canon_log(wave_sum(part));
+  // the vocabulary order (R2b): lane l holds partials 64 w + l (w = 0..7),
+  // fed the four-term groups g = l, l + 64, ... (partial g mod 512)
+  float pw[8];
+#pragma unroll
+  for (int w = 0; w < 8; ++w) pw[w] = 0.0f;
+  for (int g = lane; 4 * g < V; g += 64) {
+    const int wg = (g >> 6) & 7;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int v = 4 * g + q;
+      if (v < V) {
+        const float e = canon_exp(z[v] - mx);
+#pragma unroll
+        for (int w = 0; w < 8; ++w)
+          if (w == wg) pw[w] = pw[w] + e;
+      }
+    }
+  }
+  float gs[8];
+#pragma unroll
+  for (int w = 0; w < 8; ++w) gs[w] = wave_sum(pw[w]);
+  const float lse = mx + canon_log(((gs[0] + gs[1]) + (gs[2] + gs[3])) + ((gs[4] + gs[5]) + (gs[6] + gs[7])));
   const float sc = st.score[r];
   float ls[K];
   int lv[K];
@@ -485,23 +504,26 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
 
 // The same statistics and candidates with one 512-thread block per row, for
 // V a multiple of 4 up to kTopkMaxV: the row is loaded once into registers
-// (every load in flight at once: 16 bytes per load, up to 16 per thread), the
-// maximum (order-free) taken from them, exp(z - max) of every element computed
-// by all threads into LDS, the canonical sum by wave 0 (lane l adds elements
-// l, l + 64, ... in ascending order, then the butterfly: the same order as the
-// one-wave kernel).  The candidates then come from a threshold: the score is
-// monotone in z, so each thread's best score is score + (its max z - lse), and
-// the K-th largest of these over the lanes of a wave has at least K scores of
-// the row at or above it; the largest such bound over the waves filters the
-// row down to a short list (about 4K entries on real logits), ranked by
-// pairwise comparison.  If ties push the list past kTopkCap the scores go to
-// LDS and per-thread sorted lists merged over the block take over.  The
-// candidate order is total (score, then index), so neither the filter nor the
-// split over threads changes the result.
+// (element 4 (tid + 512 k) + q: 16 bytes per load, up to 16 per thread, all
+// in flight), the maximum (order-free) taken from them, and each thread adds
+// exp(z - max) of its own elements in ascending order: exactly the partials
+// of the vocabulary order (R2b: 512 partials fed four consecutive terms at a
+// time), so the wave butterflies and the tree of the 8 wave sums finish the
+// sum with no exchange of the exponentials.  The candidates then come from a
+// threshold: the score is monotone in z, so each thread's best score is
+// score + (its max z - lse), and the K-th largest of these over the lanes of
+// a wave has at least K scores of the row at or above it; the largest such
+// bound over the waves filters the row down to a short list (about 4K
+// entries on real logits), ranked by pairwise comparison.  If ties push the
+// list past kTopkCap, per-thread sorted lists over the threads' own elements,
+// merged over the block, take over.  The candidate order is total (score,
+// then index), so neither the filter nor the split over threads changes the
+// result.
 constexpr int kTopkMaxV = 32768;
 constexpr int kTopkThreads = 512, kTopkWaves = kTopkThreads / 64;
 constexpr int kTopkV4 = kTopkMaxV / 4 / kTopkThreads;  // float4 per thread
 constexpr int kTopkCap = 1024;                // entries of the filtered list
+static_assert(kTopkThreads == 512, "the vocabulary order has 512 partials");
 
 __device__ __forceinline__ unsigned long long block_max_u64(unsigned long long v, unsigned long long* red) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -515,11 +537,12 @@ __device__ __forceinline__ unsigned long long block_max_u64(unsigned long long v
   return m;
 }
 
-// Per-thread sorted lists over the scores in LDS, merged over the block: the
+// Per-thread sorted lists over the thread's own elements (scores
+// sc + (z - lse) of elements 4 (tid + 512 k) + q), merged over the block: the
 // path for rows whose filtered list overflows (large groups of equal scores).
 template <int K>
-__device__ __forceinline__ void topk_lists(const float* c_lds, int V, unsigned long long* redk, int* cand_tok,
-                                        float* cand_score) {
+__device__ __forceinline__ void topk_lists(const float4 (&zr)[kTopkV4], int n4, float sc, float lse,
+                                           unsigned long long* redk, int* cand_tok, float* cand_score) {
   const int tid = threadIdx.x;
   float ls[K];
   int lv[K];
@@ -528,19 +551,26 @@ __device__ __forceinline__ void topk_lists(const float* c_lds, int V, unsigned l
     ls[k] = -FLT_MAX;
     lv[k] = INT_MAX;
   }
-  for (int v = tid; v < V; v += kTopkThreads) {
-    float c = c_lds[v];
-    int cv = v;
-    if (!better(c, cv, ls[K - 1], lv[K - 1])) continue;
 #pragma unroll
-    for (int m = 0; m < K; ++m) {  // insertion by swapping keeps the list sorted
-      if (better(c, cv, ls[m], lv[m])) {
-        const float tc = ls[m];
-        const int tv = lv[m];
-        ls[m] = c;
-        lv[m] = cv;
-        c = tc;
-        cv = tv;
+  for (int k = 0; k < kTopkV4; ++k) {
+    const int i = tid + kTopkThreads * k;
+    if (i >= n4) continue;
+    const float zq[4] = {zr[k].x, zr[k].y, zr[k].z, zr[k].w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float c = sc + (zq[q] - lse);
+      int cv = 4 * i + q;
+      if (!better(c, cv, ls[K - 1], lv[K - 1])) continue;
+#pragma unroll
+      for (int m = 0; m < K; ++m) {  // insertion by swapping keeps the list sorted
+        if (better(c, cv, ls[m], lv[m])) {
+          const float tc = ls[m];
+          const int tv = lv[m];
+          ls[m] = c;
+          lv[m] = cv;
+          c = tc;
+          cv = tv;
+        }
       }
     }
   }
@@ -568,10 +598,10 @@ __device__ __forceinline__ void topk_lists(const float* c_lds, int V, unsigned l
 template <int K>
 __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* __restrict__ logits, BeamState st,
                                                          const int* __restrict__ step) {
-  __shared__ float e_lds[kTopkMaxV];
   __shared__ float list_c[kTopkCap];
   __shared__ int list_v[kTopkCap];
   __shared__ float redf[kTopkWaves];
+  __shared__ float reds[kTopkWaves];
   __shared__ unsigned long long redk[kTopkWaves];
   __shared__ int n_list;
   const int r = blockIdx.x;
@@ -583,6 +613,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* _
   const float4* z4 = reinterpret_cast<const float4*>(logits + (size_t)r * V);
   int* cand_tok = st.cand_tok + (size_t)r * K;
   float* cand_score = st.cand_score + (size_t)r * K;
+  const float sc = st.score[r];
   if (tid == 0) n_list = 0;
   // 1. the row in registers (element 4 (tid + kTopkThreads k) + q), the thread's
   //    maximum and the row's
@@ -599,37 +630,23 @@ __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* _
   mx = redf[0];
 #pragma unroll
   for (int w = 1; w < kTopkWaves; ++w) mx = fmaxf(mx, redf[w]);
-  // 2. exp(z - max) of every element into LDS, then the canonical sum
+  // 2. the sum of exp(z - max) in the vocabulary order: the thread's partial
+  //    over its elements in ascending order, the wave butterfly, the tree
+  float part = 0.0f;
 #pragma unroll
   for (int k = 0; k < kTopkV4; ++k) {
-    const int i = tid + kTopkThreads * k;
-    if (i < n4) {
-      e_lds[4 * i] = canon_exp(zr[k].x - mx);
-      e_lds[4 * i + 1] = canon_exp(zr[k].y - mx);
-      e_lds[4 * i + 2] = canon_exp(zr[k].z - mx);
-      e_lds[4 * i + 3] = canon_exp(zr[k].w - mx);
+    if (tid + kTopkThreads * k < n4) {
+      part = part + canon_exp(zr[k].x - mx);
+      part = part + canon_exp(zr[k].y - mx);
+      part = part + canon_exp(zr[k].z - mx);
+      part = part + canon_exp(zr[k].w - mx);
     }
   }
+  part = wave_sum(part);
+  if (lane == 0) reds[wave] = part;
   __syncthreads();
-  if (wave == 0) {
-    // lane l: elements l, l + 64, ... in ascending order (eight reads in
-    // flight, the adds in order)
-    float part = 0.0f;
-    int i = lane;
-    for (; i + 7 * 64 < V; i += 8 * 64) {
-      float e[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) e[u] = e_lds[i + 64 * u];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) part = part + e[u];
-    }
-    for (; i < V; i += 64) part = part + e_lds[i];
-    const float lse = mx + canon_log(wave_sum(part));
-    if (lane == 0) redf[0] = lse;
-  }
-  __syncthreads();
-  const float lse = redf[0];
-  const float sc = st.score[r];
+  const float lse =
+      mx + canon_log(((reds[0] + reds[1]) + (reds[2] + reds[3])) + ((reds[4] + reds[5]) + (reds[6] + reds[7])));
   // 3. the bound: the K-th largest thread-best score of each wave (scores
   //    below -FLT_MAX never qualify), the largest over the waves
   const float cm = sc + (tmx - lse);
@@ -641,7 +658,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* _
     const unsigned long long hold = __ballot(v == kth);
     if (lane == __ffsll((long long)hold) - 1) v = -INFINITY;  // drop one holder
   }
-  __syncthreads();  // every read of redf[0] is done
+  __syncthreads();  // every read of redf (the maximum) is done
   if (lane == 0) redf[wave] = fmaxf(kth, -FLT_MAX);
   __syncthreads();
   float tau = redf[0];
@@ -686,19 +703,8 @@ __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* _
     }
     return;
   }
-  // 5'. the overflow path: all scores into LDS, sorted lists, block merge
-#pragma unroll
-  for (int k = 0; k < kTopkV4; ++k) {
-    const int i = tid + kTopkThreads * k;
-    if (i < n4) {
-      e_lds[4 * i] = sc + (zr[k].x - lse);
-      e_lds[4 * i + 1] = sc + (zr[k].y - lse);
-      e_lds[4 * i + 2] = sc + (zr[k].z - lse);
-      e_lds[4 * i + 3] = sc + (zr[k].w - lse);
-    }
-  }
-  __syncthreads();
-  topk_lists<K>(e_lds, V, redk, cand_tok, cand_score);
+  // 5'. the overflow path: per-thread sorted lists, block merge
+  topk_lists<K>(zr, n4, sc, lse, redk, cand_tok, cand_score);
 }
 
 // Per sentence: merge the W rows' candidates, finish EOS hypotheses, refill

@@ -24,6 +24,42 @@ def test_canon_sum_worked_examples(row):
     assert oracle.canon_sum(x) == np.float32(float(expected))
 
 
+def _vocab_cases():
+    path = os.path.join(os.path.dirname(__file__), "golden", "canon_vocab_sum_order.txt")
+    rows = []
+    for line in open(path):
+        line = line.strip()
+        if line and not line.startswith("#"):
+            rows.append(line.split())
+    return rows
+
+
+@pytest.mark.parametrize("row", _vocab_cases(), ids=lambda r: r[0])
+def test_canon_vocab_sum_worked_examples(row):
+    """The vocabulary sum of the beam search's log-sum-exp (reading R2b)
+    against hand-derived values; each case also differs from the wave64 order."""
+    _, n, default, entries, expected = row
+    x = np.full(int(n), np.float32(float(default)), np.float32)
+    for e in entries.split(","):
+        i, v = e.split(":")
+        x[int(i)] = np.float32(float(v))
+    assert oracle.canon_vocab_sum(x) == np.float32(float(expected))
+    assert oracle.canon_sum(x) != np.float32(float(expected))
+
+
+def test_canon_vocab_sum_exact_on_integers_and_error_bound():
+    rng = np.random.default_rng(3)
+    for n in (1, 5, 2048, 2051, 32000, 32768):
+        xi = rng.integers(-1000, 1000, size=n).astype(np.float32)
+        assert oracle.canon_vocab_sum(xi) == np.float32(xi.astype(np.int64).sum())
+        x = rng.standard_normal(n).astype(np.float32)
+        exact = math.fsum(float(v) for v in x)
+        depth = -(-n // 2048) * 4 + 6 + 3  # terms per partial, halving, tree
+        bound = depth * 2.0 ** -24 * float(np.abs(x).sum())
+        assert abs(float(oracle.canon_vocab_sum(x)) - exact) <= bound
+    assert oracle.canon_vocab_sum(np.zeros(0, np.float32)) == 0.0
+
+
 def test_canon_sum_exact_on_integers_and_error_bound():
     rng = np.random.default_rng(1)
     for n in (1, 7, 63, 64, 65, 256, 1000, 32000):
