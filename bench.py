@@ -210,6 +210,34 @@ def ingest_counters(fetch_csv, write_csv, command):
     print(json.dumps(rec))
 
 
+def ingest_trace(stats_csv, command):
+    """The roofline kernel's average kernel-trace duration (rocprofv3
+    --kernel-trace --stats of a bench.py run, its kernel_stats.csv) into
+    profiles/counters.json, keyed by the kernel sources' hash like the
+    counters."""
+    import csv
+
+    calls, total_ns = 0, 0.0
+    with open(stats_csv) as f:
+        for row in csv.DictReader(f):
+            if ROOF_KERNEL in row["Name"].replace("mnmt::(anonymous namespace)::", ""):
+                calls += int(row["Calls"])
+                total_ns += float(row["TotalDurationNs"])
+    if not calls:
+        raise SystemExit(f"{ROOF_KERNEL} not in {stats_csv}")
+    rec = {"source_hash": _source_hash(), "kernel": ROOF_KERNEL, "avg_us": round(total_ns / calls / 1e3, 4),
+           "calls": calls, "command": command}
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    data = {}
+    if os.path.exists(path):
+        with open(path) as f:
+            data = json.load(f)
+    data[ROOF_TAG + "_trace"] = rec
+    with open(path, "w") as f:
+        json.dump(data, f, indent=1)
+    print(json.dumps(rec))
+
+
 def _host_cpu():
     try:
         with open("/proc/cpuinfo") as f:
@@ -426,11 +454,16 @@ def main():
     ap.add_argument("--sweep", action="store_true", help="only the quantized-linear sweep (20 shapes, I8 epilogue)")
     ap.add_argument("--counters", action="store_true", help="only the roofline kernel and the copy (for --pmc)")
     ap.add_argument("--ingest-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--ingest-trace", metavar="KERNEL_STATS_CSV",
+                    help="record the roofline kernel's kernel-trace average from a rocprofv3 --stats file")
     ap.add_argument("--ingest-command", default="")
     ap.add_argument("--sweep-trace", metavar="KERNEL_TRACE_CSV", help="summarize a kernel trace of --sweep")
     args = ap.parse_args()
     if args.sweep_trace:
         sweep_trace_summary(args.sweep_trace, args.ingest_command)
+        return
+    if args.ingest_trace:
+        ingest_trace(args.ingest_trace, args.ingest_command)
         return
     if args.ingest_counters:
         ingest_counters(*args.ingest_counters, args.ingest_command)
