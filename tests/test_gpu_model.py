@@ -331,6 +331,26 @@ def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None, parall
     sess.close()
 
 
+HEAD16 = G.ModelConfig("head-16", 128, 8, 256, 1, 1, 600, ln_post=0, seed=88, random_gamma=True, weight_std=0.1)
+HEAD128 = G.ModelConfig("head-128", 256, 2, 512, 1, 1, 600, ln_post=1, seed=89, random_gamma=True, weight_std=0.08)
+
+
+@pytest.mark.parametrize("cfg", [HEAD16, HEAD128], ids=lambda c: c.name)
+def test_attention_length_and_head_classes(torch_dev, cfg):
+    """The batched attention kernels' length classes (64, 128, 256 keys) and
+    head-width classes (16-64 and 128) against the oracle, up to the maximum
+    lengths (256 source tokens, 256 target positions): greedy at 3 rows
+    (batched encoder, 3-8-row decoder) and beam search at 8 rows, with a
+    one-token source among long ones."""
+    torch, dev = torch_dev
+    src, lens = G.make_sources(cfg.vocab, 3, [256, 131, 1], seed=90, s_max=256)
+    _greedy_check(torch, dev, cfg, src, lens, 200, check_logits=False)
+    src, lens = G.make_sources(cfg.vocab, 3, [100, 65, 7], seed=91, s_max=100)
+    _greedy_check(torch, dev, cfg, src, lens, 100)
+    src, lens = G.make_sources(cfg.vocab, 2, [150, 1], seed=92, s_max=150)
+    _beam_check(torch, dev, cfg, src, lens, 4, 140, 0.6)
+
+
 ODD_VOCAB = G.ModelConfig("odd-vocab", 64, 4, 128, 1, 1, 501, ln_post=0, seed=79, random_gamma=True, weight_std=0.1)
 
 
