@@ -56,22 +56,17 @@ __global__ __launch_bounds__(256) void k_embed_proj(const int32_t* __restrict__ 
 // (canonical order).  ln_quant_wave normalizes v in place (when do_ln) and
 // stores the codes (q_row) and the normalized row (x_out_row), either may be
 // null.
-// The LayerNorm's gain and bias are loaded (clamped indexes, unconditional)
-// before the reductions, so they arrive while the sums run.
+// ln_quant_wave_pre takes the LayerNorm's gain and bias already in
+// registers (element lane + 64 j in slot j); ln_quant_wave loads them
+// (clamped indexes, unconditional) before the reductions, so they arrive
+// while the sums run.
 template <int NJ>
-__device__ __forceinline__ void ln_quant_wave(float (&v)[NJ], int d, int do_ln, const float* __restrict__ g,
-                                              const float* __restrict__ b, float eps, float inv_s,
-                                              int8_t* __restrict__ q_row, float* __restrict__ x_out_row) {
+__device__ __forceinline__ void ln_quant_wave_pre(float (&v)[NJ], int d, int do_ln, const float (&gj)[NJ],
+                                                  const float (&bj)[NJ], float eps, float inv_s,
+                                                  int8_t* __restrict__ q_row, float* __restrict__ x_out_row) {
   const int lane = threadIdx.x & 63;
   const int n = (d + 63) / 64;
   if (do_ln) {
-    float gj[NJ], bj[NJ];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int i = min(lane + 64 * j, d - 1);
-      gj[j] = g[i];
-      bj[j] = b[i];
-    }
     float p = 0.0f;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
@@ -105,6 +100,27 @@ __device__ __forceinline__ void ln_quant_wave(float (&v)[NJ], int d, int do_ln, 
       if (x_out_row) x_out_row[i] = v[j];
     }
   }
+}
+
+template <int NJ>
+__device__ __forceinline__ void ln_consts(int d, int do_ln, const float* __restrict__ g, const float* __restrict__ b,
+                                          float (&gj)[NJ], float (&bj)[NJ]) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int i = min(lane + 64 * j, d - 1);
+    gj[j] = do_ln ? g[i] : 0.0f;
+    bj[j] = do_ln ? b[i] : 0.0f;
+  }
+}
+
+template <int NJ>
+__device__ __forceinline__ void ln_quant_wave(float (&v)[NJ], int d, int do_ln, const float* __restrict__ g,
+                                              const float* __restrict__ b, float eps, float inv_s,
+                                              int8_t* __restrict__ q_row, float* __restrict__ x_out_row) {
+  float gj[NJ], bj[NJ];
+  ln_consts<NJ>(d, do_ln, g, b, gj, bj);
+  ln_quant_wave_pre<NJ>(v, d, do_ln, gj, bj, eps, inv_s, q_row, x_out_row);
 }
 
 // NJ = row_class(d) / 64; the row's loads are unconditional (clamped index).
@@ -713,7 +729,11 @@ __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* _
 // (advanced by the last block).  One block per sentence: wave 0 updates the
 // sentence, then wave w prepares slots w, w + kUpdWaves, ...
 constexpr int kUpdWaves = 4;
-template <int W_MAX>
+// NJ = row_class(d) / 64.  Everything that does not depend on the update
+// (the sentence's finished count, the length penalty, the candidates, the
+// next position's row of the position table and the LayerNorm constants) is
+// loaded at kernel start; the history copy runs one slot per wave.
+template <int W_MAX, int NJ>
 __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, int* step, BeamNext nx) {
   constexpr int NC = W_MAX * 2 * W_MAX;  // candidates per sentence
   __shared__ float cs[NC];
@@ -725,10 +745,21 @@ __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, in
   __shared__ int slot_tok[W_MAX];  // each slot's token after the update
   const int b = blockIdx.x;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const bool w0 = wv == 0;  // the wave that updates the sentence
+  const bool w0 = wv == 0;  // the wave that ranks the sentence's candidates
   const int W = st.W, K = 2 * W, R = st.B * W, T = st.T, V = st.V;
   const int t = *step;
   const bool active = !st.done[b];
+  const int pos = t + 1;
+  const bool prep = pos < nx.steps && pos < nx.P;
+  float pe_r[NJ], gj[NJ], bj[NJ];
+  {
+    const int pp = min(pos, nx.P - 1);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) pe_r[j] = nx.pe[(size_t)pp * nx.d + min(lane + 64 * j, nx.d - 1)];
+    ln_consts<NJ>(nx.d, nx.do_ln, nx.g, nx.b, gj, bj);
+  }
+  const int fc0 = st.fin_count[b];
+  const float lp_next = st.lp[min(t + 1, T)];
   if (threadIdx.x < W) slot_tok[threadIdx.x] = st.cur_tok[b * W + threadIdx.x];
   if (active) {
     const int n_alive = t == 0 ? 1 : W;
@@ -756,13 +787,13 @@ __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, in
     __syncthreads();
     if (threadIdx.x == 0) {
       int n_live = 0;
-      int fc = st.fin_count[b];
+      int fc = fc0;
       const int n_top = n < K ? n : K;
       for (int rk = 0; rk < n_top && n_live < W; ++rk) {
         const int i = order[rk];
         if (cv[i] == st.eos) {
           if (rk < W && fc < W) {
-            st.fin_score[b * W + fc] = cs[i] / st.lp[t + 1];
+            st.fin_score[b * W + fc] = cs[i] / lp_next;
             st.fin_len[b * W + fc] = t + 1;
             st.fin_row[b * W + fc] = b * W + cj[i];
             ++fc;
@@ -780,11 +811,11 @@ __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, in
       done_sh = fc >= W;
     }
     __syncthreads();
-    if (!done_sh && w0) {
+    if (!done_sh) {
       const int n_live = n_live_sh;
       const int32_t* hcur = st.hist + (size_t)(t & 1) * R * T;
       int32_t* hnext = st.hist + (size_t)((t + 1) & 1) * R * T;
-      for (int s = 0; s < n_live; ++s) {
+      for (int s = wv; s < n_live; s += kUpdWaves) {
         const int p = b * W + s, par = new_par[s];
         for (int tp = lane; tp <= t && tp < T; tp += 64) hnext[(size_t)p * T + tp] = tp < t ? hcur[(size_t)par * T + tp] : par;
         if (lane == 0) {
@@ -801,23 +832,20 @@ __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, in
   }
   __syncthreads();
   // the next step's input rows: what k_embed and k_ln_quant compute, one wave per row
-  const int pos = t + 1;
-  if (pos < nx.steps && pos < nx.P) {
+  if (prep) {
     for (int s = wv; s < W; s += kUpdWaves) {
       const int p = b * W + s;
       int tk = slot_tok[s];
       tk = tk < 0 ? 0 : (tk >= nx.V ? nx.V - 1 : tk);
       const float c = nx.c_emb[tk];
-      float v[kMaxRowLen / 64];
+      float v[NJ];
 #pragma unroll
-      for (int j = 0; j < kMaxRowLen / 64; ++j) {
+      for (int j = 0; j < NJ; ++j) {
         const int i = lane + 64 * j;
-        if (i < nx.d) {
-          v[j] = fmaf((float)nx.E[(size_t)tk * nx.d + i], c, nx.pe[(size_t)pos * nx.d + i]);
-          nx.x[(size_t)p * nx.d + i] = v[j];
-        }
+        v[j] = fmaf((float)nx.E[(size_t)tk * nx.d + min(i, nx.d - 1)], c, pe_r[j]);
+        if (i < nx.d) nx.x[(size_t)p * nx.d + i] = v[j];
       }
-      ln_quant_wave(v, nx.d, nx.do_ln, nx.g, nx.b, nx.eps, nx.inv_s, nx.a + (size_t)p * nx.d, nullptr);
+      ln_quant_wave_pre<NJ>(v, nx.d, nx.do_ln, gj, bj, nx.eps, nx.inv_s, nx.a + (size_t)p * nx.d, nullptr);
     }
   }
   // the step counter, by the last block to get here (every block has read it)
@@ -1177,7 +1205,17 @@ hipError_t launch_beam_topk(const float* logits, const BeamState& st, const int*
 
 hipError_t launch_beam_update(const BeamState& st, int* step, const BeamNext& nx, hipStream_t s) {
   if (st.W > 8 || nx.d < 1 || nx.d > kMaxRowLen || !nx.x || !nx.a || !st.count) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_beam_update<8>, dim3(st.B), dim3(64 * kUpdWaves), 0, s, st, step, nx);
+  const dim3 grid(st.B), block(64 * kUpdWaves);
+#define MNMT_UPD(NJ) hipLaunchKernelGGL((k_beam_update<8, NJ>), grid, block, 0, s, st, step, nx)
+  switch (row_class(nx.d)) {
+    case 64: MNMT_UPD(1); break;
+    case 128: MNMT_UPD(2); break;
+    case 256: MNMT_UPD(4); break;
+    case 384: MNMT_UPD(6); break;
+    case 512: MNMT_UPD(8); break;
+    default: MNMT_UPD(16); break;
+  }
+#undef MNMT_UPD
   return hipGetLastError();
 }
 
