@@ -125,6 +125,14 @@ __device__ __forceinline__ void poll_row_data(const StepIn& in, int r, int d, Ro
   }
 }
 
+// Every load the kernel has issued (weights, constants, the input rows)
+// completes here, in every wave, before block 0 issues its first store: the
+// memory counter retires in order, so a wait for one of those loads placed
+// after the stores would also wait for the stores to reach the point of
+// coherence (about half a microsecond), and block 0, whose partial sums the
+// next kernel also waits for, would lag the other blocks by that much.
+__device__ __forceinline__ void loads_done() { __builtin_amdgcn_s_waitcnt(0); }
+
 // Finishes row r from the loaded registers: the pending residual update, the
 // LayerNorm, the store of the updated residual row (block 0: plain, or tagged
 // with out_tag for the counted hand-off), and the int8 codes in a_lds + r * d.
@@ -303,8 +311,11 @@ __device__ __forceinline__ void step_attn_body(const StepIn& in, const StepAttn&
     }
   }
   // 2. the rows
-  clear_acc(in, bid);
+  // (the clear after the row: its stores must not sit in the in-order
+  // memory counter ahead of the row data that finish_row waits for)
+  loads_done();
   if (wave < R) finish_row(in, wave, d, rr, a_lds, otag, bid);
+  clear_acc(in, bid);
 
   lds_barrier();
   // 3. Q (K, V) of the head on the matrix cores, requantized into LDS
@@ -494,8 +505,11 @@ __device__ __forceinline__ void step_ffn_body(const StepIn& in, const StepFfn& f
   } else {
     load_row_data(in, min(wave, R - 1), d, rr);
   }
-  clear_acc(in, bid);
+  // (the clear after the row: its stores must not sit in the in-order
+  // memory counter ahead of the row data that finish_row waits for)
+  loads_done();
   if (wave < R) finish_row(in, wave, d, rr, a_lds, otag, bid);
+  clear_acc(in, bid);
   lds_barrier();
   {
     const int arow = l16 < R ? l16 : 0;
@@ -599,8 +613,9 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     load_row_data(in, min(wave, R - 1), d, rr);
   }
   if (!RAW) {
-    clear_acc(in, blockIdx.x);
+    loads_done();
     if (wave < R) finish_row(in, wave, d, rr, a_lds, 0u, blockIdx.x);
+    clear_acc(in, blockIdx.x);
   } else if (wave < R && lane < d / 16) {
     *(v4i*)(a_lds + wave * d + 16 * lane) = xr;
   }
