@@ -164,7 +164,11 @@ __device__ __forceinline__ void enc_rows(const EncIn& in, int8_t* a_lds, Issue i
       }
     }
   }
-  // the clearing stores behind the loads
+  // every load of the kernel completes before its first store (the clears,
+  // the rows): the memory counter retires in order, so a wait for one of
+  // those loads placed after the stores would also wait for the stores to
+  // reach the point of coherence
+  __builtin_amdgcn_s_waitcnt(0);
   enc_clear(in);
   // up to four rows at a time, so that their dependent chains (butterflies,
   // square root, division) interleave
