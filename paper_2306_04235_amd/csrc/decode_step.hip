@@ -423,7 +423,14 @@ __device__ __forceinline__ void step_attn_body(const StepIn& in, const StepAttn&
   lds_barrier();
   // 5. this head's share of the output projection (K = dh), exact int32
   //    partial sums added to the accumulator
-  clear_done(in, bid);
+  // Block 0: its accumulator clear must have landed before it adds (see
+  // clear_done).  Self-attention blocks: their key/value appends must have
+  // landed before their partial sums, which the rest of the step waits on:
+  // this layer's launch of the next step reads the cache before its own wait
+  // and starts only once the launch after this one has finished, which
+  // cannot finish before these sums have landed.
+  if (SELF) __builtin_amdgcn_s_waitcnt(0);
+  else clear_done(in, bid);
   {
     const int crow = l16 < R ? l16 : 0;
     const v4i cf = kq < nc ? *(const v4i*)(ctx[crow] + 16 * kq) : v4i{0, 0, 0, 0};
