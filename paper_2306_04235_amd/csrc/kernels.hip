@@ -269,6 +269,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __re
     const int8_t* knew = row + d + hd * dh;
     const int8_t* vnew = row + 2 * d + hd * dh;
     const v4i qc = *(const v4i*)(row + hd * dh + 16 * cc);
+    // the new key and value chunks for the cache append at the end
+    const v4i kapp = *(const v4i*)(knew + 16 * min(lane, nc - 1));
+    const v4i vapp = *(const v4i*)(vnew + 16 * min(lane, nc - 1));
     AttnLdsT<NMAX, DHMAX>& w = sh[wave];
 #pragma unroll
     for (int u0 = 0; u0 < NL; u0 += NB) {
@@ -290,13 +293,6 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __re
         *(v4i*)&w.v[tp][16 * c] = vr[u];
       }
     }
-    // the new key and value into the cache (no other block reads position t
-    // of this step)
-    if (lane < nc) {
-      const size_t o = ((size_t)r * T + t) * d + hd * dh + 16 * lane;
-      *(v4i*)(kcache + o) = *(const v4i*)(knew + 16 * lane);
-      *(v4i*)(vcache + o) = *(const v4i*)(vnew + 16 * lane);
-    }
     wave_sync();  // the scores and values visible to every lane
     float sv[NI];
 #pragma unroll
@@ -305,6 +301,13 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __re
       sv[i] = tp < n ? w.p[tp] : 0.0f;
     }
     softmax_context<NI>(sv, n, dh, c_pv, w.p, &w.v[0][0], DHMAX, ctx + (size_t)r * d + hd * dh);
+    // the new key and value into the cache, after every load of the head (no
+    // other block reads position t of this step)
+    if (lane < nc) {
+      const size_t o = ((size_t)r * T + t) * d + hd * dh + 16 * lane;
+      *(v4i*)(kcache + o) = kapp;
+      *(v4i*)(vcache + o) = vapp;
+    }
   }
 }
 
@@ -810,39 +813,53 @@ __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, in
       n_live_sh = n_live;
       done_sh = fc >= W;
     }
-    __syncthreads();
-    if (!done_sh) {
-      const int n_live = n_live_sh;
-      const int32_t* hcur = st.hist + (size_t)(t & 1) * R * T;
-      int32_t* hnext = st.hist + (size_t)((t + 1) & 1) * R * T;
-      for (int s = wv; s < n_live; s += kUpdWaves) {
-        const int p = b * W + s, par = new_par[s];
-        for (int tp = lane; tp <= t && tp < T; tp += 64) hnext[(size_t)p * T + tp] = tp < t ? hcur[(size_t)par * T + tp] : par;
-        if (lane == 0) {
-          st.score[p] = new_score[s];
-          st.cur_tok[p] = new_tok[s];
-          slot_tok[s] = new_tok[s];
-          if (t < T) {
-            st.tok_hist[(size_t)t * R + p] = new_tok[s];
-            st.par_hist[(size_t)t * R + p] = par;
-          }
+  }
+  __syncthreads();  // the selection (and each slot's current token) visible to every wave
+  // One wave per slot: the slot's history copy (refilled slots) and the next
+  // step's input row (what k_embed and k_ln_quant compute), all of the slot's
+  // loads issued before its first store (the memory counter retires in
+  // order: a load waited for after a store would also wait for the store).
+  const int n_live = active && !done_sh ? n_live_sh : 0;
+  const int32_t* hcur = st.hist + (size_t)(t & 1) * R * T;
+  int32_t* hnext = st.hist + (size_t)((t + 1) & 1) * R * T;
+  for (int s = wv; s < W; s += kUpdWaves) {
+    const int p = b * W + s;
+    const bool refill = s < n_live;
+    const int par = refill ? new_par[s] : p;
+    int tk = refill ? new_tok[s] : slot_tok[s];
+    tk = tk < 0 ? 0 : (tk >= nx.V ? nx.V - 1 : tk);
+    int hv[kMaxAttnLen / 64];
+    if (refill) {
+#pragma unroll
+      for (int i = 0; i < kMaxAttnLen / 64; ++i) hv[i] = hcur[(size_t)par * T + min(lane + 64 * i, t)];
+    }
+    float e[NJ], c = 0.0f;
+    if (prep) {
+      c = nx.c_emb[tk];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) e[j] = (float)nx.E[(size_t)tk * nx.d + min(lane + 64 * j, nx.d - 1)];
+    }
+    if (refill) {
+#pragma unroll
+      for (int i = 0; i < kMaxAttnLen / 64; ++i) {
+        const int tp = lane + 64 * i;
+        if (tp <= t && tp < T) hnext[(size_t)p * T + tp] = tp < t ? hv[i] : par;
+      }
+      if (lane == 0) {
+        st.score[p] = new_score[s];
+        st.cur_tok[p] = new_tok[s];
+        if (t < T) {
+          st.tok_hist[(size_t)t * R + p] = new_tok[s];
+          st.par_hist[(size_t)t * R + p] = par;
         }
       }
     }
-  }
-  __syncthreads();
-  // the next step's input rows: what k_embed and k_ln_quant compute, one wave per row
-  if (prep) {
-    for (int s = wv; s < W; s += kUpdWaves) {
-      const int p = b * W + s;
-      int tk = slot_tok[s];
-      tk = tk < 0 ? 0 : (tk >= nx.V ? nx.V - 1 : tk);
-      const float c = nx.c_emb[tk];
+    if (prep) {
       float v[NJ];
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
         const int i = lane + 64 * j;
-        v[j] = fmaf((float)nx.E[(size_t)tk * nx.d + min(i, nx.d - 1)], c, pe_r[j]);
+        v[j] = fmaf(e[j], c, pe_r[j]);
         if (i < nx.d) nx.x[(size_t)p * nx.d + i] = v[j];
       }
       ln_quant_wave_pre<NJ>(v, nx.d, nx.do_ln, gj, bj, nx.eps, nx.inv_s, nx.a + (size_t)p * nx.d, nullptr);
