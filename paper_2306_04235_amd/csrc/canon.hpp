@@ -140,6 +140,20 @@ __device__ __forceinline__ int unpack_index(unsigned long long key) {
   return (int)(0xffffffffu - (uint32_t)(key & 0xffffffffull));
 }
 
+// Tagged form of a pack_argmax key (index < 2^18): the ordered value, a
+// 14-bit tag, 0x3FFFF - index; 0 (no candidate) becomes the bare tag.
+__device__ __forceinline__ unsigned long long tagged_key(unsigned long long key, unsigned tag) {
+  if (key == 0ull) return (unsigned long long)tag << 18;
+  const uint32_t idx = 0xffffffffu - (uint32_t)(key & 0xffffffffull);
+  return (key & 0xffffffff00000000ull) | ((unsigned long long)tag << 18) | (unsigned long long)(0x3FFFFu - idx);
+}
+__device__ __forceinline__ unsigned key_tag(unsigned long long k) { return (unsigned)(k >> 18) & 0x3FFFu; }
+__device__ __forceinline__ int tagged_index(unsigned long long k) { return (int)(0x3FFFFu - (uint32_t)(k & 0x3FFFFull)); }
+// the pack_argmax key of a tagged key
+__device__ __forceinline__ unsigned long long untag_key(unsigned long long k) {
+  return (k & 0xffffffff00000000ull) | (unsigned long long)(0xffffffffu - (uint32_t)tagged_index(k));
+}
+
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
   auto mx = [](unsigned long long u, unsigned long long w) { return u > w ? u : w; };
   auto join = [](uint32_t lo, uint32_t hi) { return ((unsigned long long)hi << 32) | lo; };

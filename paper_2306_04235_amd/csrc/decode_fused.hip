@@ -137,6 +137,7 @@ __global__ __launch_bounds__(256) void k_greedy_commit_slots(FusedGemv gv) {
     if (threadIdx.x == 0) {
       b = wbest[0];
       for (int w = 1; w < 4; ++w) b = wbest[w] > b ? wbest[w] : b;
+      if (gv.tagged) b = untag_key(b);  // tagged partials of a kernel chain (one step, one tag)
       const int tok = unpack_index(b);
       const int fin = gv.finished[m];
       if (t < gv.T) gv.out_tok[(size_t)t * gv.R + m] = fin ? gv.pad : tok;

@@ -133,6 +133,29 @@ __device__ __forceinline__ void poll_row_data(const StepIn& in, int r, int d, Ro
 // next kernel also waits for, would lag the other blocks by that much.
 __device__ __forceinline__ void loads_done() { __builtin_amdgcn_s_waitcnt(0); }
 
+// The arg-max partials of the previous step's logits kernel (lane i: slots
+// i + 64 k, clamped to the n written ones) once every one carries `want`
+// (tagged keys); bounded like chain_wait.
+__device__ __forceinline__ void poll_partials(const unsigned long long* sl, int n, unsigned want, int* err,
+                                              unsigned long long (&pk)[4]) {
+  const int lane = threadIdx.x & 63;
+  unsigned spins = 0;
+  while (true) {
+    bool ok = true;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      pk[k] = count_load(sl + min(lane + 64 * k, n - 1));
+      ok &= key_tag(pk[k]) == want;
+    }
+    if (__all(ok)) break;
+    if (++spins >= kChainSpinLimit) {
+      if (err) __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
 // Finishes row r from the loaded registers: the pending residual update, the
 // LayerNorm, the store of the updated residual row (block 0: plain, or tagged
 // with out_tag for the counted hand-off), and the int8 codes in a_lds + r * d.
@@ -283,9 +306,18 @@ __device__ __forceinline__ void step_attn_body(const StepIn& in, const StepAttn&
   if (MODE != 0) {
     const int row = min(wave, R - 1);
     const unsigned long long* sl = cm.slots + (size_t)row * cm.nslots;
+    if (cm.tagged) {
+      // no flag wait: the waves that use the partials poll them until every
+      // one carries step t - 1's tag
+      if (wave < R && (MODE == 1 || bid == 0)) {
+        poll_partials(sl, cm.nparts, step_tag(ep, cm.t - 1), in.chain.err, pk);
+        fin = __hip_atomic_load(cm.finished + row, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    } else {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) pk[k] = sl[min(lane + 64 * k, cm.nslots - 1)];
-    fin = cm.finished[row];
+      for (int k = 0; k < 4; ++k) pk[k] = sl[min(lane + 64 * k, cm.nslots - 1)];
+      fin = cm.finished[row];
+    }
   }
   if (MODE != 1) {
     if (in.cnt.count_in > 0) {
@@ -299,7 +331,8 @@ __device__ __forceinline__ void step_attn_body(const StepIn& in, const StepAttn&
     unsigned long long key = pk[0];
 #pragma unroll
     for (int k = 1; k < 4; ++k) key = pk[k] > key ? pk[k] : key;
-    const int tok = unpack_index(wave_max_u64(key));
+    const unsigned long long kmax = wave_max_u64(key);
+    const int tok = cm.tagged ? tagged_index(kmax) : unpack_index(kmax);
     // x = E[tok] c_emb[tok] + PE[t] (padding after the end of the sentence)
     int te = fin ? cm.pad : tok;
     te = te < 0 ? 0 : (te >= cm.V ? cm.V - 1 : te);
@@ -452,7 +485,8 @@ __device__ __forceinline__ void step_attn_body(const StepIn& in, const StepAttn&
     unsigned long long key = pk[0];
 #pragma unroll
     for (int k = 1; k < 4; ++k) key = pk[k] > key ? pk[k] : key;
-    const unsigned long long best = wave_max_u64(key);
+    const unsigned long long kmax = wave_max_u64(key);
+    const unsigned long long best = cm.tagged ? untag_key(kmax) : kmax;
     const int tok = unpack_index(best);
     if (wave < R && lane == 0) {
       const int tc = cm.t - 1;
@@ -612,6 +646,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     }
     co[t] = g.c_out[n];
   }
+  const unsigned tag = (!RAW && g.tagged) ? step_tag(*g.epoch, g.t) : 0u;
   RowRegs<NJ> rr;
   if (!RAW) {
     load_row_consts(in, d, rr);
@@ -656,6 +691,9 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     const unsigned long long w = wave_max_u64(best[m]);
     if (lane == 0) wmax[wave][m] = w;
   }
+  // a tagged partial is the hand-off itself: block 0's accumulator clear
+  // (every wave's share) must have landed before it is stored
+  if (!RAW && g.tagged && blockIdx.x == 0 && in.zero_acc) __builtin_amdgcn_s_waitcnt(0);
   lds_barrier();
   if (threadIdx.x < R) {
     const int m = threadIdx.x;
@@ -666,8 +704,13 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
     if (g.nslots >= (int)gridDim.x) {
       // one partial per block: a plain store, no atomic (atomics on one
       // address serialize), reduced by the consumer
-      if (RAW) slot[blockIdx.x] = b;  // read after the launch, not by a chained kernel
-      else chain_store(slot + blockIdx.x, b);
+      if (RAW) {
+        slot[blockIdx.x] = b;  // read after the launch, not by a chained kernel
+      } else if (g.tagged) {
+        chain_store(slot + blockIdx.x, tagged_key(b, tag));
+      } else {
+        chain_store(slot + blockIdx.x, b);
+      }
     } else {
       // few slots: most blocks find a larger key already there, and the
       // test spares them the serialized atomic
@@ -805,6 +848,8 @@ hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t
   const int blocks = step_logits_blocks(g.V);
   const int cblocks = step_logits_blocks_chained(g.V, g.d);
   if (in.chain.done && g.nslots < cblocks) return hipErrorInvalidValue;
+  // tagged partials: the chained grid (whose block count the consumers poll)
+  if (g.tagged && (!in.chain.done || g.V > kTagMaxV || !g.epoch)) return hipErrorInvalidValue;
   if (!g.x_i8 && !g.frag) return hipErrorInvalidValue;  // the decoder reads the fragment-order copy
 #define MNMT_RAW(DM, FR)                                                                                          \
   if (ev_start || ev_stop)                                                                                        \

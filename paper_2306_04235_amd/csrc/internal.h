@@ -148,6 +148,7 @@ struct FusedGemv {         // a linear layer over the prepared rows, and greedy 
   int32_t* out_len;
   unsigned long long* out_key;  // commit: [T][R] the step's winning arg-max key (or null)
   int T, stop_at_eos, eos, pad;
+  int tagged;              // commit: the slots hold tagged keys (tagged_key)
   int32_t* zero_acc;       // commit: cleared after the step (or null)
   int zero_n;
   float* emb_out;          // commit: embedding of the next input tokens at position t + 1 (or null)
@@ -246,6 +247,9 @@ struct StepAttn {
 struct StepCommit {
   const unsigned long long* slots;  // [R][nslots] arg-max partials of step t - 1
   int nslots;                       // at most 256
+  int tagged;                       // partials are tagged keys (tagged_key), polled until all carry step t - 1's tag
+  int nparts;                       // tagged: partials written per row (one per logits block)
+  const unsigned* epoch;            // tagged: the translation counter of the tags
   const int8_t* E;                  // embedding [V, d], its scales, the position table
   const float* c_emb;
   const float* pe;
@@ -277,7 +281,16 @@ struct StepLogits {
   int nslots;
   const int8_t* x_i8;      // int8 rows [R, d] instead of the StepIn rows (or null)
   bool frag;               // E in fragment order (launch_pack_fragments), else row-major [V, d]
+  int tagged;              // store tagged keys (tagged_key) for step t; V <= kTagMaxV
+  const unsigned* epoch;
+  int t;
 };
+// Tagged arg-max keys: the ordered value in bits 63..32, a 14-bit tag of the
+// (translation, step) in bits 31..18 and 0x3FFFF - index in bits 17..0, so
+// that among keys of one tag the maximum is still the arg max with the
+// smallest index; a partial whose tag is the step's own is that step's.
+constexpr int kTagMaxV = 1 << 18;
+__host__ __device__ inline unsigned step_tag(unsigned epoch, int t) { return (epoch * 256u + (unsigned)t) & 0x3FFFu; }
 bool step_path_fits(int R, int d, int dh, int F, int T, int S);
 bool step_logits_fits(int R, int d);  // R <= 2, d a multiple of 64 up to 512
 int step_logits_blocks(int V);        // blocks (and arg-max partials per row) of launch_step_logits
@@ -545,6 +558,7 @@ struct mnmt_session {
   unsigned long long* step_x64 = nullptr;  // tagged rows of the step kernels [3 n_dec][2][d]
   bool counted_on = true;             // off with MNMT_COUNTED=0: flags between all step kernels
   bool merged_on = true;              // off with MNMT_MERGED_LAYERS=0: three launches per decoder layer
+  bool tagged_on = true;              // off with MNMT_TAGGED=0: layer 0 waits on the logits kernel's flags
   bool chain_on = true;               // off with MNMT_SERIAL_STEPS=1 in the environment
   std::map<std::string, hipGraphExec_t> graphs;
 };

@@ -727,6 +727,13 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     prev_blocks = blocks;
   };
   const bool folded = fold && t > 0 && fold_ok(m);
+  // Tagged arg-max partials (chained, counted steps): the logits kernel's
+  // partials carry a tag of (translation, step), and the next step's layer-0
+  // blocks poll them instead of waiting on the logits kernel's flags.
+  const int V = m->info.vocab;
+  const int lblocks = step_logits_blocks_chained(V, d);
+  const bool tagged = ch && counted && S->tagged_on && fold && fold_ok(m) && V <= kTagMaxV &&
+                      lblocks <= fused_slots_per_row(V) && lblocks <= 256;
   StepCommit cm{};
   if (folded) {
     cm.slots = S->fslots;
@@ -746,6 +753,9 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
     cm.stop_at_eos = stop_at_eos;
     cm.eos = m->info.eos_id;
     cm.pad = m->info.pad_id;
+    cm.tagged = tagged;
+    cm.nparts = lblocks;
+    cm.epoch = S->epoch;
   }
   // merged: each layer's three phases in one launch (launch_step_layer), the
   // phases handing off through the counted words inside it
@@ -781,6 +791,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       } else {
         const hipStream_t ks = ch ? ch->next(in.chain, 3 * (int)l, h, t + 1) : s;
         count_io(in, 3 * (int)l, h);
+        if (cml && tagged) in.chain.wait = nullptr;  // polls the tagged partials instead
         LAUNCH(launch_step_attn(in, at, 1, h, ks, cml));
       }
       if (in.x_out) std::swap(xa, xb);
@@ -836,7 +847,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       const bool last = l + 1 == m->dec.size();
       StepChain c{};
       const hipStream_t ks = ch ? ch->next(c, 3 * (int)l, step_layer_blocks(h, L.w1.N), t + 1, last) : s;
-      if (l == 0) {
+      if (l == 0 && !(cml && tagged)) {  // (tagged: layer 0 polls the partials instead)
         for (StepIn* p : {&ia, &ib}) {
           p->chain.wait = c.wait;
           p->chain.nwait = c.nwait;
@@ -865,6 +876,9 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   g.logits = logits_out;
   g.slots = S->fslots;
   g.nslots = fused_slots_per_row(m->info.vocab);
+  g.tagged = tagged;
+  g.epoch = S->epoch;
+  g.t = t;
   const hipStream_t ks =
       ch ? ch->next(in.chain, 3 * (int)m->dec.size(), step_logits_blocks_chained(g.V, d), t + 1) : s;
   LAUNCH(launch_step_logits(in, g, ks));
@@ -873,6 +887,7 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   gv.t = t;
   gv.slots = S->fslots;
   gv.nslots = fused_slots_per_row(m->info.vocab);
+  gv.tagged = tagged;
   gv.step = S->step;
   gv.out_tok = S->out_tok;
   gv.cur_tok = S->cur_tok;
@@ -1130,6 +1145,10 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   // step instead of one (for comparison)
   const char* merged = std::getenv("MNMT_MERGED_LAYERS");
   S->merged_on = !(merged && std::atoi(merged) == 0);
+  // MNMT_TAGGED=0: the step's first layer waits on the logits kernel's flags
+  // instead of polling its tagged arg-max partials
+  const char* tagged = std::getenv("MNMT_TAGGED");
+  S->tagged_on = !(tagged && std::atoi(tagged) == 0);
   // the encoder accumulators start at zero (each encode leaves them so), the
   // chain error word too
   hipError_t h = hipMemsetAsync(S->enc_acc, 0, enc_acc_bytes(d), S->capture_stream);
