@@ -385,10 +385,17 @@ def sweep_trace_summary(trace_csv, command):
     print("\n".join(out))
 
 
-def beam_throughput(torch, mnmt, G, dev, names=("mobile_beam", "base_beam"), reps=3, check=True):
+# Beam side measurements: (workload, weight bits); 4-bit models are loaded
+# with their weights packed only, so every kernel reads the packed rows.
+BEAM_RUNS = {"mobile_beam": ("mobile_beam", 8), "mobile_beam_w4_packed": ("mobile_beam", 4),
+             "base_beam": ("base_beam", 8)}
+
+
+def beam_throughput(torch, mnmt, G, dev, names=tuple(BEAM_RUNS), reps=3, check=True):
     """The two batched beam-search workloads (mobile: 64 sentences, base: 128;
-    beam 4, length penalty 0.6), each translation one captured graph, inputs
-    resident on the device: one untimed translation, then ``reps`` timed.
+    beam 4, length penalty 0.6), and the mobile one with packed 4-bit weights,
+    each translation one captured graph, inputs resident on the device: one
+    untimed translation, then ``reps`` timed.
     The last translation's shortest sentence is compared with the oracle, and
     a composite roofline (the sum over phases of max(ops / i8 peak, bytes /
     HBM peak), paper_2306_04235_amd.workload.beam_roofline_s) over the steps
@@ -397,10 +404,15 @@ def beam_throughput(torch, mnmt, G, dev, names=("mobile_beam", "base_beam"), rep
 
     from paper_2306_04235_amd import workload as WL
 
+    import dataclasses
+
     res = {}
     for name in names:
-        w = G.WORKLOADS[name]
-        m = mnmt.Model(G.build_model(w.model))
+        wname, bits = BEAM_RUNS[name]
+        w = G.WORKLOADS[wname]
+        mcfg = w.model if bits == 8 else dataclasses.replace(w.model, name=w.model.name + "-w4", w_bits=4)
+        blob = G.build_model(mcfg)
+        m = mnmt.Model(blob, flags=mnmt.LOAD_PACKED_4BIT_ONLY if bits == 4 else 0)
         src, lens = G.workload_inputs(w)
         ts, tl = torch.from_numpy(src).to(dev), torch.from_numpy(lens).to(dev)
         sess = mnmt.Session(m, w.batch, w.s_max, w.steps, w.beam)
@@ -423,13 +435,14 @@ def beam_throughput(torch, mnmt, G, dev, names=("mobile_beam", "base_beam"), rep
             import oracle
 
             i = int(np.argmin(lens))
-            om = oracle.Model(G.build_model(w.model))
+            om = oracle.Model(blob)
             ref = om.beam(src[i:i + 1], lens[i:i + 1], w.beam, w.steps, w.alpha)
             check_tokens(f"{name} sentence {i}", out_np[i:i + 1], len_np[i:i + 1], ref)
         steps_run = int(len_np.max())
         m_dims = WL.Dims(m.info.d_model, m.info.n_heads, m.info.d_ffn, m.info.n_enc, m.info.n_dec, m.info.vocab)
         roof = WL.beam_roofline_s(m_dims, lens, w.beam, steps_run, I8_PEAK_TOPS * 1e12, HBM_PEAK_GBS * 1e9)
-        res[name] = {"workload": w.name, "ms_per_batch": round(el * 1e3, 3), "sentences_per_s": round(w.batch / el, 1),
+        res[name] = {"workload": w.name + ("" if bits == 8 else "-w4-packed"), "arena_bytes": m.arena.numel(),
+                     "ms_per_batch": round(el * 1e3, 3), "sentences_per_s": round(w.batch / el, 1),
                      "output_tokens_per_s": round(toks / el, 1), "batch": w.batch, "beam": w.beam,
                      "max_steps": w.steps, "steps_run": steps_run,
                      "composite_roofline": {"ms": round(roof["seconds"] * 1e3, 4),
@@ -449,7 +462,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-paper-shapes", action="store_true", help="skip the paper-shape side measurements")
     ap.add_argument("--no-beam", action="store_true", help="skip the batched beam-search side measurements")
-    ap.add_argument("--beam-only", nargs="?", const="all", choices=("all", "mobile_beam", "base_beam"),
+    ap.add_argument("--beam-only", nargs="?", const="all", choices=("all", *BEAM_RUNS),
                     help="only the batched beam-search measurements (for profiling), optionally one workload")
     ap.add_argument("--sweep", action="store_true", help="only the quantized-linear sweep (20 shapes, I8 epilogue)")
     ap.add_argument("--counters", action="store_true", help="only the roofline kernel and the copy (for --pmc)")
@@ -488,7 +501,7 @@ def main():
         print(json.dumps({"qlinear_sweep": qlinear_sweep(torch, mnmt, G, dev)}), flush=True)
         return
     if args.beam_only:
-        names = ("mobile_beam", "base_beam") if args.beam_only == "all" else (args.beam_only,)
+        names = tuple(BEAM_RUNS) if args.beam_only == "all" else (args.beam_only,)
         print(json.dumps({"beam_throughput": beam_throughput(torch, mnmt, G, dev, names)}), flush=True)
         return
     w = G.WORKLOADS["mobile"]

@@ -69,8 +69,9 @@
  *   in each group of 16 codes of a row, byte i (i < 8) holds code i in its
  *   low nibble and code i + 8 in its high nibble, each stored plus 8.  The
  *   batch-1 decoder step and the small-batch encoder read them packed and
- *   widen them to int8 in registers; the batched kernels read an int8 copy
- *   that the loader also keeps unless MNMT_LOAD_PACKED_4BIT_ONLY is given.
+ *   widen them to int8 in registers.  The batched kernels read an int8 copy
+ *   that the loader also keeps, or, with MNMT_LOAD_PACKED_4BIT_ONLY, the
+ *   packed rows too (widened on their way to the matrix cores).
  */
 #ifndef MNMT_H
 #define MNMT_H
@@ -152,11 +153,9 @@ typedef struct {
 
 /* Load flags (mnmt_model_bytes_ex, mnmt_model_load_ex).
  * MNMT_LOAD_PACKED_4BIT_ONLY: keep 4-bit weights only in their packed form
- * (half the bytes of int8 codes), without the int8 copy the batched kernels
- * read.  Every linear weight of the file must be 4-bit (else
- * MNMT_E_UNSUPPORTED); sessions of such a model must fit the batch-1 paths:
- * beam 1, max_batch <= 2, max_batch * max_src_len <= 64, source and target
- * lengths <= 128 (mnmt_session_create returns MNMT_E_UNSUPPORTED otherwise). */
+ * (half the bytes of int8 codes), without the int8 copy; every kernel then
+ * reads the packed rows.  Every linear weight of the file must be 4-bit
+ * (else MNMT_E_UNSUPPORTED). */
 #define MNMT_LOAD_PACKED_4BIT_ONLY 1u
 
 /* Validate a model file held in host memory and report the device arena size
@@ -256,6 +255,17 @@ int mnmt_session_tensor(const mnmt_session* session, const char* name, void** d_
  * logits kernel on the matrix cores), larger M the i8 matrix-core kernels. */
 int mnmt_qlinear(const int8_t* d_X, const int8_t* d_W, const float* d_scale, const float* d_bias,
                  int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream);
+
+/* mnmt_qlinear over 4-bit weights (the paper's W-E-A 4-8-8 setting, its
+ * quantization study): d_W4 holds the packed rows [N, K / 2] of the model
+ * file's 4-bit format (in each group of 16 codes of a row, byte i holds code
+ * i in its low nibble and code i + 8 in its high nibble, each plus 8; 8-byte
+ * aligned).  The kernels widen the codes to int8 as they load them, so Y is
+ * what mnmt_qlinear gives for the int8 codes.  Epilogues MNMT_EPI_I32 ..
+ * MNMT_EPI_LOGITS (not the arg-max ones: MNMT_E_UNSUPPORTED); otherwise as
+ * mnmt_qlinear. */
+int mnmt_qlinear_w4(const int8_t* d_X, const uint8_t* d_W4, const float* d_scale, const float* d_bias,
+                    int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream);
 
 /* Number of partial keys per row that MNMT_EPI_ARGMAX_PARTIAL writes for N
  * outputs (one per 128 outputs), or -1 for N < 1. */

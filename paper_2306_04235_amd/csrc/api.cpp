@@ -129,6 +129,26 @@ extern "C" int mnmt_qlinear_timed(const int8_t* d_X, const int8_t* d_W, const fl
   return h == hipSuccess ? MNMT_OK : hip_error(h, "qlinear stop event");
 }
 
+extern "C" int mnmt_qlinear_w4(const int8_t* d_X, const uint8_t* d_W4, const float* d_scale, const float* d_bias,
+                               int M, int K, int N, int epilogue, float gamma, void* d_Y, void* stream) {
+  if (M < 0 || N < 1 || K < 64 || K % 64 || K > 8192)
+    return set_error(MNMT_E_INVALID_ARG, "need M >= 0, N >= 1 and K a multiple of 64 in [64, 8192]");
+  if (epilogue < MNMT_EPI_I32 || epilogue > MNMT_EPI_ARGMAX_PARTIAL_PACKED)
+    return set_error(MNMT_E_INVALID_ARG, "unknown epilogue");
+  if (epilogue > MNMT_EPI_LOGITS)
+    return set_error(MNMT_E_UNSUPPORTED, "4-bit weights take the epilogues MNMT_EPI_I32 .. MNMT_EPI_LOGITS");
+  if (M == 0) return MNMT_OK;
+  const bool needs_bias = epilogue != MNMT_EPI_I32 && epilogue != MNMT_EPI_LOGITS;
+  if (!d_X || !d_W4 || !d_Y || (epilogue != MNMT_EPI_I32 && !d_scale) || (needs_bias && !d_bias))
+    return set_error(MNMT_E_INVALID_ARG, "null device pointer");
+  if (reinterpret_cast<uintptr_t>(d_X) % 16 || reinterpret_cast<uintptr_t>(d_W4) % 8)
+    return set_error(MNMT_E_INVALID_ARG, "X must be 16-byte and W4 8-byte aligned");
+  const EpiArgs e{epilogue, d_Y, N, gamma, nullptr};
+  const hipError_t h = launch_qlinear(d_X, K, reinterpret_cast<const int8_t*>(d_W4), d_scale, d_bias, M, K, N, e,
+                                      static_cast<hipStream_t>(stream), true);
+  return h == hipSuccess ? MNMT_OK : hip_error(h, "qlinear launch");
+}
+
 extern "C" int mnmt_argmax_partials(int N) { return N < 1 ? -1 : step_logits_blocks(N); }
 
 extern "C" size_t mnmt_packed_bytes(int N, int K) { return frag_bytes(N, K); }

@@ -72,6 +72,16 @@ __device__ __forceinline__ int dot16(const int4 a, const int4 b, int acc) {
   acc = __builtin_amdgcn_sdot4(a.w, b.w, acc, false);
   return acc;
 }
+__device__ __forceinline__ int dot16(const v4i a, const int4 b, int acc) {
+  return dot16(make_int4(a.x, a.y, a.z, a.w), b, acc);
+}
+
+// The 16 weight codes of row `row` at column k (a multiple of 16) of an int8
+// [N, K] weight or, W4, of its packed 4-bit rows; zeros where `ok` is false.
+template <bool W4>
+__device__ __forceinline__ WFrag<W4> load_wfrag_if(bool ok, const int8_t* W, size_t row, int K, int k) {
+  return ok ? load_wfrag<W4>(W, row, K, k) : WFrag<W4>{};
+}
 
 // Workgroup barrier that orders LDS accesses only: the fences name the local
 // address space, so the barrier waits for the wave's LDS operations but not

@@ -23,8 +23,9 @@ constexpr int kRows = 8;    // rows per fused step (greedy batch <= 8)
 constexpr int kSlots = 32;  // arg-max slots per row
 
 // MR rows of input, rows of width K <= DMAX (LPR lanes per weight row, at
-// most two 16-byte K chunks per lane), U row groups per wave.
-template <int MR, int DMAX, int U>
+// most two 16-byte K chunks per lane), U row groups per wave; W4: gv.W holds
+// packed 4-bit rows, widened in registers.
+template <int MR, int DMAX, int U, bool W4>
 __global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
   constexpr int LPR = lanes_per_row(DMAX);
   constexpr int RPI = 64 / LPR;
@@ -35,14 +36,14 @@ __global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
   const int R = gv.R, K = gv.K, N = gv.N;
   const int row0 = (blockIdx.x * 4 + wave) * RPI * U;
   // 1. weight loads first
-  int4 wv[2][U];
+  WFrag<W4> wv[2][U];
 #pragma unroll
   for (int ki = 0; ki < 2; ++ki) {
     const int k = kl * 16 + ki * LPR * 16;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int n = row0 + u * RPI + sub;
-      wv[ki][u] = (k < K && n < N) ? *(const int4*)(gv.W + (size_t)n * K + k) : make_int4(0, 0, 0, 0);
+      wv[ki][u] = load_wfrag_if<W4>(k < K && n < N, gv.W, n, K, k);
     }
   }
   // 2. input rows while the loads are in flight
@@ -63,7 +64,7 @@ __global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
         if (m < R) {
           const int4 xv = *(const int4*)(a_lds + m * K + k);
 #pragma unroll
-          for (int u = 0; u < U; ++u) acc[u][m] = dot16(wv[ki][u], xv, acc[u][m]);
+          for (int u = 0; u < U; ++u) acc[u][m] = dot16(wv[ki][u].get(), xv, acc[u][m]);
         }
       }
     }
@@ -167,17 +168,18 @@ __global__ __launch_bounds__(256) void k_greedy_commit_slots(FusedGemv gv) {
 
 // Row groups per wave: large layers (the output projection) get 8 so that
 // one round of about one block per CU has the whole matrix in flight; small
-// layers get 1 for the most blocks.
+// layers (and every packed 4-bit layer) get 1 for the most blocks.
 template <int MR, int DMAX>
 hipError_t launch_u(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
   constexpr int RPI = 64 / lanes_per_row(DMAX);
   const long blocks8 = ((long)gv.N + RPI * 32 - 1) / (RPI * 32);
-  if (blocks8 >= 128) {
-    hipLaunchKernelGGL((k_qgemv_ln<MR, DMAX, 8>), dim3((int)blocks8), dim3(256), 0, s, in, gv);
-  } else {
-    const long blocks1 = ((long)gv.N + RPI * 4 - 1) / (RPI * 4);
-    hipLaunchKernelGGL((k_qgemv_ln<MR, DMAX, 1>), dim3((int)blocks1), dim3(256), 0, s, in, gv);
-  }
+  const long blocks1 = ((long)gv.N + RPI * 4 - 1) / (RPI * 4);
+  if (gv.w4)
+    hipLaunchKernelGGL((k_qgemv_ln<MR, DMAX, 1, true>), dim3((int)blocks1), dim3(256), 0, s, in, gv);
+  else if (blocks8 >= 128)
+    hipLaunchKernelGGL((k_qgemv_ln<MR, DMAX, 8, false>), dim3((int)blocks8), dim3(256), 0, s, in, gv);
+  else
+    hipLaunchKernelGGL((k_qgemv_ln<MR, DMAX, 1, false>), dim3((int)blocks1), dim3(256), 0, s, in, gv);
   return hipGetLastError();
 }
 
@@ -199,7 +201,8 @@ int fused_slots_per_row(int V) { return max(kSlots, step_logits_blocks(V)); }
 
 hipError_t launch_qgemv_ln(const FusedIn& in, const FusedGemv& gv, hipStream_t s) {
   // K chunks per lane must be at most two: K <= 32 * LPR with LPR <= 64
-  if (gv.R < 1 || gv.R > kRows || gv.K > kMaxRowLen || gv.K % 16) return hipErrorInvalidValue;
+  if (gv.R < 1 || gv.R > kRows || gv.K > kMaxRowLen || gv.K % 16 || (gv.w4 && gv.epi == EPI_LOGITS_ARGMAX))
+    return hipErrorInvalidValue;
   if (gv.R == 1) return launch_d<1>(in, gv, s);
   if (gv.R == 2) return launch_d<2>(in, gv, s);
   if (gv.R <= 4) return launch_d<4>(in, gv, s);

@@ -126,7 +126,9 @@ __device__ __forceinline__ void store_fragment(const EpiArgs& e, const v16i& c, 
   }
 }
 
-template <int BN, int BM, int WN, int WM, int EPI>
+// W4: W holds packed 4-bit rows [N, K / 2]; each 16-code chunk is loaded as
+// its 8 packed bytes and widened to int8 on its way into LDS.
+template <int BN, int BM, int WN, int WM, int EPI, bool W4>
 __global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int ldx, const int8_t* __restrict__ W,
                                               int M, int K, int N, const float* __restrict__ scale,
                                               const float* __restrict__ bias, EpiArgs e, int tiles_m, int tiles) {
@@ -160,24 +162,32 @@ __global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int 
     }
   }
 
-  // 32-bit offsets of this thread's 16-byte chunks (the slab adds k0)
+  // 32-bit offsets of this thread's 16-byte chunks (the slab adds k0; in
+  // packed 4-bit rows a chunk is 8 bytes)
+  constexpr int WDIV = W4 ? 2 : 1;
   uint32_t ow[CW], ox[CX];
 #pragma unroll
   for (int i = 0; i < CW; ++i) {
     const int c = tid + 256 * i;
-    ow[i] = (uint32_t)min(n0 + (c >> 2), N - 1) * (uint32_t)K + 16 * (c & 3);
+    ow[i] = (uint32_t)min(n0 + (c >> 2), N - 1) * (uint32_t)(K / WDIV) + 16 / WDIV * (c & 3);
   }
 #pragma unroll
   for (int i = 0; i < CX; ++i) {
     const int c = tid + 256 * i;
     ox[i] = (uint32_t)min(m0 + (c >> 2), M - 1) * (uint32_t)ldx + 16 * (c & 3);
   }
-  v4i rw[CW], rx[CX];
+  WFrag<W4> rw[CW];
+  v4i rx[CX];
   auto gload = [&](int k0) {
-    const int8_t* wk = W + k0;
+    const int8_t* wk = W + k0 / WDIV;
     const int8_t* xk = X + k0;
 #pragma unroll
-    for (int i = 0; i < CW; ++i) rw[i] = *(const v4i*)(wk + ow[i]);
+    for (int i = 0; i < CW; ++i) {
+      if constexpr (W4)
+        rw[i].p = *(const uint2*)(wk + ow[i]);
+      else
+        rw[i].v = *(const v4i*)(wk + ow[i]);
+    }
 #pragma unroll
     for (int i = 0; i < CX; ++i) rx[i] = *(const v4i*)(xk + ox[i]);
   };
@@ -185,7 +195,7 @@ __global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int 
 #pragma unroll
     for (int i = 0; i < CW; ++i) {
       const int c = tid + 256 * i;
-      *(v4i*)(&Ws[buf][(c >> 2) * kLdsRow + 16 * (c & 3)]) = rw[i];
+      *(v4i*)(&Ws[buf][(c >> 2) * kLdsRow + 16 * (c & 3)]) = rw[i].get();
     }
 #pragma unroll
     for (int i = 0; i < CX; ++i) {
@@ -266,7 +276,8 @@ __global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int 
 // the last tile it reloads that tile), so the wait for the prefetch before it
 // goes to LDS does not include the tile's output stores issued after it
 // (loads and stores share one in-order counter).
-template <int EPI, int BN, int BM, int KC, int KCN>
+// W4: packed 4-bit rows, widened on their way into LDS (as k_gemm).
+template <int EPI, int BN, int BM, int KC, int KCN, bool W4>
 __global__ __launch_bounds__(256) void k_gemm_p(const int8_t* X, int ldx, const int8_t* W, int M, int K, int N,
                                                 const float* scale, const float* bias, EpiArgs e, int tiles_m,
                                                 int tiles, int nblk) {
@@ -294,13 +305,14 @@ __global__ __launch_bounds__(256) void k_gemm_p(const int8_t* X, int ldx, const 
   const int l32 = lane & 31, h = lane >> 5;
   const int lrow = tid / CPR, lcol = 16 * (tid % CPR);  // this thread's loads: rows lrow + RPS i, 16 bytes at lcol
 
-  v4i rw[LW], rx[LX];
+  WFrag<W4> rw[LW];
+  v4i rx[LX];
   float rs[(2 * BN + 255) / 256];
   auto gload = [&](int t, int c) {  // c: compile-time after unrolling
     const int m0 = (t % tiles_m) * BM, n0 = (t / tiles_m) * BN;
     const int k0 = c * KC + lcol;
 #pragma unroll
-    for (int i = 0; i < LW; ++i) rw[i] = *(const v4i*)(W + (size_t)(n0 + lrow + RPS * i) * K + k0);
+    for (int i = 0; i < LW; ++i) rw[i] = load_wfrag<W4>(W, (size_t)(n0 + lrow + RPS * i), K, k0);
 #pragma unroll
     for (int i = 0; i < LX; ++i) rx[i] = *(const v4i*)(X + (size_t)(m0 + lrow + RPS * i) * ldx + k0);
     if (c == 0 && EPI != MNMT_EPI_I32) {
@@ -313,7 +325,7 @@ __global__ __launch_bounds__(256) void k_gemm_p(const int8_t* X, int ldx, const 
   };
   auto lstore = [&](int c, int sb) {
 #pragma unroll
-    for (int i = 0; i < LW; ++i) *(v4i*)(&Ws[(lrow + RPS * i) * ROW + lcol]) = rw[i];
+    for (int i = 0; i < LW; ++i) *(v4i*)(&Ws[(lrow + RPS * i) * ROW + lcol]) = rw[i].get();
 #pragma unroll
     for (int i = 0; i < LX; ++i) *(v4i*)(&Xs[(lrow + RPS * i) * ROW + lcol]) = rx[i];
     if (c == 0 && EPI != MNMT_EPI_I32) {
@@ -393,14 +405,14 @@ __global__ __launch_bounds__(256) void k_gemm_p(const int8_t* X, int ldx, const 
   }
 }
 
-template <int BN, int BM, int WN, int WM>
+template <int BN, int BM, int WN, int WM, bool W4>
 hipError_t launch_cfg(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
                       int N, const EpiArgs& e, hipStream_t s) {
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   const int tiles = tiles_m * tiles_n;
   const int grid = (tiles + kXcds - 1) / kXcds * kXcds;
 #define MNMT_GEMM(EPI)                                                                                          \
-  hipLaunchKernelGGL((k_gemm<BN, BM, WN, WM, EPI>), dim3(grid), dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, \
+  hipLaunchKernelGGL((k_gemm<BN, BM, WN, WM, EPI, W4>), dim3(grid), dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, \
                      e, tiles_m, tiles)
   switch (e.kind) {
     case MNMT_EPI_I32: MNMT_GEMM(MNMT_EPI_I32); break;
@@ -415,14 +427,14 @@ hipError_t launch_cfg(const int8_t* X, int ldx, const int8_t* W, const float* sc
   return hipGetLastError();
 }
 
-template <int BN, int BM, int KC, int KCN>
+template <int BN, int BM, int KC, int KCN, bool W4>
 hipError_t launch_persistent(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
                              int K, int N, const EpiArgs& e, hipStream_t s) {
   const int tiles_m = M / BM, tiles = tiles_m * (N / BN);
   // two blocks per CU: 32 CUs per XCD
   const int nblk = min(kXcds * 64, (tiles + kXcds - 1) / kXcds * kXcds);
 #define MNMT_GEMM(EPI)                                                                                    \
-  hipLaunchKernelGGL((k_gemm_p<EPI, BN, BM, KC, KCN>), dim3(nblk), dim3(256), 0, s, X, ldx, W, M, K, N, scale, \
+  hipLaunchKernelGGL((k_gemm_p<EPI, BN, BM, KC, KCN, W4>), dim3(nblk), dim3(256), 0, s, X, ldx, W, M, K, N, scale, \
                      bias, e, tiles_m, tiles, nblk)
   switch (e.kind) {
     case MNMT_EPI_I32: MNMT_GEMM(MNMT_EPI_I32); break;
@@ -684,41 +696,50 @@ hipError_t launch_ws(const int8_t* X, int ldx, const int8_t* W, const float* sca
   return hipGetLastError();
 }
 
-}  // namespace
-
-// The persistent kernel for whole tiles (16-byte aligned rows), K a power-of-two
-// number of chunks and enough tiles for every block; otherwise the
-// largest slab-pipelined tile that still gives about two blocks per CU (256
-// CUs).
-hipError_t launch_gemm(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
-                       int N, const EpiArgs& e, hipStream_t s) {
-  if (M <= 0) return hipSuccess;
-  if (K % kBK) return hipErrorInvalidValue;
+template <bool W4>
+hipError_t launch_tiled(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
+                        int N, const EpiArgs& e, hipStream_t s, bool aligned) {
   auto tiles = [&](int bn, int bm) { return (long)((N + bn - 1) / bn) * ((M + bm - 1) / bm); };
-  const bool int8_out = e.kind == MNMT_EPI_I8 || e.kind == MNMT_EPI_I8_RELU;
-  const bool aligned = (reinterpret_cast<uintptr_t>(e.out) & 15) == 0 && e.ldo % (int8_out ? 16 : 4) == 0;
-  const bool ops_aligned = ldx % 16 == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0 &&
-                           (reinterpret_cast<uintptr_t>(W) & 15) == 0;
-  if (aligned && ops_aligned && K == kWsK && N % 256 == 0 && M % kWsRows == 0 && e.kind != MNMT_EPI_F32_RESID) {
-    const WsPlan p = ws_plan(M, N);
-    if (p.steps_per_block >= kWsMinSteps) return launch_ws(X, ldx, W, scale, bias, M, e, p, s);
-  }
   if (aligned && M % kPBM == 0 && N % kPBN == 0 && tiles(kPBN, kPBM) >= kXcds * 64 && ldx % 16 == 0 &&
       (reinterpret_cast<uintptr_t>(X) & 15) == 0 && (reinterpret_cast<uintptr_t>(W) & 15) == 0 && K % kPKC == 0) {
     switch (K / kPKC) {
-      case 1: return launch_persistent<kPBN, kPBM, kPKC, 1>(X, ldx, W, scale, bias, M, K, N, e, s);
-      case 2: return launch_persistent<kPBN, kPBM, kPKC, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
-      case 4: return launch_persistent<kPBN, kPBM, kPKC, 4>(X, ldx, W, scale, bias, M, K, N, e, s);
-      case 8: return launch_persistent<kPBN, kPBM, kPKC, 8>(X, ldx, W, scale, bias, M, K, N, e, s);
-      case 16: return launch_persistent<kPBN, kPBM, kPKC, 16>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 1: return launch_persistent<kPBN, kPBM, kPKC, 1, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 2: return launch_persistent<kPBN, kPBM, kPKC, 2, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 4: return launch_persistent<kPBN, kPBM, kPKC, 4, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 8: return launch_persistent<kPBN, kPBM, kPKC, 8, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+      case 16: return launch_persistent<kPBN, kPBM, kPKC, 16, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
       default: break;
     }
   }
   constexpr long kFill = 512;
-  if (tiles(256, 128) >= kFill) return launch_cfg<256, 128, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
-  if (tiles(128, 128) >= kFill) return launch_cfg<128, 128, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
-  if (tiles(128, 64) >= kFill) return launch_cfg<128, 64, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
-  return launch_cfg<64, 64, 2, 2>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (tiles(256, 128) >= kFill) return launch_cfg<256, 128, 2, 2, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (tiles(128, 128) >= kFill) return launch_cfg<128, 128, 2, 2, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (tiles(128, 64) >= kFill) return launch_cfg<128, 64, 2, 2, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  return launch_cfg<64, 64, 2, 2, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+}
+
+}  // namespace
+
+// The weight-stationary kernel for K = 256 and long row runs (int8 weights);
+// the persistent kernel for whole tiles (16-byte aligned rows), K a
+// power-of-two number of chunks and enough tiles for every block; otherwise
+// the largest slab-pipelined tile that still gives about two blocks per CU
+// (256 CUs).
+hipError_t launch_gemm(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
+                       int N, const EpiArgs& e, hipStream_t s, bool w4) {
+  if (M <= 0) return hipSuccess;
+  if (K % kBK) return hipErrorInvalidValue;
+  const bool int8_out = e.kind == MNMT_EPI_I8 || e.kind == MNMT_EPI_I8_RELU;
+  const bool aligned = (reinterpret_cast<uintptr_t>(e.out) & 15) == 0 && e.ldo % (int8_out ? 16 : 4) == 0;
+  const bool ops_aligned = ldx % 16 == 0 && (reinterpret_cast<uintptr_t>(X) & 15) == 0 &&
+                           (reinterpret_cast<uintptr_t>(W) & 15) == 0;
+  if (!w4 && aligned && ops_aligned && K == kWsK && N % 256 == 0 && M % kWsRows == 0 &&
+      e.kind != MNMT_EPI_F32_RESID) {
+    const WsPlan p = ws_plan(M, N);
+    if (p.steps_per_block >= kWsMinSteps) return launch_ws(X, ldx, W, scale, bias, M, e, p, s);
+  }
+  return w4 ? launch_tiled<true>(X, ldx, W, scale, bias, M, K, N, e, s, aligned)
+            : launch_tiled<false>(X, ldx, W, scale, bias, M, K, N, e, s, aligned);
 }
 
 }  // namespace mnmt

@@ -35,11 +35,15 @@ struct EpiArgs {
 };
 
 // Tiled matrix-core GEMM for large M (gemm.hip); K a multiple of 64.
+// w4: W holds the packed 4-bit rows [N, K / 2] of the model file (16-code
+// groups, byte i holding codes i and i + 8), widened to int8 on the way to
+// the matrix cores.
 hipError_t launch_gemm(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
-                       int N, const EpiArgs& e, hipStream_t s);
-// Y = epilogue(X[M,K] . W[N,K]^T); ldx = row stride of X in bytes.
+                       int N, const EpiArgs& e, hipStream_t s, bool w4 = false);
+// Y = epilogue(X[M,K] . W[N,K]^T); ldx = row stride of X in bytes; w4 as
+// for launch_gemm (not with the fused arg-max).
 hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias,
-                          int M, int K, int N, const EpiArgs& e, hipStream_t s);
+                          int M, int K, int N, const EpiArgs& e, hipStream_t s, bool w4 = false);
 
 // LayerNorm (optional) + quantization of rows of x [rows, d]:
 // do_ln: y = LN(x) with g, b, eps; else y = x.  q = quant(y, inv_s) if q;
@@ -136,6 +140,7 @@ struct FusedGemv {         // a linear layer over the prepared rows, and greedy 
   int t;                   // decode step (position) of this launch
   int epi;                 // MNMT_EPI_I8, MNMT_EPI_I8_RELU or EPI_LOGITS_ARGMAX
   const int8_t* W;
+  bool w4;                 // W holds packed 4-bit rows (K / 2 bytes each; not with the arg-max)
   const float* scale;
   const float* bias;
   void* out;               // int8 [R, N]; for the arg-max: fp32 logits [R, N] or null
@@ -383,7 +388,8 @@ hipError_t launch_enc_out(const EncIn& in, const EncOut& o, hipStream_t s);
 // rows are prepared (embedding / LayerNorm / quantization) in its prologue.
 bool qgemm_small_fits(int M, int K);
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
-                              const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s);
+                              const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s,
+                              bool w4 = false);
 hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s);
 // Arg-max slots per row of the greedy paths: the spread atomic slots of the
 // 3-8 row path and one partial per block of the 1-2 row logits kernel.
@@ -456,6 +462,13 @@ struct LinearDev {
   int N = 0, K = 0;
   float inv_in = 0.f;  // 1 / input scale (quantization of this layer's input)
 };
+
+// The weight a batched kernel reads: the int8 codes, or the packed 4-bit
+// rows when the model keeps only those (returns true).
+inline bool batched_weights(const LinearDev& a, const int8_t*& w) {
+  w = a.w ? a.w : reinterpret_cast<const int8_t*>(a.w4);
+  return a.w == nullptr;
+}
 
 // A 1-2 row kernel's pair of weights: the packed 4-bit rows when both have
 // them (returns true), else the int8 codes.

@@ -78,7 +78,8 @@ __device__ __forceinline__ void epilogue_store(const EpiArgs& e, int m, int n, i
 
 // ---------------------------------------------------------------------------
 // qgemv: MR = max rows of X, LPR = lanes per weight row, U = row groups per wave
-template <int MR, int LPR, int U>
+// W4: W holds packed 4-bit rows (K / 2 bytes each), widened in registers.
+template <int MR, int LPR, int U, bool W4>
 __global__ __launch_bounds__(256) void k_qgemv(const int8_t* __restrict__ X, int ldx, const int8_t* __restrict__ W,
                                                int M, int K, int N, const float* __restrict__ scale,
                                                const float* __restrict__ bias, EpiArgs e) {
@@ -95,18 +96,18 @@ __global__ __launch_bounds__(256) void k_qgemv(const int8_t* __restrict__ X, int
     for (int m = 0; m < MR; ++m) acc[u][m] = 0;
 
   for (int k = kl * 16; k < K; k += LPR * 16) {
-    int4 wv[U];
+    WFrag<W4> wv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int n = row0 + u * RPI + sub;
-      wv[u] = n < N ? *(const int4*)(W + (size_t)n * K + k) : make_int4(0, 0, 0, 0);
+      wv[u] = load_wfrag_if<W4>(n < N, W, n, K, k);
     }
 #pragma unroll
     for (int m = 0; m < MR; ++m) {
       if (m < M) {
         const int4 xv = *(const int4*)(X + (size_t)m * ldx + k);
 #pragma unroll
-        for (int u = 0; u < U; ++u) acc[u][m] = dot16(wv[u], xv, acc[u][m]);
+        for (int u = 0; u < U; ++u) acc[u][m] = dot16(wv[u].get(), xv, acc[u][m]);
       }
     }
   }
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(256) void k_qgemv(const int8_t* __restrict__ X, int
   }
 }
 
-template <int MR, int LPR>
+template <int MR, int LPR, bool W4>
 hipError_t gemv_u(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
                   int N, const EpiArgs& e, hipStream_t s) {
   constexpr int RPI = 64 / LPR;
@@ -156,28 +157,28 @@ hipError_t gemv_u(const int8_t* X, int ldx, const int8_t* W, const float* scale,
   const long waves4 = ((long)N + RPI * 4 - 1) / (RPI * 4);
   if (waves4 >= 1024) {
     const int blocks = (int)((waves4 + 3) / 4);
-    hipLaunchKernelGGL((k_qgemv<MR, LPR, 4>), dim3(blocks), dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, e);
+    hipLaunchKernelGGL((k_qgemv<MR, LPR, 4, W4>), dim3(blocks), dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, e);
   } else if (waves4 * 2 >= 1024) {
     const long waves = ((long)N + RPI * 2 - 1) / (RPI * 2);
-    hipLaunchKernelGGL((k_qgemv<MR, LPR, 2>), dim3((int)((waves + 3) / 4)), dim3(256), 0, s, X, ldx, W, M, K, N,
+    hipLaunchKernelGGL((k_qgemv<MR, LPR, 2, W4>), dim3((int)((waves + 3) / 4)), dim3(256), 0, s, X, ldx, W, M, K, N,
                        scale, bias, e);
   } else {
     const long waves = ((long)N + RPI - 1) / RPI;
-    hipLaunchKernelGGL((k_qgemv<MR, LPR, 1>), dim3((int)((waves + 3) / 4)), dim3(256), 0, s, X, ldx, W, M, K, N,
+    hipLaunchKernelGGL((k_qgemv<MR, LPR, 1, W4>), dim3((int)((waves + 3) / 4)), dim3(256), 0, s, X, ldx, W, M, K, N,
                        scale, bias, e);
   }
   return hipGetLastError();
 }
 
-template <int MR>
+template <int MR, bool W4>
 hipError_t gemv_lpr(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
                     int N, const EpiArgs& e, hipStream_t s) {
   const int chunks = K / 16;
-  if (chunks >= 64) return gemv_u<MR, 64>(X, ldx, W, scale, bias, M, K, N, e, s);
-  if (chunks >= 32) return gemv_u<MR, 32>(X, ldx, W, scale, bias, M, K, N, e, s);
-  if (chunks >= 16) return gemv_u<MR, 16>(X, ldx, W, scale, bias, M, K, N, e, s);
-  if (chunks >= 8) return gemv_u<MR, 8>(X, ldx, W, scale, bias, M, K, N, e, s);
-  return gemv_u<MR, 4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (chunks >= 64) return gemv_u<MR, 64, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (chunks >= 32) return gemv_u<MR, 32, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (chunks >= 16) return gemv_u<MR, 16, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (chunks >= 8) return gemv_u<MR, 8, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  return gemv_u<MR, 4, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -191,7 +192,8 @@ constexpr int kSmallMaxK = 1024;
 
 // WAVES 4: a 32x32 tile per block; WAVES 1 (no LN): a 16x16 tile per
 // one-wave block, four times the blocks over the same waves.
-template <bool LN, int KMAX, int WAVES = 4>  // K <= KMAX
+// W4: W holds packed 4-bit rows (K / 2 bytes each), widened in registers.
+template <bool LN, int KMAX, int WAVES = 4, bool W4 = false>  // K <= KMAX
 __global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const int8_t* __restrict__ X, int ldx,
                                                             const int8_t* __restrict__ W, int M, int K, int N,
                                                             const float* __restrict__ scale,
@@ -206,10 +208,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const in
   const int nk = K / 64;
   const int col = n0 + 16 * wn + (lane & 15);
   const int koff = 16 * (lane >> 4);
-  v4i bf[NK];
+  WFrag<W4> bf[NK];
 #pragma unroll
-  for (int kk = 0; kk < NK; ++kk)
-    bf[kk] = (kk < nk && col < N) ? *(const v4i*)(W + (size_t)col * K + kk * 64 + koff) : v4i{0, 0, 0, 0};
+  for (int kk = 0; kk < NK; ++kk) bf[kk] = load_wfrag_if<W4>(kk < nk && col < N, W, col, K, kk * 64 + koff);
   const int arow = m0 + 16 * wm + (lane & 15);
   // the epilogue's operands (clamped indexes, unused past M or N)
   EpiPre pre;
@@ -237,7 +238,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const in
     for (int kk = 0; kk < NK; ++kk) {
       if (kk < nk) {
         const v4i a = lr < rows ? *(const v4i*)(As + lr * KP + kk * 64 + koff) : v4i{0, 0, 0, 0};
-        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bf[kk], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, bf[kk].get(), acc, 0, 0, 0);
       }
     }
   } else {
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const in
       af[kk] = (kk < nk && arow < M) ? *(const v4i*)(X + (size_t)arow * ldx + kk * 64 + koff) : v4i{0, 0, 0, 0};
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk)
-      if (kk < nk) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[kk], bf[kk], acc, 0, 0, 0);
+      if (kk < nk) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[kk], bf[kk].get(), acc, 0, 0, 0);
   }
   // 16x16 fragment: element i of lane l sits at row 4*(l/16) + i, column l%16
 #pragma unroll
@@ -278,7 +279,7 @@ bool qgemm_rows_fit(int M, int K, int N) {
 }
 
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
-                              const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s) {
+                              const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s, bool w4) {
   if (M < 1 || M > (in ? 64 : kSmallMaxRows) || K > kSmallMaxK || K % 64 || (in && K > kMaxRowLen))
     return hipErrorInvalidValue;
   // 65-256 rows (the mobile beam decoder): one-wave blocks of 16x16 (at 512
@@ -286,14 +287,22 @@ hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const
   const bool one = !in && M > 64 && M <= 256;
   const dim3 grid = one ? dim3((N + 15) / 16, (M + 15) / 16) : dim3((N + 31) / 32, (M + 31) / 32);
   const FusedIn none{};
-#define MNMT_SMALL(KM)                                                                                       \
-  if (in)                                                                                                    \
-    hipLaunchKernelGGL((k_qgemm_small<true, KM>), grid, dim3(256), 0, s, *in, X, ldx, W, M, K, N, scale, bias, e); \
-  else if (one)                                                                                              \
-    hipLaunchKernelGGL((k_qgemm_small<false, KM, 1>), grid, dim3(64), 0, s, none, X, ldx, W, M, K, N, scale, bias, \
-                       e);                                                                                   \
-  else                                                                                                       \
-    hipLaunchKernelGGL((k_qgemm_small<false, KM>), grid, dim3(256), 0, s, none, X, ldx, W, M, K, N, scale, bias, e);
+#define MNMT_SMALL_W(KM, W4)                                                                                   \
+  if (in)                                                                                                      \
+    hipLaunchKernelGGL((k_qgemm_small<true, KM, 4, W4>), grid, dim3(256), 0, s, *in, X, ldx, W, M, K, N, scale, \
+                       bias, e);                                                                               \
+  else if (one)                                                                                                \
+    hipLaunchKernelGGL((k_qgemm_small<false, KM, 1, W4>), grid, dim3(64), 0, s, none, X, ldx, W, M, K, N, scale, \
+                       bias, e);                                                                               \
+  else                                                                                                         \
+    hipLaunchKernelGGL((k_qgemm_small<false, KM, 4, W4>), grid, dim3(256), 0, s, none, X, ldx, W, M, K, N, scale, \
+                       bias, e);
+#define MNMT_SMALL(KM)      \
+  if (w4) {                 \
+    MNMT_SMALL_W(KM, true)  \
+  } else {                  \
+    MNMT_SMALL_W(KM, false) \
+  }
   switch (row_class(K)) {
     case 64: MNMT_SMALL(64) break;
     case 128: MNMT_SMALL(128) break;
@@ -303,22 +312,30 @@ hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const
     default: MNMT_SMALL(1024) break;
   }
 #undef MNMT_SMALL
+#undef MNMT_SMALL_W
   return hipGetLastError();
 }
 
+template <bool W4>
+hipError_t gemv_rows(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
+                     int N, const EpiArgs& e, hipStream_t s) {
+  if (M == 1) return gemv_lpr<1, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (M == 2) return gemv_lpr<2, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  if (M <= 4) return gemv_lpr<4, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+  return gemv_lpr<8, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
+}
+
 hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
-                          int K, int N, const EpiArgs& e, hipStream_t s) {
+                          int K, int N, const EpiArgs& e, hipStream_t s, bool w4) {
   if (M <= 0) return hipSuccess;
-  if (M <= 8) {
-    if (M == 1) return gemv_lpr<1>(X, ldx, W, scale, bias, M, K, N, e, s);
-    if (M == 2) return gemv_lpr<2>(X, ldx, W, scale, bias, M, K, N, e, s);
-    if (M <= 4) return gemv_lpr<4>(X, ldx, W, scale, bias, M, K, N, e, s);
-    return gemv_lpr<8>(X, ldx, W, scale, bias, M, K, N, e, s);
-  }
+  if (w4 && (e.kind == EPI_LOGITS_ARGMAX || K % 64)) return hipErrorInvalidValue;
+  if (M <= 8)
+    return w4 ? gemv_rows<true>(X, ldx, W, scale, bias, M, K, N, e, s)
+              : gemv_rows<false>(X, ldx, W, scale, bias, M, K, N, e, s);
   if (e.kind == EPI_LOGITS_ARGMAX) return hipErrorInvalidValue;  // arg-max fusion is a batch-1 path
   if (qgemm_small_fits(M, K) || qgemm_rows_fit(M, K, N))
-    return launch_qgemm_small(nullptr, X, ldx, W, scale, bias, M, K, N, e, s);
-  return launch_gemm(X, ldx, W, scale, bias, M, K, N, e, s);
+    return launch_qgemm_small(nullptr, X, ldx, W, scale, bias, M, K, N, e, s, w4);
+  return launch_gemm(X, ldx, W, scale, bias, M, K, N, e, s, w4);
 }
 
 }  // namespace mnmt

@@ -41,16 +41,6 @@ struct Plan {
 
 int validate_cfg(const mnmt_model* m, const mnmt_session_cfg* c) {
   if (!m || !c) return set_error(MNMT_E_INVALID_ARG, "null model or session config");
-  if (m->packed_only) {
-    const int d = m->info.d_model, F = m->info.d_ffn;
-    const int rows = c->max_batch * c->max_src_len;
-    if (c->beam != 1 || c->max_batch > 2 || rows > 64 ||
-        !step_path_fits(c->max_batch, d, m->dh, F, c->max_tgt_len, c->max_src_len) ||
-        !enc_small_fits(rows, c->max_src_len, d, m->dh, F) || (int)m->dec.size() > EncOut::kMaxLayers)
-      return set_error(MNMT_E_UNSUPPORTED,
-                       "a model loaded with packed 4-bit weights only runs the batch-1 paths: beam 1, "
-                       "max_batch <= 2, max_batch * max_src_len <= 64, lengths <= 128");
-  }
   const int P = m->info.max_pos;
   if (c->max_batch < 1 || c->max_batch > 65536 || c->max_src_len < 1 || c->max_src_len > 256 ||
       c->max_src_len > P || c->max_tgt_len < 1 || c->max_tgt_len > 256 || c->max_tgt_len > P || c->beam < 1 ||
@@ -155,7 +145,9 @@ hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 int qlin(const LinearDev& L, const int8_t* X, int M, int kind, void* out, float gamma, hipStream_t s,
          unsigned long long* argmax = nullptr) {
   EpiArgs e{kind, out, L.N, gamma, argmax};
-  LAUNCH(launch_qlinear(X, L.K, L.w, L.scale, L.bias, M, L.K, L.N, e, s));
+  const int8_t* w;
+  const bool w4 = batched_weights(L, w);
+  LAUNCH(launch_qlinear(X, L.K, w, L.scale, L.bias, M, L.K, L.N, e, s, w4));
   return MNMT_OK;
 }
 
@@ -224,7 +216,9 @@ int run_encoder_small(mnmt_session* S, hipStream_t s) {
   };
   auto small = [&](const FusedIn* in, const int8_t* X, const LinearDev& L, int kind, void* out, float gamma) {
     EpiArgs e{kind, out, L.N, gamma, nullptr};
-    return launch_qgemm_small(in, X, L.K, L.w, L.scale, L.bias, rows, L.K, L.N, e, s);
+    const int8_t* w;
+    const bool w4 = batched_weights(L, w);
+    return launch_qgemm_small(in, X, L.K, w, L.scale, L.bias, rows, L.K, L.N, e, s, w4);
   };
   for (size_t l = 0; l < m->enc.size(); ++l) {
     const LayerDev& L = m->enc[l];
@@ -564,7 +558,7 @@ int greedy_step_fused(mnmt_session* S, int R, int t, int stop_at_eos, float* log
     gv.N = L.N;
     gv.t = t;
     gv.epi = epi;
-    gv.W = L.w;
+    gv.w4 = batched_weights(L, gv.W);
     gv.scale = L.scale;
     gv.bias = L.bias;
     gv.out = out;

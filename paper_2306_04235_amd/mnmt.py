@@ -21,7 +21,7 @@ LOAD_PACKED_4BIT_ONLY = 1
 
 EXPORTS = ("mnmt_model_bytes", "mnmt_model_load", "mnmt_model_bytes_ex", "mnmt_model_load_ex", "mnmt_model_get_info", "mnmt_model_free", "mnmt_session_bytes",
            "mnmt_session_create", "mnmt_session_free", "mnmt_encode", "mnmt_decode_step", "mnmt_translate",
-           "mnmt_session_status", "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_timed",
+           "mnmt_session_status", "mnmt_session_tensor", "mnmt_qlinear", "mnmt_qlinear_w4", "mnmt_qlinear_timed",
            "mnmt_argmax_partials", "mnmt_packed_bytes", "mnmt_pack_weights", "mnmt_logits_argmax_noalloc",
            "mnmt_fold_requant", "mnmt_debug_canon", "mnmt_debug_read", "mnmt_status_str", "mnmt_last_error")
 
@@ -78,6 +78,7 @@ def lib():
         L.mnmt_session_tensor.argtypes = [vp, C.c_char_p, C.POINTER(vp), C.POINTER(sz)]
         L.mnmt_session_status.argtypes = [vp, vp]
         L.mnmt_qlinear.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp]
+        L.mnmt_qlinear_w4.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp]
         L.mnmt_qlinear_timed.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, f32, vp, vp, vp, vp]
         L.mnmt_argmax_partials.argtypes = [i32]
         L.mnmt_packed_bytes.argtypes = [i32, i32]
@@ -146,6 +147,21 @@ def mnmt_qlinear(X, W, scale, bias, epilogue, gamma=1.0, out=None, stream=None, 
         out = torch.empty((M, N), dtype=dt, device=X.device)
     _check(lib().mnmt_qlinear(_ptr(X), _ptr(W), _ptr(scale), _ptr(bias), M, K, N, epilogue, float(gamma),
                               _ptr(out), _stream(stream)), "mnmt_qlinear")
+    return out
+
+
+def mnmt_qlinear_w4(X, W4, scale, bias, epilogue, gamma=1.0, out=None, stream=None):
+    """Y = epilogue(X W^T) for int8 CUDA tensor X [M, K] and W's packed 4-bit
+    rows W4 uint8 [N, K / 2] (the model file's format)."""
+    import torch
+
+    M, K = X.shape
+    N = W4.shape[0]
+    if out is None:
+        dt = {EPI_I32: torch.int32, EPI_I8: torch.int8, EPI_I8_RELU: torch.int8}.get(epilogue, torch.float32)
+        out = torch.empty((M, N), dtype=dt, device=X.device)
+    _check(lib().mnmt_qlinear_w4(_ptr(X), _ptr(W4), _ptr(scale), _ptr(bias), M, K, N, epilogue, float(gamma),
+                                 _ptr(out), _stream(stream)), "mnmt_qlinear_w4")
     return out
 
 

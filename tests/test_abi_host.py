@@ -18,7 +18,7 @@ from .conftest import ROOT, model_blob
 def _declared():
     with open(os.path.join(ROOT, "include", "mnmt.h")) as f:
         text = f.read()
-    return sorted(set(re.findall(r"\b(mnmt_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(mnmt_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_library_exports_every_declared_symbol():

@@ -115,6 +115,63 @@ def test_qlinear_all_epilogues(torch_dev, M, K, N):
     assert np.array_equal(got[rows].view(np.uint32), ref.view(np.uint32))
 
 
+W4_SHAPES = [(1, 256, 1024), (2, 2048, 77), (4, 1024, 256), (7, 64, 33), (33, 192, 257), (64, 512, 2048),
+             (130, 320, 1000), (256, 256, 768), (512, 512, 512), (1000, 256, 1500), (3840, 256, 768),
+             (2048, 1024, 300), (2048, 256, 8192), (8192, 512, 2048)]
+
+
+@pytest.mark.parametrize("M,K,N", W4_SHAPES, ids=lambda v: str(v))
+def test_qlinear_4bit_weights(torch_dev, M, K, N):
+    """4-bit weights (W-E-A 4-8-8) read packed by every quantized-linear path:
+    the wavefront-reduction GEMV (M <= 8), the one-round-trip matrix-core
+    kernel (its 32x32 and one-wave 16x16 blocks), the slab-pipelined GEMM and
+    the persistent GEMM (the last two shapes).  The codes in [-7, 7] are packed
+    as the model file stores them; the int32 sums and every epilogue equal the
+    oracle's on the codes."""
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+    from synth.modelfile import pack_int4
+
+    print(f"qlinear 4-bit M={M} K={K} N={N}", flush=True)
+    X, _, mult, bias = G.sweep_case(M, K, N, seed=41)
+    codes = np.random.Generator(np.random.PCG64(M * 7 + K * 3 + N)).integers(-7, 8, size=(N, K)).astype(np.int8)
+    W4 = np.frombuffer(pack_int4(codes), np.uint8).reshape(N, K // 2).copy()
+    tX, tW4 = _gpu(torch, dev, X), _gpu(torch, dev, W4)
+    rows = _rows_to_check(M, np.random.default_rng(M + 5))
+    mult4 = (mult * 127.0 / 7.0).astype(np.float32)  # outputs span about the same codes as int8 weights
+    tm, tb = _gpu(torch, dev, mult4), _gpu(torch, dev, bias)
+
+    def run(epi, scale=tm, gamma=1.0, out=None):
+        y = mnmt.mnmt_qlinear_w4(tX, tW4, scale, tb, epi, gamma=gamma, out=out)
+        torch.cuda.synchronize()
+        return y.cpu().numpy()[rows]
+
+    assert np.array_equal(run(mnmt.EPI_I32), oracle.qgemm_i32(X[rows], codes))
+    for epi, oepi in ((mnmt.EPI_I8, oracle.EPI_I8), (mnmt.EPI_I8_RELU, oracle.EPI_I8_RELU)):
+        assert np.array_equal(run(epi), oracle.qlinear(X[rows], codes, mult4, bias, oepi))
+    dq = (mult4 * 1e-3).astype(np.float32)
+    for epi in (mnmt.EPI_F32, mnmt.EPI_LOGITS):
+        ref = oracle.qlinear(X[rows], codes, dq, bias, epi)
+        assert np.array_equal(run(epi, _gpu(torch, dev, dq)).view(np.uint32), ref.view(np.uint32))
+    resid = np.random.default_rng(6).normal(0, 1, (M, N)).astype(np.float32)
+    got = run(mnmt.EPI_F32_RESID, _gpu(torch, dev, dq), 0.75, _gpu(torch, dev, resid))
+    ref = oracle.qlinear(X[rows], codes, dq, bias, oracle.EPI_F32_RESID, gamma=0.75, resid=resid[rows])
+    assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+def test_qlinear_4bit_rejects_argmax(torch_dev):
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    X = torch.zeros((1, 64), dtype=torch.int8, device=dev)
+    W4 = torch.zeros((16, 32), dtype=torch.uint8, device=dev)
+    sc = torch.ones(16, dtype=torch.float32, device=dev)
+    for epi in (mnmt.EPI_ARGMAX, mnmt.EPI_ARGMAX_PARTIAL, mnmt.EPI_ARGMAX_PARTIAL_PACKED):
+        with pytest.raises(mnmt.MnmtError) as e:
+            mnmt.mnmt_qlinear_w4(X, W4, sc, None, epi, out=torch.zeros(16, dtype=torch.int64, device=dev))
+        assert e.value.status == mnmt.E_UNSUPPORTED
+
+
 @pytest.mark.parametrize("M,K,N", [(2048, 256, 8192), (1024, 1024, 16384), (768, 2048, 22016), (4096, 512, 4096)],
                          ids=lambda v: str(v))
 def test_qlinear_persistent_gemm_epilogues(torch_dev, M, K, N):

@@ -301,13 +301,12 @@ def test_paper_model_shapes_greedy(torch_dev, cfg):
     _greedy_check(torch, dev, cfg, src, lens, 30)
 
 
-def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None, parallel=False):
+def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None, parallel=False, flags=0):
     from paper_2306_04235_amd import mnmt
 
     from .oracle_pool import beam_many
 
-
-    om, gm = _pair(cfg)
+    om, gm = _pair(cfg, flags)
     B, S = src.shape
     print(f"beam {cfg if isinstance(cfg, str) else cfg.name} B={B} S={S} W={W} T={steps}", flush=True)
     sess = mnmt.Session(gm, B, S, steps, W)
@@ -401,7 +400,7 @@ def test_4bit_packed_only_models(torch_dev):
     (half the int8 model's linear-weight bytes) and the batch-1 decoder and
     small-batch encoder kernels widen them in registers: per-step logits and
     tokens equal the oracle's on the mobile shape and on the varied model at
-    one and two rows; sessions beyond those paths are refused."""
+    one and two rows."""
     import dataclasses
 
     from paper_2306_04235_amd import mnmt
@@ -419,10 +418,31 @@ def test_4bit_packed_only_models(torch_dev):
         src, lens = G.make_sources(var4.vocab, B, [30, 21][:B], seed=95 + B, s_max=30)
         out = _greedy_check(torch, dev, var4, src, lens, 30, flags=mnmt.LOAD_PACKED_4BIT_ONLY)
         assert len(set(out[0].tolist())) >= 3
-    for mb, ms, beam in ((1, 30, 4), (3, 8, 1), (2, 40, 1)):
-        with pytest.raises(mnmt.MnmtError) as e:
-            mnmt.Session(gm, mb, ms, 30, beam)
-        assert e.value.status == mnmt.E_UNSUPPORTED
+
+
+def test_4bit_packed_only_batched_paths(torch_dev):
+    """Packed-only 4-bit models on the batched paths, which then read the
+    packed rows too: 3-row greedy steps (the fused GEMV), beam search on a
+    small model, and the mobile beam workload (64 sentences of 10-60 tokens:
+    the encoder's 3840-row projections on the tiled GEMM, the 256-row beam
+    decoder on the one-wave matrix-core blocks), a dozen sentences of it
+    against the oracle, shortest and longest included."""
+    from paper_2306_04235_amd import mnmt
+
+    torch, dev = torch_dev
+    flags = mnmt.LOAD_PACKED_4BIT_ONLY
+    div4 = dataclasses.replace(DIVERSE, name="diverse-w4", w_bits=4)
+    src, lens = G.make_sources(div4.vocab, 3, [9, 5, 7], seed=31, s_max=9)
+    _greedy_check(torch, dev, div4, src, lens, 10, flags=flags)
+    _beam_check(torch, dev, div4, src, lens, 2, 8, 0.6, flags=flags)
+    src, lens = G.make_sources(div4.vocab, 12, [9, 5, 7, 16, 3, 11, 8, 8, 2, 16, 12, 6], seed=32, s_max=16)
+    _greedy_check(torch, dev, div4, src, lens, 6, flags=flags)
+    mob4 = dataclasses.replace(G.MOBILE, name="mobile-w4", w_bits=4)
+    w = G.WORKLOADS["mobile_beam"]
+    src, lens = G.workload_inputs(w)
+    order = np.argsort(lens, kind="stable")
+    idx = sorted({int(order[0]), int(order[-1]), *range(0, 64, 6)})
+    _beam_check(torch, dev, mob4, src, lens, w.beam, w.steps, w.alpha, sample=idx, parallel=True, flags=flags)
 
 
 SHARED = G.ModelConfig("shared-preln", 64, 4, 128, 4, 3, 500, ln_post=0, seed=82, random_gamma=True,
