@@ -127,11 +127,15 @@ __device__ __forceinline__ void store_fragment(const EpiArgs& e, const v16i& c, 
 }
 
 // W4: W holds packed 4-bit rows [N, K / 2]; each 16-code chunk is loaded as
-// its 8 packed bytes and widened to int8 on its way into LDS.
+// its 8 packed bytes and widened to int8 on its way into LDS.  K split
+// (gridDim.y > 1, MNMT_EPI_I32): block row y takes columns [y kb, (y + 1) kb)
+// of K (the row length) and stores its int32 partial sums into slice y of
+// e.out, M * e.ldo words apart.
 template <int BN, int BM, int WN, int WM, int EPI, bool W4>
 __global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int ldx, const int8_t* __restrict__ W,
                                               int M, int K, int N, const float* __restrict__ scale,
-                                              const float* __restrict__ bias, EpiArgs e, int tiles_m, int tiles) {
+                                              const float* __restrict__ bias, EpiArgs e, int tiles_m, int tiles,
+                                              int kb) {
   static_assert(WN * WM == 4, "4 waves");
   constexpr int TN = BN / WN, TM = BM / WM;  // wave tile
   constexpr int FN = TN / 32, FM = TM / 32;  // 32x32 fragments per wave
@@ -178,9 +182,11 @@ __global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int 
   }
   WFrag<W4> rw[CW];
   v4i rx[CX];
+  const int kbeg = blockIdx.y * kb;  // this block's first K column
+  if (gridDim.y > 1) e.out = (int*)e.out + (size_t)blockIdx.y * M * e.ldo;
   auto gload = [&](int k0) {
-    const int8_t* wk = W + k0 / WDIV;
-    const int8_t* xk = X + k0;
+    const int8_t* wk = W + (kbeg + k0) / WDIV;
+    const int8_t* xk = X + kbeg + k0;
 #pragma unroll
     for (int i = 0; i < CW; ++i) {
       if constexpr (W4)
@@ -210,7 +216,7 @@ __global__ __launch_bounds__(256) void k_gemm(const int8_t* __restrict__ X, int 
 #pragma unroll
     for (int i = 0; i < FM; ++i) acc[j][i] = v16i{};
 
-  const int slabs = K / kBK;
+  const int slabs = kb / kBK;
   gload(0);
   lstore(0);
   __syncthreads();
@@ -407,13 +413,13 @@ __global__ __launch_bounds__(256) void k_gemm_p(const int8_t* X, int ldx, const 
 
 template <int BN, int BM, int WN, int WM, bool W4>
 hipError_t launch_cfg(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
-                      int N, const EpiArgs& e, hipStream_t s) {
+                      int N, const EpiArgs& e, hipStream_t s, int splits = 1) {
   const int tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
   const int tiles = tiles_m * tiles_n;
   const int grid = (tiles + kXcds - 1) / kXcds * kXcds;
 #define MNMT_GEMM(EPI)                                                                                          \
-  hipLaunchKernelGGL((k_gemm<BN, BM, WN, WM, EPI, W4>), dim3(grid), dim3(256), 0, s, X, ldx, W, M, K, N, scale, bias, \
-                     e, tiles_m, tiles)
+  hipLaunchKernelGGL((k_gemm<BN, BM, WN, WM, EPI, W4>), dim3(grid, splits), dim3(256), 0, s, X, ldx, W, M, K, N, \
+                     scale, bias, e, tiles_m, tiles, K / splits)
   switch (e.kind) {
     case MNMT_EPI_I32: MNMT_GEMM(MNMT_EPI_I32); break;
     case MNMT_EPI_I8: MNMT_GEMM(MNMT_EPI_I8); break;
@@ -725,6 +731,15 @@ hipError_t launch_tiled(const int8_t* X, int ldx, const int8_t* W, const float* 
 // power-of-two number of chunks and enough tiles for every block; otherwise
 // the largest slab-pipelined tile that still gives about two blocks per CU
 // (256 CUs).
+hipError_t launch_gemm_split(const int8_t* X, int ldx, const int8_t* W, int M, int K, int N, int splits,
+                             int32_t* part, hipStream_t s, bool w4) {
+  if (M <= 0) return hipSuccess;
+  if (splits < 1 || K % (splits * kBK)) return hipErrorInvalidValue;
+  const EpiArgs e{MNMT_EPI_I32, part, N, 1.f, nullptr};
+  return w4 ? launch_cfg<64, 64, 2, 2, true>(X, ldx, W, nullptr, nullptr, M, K, N, e, s, splits)
+            : launch_cfg<64, 64, 2, 2, false>(X, ldx, W, nullptr, nullptr, M, K, N, e, s, splits);
+}
+
 hipError_t launch_gemm(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M, int K,
                        int N, const EpiArgs& e, hipStream_t s, bool w4) {
   if (M <= 0) return hipSuccess;

@@ -390,6 +390,37 @@ bool qgemm_small_fits(int M, int K);
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
                               const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s,
                               bool w4 = false);
+// Long-K linear layers of the batched decoder (the feed-forward W2 of wide
+// models): K split into kSplitKb-column ranges, one row of the tiled GEMM's
+// grid each,
+// whose int32 partial sums go to part [splits][M][N]; the next row kernel
+// (launch_resid_ln_quant) adds them (integer sums: exact in any order) and
+// applies the residual epilogue.  qgemm_splits: the split count for a shape,
+// 0 where the split does not apply (it needs 8 < M <= 512, N <= 1024, K a
+// multiple of kSplitKb above 1024 with at most kMaxSplits ranges: shorter K
+// takes the one-round-trip kernel whole).
+constexpr int kSplitKb = 512, kMaxSplits = 4;
+int qgemm_splits(int M, int K, int N);
+hipError_t launch_qgemm_split(const int8_t* X, int ldx, const int8_t* W, int M, int K, int N, int32_t* part,
+                              hipStream_t s, bool w4 = false);
+// The tiled GEMM's K split behind it (64x64 tiles, `splits` K ranges).
+hipError_t launch_gemm_split(const int8_t* X, int ldx, const int8_t* W, int M, int K, int N, int splits,
+                             int32_t* part, hipStream_t s, bool w4);
+// A residual update pending from a linear layer's int32 sums:
+// x <- fma(gamma, x, fma((float)(sum of the splits' partials), scale, bias)),
+// the expression of the MNMT_EPI_F32_RESID epilogue.
+struct ResidUpdate {
+  const int32_t* part;  // [splits][rows][d]
+  int splits;
+  const float* scale;
+  const float* bias;
+  float gamma;
+};
+// launch_ln_quant after the pending update of the rows x [rows, d], which are
+// stored back (pre-LN: the updated rows; post-LN: x_out = x, the normalized
+// rows replace them).
+hipError_t launch_resid_ln_quant(float* x, int rows, int d, const ResidUpdate& u, int do_ln, const float* g,
+                                 const float* b, float eps, float inv_s, int8_t* q, bool post, hipStream_t s);
 hipError_t launch_greedy_commit_slots(const FusedGemv& gv, hipStream_t s);
 // Arg-max slots per row of the greedy paths: the spread atomic slots of the
 // 3-8 row path and one partial per block of the 1-2 row logits kernel.
@@ -549,6 +580,7 @@ struct mnmt_session {
   int8_t* dec_q = nullptr;
   int8_t* dec_h = nullptr;
   int8_t* dec_u = nullptr;  // factorized embedding: the output projection's int8 input [R, emb_dim]
+  int32_t* dec_part = nullptr;  // split-K partial sums [kMaxSplits][R][d] (launch_qgemm_split)
   std::vector<int8_t*> kcache, vcache;
   int32_t* cur_tok = nullptr;
   int* step = nullptr;

@@ -140,6 +140,48 @@ __global__ __launch_bounds__(256) void k_ln_quant(const float* __restrict__ x, i
                     x_out ? x_out + (size_t)r * d : nullptr);
 }
 
+// The pending residual update of a split-K layer, then k_ln_quant's row
+// work: x = fma(gamma, x, fma((float)acc, scale, bias)) with acc the sum of
+// the splits' int32 partials (the F32_RESID epilogue's expression), stored
+// back (replace: the normalized row instead), LayerNorm, quantization.  Every
+// load is issued before the first use (split indexes past the count repeat
+// the last split and are not added).
+template <int NJ>
+__global__ __launch_bounds__(256) void k_resid_ln_quant(float* __restrict__ x, int rows, int d, ResidUpdate u,
+                                                        int do_ln, const float* __restrict__ g,
+                                                        const float* __restrict__ b, float eps, float inv_s,
+                                                        int8_t* __restrict__ q, int replace) {
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (r >= rows) return;
+  float* xr = x + (size_t)r * d;
+  float v[NJ], sc[NJ], bi[NJ];
+  int part[kMaxSplits][NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int i = min(lane + 64 * j, d - 1);
+    v[j] = xr[i];
+    sc[j] = u.scale[i];
+    bi[j] = u.bias[i];
+#pragma unroll
+    for (int p = 0; p < kMaxSplits; ++p)
+      part[p][j] = u.part[((size_t)min(p, u.splits - 1) * rows + r) * d + i];
+  }
+  float gj[NJ], bj[NJ];
+  ln_consts<NJ>(d, do_ln, g, b, gj, bj);
+  const int n = (d + 63) / 64;
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    int acc = part[0][j];
+#pragma unroll
+    for (int p = 1; p < kMaxSplits; ++p) acc += p < u.splits ? part[p][j] : 0;
+    v[j] = fmaf(u.gamma, v[j], fmaf((float)acc, sc[j], bi[j]));
+    const int i = lane + 64 * j;
+    if (!replace && j < n && i < d) xr[i] = v[j];
+  }
+  ln_quant_wave_pre<NJ>(v, d, do_ln, gj, bj, eps, inv_s, q + (size_t)r * d, replace ? xr : nullptr);
+}
+
 __device__ __forceinline__ int dot16v(const v4i a, const v4i b, int acc) {
   acc = __builtin_amdgcn_sdot4(a.x, b.x, acc, false);
   acc = __builtin_amdgcn_sdot4(a.y, b.y, acc, false);
@@ -1018,6 +1060,26 @@ hipError_t launch_ln_quant(const float* x, int rows, int d, int do_ln, const flo
     default: MNMT_LNQ(16); break;
   }
 #undef MNMT_LNQ
+  return hipGetLastError();
+}
+
+hipError_t launch_resid_ln_quant(float* x, int rows, int d, const ResidUpdate& u, int do_ln, const float* g,
+                                 const float* b, float eps, float inv_s, int8_t* q, bool post, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (d > kMaxRowLen || u.splits < 1 || u.splits > kMaxSplits || !q) return hipErrorInvalidValue;
+  const dim3 grid((rows + 3) / 4);
+#define MNMT_RLNQ(NJ)                                                                                         \
+  hipLaunchKernelGGL(k_resid_ln_quant<NJ>, grid, dim3(256), 0, s, x, rows, d, u, do_ln, g, b, eps, inv_s, q, \
+                     post ? 1 : 0)
+  switch (row_class(d)) {
+    case 64: MNMT_RLNQ(1); break;
+    case 128: MNMT_RLNQ(2); break;
+    case 256: MNMT_RLNQ(4); break;
+    case 384: MNMT_RLNQ(6); break;
+    case 512: MNMT_RLNQ(8); break;
+    default: MNMT_RLNQ(16); break;
+  }
+#undef MNMT_RLNQ
   return hipGetLastError();
 }
 

@@ -325,6 +325,19 @@ hipError_t gemv_rows(const int8_t* X, int ldx, const int8_t* W, const float* sca
   return gemv_lpr<8, W4>(X, ldx, W, scale, bias, M, K, N, e, s);
 }
 
+int qgemm_splits(int M, int K, int N) {
+  if (M <= 8 || M > kSmallMaxRows || N > 1024 || K <= kSmallMaxK || K % kSplitKb || K / kSplitKb > kMaxSplits)
+    return 0;
+  return K / kSplitKb;
+}
+
+hipError_t launch_qgemm_split(const int8_t* X, int ldx, const int8_t* W, int M, int K, int N, int32_t* part,
+                              hipStream_t s, bool w4) {
+  const int splits = qgemm_splits(M, K, N);
+  if (!splits) return hipErrorInvalidValue;
+  return launch_gemm_split(X, ldx, W, M, K, N, splits, part, s, w4);
+}
+
 hipError_t launch_qlinear(const int8_t* X, int ldx, const int8_t* W, const float* scale, const float* bias, int M,
                           int K, int N, const EpiArgs& e, hipStream_t s, bool w4) {
   if (M <= 0) return hipSuccess;

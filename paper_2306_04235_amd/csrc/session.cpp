@@ -32,7 +32,7 @@ constexpr size_t kEncAccRows = 64;  // rows of the small-batch encoder path
 struct Plan {
   size_t src, len, region, enc_x, enc_x2, enc_a, enc_qkv, enc_h, enc_out, logits;
   std::vector<size_t> cross_kv, kc, vc;
-  size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, dec_u, fslots, enc_acc;
+  size_t dec_x, dec_x2, dec_a, dec_qkv, dec_q, dec_h, dec_u, dec_part, fslots, enc_acc;
   size_t cur_tok, step, slots, out_tok, finished, out_len, out_key, lp;
   size_t score, cand_score, cand_tok, tok_hist, par_hist, hist, fin_score, fin_len, fin_row, fin_count, done;
   size_t chain_err, enc_chain, beam_count, epoch, step_x64;
@@ -102,6 +102,7 @@ Plan make_plan(const mnmt_model* m, const mnmt_session_cfg& c) {
   p.dec_q = b.take(R * d);
   p.dec_h = b.take(R * F);
   p.dec_u = b.take(R * d);  // factorized embedding: emb_dim <= d codes per row
+  p.dec_part = b.take(4 * kMaxSplits * R * d);  // split-K partial sums of the long-K decoder layers
   for (size_t l = 0; l < Ld; ++l) {
     p.kc.push_back(b.take(R * T * d));
     p.vc.push_back(b.take(R * T * d));
@@ -460,11 +461,24 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
     if (rc0) return rc0;
     LAUNCH(launch_ln_quant(S->dec_x, R, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->dec_a, nullptr, s));
   }
-  // the linear layer L over the rows LN(x) quantized with L's input scale
+  // a residual update left pending by a split-K layer (splits > 0), applied
+  // by the next LayerNorm kernel
+  ResidUpdate pend{};
+  // LayerNorm + quantization of the rows with L's input scale into dec_a
   // (post-LN: the normalized rows also replace x)
+  auto ln_rows = [&](const LnDev& ln, float inv_s, bool replace) -> int {
+    if (pend.splits) {
+      LAUNCH(launch_resid_ln_quant(xc, R, d, pend, 1, ln.g, ln.b, eps, inv_s, S->dec_a, replace, s));
+      pend.splits = 0;
+    } else {
+      LAUNCH(launch_ln_quant(xc, R, d, 1, ln.g, ln.b, eps, inv_s, S->dec_a, replace ? xc : nullptr, s));
+    }
+    return MNMT_OK;
+  };
+  // the linear layer L over the rows LN(x) quantized with L's input scale
   auto ln_linear = [&](const LinearDev& L, const LnDev& ln, int kind, void* out) -> int {
-    LAUNCH(launch_ln_quant(xc, R, d, 1, ln.g, ln.b, eps, L.inv_in, S->dec_a, post ? xc : nullptr, s));
-    return qlin(L, S->dec_a, R, kind, out, 1.f, s);
+    const int rc = ln_rows(ln, L.inv_in, post);
+    return rc ? rc : qlin(L, S->dec_a, R, kind, out, 1.f, s);
   };
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
@@ -481,14 +495,19 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
     LAUNCH(launch_attn_dec_cross(S->dec_q, R, W, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, S->dec_a, s));
     if ((rc = qlin(L.co, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.ca_gamma, s))) return rc;
     if ((rc = ln_linear(L.w1, post ? L.ca_ln : L.ff_ln, MNMT_EPI_I8_RELU, S->dec_h))) return rc;
-    if ((rc = qlin(L.w2, S->dec_h, R, MNMT_EPI_F32_RESID, xc, L.ff_gamma, s))) return rc;
+    if (const int sp = qgemm_splits(R, L.w2.K, L.w2.N)) {  // long K: partial sums, update pending
+      const int8_t* w;
+      const bool w4 = batched_weights(L.w2, w);
+      LAUNCH(launch_qgemm_split(S->dec_h, L.w2.K, w, R, L.w2.K, L.w2.N, S->dec_part, s, w4));
+      pend = ResidUpdate{S->dec_part, sp, L.w2.scale, L.w2.bias, L.ff_gamma};
+    } else if ((rc = qlin(L.w2, S->dec_h, R, MNMT_EPI_F32_RESID, xc, L.ff_gamma, s))) {
+      return rc;
+    }
   }
   // the final LayerNorm (post-LN: the last FFN's) into dec_a for the output
   // projection
   const LayerDev& last = m->dec.back();
-  const LnDev& lnf = post ? last.ff_ln : m->dec_ln;
-  LAUNCH(launch_ln_quant(xc, R, d, 1, lnf.g, lnf.b, eps, m->inv_fin, S->dec_a, nullptr, s));
-  return MNMT_OK;
+  return ln_rows(post ? last.ff_ln : m->dec_ln, m->inv_fin, false);
 }
 
 // Greedy step: layers, tied output projection with fused arg-max (batch <= 8)
@@ -1073,6 +1092,7 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   S->dec_q = (int8_t*)at(p.dec_q);
   S->dec_h = (int8_t*)at(p.dec_h);
   S->dec_u = (int8_t*)at(p.dec_u);
+  S->dec_part = (int32_t*)at(p.dec_part);
   for (size_t l = 0; l < p.kc.size(); ++l) {
     S->kcache.push_back((int8_t*)at(p.kc[l]));
     S->vcache.push_back((int8_t*)at(p.vc[l]));

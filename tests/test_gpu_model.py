@@ -445,6 +445,30 @@ def test_4bit_packed_only_batched_paths(torch_dev):
     _beam_check(torch, dev, mob4, src, lens, w.beam, w.steps, w.alpha, sample=idx, parallel=True, flags=flags)
 
 
+SPLIT_PRE = G.ModelConfig("split-preln", 128, 4, 2048, 2, 2, 700, ln_post=0, seed=91, random_gamma=True,
+                          weight_std=0.1)
+SPLIT_POST = G.ModelConfig("split-postln", 64, 2, 1536, 1, 2, 500, ln_post=1, seed=92, random_gamma=True,
+                           weight_std=0.1)
+
+
+@pytest.mark.parametrize("cfg", [SPLIT_PRE, SPLIT_POST], ids=lambda c: c.name)
+def test_split_k_feed_forward(torch_dev, cfg):
+    """Feed-forward widths of 1536 and 2048 in the batched decoder: W2's K is
+    split over blocks whose int32 partial sums the next LayerNorm kernel adds
+    before the residual update (pre-LN with gamma != 1: the updated rows are
+    stored, post-LN: the normalized rows replace them; the final LayerNorm
+    too).  Batched greedy (12 rows) and beam search against the oracle, and
+    the same with packed 4-bit weights."""
+    from paper_2306_04235_amd import mnmt
+
+    torch, dev = torch_dev
+    src, lens = G.make_sources(cfg.vocab, 12, [9, 5, 7, 16, 3, 11, 8, 8, 2, 16, 12, 6], seed=93, s_max=16)
+    _greedy_check(torch, dev, cfg, src, lens, 8)
+    _beam_check(torch, dev, cfg, src[:5], lens[:5], 4, 8, 0.6)
+    c4 = dataclasses.replace(cfg, name=cfg.name + "-w4", w_bits=4)
+    _beam_check(torch, dev, c4, src[:5], lens[:5], 4, 8, 0.6, flags=mnmt.LOAD_PACKED_4BIT_ONLY)
+
+
 SHARED = G.ModelConfig("shared-preln", 64, 4, 128, 4, 3, 500, ln_post=0, seed=82, random_gamma=True,
                        weight_std=0.1, share_every=1)
 SHARED_256 = G.ModelConfig("shared-256", 256, 4, 1024, 6, 2, 32000, ln_post=0, seed=1103, random_gamma=True,
