@@ -68,13 +68,14 @@ hipError_t launch_embed_proj(const int32_t* tok, int rows, int S_for_pos, const 
 hipError_t launch_attn_enc(const int8_t* qkv, const int32_t* len, int B, int S, int d, int h, float c_qk,
                            float c_pv, int8_t* ctx, hipStream_t s);
 
-// Decoder self-attention at position *step: stores this step's k, v of every
+// Decoder self-attention at position t (t_host when >= 0, the step index
+// known when the work is enqueued, else *step): stores this step's k, v of every
 // row into kcache/vcache [R][T][d] and attends over positions 0..step of the
 // row's hypothesis (hist: two [R][T] tables, position -> cache row, the one
 // of parity step & 1 is read; null = the row's own cache).
 hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, const int* step, int8_t* kcache,
                                 int8_t* vcache, const int32_t* hist, float c_qk, float c_pv, int8_t* ctx,
-                                hipStream_t s);
+                                hipStream_t s, int t_host = -1);
 
 // Decoder cross-attention: row r attends over the cross keys/values of
 // sentence r / W (kv [B*S, 2d]) limited to len[b].
@@ -444,6 +445,7 @@ struct BeamState {
   const float* lp;       // [T + 1] length penalties
   int32_t* count;        // [1] blocks of the update kernel finished this step (0 between steps)
   int eos, pad, bos;
+  int t_host = -1;       // >= 0: the step index, known when the work is enqueued (else the kernels read *step)
 };
 // The next step's input rows, written by the beam update for every slot of
 // its sentence while t + 1 < steps: the embedding of the slot's token at

@@ -287,7 +287,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __re
                                                               int T, const int* __restrict__ step,
                                                               int8_t* __restrict__ kcache, int8_t* __restrict__ vcache,
                                                               const int32_t* __restrict__ hist, float c_qk,
-                                                              float c_pv, int8_t* __restrict__ ctx) {
+                                                              float c_pv, int8_t* __restrict__ ctx, int t_host) {
   constexpr int CPP = DHMAX / 16;  // lanes per position
   constexpr int PPI = 64 / CPP;    // positions per load instruction
   constexpr int NL = NMAX / PPI;   // load instructions per operand
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __re
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nc = dh / 16;
   const int c = lane % CPP, pp = lane / CPP, cc = min(c, nc - 1);
-  int t = *step;
+  int t = t_host >= 0 ? t_host : *step;
   t = t < 0 ? 0 : (t >= T ? T - 1 : t);
   const int n = t + 1;
   const int8_t* row = qkv + (size_t)r * 3 * d;
@@ -488,7 +488,7 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
                                                   const int* __restrict__ step) {
   const int r = blockIdx.x;
   const int lane = threadIdx.x;
-  const int t = *step;
+  const int t = st.t_host >= 0 ? st.t_host : *step;
   const int b = r / st.W, j = r % st.W;
   if (st.done[b] || (t == 0 && j > 0)) return;
   const int V = st.V;
@@ -667,7 +667,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* _
   __shared__ int n_list;
   const int r = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int t = *step;
+  const int t = st.t_host >= 0 ? st.t_host : *step;
   const int b = r / st.W, j = r % st.W;
   if (st.done[b] || (t == 0 && j > 0)) return;
   const int V = st.V, n4 = V / 4;
@@ -792,7 +792,7 @@ __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, in
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const bool w0 = wv == 0;  // the wave that ranks the sentence's candidates
   const int W = st.W, K = 2 * W, R = st.B * W, T = st.T, V = st.V;
-  const int t = *step;
+  const int t = st.t_host >= 0 ? st.t_host : *step;
   const bool active = !st.done[b];
   const int pos = t + 1;
   const bool prep = pos < nx.steps && pos < nx.P;
@@ -1131,14 +1131,14 @@ hipError_t launch_attn_enc(const int8_t* qkv, const int32_t* len, int B, int S, 
 
 hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, const int* step, int8_t* kcache,
                                 int8_t* vcache, const int32_t* hist, float c_qk, float c_pv, int8_t* ctx,
-                                hipStream_t s) {
+                                hipStream_t s, int t_host) {
   const int dh = d / h;
   if (T > kMaxAttnLen || dh > kMaxHeadDim || dh % 16 || R < 1) return hipErrorInvalidValue;
   const int nm = attn_len_class(T), dm = attn_dh_class(dh);
   // a block per row, a wave per head (up to 8, fewer for the widest LDS)
 #define MNMT_SELF(NM, DM, WV)                                                                                      \
   hipLaunchKernelGGL((k_attn_dec_self<NM, DM, WV>), dim3(R), dim3(64 * WV), 0, s, qkv, d, h, dh, T, step, kcache, \
-                     vcache, hist, c_qk, c_pv, ctx)
+                     vcache, hist, c_qk, c_pv, ctx, t_host)
 #define MNMT_SELF_W(NM, DM)                  \
   if (h >= 8) MNMT_SELF(NM, DM, 8);         \
   else if (h >= 4) MNMT_SELF(NM, DM, 4);    \

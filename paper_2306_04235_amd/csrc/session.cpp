@@ -449,7 +449,10 @@ int run_encoder(mnmt_session* S, hipStream_t s) {
 // final sublayer input in dec_a, ready for the output projection.
 // rows_ready: dec_x and dec_a already hold the step's input rows (written by
 // the previous step's beam update).
-int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, bool rows_ready = false) {
+// t_host: the step index when known at enqueue (>= 0), else -1 (the kernels
+// read the device step counter).
+int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, bool rows_ready = false,
+                       int t_host = -1) {
   const mnmt_model* m = S->m;
   const int d = m->info.d_model, h = m->info.n_heads, T = S->cfg.max_tgt_len;
   const bool post = m->info.ln_post;
@@ -489,7 +492,7 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
       rc = ln_linear(L.qkv, post ? m->dec[l - 1].ff_ln : L.sa_ln, MNMT_EPI_I8, S->dec_qkv);
     if (rc) return rc;
     LAUNCH(launch_attn_dec_self(S->dec_qkv, R, d, h, T, S->step, S->kcache[l], S->vcache[l],
-                                beam ? S->beam.hist : nullptr, L.sa_cqk, L.sa_cpv, S->dec_a, s));
+                                beam ? S->beam.hist : nullptr, L.sa_cqk, L.sa_cpv, S->dec_a, s, t_host));
     if ((rc = qlin(L.o, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.sa_gamma, s))) return rc;
     if ((rc = ln_linear(L.cq, post ? L.sa_ln : L.ca_ln, MNMT_EPI_I8, S->dec_q))) return rc;
     LAUNCH(launch_attn_dec_cross(S->dec_q, R, W, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, S->dec_a, s));
@@ -953,7 +956,7 @@ int beam_step(mnmt_session* S, int R, int W, int t, int steps, hipStream_t s) {
   const mnmt_model* m = S->m;
   // factorized embeddings embed their rows in the decoder (the beam update
   // prepares rows of the model width only)
-  int rc = run_decoder_layers(S, R, W, true, s, t > 0 && !factored(m));
+  int rc = run_decoder_layers(S, R, W, true, s, t > 0 && !factored(m), t);
   if (rc) return rc;
   const int d = m->info.d_model, V = m->info.vocab;
   const int8_t* X;
@@ -961,7 +964,9 @@ int beam_step(mnmt_session* S, int R, int W, int t, int steps, hipStream_t s) {
   if ((rc = logits_input(S, R, &X, &K, s))) return rc;
   EpiArgs e{MNMT_EPI_LOGITS, S->logits, V, 1.f, nullptr};
   LAUNCH(launch_qlinear(X, K, m->E, m->c_out, nullptr, R, K, V, e, s));
-  LAUNCH(launch_beam_topk(S->logits, S->beam, S->step, s));
+  BeamState st = S->beam;
+  st.t_host = t;  // the graph replays the steps in this order
+  LAUNCH(launch_beam_topk(S->logits, st, S->step, s));
   const LayerDev& L0 = m->dec[0];
   BeamNext nx{};
   nx.x = S->dec_x;
@@ -978,7 +983,7 @@ int beam_step(mnmt_session* S, int R, int W, int t, int steps, hipStream_t s) {
   nx.b = L0.sa_ln.b;
   nx.eps = m->info.ln_eps;
   nx.inv_s = L0.qkv.inv_in;
-  LAUNCH(launch_beam_update(S->beam, S->step, nx, s));
+  LAUNCH(launch_beam_update(st, S->step, nx, s));
   return MNMT_OK;
 }
 
