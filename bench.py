@@ -172,6 +172,122 @@ def counters_run():
     print("counters run done", flush=True)
 
 
+GEMM_TAG = "qgemm_4096x256x32000"
+GEMM_COUNTERS = ("SQ_INSTS_VALU_MFMA_MOPS_I8", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE", "SQ_BUSY_CYCLES")
+
+
+def _gemm_source_hash():
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "qlinear.hip", "blocks.hpp", "canon.hpp", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2306_04235_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _gemm_case(torch, dev):
+    """The largest sweep shape (4096 x 256 x 32000, int8 requantizing
+    epilogue) as a closure over random operands, and M, K, N."""
+    from paper_2306_04235_amd import mnmt
+
+    M, K, N = 4096, 256, 32000
+    Xg = torch.randint(-127, 128, (M, K), dtype=torch.int8, device=dev)
+    Wg = torch.randint(-127, 128, (N, K), dtype=torch.int8, device=dev)
+    sc = torch.full((N,), 1e-4, dtype=torch.float32, device=dev)
+    bi = torch.zeros(N, dtype=torch.float32, device=dev)
+    Yg = torch.empty((M, N), dtype=torch.int8, device=dev)
+    stream = torch.cuda.current_stream()
+    return (lambda: mnmt.mnmt_qlinear(Xg, Wg, sc, bi, mnmt.EPI_I8, out=Yg, stream=stream)), (M, K, N)
+
+
+def beam_counters_run():
+    """Short run for one rocprofv3 --pmc pass over the base beam workload:
+    one eager translation (every kernel a dispatch of its own)."""
+    import torch
+
+    from paper_2306_04235_amd import mnmt
+    from synth import generate as G
+
+    dev = torch.device("cuda:0")
+    w = G.WORKLOADS["base_beam"]
+    m = mnmt.Model(G.build_model(w.model))
+    src, lens = G.workload_inputs(w)
+    sess = mnmt.Session(m, w.batch, w.s_max, w.steps, w.beam)
+    sess.translate(torch.from_numpy(src).to(dev), torch.from_numpy(lens).to(dev), beam=w.beam, max_steps=w.steps,
+                   alpha=w.alpha, use_graph=False)
+    torch.cuda.synchronize()
+    sess.status()
+    print("beam counters run done", flush=True)
+
+
+def gemm_counters_run():
+    """Short run for one rocprofv3 --pmc pass over the GEMM: 5 launches, then
+    20 more (the counters are taken per dispatch)."""
+    import torch
+
+    g, _ = _gemm_case(torch, torch.device("cuda:0"))
+    for _ in range(25):
+        g()
+    torch.cuda.synchronize()
+    print("gemm counters run done", flush=True)
+
+
+def ingest_gemm_counters(csv_path, command):
+    """MFMA work and utilization of the GEMM's kernel from one counter pass
+    (GEMM_COUNTERS) into profiles/counters.json: i8 ops = MOPS_I8 * 512 per
+    dispatch (against 2MKN); the MFMA busy share = the MFMA busy cycles
+    (summed over the 1024 SIMDs) over 1024 x the GPU-active cycles of one XCD
+    (the file sums GRBM_GUI_ACTIVE over the 8 XCDs), rocprofv3's MfmaUtil;
+    medians over the last 20 dispatches."""
+    import csv
+
+    vals, dur = {}, {}
+    with open(csv_path) as f:
+        for row in csv.DictReader(f):
+            if "k_gemm" not in row["Kernel_Name"]:
+                continue
+            key = (row["Kernel_Name"], row["Counter_Name"])
+            vals.setdefault(key, {}).setdefault(int(row["Dispatch_Id"]), 0.0)
+            vals[key][int(row["Dispatch_Id"])] += float(row["Counter_Value"])
+            dur[int(row["Dispatch_Id"])] = (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) * 1e-9
+    kernels = {k for k, _ in vals}
+    if len(kernels) != 1:
+        raise SystemExit(f"expected one GEMM kernel, found {sorted(kernels)}")
+    kname = kernels.pop()
+
+    def med(c):
+        v = [x for _, x in sorted(vals[(kname, c)].items())][-20:]
+        return sorted(v)[len(v) // 2]
+
+    M, K, N = 4096, 256, 32000
+    mops, busy, gui = med("SQ_INSTS_VALU_MFMA_MOPS_I8"), med("SQ_VALU_MFMA_BUSY_CYCLES"), med("GRBM_GUI_ACTIVE")
+    gui_xcd = gui / 8
+    d = sorted(dur[i] for i in sorted(dur)[-20:])[10]
+    rec = {"source_hash": _gemm_source_hash(), "kernel": kname, "i8_ops_per_launch": mops * 512,
+           "alg_ops": 2 * M * K * N, "mfma_busy_cycles_per_simd": busy / 1024, "gpu_active_cycles_per_xcd": gui_xcd,
+           "duration_us": round(d * 1e6, 2),
+           "mfma_busy_frac": round(busy / 1024 / gui_xcd, 4), "command": command}
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    data = {}
+    if os.path.exists(path):
+        with open(path) as f:
+            data = json.load(f)
+    data[GEMM_TAG] = rec
+    with open(path, "w") as f:
+        json.dump(data, f, indent=1)
+    print(json.dumps(rec))
+
+
+def _gemm_counters():
+    path = os.path.join(ROOT, "profiles", "counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f).get(GEMM_TAG)
+    if not rec or rec.get("source_hash") != _gemm_source_hash():
+        return None
+    return {k: rec[k] for k in ("mfma_busy_frac", "i8_ops_per_launch", "duration_us")}
+
+
 def ingest_counters(fetch_csv, write_csv, command):
     """profiles/counters.json from the FETCH_SIZE and WRITE_SIZE passes."""
     import csv
@@ -395,16 +511,17 @@ def beam_throughput(torch, mnmt, G, dev, names=tuple(BEAM_RUNS), reps=3, check=T
     """The two batched beam-search workloads (mobile: 64 sentences, base: 128;
     beam 4, length penalty 0.6), and the mobile one with packed 4-bit weights,
     each translation one captured graph, inputs resident on the device: one
-    untimed translation, then ``reps`` timed.
+    untimed translation, then ``reps`` timed back to back, then 10 more each
+    alone between two events (median, p10, p90).
     The last translation's shortest sentence is compared with the oracle, and
     a composite roofline (the sum over phases of max(ops / i8 peak, bytes /
     HBM peak), paper_2306_04235_amd.workload.beam_roofline_s) over the steps
     the batch ran gives the fraction."""
+    import dataclasses
+
     import numpy as np
 
     from paper_2306_04235_amd import workload as WL
-
-    import dataclasses
 
     res = {}
     for name in names:
@@ -428,6 +545,14 @@ def beam_throughput(torch, mnmt, G, dev, names=tuple(BEAM_RUNS), reps=3, check=T
             run()
         torch.cuda.synchronize()
         el = (time.perf_counter() - t0) / reps
+        # per-batch distribution: each translation alone between two events
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(10)]
+        for e0, e1 in ev:
+            e0.record()
+            run()
+            e1.record()
+            e1.synchronize()
+        one = np.sort([e0.elapsed_time(e1) for e0, e1 in ev])
         sess.status()
         toks = int(outs[1].sum().item())
         out_np, len_np = outs[0].cpu().numpy(), outs[1].cpu().numpy()
@@ -445,6 +570,8 @@ def beam_throughput(torch, mnmt, G, dev, names=tuple(BEAM_RUNS), reps=3, check=T
                      "ms_per_batch": round(el * 1e3, 3), "sentences_per_s": round(w.batch / el, 1),
                      "output_tokens_per_s": round(toks / el, 1), "batch": w.batch, "beam": w.beam,
                      "max_steps": w.steps, "steps_run": steps_run,
+                     "ms_per_batch_alone": {"median": round(float(np.median(one)), 3), "p10": round(float(one[1]), 3),
+                                            "p90": round(float(one[8]), 3), "runs": len(one)},
                      "composite_roofline": {"ms": round(roof["seconds"] * 1e3, 4),
                                             "frac": round(roof["seconds"] / el, 4),
                                             "parts_ms": {k: round(v["seconds"] * 1e3, 4)
@@ -471,7 +598,17 @@ def main():
                     help="record the roofline kernel's kernel-trace average from a rocprofv3 --stats file")
     ap.add_argument("--ingest-command", default="")
     ap.add_argument("--sweep-trace", metavar="KERNEL_TRACE_CSV", help="summarize a kernel trace of --sweep")
+    ap.add_argument("--gemm-counters", action="store_true",
+                    help="only the 4096x256x32000 GEMM, 25 launches (for one --pmc pass of " + " ".join(GEMM_COUNTERS)
+                    + ")")
+    ap.add_argument("--beam-counters", action="store_true",
+                    help="only one eager translation of the base beam workload (for a --pmc pass)")
+    ap.add_argument("--ingest-gemm-counters", metavar="COUNTER_CSV",
+                    help="record the GEMM's MFMA counters from a --gemm-counters pass")
     args = ap.parse_args()
+    if args.ingest_gemm_counters:
+        ingest_gemm_counters(args.ingest_gemm_counters, args.ingest_command)
+        return
     if args.sweep_trace:
         sweep_trace_summary(args.sweep_trace, args.ingest_command)
         return
@@ -487,6 +624,12 @@ def main():
         sys.exit(2)
     if args.counters:
         counters_run()
+        return
+    if args.gemm_counters:
+        gemm_counters_run()
+        return
+    if args.beam_counters:
+        beam_counters_run()
         return
 
     import numpy as np
@@ -581,18 +724,15 @@ def main():
     roofline["frac_of_measured_llc"] = round(achieved / mem["llc_64MiB"], 4)
 
     # Largest quantized-linear sweep shape on the matrix cores.
-    M, K, N = 4096, 256, 32000
-    Xg = torch.randint(-127, 128, (M, K), dtype=torch.int8, device=dev)
-    Wg = torch.randint(-127, 128, (N, K), dtype=torch.int8, device=dev)
-    sc = torch.full((N,), 1e-4, dtype=torch.float32, device=dev)
-    bi = torch.zeros(N, dtype=torch.float32, device=dev)
-    Yg = torch.empty((M, N), dtype=torch.int8, device=dev)
-    g = lambda: mnmt.mnmt_qlinear(Xg, Wg, sc, bi, mnmt.EPI_I8, out=Yg, stream=stream)  # noqa: E731
+    g, (M, K, N) = _gemm_case(torch, dev)
     _warm(torch, g)
     gemm_ms = _events_ms(torch, g, 20, stream)
     tops = 2.0 * M * K * N / (gemm_ms * 1e-3) / 1e12
     qgemm = {"shape": [M, K, N], "epilogue": "i8 requant", "tops": round(tops, 1), "peak": I8_PEAK_TOPS,
              "frac": round(tops / I8_PEAK_TOPS, 4), "avg_us": round(gemm_ms * 1e3, 2)}
+    gc = _gemm_counters()  # committed MFMA counters of the same kernel source, if any
+    if gc:
+        qgemm["counters"] = gc
 
     # The paper's own MobileNMT-10MB / 20MB shapes on the same batch-1 path
     # (context beside the paper's phone latencies, not the headline workload),
