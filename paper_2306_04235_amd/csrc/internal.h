@@ -82,6 +82,15 @@ hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, c
 hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, const int8_t* kv, int S,
                                  const int32_t* len, float c_qk, float c_pv, int8_t* ctx, hipStream_t s);
 
+// The same with the query projection fused (the cross-attention's Q linear
+// layer: int8 rows [R, d] of the LayerNorm'd input, wq [d, d] int8 or, w4,
+// packed 4-bit, the I8 requantization with q_scale / q_bias), for W <= 16
+// and d 256 (attn_cross_q_fits).
+bool attn_cross_q_fits(int W, int d);
+hipError_t launch_attn_dec_cross_q(const int8_t* rows, const int8_t* wq, const float* q_scale, const float* q_bias,
+                                   bool w4, int R, int W, int d, int h, const int8_t* kv, int S, const int32_t* len,
+                                   float c_qk, float c_pv, int8_t* ctx, hipStream_t s);
+
 // Greedy bookkeeping after the fused logits/arg-max of a step.
 // out_key [T][R] (or null) receives each step's winning arg-max key.
 hipError_t launch_greedy_commit(unsigned long long* slots, int R, int T, int32_t* cur_tok, int32_t* out_tok,

@@ -200,6 +200,13 @@ __device__ __forceinline__ int dot16v(const v4i a, const v4i b, int acc) {
 struct SharedAttn {
   const int8_t* q;       // query row r of the head at q + r * ldq + head * dh
   int ldq;
+  // the fused query projection (kernel QF > 0): query row r of the head =
+  // requant(a[r] . wq[head * dh + j]) with scale / bias, a [rows, d] int8,
+  // wq [d, d] (QF 2: its packed 4-bit rows)
+  const int8_t* a;
+  const int8_t* wq;
+  const float* q_scale;
+  const float* q_bias;
   int rows;              // query rows per group (row r = group * rows + i)
   const int8_t* kv;      // group g's key t of the head at kv + g * kv_group + k_off + t * ldkv + head * dh
   size_t kv_group;
@@ -210,13 +217,20 @@ struct SharedAttn {
   int8_t* ctx;           // context row r at ctx + r * d + head * dh
 };
 
-template <int NMAX, int DHMAX, int WAVES>
+// QF 0: the query rows are read from a.q; QF 1 (int8 weights) or 2 (packed
+// 4-bit weights): the block computes its group's query rows of the head
+// itself (the cross-attention's Q projection, d = 64 KQ, at most 16 rows),
+// on v_mfma_i32_16x16x64_i8 with the group's rows as A, wave w taking the
+// 16-column fragments w, w + WAVES, ..., and the same requantization as the
+// linear layer's I8 epilogue, into LDS.
+template <int NMAX, int DHMAX, int WAVES, int QF = 0, int KQ = 1>
 __global__ __launch_bounds__(64 * WAVES) void k_attn_shared(SharedAttn a) {
   constexpr int DHC = DHMAX / 16, KS = DHMAX + 16, NI = NMAX / 64;
   constexpr int CH = NMAX * DHC, PER = (CH + 64 * WAVES - 1) / (64 * WAVES);
   __shared__ __attribute__((aligned(16))) int8_t kl[NMAX * KS];
   __shared__ __attribute__((aligned(16))) int8_t vl[NMAX * DHMAX];
   __shared__ __attribute__((aligned(16))) float pl[WAVES][NMAX];
+  __shared__ __attribute__((aligned(16))) int8_t ql[QF ? 16 * DHMAX : 16];
   const int hd = blockIdx.x, g = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int dh = a.dh, nc = dh / 16;
@@ -235,8 +249,35 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_shared(SharedAttn a) {
   const int rows = a.rows;
   auto qrow = [&](int i) { return a.q + ((size_t)g * rows + min(i, rows - 1)) * a.ldq + hd * dh; };
   v4i qn[DHC];
+  if constexpr (QF == 0) {
 #pragma unroll
-  for (int c = 0; c < DHC; ++c) qn[c] = *(const v4i*)(qrow(wave) + 16 * min(c, nc - 1));
+    for (int c = 0; c < DHC; ++c) qn[c] = *(const v4i*)(qrow(wave) + 16 * min(c, nc - 1));
+  } else {
+    // the head's query rows: every operand load first, one fragment per wave
+    // at a time (nc <= 8 fragments)
+    constexpr bool W4 = QF == 2;
+    const int d = 64 * KQ, l16 = lane & 15, koff = 16 * (lane >> 4);
+    const int8_t* ar = a.a + ((size_t)g * rows + min(l16, rows - 1)) * d;
+    v4i af[KQ];
+#pragma unroll
+    for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(ar + 64 * kk + koff);
+    for (int f = wave; f < nc; f += WAVES) {
+      const int col = hd * dh + 16 * f + l16;
+      WFrag<W4> bf[KQ];
+#pragma unroll
+      for (int kk = 0; kk < KQ; ++kk) bf[kk] = load_wfrag<W4>(a.wq, col, d, 64 * kk + koff);
+      const float sc = a.q_scale[col], bi = a.q_bias[col];
+      v4i acc = {0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < KQ; ++kk) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[kk], bf[kk].get(), acc, 0, 0, 0);
+      // element i of lane l: row 4 (l / 16) + i, column l % 16
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * (lane >> 4) + i;
+        if (r < rows) ql[r * DHMAX + 16 * f + l16] = code_of(fmaf((float)acc[i], sc, bi));
+      }
+    }
+  }
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
     const int c = tid + u * 64 * WAVES;
@@ -251,8 +292,12 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_shared(SharedAttn a) {
     v4i qv[DHC];
 #pragma unroll
     for (int c = 0; c < DHC; ++c) {
-      qv[c] = qn[c];
-      qn[c] = *(const v4i*)(qrow(i + WAVES) + 16 * min(c, nc - 1));
+      if constexpr (QF == 0) {
+        qv[c] = qn[c];
+        qn[c] = *(const v4i*)(qrow(i + WAVES) + 16 * min(c, nc - 1));
+      } else {
+        qv[c] = *(const v4i*)(ql + i * DHMAX + 16 * min(c, nc - 1));
+      }
     }
     float sv[NI];
 #pragma unroll
@@ -1088,11 +1133,12 @@ hipError_t launch_resid_ln_quant(float* x, int rows, int d, const ResidUpdate& u
 int attn_len_class(int n) { return n <= 64 ? 64 : n <= 128 ? 128 : 256; }
 int attn_dh_class(int dh) { return dh <= 64 ? 64 : 128; }
 
-template <int WAVES>
+template <int WAVES, int QF = 0, int KQ = 1>
 hipError_t launch_shared(const SharedAttn& a, int groups, int h, hipStream_t s) {
   const dim3 grid(h, groups);
   const int nm = attn_len_class(a.S), dm = attn_dh_class(a.dh);
-#define MNMT_SH(NM, DM) hipLaunchKernelGGL((k_attn_shared<NM, DM, WAVES>), grid, dim3(64 * WAVES), 0, s, a)
+#define MNMT_SH(NM, DM) \
+  hipLaunchKernelGGL((k_attn_shared<NM, DM, WAVES, QF, KQ>), grid, dim3(64 * WAVES), 0, s, a)
   if (dm == 64) {
     if (nm == 64) MNMT_SH(64, 64);
     else if (nm == 128) MNMT_SH(128, 64);
@@ -1159,6 +1205,38 @@ hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, c
 #undef MNMT_SELF_W
 #undef MNMT_SELF
   return hipGetLastError();
+}
+
+// d 256 only: at d 512 (the base model) each of the head x sentence blocks
+// loads 32 KB of the Q weights and the batch time did not move (34.4 against
+// 34.6 ms), so the separate Q projection stays.
+bool attn_cross_q_fits(int W, int d) { return W >= 1 && W <= 16 && d == 256; }
+
+hipError_t launch_attn_dec_cross_q(const int8_t* rows, const int8_t* wq, const float* q_scale, const float* q_bias,
+                                   bool w4, int R, int W, int d, int h, const int8_t* kv, int S, const int32_t* len,
+                                   float c_qk, float c_pv, int8_t* ctx, hipStream_t s) {
+  const int dh = d / h;
+  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16 || R % W || !attn_cross_q_fits(W, d) || !rows || !wq)
+    return hipErrorInvalidValue;
+  SharedAttn a{};
+  a.a = rows;
+  a.wq = wq;
+  a.q_scale = q_scale;
+  a.q_bias = q_bias;
+  a.rows = W;
+  a.kv = kv;
+  a.kv_group = (size_t)S * 2 * d;
+  a.ldkv = 2 * d;
+  a.k_off = 0;
+  a.v_off = d;
+  a.len = len;
+  a.S = S;
+  a.d = d;
+  a.dh = dh;
+  a.c_qk = c_qk;
+  a.c_pv = c_pv;
+  a.ctx = ctx;
+  return w4 ? launch_shared<4, 2, 4>(a, R / W, h, s) : launch_shared<4, 1, 4>(a, R / W, h, s);
 }
 
 hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, const int8_t* kv, int S,

@@ -494,9 +494,22 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
     LAUNCH(launch_attn_dec_self(S->dec_qkv, R, d, h, T, S->step, S->kcache[l], S->vcache[l],
                                 beam ? S->beam.hist : nullptr, L.sa_cqk, L.sa_cpv, S->dec_a, s, t_host));
     if ((rc = qlin(L.o, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.sa_gamma, s))) return rc;
-    if ((rc = ln_linear(L.cq, post ? L.sa_ln : L.ca_ln, MNMT_EPI_I8, S->dec_q))) return rc;
-    LAUNCH(launch_attn_dec_cross(S->dec_q, R, W, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, S->dec_a, s));
-    if ((rc = qlin(L.co, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.ca_gamma, s))) return rc;
+    int8_t* cctx = S->dec_a;  // the cross-attention context rows
+    if (attn_cross_q_fits(W, d)) {
+      // the Q projection inside the attention kernel, from the LayerNorm'd
+      // rows in dec_a; the context goes to dec_q (other blocks of a sentence
+      // still read its rows of dec_a)
+      if ((rc = ln_rows(post ? L.sa_ln : L.ca_ln, L.cq.inv_in, post))) return rc;
+      const int8_t* wq;
+      const bool w4 = batched_weights(L.cq, wq);
+      cctx = S->dec_q;
+      LAUNCH(launch_attn_dec_cross_q(S->dec_a, wq, L.cq.scale, L.cq.bias, w4, R, W, d, h, S->cross_kv[l], S->S,
+                                     S->len, L.ca_cqk, L.ca_cpv, cctx, s));
+    } else {
+      if ((rc = ln_linear(L.cq, post ? L.sa_ln : L.ca_ln, MNMT_EPI_I8, S->dec_q))) return rc;
+      LAUNCH(launch_attn_dec_cross(S->dec_q, R, W, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, cctx, s));
+    }
+    if ((rc = qlin(L.co, cctx, R, MNMT_EPI_F32_RESID, xc, L.ca_gamma, s))) return rc;
     if ((rc = ln_linear(L.w1, post ? L.ca_ln : L.ff_ln, MNMT_EPI_I8_RELU, S->dec_h))) return rc;
     if (const int sp = qgemm_splits(R, L.w2.K, L.w2.N)) {  // long K: partial sums, update pending
       const int8_t* w;
