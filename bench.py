@@ -659,8 +659,8 @@ def main():
     outs = (torch.empty((w.batch, w.steps), dtype=torch.int32, device=dev),
             torch.empty(w.batch, dtype=torch.int32, device=dev), torch.empty(w.batch, dtype=torch.float32, device=dev))
 
-    def step():
-        sess.translate(tsrc, tlen, beam=1, max_steps=w.steps, use_graph=True, out=outs)
+    def step(o=None):
+        sess.translate(tsrc, tlen, beam=1, max_steps=w.steps, use_graph=True, out=o or outs)
 
     # the oracle's translation of the same sentence, which the timed ones must equal
     if args.no_cpu_baseline:
@@ -669,14 +669,20 @@ def main():
         cpu_rec, ref = cpu_baseline(w)
     for _ in range(args.warmup):
         step()
+    # every timed translation writes its own outputs, all compared afterwards
+    touts = [(torch.empty((w.batch, w.steps), dtype=torch.int32, device=dev),
+              torch.empty(w.batch, dtype=torch.int32, device=dev),
+              torch.empty(w.batch, dtype=torch.float32, device=dev)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
+    for k in range(args.steps):
+        step(touts[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     sess.status()  # raises if a chained kernel's wait gave up during the timed translations
-    check_tokens("timed translations", outs[0].cpu().numpy(), outs[1].cpu().numpy(), ref)
+    for k, o in enumerate(touts):
+        check_tokens(f"timed translation {k}", o[0].cpu().numpy(), o[1].cpu().numpy(), ref)
+    outs = touts[-1]
     tokens = int(outs[1].sum().item()) * args.steps
     ms_per_sentence = elapsed * 1e3 / (args.steps * w.batch)
     dims = WL.Dims(info.d_model, info.n_heads, info.d_ffn, info.n_enc, info.n_dec, info.vocab)
@@ -696,8 +702,8 @@ def main():
         e1.record(cur)
         e1.synchronize()
         lat.append(e0.elapsed_time(e1))
+        check_tokens("latency translation", outs[0].cpu().numpy(), outs[1].cpu().numpy(), ref)
     sess.status()
-    check_tokens("latency translations", outs[0].cpu().numpy(), outs[1].cpu().numpy(), ref)
     lat_ms = {"median": round(float(np.median(lat)), 4), "p10": round(float(np.percentile(lat, 10)), 4),
               "p90": round(float(np.percentile(lat, 90)), 4), "runs": len(lat)}
 

@@ -44,16 +44,20 @@ __device__ __forceinline__ void chain_store(T* p, T v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// The block's flag word (in every copy), stored once every wave's writes
-// (chain_store, atomics) have completed.
-__device__ __forceinline__ void chain_signal(const StepChain& c) {
+// The flag word of block `bid` of a kernel role of `nblk` blocks (in every
+// copy), stored once every wave's writes (chain_store, atomics) have
+// completed.
+__device__ __forceinline__ void chain_signal_as(const StepChain& c, int bid, int nblk) {
   if (!c.done) return;
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0);  // this wave's stores and atomics complete
   __syncthreads();                // ... and every other wave's
-  if ((int)threadIdx.x < chain_copies(gridDim.x))
-    __hip_atomic_store(c.done + threadIdx.x * kChainCopyStride + blockIdx.x, c.val, __ATOMIC_RELAXED,
+  if ((int)threadIdx.x < chain_copies(nblk))
+    __hip_atomic_store(c.done + threadIdx.x * kChainCopyStride + bid, c.val, __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void chain_signal(const StepChain& c) {
+  chain_signal_as(c, blockIdx.x, gridDim.x);
 }
 
 }  // namespace mnmt

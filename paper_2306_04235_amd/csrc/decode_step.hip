@@ -118,7 +118,7 @@ __device__ __forceinline__ void poll_row_data(const StepIn& in, int r, int d, Ro
     }
     if (ok) break;
     if (++spins >= kChainSpinLimit) {
-      if (in.chain.err) __hip_atomic_fetch_or(in.chain.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (in.chain.err) __hip_atomic_fetch_or(in.chain.err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       break;
     }
     __builtin_amdgcn_s_sleep(2);
@@ -149,7 +149,7 @@ __device__ __forceinline__ void poll_partials(const unsigned long long* sl, int 
     }
     if (__all(ok)) break;
     if (++spins >= kChainSpinLimit) {
-      if (err) __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (err) __hip_atomic_fetch_or(err, 4, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       break;
     }
     __builtin_amdgcn_s_sleep(2);
@@ -596,18 +596,26 @@ __global__ __launch_bounds__(kStepThreads) void k_step_ffn(StepIn in, StepFfn f)
 // two thirds).  FOLD: the first layer of a folded step (the self-attention
 // blocks embed the previous step's token, the first cross-attention block
 // records it).
+// Block b of a decoder layer's launch (or of its share of the step's
+// launch): its role, then its flag (when the next role waits on flags).
 template <int DMAX, int NIS, int NIC, bool FOLD, bool W4>
-__global__ __launch_bounds__(kStepThreads) void k_step_layer(StepIn ia, StepAttn sa, StepIn ib, StepAttn ca,
-                                                             StepIn ic, StepFfn f, StepCommit cm) {
+__device__ __forceinline__ void step_layer_body(const StepIn& ia, const StepAttn& sa, const StepIn& ib,
+                                                const StepAttn& ca, const StepIn& ic, const StepFfn& f,
+                                                const StepCommit& cm, int b, int nblk) {
   const int heads = sa.d / sa.dh;
-  const int b = blockIdx.x;
   if (b < heads)
     step_attn_body<DMAX, true, NIS, FOLD ? 1 : 0, W4>(ia, sa, cm, b);
   else if (b < 2 * heads)
     step_attn_body<DMAX, false, NIC, FOLD ? 2 : 0, W4>(ib, ca, cm, b - heads);
   else
     step_ffn_body<DMAX, W4>(ic, f, b - 2 * heads);
-  chain_signal(ic.chain);  // every block (when the next kernel waits on flags)
+  chain_signal_as(ic.chain, b, nblk);  // every block (when the next role waits on flags)
+}
+
+template <int DMAX, int NIS, int NIC, bool FOLD, bool W4>
+__global__ __launch_bounds__(kStepThreads) void k_step_layer(StepIn ia, StepAttn sa, StepIn ib, StepAttn ca,
+                                                             StepIn ic, StepFfn f, StepCommit cm) {
+  step_layer_body<DMAX, NIS, NIC, FOLD, W4>(ia, sa, ib, ca, ic, f, cm, blockIdx.x, gridDim.x);
 }
 
 // Output projection over the shared embedding with the fused arg-max: each
@@ -621,8 +629,10 @@ __global__ __launch_bounds__(kStepThreads) void k_step_layer(StepIn ia, StepAttn
 constexpr int kLogitsTiles = 2;
 // in a chain: 4 tiles per wave once that still leaves about 100 blocks
 __host__ inline int chain_logits_tiles(int V) { return V >= 4 * 4 * 16 * 96 ? 4 : kLogitsTiles; }
+// bid / nblk: the block's index among the role's blocks and their number
+// (the whole grid as a kernel of its own).
 template <int DMAX, bool RAW, int TPW, bool FRAG>
-__global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLogits g) {
+__device__ __forceinline__ void step_logits_body(const StepIn& in, const StepLogits& g, int bid, int nblk) {
   constexpr int NJ = DMAX / 64;
   constexpr int KS = DMAX / 64;
   __shared__ __attribute__((aligned(16))) int8_t a_lds[kStepRows * DMAX];
@@ -630,7 +640,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   const int R = g.R, d = DMAX, N = g.V, ks = d / 64;  // DMAX is the exact width
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int l16 = lane & 15, kq = lane >> 4;
-  const int row0 = (blockIdx.x * 4 + wave) * TPW * 16;
+  const int row0 = (bid * 4 + wave) * TPW * 16;
   v4i xr = {0, 0, 0, 0};
   if (RAW) xr = *(const v4i*)(g.x_i8 + (size_t)min(wave, R - 1) * d + 16 * min(lane, d / 16 - 1));
   v4i wf[TPW][KS];
@@ -656,8 +666,8 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   }
   if (!RAW) {
     loads_done();
-    if (wave < R) finish_row(in, wave, d, rr, a_lds, 0u, blockIdx.x);
-    clear_acc(in, blockIdx.x);
+    if (wave < R) finish_row(in, wave, d, rr, a_lds, 0u, bid);
+    clear_acc(in, bid);
   } else if (wave < R && lane < d / 16) {
     *(v4i*)(a_lds + wave * d + 16 * lane) = xr;
   }
@@ -693,7 +703,7 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
   }
   // a tagged partial is the hand-off itself: block 0's accumulator clear
   // (every wave's share) must have landed before it is stored
-  if (!RAW && g.tagged && blockIdx.x == 0 && in.zero_acc) __builtin_amdgcn_s_waitcnt(0);
+  if (!RAW && g.tagged && bid == 0 && in.zero_acc) __builtin_amdgcn_s_waitcnt(0);
   lds_barrier();
   if (threadIdx.x < R) {
     const int m = threadIdx.x;
@@ -701,24 +711,51 @@ __global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLog
 #pragma unroll
     for (int w = 1; w < 4; ++w) b = wmax[w][m] > b ? wmax[w][m] : b;
     unsigned long long* slot = g.slots + (size_t)m * g.nslots;
-    if (g.nslots >= (int)gridDim.x) {
+    if (g.nslots >= nblk) {
       // one partial per block: a plain store, no atomic (atomics on one
       // address serialize), reduced by the consumer
       if (RAW) {
-        slot[blockIdx.x] = b;  // read after the launch, not by a chained kernel
+        slot[bid] = b;  // read after the launch, not by a chained kernel
       } else if (g.tagged) {
-        chain_store(slot + blockIdx.x, tagged_key(b, tag));
+        chain_store(slot + bid, tagged_key(b, tag));
       } else {
-        chain_store(slot + blockIdx.x, b);
+        chain_store(slot + bid, b);
       }
     } else {
       // few slots: most blocks find a larger key already there, and the
       // test spares them the serialized atomic
-      slot += blockIdx.x % g.nslots;
+      slot += bid % g.nslots;
       if (b > __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicMax(slot, b);
     }
   }
-  if (!RAW) chain_signal(in.chain);
+  if (!RAW) chain_signal_as(in.chain, bid, nblk);
+}
+
+template <int DMAX, bool RAW, int TPW, bool FRAG>
+__global__ __launch_bounds__(kStepThreads) void k_step_logits(StepIn in, StepLogits g) {
+  step_logits_body<DMAX, RAW, TPW, FRAG>(in, g, blockIdx.x, gridDim.x);
+}
+
+// The whole decode step in one launch (two decoder layers, then the output
+// projection with the fused arg-max): blocks [0, L) and [L, 2 L) run the two
+// layers' roles (L = step_layer_blocks), the rest the logits kernel's blocks
+// (4 tiles of 16 vocabulary rows per wave).  The hand-offs are the ones the
+// separate launches use: counted words into each layer and between the
+// layers, the last layer's flags for the logits blocks, tagged partials (or
+// the logits blocks' flags) for the next step.  Every consumer role has
+// higher block indices than its producers, and blocks are dispatched in
+// index order, so producers never wait behind their consumers.
+template <int DMAX, bool FOLD, bool W4>
+__global__ __launch_bounds__(kStepThreads) void k_step_all(StepAll p) {
+  const int L = p.layer_blocks;
+  const int b = blockIdx.x;
+  if (b < L)
+    step_layer_body<DMAX, 1, 1, FOLD, W4>(p.ia[0], p.sa[0], p.ib[0], p.ca[0], p.ic[0], p.f[0], p.cm, b, L);
+  else if (b < 2 * L)
+    step_layer_body<DMAX, 1, 1, false, W4>(p.ia[1], p.sa[1], p.ib[1], p.ca[1], p.ic[1], p.f[1], StepCommit{}, b - L,
+                                           L);
+  else
+    step_logits_body<DMAX, false, 4, true>(p.lin, p.g, b - 2 * L, (int)gridDim.x - 2 * L);
 }
 
 }  // namespace
@@ -840,6 +877,39 @@ hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s) {
   else hipLaunchKernelGGL((k_step_ffn<DM, false>), dim3(blocks), dim3(kStepThreads), 0, s, in, f);
   MNMT_BY_D(f.d, MNMT_FFN)
 #undef MNMT_FFN
+  return hipGetLastError();
+}
+
+bool step_all_fits(int n_dec, int d, int heads, int F, int T, int S, int V) {
+  return n_dec == 2 && d == 256 && d % heads == 0 && d / heads <= kStepHeadDim && F % kFfnChunk == 0 &&
+         T <= 64 && S <= 64 && V <= kTagMaxV && chain_logits_tiles(V) == 4 &&
+         step_layer_blocks(heads, F) <= kChainMaxBlocks && step_logits_blocks_chained(V, d) <= kChainMaxBlocks;
+}
+
+hipError_t launch_step_all(const StepAll& p, bool fold, hipStream_t s) {
+  const int heads = p.sa[0].d / p.sa[0].dh;
+  const bool w4 = p.sa[0].w4;
+  for (int l = 0; l < 2; ++l)
+    if (p.sa[l].w4 != w4 || p.ca[l].w4 != w4 || p.f[l].w4 != w4 || !p.sa[l].W || !p.ca[l].W || !p.f[l].W1)
+      return hipErrorInvalidValue;
+  if (p.layer_blocks != step_layer_blocks(heads, p.f[0].F) || p.f[1].F != p.f[0].F || !p.g.frag || !p.g.tagged ||
+      !step_all_fits(2, p.g.d, heads, p.f[0].F, p.sa[0].t + 1, p.ca[0].S, p.g.V))
+    return hipErrorInvalidValue;
+  if (fold && (p.cm.nslots < 1 || p.cm.nslots > 256 || p.cm.t < 1)) return hipErrorInvalidValue;
+  const int blocks = 2 * p.layer_blocks + step_logits_blocks_chained(p.g.V, p.g.d);
+  if (chain_logits_tiles(p.g.V) != 4) return hipErrorInvalidValue;
+#define MNMT_ALL(DM, FO, W) hipLaunchKernelGGL((k_step_all<DM, FO, W>), dim3(blocks), dim3(kStepThreads), 0, s, p)
+#define MNMT_ALL_D(DM)                         \
+  if (fold) {                                  \
+    if (w4) MNMT_ALL(DM, true, true);          \
+    else MNMT_ALL(DM, true, false);            \
+  } else {                                     \
+    if (w4) MNMT_ALL(DM, false, true);         \
+    else MNMT_ALL(DM, false, false);           \
+  }
+  MNMT_ALL_D(256)
+#undef MNMT_ALL_D
+#undef MNMT_ALL
   return hipGetLastError();
 }
 

@@ -304,8 +304,13 @@ struct StepLogits {
 // (translation, step) in bits 31..18 and 0x3FFFF - index in bits 17..0, so
 // that among keys of one tag the maximum is still the arg max with the
 // smallest index; a partial whose tag is the step's own is that step's.
+// Tags run 1..16383 and never 0, the tag of a cleared slot: with tag 0 in
+// use (the old & 0x3FFF form), every 64th translation's second step took the
+// cleared slots for the first step's partials.
 constexpr int kTagMaxV = 1 << 18;
-__host__ __device__ inline unsigned step_tag(unsigned epoch, int t) { return (epoch * 256u + (unsigned)t) & 0x3FFFu; }
+__host__ __device__ inline unsigned step_tag(unsigned epoch, int t) {
+  return 1u + (epoch * 256u + (unsigned)t) % 0x3FFFu;
+}
 bool step_path_fits(int R, int d, int dh, int F, int T, int S);
 bool step_logits_fits(int R, int d);  // R <= 2, d a multiple of 64 up to 512
 int step_logits_blocks(int V);        // blocks (and arg-max partials per row) of launch_step_logits
@@ -322,6 +327,24 @@ hipError_t launch_step_ffn(const StepIn& in, const StepFfn& f, hipStream_t s);
 int step_layer_blocks(int heads, int F);
 hipError_t launch_step_layer(const StepIn& ia, const StepAttn& sa, const StepIn& ib, const StepAttn& ca,
                              const StepIn& ic, const StepFfn& f, hipStream_t s, const StepCommit* cm = nullptr);
+// The whole step of a two-layer decoder in one launch (k_step_all): the two
+// layers' role arguments as launch_step_layer takes them, the first layer's
+// folded commit, and the logits kernel's arguments (chained form: its input
+// waits on the last layer's flags).
+struct StepAll {
+  StepIn ia[2], ib[2], ic[2];
+  StepAttn sa[2], ca[2];
+  StepFfn f[2];
+  StepCommit cm;
+  StepIn lin;
+  StepLogits g;
+  int layer_blocks;  // step_layer_blocks(heads, F)
+};
+// Whether k_step_all covers a step: two layers of width 256, at
+// most 64 attended positions (self and cross), a vocabulary the tagged
+// logits take with 4 tiles of 16 rows per wave (V >= 24576).
+bool step_all_fits(int n_dec, int d, int heads, int F, int T, int S, int V);
+hipError_t launch_step_all(const StepAll& p, bool fold, hipStream_t s);
 // With ev_start / ev_stop the events take the kernel's own start and end times.
 hipError_t launch_step_logits(const StepIn& in, const StepLogits& g, hipStream_t s, hipEvent_t ev_start = nullptr,
                               hipEvent_t ev_stop = nullptr);
@@ -615,6 +638,7 @@ struct mnmt_session {
   bool counted_on = true;             // off with MNMT_COUNTED=0: flags between all step kernels
   bool merged_on = true;              // off with MNMT_MERGED_LAYERS=0: three launches per decoder layer
   bool tagged_on = true;              // off with MNMT_TAGGED=0: layer 0 waits on the logits kernel's flags
+  bool single_on = false;             // on with MNMT_STEP_LAUNCH=1: one launch per step (k_step_all)
   bool chain_on = true;               // off with MNMT_SERIAL_STEPS=1 in the environment
   std::map<std::string, hipGraphExec_t> graphs;
 };

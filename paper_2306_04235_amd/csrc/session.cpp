@@ -791,6 +791,11 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   // (the logits kernel's 256 threads poll one flag word per block of the
   // last layer's launch)
   const bool merged = S->merged_on && counted && step_layer_blocks(h, m->info.d_ffn) <= 256;
+  // single: the two layers and the logits in one launch (k_step_all), whose
+  // arguments are collected here; the chain then advances once per step
+  const bool single = merged && tagged && S->single_on &&
+                      step_all_fits((int)m->dec.size(), d, h, m->info.d_ffn, T, S->S, m->info.vocab);
+  StepAll all{};
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
     const StepCommit* cml = folded && l == 0 ? &cm : nullptr;
@@ -865,7 +870,22 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
       }
       std::swap(xa, xb);
     }
-    if (merged) {
+    if (single) {
+      // the arguments of this layer's share of the step's launch; the last
+      // layer flags its blocks for the logits blocks (the chain's waits and
+      // errors are set with the launch)
+      all.ia[l] = ia;
+      all.sa[l] = sa;
+      all.ib[l] = ib;
+      all.ca[l] = ca;
+      all.ic[l] = ic;
+      all.f[l] = f;
+      if (l + 1 == m->dec.size()) {
+        all.ic[l].chain.done = S->chain + (size_t)(3 * l) * kChainSlotWords;
+        all.ic[l].chain.val = (unsigned)(t + 1);
+      }
+      if (cml) all.cm = *cml;
+    } else if (merged) {
       // the launch's chain: in the first layer the self- and cross-attention
       // blocks wait on the previous kernel's flags (the cross blocks of a
       // folded step read the previous step's arg-max partials, which only
@@ -910,7 +930,22 @@ int greedy_step_v3(mnmt_session* S, int R, int t, int stop_at_eos, float* logits
   g.t = t;
   const hipStream_t ks =
       ch ? ch->next(in.chain, 3 * (int)m->dec.size(), step_logits_blocks_chained(g.V, d), t + 1) : s;
-  LAUNCH(launch_step_logits(in, g, ks));
+  if (single) {
+    // one launch for the step: the logits blocks wait on the last layer's
+    // flags inside it; the step's first layer waits as the launch (tagged:
+    // it polls the previous step's partials instead)
+    all.layer_blocks = step_layer_blocks(h, m->info.d_ffn);
+    const int lastl = (int)m->dec.size() - 1;
+    for (int l = 0; l <= lastl; ++l) all.ia[l].chain.err = all.ib[l].chain.err = all.ic[l].chain.err = in.chain.err;
+    all.lin = in;
+    all.lin.chain.wait = all.ic[lastl].chain.done;
+    all.lin.chain.nwait = all.layer_blocks;
+    all.lin.chain.want = (unsigned)(t + 1);
+    all.g = g;
+    LAUNCH(launch_step_all(all, folded, ks));
+  } else {
+    LAUNCH(launch_step_logits(in, g, ks));
+  }
   FusedGemv gv{};
   gv.R = R;
   gv.t = t;
@@ -1181,6 +1216,11 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   // instead of polling its tagged arg-max partials
   const char* tagged = std::getenv("MNMT_TAGGED");
   S->tagged_on = !(tagged && std::atoi(tagged) == 0);
+  // MNMT_STEP_LAUNCH=1: the whole step of a two-layer decoder in one launch
+  // instead of a launch per decoder layer and one for the logits (measured
+  // slower: its logits blocks poll from the start of the step)
+  const char* single = std::getenv("MNMT_STEP_LAUNCH");
+  S->single_on = single && std::atoi(single) != 0;
   // the encoder accumulators start at zero (each encode leaves them so), the
   // chain error word too
   hipError_t h = hipMemsetAsync(S->enc_acc, 0, enc_acc_bytes(d), S->capture_stream);

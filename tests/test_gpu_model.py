@@ -222,20 +222,27 @@ def test_kernel_chain_many_sentences(torch_dev, monkeypatch):
         assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), f"sentence {k}"
 
 
-@pytest.mark.parametrize("merged", ["1", "0"])
-def test_layer_launch_forms(torch_dev, monkeypatch, merged):
-    """Each decoder layer of the batch-1 step is one launch whose
-    self-attention, cross-attention and FFN blocks hand off through the
-    counted words inside it, or with MNMT_MERGED_LAYERS=0 (read at session
-    creation) three launches.  Per-step logits bits and tokens equal the
-    oracle's at one and two rows, pre- and post-LN, with 4-bit weights, shared
-    layers and widths 64-512, eager and in graph replays."""
+LAUNCH_FORMS = {"step": {"MNMT_STEP_LAUNCH": "1"}, "layer": {}, "three": {"MNMT_MERGED_LAYERS": "0"}}
+
+
+@pytest.mark.parametrize("form", list(LAUNCH_FORMS))
+def test_layer_launch_forms(torch_dev, monkeypatch, form):
+    """The batch-1 translation's decode step in one launch (two-layer models
+    of width 256 with a 32000-word vocabulary: both layers' self-
+    attention, cross-attention and FFN blocks and the logits blocks, handing
+    off through the counted words and flags inside it; MNMT_STEP_LAUNCH=1),
+    one launch per decoder layer and one for the logits (the default), or
+    with MNMT_MERGED_LAYERS=0 three launches per layer (read at session
+    creation).  Per-step logits bits and tokens equal the oracle's at one and
+    two rows, pre- and post-LN, with 4-bit weights, shared layers and widths
+    64-512, eager and in graph replays."""
     import dataclasses
 
     torch, dev = torch_dev
     from paper_2306_04235_amd import mnmt
 
-    monkeypatch.setenv("MNMT_MERGED_LAYERS", merged)
+    for k, v in LAUNCH_FORMS[form].items():
+        monkeypatch.setenv(k, v)
     src, lens = G.workload_inputs(G.WORKLOADS["mobile"])
     _greedy_check(torch, dev, "MOBILE", src, lens, 30)
     mob4 = dataclasses.replace(G.MOBILE, name="mobile-w4", w_bits=4)
@@ -247,9 +254,9 @@ def test_layer_launch_forms(torch_dev, monkeypatch, merged):
 
 
 def test_merged_layers_many_sentences(torch_dev, monkeypatch):
-    """Two dozen batch-1 sentences in graph replays through the merged layer
-    launches against the three-kernel layers (both on the counted hand-off),
-    the first four also against the oracle."""
+    """Two dozen batch-1 sentences in graph replays through the one-launch
+    step against the per-layer launches and the three-kernel layers (all on
+    the counted hand-off), the first four also against the oracle."""
     torch, dev = torch_dev
     from paper_2306_04235_amd import mnmt
 
@@ -257,8 +264,9 @@ def test_merged_layers_many_sentences(torch_dev, monkeypatch):
     rng = np.random.default_rng(2025)
     lens_all = rng.integers(10, 31, 24)
     outs = {}
-    for merged in ("1", "0"):
-        monkeypatch.setenv("MNMT_MERGED_LAYERS", merged)
+    for form, env in LAUNCH_FORMS.items():
+        monkeypatch.setenv("MNMT_STEP_LAUNCH", env.get("MNMT_STEP_LAUNCH", "0"))
+        monkeypatch.setenv("MNMT_MERGED_LAYERS", env.get("MNMT_MERGED_LAYERS", "1"))
         sess = mnmt.Session(gm, 1, 30, 30, 1)
         got = []
         for k, n in enumerate(lens_all):
@@ -267,14 +275,43 @@ def test_merged_layers_many_sentences(torch_dev, monkeypatch):
                                              use_graph=True)
             torch.cuda.synchronize()
             got.append((out.cpu().numpy().copy(), out_len.cpu().numpy().copy()))
-            if merged == "1" and k < 4:
+            if form == "step" and k < 4:
                 o_out, o_len = om.greedy(src, lens, 30)[:2]
                 assert np.array_equal(got[-1][0], o_out) and np.array_equal(got[-1][1], o_len), f"sentence {k}"
         assert int(sess.tensor("chain_err", torch.int32, (1,)).cpu().numpy()[0]) == 0
         sess.close()
-        outs[merged] = got
-    for k, (a, b) in enumerate(zip(outs["0"], outs["1"])):
-        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), f"sentence {k}"
+        outs[form] = got
+    for other in ("layer", "three"):
+        for k, (a, b) in enumerate(zip(outs[other], outs["step"])):
+            assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1]), f"{other}: sentence {k}"
+
+
+@pytest.mark.parametrize("form", ["step", "layer"])
+def test_many_translations_in_one_session(torch_dev, monkeypatch, form):
+    """130 batch-1 translations of one sentence in one session, each alone
+    in a graph replay: the tags that the chained step kernels hand off by
+    (translation counter, step) wrap around more than once, and every
+    translation must still equal the oracle's with no chain wait giving up
+    (a tag that once coincided with that of the cleared slots derailed every
+    64th translation)."""
+    torch, dev = torch_dev
+    from paper_2306_04235_amd import mnmt
+
+    for k, v in LAUNCH_FORMS[form].items():
+        monkeypatch.setenv(k, v)
+    om, gm = _pair("MOBILE")
+    src, lens = G.workload_inputs(G.WORKLOADS["mobile"])
+    o_out, o_len = om.greedy(src, lens, 30)[:2]
+    sess = mnmt.Session(gm, 1, 30, 30, 1)
+    ts, tl = _t(torch, dev, src), _t(torch, dev, lens)
+    err = sess.tensor("chain_err", torch.int32, (1,))
+    for k in range(130):
+        out, out_len, _ = sess.translate(ts, tl, beam=1, max_steps=30, use_graph=True)
+        torch.cuda.synchronize()
+        assert int(err.cpu().numpy()[0]) == 0, f"translation {k}: a chained wait gave up"
+        assert np.array_equal(out.cpu().numpy(), o_out) and np.array_equal(out_len.cpu().numpy(), o_len), k
+    sess.status()
+    sess.close()
 
 
 WIDE384 = G.ModelConfig("wide-384", 384, 6, 768, 2, 1, 600, ln_post=0, seed=83, random_gamma=True, weight_std=0.05)
