@@ -198,8 +198,9 @@ __device__ __forceinline__ void softmax_context(float (&sv)[NI], int n, int dh, 
 // the residual stream or computed as the token embedding, optionally layer-
 // normalized, then quantized into a_lds + r * lds_stride.  `writer` blocks
 // also store the embedding (wb_input) or the normalized row (post-LN) to
-// in.x_out.  Wave w prepares rows w, w + 4, ...; each wave works on
-// kPrepGroup rows at once so that their loads and reductions overlap.
+// in.x_out.  Wave w prepares rows w, w + 4, ...; each wave works on G rows
+// at once (kPrepGroup by default) so that their loads and reductions
+// overlap: a wave with all its rows in one group pays one memory round trip.
 constexpr int kPrepGroup = 4;
 
 // Row-width classes the fused kernels are compiled for (d <= class).
@@ -217,7 +218,7 @@ __host__ __device__ constexpr int lanes_per_row(int dmax) {
 // the LayerNorm's gain and bias are loaded once before the rows: a load under
 // a lane condition makes the compiler wait for it where the paths join, which
 // would turn the loads of a row group into one memory round trip each.
-template <int NJ>  // d <= 64 * NJ
+template <int NJ, int G = kPrepGroup>  // d <= 64 * NJ; G rows per wave at once
 __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int row0, int d, int t, int8_t* a_lds,
                                              int lds_stride, bool writer) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -232,10 +233,10 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
       bj[j] = in.b[i];
     }
   }
-  for (int r0 = wave; r0 < rows; r0 += 4 * kPrepGroup) {
-    float v[kPrepGroup][NJ];
+  for (int r0 = wave; r0 < rows; r0 += 4 * G) {
+    float v[G][NJ];
 #pragma unroll
-    for (int g = 0; g < kPrepGroup; ++g) {
+    for (int g = 0; g < G; ++g) {
       const int r = r0 + 4 * g;
       const size_t gr = (size_t)(row0 + (r < rows ? r : 0));
       if (in.embed) {
@@ -255,7 +256,7 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
     }
     if (writer && in.wb_input) {
 #pragma unroll
-      for (int g = 0; g < kPrepGroup; ++g) {
+      for (int g = 0; g < G; ++g) {
         const int r = r0 + 4 * g;
         if (r >= rows) continue;
 #pragma unroll
@@ -266,23 +267,22 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
       }
     }
     if (in.do_ln) {
-      // mean: canonical sum of each row (lane partials over ascending i, butterfly)
-      float p[kPrepGroup];
+      // mean: canonical sum of each row (lane partials over ascending i, then
+      // the butterfly without the LDS crossbar)
+      float p[G];
 #pragma unroll
-      for (int g = 0; g < kPrepGroup; ++g) {
+      for (int g = 0; g < G; ++g) {
         p[g] = 0.0f;
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
           if (j < n && lane + 64 * j < d) p[g] = p[g] + v[g][j];
       }
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1)
-#pragma unroll
-        for (int g = 0; g < kPrepGroup; ++g) p[g] = p[g] + __shfl_xor(p[g], off, 64);
+      for (int g = 0; g < G; ++g) p[g] = wave_sum(p[g]);
       const float inv_d = 1.0f / (float)d;
-      float p2[kPrepGroup];
+      float p2[G];
 #pragma unroll
-      for (int g = 0; g < kPrepGroup; ++g) {
+      for (int g = 0; g < G; ++g) {
         const float mu = p[g] * inv_d;
         p2[g] = 0.0f;
 #pragma unroll
@@ -294,11 +294,9 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
         }
       }
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1)
+      for (int g = 0; g < G; ++g) p2[g] = wave_sum(p2[g]);
 #pragma unroll
-        for (int g = 0; g < kPrepGroup; ++g) p2[g] = p2[g] + __shfl_xor(p2[g], off, 64);
-#pragma unroll
-      for (int g = 0; g < kPrepGroup; ++g) {
+      for (int g = 0; g < G; ++g) {
         const float var = p2[g] * inv_d;
         const float rstd = 1.0f / sqrtf(var + in.eps);
 #pragma unroll
@@ -307,7 +305,7 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
       }
     }
 #pragma unroll
-    for (int g = 0; g < kPrepGroup; ++g) {
+    for (int g = 0; g < G; ++g) {
       const int r = r0 + 4 * g;
       if (r >= rows) continue;
 #pragma unroll

@@ -87,9 +87,12 @@ hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, co
 // packed 4-bit, the I8 requantization with q_scale / q_bias), for W <= 16
 // and d 256 (attn_cross_q_fits).
 bool attn_cross_q_fits(int W, int d);
-hipError_t launch_attn_dec_cross_q(const int8_t* rows, const int8_t* wq, const float* q_scale, const float* q_bias,
-                                   bool w4, int R, int W, int d, int h, const int8_t* kv, int S, const int32_t* len,
-                                   float c_qk, float c_pv, int8_t* ctx, hipStream_t s);
+// rows: the int8 input rows [R, d], or with ln (rows null) the LayerNorm +
+// quantization of ln->x computed by each block for its sentence's rows.
+struct FusedIn;
+hipError_t launch_attn_dec_cross_q(const int8_t* rows, const FusedIn* ln, const int8_t* wq, const float* q_scale,
+                                   const float* q_bias, bool w4, int R, int W, int d, int h, const int8_t* kv, int S,
+                                   const int32_t* len, float c_qk, float c_pv, int8_t* ctx, hipStream_t s);
 
 // Greedy bookkeeping after the fused logits/arg-max of a step.
 // out_key [T][R] (or null) receives each step's winning arg-max key.
@@ -417,9 +420,12 @@ hipError_t launch_enc_attn(const EncIn& in, const EncAttn& at, int heads, hipStr
 hipError_t launch_enc_ffn(const EncIn& in, const EncFfn& f, hipStream_t s);
 hipError_t launch_enc_out(const EncIn& in, const EncOut& o, hipStream_t s);
 
-// Small-M GEMM (M <= 64, K <= 1024) on 16x16x64 matrix cores; with `in` the
-// rows are prepared (embedding / LayerNorm / quantization) in its prologue.
+// Small-M GEMM (M <= 64, K <= 1024; up to 512 rows for the shapes
+// qgemm_rows_fit accepts) on 16x16x64 matrix cores; with `in` the rows are
+// prepared (embedding / LayerNorm / quantization, rows up to 1024 wide) in
+// its prologue.
 bool qgemm_small_fits(int M, int K);
+bool qgemm_rows_fit(int M, int K, int N);
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
                               const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s,
                               bool w4 = false);
@@ -639,6 +645,7 @@ struct mnmt_session {
   bool merged_on = true;              // off with MNMT_MERGED_LAYERS=0: three launches per decoder layer
   bool tagged_on = true;              // off with MNMT_TAGGED=0: layer 0 waits on the logits kernel's flags
   bool single_on = false;             // on with MNMT_STEP_LAUNCH=1: one launch per step (k_step_all)
+  bool ln_fused_on = true;            // off with MNMT_LN_FUSED=0: batched LayerNorms as kernels of their own
   bool chain_on = true;               // off with MNMT_SERIAL_STEPS=1 in the environment
   std::map<std::string, hipGraphExec_t> graphs;
 };

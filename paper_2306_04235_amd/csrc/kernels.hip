@@ -207,6 +207,8 @@ struct SharedAttn {
   const int8_t* wq;
   const float* q_scale;
   const float* q_bias;
+  int ln_on;             // QF > 0: the rows a are computed from ln (LayerNorm + quantization of fp32 rows)
+  FusedIn ln;
   int rows;              // query rows per group (row r = group * rows + i)
   const int8_t* kv;      // group g's key t of the head at kv + g * kv_group + k_off + t * ldkv + head * dh
   size_t kv_group;
@@ -222,15 +224,21 @@ struct SharedAttn {
 // itself (the cross-attention's Q projection, d = 64 KQ, at most 16 rows),
 // on v_mfma_i32_16x16x64_i8 with the group's rows as A, wave w taking the
 // 16-column fragments w, w + WAVES, ..., and the same requantization as the
-// linear layer's I8 epilogue, into LDS.
+// linear layer's I8 epilogue, into LDS.  With ln_on the group's A rows are
+// the LayerNorm + quantization of its fp32 rows (prepare_rows, one row per
+// wave at a time), computed while the weight, key and value loads are in
+// flight.
 template <int NMAX, int DHMAX, int WAVES, int QF = 0, int KQ = 1>
 __global__ __launch_bounds__(64 * WAVES) void k_attn_shared(SharedAttn a) {
+  static_assert(QF == 0 || WAVES == 4, "the row prologue runs on 4 waves");
   constexpr int DHC = DHMAX / 16, KS = DHMAX + 16, NI = NMAX / 64;
   constexpr int CH = NMAX * DHC, PER = (CH + 64 * WAVES - 1) / (64 * WAVES);
+  constexpr int AL = 64 * KQ + 16;  // LDS row stride of the normalized rows
   __shared__ __attribute__((aligned(16))) int8_t kl[NMAX * KS];
   __shared__ __attribute__((aligned(16))) int8_t vl[NMAX * DHMAX];
   __shared__ __attribute__((aligned(16))) float pl[WAVES][NMAX];
   __shared__ __attribute__((aligned(16))) int8_t ql[QF ? 16 * DHMAX : 16];
+  __shared__ __attribute__((aligned(16))) int8_t al[QF ? 16 * AL : 16];
   const int hd = blockIdx.x, g = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int dh = a.dh, nc = dh / 16;
@@ -257,15 +265,26 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_shared(SharedAttn a) {
     // at a time (nc <= 8 fragments)
     constexpr bool W4 = QF == 2;
     const int d = 64 * KQ, l16 = lane & 15, koff = 16 * (lane >> 4);
-    const int8_t* ar = a.a + ((size_t)g * rows + min(l16, rows - 1)) * d;
-    v4i af[KQ];
+    WFrag<W4> bf[KQ];
 #pragma unroll
-    for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(ar + 64 * kk + koff);
+    for (int kk = 0; kk < KQ; ++kk) bf[kk] = load_wfrag_if<W4>(wave < nc, a.wq, hd * dh + 16 * wave + l16, d, 64 * kk + koff);
+    v4i af[KQ];
+    if (a.ln_on) {
+      prepare_rows<KQ>(a.ln, rows, g * rows, d, 0, al, AL, false);
+      lds_barrier();
+#pragma unroll
+      for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(al + min(l16, rows - 1) * AL + 64 * kk + koff);
+    } else {
+      const int8_t* ar = a.a + ((size_t)g * rows + min(l16, rows - 1)) * d;
+#pragma unroll
+      for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(ar + 64 * kk + koff);
+    }
     for (int f = wave; f < nc; f += WAVES) {
       const int col = hd * dh + 16 * f + l16;
-      WFrag<W4> bf[KQ];
+      if (f != wave) {
 #pragma unroll
-      for (int kk = 0; kk < KQ; ++kk) bf[kk] = load_wfrag<W4>(a.wq, col, d, 64 * kk + koff);
+        for (int kk = 0; kk < KQ; ++kk) bf[kk] = load_wfrag<W4>(a.wq, col, d, 64 * kk + koff);
+      }
       const float sc = a.q_scale[col], bi = a.q_bias[col];
       v4i acc = {0, 0, 0, 0};
 #pragma unroll
@@ -1212,14 +1231,19 @@ hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, c
 // 34.6 ms), so the separate Q projection stays.
 bool attn_cross_q_fits(int W, int d) { return W >= 1 && W <= 16 && d == 256; }
 
-hipError_t launch_attn_dec_cross_q(const int8_t* rows, const int8_t* wq, const float* q_scale, const float* q_bias,
-                                   bool w4, int R, int W, int d, int h, const int8_t* kv, int S, const int32_t* len,
-                                   float c_qk, float c_pv, int8_t* ctx, hipStream_t s) {
+hipError_t launch_attn_dec_cross_q(const int8_t* rows, const FusedIn* ln, const int8_t* wq, const float* q_scale,
+                                   const float* q_bias, bool w4, int R, int W, int d, int h, const int8_t* kv, int S,
+                                   const int32_t* len, float c_qk, float c_pv, int8_t* ctx, hipStream_t s) {
   const int dh = d / h;
-  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16 || R % W || !attn_cross_q_fits(W, d) || !rows || !wq)
+  if (S > kMaxAttnLen || dh > kMaxHeadDim || dh % 16 || R % W || !attn_cross_q_fits(W, d) || !wq ||
+      (ln ? !ln->x || ln->embed || ln->x_out : !rows))
     return hipErrorInvalidValue;
   SharedAttn a{};
   a.a = rows;
+  if (ln) {
+    a.ln_on = 1;
+    a.ln = *ln;
+  }
   a.wq = wq;
   a.q_scale = q_scale;
   a.q_bias = q_bias;

@@ -191,20 +191,24 @@ hipError_t gemv_lpr(const int8_t* X, int ldx, const int8_t* W, const float* scal
 constexpr int kSmallMaxK = 1024;
 
 // WAVES 4: a 32x32 tile per block; WAVES 1 (no LN): a 16x16 tile per
-// one-wave block, four times the blocks over the same waves.
+// one-wave block, four times the blocks over the same waves.  WIDE (with LN):
+// 16 rows x 64 columns per block, wave w the columns 16 w.., so that each
+// wave normalizes 4 of the rows (the LayerNorm is repeated by every column
+// block, and its instructions, not the loads, set the prologue's length).
 // W4: W holds packed 4-bit rows (K / 2 bytes each), widened in registers.
-template <bool LN, int KMAX, int WAVES = 4, bool W4 = false>  // K <= KMAX
+template <bool LN, int KMAX, int WAVES = 4, bool W4 = false, bool WIDE = false>  // K <= KMAX
 __global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const int8_t* __restrict__ X, int ldx,
                                                             const int8_t* __restrict__ W, int M, int K, int N,
                                                             const float* __restrict__ scale,
                                                             const float* __restrict__ bias, EpiArgs e) {
   static_assert(WAVES == 4 || (WAVES == 1 && !LN), "32x32 tiles, or 16x16 without the row prologue");
+  static_assert(!WIDE || (LN && WAVES == 4), "16x64 tiles normalize their rows");
   constexpr int NK = (KMAX + 63) / 64;
-  constexpr int TILE = WAVES == 4 ? 32 : 16;
-  __shared__ __attribute__((aligned(16))) int8_t As[LN ? 32 * (KMAX + 16) : 16];
+  constexpr int TM = WIDE ? 16 : WAVES == 4 ? 32 : 16, TN = WIDE ? 64 : TM;
+  __shared__ __attribute__((aligned(16))) int8_t As[LN ? TM * (KMAX + 16) : 16];
   const int lane = threadIdx.x & 63, wave = WAVES == 4 ? threadIdx.x >> 6 : 0;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * TILE, n0 = blockIdx.x * TILE;
+  const int wm = WIDE ? 0 : wave >> 1, wn = WIDE ? wave : wave & 1;
+  const int m0 = blockIdx.y * TM, n0 = blockIdx.x * TN;
   const int nk = K / 64;
   const int col = n0 + 16 * wn + (lane & 15);
   const int koff = 16 * (lane >> 4);
@@ -230,8 +234,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_qgemm_small(FusedIn in, const in
   v4i acc = {0, 0, 0, 0};
   if (LN) {
     const int KP = K + 16;
-    const int rows = M - m0 < 32 ? M - m0 : 32;
-    prepare_rows<(KMAX + 63) / 64>(in, rows, m0, K, 0, As, KP, blockIdx.x == 0);
+    const int rows = M - m0 < TM ? M - m0 : TM;
+    // the wave's TM / 4 rows in one group (one round trip) up to 512-wide rows
+    prepare_rows<(KMAX + 63) / 64, KMAX <= 512 ? TM / 4 : kPrepGroup>(in, rows, m0, K, 0, As, KP, blockIdx.x == 0);
     __syncthreads();
     const int lr = 16 * wm + (lane & 15);
 #pragma unroll
@@ -280,15 +285,20 @@ bool qgemm_rows_fit(int M, int K, int N) {
 
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
                               const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s, bool w4) {
-  if (M < 1 || M > (in ? 64 : kSmallMaxRows) || K > kSmallMaxK || K % 64 || (in && K > kMaxRowLen))
-    return hipErrorInvalidValue;
+  if (M < 1 || M > kSmallMaxRows || K > kSmallMaxK || K % 64 || (in && K > kMaxRowLen)) return hipErrorInvalidValue;
   // 65-256 rows (the mobile beam decoder): one-wave blocks of 16x16 (at 512
-  // rows their four-fold block count made the base beam step slower)
-  const bool one = !in && M > 64 && M <= 256;
-  const dim3 grid = one ? dim3((N + 15) / 16, (M + 15) / 16) : dim3((N + 31) / 32, (M + 31) / 32);
+  // rows their four-fold block count made the base beam step slower); rows
+  // normalized in the prologue above 64 rows: 16x64 tiles
+  const bool one = !in && M > 64 && M <= 256, wide = in && M > 64;
+  const dim3 grid = one    ? dim3((N + 15) / 16, (M + 15) / 16)
+                    : wide ? dim3((N + 63) / 64, (M + 15) / 16)
+                           : dim3((N + 31) / 32, (M + 31) / 32);
   const FusedIn none{};
 #define MNMT_SMALL_W(KM, W4)                                                                                   \
-  if (in)                                                                                                      \
+  if (wide)                                                                                                    \
+    hipLaunchKernelGGL((k_qgemm_small<true, KM, 4, W4, true>), grid, dim3(256), 0, s, *in, X, ldx, W, M, K, N,  \
+                       scale, bias, e);                                                                        \
+  else if (in)                                                                                                 \
     hipLaunchKernelGGL((k_qgemm_small<true, KM, 4, W4>), grid, dim3(256), 0, s, *in, X, ldx, W, M, K, N, scale, \
                        bias, e);                                                                               \
   else if (one)                                                                                                \

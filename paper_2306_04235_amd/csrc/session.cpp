@@ -478,8 +478,24 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
     }
     return MNMT_OK;
   };
-  // the linear layer L over the rows LN(x) quantized with L's input scale
+  // the linear layer L over the rows LN(x) quantized with L's input scale;
+  // pre-LN rows that the one-round-trip GEMM takes are normalized in its
+  // prologue (each block its 32 rows) instead of by a kernel of their own
   auto ln_linear = [&](const LinearDev& L, const LnDev& ln, int kind, void* out) -> int {
+    if (S->ln_fused_on && !post && !pend.splits && R > 64 && qgemm_rows_fit(R, L.K, L.N) && L.K == d) {
+      FusedIn in{};
+      in.x = xc;
+      in.do_ln = 1;
+      in.g = ln.g;
+      in.b = ln.b;
+      in.eps = eps;
+      in.inv_s = L.inv_in;
+      const int8_t* w;
+      const bool w4 = batched_weights(L, w);
+      const EpiArgs e{kind, out, L.N, 1.f, nullptr};
+      LAUNCH(launch_qgemm_small(&in, nullptr, 0, w, L.scale, L.bias, R, L.K, L.N, e, s, w4));
+      return MNMT_OK;
+    }
     const int rc = ln_rows(ln, L.inv_in, post);
     return rc ? rc : qlin(L, S->dec_a, R, kind, out, 1.f, s);
   };
@@ -499,12 +515,24 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
       // the Q projection inside the attention kernel, from the LayerNorm'd
       // rows in dec_a; the context goes to dec_q (other blocks of a sentence
       // still read its rows of dec_a)
-      if ((rc = ln_rows(post ? L.sa_ln : L.ca_ln, L.cq.inv_in, post))) return rc;
+      // (pre-LN: each block normalizes its sentence's rows itself)
+      const bool own_ln = S->ln_fused_on && !post && !pend.splits;
+      FusedIn in{};
+      if (own_ln) {
+        in.x = xc;
+        in.do_ln = 1;
+        in.g = L.ca_ln.g;
+        in.b = L.ca_ln.b;
+        in.eps = eps;
+        in.inv_s = L.cq.inv_in;
+      } else if ((rc = ln_rows(post ? L.sa_ln : L.ca_ln, L.cq.inv_in, post))) {
+        return rc;
+      }
       const int8_t* wq;
       const bool w4 = batched_weights(L.cq, wq);
       cctx = S->dec_q;
-      LAUNCH(launch_attn_dec_cross_q(S->dec_a, wq, L.cq.scale, L.cq.bias, w4, R, W, d, h, S->cross_kv[l], S->S,
-                                     S->len, L.ca_cqk, L.ca_cpv, cctx, s));
+      LAUNCH(launch_attn_dec_cross_q(own_ln ? nullptr : S->dec_a, own_ln ? &in : nullptr, wq, L.cq.scale, L.cq.bias,
+                                     w4, R, W, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, cctx, s));
     } else {
       if ((rc = ln_linear(L.cq, post ? L.sa_ln : L.ca_ln, MNMT_EPI_I8, S->dec_q))) return rc;
       LAUNCH(launch_attn_dec_cross(S->dec_q, R, W, d, h, S->cross_kv[l], S->S, S->len, L.ca_cqk, L.ca_cpv, cctx, s));
@@ -1221,6 +1249,10 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   // slower: its logits blocks poll from the start of the step)
   const char* single = std::getenv("MNMT_STEP_LAUNCH");
   S->single_on = single && std::atoi(single) != 0;
+  // MNMT_LN_FUSED=0: the batched decoder's pre-LN LayerNorms as kernels of
+  // their own instead of in the prologue of the linear layer they feed
+  const char* lnf = std::getenv("MNMT_LN_FUSED");
+  S->ln_fused_on = !(lnf && std::atoi(lnf) == 0);
   // the encoder accumulators start at zero (each encode leaves them so), the
   // chain error word too
   hipError_t h = hipMemsetAsync(S->enc_acc, 0, enc_acc_bytes(d), S->capture_stream);

@@ -367,6 +367,24 @@ def _beam_check(torch, dev, cfg, src, lens, W, steps, alpha, sample=None, parall
     sess.close()
 
 
+VARIED_BEAM = G.ModelConfig("varied-256-beam", 256, 4, 1024, 2, 2, 2000, ln_post=0, seed=1104, random_gamma=True,
+                            weight_std=0.2)
+
+
+@pytest.mark.parametrize("cfg", [DIVERSE, VARIED_BEAM], ids=lambda c: c.name)
+def test_batched_layernorm_forms(torch_dev, monkeypatch, cfg):
+    """Pre-LN beam search above 64 rows (19 sentences of beam 4: 76 rows, a
+    ragged last tile of 32 rows): the LayerNorms in the prologue of the
+    linear layers they feed (each block of the one-round-trip GEMM normalizes
+    its rows) and, with MNMT_LN_FUSED=0 (read at session creation), as
+    kernels of their own; both against the oracle on every sentence."""
+    torch, dev = torch_dev
+    src, lens = G.make_sources(cfg.vocab, 19, (2, 24), seed=97, s_max=24)
+    for fused in ("1", "0"):
+        monkeypatch.setenv("MNMT_LN_FUSED", fused)
+        _beam_check(torch, dev, cfg, src, lens, 4, 12, 0.6, parallel=True)
+
+
 HEAD16 = G.ModelConfig("head-16", 128, 8, 256, 1, 1, 600, ln_post=0, seed=88, random_gamma=True, weight_std=0.1)
 HEAD128 = G.ModelConfig("head-128", 256, 2, 512, 1, 1, 600, ln_post=1, seed=89, random_gamma=True, weight_std=0.08)
 
