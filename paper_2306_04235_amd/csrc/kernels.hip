@@ -635,15 +635,17 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
 // of the vocabulary order (R2b: 512 partials fed four consecutive terms at a
 // time), so the wave butterflies and the tree of the 8 wave sums finish the
 // sum with no exchange of the exponentials.  The candidates then come from a
-// threshold: the score is monotone in z, so each thread's best score is
-// score + (its max z - lse), and the K-th largest of these over the lanes of
-// a wave has at least K scores of the row at or above it; the largest such
-// bound over the waves filters the row down to a short list (about 4K
-// entries on real logits), ranked by pairwise comparison.  If ties push the
-// list past kTopkCap, per-thread sorted lists over the threads' own elements,
-// merged over the block, take over.  The candidate order is total (score,
-// then index), so neither the filter nor the split over threads changes the
-// result.
+// threshold: the score is monotone in z, so for K <= 8 the smallest of the 8
+// wave maxima of z bounds at least 8 scores from below (one per wave), and
+// otherwise each thread's best score is score + (its max z - lse) and the
+// K-th largest of these over the lanes of a wave has at least K scores of the
+// row at or above it (the largest such bound over the waves is taken).  The
+// bound filters the row down to a short list (2-8K entries on real logits),
+// ranked by one wave (up to 64 entries) or pairwise comparison.  If ties push
+// the list past kTopkCap, per-thread sorted lists over the threads' own
+// elements, merged over the block, take over.  The candidate order is total
+// (score, then index), so neither the filter nor the split over threads
+// changes the result.
 constexpr int kTopkMaxV = 32768;
 constexpr int kTopkThreads = 512, kTopkWaves = kTopkThreads / 64;
 constexpr int kTopkV4 = kTopkMaxV / 4 / kTopkThreads;  // float4 per thread
@@ -665,9 +667,11 @@ __device__ __forceinline__ unsigned long long block_max_u64(unsigned long long v
 // Per-thread sorted lists over the thread's own elements (scores
 // sc + (z - lse) of elements 4 (tid + 512 k) + q), merged over the block: the
 // path for rows whose filtered list overflows (large groups of equal scores).
+// It reads the row again from memory, in a loop that is not unrolled: the
+// common path then holds neither the row's registers nor this code inline.
 template <int K>
-__device__ __forceinline__ void topk_lists(const float4 (&zr)[kTopkV4], int n4, float sc, float lse,
-                                           unsigned long long* redk, int* cand_tok, float* cand_score) {
+__device__ __noinline__ void topk_lists(const float4* __restrict__ z4, int n4, float sc, float lse,
+                                        unsigned long long* redk, int* cand_tok, float* cand_score) {
   const int tid = threadIdx.x;
   float ls[K];
   int lv[K];
@@ -676,11 +680,12 @@ __device__ __forceinline__ void topk_lists(const float4 (&zr)[kTopkV4], int n4, 
     ls[k] = -FLT_MAX;
     lv[k] = INT_MAX;
   }
-#pragma unroll
+#pragma unroll 1
   for (int k = 0; k < kTopkV4; ++k) {
     const int i = tid + kTopkThreads * k;
     if (i >= n4) continue;
-    const float zq[4] = {zr[k].x, zr[k].y, zr[k].z, zr[k].w};
+    const float4 zk = z4[i];
+    const float zq[4] = {zk.x, zk.y, zk.z, zk.w};
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       float c = sc + (zq[q] - lse);
@@ -723,8 +728,9 @@ __device__ __forceinline__ void topk_lists(const float4 (&zr)[kTopkV4], int n4, 
 template <int K>
 __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* __restrict__ logits, BeamState st,
                                                          const int* __restrict__ step) {
-  __shared__ float list_c[kTopkCap];
-  __shared__ int list_v[kTopkCap];
+  // 8 entries past the cap: the ranking reads the list 8 entries at a time
+  __shared__ __attribute__((aligned(16))) float list_c[kTopkCap + 8];
+  __shared__ __attribute__((aligned(16))) int list_v[kTopkCap + 8];
   __shared__ float redf[kTopkWaves];
   __shared__ float reds[kTopkWaves];
   __shared__ unsigned long long redk[kTopkWaves];
@@ -772,51 +778,102 @@ __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* _
   __syncthreads();
   const float lse =
       mx + canon_log(((reds[0] + reds[1]) + (reds[2] + reds[3])) + ((reds[4] + reds[5]) + (reds[6] + reds[7])));
-  // 3. the bound: the K-th largest thread-best score of each wave (scores
-  //    below -FLT_MAX never qualify), the largest over the waves
-  const float cm = sc + (tmx - lse);
-  float v = cm >= -FLT_MAX ? cm : -INFINITY;
-  float kth = -INFINITY;
+  // 3. the bound (scores below -FLT_MAX never qualify).  K <= 8 with every
+  //    wave holding elements (V > 1792): the smallest of the 8 wave maxima
+  //    (already in redf), since each wave has an element at or above it.
+  //    Otherwise the K-th largest thread-best score of each wave, the largest
+  //    over the waves.
+  float tau;
+  if (K <= kTopkWaves && n4 > kTopkThreads - 64) {
+    float zmin = redf[0];
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    kth = wave_max(v);
-    const unsigned long long hold = __ballot(v == kth);
-    if (lane == __ffsll((long long)hold) - 1) v = -INFINITY;  // drop one holder
+    for (int w = 1; w < kTopkWaves; ++w) zmin = fminf(zmin, redf[w]);
+    tau = fmaxf(sc + (zmin - lse), -FLT_MAX);
+  } else {
+    const float cm = sc + (tmx - lse);
+    float v = cm >= -FLT_MAX ? cm : -INFINITY;
+    float kth = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      kth = wave_max(v);
+      const unsigned long long hold = __ballot(v == kth);
+      if (lane == __ffsll((long long)hold) - 1) v = -INFINITY;  // drop one holder
+    }
+    __syncthreads();  // every read of redf (the maximum) is done
+    if (lane == 0) redf[wave] = fmaxf(kth, -FLT_MAX);
+    __syncthreads();
+    tau = redf[0];
+#pragma unroll
+    for (int w = 1; w < kTopkWaves; ++w) tau = fmaxf(tau, redf[w]);
   }
-  __syncthreads();  // every read of redf (the maximum) is done
-  if (lane == 0) redf[wave] = fmaxf(kth, -FLT_MAX);
-  __syncthreads();
-  float tau = redf[0];
-#pragma unroll
-  for (int w = 1; w < kTopkWaves; ++w) tau = fmaxf(tau, redf[w]);
-  // 4. the filtered list: every score at or above the bound
+  // 4. the filtered list: every score at or above the bound (one branch and
+  //    at most one list slot reservation per 4 elements)
 #pragma unroll
   for (int k = 0; k < kTopkV4; ++k) {
     const int i = tid + kTopkThreads * k;
-    if (i < n4) {
-      const float c4[4] = {sc + (zr[k].x - lse), sc + (zr[k].y - lse), sc + (zr[k].z - lse),
-                           sc + (zr[k].w - lse)};
+    const float c4[4] = {sc + (zr[k].x - lse), sc + (zr[k].y - lse), sc + (zr[k].z - lse),
+                         sc + (zr[k].w - lse)};
+    const int m = (int)(c4[0] >= tau) + (int)(c4[1] >= tau) + (int)(c4[2] >= tau) + (int)(c4[3] >= tau);
+    if (i < n4 && m > 0) {
+      int pos = atomicAdd(&n_list, m);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if (c4[q] >= tau) {
-          const int pos = atomicAdd(&n_list, 1);
           if (pos < kTopkCap) {
             list_c[pos] = c4[q];
             list_v[pos] = 4 * i + q;
           }
+          ++pos;
         }
       }
     }
   }
   __syncthreads();
   const int n = n_list;
+  if (n <= 64) {
+    // 5. up to 64 entries, one per lane of wave 0: rank = the number of
+    //    lanes whose (score, -index) key is larger (keys are distinct; the
+    //    order of pack_argmax is better()'s with -0 read as +0)
+    if (wave == 0) {
+      const bool live = lane < n;
+      const float ci = live ? list_c[lane] : -FLT_MAX;
+      const int vi = live ? list_v[lane] : 0;
+      const unsigned long long key = live ? pack_argmax(ci == 0.0f ? 0.0f : ci, vi) : 0ull;
+      const int hi = (int)(key >> 32), lo = (int)(uint32_t)key;
+      int rank = 0;
+#pragma unroll
+      for (int o = 0; o < 64; ++o) {
+        const unsigned long long ko = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane(hi, o) << 32) |
+                                      (uint32_t)__builtin_amdgcn_readlane(lo, o);
+        rank += ko > key ? 1 : 0;
+      }
+      if (live && rank < K) {
+        cand_tok[rank] = vi;
+        cand_score[rank] = ci;
+      }
+      if (!live && lane < K) {  // fewer than K scores qualify
+        cand_tok[lane] = 0;
+        cand_score[lane] = -FLT_MAX;
+      }
+    }
+    return;
+  }
   if (n <= kTopkCap) {
-    // 5. rank = the number of list entries that beat the entry
+    // 5. rank = the number of list entries that beat the entry, the list
+    //    read 8 entries at a time (four 16-byte reads issued together, the
+    //    entries past n masked)
     for (int i = tid; i < n; i += kTopkThreads) {
       const float ci = list_c[i];
       const int vi = list_v[i];
       int rank = 0;
-      for (int o = 0; o < n; ++o) rank += better(list_c[o], list_v[o], ci, vi) ? 1 : 0;
+      for (int o0 = 0; o0 < n; o0 += 8) {
+        const float4 c0 = *(const float4*)&list_c[o0], c1 = *(const float4*)&list_c[o0 + 4];
+        const int4 v0 = *(const int4*)&list_v[o0], v1 = *(const int4*)&list_v[o0 + 4];
+        const float co[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+        const int vo[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+        for (int u = 0; u < 8; ++u) rank += (o0 + u < n && better(co[u], vo[u], ci, vi)) ? 1 : 0;
+      }
       if (rank < K) {
         cand_tok[rank] = vi;
         cand_score[rank] = ci;
@@ -829,7 +886,7 @@ __global__ __launch_bounds__(kTopkThreads) void k_beam_topk_block(const float* _
     return;
   }
   // 5'. the overflow path: per-thread sorted lists, block merge
-  topk_lists<K>(zr, n4, sc, lse, redk, cand_tok, cand_score);
+  topk_lists<K>(z4, n4, sc, lse, redk, cand_tok, cand_score);
 }
 
 // Per sentence: merge the W rows' candidates, finish EOS hypotheses, refill
