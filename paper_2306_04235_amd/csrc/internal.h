@@ -77,6 +77,18 @@ hipError_t launch_attn_dec_self(const int8_t* qkv, int R, int d, int h, int T, c
                                 int8_t* vcache, const int32_t* hist, float c_qk, float c_pv, int8_t* ctx,
                                 hipStream_t s, int t_host = -1);
 
+// The same with the Q/K/V projection inside (the batched decoder: one block
+// per head and sentence of W <= 16 rows, d 128 or 256, heads 16-64 wide):
+// rows are the int8 input rows [R, d], or with ln (rows null) the LayerNorm
+// + quantization of ln->x computed by each block; wqkv [3d, d] (w4: packed
+// 4-bit rows) with the I8 requantization of scale / bias.
+struct FusedIn;
+bool attn_self_qkv_fits(int W, int d, int h, int T);
+hipError_t launch_attn_self_qkv(const int8_t* rows, const FusedIn* ln, const int8_t* wqkv, const float* scale,
+                                const float* bias, bool w4, int R, int W, int d, int h, int T, const int* step,
+                                int8_t* kcache, int8_t* vcache, const int32_t* hist, float c_qk, float c_pv,
+                                int8_t* ctx, hipStream_t s, int t_host);
+
 // Decoder cross-attention: row r attends over the cross keys/values of
 // sentence r / W (kv [B*S, 2d]) limited to len[b].
 hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, const int8_t* kv, int S,
@@ -646,6 +658,7 @@ struct mnmt_session {
   bool tagged_on = true;              // off with MNMT_TAGGED=0: layer 0 waits on the logits kernel's flags
   bool single_on = false;             // on with MNMT_STEP_LAUNCH=1: one launch per step (k_step_all)
   bool ln_fused_on = true;            // off with MNMT_LN_FUSED=0: batched LayerNorms as kernels of their own
+  bool qkv_fused_on = true;           // off with MNMT_QKV_FUSED=0: the batched Q/K/V projection as its own GEMM
   bool chain_on = true;               // off with MNMT_SERIAL_STEPS=1 in the environment
   std::map<std::string, hipGraphExec_t> graphs;
 };

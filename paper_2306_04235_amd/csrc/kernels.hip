@@ -417,6 +417,148 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __re
   }
 }
 
+// Decoder self-attention with the Q/K/V projection inside (the batched
+// decoder, d = 64 KQ, heads up to 64 wide, W <= 16 rows per sentence): block
+// = (head, sentence), 4 waves.  The block computes its sentence's W rows of
+// the head's q, k and v itself on v_mfma_i32_16x16x64_i8 (the rows as A, W
+// of its 16 rows real; wave w takes the 16-column fragments w, w + 4, w + 8
+// of the head's 3 dh columns, q then k then v), with the linear layer's I8
+// requantization, into LDS.  The input rows are int8 codes (a) or, with
+// ln_on, the LayerNorm + quantization of fp32 rows that the block computes
+// while its weight loads are in flight.  Wave w then attends for rows w,
+// w + 4, ... as k_attn_dec_self does: cached positions 0..t-1 through the
+// row's history, position t from LDS; the new key and value are appended to
+// the cache after the wave's loads (no block reads position t of this step).
+struct SelfQkvAttn {
+  const int8_t* a;        // input rows [R, d] (ln_on == 0)
+  int ln_on;
+  FusedIn ln;
+  const int8_t* wqkv;     // [3d, d] int8 (W4: packed 4-bit rows)
+  const float* scale;     // [3d]
+  const float* bias;
+  int W, d, h, dh, T;
+  const int* step;
+  int t_host;
+  int8_t* kcache;         // [R][T][d]
+  int8_t* vcache;
+  const int32_t* hist;    // [2][R][T] or null
+  float c_qk, c_pv;
+  int8_t* ctx;            // [R, d]
+};
+
+template <int NMAX, int KQ, bool W4>
+__global__ __launch_bounds__(256) void k_attn_self_qkv(SelfQkvAttn a) {
+  constexpr int DHMAX = 64, CPP = DHMAX / 16, PPI = 64 / CPP, NL = NMAX / PPI, NB = NL < 8 ? NL : 8;
+  constexpr int NI = NMAX / 64, D = 64 * KQ, AL = D + 16, QL = 3 * DHMAX, FPW = 3 * DHMAX / 16 / 4;
+  __shared__ __attribute__((aligned(16))) int8_t al[16 * AL];
+  __shared__ __attribute__((aligned(16))) int8_t ql[16 * QL];
+  __shared__ AttnLdsT<NMAX, DHMAX> sh[4];
+  const int hd = blockIdx.x, g = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rows = a.W, dh = a.dh, nc = dh / 16, T = a.T;
+  const int R = gridDim.y * rows;
+  const int l16 = lane & 15, koff = 16 * (lane >> 4);
+  // 1. the wave's weight fragments and their requantization constants
+  WFrag<W4> bf[FPW][KQ];
+  float fsc[FPW], fbi[FPW];
+#pragma unroll
+  for (int u = 0; u < FPW; ++u) {
+    const int f = wave + 4 * u;
+    const bool ok = f < 3 * nc;
+    const int col = ok ? (f / nc) * D + hd * dh + 16 * (f % nc) + l16 : 0;
+#pragma unroll
+    for (int kk = 0; kk < KQ; ++kk) bf[u][kk] = load_wfrag_if<W4>(ok, a.wqkv, col, D, 64 * kk + koff);
+    fsc[u] = a.scale[col];
+    fbi[u] = a.bias[col];
+  }
+  int t = a.t_host >= 0 ? a.t_host : *a.step;
+  t = t < 0 ? 0 : (t >= T ? T - 1 : t);
+  // 2. the sentence's input rows
+  v4i af[KQ];
+  if (a.ln_on) {
+    prepare_rows<KQ>(a.ln, rows, g * rows, D, 0, al, AL, false);
+    lds_barrier();
+#pragma unroll
+    for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(al + min(l16, rows - 1) * AL + 64 * kk + koff);
+  } else {
+    const int8_t* ar = a.a + ((size_t)g * rows + min(l16, rows - 1)) * D;
+#pragma unroll
+    for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(ar + 64 * kk + koff);
+  }
+  // 3. q | k | v of the rows (row i at ql + i QL: q, then k at DHMAX, v at 2 DHMAX)
+#pragma unroll
+  for (int u = 0; u < FPW; ++u) {
+    const int f = wave + 4 * u;
+    if (f < 3 * nc) {
+      v4i acc = {0, 0, 0, 0};
+#pragma unroll
+      for (int kk = 0; kk < KQ; ++kk) acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[kk], bf[u][kk].get(), acc, 0, 0, 0);
+      const int sel = f / nc, ff = f % nc;
+      // element i of lane l: row 4 (l / 16) + i, column l % 16
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * (lane >> 4) + i;
+        if (r < rows) ql[r * QL + sel * DHMAX + 16 * ff + l16] = code_of(fmaf((float)acc[i], fsc[u], fbi[u]));
+      }
+    }
+  }
+  lds_barrier();
+  // 4. attention for the wave's rows
+  const int n = t + 1, tc = t > 0 ? t - 1 : 0;  // cached positions 0..t-1 (tc: an in-bounds stand-in for t)
+  const int c = lane % CPP, pp = lane / CPP, cc = min(c, nc - 1);
+  AttnLdsT<NMAX, DHMAX>& w = sh[wave];
+  for (int i = wave; i < rows; i += 4) {
+    const int r = g * rows + i;
+    const int8_t* qr = ql + i * QL;
+    const v4i qc = *(const v4i*)(qr + 16 * cc);
+    const v4i kn = *(const v4i*)(qr + DHMAX + 16 * cc);
+    const v4i vn = *(const v4i*)(qr + 2 * DHMAX + 16 * cc);
+    const int32_t* hr = a.hist ? a.hist + ((size_t)(t & 1) * R + r) * T : nullptr;
+    int src[NL];
+#pragma unroll
+    for (int u = 0; u < NL; ++u) src[u] = hr ? hr[min(u * PPI + pp, t)] : r;
+#pragma unroll
+    for (int u0 = 0; u0 < NL; u0 += NB) {
+      v4i kr[NB], vr[NB];
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        const int tp = min((u0 + u) * PPI + pp, t);
+        const size_t off = ((size_t)src[u0 + u] * T + min(tp, tc)) * D + hd * dh + 16 * cc;
+        kr[u] = *(const v4i*)(a.kcache + off);
+        vr[u] = *(const v4i*)(a.vcache + off);
+        if (tp == t) {
+          kr[u] = kn;
+          vr[u] = vn;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < NB; ++u) {
+        int acc = c < nc ? dot16v(kr[u], qc, 0) : 0;
+#pragma unroll
+        for (int o = 1; o < CPP; o <<= 1) acc += __shfl_xor(acc, o, 64);
+        const int tp = (u0 + u) * PPI + pp;
+        if (c == 0 && tp < n) w.p[tp] = (float)acc * a.c_qk;
+        *(v4i*)&w.v[tp][16 * c] = vr[u];
+      }
+    }
+    wave_sync();  // the scores and values visible to every lane
+    float sv[NI];
+#pragma unroll
+    for (int ii = 0; ii < NI; ++ii) {
+      const int tp = lane + 64 * ii;
+      sv[ii] = tp < n ? w.p[tp] : 0.0f;
+    }
+    softmax_context<NI>(sv, n, dh, a.c_pv, w.p, &w.v[0][0], DHMAX, a.ctx + (size_t)r * D + hd * dh);
+    // the new key and value into the cache, after every load of the row
+    if (lane < nc) {
+      const size_t o = ((size_t)r * T + t) * D + hd * dh + 16 * lane;
+      *(v4i*)(a.kcache + o) = *(const v4i*)(qr + DHMAX + 16 * lane);
+      *(v4i*)(a.vcache + o) = *(const v4i*)(qr + 2 * DHMAX + 16 * lane);
+    }
+    wave_sync();  // every lane's reads of w before the next row's writes
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Greedy search bookkeeping.
 __global__ void k_greedy_reset(unsigned long long* slots, int R, int steps, int32_t* cur_tok, int32_t* finished,
@@ -640,7 +782,7 @@ __global__ __launch_bounds__(64) void k_beam_topk(const float* __restrict__ logi
 // otherwise each thread's best score is score + (its max z - lse) and the
 // K-th largest of these over the lanes of a wave has at least K scores of the
 // row at or above it (the largest such bound over the waves is taken).  The
-// bound filters the row down to a short list (2-8K entries on real logits),
+// bound filters the row down to a short list (about 3K entries on real logits),
 // ranked by one wave (up to 64 entries) or pairwise comparison.  If ties push
 // the list past kTopkCap, per-thread sorted lists over the threads' own
 // elements, merged over the block, take over.  The candidate order is total
@@ -1318,6 +1460,66 @@ hipError_t launch_attn_dec_cross_q(const int8_t* rows, const FusedIn* ln, const 
   a.c_pv = c_pv;
   a.ctx = ctx;
   return w4 ? launch_shared<4, 2, 4>(a, R / W, h, s) : launch_shared<4, 1, 4>(a, R / W, h, s);
+}
+
+bool attn_self_qkv_fits(int W, int d, int h, int T) {
+  const int dh = h > 0 ? d / h : 0;
+  return W >= 1 && W <= 16 && (d == 128 || d == 256) && h * dh == d && dh >= 16 && dh <= 64 && dh % 16 == 0 &&
+         T >= 1 && T <= kMaxAttnLen;
+}
+
+hipError_t launch_attn_self_qkv(const int8_t* rows, const FusedIn* ln, const int8_t* wqkv, const float* scale,
+                                const float* bias, bool w4, int R, int W, int d, int h, int T, const int* step,
+                                int8_t* kcache, int8_t* vcache, const int32_t* hist, float c_qk, float c_pv,
+                                int8_t* ctx, hipStream_t s, int t_host) {
+  if (!attn_self_qkv_fits(W, d, h, T) || R % W || !wqkv || !kcache || !vcache || !ctx ||
+      (ln ? !ln->x || ln->embed || ln->x_out : !rows))
+    return hipErrorInvalidValue;
+  SelfQkvAttn a{};
+  a.a = rows;
+  if (ln) {
+    a.ln_on = 1;
+    a.ln = *ln;
+  }
+  a.wqkv = wqkv;
+  a.scale = scale;
+  a.bias = bias;
+  a.W = W;
+  a.d = d;
+  a.h = h;
+  a.dh = d / h;
+  a.T = T;
+  a.step = step;
+  a.t_host = t_host;
+  a.kcache = kcache;
+  a.vcache = vcache;
+  a.hist = hist;
+  a.c_qk = c_qk;
+  a.c_pv = c_pv;
+  a.ctx = ctx;
+  const dim3 grid(h, R / W);
+  const int nm = attn_len_class(T);
+#define MNMT_SQ(NM, KQ)                                                          \
+  if (w4)                                                                        \
+    hipLaunchKernelGGL((k_attn_self_qkv<NM, KQ, true>), grid, dim3(256), 0, s, a); \
+  else                                                                           \
+    hipLaunchKernelGGL((k_attn_self_qkv<NM, KQ, false>), grid, dim3(256), 0, s, a);
+#define MNMT_SQ_K(NM) \
+  if (d == 128) {     \
+    MNMT_SQ(NM, 2)    \
+  } else {            \
+    MNMT_SQ(NM, 4)    \
+  }
+  if (nm == 64) {
+    MNMT_SQ_K(64)
+  } else if (nm == 128) {
+    MNMT_SQ_K(128)
+  } else {
+    MNMT_SQ_K(256)
+  }
+#undef MNMT_SQ_K
+#undef MNMT_SQ
+  return hipGetLastError();
 }
 
 hipError_t launch_attn_dec_cross(const int8_t* q, int R, int W, int d, int h, const int8_t* kv, int S,

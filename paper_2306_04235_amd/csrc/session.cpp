@@ -502,14 +502,37 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
     int rc;
-    if (l == 0)  // the step's input rows, quantized by the embedding step or the beam update
-      rc = qlin(L.qkv, S->dec_a, R, MNMT_EPI_I8, S->dec_qkv, 1.f, s);
-    else  // pre-LN: the layer's own LayerNorm; post-LN: the previous FFN's
-      rc = ln_linear(L.qkv, post ? m->dec[l - 1].ff_ln : L.sa_ln, MNMT_EPI_I8, S->dec_qkv);
-    if (rc) return rc;
-    LAUNCH(launch_attn_dec_self(S->dec_qkv, R, d, h, T, S->step, S->kcache[l], S->vcache[l],
-                                beam ? S->beam.hist : nullptr, L.sa_cqk, L.sa_cpv, S->dec_a, s, t_host));
-    if ((rc = qlin(L.o, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.sa_gamma, s))) return rc;
+    if (S->qkv_fused_on && S->ln_fused_on && beam && !post && !pend.splits && R > 64 &&
+        attn_self_qkv_fits(W, d, h, T)) {
+      // the Q/K/V projection inside the self-attention kernel (one block per
+      // head and sentence), from the step's int8 input rows (layer 0) or the
+      // LayerNorm each block computes (later layers); the context goes to
+      // dec_q (other blocks of a sentence still read its rows of dec_a)
+      FusedIn in{};
+      if (l > 0) {
+        in.x = xc;
+        in.do_ln = 1;
+        in.g = L.sa_ln.g;
+        in.b = L.sa_ln.b;
+        in.eps = eps;
+        in.inv_s = L.qkv.inv_in;
+      }
+      const int8_t* w;
+      const bool w4 = batched_weights(L.qkv, w);
+      LAUNCH(launch_attn_self_qkv(l > 0 ? nullptr : S->dec_a, l > 0 ? &in : nullptr, w, L.qkv.scale, L.qkv.bias, w4,
+                                  R, W, d, h, T, S->step, S->kcache[l], S->vcache[l], S->beam.hist, L.sa_cqk,
+                                  L.sa_cpv, S->dec_q, s, t_host));
+      if ((rc = qlin(L.o, S->dec_q, R, MNMT_EPI_F32_RESID, xc, L.sa_gamma, s))) return rc;
+    } else {
+      if (l == 0)  // the step's input rows, quantized by the embedding step or the beam update
+        rc = qlin(L.qkv, S->dec_a, R, MNMT_EPI_I8, S->dec_qkv, 1.f, s);
+      else  // pre-LN: the layer's own LayerNorm; post-LN: the previous FFN's
+        rc = ln_linear(L.qkv, post ? m->dec[l - 1].ff_ln : L.sa_ln, MNMT_EPI_I8, S->dec_qkv);
+      if (rc) return rc;
+      LAUNCH(launch_attn_dec_self(S->dec_qkv, R, d, h, T, S->step, S->kcache[l], S->vcache[l],
+                                  beam ? S->beam.hist : nullptr, L.sa_cqk, L.sa_cpv, S->dec_a, s, t_host));
+      if ((rc = qlin(L.o, S->dec_a, R, MNMT_EPI_F32_RESID, xc, L.sa_gamma, s))) return rc;
+    }
     int8_t* cctx = S->dec_a;  // the cross-attention context rows
     if (attn_cross_q_fits(W, d)) {
       // the Q projection inside the attention kernel, from the LayerNorm'd
@@ -1253,6 +1276,10 @@ extern "C" int mnmt_session_create(const mnmt_model* model, const mnmt_session_c
   // their own instead of in the prologue of the linear layer they feed
   const char* lnf = std::getenv("MNMT_LN_FUSED");
   S->ln_fused_on = !(lnf && std::atoi(lnf) == 0);
+  // MNMT_QKV_FUSED=0: the batched pre-LN decoder's Q/K/V projection as a
+  // GEMM of its own instead of inside the self-attention kernel
+  const char* qkvf = std::getenv("MNMT_QKV_FUSED");
+  S->qkv_fused_on = !(qkvf && std::atoi(qkvf) == 0);
   // the encoder accumulators start at zero (each encode leaves them so), the
   // chain error word too
   hipError_t h = hipMemsetAsync(S->enc_acc, 0, enc_acc_bytes(d), S->capture_stream);
