@@ -1083,14 +1083,34 @@ __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, in
     }
     __syncthreads();
     // rank of each candidate = number of better candidates (flat index j*V + v breaks ties)
-    for (int i = lane; w0 && i < n; i += 64) {
-      int rank = 0;
-      const long fi = (long)cj[i] * V + cv[i];
-      for (int o = 0; o < n; ++o) {
-        const long fo = (long)cj[o] * V + cv[o];
-        rank += (cs[o] > cs[i] || (cs[o] == cs[i] && fo < fi)) ? 1 : 0;
+    if (n <= 64 && (long)W * V <= 0x7fffffffL) {
+      // one candidate per lane of wave 0, each counting the larger of the 64
+      // (score, -flat index) keys read across lanes (pack_argmax order, which
+      // is the comparison's with -0 read as +0; dead lanes hold key 0)
+      if (w0) {
+        const bool live = lane < n;
+        const float ci = live ? cs[lane] : 0.0f;
+        const unsigned long long key = live ? pack_argmax(ci == 0.0f ? 0.0f : ci, cj[lane] * V + cv[lane]) : 0ull;
+        const int hi = (int)(key >> 32), lo = (int)(uint32_t)key;
+        int rank = 0;
+#pragma unroll
+        for (int o = 0; o < 64; ++o) {
+          const unsigned long long ko = ((unsigned long long)(uint32_t)__builtin_amdgcn_readlane(hi, o) << 32) |
+                                        (uint32_t)__builtin_amdgcn_readlane(lo, o);
+          rank += ko > key ? 1 : 0;
+        }
+        if (live && rank < K) order[rank] = lane;
       }
-      if (rank < K) order[rank] = i;
+    } else {
+      for (int i = lane; w0 && i < n; i += 64) {
+        int rank = 0;
+        const long fi = (long)cj[i] * V + cv[i];
+        for (int o = 0; o < n; ++o) {
+          const long fo = (long)cj[o] * V + cv[o];
+          rank += (cs[o] > cs[i] || (cs[o] == cs[i] && fo < fi)) ? 1 : 0;
+        }
+        if (rank < K) order[rank] = i;
+      }
     }
     __syncthreads();
     if (threadIdx.x == 0) {
