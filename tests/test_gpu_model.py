@@ -374,15 +374,27 @@ VARIED_BEAM = G.ModelConfig("varied-256-beam", 256, 4, 1024, 2, 2, 2000, ln_post
 @pytest.mark.parametrize("cfg", [DIVERSE, VARIED_BEAM], ids=lambda c: c.name)
 def test_batched_layernorm_forms(torch_dev, monkeypatch, cfg):
     """Pre-LN beam search above 64 rows (19 sentences of beam 4: 76 rows, a
-    ragged last tile of 32 rows): the LayerNorms in the prologue of the
-    linear layers they feed (each block of the one-round-trip GEMM normalizes
-    its rows) and, with MNMT_LN_FUSED=0 (read at session creation), as
-    kernels of their own; both against the oracle on every sentence."""
+    ragged last tile of 16 rows): the LayerNorms in the prologue of the
+    kernels they feed (each block of the one-round-trip GEMM normalizes its
+    rows) and, with MNMT_LN_FUSED=0 (read at session creation), as kernels of
+    their own; the self-attention computing its rows' Q/K/V and, with
+    MNMT_QKV_FUSED=0, the projection as a GEMM; the fused self-attention's
+    128- and 256-position classes over 100 and 200 steps; every sentence
+    against the oracle."""
     torch, dev = torch_dev
     src, lens = G.make_sources(cfg.vocab, 19, (2, 24), seed=97, s_max=24)
     for fused in ("1", "0"):
         monkeypatch.setenv("MNMT_LN_FUSED", fused)
         _beam_check(torch, dev, cfg, src, lens, 4, 12, 0.6, parallel=True)
+    monkeypatch.setenv("MNMT_LN_FUSED", "1")
+    monkeypatch.setenv("MNMT_QKV_FUSED", "0")
+    _beam_check(torch, dev, cfg, src, lens, 4, 12, 0.6, parallel=True)
+    monkeypatch.setenv("MNMT_QKV_FUSED", "1")
+    # the longer key-length classes of the fused self-attention (up to 128 and
+    # 256 target positions), 17 sentences (68 rows)
+    src, lens = G.make_sources(cfg.vocab, 17, (1, 40), seed=98, s_max=40)
+    for steps in (100, 200):
+        _beam_check(torch, dev, cfg, src, lens, 4, steps, 0.6, parallel=True)
 
 
 HEAD16 = G.ModelConfig("head-16", 128, 8, 256, 1, 1, 600, ln_post=0, seed=88, random_gamma=True, weight_std=0.1)
