@@ -436,7 +436,7 @@ struct SelfQkvAttn {
   const int8_t* wqkv;     // [3d, d] int8 (W4: packed 4-bit rows)
   const float* scale;     // [3d]
   const float* bias;
-  int W, d, h, dh, T;
+  int W, dh, T;           // rows per sentence, head width, cache positions
   const int* step;
   int t_host;
   int8_t* kcache;         // [R][T][d]
@@ -1505,8 +1505,6 @@ hipError_t launch_attn_self_qkv(const int8_t* rows, const FusedIn* ln, const int
   a.scale = scale;
   a.bias = bias;
   a.W = W;
-  a.d = d;
-  a.h = h;
   a.dh = d / h;
   a.T = T;
   a.step = step;
