@@ -218,7 +218,7 @@ __host__ __device__ constexpr int lanes_per_row(int dmax) {
 // the LayerNorm's gain and bias are loaded once before the rows: a load under
 // a lane condition makes the compiler wait for it where the paths join, which
 // would turn the loads of a row group into one memory round trip each.
-template <int NJ, int G = kPrepGroup>  // d <= 64 * NJ; G rows per wave at once
+template <int NJ, int G = kPrepGroup, bool PEND = false>  // d <= 64 * NJ; G rows per wave at once; PEND: in.nparts may be > 0
 __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int row0, int d, int t, int8_t* a_lds,
                                              int lds_stride, bool writer) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -235,11 +235,13 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
   }
   for (int r0 = wave; r0 < rows; r0 += 4 * G) {
     float v[G][NJ];
+    // the branches are uniform and hold whole loops, so that every load of
+    // the group is issued before the first use in each of them
+    if (in.embed) {
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const int r = r0 + 4 * g;
-      const size_t gr = (size_t)(row0 + (r < rows ? r : 0));
-      if (in.embed) {
+      for (int g = 0; g < G; ++g) {
+        const int r = r0 + 4 * g;
+        const size_t gr = (size_t)(row0 + (r < rows ? r : 0));
         int tok = in.tok[gr];
         tok = tok < 0 ? 0 : (tok >= in.V ? in.V - 1 : tok);
         const int pos = in.S_pos > 0 ? (int)(gr % (size_t)in.S_pos) : t;
@@ -249,10 +251,48 @@ __device__ __forceinline__ void prepare_rows(const FusedIn& in, int rows, int ro
           const int i = min(lane + 64 * j, d - 1);
           v[g][j] = fmaf((float)in.E[(size_t)tok * d + i], c, in.pe[(size_t)pos * d + i]);
         }
-      } else {
+      }
+    } else if (!PEND || in.nparts == 0) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int r = r0 + 4 * g;
+        const size_t gr = (size_t)(row0 + (r < rows ? r : 0));
 #pragma unroll
         for (int j = 0; j < NJ; ++j) v[g][j] = in.x[gr * d + min(lane + 64 * j, d - 1)];
       }
+    } else if constexpr (PEND) {
+      // the pending update: the rows, their partial sums and the constants
+      // loaded together (slices past nparts repeat the last, not added)
+      int pa[G][kMaxSplits][NJ];
+      float ps[NJ], pb[NJ];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int i = min(lane + 64 * j, d - 1);
+        ps[j] = in.pscale[i];
+        pb[j] = in.pbias[i];
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int r = r0 + 4 * g;
+        const size_t gr = (size_t)(row0 + (r < rows ? r : 0));
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          const int i = min(lane + 64 * j, d - 1);
+          v[g][j] = in.x[gr * d + i];
+#pragma unroll
+          for (int p = 0; p < kMaxSplits; ++p)
+            pa[g][p][j] = in.part[(size_t)min(p, in.nparts - 1) * in.part_stride + gr * d + i];
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+          int acc = pa[g][0][j];
+#pragma unroll
+          for (int p = 1; p < kMaxSplits; ++p) acc += p < in.nparts ? pa[g][p][j] : 0;
+          v[g][j] = fmaf(in.pgamma, v[g][j], fmaf((float)acc, ps[j], pb[j]));
+        }
     }
     if (writer && in.wb_input) {
 #pragma unroll

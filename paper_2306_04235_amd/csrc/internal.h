@@ -159,6 +159,16 @@ struct FusedIn {           // how a kernel obtains its int8 input rows
   const float* b;
   float eps;
   float inv_s;             // 1 / input scale of the consuming linear layer
+  // a pending residual update (nparts > 0): x <- fma(pgamma, x, fma(acc,
+  // pscale, pbias)) with acc the sum of nparts int32 slices part + p
+  // part_stride (a linear layer's partial sums over ranges of its K); the
+  // writer blocks store the updated rows to x_out (wb_input)
+  const int32_t* part;
+  int nparts;
+  size_t part_stride;
+  const float* pscale;
+  const float* pbias;
+  float pgamma;
 };
 struct FusedGemv {         // a linear layer over the prepared rows, and greedy bookkeeping
   int R, K, N;

@@ -418,9 +418,10 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __re
 }
 
 // Decoder self-attention with the Q/K/V projection inside (the batched
-// decoder, d = 64 KQ, heads up to 64 wide, W <= 16 rows per sentence): block
-// = (head, sentence), 4 waves.  The block computes its sentence's W rows of
-// the head's q, k and v itself on v_mfma_i32_16x16x64_i8 (the rows as A, W
+// decoder, d = 64 KQ, heads up to 64 wide): block = (head, group of RB <= 16
+// rows), 4 waves; the rows are independent (each has its own cache row and
+// history), so a group may span sentences.  The block computes its rows of
+// the head's q, k and v itself on v_mfma_i32_16x16x64_i8 (the rows as A, RB
 // of its 16 rows real; wave w takes the 16-column fragments w, w + 4, w + 8
 // of the head's 3 dh columns, q then k then v), with the linear layer's I8
 // requantization, into LDS.  The input rows are int8 codes (a) or, with
@@ -436,7 +437,7 @@ struct SelfQkvAttn {
   const int8_t* wqkv;     // [3d, d] int8 (W4: packed 4-bit rows)
   const float* scale;     // [3d]
   const float* bias;
-  int W, dh, T;           // rows per sentence, head width, cache positions
+  int RB, R, dh, T;       // rows per block (at most 16), rows, head width, cache positions
   const int* step;
   int t_host;
   int8_t* kcache;         // [R][T][d]
@@ -455,8 +456,7 @@ __global__ __launch_bounds__(256) void k_attn_self_qkv(SelfQkvAttn a) {
   __shared__ AttnLdsT<NMAX, DHMAX> sh[4];
   const int hd = blockIdx.x, g = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rows = a.W, dh = a.dh, nc = dh / 16, T = a.T;
-  const int R = gridDim.y * rows;
+  const int R = a.R, row0 = g * a.RB, rows = min(a.RB, R - row0), dh = a.dh, nc = dh / 16, T = a.T;
   const int l16 = lane & 15, koff = 16 * (lane >> 4);
   // 1. the wave's weight fragments and their requantization constants
   WFrag<W4> bf[FPW][KQ];
@@ -476,12 +476,14 @@ __global__ __launch_bounds__(256) void k_attn_self_qkv(SelfQkvAttn a) {
   // 2. the sentence's input rows
   v4i af[KQ];
   if (a.ln_on) {
-    prepare_rows<KQ>(a.ln, rows, g * rows, D, 0, al, AL, false);
+    // one row per wave (rows of more than four hypotheses take turns); the
+    // head-0 blocks store the rows after a pending update
+    prepare_rows<KQ, 1, true>(a.ln, rows, row0, D, 0, al, AL, hd == 0);
     lds_barrier();
 #pragma unroll
     for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(al + min(l16, rows - 1) * AL + 64 * kk + koff);
   } else {
-    const int8_t* ar = a.a + ((size_t)g * rows + min(l16, rows - 1)) * D;
+    const int8_t* ar = a.a + ((size_t)row0 + min(l16, rows - 1)) * D;
 #pragma unroll
     for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(ar + 64 * kk + koff);
   }
@@ -508,7 +510,7 @@ __global__ __launch_bounds__(256) void k_attn_self_qkv(SelfQkvAttn a) {
   const int c = lane % CPP, pp = lane / CPP, cc = min(c, nc - 1);
   AttnLdsT<NMAX, DHMAX>& w = sh[wave];
   for (int i = wave; i < rows; i += 4) {
-    const int r = g * rows + i;
+    const int r = row0 + i;
     const int8_t* qr = ql + i * QL;
     const v4i qc = *(const v4i*)(qr + 16 * cc);
     const v4i kn = *(const v4i*)(qr + DHMAX + 16 * cc);
@@ -1493,7 +1495,9 @@ hipError_t launch_attn_self_qkv(const int8_t* rows, const FusedIn* ln, const int
                                 int8_t* kcache, int8_t* vcache, const int32_t* hist, float c_qk, float c_pv,
                                 int8_t* ctx, hipStream_t s, int t_host) {
   if (!attn_self_qkv_fits(W, d, h, T) || R % W || !wqkv || !kcache || !vcache || !ctx ||
-      (ln ? !ln->x || ln->embed || ln->x_out : !rows))
+      (ln ? !ln->x || ln->embed || (ln->x_out && (!ln->wb_input || ln->x_out == ln->x)) ||
+                (ln->nparts && (ln->nparts > kMaxSplits || !ln->part || !ln->x_out))
+          : !rows))
     return hipErrorInvalidValue;
   SelfQkvAttn a{};
   a.a = rows;
@@ -1504,7 +1508,14 @@ hipError_t launch_attn_self_qkv(const int8_t* rows, const FusedIn* ln, const int
   a.wqkv = wqkv;
   a.scale = scale;
   a.bias = bias;
-  a.W = W;
+  // one sentence per block: 16-row groups (four mobile sentences) measured
+  // 7.73 against 6.90 ms per mobile beam batch, a quarter of the blocks each
+  // attending for four rows per wave.  At d 512 (the base model) the fused
+  // form lost to the separate projection with either grouping (37.4-37.6
+  // against 34.1 ms per batch): each block reads a 96 KB slice of W_qkv.
+  const int rb = W;
+  a.RB = rb;
+  a.R = R;
   a.dh = d / h;
   a.T = T;
   a.step = step;
@@ -1515,7 +1526,7 @@ hipError_t launch_attn_self_qkv(const int8_t* rows, const FusedIn* ln, const int
   a.c_qk = c_qk;
   a.c_pv = c_pv;
   a.ctx = ctx;
-  const dim3 grid(h, R / W);
+  const dim3 grid(h, (R + rb - 1) / rb);
   const int nm = attn_len_class(T);
 #define MNMT_SQ(NM, KQ)                                                          \
   if (w4)                                                                        \

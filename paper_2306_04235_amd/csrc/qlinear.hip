@@ -285,7 +285,8 @@ bool qgemm_rows_fit(int M, int K, int N) {
 
 hipError_t launch_qgemm_small(const FusedIn* in, const int8_t* X, int ldx, const int8_t* W, const float* scale,
                               const float* bias, int M, int K, int N, const EpiArgs& e, hipStream_t s, bool w4) {
-  if (M < 1 || M > kSmallMaxRows || K > kSmallMaxK || K % 64 || (in && K > kMaxRowLen)) return hipErrorInvalidValue;
+  if (M < 1 || M > kSmallMaxRows || K > kSmallMaxK || K % 64 || (in && (K > kMaxRowLen || in->nparts)))
+    return hipErrorInvalidValue;
   // 65-256 rows (the mobile beam decoder): one-wave blocks of 16x16 (at 512
   // rows their four-fold block count made the base beam step slower); rows
   // normalized in the prologue above 64 rows: 16x64 tiles

@@ -465,8 +465,10 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
     LAUNCH(launch_ln_quant(S->dec_x, R, d, !post, L0.sa_ln.g, L0.sa_ln.b, eps, L0.qkv.inv_in, S->dec_a, nullptr, s));
   }
   // a residual update left pending by a split-K layer (splits > 0), applied
-  // by the next LayerNorm kernel
+  // by the next LayerNorm kernel or in the prologue of the fused
+  // self-attention kernel
   ResidUpdate pend{};
+  float* const xbuf[2] = {S->dec_x, S->dec_x2};
   // LayerNorm + quantization of the rows with L's input scale into dec_a
   // (post-LN: the normalized rows also replace x)
   auto ln_rows = [&](const LnDev& ln, float inv_s, bool replace) -> int {
@@ -502,13 +504,17 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
   for (size_t l = 0; l < m->dec.size(); ++l) {
     const LayerDev& L = m->dec[l];
     int rc;
-    if (S->qkv_fused_on && S->ln_fused_on && beam && !post && !pend.splits && R > 64 &&
-        attn_self_qkv_fits(W, d, h, T)) {
+    if (S->qkv_fused_on && S->ln_fused_on && beam && !post && R > 64 && attn_self_qkv_fits(W, d, h, T) &&
+        (l > 0 || !pend.splits)) {
       // the Q/K/V projection inside the self-attention kernel (one block per
       // head and sentence), from the step's int8 input rows (layer 0) or the
-      // LayerNorm each block computes (later layers); the context goes to
-      // dec_q (other blocks of a sentence still read its rows of dec_a)
+      // LayerNorm each block computes (later layers, after the pending update
+      // of a split W2: the head-0 blocks store the updated rows into the
+      // other residual buffer, since the other blocks still read the old
+      // ones); the context goes to dec_q (other blocks of a sentence still
+      // read its rows of dec_a)
       FusedIn in{};
+      float* xn = xc;
       if (l > 0) {
         in.x = xc;
         in.do_ln = 1;
@@ -516,12 +522,24 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
         in.b = L.sa_ln.b;
         in.eps = eps;
         in.inv_s = L.qkv.inv_in;
+        if (pend.splits) {
+          in.part = pend.part;
+          in.nparts = pend.splits;
+          in.part_stride = (size_t)R * d;
+          in.pscale = pend.scale;
+          in.pbias = pend.bias;
+          in.pgamma = pend.gamma;
+          in.x_out = xn = xc == xbuf[0] ? xbuf[1] : xbuf[0];
+          in.wb_input = 1;
+          pend.splits = 0;
+        }
       }
       const int8_t* w;
       const bool w4 = batched_weights(L.qkv, w);
       LAUNCH(launch_attn_self_qkv(l > 0 ? nullptr : S->dec_a, l > 0 ? &in : nullptr, w, L.qkv.scale, L.qkv.bias, w4,
                                   R, W, d, h, T, S->step, S->kcache[l], S->vcache[l], S->beam.hist, L.sa_cqk,
                                   L.sa_cpv, S->dec_q, s, t_host));
+      xc = xn;
       if ((rc = qlin(L.o, S->dec_q, R, MNMT_EPI_F32_RESID, xc, L.sa_gamma, s))) return rc;
     } else {
       if (l == 0)  // the step's input rows, quantized by the embedding step or the beam update

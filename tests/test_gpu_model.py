@@ -371,7 +371,14 @@ VARIED_BEAM = G.ModelConfig("varied-256-beam", 256, 4, 1024, 2, 2, 2000, ln_post
                             weight_std=0.2)
 
 
-@pytest.mark.parametrize("cfg", [DIVERSE, VARIED_BEAM], ids=lambda c: c.name)
+# a long feed-forward (K 2048): W2's split partial sums are added by the next
+# layer's fused self-attention prologue, which stores the updated rows into
+# the second residual buffer
+SPLIT_BEAM = G.ModelConfig("split-preln-beam", 128, 4, 2048, 2, 3, 700, ln_post=0, seed=94, random_gamma=True,
+                           weight_std=0.1)
+
+
+@pytest.mark.parametrize("cfg", [DIVERSE, VARIED_BEAM, SPLIT_BEAM], ids=lambda c: c.name)
 def test_batched_layernorm_forms(torch_dev, monkeypatch, cfg):
     """Pre-LN beam search above 64 rows (19 sentences of beam 4: 76 rows, a
     ragged last tile of 16 rows): the LayerNorms in the prologue of the
