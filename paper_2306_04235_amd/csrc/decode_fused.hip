@@ -47,7 +47,8 @@ __global__ __launch_bounds__(256) void k_qgemv_ln(FusedIn in, FusedGemv gv) {
     }
   }
   // 2. input rows while the loads are in flight
-  prepare_rows<(DMAX + 63) / 64>(in, R, 0, K, gv.t, a_lds, K, blockIdx.x == 0);
+  // (at most 8 rows: two per wave, no wave loading rows past R)
+  prepare_rows<(DMAX + 63) / 64, kRows / 4>(in, R, 0, K, gv.t, a_lds, K, blockIdx.x == 0);
   __syncthreads();
   // 3. dot products
   int acc[U][MR];

@@ -270,7 +270,10 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_shared(SharedAttn a) {
     for (int kk = 0; kk < KQ; ++kk) bf[kk] = load_wfrag_if<W4>(wave < nc, a.wq, hd * dh + 16 * wave + l16, d, 64 * kk + koff);
     v4i af[KQ];
     if (a.ln_on) {
-      prepare_rows<KQ>(a.ln, rows, g * rows, d, 0, al, AL, false);
+      // one row per wave at a time: with the default four, each wave of a
+      // four-row sentence loaded three clamped copies of its row as well
+      // (6.98 -> 6.80 ms per mobile beam batch without them)
+      prepare_rows<KQ, 1>(a.ln, rows, g * rows, d, 0, al, AL, false);
       lds_barrier();
 #pragma unroll
       for (int kk = 0; kk < KQ; ++kk) af[kk] = *(const v4i*)(al + min(l16, rows - 1) * AL + 64 * kk + koff);
