@@ -429,7 +429,9 @@ __global__ __launch_bounds__(64 * WAVES) void k_attn_dec_self(const int8_t* __re
 // of the head's 3 dh columns, q then k then v), with the linear layer's I8
 // requantization, into LDS.  The input rows are int8 codes (a) or, with
 // ln_on, the LayerNorm + quantization of fp32 rows that the block computes
-// while its weight loads are in flight.  Wave w then attends for rows w,
+// while its weight loads are in flight (after the pending update of a split
+// W2 when ln.nparts > 0: the head-0 blocks store the updated rows to
+// ln.x_out).  Wave w then attends for rows w,
 // w + 4, ... as k_attn_dec_self does: cached positions 0..t-1 through the
 // row's history, position t from LDS; the new key and value are appended to
 // the cache after the wave's loads (no block reads position t of this step).
