@@ -481,8 +481,9 @@ int run_decoder_layers(mnmt_session* S, int R, int W, bool beam, hipStream_t s, 
     return MNMT_OK;
   };
   // the linear layer L over the rows LN(x) quantized with L's input scale;
-  // pre-LN rows that the one-round-trip GEMM takes are normalized in its
-  // prologue (each block its 32 rows) instead of by a kernel of their own
+  // pre-LN rows that the one-round-trip GEMM takes above 64 rows are
+  // normalized in its prologue (each 16x64 block its 16 rows) instead of by a
+  // kernel of their own
   auto ln_linear = [&](const LinearDev& L, const LnDev& ln, int kind, void* out) -> int {
     if (S->ln_fused_on && !post && !pend.splits && R > 64 && qgemm_rows_fit(R, L.K, L.N) && L.K == d) {
       FusedIn in{};
