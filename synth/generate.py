@@ -35,6 +35,7 @@ from .modelfile import Header, Int4Rows, write_model
 
 WEIGHT_STD = 0.02
 SPECIAL = 4  # ids 0..3 are PAD, BOS, EOS, UNK
+EOS = 2
 
 
 @dataclass(frozen=True)
@@ -57,6 +58,7 @@ class ModelConfig:
     w_bits: int = 8  # 4: linear weights as 4-bit codes (the paper's W-E-A 4-8-8; the embedding stays 8-bit)
     share_every: int = 0  # > 0: layer l >= share_every reuses the parameters of layer l % share_every (per stack)
     emb_dim: int = 0  # > 0: factorized embedding [V, emb_dim] with a [d_model, emb_dim] projection
+    eos_gain: float = 1.0  # the EOS row of the embedding drawn this many times larger (its tied logit too)
 
 
 # The model shapes of the five workloads.
@@ -125,6 +127,9 @@ def build_model(cfg: ModelConfig) -> bytes:
     e = rng.normal(0.0, cfg.emb_std, size=(cfg.emb_distinct or cfg.vocab, ef))
     if cfg.emb_distinct:
         e = e[np.arange(cfg.vocab) % cfg.emb_distinct]
+    if cfg.eos_gain != 1.0:  # hypotheses that end at varied steps
+        e = e.copy()
+        e[EOS] = e[EOS] * cfg.eos_gain
     t["emb.w"], t["emb.s"] = _quantize_rows(e)
     if cfg.emb_dim:  # factorized: P [d, E] with entries N(0, 1/E), one per-tensor scale
         pw = rng.normal(0.0, 1.0 / np.sqrt(ef), size=(d, ef))

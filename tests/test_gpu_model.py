@@ -404,6 +404,36 @@ def test_batched_layernorm_forms(torch_dev, monkeypatch, cfg):
         _beam_check(torch, dev, cfg, src, lens, 4, steps, 0.6, parallel=True)
 
 
+# models whose EOS row of the embedding is drawn larger, so that hypotheses
+# and greedy sentences end at varied steps (the search's end-of-sentence
+# rules: finished hypotheses, length penalty, finished sentences skipped)
+VARIED_EOS = dataclasses.replace(VARIED_BEAM, name="varied-256-eos", eos_gain=3.0)
+DIVERSE_EOS = dataclasses.replace(DIVERSE, name="diverse-eos", eos_gain=4.0)
+
+
+def test_end_of_sentence_search(torch_dev):
+    """Beam search and greedy search with stop_at_eos on models that emit EOS
+    at varied steps (the oracle's lengths range from 1 to the maximum):
+    batched beam above and below 64 rows (the fused and the general batched
+    decoder), small-model beam at widths 2, 4, 6, and greedy at 1, 2 and 5
+    rows (the chained batch-1 step, the 2-row and the 3-8-row paths)."""
+    torch, dev = torch_dev
+    src, lens = G.make_sources(VARIED_EOS.vocab, 19, (2, 24), seed=97, s_max=24)
+    for W in (4, 2):
+        _beam_check(torch, dev, VARIED_EOS, src, lens, W, 20, 0.6, parallel=True)
+    src, lens = G.make_sources(DIVERSE_EOS.vocab, 4, [5, 1, 9, 9], seed=31, s_max=9)
+    for W in (2, 4, 6):
+        _beam_check(torch, dev, DIVERSE_EOS, src, lens, W, 16, 0.6)
+    for B, seed in ((1, 45), (1, 48), (2, 42), (5, 45)):
+        src, lens = G.make_sources(VARIED_EOS.vocab, B, (3, 30), seed=seed, s_max=30)
+        _greedy_check(torch, dev, VARIED_EOS, src, lens, 20, stop_at_eos=True, check_logits=False)
+    # the oracle's lengths do vary (the test exercises the end-of-sentence rules)
+    om, _ = _pair(VARIED_EOS)
+    src, lens = G.make_sources(VARIED_EOS.vocab, 19, (2, 24), seed=97, s_max=24)
+    _, o_len, _ = om.beam(src[:6], lens[:6], 4, 20, 0.6)
+    assert o_len.min() < 20 and o_len.max() > 1
+
+
 HEAD16 = G.ModelConfig("head-16", 128, 8, 256, 1, 1, 600, ln_post=0, seed=88, random_gamma=True, weight_std=0.1)
 HEAD128 = G.ModelConfig("head-128", 256, 2, 512, 1, 1, 600, ln_post=1, seed=89, random_gamma=True, weight_std=0.08)
 
