@@ -454,6 +454,19 @@ def test_attention_length_and_head_classes(torch_dev, cfg):
     _beam_check(torch, dev, cfg, src, lens, 4, 140, 0.6)
 
 
+def test_postln_beam_above_64_rows(torch_dev):
+    """Post-LN beam search above 64 rows (the normalized rows replace the
+    residual stream, so the batched decoder keeps its LayerNorm kernels):
+    76 rows of a d-64 model on the one-wave 16x16 GEMM blocks, and 68 rows
+    of a d-256 model with 128-wide heads, whose cross-attention computes its
+    query rows itself, against the oracle on every sentence."""
+    torch, dev = torch_dev
+    src, lens = G.make_sources(SMALL_POST.vocab, 19, (2, 24), seed=99, s_max=24)
+    _beam_check(torch, dev, SMALL_POST, src, lens, 4, 12, 0.6, parallel=True)
+    src, lens = G.make_sources(HEAD128.vocab, 17, (2, 40), seed=100, s_max=40)
+    _beam_check(torch, dev, HEAD128, src, lens, 4, 12, 0.6, parallel=True)
+
+
 ODD_VOCAB = G.ModelConfig("odd-vocab", 64, 4, 128, 1, 1, 501, ln_post=0, seed=79, random_gamma=True, weight_std=0.1)
 
 
