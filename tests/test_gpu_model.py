@@ -397,6 +397,10 @@ def test_batched_layernorm_forms(torch_dev, monkeypatch, cfg):
     monkeypatch.setenv("MNMT_QKV_FUSED", "0")
     _beam_check(torch, dev, cfg, src, lens, 4, 12, 0.6, parallel=True)
     monkeypatch.setenv("MNMT_QKV_FUSED", "1")
+    # eight hypotheses per sentence (two rows per wave in the fused
+    # self-attention, the K > 8 bound of the top-k), 9 sentences (72 rows)
+    src8, lens8 = G.make_sources(cfg.vocab, 9, (2, 24), seed=96, s_max=24)
+    _beam_check(torch, dev, cfg, src8, lens8, 8, 12, 0.6, parallel=True)
     # the longer key-length classes of the fused self-attention (up to 128 and
     # 256 target positions), 17 sentences (68 rows)
     src, lens = G.make_sources(cfg.vocab, 17, (1, 40), seed=98, s_max=40)
@@ -554,6 +558,9 @@ def test_4bit_packed_only_batched_paths(torch_dev):
     _beam_check(torch, dev, div4, src, lens, 2, 8, 0.6, flags=flags)
     src, lens = G.make_sources(div4.vocab, 12, [9, 5, 7, 16, 3, 11, 8, 8, 2, 16, 12, 6], seed=32, s_max=16)
     _greedy_check(torch, dev, div4, src, lens, 6, flags=flags)
+    # above 64 rows at d 128: the fused self-attention on packed W_qkv rows
+    src, lens = G.make_sources(div4.vocab, 19, (2, 16), seed=34, s_max=16)
+    _beam_check(torch, dev, div4, src, lens, 4, 10, 0.6, parallel=True, flags=flags)
     mob4 = dataclasses.replace(G.MOBILE, name="mobile-w4", w_bits=4)
     w = G.WORKLOADS["mobile_beam"]
     src, lens = G.workload_inputs(w)
