@@ -401,6 +401,11 @@ def test_batched_layernorm_forms(torch_dev, monkeypatch, cfg):
     # self-attention, the K > 8 bound of the top-k), 9 sentences (72 rows)
     src8, lens8 = G.make_sources(cfg.vocab, 9, (2, 24), seed=96, s_max=24)
     _beam_check(torch, dev, cfg, src8, lens8, 8, 12, 0.6, parallel=True)
+    # two and six hypotheses per sentence above 64 rows (40 and 12 sentences)
+    src2, lens2 = G.make_sources(cfg.vocab, 40, (2, 24), seed=95, s_max=24)
+    _beam_check(torch, dev, cfg, src2, lens2, 2, 12, 0.6, parallel=True)
+    src6, lens6 = G.make_sources(cfg.vocab, 12, (2, 24), seed=94, s_max=24)
+    _beam_check(torch, dev, cfg, src6, lens6, 6, 12, 0.6, parallel=True)
     # the longer key-length classes of the fused self-attention (up to 128 and
     # 256 target positions), 17 sentences (68 rows)
     src, lens = G.make_sources(cfg.vocab, 17, (1, 40), seed=98, s_max=40)
