@@ -1205,30 +1205,25 @@ __global__ __launch_bounds__(64 * kUpdWaves) void k_beam_update(BeamState st, in
   }
 }
 
-// Backtrack the tokens of the hypothesis held by `row` after step `last`
-// (positions 0..last) into out[0..last].
-__device__ void backtrack(const BeamState& st, int row, int last, int32_t* out) {
-  const int R = st.B * st.W;
-  for (int t = last; t >= 0; --t) {
-    out[t] = st.tok_hist[(size_t)t * R + row];
-    row = st.par_hist[(size_t)t * R + row];
-  }
-}
-
 // Per sentence: finish the live hypotheses if the sentence never completed,
 // pick the best normalized score (the first finished among equals: EOS
 // hypotheses in the order they finished, then the live slots in slot order)
-// and write its tokens.  One thread per sentence.
-__global__ void k_beam_finalize(BeamState st, int steps, int32_t* out, int32_t* out_len, float* out_score,
-                                const int* chain_err) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= st.B) return;
-  const int W = st.W;
+// and write its tokens.  One wave per sentence: the sentence's parent slots
+// of steps 0..last go to LDS in one round of loads, lane 0 follows the
+// parents back from the chosen hypothesis there, and the lanes then read the
+// tokens of the path together (each step's token is that of the path's slot).
+constexpr int kFinMaxSteps = 256, kFinMaxW = 8;
+__global__ __launch_bounds__(64) void k_beam_finalize(BeamState st, int steps, int32_t* out, int32_t* out_len,
+                                                      float* out_score, const int* chain_err) {
+  __shared__ uint8_t par_s[kFinMaxSteps][kFinMaxW];  // parent slot of (step, slot)
+  __shared__ uint8_t path[kFinMaxSteps];             // the hypothesis' slot at each step
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int W = st.W, R = st.B * W, r0 = b * W;
   int kind = -1, idx = 0;  // kind 0: finished entry idx; kind 1: live slot idx
   float best = 0.0f;
   const int fc = st.fin_count[b];
   for (int i = 0; i < fc; ++i) {
-    const float v = st.fin_score[b * W + i];
+    const float v = st.fin_score[r0 + i];
     if (kind < 0 || v > best) {
       best = v;
       kind = 0;
@@ -1237,7 +1232,7 @@ __global__ void k_beam_finalize(BeamState st, int steps, int32_t* out, int32_t* 
   }
   if (!st.done[b]) {
     for (int s = 0; s < W; ++s) {
-      const float v = st.score[b * W + s] / st.lp[steps];
+      const float v = st.score[r0 + s] / st.lp[steps];
       if (kind < 0 || v > best) {
         best = v;
         kind = 1;
@@ -1245,19 +1240,31 @@ __global__ void k_beam_finalize(BeamState st, int steps, int32_t* out, int32_t* 
       }
     }
   }
-  int32_t* o = out + (size_t)b * steps;
-  int L;
-  if (kind == 1) {
-    L = steps;
-    backtrack(st, b * W + idx, steps - 1, o);
-  } else {
-    L = st.fin_len[b * W + idx];
-    if (L > 1) backtrack(st, st.fin_row[b * W + idx], L - 2, o);
-    o[L - 1] = st.eos;
+  // the tokens of steps 0..last come from the path ending in `row`
+  const int L = kind == 1 ? steps : st.fin_len[r0 + idx];
+  const int last = min(kind == 1 ? steps - 1 : L - 2, steps - 1);
+  const int row = kind == 1 ? r0 + idx : st.fin_row[r0 + idx];
+  for (int e = lane; e < (last + 1) * W; e += 64) {
+    const int t = e / W, j = e % W;
+    par_s[t][j] = (uint8_t)min(max(st.par_hist[(size_t)t * R + r0 + j] - r0, 0), W - 1);
   }
-    for (int t = L; t < steps; ++t) o[t] = st.pad;
-  out_len[b] = (chain_err && *chain_err) ? -1 : L;
-  if (out_score) out_score[b] = best;
+  __syncthreads();
+  if (lane == 0) {
+    int slot = min(max(row - r0, 0), W - 1);
+    for (int t = last; t >= 0; --t) {
+      path[t] = (uint8_t)slot;
+      slot = par_s[t][slot];
+    }
+  }
+  __syncthreads();
+  int32_t* o = out + (size_t)b * steps;
+  for (int t = lane; t <= last; t += 64) o[t] = st.tok_hist[(size_t)t * R + r0 + path[t]];
+  if (kind == 0 && lane == 0) o[L - 1] = st.eos;
+  for (int t = L + lane; t < steps; t += 64) o[t] = st.pad;
+  if (lane == 0) {
+    out_len[b] = (chain_err && *chain_err) ? -1 : L;
+    if (out_score) out_score[b] = best;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1695,8 +1702,8 @@ hipError_t launch_beam_update(const BeamState& st, int* step, const BeamNext& nx
 
 hipError_t launch_beam_finalize(const BeamState& st, int steps, int32_t* out, int32_t* out_len, float* out_score,
                                 const int* chain_err, hipStream_t s) {
-  hipLaunchKernelGGL(k_beam_finalize, dim3((st.B + 63) / 64), dim3(64), 0, s, st, steps, out, out_len, out_score,
-                     chain_err);
+  if (steps < 0 || steps > kFinMaxSteps || st.W < 1 || st.W > kFinMaxW) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_beam_finalize, dim3(st.B), dim3(64), 0, s, st, steps, out, out_len, out_score, chain_err);
   return hipGetLastError();
 }
 
