@@ -671,19 +671,28 @@ __device__ __forceinline__ bool better(float c1, int i1, float c2, int i2) {
   return c1 > c2 || (c1 == c2 && i1 < i2);
 }
 
-__global__ void k_beam_reset(BeamState st, int* step) {
-  const int R = st.B * st.W;
-  for (int r = threadIdx.x + blockIdx.x * blockDim.x; r < R; r += blockDim.x * gridDim.x) {
+// The search state before the first step, one element per thread over a
+// grid that covers the [R][T] histories (consecutive threads write
+// consecutive words of every array).
+__global__ __launch_bounds__(256) void k_beam_reset(BeamState st, int* step) {
+  const int R = st.B * st.W, T = st.T;
+  const size_t RT = (size_t)R * T, stride = (size_t)blockDim.x * gridDim.x;
+  const size_t i0 = threadIdx.x + (size_t)blockIdx.x * blockDim.x;
+  for (size_t e = i0; e < RT; e += stride) {
+    // every position points at a valid cache row: hist is [2][R][T] ...
+    const int32_t rh = (int32_t)(e / T);
+    st.hist[e] = rh;
+    st.hist[RT + e] = rh;
+    // ... the token and parent histories [T][R]
+    const int32_t rt = (int32_t)(e % R);
+    st.tok_hist[e] = st.pad;
+    st.par_hist[e] = rt;
+  }
+  for (size_t r = i0; r < (size_t)R; r += stride) {
     st.score[r] = 0.0f;
     st.cur_tok[r] = st.bos;
-    for (int t = 0; t < st.T; ++t) {  // every position points at a valid cache row
-      st.hist[(size_t)r * st.T + t] = r;
-      st.hist[(size_t)(R + r) * st.T + t] = r;
-      st.tok_hist[(size_t)t * R + r] = st.pad;
-      st.par_hist[(size_t)t * R + r] = r;
-    }
   }
-  for (int b = threadIdx.x + blockIdx.x * blockDim.x; b < st.B; b += blockDim.x * gridDim.x) {
+  for (size_t b = i0; b < (size_t)st.B; b += stride) {
     st.fin_count[b] = 0;
     st.done[b] = 0;
   }
@@ -1647,8 +1656,10 @@ hipError_t launch_copy_i32(const int32_t* src, int32_t* dst, int n, hipStream_t 
 }
 
 hipError_t launch_beam_reset(const BeamState& st, int* step, hipStream_t s) {
-  const int R = st.B * st.W;
-  hipLaunchKernelGGL(k_beam_reset, dim3((R + 255) / 256), dim3(256), 0, s, st, step);
+  const size_t RT = (size_t)st.B * st.W * st.T;
+  const size_t nb = (RT + 255) / 256;
+  const int blocks = nb < 1 ? 1 : (nb > 1024 ? 1024 : (int)nb);
+  hipLaunchKernelGGL(k_beam_reset, dim3(blocks), dim3(256), 0, s, st, step);
   return hipGetLastError();
 }
 
